@@ -1,0 +1,155 @@
+"""fp64 CPU oracle for the resettable memoroid scan -- TEST INFRASTRUCTURE.
+
+Only the tests, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The product library never does, and the
+two share no code: the arithmetic lives in ``oracle.c`` (plain sequential fp64
+loops, compiled with gcc), this module only marshals numpy arrays through
+ctypes.
+
+Each wrapper takes numpy arrays already decoded exactly to float64 / complex128
+(fp32 and complex64 widen exactly; bf16 is decoded by the input generator) and
+returns float64 / complex128 results together with the magnitude companions
+described in ``oracle.h``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.c into liboracle.so with gcc (plain -O2, no fast-math,
+    no FP contraction, so every expression is evaluated as written)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-std=c99", "-O2", "-ffp-contract=off", "-fno-fast-math",
+               "-fPIC", "-shared", "-Wall", "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB_PATH)
+        P, I64 = ctypes.c_void_p, ctypes.c_int64
+        lib.oracle_episode_idx.argtypes = [P, I64, I64, P]
+        for name in ("oracle_diag_fwd", "oracle_diag_fwd_c"):
+            getattr(lib, name).argtypes = [P, I64, P, P, I64, I64, I64, P, P]
+        for name in ("oracle_diag_bwd", "oracle_diag_bwd_c"):
+            getattr(lib, name).argtypes = [P, I64, P, P, P, I64, I64, I64, P, P, P, P]
+        lib.oracle_phi.argtypes = [ctypes.c_double]
+        lib.oracle_phi.restype = ctypes.c_double
+        lib.oracle_linattn.argtypes = [P, P, P, P, I64, I64, I64, I64, P, P]
+        for name in ("oracle_episode_idx", "oracle_diag_fwd", "oracle_diag_fwd_c",
+                     "oracle_diag_bwd", "oracle_diag_bwd_c", "oracle_linattn"):
+            getattr(lib, name).restype = None
+        _lib = lib
+    return _lib
+
+
+def _ptr(arr):
+    return None if arr is None else arr.ctypes.data_as(ctypes.c_void_p)
+
+
+def _flags(start, B, T):
+    s = np.ascontiguousarray(start, dtype=np.uint8)
+    if s.size != B * T:
+        raise ValueError("start must hold B*T flags")
+    return s.reshape(B, T)
+
+
+def episode_idx(start) -> np.ndarray:
+    """Per-step episode index; start is [B, T] (or [T])."""
+    s = np.asarray(start, dtype=np.uint8)
+    s2 = s.reshape(1, -1) if s.ndim == 1 else s
+    B, T = s2.shape
+    s2 = _flags(s2, B, T)
+    out = np.empty((B, T), dtype=np.int32)
+    _load().oracle_episode_idx(_ptr(s2), B, T, _ptr(out))
+    return out.reshape(s.shape)
+
+
+def _diag_shapes(a, x, start):
+    x = np.asarray(x)
+    if x.ndim == 2:
+        x = x[None]
+    B, T, d = x.shape
+    cplx = np.iscomplexobj(x) or np.iscomplexobj(a)
+    dt = np.complex128 if cplx else np.float64
+    x = np.ascontiguousarray(x, dtype=dt)
+    a = np.asarray(a)
+    if a.ndim == 1:
+        if a.shape[0] != d:
+            raise ValueError("time-invariant a must have shape [d]")
+        stride = 0
+    else:
+        a = a.reshape(B, T, d)
+        stride = d
+    a = np.ascontiguousarray(a, dtype=dt)
+    s = _flags(start, B, T)
+    return a, x, s, B, T, d, stride, cplx, dt
+
+
+def diag_fwd(a, x, start):
+    """h_t = x_t at a begin step, else a_t h_{t-1} + x_t.
+
+    a: [B,T,d] (per step) or [d] (time-invariant); x: [B,T,d]; start: [B,T].
+    Returns (h, m) with m the magnitude companion (float64)."""
+    a, x, s, B, T, d, stride, cplx, dt = _diag_shapes(a, x, start)
+    h = np.empty((B, T, d), dtype=dt)
+    m = np.empty((B, T, d), dtype=np.float64)
+    fn = _load().oracle_diag_fwd_c if cplx else _load().oracle_diag_fwd
+    fn(_ptr(a), stride, _ptr(x), _ptr(s), B, T, d, _ptr(h), _ptr(m))
+    return h, m
+
+
+def diag_bwd(a, start, h, g):
+    """Reverse scan: returns (dx, da, m_dx, m_da); da is [B,T,d] for per-step a
+    and [d] (summed) for time-invariant a."""
+    a, g, s, B, T, d, stride, cplx, dt = _diag_shapes(a, g, start)
+    h = np.ascontiguousarray(np.asarray(h).reshape(B, T, d), dtype=dt)
+    dx = np.empty((B, T, d), dtype=dt)
+    m_dx = np.empty((B, T, d), dtype=np.float64)
+    da_shape = (B, T, d) if stride else (d,)
+    da = np.empty(da_shape, dtype=dt)
+    m_da = np.empty(da_shape, dtype=np.float64)
+    fn = _load().oracle_diag_bwd_c if cplx else _load().oracle_diag_bwd
+    fn(_ptr(a), stride, _ptr(s), _ptr(h), _ptr(g), B, T, d,
+       _ptr(dx), _ptr(da), _ptr(m_dx), _ptr(m_da))
+    return dx, da, m_dx, m_da
+
+
+def phi(u: float) -> float:
+    return _load().oracle_phi(float(u))
+
+
+def linattn(q, k, v, start):
+    """Linear-transformer memoroid readout over one tape.
+
+    q, k: [T,H,dk]; v: [T,H,dv]; start: [T].  Returns (out, m), both
+    [T,H,dv] float64."""
+    q = np.ascontiguousarray(q, dtype=np.float64)
+    k = np.ascontiguousarray(k, dtype=np.float64)
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    T, H, dk = q.shape
+    dv = v.shape[2]
+    if k.shape != (T, H, dk) or v.shape[:2] != (T, H):
+        raise ValueError("q, k must be [T,H,dk] and v [T,H,dv]")
+    s = _flags(start, 1, T)
+    out = np.empty((T, H, dv), dtype=np.float64)
+    m = np.empty((T, H, dv), dtype=np.float64)
+    _load().oracle_linattn(_ptr(q), _ptr(k), _ptr(v), _ptr(s), T, H, dk, dv,
+                           _ptr(out), _ptr(m))
+    return out, m

@@ -1,0 +1,212 @@
+/*
+ * oracle.c -- fp64 sequential reference for the resettable memoroid scan.
+ * TEST INFRASTRUCTURE ONLY: see oracle.h.  Built with gcc as a plain shared
+ * object; no code here is shared with the HIP library.
+ *
+ * Every loop runs the recurrence step by step in tape order, exactly as the
+ * memoroid definition of Section 4 states it (h_t = e_I . f(P_0) . ... . f(P_t)),
+ * with the resettable transform of the Section 4 reset theorem taking the form
+ * "at a begin step the state restarts from the identity".
+ */
+#include "oracle.h"
+
+#include <complex.h>
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* t = 0 of every tape is a begin step: the scan starts from g_I = (e_I, 0). */
+static int is_begin(const uint8_t* start, int64_t T, int64_t b, int64_t t) {
+    return t == 0 || start[b * T + t] != 0;
+}
+
+void oracle_episode_idx(const uint8_t* start, int64_t B, int64_t T, int32_t* idx) {
+    for (int64_t b = 0; b < B; ++b) {
+        int32_t c = -1;
+        for (int64_t t = 0; t < T; ++t) {
+            if (is_begin(start, T, b, t)) c += 1;
+            idx[b * T + t] = c;
+        }
+    }
+}
+
+/* ---------------------------------------------------------------- diag fwd */
+
+void oracle_diag_fwd(const double* a, int64_t a_stride_t, const double* x,
+                     const uint8_t* start, int64_t B, int64_t T, int64_t d,
+                     double* h, double* m) {
+    for (int64_t b = 0; b < B; ++b) {
+        for (int64_t t = 0; t < T; ++t) {
+            const int64_t row = (b * T + t) * d;
+            const double* at = a_stride_t ? a + row : a;
+            const int begin = is_begin(start, T, b, t);
+            for (int64_t j = 0; j < d; ++j) {
+                if (begin) {
+                    h[row + j] = x[row + j];
+                    if (m) m[row + j] = fabs(x[row + j]);
+                } else {
+                    h[row + j] = at[j] * h[row - d + j] + x[row + j];
+                    if (m) m[row + j] = fabs(at[j]) * m[row - d + j] + fabs(x[row + j]);
+                }
+            }
+        }
+    }
+}
+
+void oracle_diag_fwd_c(const double* a_, int64_t a_stride_t, const double* x_,
+                       const uint8_t* start, int64_t B, int64_t T, int64_t d,
+                       double* h_, double* m) {
+    const double complex* a = (const double complex*)a_;
+    const double complex* x = (const double complex*)x_;
+    double complex* h = (double complex*)h_;
+    for (int64_t b = 0; b < B; ++b) {
+        for (int64_t t = 0; t < T; ++t) {
+            const int64_t row = (b * T + t) * d;
+            const double complex* at = a_stride_t ? a + row : a;
+            const int begin = is_begin(start, T, b, t);
+            for (int64_t j = 0; j < d; ++j) {
+                if (begin) {
+                    h[row + j] = x[row + j];
+                    if (m) m[row + j] = cabs(x[row + j]);
+                } else {
+                    h[row + j] = at[j] * h[row - d + j] + x[row + j];
+                    if (m) m[row + j] = cabs(at[j]) * m[row - d + j] + cabs(x[row + j]);
+                }
+            }
+        }
+    }
+}
+
+/* ---------------------------------------------------------------- diag bwd */
+
+void oracle_diag_bwd(const double* a, int64_t a_stride_t, const uint8_t* start,
+                     const double* h, const double* g,
+                     int64_t B, int64_t T, int64_t d,
+                     double* dx, double* da, double* m_dx, double* m_da) {
+    double* lam = (double*)calloc((size_t)(d > 0 ? d : 1), sizeof(double));
+    double* mlam = (double*)calloc((size_t)(d > 0 ? d : 1), sizeof(double));
+    if (da && !a_stride_t) memset(da, 0, (size_t)d * sizeof(double));
+    if (m_da && !a_stride_t) memset(m_da, 0, (size_t)d * sizeof(double));
+    for (int64_t b = 0; b < B; ++b) {
+        for (int64_t t = T - 1; t >= 0; --t) {
+            const int64_t row = (b * T + t) * d;
+            /* the state of step t flows into step t+1 unless t+1 begins a new
+               episode or lies past the end of the tape */
+            const int flows = (t + 1 < T) && !is_begin(start, T, b, t + 1);
+            const double* anext = flows ? (a_stride_t ? a + row + d : a) : NULL;
+            const int begin = is_begin(start, T, b, t);
+            for (int64_t j = 0; j < d; ++j) {
+                lam[j] = g[row + j] + (flows ? anext[j] * lam[j] : 0.0);
+                mlam[j] = fabs(g[row + j]) + (flows ? fabs(anext[j]) * mlam[j] : 0.0);
+                dx[row + j] = lam[j];
+                if (m_dx) m_dx[row + j] = mlam[j];
+                const double dat = begin ? 0.0 : lam[j] * h[row - d + j];
+                const double mdat = begin ? 0.0 : mlam[j] * fabs(h[row - d + j]);
+                if (da) {
+                    if (a_stride_t) da[row + j] = dat; else da[j] += dat;
+                }
+                if (m_da) {
+                    if (a_stride_t) m_da[row + j] = mdat; else m_da[j] += mdat;
+                }
+            }
+        }
+    }
+    free(lam);
+    free(mlam);
+}
+
+void oracle_diag_bwd_c(const double* a_, int64_t a_stride_t, const uint8_t* start,
+                       const double* h_, const double* g_,
+                       int64_t B, int64_t T, int64_t d,
+                       double* dx_, double* da_, double* m_dx, double* m_da) {
+    const double complex* a = (const double complex*)a_;
+    const double complex* h = (const double complex*)h_;
+    const double complex* g = (const double complex*)g_;
+    double complex* dx = (double complex*)dx_;
+    double complex* da = (double complex*)da_;
+    double complex* lam = (double complex*)calloc((size_t)(d > 0 ? d : 1), sizeof(double complex));
+    double* mlam = (double*)calloc((size_t)(d > 0 ? d : 1), sizeof(double));
+    if (da && !a_stride_t) memset(da, 0, (size_t)d * sizeof(double complex));
+    if (m_da && !a_stride_t) memset(m_da, 0, (size_t)d * sizeof(double));
+    for (int64_t b = 0; b < B; ++b) {
+        for (int64_t t = T - 1; t >= 0; --t) {
+            const int64_t row = (b * T + t) * d;
+            const int flows = (t + 1 < T) && !is_begin(start, T, b, t + 1);
+            const double complex* anext = flows ? (a_stride_t ? a + row + d : a) : NULL;
+            const int begin = is_begin(start, T, b, t);
+            for (int64_t j = 0; j < d; ++j) {
+                lam[j] = g[row + j] + (flows ? conj(anext[j]) * lam[j] : 0.0);
+                mlam[j] = cabs(g[row + j]) + (flows ? cabs(anext[j]) * mlam[j] : 0.0);
+                dx[row + j] = lam[j];
+                if (m_dx) m_dx[row + j] = mlam[j];
+                const double complex dat = begin ? 0.0 : lam[j] * conj(h[row - d + j]);
+                const double mdat = begin ? 0.0 : mlam[j] * cabs(h[row - d + j]);
+                if (da) {
+                    if (a_stride_t) da[row + j] = dat; else da[j] += dat;
+                }
+                if (m_da) {
+                    if (a_stride_t) m_da[row + j] = mdat; else m_da[j] += mdat;
+                }
+            }
+        }
+    }
+    free(lam);
+    free(mlam);
+}
+
+/* ----------------------------------------------------------- linear attn */
+
+double oracle_phi(double u) { return u > 0.0 ? u + 1.0 : exp(u); }
+
+void oracle_linattn(const double* q, const double* k, const double* v,
+                    const uint8_t* start, int64_t T, int64_t H, int64_t dk, int64_t dv,
+                    double* out, double* m) {
+    double* S = (double*)malloc((size_t)(dk * dv > 0 ? dk * dv : 1) * sizeof(double));
+    double* Sabs = (double*)malloc((size_t)(dk * dv > 0 ? dk * dv : 1) * sizeof(double));
+    double* z = (double*)malloc((size_t)(dk > 0 ? dk : 1) * sizeof(double));
+    double* kf = (double*)malloc((size_t)(dk > 0 ? dk : 1) * sizeof(double));
+    double* qf = (double*)malloc((size_t)(dk > 0 ? dk : 1) * sizeof(double));
+    for (int64_t hh = 0; hh < H; ++hh) {
+        for (int64_t t = 0; t < T; ++t) {
+            if (is_begin(start, T, 0, t)) {
+                memset(S, 0, (size_t)(dk * dv) * sizeof(double));
+                memset(Sabs, 0, (size_t)(dk * dv) * sizeof(double));
+                memset(z, 0, (size_t)dk * sizeof(double));
+            }
+            const double* qt = q + (t * H + hh) * dk;
+            const double* kt = k + (t * H + hh) * dk;
+            const double* vt = v + (t * H + hh) * dv;
+            for (int64_t i = 0; i < dk; ++i) {
+                kf[i] = oracle_phi(kt[i]);
+                qf[i] = oracle_phi(qt[i]);
+            }
+            /* X_n = X_{n-1} + phi(k) v^T ;  x_n = x_{n-1} + phi(k) */
+            for (int64_t i = 0; i < dk; ++i) {
+                z[i] += kf[i];
+                for (int64_t j = 0; j < dv; ++j) {
+                    S[i * dv + j] += kf[i] * vt[j];
+                    Sabs[i * dv + j] += kf[i] * fabs(vt[j]);
+                }
+            }
+            /* readout phi(q)^T S / (phi(q)^T z) */
+            double den = 0.0;
+            for (int64_t i = 0; i < dk; ++i) den += qf[i] * z[i];
+            double* ot = out + (t * H + hh) * dv;
+            double* mt = m ? m + (t * H + hh) * dv : NULL;
+            for (int64_t j = 0; j < dv; ++j) {
+                double num = 0.0, numabs = 0.0;
+                for (int64_t i = 0; i < dk; ++i) {
+                    num += qf[i] * S[i * dv + j];
+                    numabs += qf[i] * Sabs[i * dv + j];
+                }
+                ot[j] = num / den;
+                if (mt) mt[j] = numabs / den;
+            }
+        }
+    }
+    free(S);
+    free(Sabs);
+    free(z);
+    free(kf);
+    free(qf);
+}

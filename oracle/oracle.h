@@ -1,0 +1,109 @@
+/*
+ * oracle.h -- plain, slow, obviously correct CPU reference for the resettable
+ * memoroid scan ("Recurrent Reinforcement Learning with Memoroids",
+ * arXiv 2402.09900).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library links, includes
+ * or calls this code; only the tests, the smoke check and the CPU-baseline leg
+ * of the benchmark use it.  It shares no header, helper or constant with the
+ * HIP path.
+ *
+ * Every routine is the sequential definition written out in fp64:
+ *   - the memoroid recurrence  h_t = e_I . f(P_0) . ... . f(P_t)      (Def. of
+ *     a memoroid, Section 4 "Approach");
+ *   - with the resettable monoid transform of Section 4 "Inline Recurrent
+ *     State Resets" (resettable-monoid theorem): within an episode the
+ *     transformed operator equals the original one, and no information crosses
+ *     an episode boundary.  A begin flag b_t = 1 marks the first step of an
+ *     episode (Section 2.1), so the state at a begin step holds that step's
+ *     input and nothing older.
+ *
+ * Conventions shared by all routines (readings of the paper, see the design
+ * notes of the repository):
+ *   - start[b*T + t] != 0 means "an episode begins at step t of tape b"; any
+ *     nonzero byte counts, and t = 0 of every tape is a begin step whatever the
+ *     byte says (the pre-tape state is the identity g_I = (e_I, 0)).
+ *   - data is row-major [B][T][d], features contiguous.
+ *   - complex arrays are interleaved (re, im) doubles, i.e. C99 double complex.
+ *   - the reset is a select, not the arithmetic A*(1-b') + e_I*b' form, so that
+ *     a NaN/Inf in one episode never reaches the next (0*Inf = NaN would).
+ *   - "magnitude companion" outputs (m, m_*) are the same recurrence run on
+ *     absolute values; they bound the size of the rounding error any
+ *     reordering of the sums can make, and the tests divide errors by
+ *     max(|r|, m).  Pass NULL to skip them.
+ *
+ * Parity status: every routine here is pinned by CPU tests (brute force over
+ * bracketings, closed forms, autograd, quadratic forms, worked examples of
+ * Fig. 1 and Fig. 2).  No routine is "parity unpinned".
+ */
+#ifndef MEMOROID_ORACLE_H
+#define MEMOROID_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Episode index of every step: the number of begin steps at or before t in
+ * the same tape, minus one (Fig. 2; Alg. 1 stores I = where(b)).  idx[B][T]. */
+void oracle_episode_idx(const uint8_t* start, int64_t B, int64_t T, int32_t* idx);
+
+/* Diagonal linear memoroid, forward (S5 / LRU memoroids of App. G.2-G.3 with a
+ * diagonal transition): h_t = x_t if step t begins an episode, else
+ * a_t * h_{t-1} + x_t.
+ *   a: a_stride_t == d -> per-step a[B][T][d];  a_stride_t == 0 -> a[d] shared
+ *      by every tape and step (time-invariant transition).
+ *   m: optional magnitude companion [B][T][d]:  m_t = |x_t| (+ |a_t| m_{t-1}). */
+void oracle_diag_fwd(const double* a, int64_t a_stride_t, const double* x,
+                     const uint8_t* start, int64_t B, int64_t T, int64_t d,
+                     double* h, double* m);
+
+/* Complex version (LRU memoroid of App. G.3).  a, x, h interleaved complex. */
+void oracle_diag_fwd_c(const double* a, int64_t a_stride_t, const double* x,
+                       const uint8_t* start, int64_t B, int64_t T, int64_t d,
+                       double* h, double* m);
+
+/* Reverse (gradient) scan of the diagonal memoroid.  The paper obtains it by
+ * automatic differentiation; written out with the conjugate convention of
+ * complex autograd (grad = dL/d conj(z)):
+ *   lam_t = g_t + [step t+1 exists in the tape and is not a begin step] * conj(a_{t+1}) * lam_{t+1}
+ *   dx_t  = lam_t
+ *   da_t  = [t is not a begin step] * lam_t * conj(h_{t-1})
+ * h is the forward output (an input here), g = dL/dh.
+ *   da: [B][T][d] when a_stride_t == d;  [d] (summed over tapes and steps)
+ *       when a_stride_t == 0.  NULL skips it.
+ *   m_dx (optional, [B][T][d]): companion of lam on |a|, |g|.
+ *   m_da (optional, shape of da): sum/element of m_dx,t * |h_{t-1}|. */
+void oracle_diag_bwd(const double* a, int64_t a_stride_t, const uint8_t* start,
+                     const double* h, const double* g,
+                     int64_t B, int64_t T, int64_t d,
+                     double* dx, double* da, double* m_dx, double* m_da);
+
+void oracle_diag_bwd_c(const double* a, int64_t a_stride_t, const uint8_t* start,
+                       const double* h, const double* g,
+                       int64_t B, int64_t T, int64_t d,
+                       double* dx, double* da, double* m_dx, double* m_da);
+
+/* phi(u) = 1 + ELU(u) with alpha = 1 (App. G.1), evaluated as u + 1 for u > 0
+ * and exp(u) otherwise, which is the same function without the 1 + (e^u - 1)
+ * cancellation. */
+double oracle_phi(double u);
+
+/* Linear-transformer memoroid (App. G.1) over one tape with H independent
+ * heads.  Per head, with S (dk x dv) and z (dk) reset to zero at every begin
+ * step:
+ *   S_t = S_{t-1} + phi(k_t) v_t^T,  z_t = z_{t-1} + phi(k_t),
+ *   out_t = phi(q_t)^T S_t / (phi(q_t)^T z_t).
+ * q, k: [T][H][dk]; v, out: [T][H][dv] (raw, pre-phi q and k).
+ * m (optional, [T][H][dv]): phi(q)^T S_abs / (phi(q)^T z) with S_abs built
+ * from |v|. */
+void oracle_linattn(const double* q, const double* k, const double* v,
+                    const uint8_t* start, int64_t T, int64_t H, int64_t dk, int64_t dv,
+                    double* out, double* m);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif
