@@ -1,0 +1,264 @@
+#!/usr/bin/env python3
+"""Throughput of the resettable memoroid scan on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload N]
+
+A step is one pass of the whole hot path over one synthetic tape already
+resident in HBM: for the diagonal workloads the forward scan (with episode
+indices) and, where the workload has one, the reverse (gradient) scan; for the
+linear-attention workload the chunked forward readout.  Prints ONE JSON line.
+
+Workloads (seeded, synthetic; laws in paper_2402_09900_amd.tapes):
+  1  diag real f32, T=1024, d=32, 8 episodes, forward
+  2  diag complex64 (LRU-style, time-invariant a), T=65536, d=256, Geometric(200)
+     episodes, forward + reverse                                   [default]
+  3  linear-transformer memoroid, T=32768, 4 heads x 64, Geometric(500), chunk 64
+  4  diag real, 64 tapes x T=16384, d=512, bf16 in / fp32 state / bf16 out
+  5  diag real f32, T=1048576, d=256, lognormal(5, 1.5) episodes, forward + reverse
+
+value = tape timesteps x features per second of the whole step (B*T*d, or
+T*H*dv for linear attention).  roofline: the dominant kernel's algorithmic
+bytes (or flops) per launch over its average launch time, measured here with
+HIP events on the launch stream.  cpu_baseline: the fp64 oracle timed on this
+host on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "tape timesteps×features/sec for resettable scan; % of HBM peak (diag)"
+UNIT = "timestep-features/s"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+FP32_MFMA_PEAK_TFLOPS = 157.3  # MI355X dense fp32 matrix
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    return p.parse_args()
+
+
+class Timer:
+    """HIP events on the launch stream around one library call."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.pairs = []
+
+    def __call__(self, fn):
+        t = self.torch
+        e0, e1 = t.cuda.Event(enable_timing=True), t.cuda.Event(enable_timing=True)
+        e0.record(t.cuda.current_stream())
+        fn()
+        e1.record(t.cuda.current_stream())
+        self.pairs.append((e0, e1))
+
+    def mean_ms(self):
+        return float(np.mean([a.elapsed_time(b) for a, b in self.pairs])) if self.pairs else 0.0
+
+
+def dev_tensor(torch, arr, kind):
+    arr = np.ascontiguousarray(arr)
+    if kind == "bf16":
+        return torch.from_numpy(arr.view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(arr).cuda()
+
+
+def setup_diag(torch, mb, tapes, key):
+    w = tapes.make_diag(key)
+    kind = w.dtype
+    code = {"f32": mb.F32, "bf16": mb.BF16, "c64": mb.C64}
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "c64": torch.complex64}
+    a, x, s = dev_tensor(torch, w.a, kind), dev_tensor(torch, w.x, kind), dev_tensor(torch, w.start, "u8")
+    B, T, d = w.B, w.T, w.d
+    h = torch.empty((B, T, d), dtype=tdt[w.out_dtype], device="cuda")
+    idx = torch.empty((B, T), dtype=torch.int32, device="cuda")
+    stride = 0 if w.a_invariant else d
+    nb = mb.memoroid_scan_diag_workspace_bytes(B, T, d, code[kind], code[w.out_dtype])
+    ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+    ebytes = {"f32": 4, "bf16": 2, "c64": 8}
+    n = B * T * d
+    a_bytes = (d if w.a_invariant else n) * ebytes[kind]
+    calls = {}
+    bytes_per = {}
+    stream = lambda: torch.cuda.current_stream().cuda_stream  # noqa: E731
+
+    def fwd():
+        st = mb.memoroid_scan_diag(a.data_ptr(), stride, x.data_ptr(), s.data_ptr(), h.data_ptr(), idx.data_ptr(),
+                                   B, T, d, code[kind], code[w.out_dtype], ws.data_ptr(), ws.numel(), stream())
+        assert st == 0, mb.status_string(st)
+    calls["fwd"] = fwd
+    bytes_per["fwd"] = a_bytes + n * ebytes[kind] + n * ebytes[w.out_dtype] + B * T * (1 + 4)
+    if w.backward:
+        g = dev_tensor(torch, w.g, kind)
+        hb = h if w.out_dtype == kind else h.to(tdt[kind])
+        gx = torch.empty_like(g)
+        ga = torch.empty((d,) if w.a_invariant else (B, T, d), dtype=tdt[kind], device="cuda")
+        nbb = mb.memoroid_scan_diag_bwd_workspace_bytes(B, T, d, code[kind], stride)
+        wsb = torch.empty(nbb, dtype=torch.uint8, device="cuda")
+
+        def bwd():
+            st = mb.memoroid_scan_diag_bwd(a.data_ptr(), stride, s.data_ptr(), hb.data_ptr(), g.data_ptr(),
+                                           gx.data_ptr(), ga.data_ptr(), B, T, d, code[kind], wsb.data_ptr(),
+                                           wsb.numel(), stream())
+            assert st == 0, mb.status_string(st)
+        calls["bwd"] = bwd
+        # read a_{t+1}, g, h_{t-1}; write dx, da (da per step, or [d])
+        da_bytes = (d if w.a_invariant else n) * ebytes[kind]
+        bytes_per["bwd"] = a_bytes + 3 * n * ebytes[kind] + da_bytes + B * T
+    return w, calls, bytes_per, n
+
+
+def setup_linattn(torch, mb, tapes):
+    la = tapes.make_linattn()
+    q, k, v = (dev_tensor(torch, t, "f32") for t in (la.q, la.k, la.v))
+    s = dev_tensor(torch, la.start, "u8")
+    out = torch.empty_like(v)
+    idx = torch.empty((la.T,), dtype=torch.int32, device="cuda")
+    nb = mb.memoroid_scan_linattn_workspace_bytes(la.T, la.H, 64, 64, 64)
+    ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+
+    def fwd():
+        st = mb.memoroid_scan_linattn(q.data_ptr(), k.data_ptr(), v.data_ptr(), s.data_ptr(), out.data_ptr(),
+                                      idx.data_ptr(), la.T, la.H, 64, 64, 64, ws.data_ptr(), ws.numel(),
+                                      torch.cuda.current_stream().cuda_stream)
+        assert st == 0, mb.status_string(st)
+    n = la.T * la.H * la.dv
+    # algorithmic: q, k, v read and out written once (4 B each), flags, idx
+    bytes_per = {"fwd": 4 * n * 4 + la.T * 5}
+    # chunked-dense flops: 4 contractions of 2*64^3 per (chunk, head)
+    flops = 4 * 2 * 64 ** 3 * (la.T // 64) * la.H
+    return la, {"fwd": fwd}, bytes_per, n, flops
+
+
+def cpu_baseline(key, tapes, budget_s=20.0):
+    """The oracle as it stands, single thread, on a bounded sample."""
+    import oracle
+    w = tapes.WORKLOADS[key]
+    if w.kind == "linattn":
+        T = min(w.T, 4096)
+        la = tapes.make_linattn(T=T)
+        t0 = time.perf_counter()
+        oracle.linattn(la.q.astype(np.float64), la.k.astype(np.float64), la.v.astype(np.float64), la.start)
+        dt = time.perf_counter() - t0
+        return {"value": T * la.H * la.dv / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
+                "sample": "first %d steps of the tape, all %d heads, forward readout" % (T, la.H)}
+    # diagonal: whole tapes of the workload's law, capped so the oracle runs
+    # for about budget_s seconds at most
+    T = w.T
+    B = w.B
+    d = w.d
+    cap = 64 << 20 if w.dtype != "c64" else 24 << 20
+    if B * T * d > cap:
+        if B > 1:
+            B = max(1, cap // (T * d))
+        else:
+            T = max(1, cap // d)
+    t = tapes.make_diag(key, B=B, T=T)
+    a, x = t.decoded("a"), t.decoded("x")
+    t0 = time.perf_counter()
+    h, _ = oracle.diag_fwd(a, x, t.start)
+    if w.backward:
+        oracle.diag_bwd(a, t.start, h, t.decoded("g"))
+    dt = time.perf_counter() - t0
+    what = "forward + reverse" if w.backward else "forward"
+    return {"value": B * T * d / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
+            "sample": "%d tape(s) x %d steps x %d features of the same law, %s, fp64, %.1f s"
+                      % (B, T, d, what, dt)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: the scan is measured at one GPU's share of the tape; "
+              "--gpus %d is not supported" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2402_09900_amd import binding as mb
+    from paper_2402_09900_amd import tapes
+
+    key = args.workload
+    wl = tapes.WORKLOADS[key]
+    flops = None
+    if wl.kind == "linattn":
+        w, calls, bytes_per, n, flops = setup_linattn(torch, mb, tapes)
+    else:
+        w, calls, bytes_per, n = setup_diag(torch, mb, tapes, key)
+    timers = {name: Timer(torch) for name in calls}
+
+    def step(timed):
+        for name, fn in calls.items():
+            if timed:
+                timers[name](fn)
+            else:
+                fn()
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall * 1e3 / max(args.steps, 1)
+    value = n / (ms_per_step * 1e-3)
+
+    per_call_ms = {name: timers[name].mean_ms() for name in calls}
+    dom = max(per_call_ms, key=per_call_ms.get)
+    if flops is not None:
+        achieved = flops / (per_call_ms[dom] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": FP32_MFMA_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": None}
+    else:
+        achieved = bytes_per[dom] / (per_call_ms[dom] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None}
+    roof["kernel"] = {"fwd": "memoroid_scan_diag" if wl.kind == "diag" else "memoroid_scan_linattn",
+                      "bwd": "memoroid_scan_diag_bwd"}[dom]
+    roof["ms_per_launch"] = round(per_call_ms[dom], 4)
+    roof["algorithmic_bytes_per_launch"] = int(bytes_per[dom])
+    if flops is not None:
+        roof["algorithmic_flops_per_launch"] = int(flops)
+
+    result = {
+        "metric": METRIC,
+        "value": value,
+        "unit": UNIT,
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": {"f32": "f32", "bf16": "bf16 in / f32 state", "c64": "c64"}[wl.dtype],
+        "data": "synthetic",
+        "config": {"workload": wl.name, "B": wl.B, "T": wl.T,
+                   ("heads" if wl.kind == "linattn" else "d"): wl.d,
+                   "passes": list(calls.keys()),
+                   "ms_per_call": {k: round(v, 4) for k, v in per_call_ms.items()},
+                   "GBps_per_call": {k: round(bytes_per[k] / (per_call_ms[k] * 1e-3) / 1e9, 1)
+                                     for k in calls}},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(key, tapes)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

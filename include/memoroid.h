@@ -1,0 +1,178 @@
+/*
+ * memoroid.h -- C ABI of libmemoroid.so: resettable memoroid scans on AMD
+ * MI355X (gfx950).
+ *
+ * The library computes the hot path of "Recurrent Reinforcement Learning with
+ * Memoroids" (arXiv 2402.09900): the inclusive scan of a memoroid over a tape
+ * of episodes laid end to end (Tape-Based Batching, Section 4.1), where the
+ * resettable monoid transform (Section 4, "Inline Recurrent State Resets")
+ * stops all information flow at every episode boundary, and the reverse scan
+ * that back-propagates through it.
+ *
+ * Conventions common to every entry point
+ * ---------------------------------------
+ *  - Every data pointer is a DEVICE pointer (hipMalloc / torch CUDA memory),
+ *    owned by the caller.  The library allocates nothing on the call path and
+ *    keeps no state between calls.
+ *  - Calls are asynchronous: they validate the arguments, enqueue kernels on
+ *    `stream` (a hipStream_t passed as void*, NULL = the null stream) and
+ *    return.  Faults inside a kernel surface at the caller's next
+ *    synchronisation.
+ *  - Return value: MEMOROID_OK (0) or a negative memoroid_status.  Argument
+ *    errors are detected before any HIP call, so nothing is enqueued when a
+ *    call fails validation.  No C++ exception crosses this boundary.
+ *  - A tape is row-major [B][T][d] with the d features of a step contiguous;
+ *    start[B][T] holds one byte per step, nonzero meaning "an episode begins
+ *    at this step" (the begin flag b of Section 2.1).  Step 0 of every tape is
+ *    treated as a begin step whatever its byte is: the scan starts from the
+ *    identity g_I = (e_I, 0) of the resettable monoid.
+ *  - Resets are selects: the state after a begin step holds that step's input
+ *    and nothing older, so a NaN or Inf never crosses an episode boundary.
+ *  - An empty problem (B, T or d equal to 0) returns MEMOROID_OK and enqueues
+ *    nothing.
+ *  - Outputs must not alias inputs (MEMOROID_EINVAL if the same pointer is
+ *    passed for both).
+ *  - Every pointer must be aligned to its element size (4 bytes for f32, 2 for
+ *    bf16, 8 for complex64, 4 for int32).  Rows whose pointers are 16-byte
+ *    aligned and whose d is a multiple of the vector width (4 f32, 8 bf16,
+ *    2 complex64) take the vectorised kernels; other shapes take a scalar
+ *    kernel with identical results.
+ *  - The workspace is caller-allocated device memory of at least the size the
+ *    matching *_workspace_bytes query returns for the same arguments.  Its
+ *    contents are undefined on entry and on exit; the call initialises what it
+ *    needs on `stream`.  Concurrent calls must use distinct workspaces.
+ */
+#ifndef MEMOROID_H
+#define MEMOROID_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MEMOROID_ABI_VERSION 1
+
+typedef enum {
+    MEMOROID_OK = 0,
+    MEMOROID_EINVAL = -1,       /* bad pointer, extent, stride, alignment or aliasing */
+    MEMOROID_EUNSUPPORTED = -2, /* valid but unsupported dtype pair or shape */
+    MEMOROID_EWORKSPACE = -3,   /* workspace NULL or smaller than the query's size */
+    MEMOROID_EHIP = -4,         /* a HIP runtime call or kernel launch failed */
+    MEMOROID_ETIMEOUT = -5      /* memoroid_workspace_status: a cross-tile wait gave up */
+} memoroid_status;
+
+typedef enum {
+    MEMOROID_F32 = 0,   /* float */
+    MEMOROID_BF16 = 1,  /* bfloat16, stored as uint16 bit patterns */
+    MEMOROID_C64 = 2    /* complex float, interleaved (re, im) */
+} memoroid_dtype;
+
+/* Version of this header the library was built from (MEMOROID_ABI_VERSION). */
+int memoroid_abi_version(void);
+
+/* Static, human-readable text for a memoroid_status value. */
+const char* memoroid_status_string(int status);
+
+/* ------------------------------------------------------------------------
+ * Diagonal linear memoroid, forward.
+ *
+ * The S5 and LRU memoroids (App. G.2, G.3) with a diagonal transition, whose
+ * monoid is (X, x) . (X', x') = (X'X, X'x + x') with e_I = (1, 0), give under
+ * the reset transform the recurrence
+ *     h_t = x_t                       if step t begins an episode,
+ *     h_t = a_t * h_{t-1} + x_t       otherwise,
+ * element-wise over the d features (complex multiply for MEMOROID_C64).  The
+ * FFM memoroid (App. G.4) is the complex case with a time-invariant a.
+ *
+ *   a          per-step a[B][T][d] when a_stride_t == d, or one a[d] shared by
+ *              every tape and step when a_stride_t == 0 (the time-invariant
+ *              transition of S5 / LRU / FFM).  Any other stride: EINVAL.
+ *   x          x[B][T][d], the lifted inputs f(o_t) computed by the caller.
+ *   start      start[B][T] begin flags.
+ *   h          out h[B][T][d].
+ *   episode_idx  optional out int32[B][T]: number of begin steps at or before
+ *              t in the same tape, minus one (the episode index of Fig. 2).
+ *              NULL skips it.
+ *   in_dtype / out_dtype: (F32,F32), (BF16,BF16), (BF16,F32), (C64,C64).
+ *              bf16 inputs are decoded exactly and the state is carried in
+ *              fp32; bf16 outputs are rounded to nearest even.  Other pairs:
+ *              EUNSUPPORTED.
+ * ------------------------------------------------------------------------ */
+size_t memoroid_scan_diag_workspace_bytes(int64_t B, int64_t T, int64_t d,
+                                          int in_dtype, int out_dtype);
+
+int memoroid_scan_diag(const void* a, int64_t a_stride_t,
+                       const void* x, const uint8_t* start,
+                       void* h, int32_t* episode_idx,
+                       int64_t B, int64_t T, int64_t d,
+                       int in_dtype, int out_dtype,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Diagonal linear memoroid, reverse scan (gradients).
+ *
+ * The paper differentiates through the scan with automatic differentiation;
+ * this is that derivative written out, with the conjugate convention of
+ * complex autograd (a gradient is dL/d conj(z)):
+ *     lam_t = g_t + [t+1 < T and t+1 is not a begin step] * conj(a_{t+1}) * lam_{t+1}
+ *     grad_x_t = lam_t
+ *     grad_a_t = [t is not a begin step] * lam_t * conj(h_{t-1})
+ * i.e. the same resettable scan run from the end of the tape, with the
+ * episode ends (the steps before begin steps, and the tape end) as resets.
+ *
+ *   a, a_stride_t  as in memoroid_scan_diag.
+ *   start      start[B][T].
+ *   h          the forward output h[B][T][d] (saved activation).
+ *   grad_h     upstream gradient g = dL/dh, [B][T][d].
+ *   grad_x     out [B][T][d].
+ *   grad_a     out [B][T][d] when a_stride_t == d; out [d], summed over every
+ *              tape and step, when a_stride_t == 0.  NULL skips it.
+ *   dtype      MEMOROID_F32 or MEMOROID_C64 (all tensors of that dtype).
+ * ------------------------------------------------------------------------ */
+size_t memoroid_scan_diag_bwd_workspace_bytes(int64_t B, int64_t T, int64_t d,
+                                              int dtype, int64_t a_stride_t);
+
+int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t,
+                           const uint8_t* start, const void* h, const void* grad_h,
+                           void* grad_x, void* grad_a,
+                           int64_t B, int64_t T, int64_t d, int dtype,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Linear-transformer memoroid (App. G.1), forward readout, one tape of T
+ * steps with H independent heads.  Per head, with S (dk x dv) and z (dk)
+ * reset to zero at every begin step:
+ *     S_t = S_{t-1} + phi(k_t) v_t^T,   z_t = z_{t-1} + phi(k_t),
+ *     out_t = phi(q_t)^T S_t / (phi(q_t)^T z_t),   phi(u) = 1 + ELU(u).
+ * The MLP and residual of the paper's readout g are left to the caller.
+ *
+ *   q, k       raw (pre-phi) [T][H][dk] fp32;  v: [T][H][dv] fp32.
+ *   start      start[T].
+ *   out        out [T][H][dv] fp32.
+ *   episode_idx  optional out int32[T] (as above); NULL skips it.
+ *   dk, dv, chunk: this version supports dk == dv == 64 and chunk == 64
+ *              (EUNSUPPORTED otherwise).
+ * ------------------------------------------------------------------------ */
+size_t memoroid_scan_linattn_workspace_bytes(int64_t T, int64_t H, int64_t dk,
+                                             int64_t dv, int64_t chunk);
+
+int memoroid_scan_linattn(const float* q, const float* k, const float* v,
+                          const uint8_t* start, float* out, int32_t* episode_idx,
+                          int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t chunk,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Health of the last call that used `workspace`: synchronises `stream`,
+ * then returns MEMOROID_OK, or MEMOROID_ETIMEOUT if a kernel's bounded wait
+ * for a predecessor tile gave up (its outputs are then invalid), or
+ * MEMOROID_EHIP if the copy failed.  Intended for tests and debugging.
+ * ------------------------------------------------------------------------ */
+int memoroid_workspace_status(const void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MEMOROID_H */

@@ -1,0 +1,308 @@
+"""Python binding of libmemoroid.so (C ABI in include/memoroid.h).
+
+Two layers, both argument marshalling only -- every step of the computation
+runs in the library's HIP kernels:
+
+* ``memoroid_*`` functions with the C names and signatures (plain integers
+  for pointers), for callers that manage device memory themselves;
+* ``scan_diag``, ``scan_diag_bwd``, ``scan_linattn`` taking torch CUDA
+  tensors: they check shapes, dtypes and contiguity, allocate outputs and the
+  workspace with ``torch.empty`` and launch on the current torch stream.
+  ``DiagScan`` wraps the diagonal pair as a ``torch.autograd.Function``.
+
+Loading fails loudly (``MemoroidError``) if the shared library is missing:
+there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmemoroid.so")
+
+OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP, ETIMEOUT = 0, -1, -2, -3, -4, -5
+F32, BF16, C64 = 0, 1, 2
+
+_lib = None
+
+
+class MemoroidError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__("%s failed: %s (status %d)" % (where, status_string(status), status))
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library (loaded on first use)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise MemoroidError(EHIP, "loading %s (not built: run python -m paper_2402_09900_amd.build)"
+                                % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        P, I64, I32, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
+        L.memoroid_abi_version.restype = I32
+        L.memoroid_abi_version.argtypes = []
+        L.memoroid_status_string.restype = ctypes.c_char_p
+        L.memoroid_status_string.argtypes = [I32]
+        L.memoroid_scan_diag_workspace_bytes.restype = SZ
+        L.memoroid_scan_diag_workspace_bytes.argtypes = [I64, I64, I64, I32, I32]
+        L.memoroid_scan_diag.restype = I32
+        L.memoroid_scan_diag.argtypes = [P, I64, P, P, P, P, I64, I64, I64, I32, I32, P, SZ, P]
+        L.memoroid_scan_diag_bwd_workspace_bytes.restype = SZ
+        L.memoroid_scan_diag_bwd_workspace_bytes.argtypes = [I64, I64, I64, I32, I64]
+        L.memoroid_scan_diag_bwd.restype = I32
+        L.memoroid_scan_diag_bwd.argtypes = [P, I64, P, P, P, P, P, I64, I64, I64, I32, P, SZ, P]
+        L.memoroid_scan_linattn_workspace_bytes.restype = SZ
+        L.memoroid_scan_linattn_workspace_bytes.argtypes = [I64, I64, I64, I64, I64]
+        L.memoroid_scan_linattn.restype = I32
+        L.memoroid_scan_linattn.argtypes = [P, P, P, P, P, P, I64, I64, I64, I64, I64, P, SZ, P]
+        L.memoroid_workspace_status.restype = I32
+        L.memoroid_workspace_status.argtypes = [P, SZ, P]
+        _lib = L
+    return _lib
+
+
+# ------------------------------------------------------------ C-named layer
+
+def memoroid_abi_version() -> int:
+    return lib().memoroid_abi_version()
+
+
+def status_string(status: int) -> str:
+    try:
+        return lib().memoroid_status_string(status).decode()
+    except MemoroidError:
+        return "status %d" % status
+
+
+def memoroid_status_string(status: int) -> str:
+    return status_string(status)
+
+
+def memoroid_scan_diag_workspace_bytes(B, T, d, in_dtype, out_dtype) -> int:
+    return lib().memoroid_scan_diag_workspace_bytes(B, T, d, in_dtype, out_dtype)
+
+
+def memoroid_scan_diag(a, a_stride_t, x, start, h, episode_idx, B, T, d, in_dtype, out_dtype,
+                       workspace, workspace_bytes, stream) -> int:
+    return lib().memoroid_scan_diag(a, a_stride_t, x, start, h, episode_idx, B, T, d, in_dtype,
+                                    out_dtype, workspace, workspace_bytes, stream)
+
+
+def memoroid_scan_diag_bwd_workspace_bytes(B, T, d, dtype, a_stride_t) -> int:
+    return lib().memoroid_scan_diag_bwd_workspace_bytes(B, T, d, dtype, a_stride_t)
+
+
+def memoroid_scan_diag_bwd(a, a_stride_t, start, h, grad_h, grad_x, grad_a, B, T, d, dtype,
+                           workspace, workspace_bytes, stream) -> int:
+    return lib().memoroid_scan_diag_bwd(a, a_stride_t, start, h, grad_h, grad_x, grad_a, B, T, d,
+                                        dtype, workspace, workspace_bytes, stream)
+
+
+def memoroid_scan_linattn_workspace_bytes(T, H, dk, dv, chunk) -> int:
+    return lib().memoroid_scan_linattn_workspace_bytes(T, H, dk, dv, chunk)
+
+
+def memoroid_scan_linattn(q, k, v, start, out, episode_idx, T, H, dk, dv, chunk,
+                          workspace, workspace_bytes, stream) -> int:
+    return lib().memoroid_scan_linattn(q, k, v, start, out, episode_idx, T, H, dk, dv, chunk,
+                                       workspace, workspace_bytes, stream)
+
+
+def memoroid_workspace_status(workspace, workspace_bytes, stream) -> int:
+    return lib().memoroid_workspace_status(workspace, workspace_bytes, stream)
+
+
+# ------------------------------------------------------------- torch layer
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.complex64:
+        return C64
+    raise TypeError("unsupported dtype %s (float32, bfloat16 or complex64)" % t.dtype)
+
+
+def _stream_ptr(device) -> int:
+    torch = _torch()
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _check_cuda(*ts):
+    dev = None
+    for t in ts:
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError("tensors must live on a CUDA (HIP) device")
+        if not t.is_contiguous():
+            raise ValueError("tensors must be contiguous")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise ValueError("tensors must live on one device")
+    return dev
+
+
+def _raise(status: int, where: str):
+    if status != OK:
+        raise MemoroidError(status, where)
+
+
+def _workspace(nbytes: int, device, workspace=None):
+    torch = _torch()
+    if workspace is not None and workspace.numel() >= nbytes:
+        return workspace
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+def _diag_shapes(a, x, start):
+    if x.dim() == 2:
+        x = x.unsqueeze(0)
+    if x.dim() != 3:
+        raise ValueError("x must be [B, T, d] or [T, d]")
+    B, T, d = x.shape
+    if a.dim() == 1:
+        if a.shape[0] != d:
+            raise ValueError("time-invariant a must have shape [d]")
+        stride = 0
+    else:
+        a = a.reshape(B, T, d)
+        stride = d
+    start = start.reshape(B, T)
+    return a, x, start, B, T, d, stride
+
+
+def scan_diag(a, x, start, out_dtype=None, episode_idx: bool = False, workspace=None):
+    """h_t = x_t at a begin step, else a_t * h_{t-1} + x_t (per feature).
+
+    a: [B,T,d] per step or [d] time-invariant; x: [B,T,d] (or [T,d]);
+    start: uint8 [B,T].  Dtypes: float32, bfloat16 (fp32 state; out_dtype
+    bfloat16 by default, or float32) or complex64.  Returns h, plus the int32
+    episode index [B,T] when episode_idx is true."""
+    torch = _torch()
+    a, x, start, B, T, d, stride = _diag_shapes(a, x, start)
+    dev = _check_cuda(a, x, start)
+    if start.dtype != torch.uint8:
+        raise TypeError("start must be uint8")
+    if a.dtype != x.dtype:
+        raise TypeError("a and x must share a dtype")
+    in_dt = _dtype_code(x)
+    out_torch = x.dtype if out_dtype is None else out_dtype
+    out_dt = _dtype_code(torch.empty(0, dtype=out_torch))
+    h = torch.empty((B, T, d), dtype=out_torch, device=dev)
+    idx = torch.empty((B, T), dtype=torch.int32, device=dev) if episode_idx else None
+    nbytes = lib().memoroid_scan_diag_workspace_bytes(B, T, d, in_dt, out_dt)
+    ws = _workspace(nbytes, dev, workspace)
+    st = lib().memoroid_scan_diag(a.data_ptr(), stride, x.data_ptr(), start.data_ptr(), h.data_ptr(),
+                                  idx.data_ptr() if idx is not None else None, B, T, d, in_dt, out_dt,
+                                  ws.data_ptr(), ws.numel(), _stream_ptr(dev))
+    _raise(st, "memoroid_scan_diag")
+    return (h, idx) if episode_idx else h
+
+
+def scan_diag_bwd(a, start, h, grad_h, need_grad_a: bool = True, workspace=None):
+    """Reverse scan: returns (grad_x, grad_a); grad_a is [B,T,d] for per-step
+    a, [d] for time-invariant a, None if not requested."""
+    torch = _torch()
+    a, grad_h, start, B, T, d, stride = _diag_shapes(a, grad_h, start)
+    h = h.reshape(B, T, d) if h is not None else None
+    dev = _check_cuda(a, grad_h, start, h)
+    if start.dtype != torch.uint8:
+        raise TypeError("start must be uint8")
+    dt = _dtype_code(grad_h)
+    if dt == BF16:
+        raise TypeError("the reverse scan takes float32 or complex64")
+    for t in (a, h):
+        if t is not None and t.dtype != grad_h.dtype:
+            raise TypeError("a, h and grad_h must share a dtype")
+    gx = torch.empty((B, T, d), dtype=grad_h.dtype, device=dev)
+    ga = None
+    if need_grad_a:
+        ga = torch.empty((B, T, d) if stride else (d,), dtype=grad_h.dtype, device=dev)
+    nbytes = lib().memoroid_scan_diag_bwd_workspace_bytes(B, T, d, dt, stride)
+    ws = _workspace(nbytes, dev, workspace)
+    st = lib().memoroid_scan_diag_bwd(a.data_ptr(), stride, start.data_ptr(),
+                                      h.data_ptr() if h is not None else None, grad_h.data_ptr(),
+                                      gx.data_ptr(), ga.data_ptr() if ga is not None else None,
+                                      B, T, d, dt, ws.data_ptr(), ws.numel(), _stream_ptr(dev))
+    _raise(st, "memoroid_scan_diag_bwd")
+    return gx, ga
+
+
+def scan_linattn(q, k, v, start, episode_idx: bool = False, chunk: int = 64, workspace=None):
+    """Linear-transformer memoroid readout phi(q)^T S / (phi(q)^T z) over one
+    tape.  q, k: [T,H,dk]; v: [T,H,dv] float32; start: uint8 [T]."""
+    torch = _torch()
+    dev = _check_cuda(q, k, v, start)
+    T, H, dk = q.shape
+    dv = v.shape[2]
+    if k.shape != q.shape or v.shape[:2] != (T, H):
+        raise ValueError("q, k must be [T,H,dk] and v [T,H,dv]")
+    for t in (q, k, v):
+        if t.dtype != torch.float32:
+            raise TypeError("q, k, v must be float32")
+    if start.dtype != torch.uint8 or start.numel() != T:
+        raise TypeError("start must be uint8 [T]")
+    out = torch.empty((T, H, dv), dtype=torch.float32, device=dev)
+    idx = torch.empty((T,), dtype=torch.int32, device=dev) if episode_idx else None
+    nbytes = lib().memoroid_scan_linattn_workspace_bytes(T, H, dk, dv, chunk)
+    ws = _workspace(nbytes, dev, workspace)
+    st = lib().memoroid_scan_linattn(q.data_ptr(), k.data_ptr(), v.data_ptr(), start.data_ptr(),
+                                     out.data_ptr(), idx.data_ptr() if idx is not None else None,
+                                     T, H, dk, dv, chunk, ws.data_ptr(), ws.numel(), _stream_ptr(dev))
+    _raise(st, "memoroid_scan_linattn")
+    return (out, idx) if episode_idx else out
+
+
+def workspace_status(workspace) -> int:
+    """Synchronise and report whether the last call on `workspace` timed out
+    in a cross-tile wait (ETIMEOUT) or completed normally (OK)."""
+    return lib().memoroid_workspace_status(workspace.data_ptr(), workspace.numel(),
+                                           _stream_ptr(workspace.device))
+
+
+def _make_autograd():
+    torch = _torch()
+
+    class DiagScan(torch.autograd.Function):
+        """Differentiable diagonal resettable scan (float32 / complex64)."""
+
+        @staticmethod
+        def forward(ctx, a, x, start):
+            h = scan_diag(a, x, start)
+            ctx.save_for_backward(a, start, h)
+            ctx.x_shape = x.shape
+            return h.reshape(x.shape)
+
+        @staticmethod
+        def backward(ctx, grad_h):
+            a, start, h = ctx.saved_tensors
+            gx, ga = scan_diag_bwd(a, start, h, grad_h.contiguous(), need_grad_a=ctx.needs_input_grad[0])
+            if ga is not None:
+                ga = ga.reshape(a.shape)
+            return ga, gx.reshape(ctx.x_shape), None
+
+    return DiagScan
+
+
+_DiagScan = None
+
+
+def diag_scan(a, x, start):
+    """Autograd-aware scan_diag."""
+    global _DiagScan
+    if _DiagScan is None:
+        _DiagScan = _make_autograd()
+    return _DiagScan.apply(a, x, start)

@@ -1,0 +1,391 @@
+// abi.hip -- the extern "C" entry points declared in include/memoroid.h:
+// argument validation (before any HIP call), tiling plans, workspace layout
+// and kernel launches.
+#include <limits.h>
+#include <string.h>
+
+#include "memoroid.h"
+#include "kernels.hpp"
+#include "scan_common.hpp"
+
+using namespace memoroid;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+int elem_bytes(int dt) { return dt == MEMOROID_F32 ? 4 : dt == MEMOROID_BF16 ? 2 : 8; }
+int vec_width(int dt) { return dt == MEMOROID_F32 ? 4 : dt == MEMOROID_BF16 ? 8 : 2; }
+int64_t next_pow2(int64_t v) {
+    int64_t p = 1;
+    while (p < v) p <<= 1;
+    return p;
+}
+bool aligned(const void* p, size_t n) { return ((uintptr_t)p % n) == 0; }
+
+// Overflow-checked product of non-negative extents.
+bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+    if (a != 0 && b > INT64_MAX / a) return false;
+    *out = a * b;
+    return true;
+}
+
+struct DiagPlan {
+    int VEC = 1;
+    int Qp = 1;
+    int Dp = 1;
+    int nfb = 1;
+    int64_t L = 1;
+    int64_t nt = 0;
+    int64_t nchains = 0;
+    int64_t ntiles = 0;
+    size_t off_agg = 0, off_incl = 0, off_part = 0, off_sum1 = 0, off_sum2 = 0, off_counts = 0;
+    size_t fill_bytes = 0;   // bytes from off_agg that must start as 0xFF
+    size_t total = 0;
+};
+
+// Tiling and workspace layout of a diagonal scan.  `vec` selects the
+// vectorised lane width; `state_complex` picks the descriptor size.
+bool plan_diag(int64_t B, int64_t T, int64_t d, int state_dtype, bool vec, int rows, bool bwd,
+               bool ainv, bool want_grad_a, DiagPlan* p) {
+    const int VEC = vec ? vec_width(state_dtype) : 1;
+    const int64_t lanes = (d + VEC - 1) / VEC;
+    const int64_t Qp = lanes >= 64 ? 64 : next_pow2(lanes);
+    p->VEC = VEC;
+    p->Qp = (int)Qp;
+    p->Dp = (int)(Qp * VEC);
+    p->nfb = (int)((d + p->Dp - 1) / p->Dp);
+    p->L = (256 / Qp) * rows;
+    p->nt = (T + p->L - 1) / p->L;
+    if (!mul_ok(B, p->nfb, &p->nchains)) return false;
+    if (!mul_ok(p->nt, p->nchains, &p->ntiles)) return false;
+    if (p->ntiles >= (int64_t)INT32_MAX || p->nchains >= (int64_t)INT32_MAX) return false;
+    const bool cplx = state_dtype == MEMOROID_C64;
+    const size_t agg_b = cplx ? 16 : 8, incl_b = cplx ? 8 : 4;
+    int64_t ndesc;
+    if (!mul_ok(p->ntiles, p->Dp, &ndesc)) return false;
+    if (ndesc > INT64_MAX / 32) return false;
+    size_t off = kAlign;                                   // header
+    p->off_agg = off;
+    off = align_up(off + (size_t)ndesc * agg_b);
+    p->off_incl = off;
+    off = align_up(off + (size_t)ndesc * incl_b);
+    p->fill_bytes = off - p->off_agg;
+    if (bwd && ainv && want_grad_a) {
+        const size_t sb = cplx ? 8 : 4;
+        const int64_t rows_part = p->nt * B;
+        p->off_part = off;
+        off = align_up(off + (size_t)rows_part * (size_t)d * sb);
+        const int64_t r1 = (rows_part + 63) / 64, r2 = (r1 + 63) / 64;
+        p->off_sum1 = off;
+        off = align_up(off + (size_t)r1 * (size_t)d * sb);
+        p->off_sum2 = off;
+        off = align_up(off + (size_t)r2 * (size_t)d * sb);
+    }
+    p->off_counts = off;
+    if (!bwd) off = align_up(off + (size_t)B * (size_t)((T + kEpBlock - 1) / kEpBlock) * 4);
+    p->total = off;
+    return true;
+}
+
+int check_hip(hipError_t e) { return e == hipSuccess ? MEMOROID_OK : MEMOROID_EHIP; }
+
+bool diag_dtypes_ok(int in_dt, int out_dt) {
+    return (in_dt == MEMOROID_F32 && out_dt == MEMOROID_F32) || (in_dt == MEMOROID_BF16 && out_dt == MEMOROID_BF16) ||
+           (in_dt == MEMOROID_BF16 && out_dt == MEMOROID_F32) || (in_dt == MEMOROID_C64 && out_dt == MEMOROID_C64);
+}
+
+
+// Reduce a [rows][cols] float matrix over rows into out[cols], 64 rows per
+// pass, in a fixed order.
+int reduce_rows(const float* part, float* s1, float* s2, float* out, int64_t rows, int64_t cols,
+                hipStream_t s) {
+    const float* cur = part;
+    float* bufs[2] = {s1, s2};
+    int which = 0;
+    while (rows > 64) {
+        if (colsum_launch(cur, bufs[which], rows, cols, 64, s) != hipSuccess) return MEMOROID_EHIP;
+        cur = bufs[which];
+        which ^= 1;
+        rows = (rows + 63) / 64;
+    }
+    return check_hip(colsum_launch(cur, out, rows, cols, rows > 0 ? rows : 1, s));
+}
+
+}  // namespace
+
+extern "C" {
+
+int memoroid_abi_version(void) { return MEMOROID_ABI_VERSION; }
+
+const char* memoroid_status_string(int status) {
+    switch (status) {
+        case MEMOROID_OK: return "ok";
+        case MEMOROID_EINVAL: return "invalid argument (pointer, extent, stride, alignment or aliasing)";
+        case MEMOROID_EUNSUPPORTED: return "unsupported dtype combination or shape";
+        case MEMOROID_EWORKSPACE: return "workspace missing or too small";
+        case MEMOROID_EHIP: return "HIP runtime error";
+        case MEMOROID_ETIMEOUT: return "a cross-tile wait gave up; outputs are invalid";
+        default: return "unknown status";
+    }
+}
+
+// ------------------------------------------------------------- diag forward
+
+size_t memoroid_scan_diag_workspace_bytes(int64_t B, int64_t T, int64_t d, int in_dtype, int out_dtype) {
+    if (B < 0 || T < 0 || d < 0 || !diag_dtypes_ok(in_dtype, out_dtype)) return 0;
+    if (B == 0 || T == 0 || d == 0) return 0;
+    DiagPlan pv, ps;
+    const int sd = in_dtype == MEMOROID_C64 ? MEMOROID_C64 : (in_dtype == MEMOROID_BF16 ? MEMOROID_BF16 : MEMOROID_F32);
+    size_t best = 0;
+    for (int vec = 0; vec < 2; ++vec) {
+        DiagPlan& p = vec ? pv : ps;
+        if (!plan_diag(B, T, d, sd, vec, kFwdRows, false, false, false, &p)) return 0;
+        if (p.total > best) best = p.total;
+    }
+    return best;
+}
+
+int memoroid_scan_diag(const void* a, int64_t a_stride_t, const void* x, const uint8_t* start, void* h,
+                       int32_t* episode_idx, int64_t B, int64_t T, int64_t d, int in_dtype, int out_dtype,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+    if (B < 0 || T < 0 || d < 0) return MEMOROID_EINVAL;
+    if (!diag_dtypes_ok(in_dtype, out_dtype)) return MEMOROID_EUNSUPPORTED;
+    if (B == 0 || T == 0 || d == 0) return MEMOROID_OK;
+    int64_t BT, BTd;
+    if (!mul_ok(B, T, &BT) || !mul_ok(BT, d, &BTd) || BTd > INT64_MAX / 16) return MEMOROID_EINVAL;
+    if (!a || !x || !start || !h) return MEMOROID_EINVAL;
+    if (a_stride_t != 0 && a_stride_t != d) return MEMOROID_EINVAL;
+    const int ib = elem_bytes(in_dtype), ob = elem_bytes(out_dtype);
+    if (!aligned(a, ib) || !aligned(x, ib) || !aligned(h, ob) || (episode_idx && !aligned(episode_idx, 4)))
+        return MEMOROID_EINVAL;
+    if (h == x || h == a || (const void*)episode_idx == (const void*)h || (const void*)episode_idx == x ||
+        (const void*)episode_idx == a || (const void*)episode_idx == (const void*)start)
+        return MEMOROID_EINVAL;
+    if (episode_idx && B > 65535) return MEMOROID_EUNSUPPORTED;
+    const bool ainv = a_stride_t == 0;
+    const int VW = vec_width(in_dtype);
+    const bool vec = d % VW == 0 && aligned(x, 16) && aligned(h, 16) && aligned(a, 16);
+    const int sd = in_dtype == MEMOROID_C64 ? MEMOROID_C64 : (in_dtype == MEMOROID_BF16 ? MEMOROID_BF16 : MEMOROID_F32);
+    DiagPlan p;
+    if (!plan_diag(B, T, d, sd, vec, kFwdRows, false, ainv, false, &p)) return MEMOROID_EUNSUPPORTED;
+    if (!workspace) return MEMOROID_EWORKSPACE;
+    if (workspace_bytes < memoroid_scan_diag_workspace_bytes(B, T, d, in_dtype, out_dtype) ||
+        workspace_bytes < p.total)
+        return MEMOROID_EWORKSPACE;
+    if (!aligned(workspace, 16)) return MEMOROID_EINVAL;
+
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    if (ws_init_launch(ws, ws + p.off_agg, p.fill_bytes, s) != hipSuccess) return MEMOROID_EHIP;
+    DiagFwdArgs args{};
+    args.a = a;
+    args.x = x;
+    args.start = start;
+    args.h = h;
+    args.T = T;
+    args.d = d;
+    args.Qp = p.Qp;
+    args.nfb = p.nfb;
+    args.nchains = (int32_t)p.nchains;
+    args.agg = ws + p.off_agg;
+    args.incl = ws + p.off_incl;
+    args.hdr = (WsHeader*)ws;
+    const int ik = in_dtype == MEMOROID_F32 ? K_F32 : in_dtype == MEMOROID_BF16 ? K_BF16 : K_C64;
+    const int ok = out_dtype == MEMOROID_F32 ? K_F32 : out_dtype == MEMOROID_BF16 ? K_BF16 : K_C64;
+    if (diag_fwd_launch(ik, ok, vec, ainv, args, p.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
+    if (episode_idx) {
+        if (episode_idx_launch(start, episode_idx, B, T, (int32_t*)(ws + p.off_counts), s) != hipSuccess)
+            return MEMOROID_EHIP;
+    }
+    return MEMOROID_OK;
+}
+
+// ------------------------------------------------------------ diag backward
+
+size_t memoroid_scan_diag_bwd_workspace_bytes(int64_t B, int64_t T, int64_t d, int dtype, int64_t a_stride_t) {
+    if (B < 0 || T < 0 || d < 0 || (dtype != MEMOROID_F32 && dtype != MEMOROID_C64)) return 0;
+    if (B == 0 || T == 0 || d == 0) return 0;
+    size_t best = 0;
+    for (int vec = 0; vec < 2; ++vec) {
+        DiagPlan p;
+        if (!plan_diag(B, T, d, dtype, vec, kBwdRows, true, a_stride_t == 0, true, &p)) return 0;
+        if (p.total > best) best = p.total;
+    }
+    return best;
+}
+
+int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t, const uint8_t* start, const void* h,
+                           const void* grad_h, void* grad_x, void* grad_a, int64_t B, int64_t T, int64_t d,
+                           int dtype, void* workspace, size_t workspace_bytes, void* stream) {
+    if (B < 0 || T < 0 || d < 0) return MEMOROID_EINVAL;
+    if (dtype != MEMOROID_F32 && dtype != MEMOROID_C64) return MEMOROID_EUNSUPPORTED;
+    if (B == 0 || T == 0 || d == 0) return MEMOROID_OK;
+    int64_t BT, BTd;
+    if (!mul_ok(B, T, &BT) || !mul_ok(BT, d, &BTd) || BTd > INT64_MAX / 16) return MEMOROID_EINVAL;
+    if (!a || !start || !grad_h || !grad_x || (grad_a && !h)) return MEMOROID_EINVAL;
+    if (a_stride_t != 0 && a_stride_t != d) return MEMOROID_EINVAL;
+    const int eb = elem_bytes(dtype);
+    if (!aligned(a, eb) || !aligned(grad_h, eb) || !aligned(grad_x, eb) || (h && !aligned(h, eb)) ||
+        (grad_a && !aligned(grad_a, eb)))
+        return MEMOROID_EINVAL;
+    if (grad_x == grad_h || grad_x == a || (h && grad_x == h) ||
+        (grad_a && (grad_a == grad_x || grad_a == grad_h || grad_a == a || grad_a == h)))
+        return MEMOROID_EINVAL;
+    const bool ainv = a_stride_t == 0;
+    const int VW = vec_width(dtype);
+    const bool vec = d % VW == 0 && aligned(a, 16) && aligned(grad_h, 16) && aligned(grad_x, 16) &&
+                     (!h || aligned(h, 16)) && (!grad_a || aligned(grad_a, 16));
+    DiagPlan p;
+    if (!plan_diag(B, T, d, dtype, vec, kBwdRows, true, ainv, grad_a != nullptr, &p)) return MEMOROID_EUNSUPPORTED;
+    if (!workspace) return MEMOROID_EWORKSPACE;
+    if (workspace_bytes < memoroid_scan_diag_bwd_workspace_bytes(B, T, d, dtype, a_stride_t) ||
+        workspace_bytes < p.total)
+        return MEMOROID_EWORKSPACE;
+    if (!aligned(workspace, 16)) return MEMOROID_EINVAL;
+
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    if (ws_init_launch(ws, ws + p.off_agg, p.fill_bytes, s) != hipSuccess) return MEMOROID_EHIP;
+    DiagBwdArgs args{};
+    args.a = a;
+    args.start = start;
+    args.h = h;
+    args.g = grad_h;
+    args.dx = grad_x;
+    args.da = ainv ? nullptr : grad_a;
+    args.da_part = (ainv && grad_a) ? ws + p.off_part : nullptr;
+    args.T = T;
+    args.d = d;
+    args.nt = p.nt;
+    args.Qp = p.Qp;
+    args.nfb = p.nfb;
+    args.nchains = (int32_t)p.nchains;
+    args.agg = ws + p.off_agg;
+    args.incl = ws + p.off_incl;
+    args.hdr = (WsHeader*)ws;
+    const int k = dtype == MEMOROID_F32 ? K_F32 : K_C64;
+    if (diag_bwd_launch(k, vec, ainv, args, p.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
+    if (ainv && grad_a) {
+        const int64_t cols = d * (dtype == MEMOROID_C64 ? 2 : 1);
+        const int st = reduce_rows((const float*)(ws + p.off_part), (float*)(ws + p.off_sum1),
+                                   (float*)(ws + p.off_sum2), (float*)grad_a, p.nt * B, cols, s);
+        if (st != MEMOROID_OK) return st;
+    }
+    return MEMOROID_OK;
+}
+
+// ---------------------------------------------------------- linear attention
+// Summaries per (chunk, head) -> resettable sum-scan of the chunk states over
+// chunks (the diagonal scan with a = 1, the monoid of App. G.1 being a sum)
+// -> outputs per (chunk, head).
+
+namespace {
+
+struct LinPlan {
+    int64_t nch = 0, dstate = 0;
+    size_t off_dS = 0, off_Sinc = 0, off_R = 0, off_ones = 0, off_scan = 0, off_counts = 0, total = 0;
+    DiagPlan scan;
+    bool scan_vec = true;
+};
+
+bool plan_linattn(int64_t T, int64_t H, LinPlan* p) {
+    p->nch = (T + kLinChunk - 1) / kLinChunk;
+    p->dstate = H * kLinStateWords;
+    const size_t states = (size_t)p->nch * (size_t)p->dstate * 4;
+    // the state scan's own workspace comes first, so that its header (and
+    // timeout word) sits at offset 0 like every other call's
+    size_t off = 0;
+    p->off_scan = off;
+    // the state scan always runs vectorised: dstate % 4 == 0 and every
+    // buffer is 256-byte aligned inside the workspace
+    if (!plan_diag(1, p->nch, p->dstate, MEMOROID_F32, true, kFwdRows, false, true, false, &p->scan)) return false;
+    off = align_up(off + p->scan.total);
+    p->off_dS = off;
+    off = align_up(off + states);
+    p->off_Sinc = off;
+    off = align_up(off + states);
+    p->off_R = off;
+    off = align_up(off + (size_t)p->nch);
+    p->off_ones = off;
+    off = align_up(off + (size_t)p->dstate * 4);
+    p->off_counts = off;
+    off = align_up(off + (size_t)((T + kEpBlock - 1) / kEpBlock) * 4);
+    p->total = off;
+    return true;
+}
+
+}  // namespace
+
+size_t memoroid_scan_linattn_workspace_bytes(int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t chunk) {
+    if (T <= 0 || H <= 0 || dk != 64 || dv != 64 || chunk != 64) return 0;
+    if (T > (int64_t)INT32_MAX / 2 || H > 65535) return 0;
+    LinPlan p;
+    if (!plan_linattn(T, H, &p)) return 0;
+    return p.total;
+}
+
+int memoroid_scan_linattn(const float* q, const float* k, const float* v, const uint8_t* start, float* out,
+                          int32_t* episode_idx, int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t chunk,
+                          void* workspace, size_t workspace_bytes, void* stream) {
+    if (T < 0 || H < 0 || dk < 0 || dv < 0 || chunk < 0) return MEMOROID_EINVAL;
+    if (dk != 64 || dv != 64 || chunk != 64) return MEMOROID_EUNSUPPORTED;
+    if (T == 0 || H == 0) return MEMOROID_OK;
+    if (T > (int64_t)INT32_MAX / 2 || H > 65535) return MEMOROID_EUNSUPPORTED;
+    if (!q || !k || !v || !start || !out) return MEMOROID_EINVAL;
+    if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
+        (episode_idx && !aligned(episode_idx, 4)))
+        return MEMOROID_EINVAL;
+    if (out == q || out == k || out == v ||
+        (episode_idx && ((void*)episode_idx == (void*)out || (const void*)episode_idx == (const void*)start)))
+        return MEMOROID_EINVAL;
+    LinPlan p;
+    if (!plan_linattn(T, H, &p)) return MEMOROID_EUNSUPPORTED;
+    if (!workspace) return MEMOROID_EWORKSPACE;
+    if (workspace_bytes < p.total) return MEMOROID_EWORKSPACE;
+    if (!aligned(workspace, 256)) return MEMOROID_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    float* dS = (float*)(ws + p.off_dS);
+    float* Sinc = (float*)(ws + p.off_Sinc);
+    uint8_t* R = (uint8_t*)(ws + p.off_R);
+    float* ones = (float*)(ws + p.off_ones);
+    char* sw = ws + p.off_scan;
+    if (fill_f32_launch(ones, p.dstate, 1.0f, s) != hipSuccess) return MEMOROID_EHIP;
+    if (linattn_summary_launch(k, v, start, dS, R, T, H, s) != hipSuccess) return MEMOROID_EHIP;
+    if (ws_init_launch(sw, sw + p.scan.off_agg, p.scan.fill_bytes, s) != hipSuccess) return MEMOROID_EHIP;
+    DiagFwdArgs args{};
+    args.a = ones;
+    args.x = dS;
+    args.start = R;
+    args.h = Sinc;
+    args.T = p.nch;
+    args.d = p.dstate;
+    args.Qp = p.scan.Qp;
+    args.nfb = p.scan.nfb;
+    args.nchains = (int32_t)p.scan.nchains;
+    args.agg = sw + p.scan.off_agg;
+    args.incl = sw + p.scan.off_incl;
+    args.hdr = (WsHeader*)sw;
+    if (diag_fwd_launch(K_F32, K_F32, true, true, args, p.scan.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
+    if (linattn_output_launch(q, k, v, start, Sinc, out, T, H, s) != hipSuccess) return MEMOROID_EHIP;
+    if (episode_idx) {
+        if (episode_idx_launch(start, episode_idx, 1, T, (int32_t*)(ws + p.off_counts), s) != hipSuccess)
+            return MEMOROID_EHIP;
+    }
+    return MEMOROID_OK;
+}
+
+// ------------------------------------------------------------------ status
+
+int memoroid_workspace_status(const void* workspace, size_t workspace_bytes, void* stream) {
+    if (!workspace || workspace_bytes < sizeof(WsHeader)) return MEMOROID_EINVAL;
+    uint32_t hdr[2] = {0, 0};
+    hipStream_t s = (hipStream_t)stream;
+    if (hipMemcpyAsync(hdr, workspace, sizeof(hdr), hipMemcpyDeviceToHost, s) != hipSuccess) return MEMOROID_EHIP;
+    if (hipStreamSynchronize(s) != hipSuccess) return MEMOROID_EHIP;
+    return hdr[1] ? MEMOROID_ETIMEOUT : MEMOROID_OK;
+}
+
+}  // extern "C"

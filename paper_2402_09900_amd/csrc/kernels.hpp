@@ -1,0 +1,81 @@
+// kernels.hpp -- internal interface between the C ABI (abi.hip) and the
+// kernel translation units.  Not installed; not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace memoroid {
+
+struct WsHeader;
+
+// Steps per lane held in registers by the diagonal scans (tile length is
+// 256 / Qp * rows: 64 steps for full-width feature blocks).
+constexpr int kFwdRows = 16;
+constexpr int kBwdRows = 16;
+
+struct DiagFwdArgs {
+    const void* a;
+    const void* x;
+    const uint8_t* start;
+    void* h;
+    int64_t T;
+    int64_t d;
+    int32_t Qp;        // lanes per step row of a tile (power of two, <= 64)
+    int32_t nfb;       // feature blocks per tape
+    int32_t nchains;   // tapes * feature blocks
+    int32_t pad0;
+    void* agg;         // [tiles][Dp] aggregate descriptor words
+    void* incl;        // [tiles][Dp] inclusive-prefix descriptor words
+    WsHeader* hdr;
+};
+
+struct DiagBwdArgs {
+    const void* a;
+    const uint8_t* start;
+    const void* h;
+    const void* g;
+    void* dx;
+    void* da;          // per-step da, or NULL
+    void* da_part;     // time-invariant a: [tiles per chain * B][d] partial sums
+    int64_t T;
+    int64_t d;
+    int64_t nt;        // tiles per chain
+    int32_t Qp;
+    int32_t nfb;
+    int32_t nchains;
+    int32_t pad0;
+    void* agg;
+    void* incl;
+    WsHeader* hdr;
+};
+
+hipError_t diag_fwd_launch(int in_kind, int out_kind, bool vec, bool ainv,
+                           const DiagFwdArgs& args, int64_t ntiles, hipStream_t s);
+hipError_t diag_bwd_launch(int kind, bool vec, bool ainv, const DiagBwdArgs& args,
+                           int64_t ntiles, hipStream_t s);
+hipError_t colsum_launch(const float* in, float* out, int64_t rows, int64_t cols,
+                         int64_t chunk, hipStream_t s);
+
+// Fill `bytes` (multiple of 16, 16-byte aligned) at p with 0xFF, and zero the
+// 256-byte header at hdr.  A kernel, not hipMemsetAsync, so that a caller may
+// capture the call in a HIP graph.
+hipError_t ws_init_launch(void* hdr, void* p, size_t bytes, hipStream_t s);
+
+// Episode index of every step (begin steps at or before t, minus one).
+constexpr int kEpBlock = 4096;   // steps per workgroup
+hipError_t episode_idx_launch(const uint8_t* start, int32_t* idx, int64_t B, int64_t T,
+                              int32_t* counts, hipStream_t s);
+
+// Linear-attention memoroid: per-(chunk, head) state summaries, and outputs
+// from the scanned chunk states.  A state is S^T (64x64, row n holds column n
+// of S) followed by z (64), kLinStateWords floats.
+constexpr int kLinChunk = 64;
+constexpr int kLinStateWords = 64 * 64 + 64;
+hipError_t linattn_summary_launch(const float* k, const float* v, const uint8_t* start, float* dS,
+                                  uint8_t* R, int64_t T, int64_t H, hipStream_t s);
+hipError_t linattn_output_launch(const float* q, const float* k, const float* v, const uint8_t* start,
+                                 const float* Sinc, float* out, int64_t T, int64_t H, hipStream_t s);
+hipError_t fill_f32_launch(float* p, int64_t n, float value, hipStream_t s);
+
+}  // namespace memoroid

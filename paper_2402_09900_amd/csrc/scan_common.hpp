@@ -1,0 +1,265 @@
+// scan_common.hpp -- device helpers shared by the scan kernels (gfx950).
+//
+//  * element kinds (f32, bf16, complex64) with exact decode / RNE encode;
+//  * register-resident raw vectors loaded and stored with one wide access;
+//  * the state algebra of the diagonal memoroid under the reset transform;
+//  * self-validating cross-tile descriptor words for the single-pass scan.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace memoroid {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+enum Kind { K_F32 = 0, K_BF16 = 1, K_C64 = 2 };
+
+template <Kind K> struct KindInfo;
+template <> struct KindInfo<K_F32> { static constexpr int bytes = 4; static constexpr int vec = 4; };
+template <> struct KindInfo<K_BF16> { static constexpr int bytes = 2; static constexpr int vec = 8; };
+template <> struct KindInfo<K_C64> { static constexpr int bytes = 8; static constexpr int vec = 2; };
+
+// ------------------------------------------------------------ complex float
+
+struct cf {
+    float re, im;
+};
+
+__device__ __forceinline__ cf operator*(cf a, cf b) {
+    return cf{a.re * b.re - a.im * b.im, a.re * b.im + a.im * b.re};
+}
+__device__ __forceinline__ cf operator+(cf a, cf b) { return cf{a.re + b.re, a.im + b.im}; }
+__device__ __forceinline__ cf conj(cf a) { return cf{a.re, -a.im}; }
+__device__ __forceinline__ float conj(float a) { return a; }
+
+// a * b + c, fused per component where the arithmetic allows
+__device__ __forceinline__ float mad(float a, float b, float c) { return __builtin_fmaf(a, b, c); }
+__device__ __forceinline__ cf mad(cf a, cf b, cf c) {
+    return cf{__builtin_fmaf(a.re, b.re, __builtin_fmaf(-a.im, b.im, c.re)),
+              __builtin_fmaf(a.re, b.im, __builtin_fmaf(a.im, b.re, c.im))};
+}
+
+template <class S> __device__ __forceinline__ S s_one();
+template <> __device__ __forceinline__ float s_one<float>() { return 1.0f; }
+template <> __device__ __forceinline__ cf s_one<cf>() { return cf{1.0f, 0.0f}; }
+template <class S> __device__ __forceinline__ S s_zero();
+template <> __device__ __forceinline__ float s_zero<float>() { return 0.0f; }
+template <> __device__ __forceinline__ cf s_zero<cf>() { return cf{0.0f, 0.0f}; }
+
+template <Kind K> struct StateOf { using type = float; };
+template <> struct StateOf<K_C64> { using type = cf; };
+
+// ---------------------------------------------------------------- bf16 codec
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// float -> bf16 bits, round to nearest even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x0040u;
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+// -------------------------------------------------------------- raw vectors
+// RawVec<K, VEC> holds VEC elements of kind K in their storage format, in
+// ceil(VEC*bytes/4) 32-bit registers, and moves with a single global access.
+
+template <Kind K, int VEC> struct RawVec {
+    static constexpr int BYTES = VEC * KindInfo<K>::bytes;
+    static constexpr int WORDS = BYTES >= 4 ? BYTES / 4 : 1;
+    uint32_t w[WORDS];
+};
+
+template <int BYTES> struct WideAccess;
+
+template <> struct WideAccess<2> {
+    template <int W> __device__ static void load(uint32_t (&w)[W], const void* p) {
+        w[0] = *(const uint16_t*)p;
+    }
+    template <int W> __device__ static void store_nt(void* p, const uint32_t (&w)[W]) {
+        __builtin_nontemporal_store((uint16_t)w[0], (uint16_t*)p);
+    }
+};
+template <> struct WideAccess<4> {
+    template <int W> __device__ static void load(uint32_t (&w)[W], const void* p) {
+        w[0] = *(const uint32_t*)p;
+    }
+    template <int W> __device__ static void store_nt(void* p, const uint32_t (&w)[W]) {
+        __builtin_nontemporal_store(w[0], (uint32_t*)p);
+    }
+};
+template <> struct WideAccess<8> {
+    template <int W> __device__ static void load(uint32_t (&w)[W], const void* p) {
+        u32x2 v = *(const u32x2*)p;
+        w[0] = v.x; w[1] = v.y;
+    }
+    template <int W> __device__ static void store_nt(void* p, const uint32_t (&w)[W]) {
+        u32x2 v = {w[0], w[1]};
+        __builtin_nontemporal_store(v, (u32x2*)p);
+    }
+};
+template <> struct WideAccess<16> {
+    template <int W> __device__ static void load(uint32_t (&w)[W], const void* p) {
+        u32x4 v = *(const u32x4*)p;
+        w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+    }
+    template <int W> __device__ static void store_nt(void* p, const uint32_t (&w)[W]) {
+        u32x4 v = {w[0], w[1], w[2], w[3]};
+        __builtin_nontemporal_store(v, (u32x4*)p);
+    }
+};
+template <> struct WideAccess<32> {
+    template <int W> __device__ static void load(uint32_t (&w)[W], const void* p) {
+        u32x4 v0 = ((const u32x4*)p)[0];
+        u32x4 v1 = ((const u32x4*)p)[1];
+        w[0] = v0.x; w[1] = v0.y; w[2] = v0.z; w[3] = v0.w;
+        w[4] = v1.x; w[5] = v1.y; w[6] = v1.z; w[7] = v1.w;
+    }
+    template <int W> __device__ static void store_nt(void* p, const uint32_t (&w)[W]) {
+        u32x4 v0 = {w[0], w[1], w[2], w[3]};
+        u32x4 v1 = {w[4], w[5], w[6], w[7]};
+        __builtin_nontemporal_store(v0, (u32x4*)p);
+        __builtin_nontemporal_store(v1, (u32x4*)p + 1);
+    }
+};
+
+template <Kind K, int VEC>
+__device__ __forceinline__ void raw_load(RawVec<K, VEC>& r, const void* p) {
+    WideAccess<RawVec<K, VEC>::BYTES>::load(r.w, p);
+}
+
+template <Kind K, int VEC>
+__device__ __forceinline__ void raw_store_nt(void* p, const RawVec<K, VEC>& r) {
+    WideAccess<RawVec<K, VEC>::BYTES>::store_nt(p, r.w);
+}
+
+// decode element i of a raw vector into its state type
+template <Kind K, int VEC> struct Codec;
+
+template <int VEC> struct Codec<K_F32, VEC> {
+    __device__ static float get(const RawVec<K_F32, VEC>& r, int i) { return __uint_as_float(r.w[i]); }
+    __device__ static void put(RawVec<K_F32, VEC>& r, int i, float v) { r.w[i] = __float_as_uint(v); }
+};
+template <int VEC> struct Codec<K_BF16, VEC> {
+    __device__ static float get(const RawVec<K_BF16, VEC>& r, int i) {
+        return (i & 1) ? bf16_hi(r.w[i >> 1]) : bf16_lo(r.w[i >> 1]);
+    }
+    __device__ static void put(RawVec<K_BF16, VEC>& r, int i, float v) {
+        const uint32_t b = f32_to_bf16(v);
+        if (i & 1) r.w[i >> 1] = (r.w[i >> 1] & 0x0000FFFFu) | (b << 16);
+        else r.w[i >> 1] = (r.w[i >> 1] & 0xFFFF0000u) | b;
+    }
+};
+template <int VEC> struct Codec<K_C64, VEC> {
+    __device__ static cf get(const RawVec<K_C64, VEC>& r, int i) {
+        return cf{__uint_as_float(r.w[2 * i]), __uint_as_float(r.w[2 * i + 1])};
+    }
+    __device__ static void put(RawVec<K_C64, VEC>& r, int i, cf v) {
+        r.w[2 * i] = __float_as_uint(v.re);
+        r.w[2 * i + 1] = __float_as_uint(v.im);
+    }
+};
+
+// ------------------------------------------------------- descriptor words
+// Cross-tile communication of the single-pass scan.  Every word is written
+// once per call with a relaxed agent-scope atomic store and read with relaxed
+// agent-scope atomic loads, and validates itself: the workspace is filled with
+// all-ones bytes before the scan, and a published value never has that bit
+// pattern because every float is canonicalised (any NaN becomes 0x7FC00000)
+// before it is stored.  No fence is needed: a reader that sees a valid word
+// sees the whole value, and no other memory is ordered against it.
+
+constexpr uint32_t kEmpty32 = 0xFFFFFFFFu;
+constexpr uint64_t kEmpty64 = 0xFFFFFFFFFFFFFFFFull;
+
+__device__ __forceinline__ float canon(float v) { return v != v ? __uint_as_float(0x7FC00000u) : v; }
+
+__device__ __forceinline__ uint64_t pack2(float lo, float hi) {
+    return (uint64_t)__float_as_uint(canon(lo)) | ((uint64_t)__float_as_uint(canon(hi)) << 32);
+}
+__device__ __forceinline__ float unpack_lo(uint64_t w) { return __uint_as_float((uint32_t)w); }
+__device__ __forceinline__ float unpack_hi(uint64_t w) { return __uint_as_float((uint32_t)(w >> 32)); }
+
+__device__ __forceinline__ void publish64(uint64_t* p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t peek64(const uint64_t* p) {
+    return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void publish32(uint32_t* p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t peek32(const uint32_t* p) {
+    return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Per-feature tile summary of the scan state, in the two forms a successor
+// can use.  AGG: (A, H) of a tile without a begin step, i.e. h_end =
+// A * h_before + H.  INCL: h_end itself (the tile's inclusive prefix).
+//   real:    AGG = one 64-bit word (A, H);      INCL = one 32-bit word H
+//   complex: AGG = two 64-bit words A, H;       INCL = one 64-bit word H
+template <class S> struct Desc;
+
+template <> struct Desc<float> {
+    static constexpr int agg_bytes = 8;
+    static constexpr int incl_bytes = 4;
+    __device__ static void put_agg(void* base, int64_t i, float A, float H) {
+        publish64((uint64_t*)base + i, pack2(A, H));
+    }
+    __device__ static void put_incl(void* base, int64_t i, float H) {
+        publish32((uint32_t*)base + i, __float_as_uint(canon(H)));
+    }
+    __device__ static bool get_agg(const void* base, int64_t i, float& A, float& H) {
+        const uint64_t w = peek64((const uint64_t*)base + i);
+        A = unpack_lo(w);
+        H = unpack_hi(w);
+        return w != kEmpty64;
+    }
+    __device__ static bool get_incl(const void* base, int64_t i, float& H) {
+        const uint32_t w = peek32((const uint32_t*)base + i);
+        H = __uint_as_float(w);
+        return w != kEmpty32;
+    }
+};
+
+template <> struct Desc<cf> {
+    static constexpr int agg_bytes = 16;
+    static constexpr int incl_bytes = 8;
+    __device__ static void put_agg(void* base, int64_t i, cf A, cf H) {
+        publish64((uint64_t*)base + 2 * i, pack2(A.re, A.im));
+        publish64((uint64_t*)base + 2 * i + 1, pack2(H.re, H.im));
+    }
+    __device__ static void put_incl(void* base, int64_t i, cf H) {
+        publish64((uint64_t*)base + i, pack2(H.re, H.im));
+    }
+    __device__ static bool get_agg(const void* base, int64_t i, cf& A, cf& H) {
+        const uint64_t wa = peek64((const uint64_t*)base + 2 * i);
+        const uint64_t wh = peek64((const uint64_t*)base + 2 * i + 1);
+        A = cf{unpack_lo(wa), unpack_hi(wa)};
+        H = cf{unpack_lo(wh), unpack_hi(wh)};
+        return wa != kEmpty64 && wh != kEmpty64;
+    }
+    __device__ static bool get_incl(const void* base, int64_t i, cf& H) {
+        const uint64_t w = peek64((const uint64_t*)base + i);
+        H = cf{unpack_lo(w), unpack_hi(w)};
+        return w != kEmpty64;
+    }
+};
+
+// Bound on polls of one predecessor descriptor before a wait gives up and
+// flags MEMOROID_ETIMEOUT in the workspace (about a second of polling).  The
+// ticketed tile order guarantees every awaited tile is running or done, so
+// the bound only matters if that guarantee were broken.
+constexpr uint32_t kMaxPolls = 1u << 22;
+
+// Workspace header shared by the scan kernels (first 256 bytes).
+struct WsHeader {
+    uint32_t ticket;     // next tile ticket
+    uint32_t timeout;    // nonzero: some wait gave up
+    uint32_t pad[62];
+};
+
+}  // namespace memoroid

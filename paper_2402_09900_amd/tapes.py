@@ -280,3 +280,30 @@ def make_linattn(key: int = 3, seed: Optional[int] = None, T: Optional[int] = No
 
 def flags_sha256(start: np.ndarray) -> str:
     return hashlib.sha256(np.ascontiguousarray(start, dtype=np.uint8).tobytes()).hexdigest()
+
+
+def make_custom_diag(dtype: str, B: int, T: int, d: int, a_invariant: bool, seed: int,
+                     a_range=(0.5, 0.99), mean_episode: float = 50.0, with_grad: bool = True,
+                     out_dtype: Optional[str] = None) -> DiagTape:
+    """A diagonal tape of any shape and dtype for edge-case tests: Geometric
+    episode lengths of the given mean, |a| ~ U(a_range) (uniform phase for
+    complex), x and g standard normal."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    start = np.stack([_geometric(mean_episode)(rng, T) for _ in range(B)]) if T > 0 else np.zeros((B, 0), np.uint8)
+    start = start.reshape(B, T).astype(np.uint8)
+    shape_a = (d,) if a_invariant else (B, T, d)
+    lo, hi = a_range
+    if dtype == "c64":
+        mag = _uniform_f32(rng, lo, hi, shape_a).astype(np.float64)
+        a = (mag * np.exp(2j * math.pi * rng.random(shape_a))).astype(np.complex64)
+        x = _cnormal_c64(rng, (B, T, d))
+        g = _cnormal_c64(rng, (B, T, d)) if with_grad else None
+    else:
+        a = _uniform_f32(rng, lo, hi, shape_a)
+        x = _normal_f32(rng, (B, T, d))
+        g = _normal_f32(rng, (B, T, d)) if with_grad else None
+        if dtype == "bf16":
+            a, x = f32_to_bf16_bits(a), f32_to_bf16_bits(x)
+            g = None
+    return DiagTape(a=a, x=x, start=start, g=g, dtype=dtype, out_dtype=out_dtype or dtype,
+                    B=B, T=T, d=d, a_invariant=a_invariant)

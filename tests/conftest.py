@@ -23,3 +23,22 @@ def read_golden(name):
             key, _, val = line.partition(":")
             out.setdefault(key.strip(), []).append(val.split())
     return out
+
+
+def cond_err(y, ref, mag):
+    """Largest error of y against the fp64 reference, relative to
+    max(|ref|, magnitude companion): the rounding error any order of the
+    sums can make scales with the companion, so this is the plain relative
+    error wherever the sums do not cancel."""
+    import numpy as np
+    y = np.asarray(y)
+    ref = np.asarray(ref)
+    den = np.maximum(np.abs(ref), np.asarray(mag))
+    den = np.where(den > 0, den, 1.0)
+    err = np.abs(y.astype(ref.dtype) - ref) / den
+    return float(err.max()) if err.size else 0.0
+
+
+def announce(msg):
+    """Name the case before a GPU step (a fault ends the process)."""
+    print("\n[case] " + msg, flush=True)

@@ -1,0 +1,131 @@
+"""The C ABI on the CPU: the library loads, exports every declared symbol and
+rejects bad arguments before touching the GPU.  No kernel is launched here:
+every call below fails validation or is an empty problem."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from conftest import ROOT
+from paper_2402_09900_amd import binding as mb
+
+HEADER = os.path.join(ROOT, "include", "memoroid.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(memoroid_\w+)\s*\(", src)))
+
+
+def test_header_compiles_as_c_and_cxx(tmp_path):
+    for lang, comp in (("c", "gcc"), ("c++", "g++")):
+        subprocess.run([comp, "-x", lang, "-fsyntax-only", "-Wall", "-Werror", HEADER], check=True)
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert "memoroid_scan_diag" in names and "memoroid_scan_linattn" in names
+    lib = ctypes.CDLL(mb.LIB_PATH)
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+    for n in names:
+        assert hasattr(mb, n), "binding lacks " + n
+
+
+def test_version_and_status_strings():
+    assert mb.memoroid_abi_version() == 1
+    for s in (mb.OK, mb.EINVAL, mb.EUNSUPPORTED, mb.EWORKSPACE, mb.EHIP, mb.ETIMEOUT):
+        assert mb.status_string(s) and mb.status_string(s) != "unknown status"
+    assert mb.status_string(12345) == "unknown status"
+
+
+def test_workspace_queries():
+    f = mb.memoroid_scan_diag_workspace_bytes
+    assert f(1, 1 << 20, 256, mb.F32, mb.F32) > 0
+    assert f(64, 16384, 512, mb.BF16, mb.BF16) > 0
+    assert f(1, 65536, 256, mb.C64, mb.C64) > 0
+    assert f(1, 100, 8, mb.F32, mb.BF16) == 0          # unsupported pair
+    assert f(1, 100, 8, mb.C64, mb.F32) == 0
+    assert f(-1, 100, 8, mb.F32, mb.F32) == 0
+    assert f(0, 100, 8, mb.F32, mb.F32) == 0            # empty problem needs nothing
+    g = mb.memoroid_scan_diag_bwd_workspace_bytes
+    assert g(1, 65536, 256, mb.C64, 0) > g(1, 65536, 256, mb.C64, 256) > 0   # da partials
+    assert g(1, 100, 8, mb.BF16, 8) == 0
+    h = mb.memoroid_scan_linattn_workspace_bytes
+    assert h(32768, 4, 64, 64, 64) > 0
+    assert h(32768, 4, 32, 64, 64) == 0
+    # descriptor storage grows linearly in T
+    assert f(1, 1 << 21, 256, mb.F32, mb.F32) < 2.2 * f(1, 1 << 20, 256, mb.F32, mb.F32)
+
+
+# fake, well-aligned device addresses: validation must reject the call before
+# any of them is dereferenced or any HIP call is made
+A, X, S, H, W, I = 0x10000, 0x20000, 0x30000, 0x40000, 0x50000, 0x60000
+
+
+def diag(**kw):
+    args = dict(a=A, a_stride_t=8, x=X, start=S, h=H, episode_idx=None, B=2, T=100, d=8,
+                in_dtype=mb.F32, out_dtype=mb.F32, workspace=W, workspace_bytes=1 << 30, stream=None)
+    args.update(kw)
+    return mb.memoroid_scan_diag(*args.values())
+
+
+def test_diag_validation():
+    assert diag(B=-1) == mb.EINVAL
+    assert diag(T=-5) == mb.EINVAL
+    assert diag(B=0) == mb.OK and diag(T=0) == mb.OK and diag(d=0) == mb.OK
+    assert diag(in_dtype=mb.F32, out_dtype=mb.BF16) == mb.EUNSUPPORTED
+    assert diag(in_dtype=7) == mb.EUNSUPPORTED
+    assert diag(x=None) == mb.EINVAL
+    assert diag(a=None) == mb.EINVAL
+    assert diag(start=None) == mb.EINVAL
+    assert diag(h=None) == mb.EINVAL
+    assert diag(a_stride_t=3) == mb.EINVAL
+    assert diag(x=X + 2) == mb.EINVAL                   # misaligned f32
+    assert diag(h=X) == mb.EINVAL                       # output aliases input
+    assert diag(episode_idx=H) == mb.EINVAL
+    assert diag(workspace=None) == mb.EWORKSPACE
+    need = mb.memoroid_scan_diag_workspace_bytes(2, 100, 8, mb.F32, mb.F32)
+    assert diag(workspace_bytes=need - 1) == mb.EWORKSPACE
+    assert diag(B=1 << 40, T=1 << 40) == mb.EINVAL      # extent overflow
+    assert diag(in_dtype=mb.C64, out_dtype=mb.C64, x=X + 4) == mb.EINVAL
+
+
+def test_diag_bwd_validation():
+    def bwd(**kw):
+        args = dict(a=A, a_stride_t=8, start=S, h=H, grad_h=X, grad_x=I, grad_a=W + 0x1000, B=1, T=50,
+                    d=8, dtype=mb.F32, workspace=W, workspace_bytes=1 << 30, stream=None)
+        args.update(kw)
+        return mb.memoroid_scan_diag_bwd(*args.values())
+    assert bwd(dtype=mb.BF16) == mb.EUNSUPPORTED
+    assert bwd(T=0) == mb.OK
+    assert bwd(grad_x=X) == mb.EINVAL                   # aliases grad_h
+    assert bwd(h=None) == mb.EINVAL                     # grad_a needs h
+    assert bwd(a_stride_t=2) == mb.EINVAL
+    assert bwd(workspace=None) == mb.EWORKSPACE
+    assert bwd(workspace_bytes=16) == mb.EWORKSPACE
+
+
+def test_linattn_validation():
+    def la(**kw):
+        args = dict(q=A, k=X, v=S, start=H + 0x100, out=I, episode_idx=None, T=1000, H=4, dk=64, dv=64,
+                    chunk=64, workspace=W, workspace_bytes=1 << 30, stream=None)
+        args.update(kw)
+        return mb.memoroid_scan_linattn(*args.values())
+    assert la(dk=32) == mb.EUNSUPPORTED
+    assert la(chunk=128) == mb.EUNSUPPORTED
+    assert la(T=0) == mb.OK
+    assert la(out=A) == mb.EINVAL
+    assert la(q=A + 4) == mb.EINVAL
+    assert la(workspace=None) == mb.EWORKSPACE
+    assert la(workspace_bytes=1000) == mb.EWORKSPACE
+
+
+def test_torch_layer_rejects_cpu_tensors():
+    torch = pytest.importorskip("torch")
+    a = torch.rand(4, 8)
+    with pytest.raises(ValueError):
+        mb.scan_diag(a, torch.rand(4, 8), torch.zeros(4, dtype=torch.uint8))

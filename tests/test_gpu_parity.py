@@ -1,0 +1,337 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle.
+
+Every case draws seeded inputs from paper_2402_09900_amd.tapes, runs the
+library on the GPU and the oracle on the CPU on the same bytes, and compares
+element by element:
+  * floats: max over elements of |y - r| / max(|r|, m), with m the oracle's
+    magnitude companion, at most 1e-4 for fp32/complex64 arithmetic and 2e-2
+    for bf16 inputs (fp32 state);
+  * integers (episode indices): bit-exact.
+Full-size workloads run at their real shape in the launch configuration the
+benchmark times, and are compared on whole tapes / feature columns that the
+oracle computes independently (every tape and feature is its own scan).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from conftest import announce, cond_err
+from paper_2402_09900_amd import tapes
+
+torch = pytest.importorskip("torch")
+from paper_2402_09900_amd import binding as mb  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+TOL = {"f32": 1e-4, "c64": 1e-4, "bf16": 2e-2}
+
+
+def to_dev(arr, kind):
+    arr = np.ascontiguousarray(arr)
+    if kind == "bf16":
+        return torch.from_numpy(arr.view(np.int16)).view(torch.bfloat16).to(DEV)
+    return torch.from_numpy(arr).to(DEV)
+
+
+def from_dev(t):
+    if t.dtype == torch.bfloat16:
+        bits = t.view(torch.int16).cpu().numpy().view(np.uint16)
+        return tapes.bf16_bits_to_f32(bits).astype(np.float64)
+    return t.cpu().numpy()
+
+
+def run_fwd(w, out_kind=None, idx=False):
+    out_kind = out_kind or w.out_dtype
+    out_t = {"f32": torch.float32, "bf16": torch.bfloat16, "c64": torch.complex64}[out_kind]
+    a, x, s = to_dev(w.a, w.dtype), to_dev(w.x, w.dtype), to_dev(w.start, "u8")
+    ws = torch.empty(max(mb.memoroid_scan_diag_workspace_bytes(
+        w.B, w.T, w.d, {"f32": 0, "bf16": 1, "c64": 2}[w.dtype], {"f32": 0, "bf16": 1, "c64": 2}[out_kind]), 256),
+        dtype=torch.uint8, device=DEV)
+    res = mb.scan_diag(a, x, s, out_dtype=out_t, episode_idx=idx, workspace=ws)
+    assert mb.workspace_status(ws) == mb.OK
+    return res
+
+
+def dec(arr, kind):
+    """Exact float64 / complex128 decode of a stored input."""
+    if kind == "bf16":
+        return tapes.bf16_bits_to_f32(arr).astype(np.float64)
+    return arr.astype(np.complex128 if kind == "c64" else np.float64)
+
+
+def select(w, name, tapes_sel=None, cols=None):
+    """Decoded slice [tapes][:, cols] of a tape input (a time-invariant a is
+    [d] and only takes the column selection)."""
+    arr = getattr(w, name)
+    if name == "a" and w.a_invariant:
+        return dec(arr if cols is None else arr[cols], w.dtype)
+    if tapes_sel is not None:
+        arr = arr[tapes_sel]
+    if cols is not None:
+        arr = arr[:, :, cols]
+    return dec(arr, w.dtype)
+
+
+def check_fwd(w, out_kind=None, cols=None, tapes_sel=None, label=""):
+    announce("fwd %s B=%d T=%d d=%d %s inv=%s %s" % (label, w.B, w.T, w.d, w.dtype, w.a_invariant, out_kind))
+    h, idx = run_fwd(w, out_kind, idx=True)
+    np.testing.assert_array_equal(idx.cpu().numpy(), oracle.episode_idx(w.start))
+    if tapes_sel is not None:
+        h = h[tapes_sel]
+    if cols is not None:
+        h = h[:, :, cols]
+    h = from_dev(h.contiguous())
+    s = w.start if tapes_sel is None else w.start[tapes_sel]
+    ref, mag = oracle.diag_fwd(select(w, "a", tapes_sel, cols), select(w, "x", tapes_sel, cols), s)
+    err = cond_err(h, ref, mag)
+    tol = TOL[w.dtype if (out_kind or w.out_dtype) != "bf16" else "bf16"]
+    assert err <= tol, (label, err)
+    return err
+
+
+def check_bwd(w, cols=None, label=""):
+    announce("bwd %s B=%d T=%d d=%d %s inv=%s" % (label, w.B, w.T, w.d, w.dtype, w.a_invariant))
+    s = w.start
+    a_s, x_s, g_s = select(w, "a", None, cols), select(w, "x", None, cols), select(w, "g", None, cols)
+    h_ref, _ = oracle.diag_fwd(a_s, x_s, s)
+    # both sides consume the same h: the oracle's forward, stored in the
+    # tape's dtype
+    store = np.complex64 if w.dtype == "c64" else np.float32
+    if cols is None:
+        h_in = h_ref.astype(store)
+    else:
+        # sampled columns of a full-size tape: only the sampled columns are
+        # compared, so the others may hold any finite h
+        h_in = w.x.copy()
+        h_in[:, :, cols] = h_ref.astype(store)
+    ws = torch.empty(max(mb.memoroid_scan_diag_bwd_workspace_bytes(
+        w.B, w.T, w.d, 2 if w.dtype == "c64" else 0, 0 if w.a_invariant else w.d), 256),
+        dtype=torch.uint8, device=DEV)
+    gx, ga = mb.scan_diag_bwd(to_dev(w.a, w.dtype), to_dev(s, "u8"), to_dev(h_in, w.dtype),
+                              to_dev(w.g, w.dtype), workspace=ws)
+    assert mb.workspace_status(ws) == mb.OK
+    if cols is not None:
+        gx = gx[:, :, cols]
+        ga = ga if w.a_invariant else ga[:, :, cols]
+    gx, ga = from_dev(gx.contiguous()), from_dev(ga.contiguous())
+    h_used = dec(h_in if cols is None else h_in[:, :, cols], w.dtype)
+    dx, da, m_dx, m_da = oracle.diag_bwd(a_s, s, h_used, g_s)
+    assert not (w.a_invariant and cols is not None), "a time-invariant da sums every column"
+    e_dx = cond_err(gx, dx, m_dx)
+    e_da = cond_err(ga, da, m_da)
+    assert e_dx <= TOL[w.dtype], (label, "dx", e_dx)
+    assert e_da <= TOL[w.dtype], (label, "da", e_da)
+    return e_dx, e_da
+
+
+# ------------------------------------------------------- the five workloads
+
+
+def test_workload1_full():
+    w = tapes.make_diag(1)
+    check_fwd(w, label="workload1")
+
+
+@pytest.fixture(scope="module")
+def w2():
+    return tapes.make_diag(2)
+
+
+def test_workload2_full_fwd(w2):
+    check_fwd(w2, label="workload2")
+
+
+def test_workload2_full_bwd(w2):
+    check_bwd(w2, label="workload2")
+
+
+def test_workload2_reduced_ragged():
+    w = tapes.make_diag(2, T=4096 + 37, d=256, seed=102)
+    check_fwd(w, label="workload2-small")
+    check_bwd(w, label="workload2-small")
+
+
+def check_linattn(la, label):
+    announce("linattn %s T=%d H=%d" % (label, la.T, la.H))
+    q, k, v = (to_dev(t, "f32") for t in (la.q, la.k, la.v))
+    st = to_dev(la.start, "u8")
+    ws = torch.empty(mb.memoroid_scan_linattn_workspace_bytes(la.T, la.H, 64, 64, 64), dtype=torch.uint8,
+                     device=DEV)
+    out, idx = mb.scan_linattn(q, k, v, st, episode_idx=True, workspace=ws)
+    assert mb.workspace_status(ws) == mb.OK
+    ref, mag = oracle.linattn(la.q.astype(np.float64), la.k.astype(np.float64), la.v.astype(np.float64),
+                              la.start)
+    err = cond_err(out.cpu().numpy(), ref, mag)
+    np.testing.assert_array_equal(idx.cpu().numpy(), oracle.episode_idx(la.start))
+    assert err <= TOL["f32"], (label, err)
+    return err
+
+
+def test_workload3_reduced_ragged():
+    check_linattn(tapes.make_linattn(T=2048 + 13, seed=103), "workload3-small")
+
+
+def test_workload3_full():
+    check_linattn(tapes.make_linattn(), "workload3")
+
+
+def test_workload3_short_episodes():
+    la = tapes.make_linattn(T=777, seed=104)
+    la.start[:] = 0
+    la.start[::3] = 1
+    la.start[100:140] = 1       # single-step episodes
+    check_linattn(la, "workload3-short-episodes")
+
+
+@pytest.fixture(scope="module")
+def w4():
+    return tapes.make_diag(4)
+
+
+def test_workload4_full_sampled_tapes(w4):
+    check_fwd(w4, tapes_sel=[0, 17, 63], label="workload4")
+
+
+def test_workload4_reduced_both_outputs():
+    w = tapes.make_diag(4, B=3, T=3000, d=512, seed=104)
+    check_fwd(w, label="workload4-small")
+    check_fwd(w, out_kind="f32", label="workload4-small-f32out")
+
+
+@pytest.fixture(scope="module")
+def w5():
+    return tapes.make_diag(5)
+
+
+def test_workload5_full_fwd_sampled_columns(w5):
+    check_fwd(w5, cols=[0, 1, 77, 128, 200, 255], label="workload5")
+
+
+def test_workload5_full_bwd_sampled_columns(w5):
+    check_bwd(w5, cols=[0, 3, 64, 130, 254, 255], label="workload5")
+
+
+def test_workload5_reduced_ragged():
+    w = tapes.make_diag(5, T=20000 + 5, d=256, seed=105)
+    check_fwd(w, label="workload5-small")
+    check_bwd(w, label="workload5-small")
+
+
+# ------------------------------------------------------------------ edges
+
+SHAPES = [(1, 1, 1), (1, 2, 3), (2, 63, 4), (1, 64, 32), (3, 65, 33), (1, 129, 256), (2, 1000, 260),
+          (1, 257, 512), (1, 5000, 8), (2, 300, 1024)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "c64"])
+@pytest.mark.parametrize("inv", [False, True])
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "B%dT%dd%d" % s)
+def test_edge_shapes(dtype, inv, shape):
+    B, T, d = shape
+    w = tapes.make_custom_diag(dtype, B, T, d, inv, seed=1000 + T + d, mean_episode=40.0)
+    check_fwd(w, label="edge")
+    if dtype != "bf16":
+        check_bwd(w, label="edge")
+
+
+@pytest.mark.parametrize("pattern", ["all_begins", "single_episode", "begin_at_end", "flag_bytes"])
+@pytest.mark.parametrize("dtype", ["f32", "c64"])
+def test_flag_patterns(pattern, dtype):
+    T = 20000 if pattern == "single_episode" else 3001
+    w = tapes.make_custom_diag(dtype, 2, T, 256, False, seed=7, a_range=(0.9, 0.9999))
+    if pattern == "all_begins":
+        w.start[:] = 1
+    elif pattern == "single_episode":
+        w.start[:] = 0
+    elif pattern == "begin_at_end":
+        w.start[:] = 0
+        w.start[:, -1] = 1
+    else:
+        rng = np.random.default_rng(3)
+        nz = w.start != 0
+        w.start[nz] = rng.integers(2, 256, size=int(nz.sum())).astype(np.uint8)
+        w.start[0, 0] = 0      # a zero byte at t = 0 still begins an episode
+    check_fwd(w, label=pattern)
+    check_bwd(w, label=pattern)
+
+
+def test_bf16_a_rounding_to_one():
+    """a drawn near 1 rounds to exactly 1.0 in bf16: no decay, a running sum."""
+    w = tapes.make_custom_diag("bf16", 1, 4000, 64, False, seed=8, a_range=(0.9985, 0.9999))
+    assert np.all(tapes.bf16_bits_to_f32(w.a) == 1.0)
+    check_fwd(w, out_kind="f32", label="bf16-a-one")
+
+
+def test_scalar_path_on_misaligned_rows():
+    """Base pointers off 16-byte alignment take the scalar kernels."""
+    w = tapes.make_custom_diag("f32", 1, 777, 64, False, seed=9)
+    B, T, d = w.B, w.T, w.d
+    buf_a = torch.zeros(B * T * d + 1, device=DEV)
+    buf_x = torch.zeros(B * T * d + 1, device=DEV)
+    buf_a[1:] = to_dev(w.a.reshape(-1), "f32")
+    buf_x[1:] = to_dev(w.x.reshape(-1), "f32")
+    a = buf_a[1:].view(B, T, d)
+    x = buf_x[1:].view(B, T, d)
+    h = mb.scan_diag(a, x, to_dev(w.start, "u8"))
+    ref, mag = oracle.diag_fwd(w.decoded("a"), w.decoded("x"), w.start)
+    assert cond_err(from_dev(h), ref, mag) <= 1e-4
+
+
+def test_nan_stays_in_its_episode():
+    w = tapes.make_custom_diag("f32", 1, 3000, 32, False, seed=10)
+    w.start[:] = 0
+    w.start[0, [0, 700, 1500, 2200]] = 1
+    w.x[0, 800, 3] = np.nan
+    w.a[0, 1600, 5] = np.inf
+    h = from_dev(run_fwd(w))
+    assert np.isnan(h[0, 800:1500, 3]).all()
+    assert np.isfinite(h[0, :800]).all() and np.isfinite(h[0, 1500:, 3]).all()
+    assert np.isfinite(h[0, 2200:]).all()
+    g = w.g.copy()
+    g[0, 1000, 7] = np.nan
+    gx, _ = mb.scan_diag_bwd(to_dev(w.a, "f32"), to_dev(w.start, "u8"), to_dev(np.ones_like(w.x), "f32"),
+                             to_dev(g, "f32"))
+    gx = from_dev(gx)
+    assert np.isnan(gx[0, 700:1001, 7]).all()
+    assert np.isfinite(gx[0, :700, 7]).all() and np.isfinite(gx[0, 1001:, 7]).all()
+
+
+def test_linattn_nan_stays_in_its_episode():
+    la = tapes.make_linattn(T=640, seed=11)
+    la.start[:] = 0
+    la.start[[0, 100, 130, 300]] = 1
+    la.v[120, 2, 5] = np.nan
+    q, k, v = (to_dev(t, "f32") for t in (la.q, la.k, la.v))
+    out = mb.scan_linattn(q, k, v, to_dev(la.start, "u8")).cpu().numpy()
+    assert np.isnan(out[120:130, 2, 5]).all()
+    assert np.isfinite(out[:120]).all() and np.isfinite(out[130:]).all()
+    assert np.isfinite(out[:, [0, 1, 3]]).all()
+
+
+def test_repeated_runs_agree():
+    w = tapes.make_diag(5, T=200000, d=256, seed=12)
+    ref, mag = oracle.diag_fwd(w.decoded("a"), w.decoded("x"), w.start)
+    for rep in range(4):
+        announce("repeat %d" % rep)
+        assert cond_err(from_dev(run_fwd(w)), ref, mag) <= 1e-4
+
+
+def test_autograd_function():
+    w = tapes.make_custom_diag("c64", 2, 1500, 64, True, seed=13)
+    a = to_dev(w.a, "c64").requires_grad_(True)
+    x = to_dev(w.x, "c64").requires_grad_(True)
+    h = mb.diag_scan(a, x, to_dev(w.start, "u8"))
+    h.backward(to_dev(w.g, "c64"))
+    h_ref, m_h = oracle.diag_fwd(w.decoded("a"), w.decoded("x"), w.start)
+    assert cond_err(from_dev(h.detach()), h_ref, m_h) <= 1e-4
+    dx, da, m_dx, _ = oracle.diag_bwd(w.decoded("a"), w.start, h_ref, w.decoded("g"))
+    assert cond_err(from_dev(x.grad), dx, m_dx) <= 1e-4
+    # da here uses the GPU's own h, whose error scales with the forward
+    # companion m_h: bound da's error by sum_t m_lam,t * m_h,t-1
+    nb = (w.start == 0)
+    nb[:, 0] = False
+    mh_prev = np.concatenate([np.zeros_like(m_h[:, :1]), m_h[:, :-1]], axis=1)
+    loose = (m_dx * mh_prev * nb[..., None]).sum(axis=(0, 1))
+    err = np.abs(from_dev(a.grad) - da) / np.maximum(np.abs(da), loose)
+    assert err.max() <= 1e-4
