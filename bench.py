@@ -102,7 +102,7 @@ def setup_diag(torch, mb, tapes, key):
         assert st == 0, mb.status_string(st)
     calls["fwd"] = fwd
     bytes_per["fwd"] = a_bytes + n * ebytes[kind] + n * ebytes[w.out_dtype] + B * T * (1 + 4)
-    if w.backward:
+    if w.g is not None:
         g = dev_tensor(torch, w.g, kind)
         hb = h if w.out_dtype == kind else h.to(tdt[kind])
         gx = torch.empty_like(g)

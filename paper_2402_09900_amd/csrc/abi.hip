@@ -13,10 +13,11 @@ using namespace memoroid;
 namespace {
 
 constexpr size_t kAlign = 256;
+constexpr int64_t kChainRowBytes = 128;
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 int elem_bytes(int dt) { return dt == MEMOROID_F32 ? 4 : dt == MEMOROID_BF16 ? 2 : 8; }
-int vec_width(int dt) { return dt == MEMOROID_F32 ? 4 : dt == MEMOROID_BF16 ? 8 : 2; }
+int vec_width(int dt) { return dt == MEMOROID_F32 ? 4 : dt == MEMOROID_BF16 ? 4 : 2; }
 int64_t next_pow2(int64_t v) {
     int64_t p = 1;
     while (p < v) p <<= 1;
@@ -51,7 +52,9 @@ bool plan_diag(int64_t B, int64_t T, int64_t d, int state_dtype, bool vec, int r
                bool ainv, bool want_grad_a, DiagPlan* p) {
     const int VEC = vec ? vec_width(state_dtype) : 1;
     const int64_t lanes = (d + VEC - 1) / VEC;
-    const int64_t Qp = lanes >= 64 ? 64 : next_pow2(lanes);
+    // a chain's row block is (at most) one 128-byte line of the feature row
+    const int64_t qp_cap = kChainRowBytes / (VEC * elem_bytes(state_dtype)) > 0 ? kChainRowBytes / (VEC * elem_bytes(state_dtype)) : 1;
+    const int64_t Qp = next_pow2(lanes) < qp_cap ? next_pow2(lanes) : qp_cap;
     p->VEC = VEC;
     p->Qp = (int)Qp;
     p->Dp = (int)(Qp * VEC);
@@ -105,12 +108,12 @@ int reduce_rows(const float* part, float* s1, float* s2, float* out, int64_t row
     float* bufs[2] = {s1, s2};
     int which = 0;
     while (rows > 64) {
-        if (colsum_launch(cur, bufs[which], rows, cols, 64, s) != hipSuccess) return MEMOROID_EHIP;
+        if (colsum_launch(cur, bufs[which], rows, cols, s) != hipSuccess) return MEMOROID_EHIP;
         cur = bufs[which];
         which ^= 1;
         rows = (rows + 63) / 64;
     }
-    return check_hip(colsum_launch(cur, out, rows, cols, rows > 0 ? rows : 1, s));
+    return check_hip(colsum_launch(cur, out, rows, cols, s));
 }
 
 }  // namespace
@@ -141,7 +144,7 @@ size_t memoroid_scan_diag_workspace_bytes(int64_t B, int64_t T, int64_t d, int i
     size_t best = 0;
     for (int vec = 0; vec < 2; ++vec) {
         DiagPlan& p = vec ? pv : ps;
-        if (!plan_diag(B, T, d, sd, vec, kFwdRows, false, false, false, &p)) return 0;
+        if (!plan_diag(B, T, d, sd, vec, diag_rows(false, false), false, false, false, &p)) return 0;
         if (p.total > best) best = p.total;
     }
     return best;
@@ -169,7 +172,7 @@ int memoroid_scan_diag(const void* a, int64_t a_stride_t, const void* x, const u
     const bool vec = d % VW == 0 && aligned(x, 16) && aligned(h, 16) && aligned(a, 16);
     const int sd = in_dtype == MEMOROID_C64 ? MEMOROID_C64 : (in_dtype == MEMOROID_BF16 ? MEMOROID_BF16 : MEMOROID_F32);
     DiagPlan p;
-    if (!plan_diag(B, T, d, sd, vec, kFwdRows, false, ainv, false, &p)) return MEMOROID_EUNSUPPORTED;
+    if (!plan_diag(B, T, d, sd, vec, diag_rows(false, ainv), false, ainv, false, &p)) return MEMOROID_EUNSUPPORTED;
     if (!workspace) return MEMOROID_EWORKSPACE;
     if (workspace_bytes < memoroid_scan_diag_workspace_bytes(B, T, d, in_dtype, out_dtype) ||
         workspace_bytes < p.total)
@@ -210,7 +213,7 @@ size_t memoroid_scan_diag_bwd_workspace_bytes(int64_t B, int64_t T, int64_t d, i
     size_t best = 0;
     for (int vec = 0; vec < 2; ++vec) {
         DiagPlan p;
-        if (!plan_diag(B, T, d, dtype, vec, kBwdRows, true, a_stride_t == 0, true, &p)) return 0;
+        if (!plan_diag(B, T, d, dtype, vec, diag_rows(true, a_stride_t == 0), true, a_stride_t == 0, true, &p)) return 0;
         if (p.total > best) best = p.total;
     }
     return best;
@@ -238,7 +241,7 @@ int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t, const uint8_t* sta
     const bool vec = d % VW == 0 && aligned(a, 16) && aligned(grad_h, 16) && aligned(grad_x, 16) &&
                      (!h || aligned(h, 16)) && (!grad_a || aligned(grad_a, 16));
     DiagPlan p;
-    if (!plan_diag(B, T, d, dtype, vec, kBwdRows, true, ainv, grad_a != nullptr, &p)) return MEMOROID_EUNSUPPORTED;
+    if (!plan_diag(B, T, d, dtype, vec, diag_rows(true, ainv), true, ainv, grad_a != nullptr, &p)) return MEMOROID_EUNSUPPORTED;
     if (!workspace) return MEMOROID_EWORKSPACE;
     if (workspace_bytes < memoroid_scan_diag_bwd_workspace_bytes(B, T, d, dtype, a_stride_t) ||
         workspace_bytes < p.total)
@@ -300,7 +303,7 @@ bool plan_linattn(int64_t T, int64_t H, LinPlan* p) {
     p->off_scan = off;
     // the state scan always runs vectorised: dstate % 4 == 0 and every
     // buffer is 256-byte aligned inside the workspace
-    if (!plan_diag(1, p->nch, p->dstate, MEMOROID_F32, true, kFwdRows, false, true, false, &p->scan)) return false;
+    if (!plan_diag(1, p->nch, p->dstate, MEMOROID_F32, true, diag_rows(false, true), false, true, false, &p->scan)) return false;
     off = align_up(off + p->scan.total);
     p->off_dS = off;
     off = align_up(off + states);

@@ -7,13 +7,14 @@
 //     lam_t = conj(a_{t+1}) * lam_{t+1} + g_t    otherwise,
 // where an episode end is the last step of the tape or a step followed by a
 // begin step; then dx_t = lam_t and da_t = [t not a begin] lam_t conj(h_{t-1}).
-// This is the forward scan's machinery mirrored in time: the same tiles, but
-// handed out from the end of the tape, each step's coefficient taken from the
-// step after it, and episode ends acting as resets.
+// This is the forward scan's machinery (diag_fwd.hip) mirrored in time: the
+// same tiles, handed out from the end of the tape, each step's coefficient
+// taken from the step after it, and episode ends acting as resets.
 //
 // For a time-invariant a, da is the sum over all tapes and steps; each tile
-// writes one deterministic partial per feature and colsum kernels (below) add
-// them up in a fixed order.
+// writes one partial per feature, summed inside the tile in a fixed order, and
+// colsum kernels (below) add the partials up in a fixed order too, so the
+// result does not depend on timing.
 #include "scan_common.hpp"
 #include "kernels.hpp"
 
@@ -23,14 +24,17 @@ template <Kind K, int VEC, int R, bool AINV>
 __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     using S = typename StateOf<K>::type;
     using C = Codec<K, VEC>;
+    using SegT = Seg<S, VEC>;
     constexpr int NT = 256;
+    constexpr int NW = NT / 64;
     constexpr int EB = KindInfo<K>::bytes;
 
     __shared__ uint32_t s_ticket;
-    __shared__ S sA[NT * VEC];
-    __shared__ S sH[NT * VEC];
-    __shared__ uint8_t sF[NT];
+    __shared__ S sWA[NW][64 * VEC];
+    __shared__ S sWH[NW][64 * VEC];
+    __shared__ uint32_t sWF[NW];
     __shared__ S sCarry[64 * VEC];
+    __shared__ LookbackLds<S, VEC> sLb;
 
     const int tid = threadIdx.x;
     if (tid == 0) s_ticket = atomicAdd(&p.hdr->ticket, 1u);
@@ -42,38 +46,58 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     const int b = chain / p.nfb;
     const int fb = chain - b * p.nfb;
     const int Qp = p.Qp;
-    const int G = NT / Qp;
-    const int q = tid & (Qp - 1);
-    const int g = tid / Qp;
+    const int Gw = 64 / Qp;
+    const int wave = tid >> 6;
+    const int lane = tid & 63;
+    const int q = lane & (Qp - 1);
+    const int j = lane / Qp;
     const int Dp = Qp * VEC;
-    const int64_t L = (int64_t)G * R;
+    const int64_t L = (int64_t)NW * Gw * R;
     const int64_t tile_row0 = tile * L;
-    const int64_t row0 = tile_row0 + (int64_t)g * R;
+    const int64_t row0 = tile_row0 + (int64_t)(wave * Gw + j) * R;
     const int64_t f0 = (int64_t)fb * Dp + (int64_t)q * VEC;
     const bool active = f0 < p.d;
     const uint8_t* st = p.start + (int64_t)b * p.T;
     const int64_t T = p.T;
     const int64_t rowbase = (int64_t)b * T;
+    const bool want_da = AINV ? p.da_part != nullptr : p.da != nullptr;
 
-    // ---- loads: g_t, a_{t+1}, and the flags of steps t and t+1
+    // ---- loads.  The begin flags of the lane's steps t and t+1 (and of the
+    // step after the tile) first, by unconditional byte loads at clamped
+    // addresses, so that waiting for them leaves every data load in flight;
+    // then g_t, a_{t+1} and h_{t-1} of every step, one wide access each.
+    uint32_t fl[R + 1];
+#pragma unroll
+    for (int r = 0; r <= R; ++r) {
+        const int64_t t = row0 + r < T ? row0 + r : T - 1;
+        fl[r] = st[t];
+    }
+    const int64_t t_last = (tile_row0 + L < T ? tile_row0 + L : T) - 1;
+    const uint32_t fl_after = st[t_last + 1 < T ? t_last + 1 : T - 1];
+    __builtin_amdgcn_sched_barrier(0);
     RawVec<K, VEC> rg[R];
     RawVec<K, VEC> ra[AINV ? 1 : R];
+    RawVec<K, VEC> rh[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int64_t t = row0 + r;
+        if (active && t < T) {
+            raw_load(rg[r], (const char*)p.g + ((rowbase + t) * p.d + f0) * EB);
+            if constexpr (!AINV) {
+                if (t + 1 < T) raw_load(ra[r], (const char*)p.a + ((rowbase + t + 1) * p.d + f0) * EB);
+            }
+            if (want_da && t > 0) raw_load(rh[r], (const char*)p.h + ((rowbase + t - 1) * p.d + f0) * EB);
+        }
+    }
+    __builtin_amdgcn_sched_barrier(0);
     uint32_t ends = 0, begins = 0, valid = 0;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         const int64_t t = row0 + r;
-        if (t < T) {
-            valid |= 1u << r;
-            if (t == 0 || st[t] != 0) begins |= 1u << r;
-            const bool end = (t + 1 == T) || st[t + 1] != 0;
-            if (end) ends |= 1u << r;
-            if (active) {
-                raw_load(rg[r], (const char*)p.g + ((rowbase + t) * p.d + f0) * EB);
-                if constexpr (!AINV) {
-                    if (!end) raw_load(ra[r], (const char*)p.a + ((rowbase + t + 1) * p.d + f0) * EB);
-                }
-            }
-        }
+        const uint32_t in = t < T ? 1u : 0u;
+        valid |= in << r;
+        begins |= (in & ((t == 0 ? 1u : 0u) | (fl[r] != 0u ? 1u : 0u))) << r;
+        ends |= (in & ((t + 1 == T ? 1u : 0u) | (fl[r + 1] != 0u ? 1u : 0u))) << r;
     }
     S ainv[VEC];
     if constexpr (AINV) {
@@ -88,9 +112,7 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     };
 
     // ---- per-lane summary, walking its R steps backwards
-    S A[VEC], H[VEC];
-#pragma unroll
-    for (int v = 0; v < VEC; ++v) { A[v] = s_one<S>(); H[v] = s_zero<S>(); }
+    SegT own = seg_identity<S, VEC>();
 #pragma unroll
     for (int r = R - 1; r >= 0; --r) {
         if (!((valid >> r) & 1u)) continue;
@@ -99,170 +121,128 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
         for (int v = 0; v < VEC; ++v) {
             const S gv = C::get(rg[r], v);
             if (e) {
-                A[v] = s_one<S>();
-                H[v] = gv;
+                own.A[v] = s_one<S>();
+                own.H[v] = gv;
             } else {
                 const S cv = coef(r, v);
-                H[v] = mad(cv, H[v], gv);
-                A[v] = A[v] * cv;
+                own.H[v] = mad(cv, own.H[v], gv);
+                own.A[v] = own.A[v] * cv;
             }
         }
     }
-    const bool f_own = ends != 0;
+    own.f = ends != 0;
 
-    // ---- combine groups (later groups come first in scan order)
+    // ---- scan the wavefront's groups (later groups first), then combine the
+    // wavefront totals (later wavefronts first) through LDS
+    SegT inc = own, exc;
+    wave_group_scan<S, VEC, true>(inc, exc, Qp);
+    if (j == 0) {
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) {
-        sA[tid * VEC + v] = A[v];
-        sH[tid * VEC + v] = H[v];
+        for (int v = 0; v < VEC; ++v) {
+            sWA[wave][q * VEC + v] = inc.A[v];
+            sWH[wave][q * VEC + v] = inc.H[v];
+        }
+        if (q == 0) sWF[wave] = inc.f;
     }
-    sF[tid] = f_own;
     __syncthreads();
-
-    S eA[VEC], eH[VEC];
-    bool ef = false;
-#pragma unroll
-    for (int v = 0; v < VEC; ++v) { eA[v] = s_one<S>(); eH[v] = s_zero<S>(); }
-    for (int gg = G - 1; gg > g; --gg) {
-        const int j = gg * Qp + q;
-        const bool fj = sF[j];
+    auto wave_total = [&](int w) -> SegT {
+        SegT t;
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {
-            const S Aj = sA[j * VEC + v], Hj = sH[j * VEC + v];
-            if (fj) {
-                eA[v] = Aj;
-                eH[v] = Hj;
-            } else {
-                eH[v] = mad(Aj, eH[v], Hj);
-                eA[v] = Aj * eA[v];
-            }
+            t.A[v] = sWA[w][q * VEC + v];
+            t.H[v] = sWH[w][q * VEC + v];
         }
-        ef = ef || fj;
-    }
+        t.f = sWF[w] != 0;
+        return t;
+    };
+    SegT before = seg_identity<S, VEC>();        // later steps of the tile, in scan order
+    for (int w = NW - 1; w > wave; --w) before = seg_then<S, VEC>(before, wave_total(w));
+    const SegT pre = seg_then<S, VEC>(before, exc);
 
-    // ---- group 0 (earliest steps) holds the tile summary: publish, look back
-    if (g == 0) {
-        S iA[VEC], iH[VEC];
-#pragma unroll
-        for (int v = 0; v < VEC; ++v) {
-            if (f_own) {
-                iA[v] = A[v];
-                iH[v] = H[v];
-            } else {
-                iH[v] = mad(A[v], eH[v], H[v]);
-                iA[v] = A[v] * eA[v];
-            }
-        }
-        const bool tile_any = ef || f_own;
-        const int64_t di = (int64_t)ticket * Dp + (int64_t)q * VEC;
-        if (active) {
+    // ---- wavefront 0 publishes the tile summary; the last wavefront looks
+    // back for the carry from the later tiles (publishing and polling use
+    // different wavefronts: loads and stores share one completion counter)
+    const bool summary_lane = wave == 0 && j == 0 && active;
+    SegT tot = seg_identity<S, VEC>();
+    if (wave == 0) {
+        tot = seg_then<S, VEC>(before, wave_total(0));
+        if (summary_lane) {
 #pragma unroll
             for (int v = 0; v < VEC; ++v) {
-                if (tile_any) Desc<S>::put_incl(p.incl, di + v, iH[v]);
-                else Desc<S>::put_agg(p.agg, di + v, iA[v], iH[v]);
+                if (tot.f) Desc<S>::put_incl(p.incl, desc_slot(ticket, Dp, Qp, q, v), tot.H[v]);
+                else Desc<S>::put_agg(p.agg, desc_slot(ticket, Dp, Qp, q, v), tot.A[v], tot.H[v]);
             }
         }
+    }
+    if (wave == NW - 1) {
+        const bool need_carry = !((t_last + 1 == T) || fl_after != 0);
         S carry[VEC];
+        lookback<S, VEC>(p.agg, p.incl, (int64_t)ticket - p.nchains, p.nchains, Dp, Qp, need_carry && active, carry,
+                         sLb, &p.hdr->timeout);
+        if (j == 0) {
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) carry[v] = s_zero<S>();
-        const int64_t t_last = (tile_row0 + L < T ? tile_row0 + L : T) - 1;
-        const bool need_carry = !((t_last + 1 == T) || st[t_last + 1] != 0);
-        if (active && need_carry) {
-            S accA[VEC], accH[VEC];
-#pragma unroll
-            for (int v = 0; v < VEC; ++v) { accA[v] = s_one<S>(); accH[v] = s_zero<S>(); }
-            int64_t pred = (int64_t)ticket - p.nchains;
-            uint32_t polls = 0;
-            while (true) {
-                const int64_t pi = pred * Dp + (int64_t)q * VEC;
-                S ih[VEC];
-                bool ok = true;
-#pragma unroll
-                for (int v = 0; v < VEC; ++v) ok = Desc<S>::get_incl(p.incl, pi + v, ih[v]) && ok;
-                if (ok) {
-#pragma unroll
-                    for (int v = 0; v < VEC; ++v) carry[v] = mad(accA[v], ih[v], accH[v]);
-                    break;
-                }
-                S ga[VEC], gh[VEC];
-                ok = true;
-#pragma unroll
-                for (int v = 0; v < VEC; ++v) ok = Desc<S>::get_agg(p.agg, pi + v, ga[v], gh[v]) && ok;
-                if (ok) {
-#pragma unroll
-                    for (int v = 0; v < VEC; ++v) {
-                        accH[v] = mad(accA[v], gh[v], accH[v]);
-                        accA[v] = accA[v] * ga[v];
-                    }
-                    pred -= p.nchains;
-                    continue;
-                }
-                if (++polls > kMaxPolls) {
-                    __hip_atomic_store(&p.hdr->timeout, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(1);
-            }
+            for (int v = 0; v < VEC; ++v) sCarry[q * VEC + v] = carry[v];
         }
-        if (active && !tile_any) {
-#pragma unroll
-            for (int v = 0; v < VEC; ++v) Desc<S>::put_incl(p.incl, di + v, mad(iA[v], carry[v], iH[v]));
-        }
-#pragma unroll
-        for (int v = 0; v < VEC; ++v) sCarry[q * VEC + v] = carry[v];
     }
     __syncthreads();
 
-    // ---- replay backwards from the carry-in; emit dx, da
+    // ---- the tile's inclusive prefix goes out first; then replay backwards
+    // from the carry-in and emit dx (built in the registers that held g) and
+    // da (in those that held a), so no store waits on another
     S lam[VEC];
 #pragma unroll
     for (int v = 0; v < VEC; ++v) {
         const S c = sCarry[q * VEC + v];
-        lam[v] = ef ? eH[v] : mad(eA[v], c, eH[v]);
+        if (summary_lane && !tot.f)
+            Desc<S>::put_incl(p.incl, desc_slot(ticket, Dp, Qp, q, v), mad(tot.A[v], c, tot.H[v]));
+        lam[v] = seg_apply<S, VEC>(pre, v, c);
     }
     S dsum[VEC];
 #pragma unroll
     for (int v = 0; v < VEC; ++v) dsum[v] = s_zero<S>();
-    const bool want_da = AINV ? p.da_part != nullptr : p.da != nullptr;
     if (active) {
 #pragma unroll
         for (int r = R - 1; r >= 0; --r) {
-            if (!((valid >> r) & 1u)) continue;
-            const int64_t t = row0 + r;
             const bool e = (ends >> r) & 1u;
             const bool bg = (begins >> r) & 1u;
-            RawVec<K, VEC> hprev;
-            if (want_da && !bg) raw_load(hprev, (const char*)p.h + ((rowbase + t - 1) * p.d + f0) * EB);
-            RawVec<K, VEC> odx, oda;
 #pragma unroll
             for (int v = 0; v < VEC; ++v) {
                 const S gv = C::get(rg[r], v);
                 lam[v] = e ? gv : mad(coef(r, v), lam[v], gv);
-                C::put(odx, v, lam[v]);
-                const S dav = bg ? s_zero<S>() : lam[v] * conj(C::get(hprev, v));
-                if constexpr (AINV) dsum[v] = dsum[v] + dav;
-                else C::put(oda, v, dav);
+                const S dav = bg ? s_zero<S>() : lam[v] * conj(C::get(rh[r], v));
+                if constexpr (AINV) {
+                    if ((valid >> r) & 1u) dsum[v] = dsum[v] + dav;
+                } else {
+                    C::put(ra[r], v, dav);
+                }
+                C::put(rg[r], v, lam[v]);
             }
-            const int64_t off = ((rowbase + t) * p.d + f0) * EB;
-            raw_store_nt((char*)p.dx + off, odx);
+        }
+#pragma unroll
+        for (int r = R - 1; r >= 0; --r) {
+            if (!((valid >> r) & 1u)) continue;
+            const int64_t off = ((rowbase + row0 + r) * p.d + f0) * EB;
+            raw_store_nt((char*)p.dx + off, rg[r]);
             if constexpr (!AINV) {
-                if (want_da) raw_store_nt((char*)p.da + off, oda);
+                if (want_da) raw_store_nt((char*)p.da + off, ra[r]);
             }
         }
     }
     if constexpr (AINV) {
         if (want_da) {
-            // deterministic per-tile partial: sum the groups in a fixed order
+            // per-tile partial of da, summed over the tile's lanes in a fixed
+            // order (wavefront, then group)
             __syncthreads();
 #pragma unroll
-            for (int v = 0; v < VEC; ++v) sH[tid * VEC + v] = dsum[v];
+            for (int v = 0; v < VEC; ++v) sWH[wave][lane * VEC + v] = dsum[v];
             __syncthreads();
-            if (g == 0 && active) {
+            if (wave == 0 && j == 0 && active) {
                 RawVec<K, VEC> o;
 #pragma unroll
                 for (int v = 0; v < VEC; ++v) {
                     S s = s_zero<S>();
-                    for (int gg = 0; gg < G; ++gg) s = s + sH[(gg * Qp + q) * VEC + v];
+                    for (int w = 0; w < NW; ++w)
+                        for (int jj = 0; jj < Gw; ++jj) s = s + sWH[w][(jj * Qp + q) * VEC + v];
                     C::put(o, v, s);
                 }
                 // partial row = (tile, tape); columns = the d features
@@ -273,17 +253,28 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     }
 }
 
-// Column sums of a row-major [rows][cols] float matrix, `chunk` rows per
-// thread, in row order: out[(r / chunk)][c] = sum of rows r .. r+chunk-1.
+// Column sums of a row-major [rows][cols] float matrix over blocks of 64
+// rows: out[r / 64][c] = sum of rows r .. r+63 of column c.  A workgroup takes
+// 64 columns; its four wavefronts each add 16 consecutive rows (independent
+// loads), then the four partial sums are added in wavefront order, so the
+// result does not depend on timing.
 __global__ __launch_bounds__(256) void colsum_kernel(const float* in, float* out, int64_t rows,
-                                                     int64_t cols, int64_t chunk) {
-    const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const int64_t r0 = (int64_t)blockIdx.y * chunk;
-    if (c >= cols) return;
-    const int64_t r1 = r0 + chunk < rows ? r0 + chunk : rows;
+                                                     int64_t cols) {
+    __shared__ float part[4][64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int64_t c = (int64_t)blockIdx.x * 64 + lane;
+    const int64_t r0 = (int64_t)blockIdx.y * 64 + w * 16;
     float s = 0.0f;
-    for (int64_t r = r0; r < r1; ++r) s += in[r * cols + c];
-    out[(int64_t)blockIdx.y * cols + c] = s;
+    if (c < cols) {
+        float v[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) v[i] = r0 + i < rows ? in[(r0 + i) * cols + c] : 0.0f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s += v[i];
+    }
+    part[w][lane] = s;
+    __syncthreads();
+    if (w == 0 && c < cols) out[(int64_t)blockIdx.y * cols + c] = ((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane];
 }
 
 // ------------------------------------------------------------------ launch
@@ -299,19 +290,21 @@ static hipError_t launch_bwd(const DiagBwdArgs& args, int64_t ntiles, bool ainv,
 
 hipError_t diag_bwd_launch(int kind, bool vec, bool ainv, const DiagBwdArgs& args, int64_t ntiles,
                            hipStream_t s) {
-    constexpr int R = kBwdRows;
-    if (kind == K_F32)
-        return vec ? launch_bwd<K_F32, 4, R>(args, ntiles, ainv, s) : launch_bwd<K_F32, 1, R>(args, ntiles, ainv, s);
-    if (kind == K_C64)
-        return vec ? launch_bwd<K_C64, 2, R>(args, ntiles, ainv, s) : launch_bwd<K_C64, 1, R>(args, ntiles, ainv, s);
+    constexpr int RI = diag_rows(true, true), RS = diag_rows(true, false);
+    if (kind == K_F32) {
+        if (ainv) return vec ? launch_bwd<K_F32, KindInfo<K_F32>::vec, RI>(args, ntiles, true, s) : launch_bwd<K_F32, 1, RI>(args, ntiles, true, s);
+        return vec ? launch_bwd<K_F32, KindInfo<K_F32>::vec, RS>(args, ntiles, false, s) : launch_bwd<K_F32, 1, RS>(args, ntiles, false, s);
+    }
+    if (kind == K_C64) {
+        if (ainv) return vec ? launch_bwd<K_C64, KindInfo<K_C64>::vec, RI>(args, ntiles, true, s) : launch_bwd<K_C64, 1, RI>(args, ntiles, true, s);
+        return vec ? launch_bwd<K_C64, KindInfo<K_C64>::vec, RS>(args, ntiles, false, s) : launch_bwd<K_C64, 1, RS>(args, ntiles, false, s);
+    }
     return hipErrorInvalidValue;
 }
 
-hipError_t colsum_launch(const float* in, float* out, int64_t rows, int64_t cols, int64_t chunk,
-                         hipStream_t s) {
-    const int64_t nchunks = (rows + chunk - 1) / chunk;
-    dim3 grid((unsigned)((cols + 255) / 256), (unsigned)nchunks);
-    hipLaunchKernelGGL(colsum_kernel, grid, dim3(256), 0, s, in, out, rows, cols, chunk);
+hipError_t colsum_launch(const float* in, float* out, int64_t rows, int64_t cols, hipStream_t s) {
+    dim3 grid((unsigned)((cols + 63) / 64), (unsigned)((rows + 63) / 64));
+    hipLaunchKernelGGL(colsum_kernel, grid, dim3(256), 0, s, in, out, rows, cols);
     return hipGetLastError();
 }
 

@@ -8,27 +8,30 @@
 //
 // Work decomposition
 //   chain  = (tape b, feature block fb): an independent scan over T steps of
-//            Dp = Qp * VEC features; blocks are as wide as one wavefront row
-//            (64 lanes x 16 bytes) so every row access is a coalesced burst.
-//   tile   = L = G * R consecutive steps of one chain, one workgroup.  Lane q
-//            of group g owns VEC features and R consecutive steps; groups are
-//            consecutive in time (for Qp = 64 a group is one wavefront).
+//            Dp = Qp * VEC features.  Qp lanes of VEC features each cover one
+//            step's block; a block is one 128-byte line of the feature row
+//            (narrow chains make the tiles long in time, so an episode spans
+//            few tiles and the carry rarely has far to travel).
+//   tile   = one workgroup of 4 wavefronts.  Lane (j, q) of wavefront w
+//            (lane = j * Qp + q) owns the VEC features at q and R consecutive
+//            steps; its group is w * Gw + j with Gw = 64 / Qp, groups being
+//            consecutive in time: L = 4 * Gw * R steps per tile.
 //   ticket = tiles are numbered by an atomic counter in launch order,
 //            interleaving chains (ticket = tile * nchains + chain), so every
 //            tile a workgroup waits for was handed to a workgroup that is
 //            already running or finished.
 //
-// Per tile: (1) load a, x for all R steps into registers with one wide load
-// per step; (2) each lane folds its R steps into a summary (A, H, any-begin);
-// (3) groups combine their summaries through LDS into exclusive prefixes and
-// the tile summary; (4) the last group publishes the tile summary to the
-// workspace at once -- as the inclusive prefix if the tile holds a begin step
-// (nothing older can reach past it), else as an aggregate -- then looks back
-// over predecessor tiles of its chain, folding aggregates until it meets an
-// inclusive prefix, and publishes its own inclusive prefix; (5) every lane
-// replays its R steps from its carry-in and streams h out.  a and x are read
-// from HBM once and h written once; the cross-tile traffic is a few words per
-// feature per tile.
+// Per tile: (1) every load is issued up front: the begin flags of the lane's
+// steps, then a and x, one wide access per step; (2) each lane folds its R
+// steps into a segment summary (A, H, has-begin); (3) the groups of a
+// wavefront scan their summaries with cross-lane shuffles, and the four
+// wavefront totals are combined through LDS; (4) the last wavefront publishes
+// the tile summary at once -- as the inclusive prefix if the tile holds a
+// begin step (nothing older can reach past it), else as an aggregate -- while
+// the first wavefront looks back over predecessor tiles for the carry-in;
+// (5) the tile's inclusive prefix is published, and every lane replays its
+// steps from its carry-in and streams h out.  a and x are read from HBM once
+// and h written once; cross-tile traffic is a few bytes per feature per tile.
 #include "scan_common.hpp"
 #include "kernels.hpp"
 
@@ -39,15 +42,18 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     using S = typename StateOf<IN>::type;
     using CIn = Codec<IN, VEC>;
     using COut = Codec<OUT, VEC>;
+    using SegT = Seg<S, VEC>;
     constexpr int NT = 256;
+    constexpr int NW = NT / 64;
     constexpr int IB = KindInfo<IN>::bytes;
     constexpr int OB = KindInfo<OUT>::bytes;
 
     __shared__ uint32_t s_ticket;
-    __shared__ S sA[NT * VEC];
-    __shared__ S sH[NT * VEC];
-    __shared__ uint8_t sF[NT];
+    __shared__ S sWA[NW][64 * VEC];        // wavefront totals, per feature of the block
+    __shared__ S sWH[NW][64 * VEC];
+    __shared__ uint32_t sWF[NW];
     __shared__ S sCarry[64 * VEC];
+    __shared__ LookbackLds<S, VEC> sLb;
 
     const int tid = threadIdx.x;
     if (tid == 0) s_ticket = atomicAdd(&p.hdr->ticket, 1u);
@@ -58,33 +64,50 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     const int b = chain / p.nfb;
     const int fb = chain - b * p.nfb;
     const int Qp = p.Qp;
-    const int G = NT / Qp;
-    const int q = tid & (Qp - 1);
-    const int g = tid / Qp;
+    const int Gw = 64 / Qp;
+    const int wave = tid >> 6;
+    const int lane = tid & 63;
+    const int q = lane & (Qp - 1);
+    const int j = lane / Qp;
     const int Dp = Qp * VEC;
-    const int64_t L = (int64_t)G * R;
+    const int64_t L = (int64_t)NW * Gw * R;
     const int64_t tile_row0 = tile * L;
-    const int64_t row0 = tile_row0 + (int64_t)g * R;
+    const int64_t row0 = tile_row0 + (int64_t)(wave * Gw + j) * R;
     const int64_t f0 = (int64_t)fb * Dp + (int64_t)q * VEC;
     const bool active = f0 < p.d;
     const uint8_t* st = p.start + (int64_t)b * p.T;
 
-    // ---- (1) loads: one wide access per step and tensor
+    // ---- (1) loads.  Flags of the lane's own steps (and of the tile's first
+    // step) first, by unconditional byte loads at clamped addresses, so that
+    // waiting for them leaves every data load in flight; then one wide access
+    // per step and tensor.
+    uint32_t fl[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int64_t t = row0 + r < p.T ? row0 + r : p.T - 1;
+        fl[r] = st[t];
+    }
+    const uint32_t fl_tile0 = st[tile_row0];
+    __builtin_amdgcn_sched_barrier(0);
     RawVec<IN, VEC> ra[AINV ? 1 : R];
     RawVec<IN, VEC> rx[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int64_t t = row0 + r;
+        if (active && t < p.T) {
+            const int64_t off = ((int64_t)b * p.T + t) * p.d + f0;
+            raw_load(rx[r], (const char*)p.x + off * IB);
+            if constexpr (!AINV) raw_load(ra[r], (const char*)p.a + off * IB);
+        }
+    }
+    __builtin_amdgcn_sched_barrier(0);
     uint32_t begins = 0, valid = 0;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         const int64_t t = row0 + r;
-        if (t < p.T) {
-            valid |= 1u << r;
-            if (t == 0 || st[t] != 0) begins |= 1u << r;
-            if (active) {
-                const int64_t off = ((int64_t)b * p.T + t) * p.d + f0;
-                raw_load(rx[r], (const char*)p.x + off * IB);
-                if constexpr (!AINV) raw_load(ra[r], (const char*)p.a + off * IB);
-            }
-        }
+        const uint32_t in = t < p.T ? 1u : 0u;
+        valid |= in << r;
+        begins |= (in & ((t == 0 ? 1u : 0u) | (fl[r] != 0u ? 1u : 0u))) << r;
     }
     S ainv[VEC];
     if constexpr (AINV) {
@@ -98,10 +121,8 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
         else return CIn::get(ra[r], v);
     };
 
-    // ---- (2) per-lane summary of R steps
-    S A[VEC], H[VEC];
-#pragma unroll
-    for (int v = 0; v < VEC; ++v) { A[v] = s_one<S>(); H[v] = s_zero<S>(); }
+    // ---- (2) per-lane summary of its R steps (steps past T are identities)
+    SegT own = seg_identity<S, VEC>();
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         if (!((valid >> r) & 1u)) continue;
@@ -110,140 +131,106 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
         for (int v = 0; v < VEC; ++v) {
             const S xv = CIn::get(rx[r], v);
             if (bg) {
-                A[v] = s_one<S>();
-                H[v] = xv;
+                own.A[v] = s_one<S>();
+                own.H[v] = xv;
             } else {
                 const S av = a_at(r, v);
-                H[v] = mad(av, H[v], xv);
-                A[v] = A[v] * av;
+                own.H[v] = mad(av, own.H[v], xv);
+                own.A[v] = own.A[v] * av;
             }
         }
     }
-    const bool f_own = begins != 0;
+    own.f = begins != 0;
 
-    // ---- (3) combine groups through LDS
+    // ---- (3) scan the wavefront's groups; combine wavefront totals in LDS
+    SegT inc = own, exc;
+    wave_group_scan<S, VEC, false>(inc, exc, Qp);
+    if (j == Gw - 1) {
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) {
-        sA[tid * VEC + v] = A[v];
-        sH[tid * VEC + v] = H[v];
+        for (int v = 0; v < VEC; ++v) {
+            sWA[wave][q * VEC + v] = inc.A[v];
+            sWH[wave][q * VEC + v] = inc.H[v];
+        }
+        if (q == 0) sWF[wave] = inc.f;
     }
-    sF[tid] = f_own;
     __syncthreads();
-
-    S eA[VEC], eH[VEC];
-    bool ef = false;
-#pragma unroll
-    for (int v = 0; v < VEC; ++v) { eA[v] = s_one<S>(); eH[v] = s_zero<S>(); }
-    for (int gg = 0; gg < g; ++gg) {
-        const int j = gg * Qp + q;
-        const bool fj = sF[j];
+    auto wave_total = [&](int w) -> SegT {
+        SegT t;
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {
-            const S Aj = sA[j * VEC + v], Hj = sH[j * VEC + v];
-            if (fj) {
-                eA[v] = Aj;
-                eH[v] = Hj;
-            } else {
-                eH[v] = mad(Aj, eH[v], Hj);
-                eA[v] = Aj * eA[v];
-            }
+            t.A[v] = sWA[w][q * VEC + v];
+            t.H[v] = sWH[w][q * VEC + v];
         }
-        ef = ef || fj;
-    }
+        t.f = sWF[w] != 0;
+        return t;
+    };
+    SegT before = seg_identity<S, VEC>();        // tile steps before this wavefront
+    for (int w = 0; w < wave; ++w) before = seg_then<S, VEC>(before, wave_total(w));
+    const SegT pre = seg_then<S, VEC>(before, exc);   // tile steps before this lane's group
 
-    // ---- (4) publish, look back, publish inclusive
-    if (g == G - 1) {
-        S iA[VEC], iH[VEC];
-#pragma unroll
-        for (int v = 0; v < VEC; ++v) {
-            if (f_own) {
-                iA[v] = A[v];
-                iH[v] = H[v];
-            } else {
-                iH[v] = mad(A[v], eH[v], H[v]);
-                iA[v] = A[v] * eA[v];
-            }
-        }
-        const bool tile_any = ef || f_own;
-        const int64_t di = (int64_t)ticket * Dp + (int64_t)q * VEC;
-        if (active) {
+    // ---- (4) publish the tile summary (last wavefront, one group of lanes)
+    // and look back for the carry-in (first wavefront).  On this hardware a
+    // wavefront's loads and stores share one completion counter, so a
+    // wavefront with stores in flight could not see its polls' data before
+    // those stores are acknowledged: publishing and polling use different
+    // wavefronts.
+    const bool summary_lane = wave == NW - 1 && j == 0 && active;
+    SegT tot = seg_identity<S, VEC>();
+    if (wave == NW - 1) {
+        tot = seg_then<S, VEC>(before, wave_total(NW - 1));
+        if (summary_lane) {
 #pragma unroll
             for (int v = 0; v < VEC; ++v) {
-                if (tile_any) Desc<S>::put_incl(p.incl, di + v, iH[v]);
-                else Desc<S>::put_agg(p.agg, di + v, iA[v], iH[v]);
+                if (tot.f) Desc<S>::put_incl(p.incl, desc_slot(ticket, Dp, Qp, q, v), tot.H[v]);
+                else Desc<S>::put_agg(p.agg, desc_slot(ticket, Dp, Qp, q, v), tot.A[v], tot.H[v]);
             }
         }
+    }
+    if (wave == 0) {
+        const bool need_carry = !(tile_row0 == 0 || fl_tile0 != 0);
         S carry[VEC];
+        lookback<S, VEC>(p.agg, p.incl, (int64_t)ticket - p.nchains, p.nchains, Dp, Qp, need_carry && active, carry,
+                         sLb, &p.hdr->timeout);
+        if (j == 0) {
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) carry[v] = s_zero<S>();
-        const bool need_carry = !(tile_row0 == 0 || st[tile_row0] != 0);
-        if (active && need_carry) {
-            S accA[VEC], accH[VEC];
-#pragma unroll
-            for (int v = 0; v < VEC; ++v) { accA[v] = s_one<S>(); accH[v] = s_zero<S>(); }
-            int64_t pred = (int64_t)ticket - p.nchains;
-            uint32_t polls = 0;
-            while (true) {
-                const int64_t pi = pred * Dp + (int64_t)q * VEC;
-                S ih[VEC];
-                bool ok = true;
-#pragma unroll
-                for (int v = 0; v < VEC; ++v) ok = Desc<S>::get_incl(p.incl, pi + v, ih[v]) && ok;
-                if (ok) {
-#pragma unroll
-                    for (int v = 0; v < VEC; ++v) carry[v] = mad(accA[v], ih[v], accH[v]);
-                    break;
-                }
-                S ga[VEC], gh[VEC];
-                ok = true;
-#pragma unroll
-                for (int v = 0; v < VEC; ++v) ok = Desc<S>::get_agg(p.agg, pi + v, ga[v], gh[v]) && ok;
-                if (ok) {
-#pragma unroll
-                    for (int v = 0; v < VEC; ++v) {
-                        accH[v] = mad(accA[v], gh[v], accH[v]);
-                        accA[v] = accA[v] * ga[v];
-                    }
-                    pred -= p.nchains;
-                    continue;
-                }
-                if (++polls > kMaxPolls) {
-                    __hip_atomic_store(&p.hdr->timeout, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(1);
-            }
+            for (int v = 0; v < VEC; ++v) sCarry[q * VEC + v] = carry[v];
         }
-        if (active && !tile_any) {
-#pragma unroll
-            for (int v = 0; v < VEC; ++v) Desc<S>::put_incl(p.incl, di + v, mad(iA[v], carry[v], iH[v]));
-        }
-#pragma unroll
-        for (int v = 0; v < VEC; ++v) sCarry[q * VEC + v] = carry[v];
     }
     __syncthreads();
 
-    // ---- (5) replay from the carry-in and stream h out
+    // ---- (5) the tile's inclusive prefix goes out first (successors may be
+    // waiting for it); then every lane replays its steps from its carry-in and
+    // streams h out.  All outputs are computed before any store (in the
+    // registers that held x when the dtypes match), so the stores go out in
+    // one burst and never wait on one another.
     S hv[VEC];
 #pragma unroll
     for (int v = 0; v < VEC; ++v) {
         const S c = sCarry[q * VEC + v];
-        hv[v] = ef ? eH[v] : mad(eA[v], c, eH[v]);
+        if (summary_lane && !tot.f)
+            Desc<S>::put_incl(p.incl, desc_slot(ticket, Dp, Qp, q, v), mad(tot.A[v], c, tot.H[v]));
+        hv[v] = seg_apply<S, VEC>(pre, v, c);
     }
     if (!active) return;
+    constexpr bool kInPlace = (int)IN == (int)OUT;
+    RawVec<OUT, VEC> o[kInPlace ? 1 : R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-        if (!((valid >> r) & 1u)) continue;
         const bool bg = (begins >> r) & 1u;
-        RawVec<OUT, VEC> o;
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {
             const S xv = CIn::get(rx[r], v);
             hv[v] = bg ? xv : mad(a_at(r, v), hv[v], xv);
-            COut::put(o, v, hv[v]);
+            if constexpr (kInPlace) CIn::put(rx[r], v, hv[v]);
+            else COut::put(o[r], v, hv[v]);
         }
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        if (!((valid >> r) & 1u)) continue;
         const int64_t off = ((int64_t)b * p.T + row0 + r) * p.d + f0;
-        raw_store_nt((char*)p.h + off * OB, o);
+        if constexpr (kInPlace) raw_store_nt((char*)p.h + off * OB, rx[r]);
+        else raw_store_nt((char*)p.h + off * OB, o[r]);
     }
 }
 
@@ -258,25 +245,21 @@ static hipError_t launch_fwd(const DiagFwdArgs& args, int64_t ntiles, bool ainv,
     return hipGetLastError();
 }
 
-int diag_fwd_rows_per_lane(int in_kind) {
-    (void)in_kind;
-    return kFwdRows;
-}
-
 hipError_t diag_fwd_launch(int in_kind, int out_kind, bool vec, bool ainv,
                            const DiagFwdArgs& args, int64_t ntiles, hipStream_t s) {
     constexpr int R = kFwdRows;
+    constexpr int VF = KindInfo<K_F32>::vec, VB = KindInfo<K_BF16>::vec, VC = KindInfo<K_C64>::vec;
     if (in_kind == K_F32 && out_kind == K_F32)
-        return vec ? launch_fwd<K_F32, K_F32, 4, R>(args, ntiles, ainv, s)
+        return vec ? launch_fwd<K_F32, K_F32, VF, R>(args, ntiles, ainv, s)
                    : launch_fwd<K_F32, K_F32, 1, R>(args, ntiles, ainv, s);
     if (in_kind == K_BF16 && out_kind == K_BF16)
-        return vec ? launch_fwd<K_BF16, K_BF16, 8, R>(args, ntiles, ainv, s)
+        return vec ? launch_fwd<K_BF16, K_BF16, VB, R>(args, ntiles, ainv, s)
                    : launch_fwd<K_BF16, K_BF16, 1, R>(args, ntiles, ainv, s);
     if (in_kind == K_BF16 && out_kind == K_F32)
-        return vec ? launch_fwd<K_BF16, K_F32, 8, R>(args, ntiles, ainv, s)
+        return vec ? launch_fwd<K_BF16, K_F32, VB, R>(args, ntiles, ainv, s)
                    : launch_fwd<K_BF16, K_F32, 1, R>(args, ntiles, ainv, s);
     if (in_kind == K_C64 && out_kind == K_C64)
-        return vec ? launch_fwd<K_C64, K_C64, 2, R>(args, ntiles, ainv, s)
+        return vec ? launch_fwd<K_C64, K_C64, VC, R>(args, ntiles, ainv, s)
                    : launch_fwd<K_C64, K_C64, 1, R>(args, ntiles, ainv, s);
     return hipErrorInvalidValue;
 }

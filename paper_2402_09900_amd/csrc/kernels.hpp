@@ -9,10 +9,14 @@ namespace memoroid {
 
 struct WsHeader;
 
-// Steps per lane held in registers by the diagonal scans (tile length is
-// 256 / Qp * rows: 64 steps for full-width feature blocks).
+// Steps per lane held in registers by the diagonal scans (a tile is
+// 256 / Qp * rows steps long: 64 for full-width feature blocks).  The reverse
+// scan with a per-step a keeps three tensors per step (g, a, h) and so holds
+// fewer steps, to stay within 256 registers (two workgroups per CU).
 constexpr int kFwdRows = 16;
 constexpr int kBwdRows = 16;
+constexpr int kBwdRowsPerStepA = 12;
+constexpr int diag_rows(bool bwd, bool ainv) { return !bwd ? kFwdRows : (ainv ? kBwdRows : kBwdRowsPerStepA); }
 
 struct DiagFwdArgs {
     const void* a;
@@ -54,8 +58,8 @@ hipError_t diag_fwd_launch(int in_kind, int out_kind, bool vec, bool ainv,
                            const DiagFwdArgs& args, int64_t ntiles, hipStream_t s);
 hipError_t diag_bwd_launch(int kind, bool vec, bool ainv, const DiagBwdArgs& args,
                            int64_t ntiles, hipStream_t s);
-hipError_t colsum_launch(const float* in, float* out, int64_t rows, int64_t cols,
-                         int64_t chunk, hipStream_t s);
+// out[r / 64][c] = sum over rows r .. r+63 of in[r][c] (fixed order).
+hipError_t colsum_launch(const float* in, float* out, int64_t rows, int64_t cols, hipStream_t s);
 
 // Fill `bytes` (multiple of 16, 16-byte aligned) at p with 0xFF, and zero the
 // 256-byte header at hdr.  A kernel, not hipMemsetAsync, so that a caller may

@@ -18,7 +18,7 @@ enum Kind { K_F32 = 0, K_BF16 = 1, K_C64 = 2 };
 
 template <Kind K> struct KindInfo;
 template <> struct KindInfo<K_F32> { static constexpr int bytes = 4; static constexpr int vec = 4; };
-template <> struct KindInfo<K_BF16> { static constexpr int bytes = 2; static constexpr int vec = 8; };
+template <> struct KindInfo<K_BF16> { static constexpr int bytes = 2; static constexpr int vec = 4; };
 template <> struct KindInfo<K_C64> { static constexpr int bytes = 8; static constexpr int vec = 2; };
 
 // ------------------------------------------------------------ complex float
@@ -249,11 +249,204 @@ template <> struct Desc<cf> {
     }
 };
 
+// Descriptor slot of feature v of lane q inside tile `ticket`'s block of Dp
+// features: lanes are contiguous for a fixed v, so the accesses of a
+// wavefront coalesce.
+__device__ __forceinline__ int64_t desc_slot(int64_t ticket, int Dp, int Qp, int q, int v) {
+    return ticket * Dp + (int64_t)v * Qp + q;
+}
+
+
+
 // Bound on polls of one predecessor descriptor before a wait gives up and
 // flags MEMOROID_ETIMEOUT in the workspace (about a second of polling).  The
 // ticketed tile order guarantees every awaited tile is running or done, so
 // the bound only matters if that guarantee were broken.
 constexpr uint32_t kMaxPolls = 1u << 22;
+
+// ------------------------------------------------------------- look-back
+// Carry-in of a tile: the chain's state just before the tile, found by
+// walking back over predecessor tiles (tickets pred, pred - nchains, ...):
+// aggregates are folded until an inclusive prefix closes the walk.  One whole
+// wavefront runs it.  Its lanes form 64 / Qp groups of Qp lanes; lane (j, q)
+// polls predecessor base - j * nchains for the features of lane position q,
+// so each round trip to memory examines a window of 64 / Qp predecessors.
+// The window's entries go through LDS, and every lane then walks the window
+// in order for its q (lanes sharing q compute identical results).  A round
+// ends by resolving, by consuming the ready prefix of the window, or, if the
+// nearest predecessor is not yet published, by sleeping and polling again.
+// `need` false (no carry needed, or features past d) yields zeros.
+template <class S, int VEC>
+struct LookbackLds {
+    uint32_t st[64];
+    S a[64 * VEC];
+    S h[64 * VEC];
+};
+
+template <class S, int VEC>
+__device__ __forceinline__ void lookback(const void* agg, const void* incl, int64_t first_pred, int nchains,
+                                         int Dp, int Qp, bool need, S (&carry)[VEC], LookbackLds<S, VEC>& lds,
+                                         uint32_t* timeout) {
+    const int lane = threadIdx.x & 63;
+    const int q = lane & (Qp - 1);
+    const int j = lane / Qp;
+    const int Gw = 64 / Qp;
+    S accA[VEC], accH[VEC];
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) {
+        accA[v] = s_one<S>();
+        accH[v] = s_zero<S>();
+        carry[v] = s_zero<S>();
+    }
+    int64_t base = first_pred;
+    bool done = !need;
+    uint32_t polls = 0;
+    while (!__all(done)) {
+        const int64_t pj = base - (int64_t)j * nchains;
+        uint32_t stt = 0;
+        S va[VEC], vh[VEC];
+        if (!done && pj >= 0) {
+            S ih[VEC], ga[VEC], gh[VEC];
+            bool inc_ok = true, agg_ok = true;
+#pragma unroll
+            for (int v = 0; v < VEC; ++v)
+                inc_ok = Desc<S>::get_incl(incl, desc_slot(pj, Dp, Qp, q, v), ih[v]) && inc_ok;
+#pragma unroll
+            for (int v = 0; v < VEC; ++v)
+                agg_ok = Desc<S>::get_agg(agg, desc_slot(pj, Dp, Qp, q, v), ga[v], gh[v]) && agg_ok;
+            stt = inc_ok ? 2u : (agg_ok ? 1u : 0u);
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) {
+                va[v] = ga[v];
+                vh[v] = inc_ok ? ih[v] : gh[v];
+            }
+        }
+        lds.st[lane] = stt;
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+            lds.a[lane * VEC + v] = va[v];
+            lds.h[lane * VEC + v] = vh[v];
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        if (!done) {
+            int consumed = 0;
+            bool resolved = false;
+            for (int jj = 0; jj < Gw; ++jj) {
+                const int e = jj * Qp + q;
+                const uint32_t se = lds.st[e];
+                if (se == 2u) {
+#pragma unroll
+                    for (int v = 0; v < VEC; ++v) carry[v] = mad(accA[v], lds.h[e * VEC + v], accH[v]);
+                    resolved = true;
+                    break;
+                }
+                if (se != 1u) break;
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) {
+                    accH[v] = mad(accA[v], lds.h[e * VEC + v], accH[v]);
+                    accA[v] = accA[v] * lds.a[e * VEC + v];
+                }
+                ++consumed;
+            }
+            base -= (int64_t)consumed * nchains;
+            if (resolved) {
+                done = true;
+            } else if (consumed == 0) {
+                if (++polls > kMaxPolls) {
+                    __hip_atomic_store(timeout, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    done = true;
+                } else {
+                    __builtin_amdgcn_s_sleep(1);
+                }
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+}
+
+// ------------------------------------------------------------ segments
+// Summary of a run of consecutive steps (in scan order) of one feature: the
+// state after the run is  f ? H : A * (state before) + H,  f meaning "the run
+// holds an episode boundary".  This is the resettable monoid of the Section 4
+// theorem specialised to the diagonal recurrence, carried as a select.
+template <class S, int VEC>
+struct Seg {
+    S A[VEC], H[VEC];
+    bool f;
+};
+
+template <class S, int VEC>
+__device__ __forceinline__ Seg<S, VEC> seg_identity() {
+    Seg<S, VEC> r;
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) {
+        r.A[v] = s_one<S>();
+        r.H[v] = s_zero<S>();
+    }
+    r.f = false;
+    return r;
+}
+
+// the run `first` followed by the run `second`
+template <class S, int VEC>
+__device__ __forceinline__ Seg<S, VEC> seg_then(const Seg<S, VEC>& first, const Seg<S, VEC>& second) {
+    if (second.f) return second;
+    Seg<S, VEC> r;
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) {
+        r.H[v] = mad(second.A[v], first.H[v], second.H[v]);
+        r.A[v] = second.A[v] * first.A[v];
+    }
+    r.f = first.f;
+    return r;
+}
+
+// state after the run, given the state before it
+template <class S, int VEC>
+__device__ __forceinline__ S seg_apply(const Seg<S, VEC>& sg, int v, S before) {
+    return sg.f ? sg.H[v] : mad(sg.A[v], before, sg.H[v]);
+}
+
+__device__ __forceinline__ float shfl_from(float x, int src) { return __shfl(x, src, 64); }
+__device__ __forceinline__ cf shfl_from(cf x, int src) { return cf{__shfl(x.re, src, 64), __shfl(x.im, src, 64)}; }
+
+template <class S, int VEC>
+__device__ __forceinline__ Seg<S, VEC> seg_shfl(const Seg<S, VEC>& x, int src) {
+    Seg<S, VEC> r;
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) {
+        r.A[v] = shfl_from(x.A[v], src);
+        r.H[v] = shfl_from(x.H[v], src);
+    }
+    r.f = __shfl((int)x.f, src, 64) != 0;
+    return r;
+}
+
+// Scan across the Gw = 64 / Qp lane groups of a wavefront (lane = j * Qp + q;
+// group j holds consecutive steps, group j + 1 the ones after).  Forward
+// (REV = false): groups earlier in time come first; reverse: later ones.  On
+// return `inc` is the run from the wavefront's first group (in scan order)
+// through this lane's group, and `exc` the run before this lane's group.
+// Kogge-Stone over log2(Gw) cross-lane shuffles; no LDS, no barrier.
+template <class S, int VEC, bool REV>
+__device__ __forceinline__ void wave_group_scan(Seg<S, VEC>& inc, Seg<S, VEC>& exc, int Qp) {
+    const int lane = threadIdx.x & 63;
+    const int j = lane / Qp;
+    const int Gw = 64 / Qp;
+    for (int k = 1; k < Gw; k <<= 1) {
+        const int src = REV ? lane + k * Qp : lane - k * Qp;
+        const bool has = REV ? (j + k < Gw) : (j >= k);
+        const Seg<S, VEC> o = seg_shfl<S, VEC>(inc, has ? src : lane);
+        if (has) inc = seg_then<S, VEC>(o, inc);
+    }
+    const bool has = REV ? (j + 1 < Gw) : (j >= 1);
+    const Seg<S, VEC> o = seg_shfl<S, VEC>(inc, has ? (REV ? lane + Qp : lane - Qp) : lane);
+    exc = has ? o : seg_identity<S, VEC>();
+}
 
 // Workspace header shared by the scan kernels (first 256 bytes).
 struct WsHeader {
