@@ -41,7 +41,7 @@ struct DiagPlan {
     int64_t nt = 0;
     int64_t nchains = 0;
     int64_t ntiles = 0;
-    size_t off_agg = 0, off_incl = 0, off_part = 0, off_sum1 = 0, off_sum2 = 0, off_counts = 0;
+    size_t off_agg = 0, off_incl = 0, off_cnt = 0, off_part = 0, off_sum1 = 0, off_sum2 = 0;
     size_t fill_bytes = 0;   // bytes from off_agg that must start as 0xFF
     size_t total = 0;
 };
@@ -74,6 +74,8 @@ bool plan_diag(int64_t B, int64_t T, int64_t d, int state_dtype, bool vec, int r
     off = align_up(off + (size_t)ndesc * agg_b);
     p->off_incl = off;
     off = align_up(off + (size_t)ndesc * incl_b);
+    p->off_cnt = off;                                      // begin-count words, [tiles per chain][B]
+    if (!bwd) off = align_up(off + (size_t)p->nt * (size_t)B * 8);
     p->fill_bytes = off - p->off_agg;
     if (bwd && ainv && want_grad_a) {
         const size_t sb = cplx ? 8 : 4;
@@ -86,8 +88,6 @@ bool plan_diag(int64_t B, int64_t T, int64_t d, int state_dtype, bool vec, int r
         p->off_sum2 = off;
         off = align_up(off + (size_t)r2 * (size_t)d * sb);
     }
-    p->off_counts = off;
-    if (!bwd) off = align_up(off + (size_t)B * (size_t)((T + kEpBlock - 1) / kEpBlock) * 4);
     p->total = off;
     return true;
 }
@@ -100,20 +100,22 @@ bool diag_dtypes_ok(int in_dt, int out_dt) {
 }
 
 
-// Reduce a [rows][cols] float matrix over rows into out[cols], 64 rows per
-// pass, in a fixed order.
+// Reduce a [rows][cols] float matrix over rows into out[cols] in a fixed
+// order: one pass when there are at most 1024 rows (256 per wavefront),
+// otherwise passes of 64 rows until that holds.
 int reduce_rows(const float* part, float* s1, float* s2, float* out, int64_t rows, int64_t cols,
                 hipStream_t s) {
     const float* cur = part;
     float* bufs[2] = {s1, s2};
     int which = 0;
-    while (rows > 64) {
-        if (colsum_launch(cur, bufs[which], rows, cols, s) != hipSuccess) return MEMOROID_EHIP;
+    while (rows > 1024) {
+        if (colsum_launch(cur, bufs[which], rows, cols, 16, s) != hipSuccess) return MEMOROID_EHIP;
         cur = bufs[which];
         which ^= 1;
         rows = (rows + 63) / 64;
     }
-    return check_hip(colsum_launch(cur, out, rows, cols, s));
+    const int64_t rpw = rows > 0 ? (rows + 3) / 4 : 1;
+    return check_hip(colsum_launch(cur, out, rows, cols, rpw, s));
 }
 
 }  // namespace
@@ -166,7 +168,6 @@ int memoroid_scan_diag(const void* a, int64_t a_stride_t, const void* x, const u
     if (h == x || h == a || (const void*)episode_idx == (const void*)h || (const void*)episode_idx == x ||
         (const void*)episode_idx == a || (const void*)episode_idx == (const void*)start)
         return MEMOROID_EINVAL;
-    if (episode_idx && B > 65535) return MEMOROID_EUNSUPPORTED;
     const bool ainv = a_stride_t == 0;
     const int VW = vec_width(in_dtype);
     const bool vec = d % VW == 0 && aligned(x, 16) && aligned(h, 16) && aligned(a, 16);
@@ -195,13 +196,11 @@ int memoroid_scan_diag(const void* a, int64_t a_stride_t, const void* x, const u
     args.agg = ws + p.off_agg;
     args.incl = ws + p.off_incl;
     args.hdr = (WsHeader*)ws;
+    args.idx = episode_idx;
+    args.cnt = (uint64_t*)(ws + p.off_cnt);
     const int ik = in_dtype == MEMOROID_F32 ? K_F32 : in_dtype == MEMOROID_BF16 ? K_BF16 : K_C64;
     const int ok = out_dtype == MEMOROID_F32 ? K_F32 : out_dtype == MEMOROID_BF16 ? K_BF16 : K_C64;
     if (diag_fwd_launch(ik, ok, vec, ainv, args, p.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
-    if (episode_idx) {
-        if (episode_idx_launch(start, episode_idx, B, T, (int32_t*)(ws + p.off_counts), s) != hipSuccess)
-            return MEMOROID_EHIP;
-    }
     return MEMOROID_OK;
 }
 
@@ -269,9 +268,9 @@ int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t, const uint8_t* sta
     args.incl = ws + p.off_incl;
     args.hdr = (WsHeader*)ws;
     const int k = dtype == MEMOROID_F32 ? K_F32 : K_C64;
+    const int64_t cols = d * (dtype == MEMOROID_C64 ? 2 : 1);
     if (diag_bwd_launch(k, vec, ainv, args, p.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
     if (ainv && grad_a) {
-        const int64_t cols = d * (dtype == MEMOROID_C64 ? 2 : 1);
         const int st = reduce_rows((const float*)(ws + p.off_part), (float*)(ws + p.off_sum1),
                                    (float*)(ws + p.off_sum2), (float*)grad_a, p.nt * B, cols, s);
         if (st != MEMOROID_OK) return st;

@@ -253,24 +253,29 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     }
 }
 
-// Column sums of a row-major [rows][cols] float matrix over blocks of 64
-// rows: out[r / 64][c] = sum of rows r .. r+63 of column c.  A workgroup takes
-// 64 columns; its four wavefronts each add 16 consecutive rows (independent
-// loads), then the four partial sums are added in wavefront order, so the
-// result does not depend on timing.
+// Column sums of a row-major [rows][cols] float matrix over blocks of
+// 4 * rpw rows: out[r / (4 rpw)][c] = sum of rows r .. r + 4 rpw - 1 of column
+// c.  A workgroup takes 64 columns; each of its four wavefronts adds rpw
+// consecutive rows (loads issued 16 at a time), then the four partial sums
+// are added in wavefront order, so the result does not depend on timing.
 __global__ __launch_bounds__(256) void colsum_kernel(const float* in, float* out, int64_t rows,
-                                                     int64_t cols) {
+                                                     int64_t cols, int64_t rpw) {
     __shared__ float part[4][64];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int64_t c = (int64_t)blockIdx.x * 64 + lane;
-    const int64_t r0 = (int64_t)blockIdx.y * 64 + w * 16;
+    const int64_t r0 = (int64_t)blockIdx.y * 4 * rpw + w * rpw;
     float s = 0.0f;
     if (c < cols) {
-        float v[16];
+        for (int64_t i0 = 0; i0 < rpw; i0 += 16) {
+            float v[16];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) v[i] = r0 + i < rows ? in[(r0 + i) * cols + c] : 0.0f;
+            for (int i = 0; i < 16; ++i) {
+                const int64_t r = r0 + i0 + i;
+                v[i] = (i0 + i < rpw && r < rows) ? in[r * cols + c] : 0.0f;
+            }
 #pragma unroll
-        for (int i = 0; i < 16; ++i) s += v[i];
+            for (int i = 0; i < 16; ++i) s += v[i];
+        }
     }
     part[w][lane] = s;
     __syncthreads();
@@ -302,9 +307,9 @@ hipError_t diag_bwd_launch(int kind, bool vec, bool ainv, const DiagBwdArgs& arg
     return hipErrorInvalidValue;
 }
 
-hipError_t colsum_launch(const float* in, float* out, int64_t rows, int64_t cols, hipStream_t s) {
-    dim3 grid((unsigned)((cols + 63) / 64), (unsigned)((rows + 63) / 64));
-    hipLaunchKernelGGL(colsum_kernel, grid, dim3(256), 0, s, in, out, rows, cols);
+hipError_t colsum_launch(const float* in, float* out, int64_t rows, int64_t cols, int64_t rpw, hipStream_t s) {
+    dim3 grid((unsigned)((cols + 63) / 64), (unsigned)((rows + 4 * rpw - 1) / (4 * rpw)));
+    hipLaunchKernelGGL(colsum_kernel, grid, dim3(256), 0, s, in, out, rows, cols, rpw);
     return hipGetLastError();
 }
 

@@ -54,6 +54,8 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     __shared__ uint32_t sWF[NW];
     __shared__ S sCarry[64 * VEC];
     __shared__ LookbackLds<S, VEC> sLb;
+    __shared__ uint32_t sWC[NW];           // begin counts per wavefront (episode index)
+    __shared__ uint32_t sCntBefore;        // begins on the tape before this tile
 
     const int tid = threadIdx.x;
     if (tid == 0) s_ticket = atomicAdd(&p.hdr->ticket, 1u);
@@ -142,6 +144,21 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     }
     own.f = begins != 0;
 
+    // ---- episode index (optional): the tiles of each tape's first feature
+    // block count begin steps; the count of the lane's earlier groups comes
+    // from a cross-lane prefix sum over the wavefront's groups
+    const bool want_idx = p.idx != nullptr && fb == 0;
+    const int B = p.nchains / p.nfb;
+    const uint32_t c_own = __builtin_popcount(begins);
+    uint32_t c_inc = c_own;
+    if (want_idx) {
+        for (int k = 1; k < Gw; k <<= 1) {
+            const uint32_t o = (uint32_t)__shfl((int)c_inc, j >= k ? lane - k * Qp : lane, 64);
+            if (j >= k) c_inc += o;
+        }
+        if (j == Gw - 1 && q == 0) sWC[wave] = c_inc;
+    }
+
     // ---- (3) scan the wavefront's groups; combine wavefront totals in LDS
     SegT inc = own, exc;
     wave_group_scan<S, VEC, false>(inc, exc, Qp);
@@ -186,6 +203,20 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
             }
         }
     }
+    uint32_t c_before = 0, c_tile = 0;           // begins before this wavefront / in the tile
+    if (want_idx) {
+        for (int w = 0; w < NW; ++w) {
+            if (w < wave) c_before += sWC[w];
+            c_tile += sWC[w];
+        }
+        if (wave == NW - 1 && lane == 0)
+            publish64(p.cnt + tile * B + b, (tile == 0 ? kCountIncl : kCountOwn) | c_tile);
+        if (wave == 1) {
+            const uint32_t before_tile =
+                tile == 0 ? 0u : count_lookback(p.cnt, (tile - 1) * B + b, B, &p.hdr->timeout);
+            if (lane == 0) sCntBefore = before_tile;
+        }
+    }
     if (wave == 0) {
         const bool need_carry = !(tile_row0 == 0 || fl_tile0 != 0);
         S carry[VEC];
@@ -210,6 +241,19 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
         if (summary_lane && !tot.f)
             Desc<S>::put_incl(p.incl, desc_slot(ticket, Dp, Qp, q, v), mad(tot.A[v], c, tot.H[v]));
         hv[v] = seg_apply<S, VEC>(pre, v, c);
+    }
+    if (want_idx) {
+        const uint32_t base_cnt = sCntBefore;
+        if (wave == NW - 1 && lane == 0 && tile > 0) publish64(p.cnt + tile * B + b, kCountIncl | (base_cnt + c_tile));
+        if (q == 0) {
+            uint32_t run = base_cnt + c_before + (c_inc - c_own);
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                if (!((valid >> r) & 1u)) continue;
+                run += (begins >> r) & 1u;
+                p.idx[(int64_t)b * p.T + row0 + r] = (int32_t)run - 1;
+            }
+        }
     }
     if (!active) return;
     constexpr bool kInPlace = (int)IN == (int)OUT;

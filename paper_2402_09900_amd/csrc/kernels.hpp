@@ -32,6 +32,8 @@ struct DiagFwdArgs {
     void* agg;         // [tiles][Dp] aggregate descriptor words
     void* incl;        // [tiles][Dp] inclusive-prefix descriptor words
     WsHeader* hdr;
+    int32_t* idx;      // episode index out [B][T], or NULL
+    uint64_t* cnt;     // [tiles per chain][B] begin-count descriptor words
 };
 
 struct DiagBwdArgs {
@@ -58,8 +60,9 @@ hipError_t diag_fwd_launch(int in_kind, int out_kind, bool vec, bool ainv,
                            const DiagFwdArgs& args, int64_t ntiles, hipStream_t s);
 hipError_t diag_bwd_launch(int kind, bool vec, bool ainv, const DiagBwdArgs& args,
                            int64_t ntiles, hipStream_t s);
-// out[r / 64][c] = sum over rows r .. r+63 of in[r][c] (fixed order).
-hipError_t colsum_launch(const float* in, float* out, int64_t rows, int64_t cols, hipStream_t s);
+// out[r / (4 rpw)][c] = sum over rows r .. r + 4 rpw - 1 of in[r][c], in a
+// fixed order (rpw: rows per wavefront).
+hipError_t colsum_launch(const float* in, float* out, int64_t rows, int64_t cols, int64_t rpw, hipStream_t s);
 
 // Fill `bytes` (multiple of 16, 16-byte aligned) at p with 0xFF, and zero the
 // 256-byte header at hdr.  A kernel, not hipMemsetAsync, so that a caller may

@@ -448,6 +448,56 @@ __device__ __forceinline__ void wave_group_scan(Seg<S, VEC>& inc, Seg<S, VEC>& e
     exc = has ? o : seg_identity<S, VEC>();
 }
 
+// ------------------------------------------------------- count look-back
+// Running count of begin steps before a tile (the episode index is that count
+// minus one), carried by one 64-bit word per tile: all ones = not yet
+// published, bit 62 = the tile's own count, bit 63 = the count through the
+// end of the tile; the low 32 bits hold the value.  A count never resets, so
+// the walk always goes back to an inclusive word; one wavefront polls 64
+// predecessors per round trip (lane l: predecessor base - l * stride) and the
+// ready prefix of the window is summed with cross-lane reductions.
+constexpr uint64_t kCountOwn = 1ull << 62;
+constexpr uint64_t kCountIncl = 2ull << 62;
+
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += (uint32_t)__shfl_xor((int)v, off, 64);
+    return v;
+}
+
+__device__ __forceinline__ uint32_t count_lookback(const uint64_t* desc, int64_t first_pred, int64_t stride,
+                                                   uint32_t* timeout) {
+    const int lane = threadIdx.x & 63;
+    uint32_t acc = 0;
+    int64_t base = first_pred;
+    uint32_t polls = 0;
+    while (true) {
+        const int64_t i = base - (int64_t)lane * stride;
+        // before the first tile of the tape the count is an inclusive zero
+        const uint64_t w = i >= 0 ? peek64(desc + i) : kCountIncl;
+        const bool empty = w == kEmpty64;
+        const bool incl = !empty && (w & kCountIncl) != 0;
+        const uint64_t m_empty = __ballot(empty);
+        const uint64_t m_incl = __ballot(incl);
+        const int first_incl = m_incl ? __builtin_ctzll(m_incl) : 64;
+        const int first_empty = m_empty ? __builtin_ctzll(m_empty) : 64;
+        if (first_incl < first_empty) {
+            const uint32_t mine = lane <= first_incl ? (uint32_t)w : 0u;
+            return acc + wave_sum_u32(mine);
+        }
+        const uint32_t mine = lane < first_empty ? (uint32_t)w : 0u;
+        acc += wave_sum_u32(mine);
+        base -= (int64_t)first_empty * stride;
+        if (first_empty == 0) {
+            if (++polls > kMaxPolls) {
+                __hip_atomic_store(timeout, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                return acc;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+    }
+}
+
 // Workspace header shared by the scan kernels (first 256 bytes).
 struct WsHeader {
     uint32_t ticket;     // next tile ticket

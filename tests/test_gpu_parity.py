@@ -335,3 +335,10 @@ def test_autograd_function():
     loose = (m_dx * mh_prev * nb[..., None]).sum(axis=(0, 1))
     err = np.abs(from_dev(a.grad) - da) / np.maximum(np.abs(da), loose)
     assert err.max() <= 1e-4
+
+
+def test_invariant_da_long_tape_uses_column_sum_kernels():
+    """More partial rows than the in-kernel da reduction takes: the column-sum
+    kernels add them up instead."""
+    w = tapes.make_custom_diag("c64", 1, 600_000, 32, True, seed=14, a_range=(0.9, 0.999), mean_episode=300.0)
+    check_bwd(w, label="long-invariant")
