@@ -13,7 +13,6 @@ using namespace memoroid;
 namespace {
 
 constexpr size_t kAlign = 256;
-constexpr int64_t kChainRowBytes = 128;
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 int elem_bytes(int dt) { return dt == MEMOROID_F32 ? 4 : dt == MEMOROID_BF16 ? 2 : 8; }
@@ -287,9 +286,8 @@ namespace {
 
 struct LinPlan {
     int64_t nch = 0, dstate = 0;
-    size_t off_dS = 0, off_Sinc = 0, off_R = 0, off_ones = 0, off_scan = 0, off_counts = 0, total = 0;
+    size_t off_dS = 0, off_Sinc = 0, off_R = 0, off_scan = 0, off_cnt = 0, total = 0;
     DiagPlan scan;
-    bool scan_vec = true;
 };
 
 bool plan_linattn(int64_t T, int64_t H, LinPlan* p) {
@@ -297,23 +295,23 @@ bool plan_linattn(int64_t T, int64_t H, LinPlan* p) {
     p->dstate = H * kLinStateWords;
     const size_t states = (size_t)p->nch * (size_t)p->dstate * 4;
     // the state scan's own workspace comes first, so that its header (and
-    // timeout word) sits at offset 0 like every other call's
+    // timeout word) sits at offset 0 like every other call's; the chunk
+    // begin-count words follow its descriptors so one fill covers both
     size_t off = 0;
     p->off_scan = off;
     // the state scan always runs vectorised: dstate % 4 == 0 and every
     // buffer is 256-byte aligned inside the workspace
-    if (!plan_diag(1, p->nch, p->dstate, MEMOROID_F32, true, diag_rows(false, true), false, true, false, &p->scan)) return false;
+    if (!plan_diag(1, p->nch, p->dstate, MEMOROID_F32, true, diag_rows(false, true), false, true, false, &p->scan))
+        return false;
     off = align_up(off + p->scan.total);
+    p->off_cnt = off;
+    off = align_up(off + (size_t)p->nch * 8);
     p->off_dS = off;
     off = align_up(off + states);
     p->off_Sinc = off;
     off = align_up(off + states);
     p->off_R = off;
     off = align_up(off + (size_t)p->nch);
-    p->off_ones = off;
-    off = align_up(off + (size_t)p->dstate * 4);
-    p->off_counts = off;
-    off = align_up(off + (size_t)((T + kEpBlock - 1) / kEpBlock) * 4);
     p->total = off;
     return true;
 }
@@ -349,16 +347,24 @@ int memoroid_scan_linattn(const float* q, const float* k, const float* v, const 
     if (!aligned(workspace, 256)) return MEMOROID_EINVAL;
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
+    char* sw = ws + p.off_scan;
     float* dS = (float*)(ws + p.off_dS);
     float* Sinc = (float*)(ws + p.off_Sinc);
     uint8_t* R = (uint8_t*)(ws + p.off_R);
-    float* ones = (float*)(ws + p.off_ones);
-    char* sw = ws + p.off_scan;
-    if (fill_f32_launch(ones, p.dstate, 1.0f, s) != hipSuccess) return MEMOROID_EHIP;
-    if (linattn_summary_launch(k, v, start, dS, R, T, H, s) != hipSuccess) return MEMOROID_EHIP;
-    if (ws_init_launch(sw, sw + p.scan.off_agg, p.scan.fill_bytes, s) != hipSuccess) return MEMOROID_EHIP;
+    LinSummaryArgs sa{};
+    sa.k = k;
+    sa.v = v;
+    sa.start = start;
+    sa.dS = dS;
+    sa.R = R;
+    sa.T = T;
+    sa.H = H;
+    sa.hdr = (uint32_t*)sw;
+    sa.fill = (u32x4*)(sw + p.scan.off_agg);
+    sa.fill16 = (int64_t)((p.off_cnt + (size_t)p.nch * 8 - (p.off_scan + p.scan.off_agg) + 15) / 16);
+    if (linattn_summary_launch(sa, s) != hipSuccess) return MEMOROID_EHIP;
     DiagFwdArgs args{};
-    args.a = ones;
+    args.a = nullptr;            // a = 1: the state scan is a resettable sum
     args.x = dS;
     args.start = R;
     args.h = Sinc;
@@ -370,12 +376,22 @@ int memoroid_scan_linattn(const float* q, const float* k, const float* v, const 
     args.agg = sw + p.scan.off_agg;
     args.incl = sw + p.scan.off_incl;
     args.hdr = (WsHeader*)sw;
+    args.idx = nullptr;
+    args.cnt = nullptr;
     if (diag_fwd_launch(K_F32, K_F32, true, true, args, p.scan.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
-    if (linattn_output_launch(q, k, v, start, Sinc, out, T, H, s) != hipSuccess) return MEMOROID_EHIP;
-    if (episode_idx) {
-        if (episode_idx_launch(start, episode_idx, 1, T, (int32_t*)(ws + p.off_counts), s) != hipSuccess)
-            return MEMOROID_EHIP;
-    }
+    LinOutputArgs oa{};
+    oa.q = q;
+    oa.k = k;
+    oa.v = v;
+    oa.start = start;
+    oa.Sinc = Sinc;
+    oa.out = out;
+    oa.T = T;
+    oa.H = H;
+    oa.idx = episode_idx;
+    oa.cnt = (uint64_t*)(ws + p.off_cnt);
+    oa.timeout = &((WsHeader*)sw)->timeout;
+    if (linattn_output_launch(oa, s) != hipSuccess) return MEMOROID_EHIP;
     return MEMOROID_OK;
 }
 

@@ -113,10 +113,13 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     }
     S ainv[VEC];
     if constexpr (AINV) {
+        // a NULL time-invariant a stands for a = 1 (the sum monoid, used by
+        // the linear-attention state scan)
         RawVec<IN, VEC> r0;
-        if (active) raw_load(r0, (const char*)p.a + f0 * IB);
+        const bool have = active && p.a != nullptr;
+        if (have) raw_load(r0, (const char*)p.a + f0 * IB);
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) ainv[v] = active ? CIn::get(r0, v) : s_one<S>();
+        for (int v = 0; v < VEC; ++v) ainv[v] = have ? CIn::get(r0, v) : s_one<S>();
     }
     auto a_at = [&](int r, int v) -> S {
         if constexpr (AINV) return ainv[v];

@@ -7,15 +7,31 @@
 
 namespace memoroid {
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
 struct WsHeader;
 
 // Steps per lane held in registers by the diagonal scans (a tile is
 // 256 / Qp * rows steps long: 64 for full-width feature blocks).  The reverse
 // scan with a per-step a keeps three tensors per step (g, a, h) and so holds
 // fewer steps, to stay within 256 registers (two workgroups per CU).
-constexpr int kFwdRows = 16;
-constexpr int kBwdRows = 16;
-constexpr int kBwdRowsPerStepA = 12;
+#ifndef MEMOROID_FWD_ROWS
+#define MEMOROID_FWD_ROWS 16
+#endif
+#ifndef MEMOROID_BWD_ROWS
+#define MEMOROID_BWD_ROWS 16
+#endif
+#ifndef MEMOROID_BWD_ROWS_PER_STEP_A
+#define MEMOROID_BWD_ROWS_PER_STEP_A 12
+#endif
+#ifndef MEMOROID_CHAIN_ROW_BYTES
+#define MEMOROID_CHAIN_ROW_BYTES 128
+#endif
+constexpr int kFwdRows = MEMOROID_FWD_ROWS;
+constexpr int kBwdRows = MEMOROID_BWD_ROWS;
+constexpr int kBwdRowsPerStepA = MEMOROID_BWD_ROWS_PER_STEP_A;
+// Bytes of a feature row one chain covers (one 128-byte line by default).
+constexpr int64_t kChainRowBytes = MEMOROID_CHAIN_ROW_BYTES;
 constexpr int diag_rows(bool bwd, bool ainv) { return !bwd ? kFwdRows : (ainv ? kBwdRows : kBwdRowsPerStepA); }
 
 struct DiagFwdArgs {
@@ -69,20 +85,40 @@ hipError_t colsum_launch(const float* in, float* out, int64_t rows, int64_t cols
 // capture the call in a HIP graph.
 hipError_t ws_init_launch(void* hdr, void* p, size_t bytes, hipStream_t s);
 
-// Episode index of every step (begin steps at or before t, minus one).
-constexpr int kEpBlock = 4096;   // steps per workgroup
-hipError_t episode_idx_launch(const uint8_t* start, int32_t* idx, int64_t B, int64_t T,
-                              int32_t* counts, hipStream_t s);
-
 // Linear-attention memoroid: per-(chunk, head) state summaries, and outputs
 // from the scanned chunk states.  A state is S^T (64x64, row n holds column n
 // of S) followed by z (64), kLinStateWords floats.
 constexpr int kLinChunk = 64;
 constexpr int kLinStateWords = 64 * 64 + 64;
-hipError_t linattn_summary_launch(const float* k, const float* v, const uint8_t* start, float* dS,
-                                  uint8_t* R, int64_t T, int64_t H, hipStream_t s);
-hipError_t linattn_output_launch(const float* q, const float* k, const float* v, const uint8_t* start,
-                                 const float* Sinc, float* out, int64_t T, int64_t H, hipStream_t s);
-hipError_t fill_f32_launch(float* p, int64_t n, float value, hipStream_t s);
+
+struct LinSummaryArgs {
+    const float* k;
+    const float* v;
+    const uint8_t* start;
+    float* dS;          // [chunks][H][kLinStateWords]
+    uint8_t* R;         // [chunks] chunk holds a begin step
+    int64_t T;
+    int64_t H;
+    uint32_t* hdr;      // state-scan workspace header (zeroed here)
+    u32x4* fill;        // descriptors to fill with all-ones bytes (16-byte units)
+    int64_t fill16;
+};
+
+struct LinOutputArgs {
+    const float* q;
+    const float* k;
+    const float* v;
+    const uint8_t* start;
+    const float* Sinc;  // scanned states, [chunks][H][kLinStateWords]
+    float* out;
+    int64_t T;
+    int64_t H;
+    int32_t* idx;       // episode index out [T], or NULL
+    uint64_t* cnt;      // [chunks] begin-count words (filled by the summary kernel)
+    uint32_t* timeout;
+};
+
+hipError_t linattn_summary_launch(const LinSummaryArgs& a, hipStream_t s);
+hipError_t linattn_output_launch(const LinOutputArgs& a, hipStream_t s);
 
 }  // namespace memoroid

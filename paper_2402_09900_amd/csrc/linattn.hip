@@ -9,19 +9,23 @@
 //   summary kernel (one workgroup per chunk and head):
 //     dS^T = V^T phi(K)  over the rows after the chunk's last begin step
 //     dz   = column sums of those phi(K) rows;  R = "chunk holds a begin"
+//     (it also initialises the state scan's workspace);
 //   the chunk states are then scanned with the resettable diagonal scan
 //   (a = 1: the sum monoid), giving S_inc(c) = state after chunk c;
 //   output kernel (one workgroup per chunk and head), with r_i the last begin
 //   step <= i inside the chunk (-1 if none):
 //     A   = phi(Q) phi(K)^T,  masked to j <= i and j >= r_i
 //     num = A V + [r_i < 0] phi(Q) S_inc(c-1),  den = rowsum(A) + [r_i < 0] phi(Q).z
-//     out = num / den.
+//     out = num / den;
+//   the head-0 workgroups also produce the episode index of the chunk's steps.
 //
-// Contractions use v_mfma_f32_16x16x4_f32.  Operands are staged in LDS with
-// the contraction index contiguous, so one lane's 16 k-values of a fragment
-// come from four 16-byte LDS reads; within one MFMA the four k-slots of the
-// instruction take k = 16*slot + s, a permutation of the contraction index
-// applied identically to both operands.
+// Contractions use v_mfma_f32_16x16x4_f32 on operands staged in LDS in their
+// natural (row-major) layout.  In one MFMA the four k-slots take k = 16*slot
+// + s, a permutation of the contraction index applied to both operands, so
+// an operand stored with k contiguous is read with 16-byte LDS loads; one
+// stored with k as its row index is read with 4-byte loads whose rows are
+// rotated by 16 columns per 16 rows, which spreads the four k-slots over
+// different LDS banks.
 #include "scan_common.hpp"
 #include "kernels.hpp"
 
@@ -29,20 +33,54 @@ namespace memoroid {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kC = 64;            // chunk length (steps) and head width
-constexpr int kLD = 68;           // LDS row stride in floats (16-byte aligned rows)
+constexpr int kC = 64;                      // chunk length (steps) and head width
+constexpr int kLD = 68;                     // LDS row stride in floats (16-byte aligned rows)
 constexpr int kStateWords = kC * kC + kC;   // S^T (64x64) followed by z (64)
 
-__device__ __forceinline__ float phi(float u) { return u > 0.0f ? u + 1.0f : expf(u); }
+// phi(u) = 1 + ELU(u): u + 1 for u > 0, exp(u) otherwise.  exp uses the
+// hardware base-2 exponential (relative error a few ulp, far inside the fp32
+// tolerance of the readout).
+__device__ __forceinline__ float phi(float u) { return u > 0.0f ? u + 1.0f : __expf(u); }
 
-// Stage rows [0, 64) of one chunk of a [T][H][64] tensor into LDS, applying
-// phi if requested; rows outside [lo, hi) are written as zeros (a select, so
-// non-finite values in excluded rows never enter).  TRANS stores element
-// (row, col) at s[col * kLD + row], otherwise at s[row * kLD + col].
-// Returns nonzero if a staged value is not finite.
-template <bool PHI, bool TRANS>
-__device__ __forceinline__ int stage(float* s, const float* src, int64_t t0, int64_t H, int64_t h,
-                                     int lo, int hi) {
+// column of element (row, col) in a rotated buffer
+__device__ __forceinline__ int rot_col(int row, int col) { return (col + 16 * (row >> 4)) & (kC - 1); }
+
+// Fetch one chunk of a [T][H][64] tensor into registers (4 float4 per
+// thread, rows outside [lo, hi) as zeros) and write it to LDS later with
+// store_rows; returns nonzero if a value is not finite.
+__device__ __forceinline__ int fetch_rows(f32x4 (&v)[4], const float* src, int64_t t0, int64_t H, int64_t h, int lo,
+                                          int hi) {
+    int bad = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int f = threadIdx.x + 256 * u;
+        const int row = f >> 4, c4 = (f & 15) * 4;
+        v[u] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        if (row >= lo && row < hi) {
+            v[u] = *(const f32x4*)(src + ((t0 + row) * H + h) * kC + c4);
+            bad |= !(__builtin_isfinite(v[u].x) && __builtin_isfinite(v[u].y) && __builtin_isfinite(v[u].z) &&
+                     __builtin_isfinite(v[u].w));
+        }
+    }
+    return bad;
+}
+
+template <bool ROT>
+__device__ __forceinline__ void store_rows(float* s, const f32x4 (&v)[4]) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int f = threadIdx.x + 256 * u;
+        const int row = f >> 4, c4 = (f & 15) * 4;
+        *(f32x4*)(s + row * kLD + (ROT ? rot_col(row, c4) : c4)) = v[u];
+    }
+}
+
+// Stage one chunk (64 rows) of a [T][H][64] tensor into LDS, row-major,
+// applying phi if requested; rows outside [lo, hi) are written as zeros (a
+// select, so non-finite values in excluded rows never enter).  ROT rotates
+// each row as rot_col does.  Returns nonzero if a staged value is not finite.
+template <bool PHI, bool ROT>
+__device__ __forceinline__ int stage(float* s, const float* src, int64_t t0, int64_t H, int64_t h, int lo, int hi) {
     int bad = 0;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -57,38 +95,45 @@ __device__ __forceinline__ int stage(float* s, const float* src, int64_t t0, int
             bad |= !(__builtin_isfinite(v.x) && __builtin_isfinite(v.y) && __builtin_isfinite(v.z) &&
                      __builtin_isfinite(v.w));
         }
-        if (TRANS) {
-            s[(c4 + 0) * kLD + row] = v.x;
-            s[(c4 + 1) * kLD + row] = v.y;
-            s[(c4 + 2) * kLD + row] = v.z;
-            s[(c4 + 3) * kLD + row] = v.w;
-        } else {
-            *(f32x4*)(s + row * kLD + c4) = v;
-        }
+        *(f32x4*)(s + row * kLD + (ROT ? rot_col(row, c4) : c4)) = v;
     }
     return bad;
 }
 
-// C = A * Bt^T for 64x64 LDS tiles: A[i][k] = sA[i*kLD + k], Bt[j][k] =
-// sBt[j*kLD + k].  Wave w computes rows 16w .. 16w+15; on return
-// acc[jt][r] = C[16w + 4*(lane/16) + r][16*jt + lane%16].
-__device__ __forceinline__ void mfma_64x64x64(const float* sA, const float* sBt, f32x4 acc[4]) {
+// acc += A * B for 64x64 LDS tiles.  Wave w computes rows 16w .. 16w+15; on
+// return acc[jt][r] = C[16w + 4*(lane/16) + r][16*jt + lane%16].
+//   A_ROWS: A[i][k] = sA[i*kLD + k]          else A[i][k] = sA[k*kLD + rot_col(k, i)]
+//   B_ROWS: B[k][j] = sB[j*kLD + k]          else B[k][j] = sB[k*kLD + rot_col(k, j)]
+template <bool A_ROWS, bool B_ROWS>
+__device__ __forceinline__ void mfma_64x64x64(const float* sA, const float* sB, f32x4 acc[4]) {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int i = 16 * w + (lane & 15), kk = (lane >> 4) * 16;
     float af[16];
+    if constexpr (A_ROWS) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const f32x4 v = *(const f32x4*)(sA + i * kLD + kk + 4 * u);
-        af[4 * u] = v.x; af[4 * u + 1] = v.y; af[4 * u + 2] = v.z; af[4 * u + 3] = v.w;
+        for (int u = 0; u < 4; ++u) {
+            const f32x4 v = *(const f32x4*)(sA + i * kLD + kk + 4 * u);
+            af[4 * u] = v.x; af[4 * u + 1] = v.y; af[4 * u + 2] = v.z; af[4 * u + 3] = v.w;
+        }
+    } else {
+        const int c = rot_col(kk, i);            // (kk + s) >> 4 == kk >> 4 for s < 16
+#pragma unroll
+        for (int s = 0; s < 16; ++s) af[s] = sA[(kk + s) * kLD + c];
     }
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) {
         const int j = 16 * jt + (lane & 15);
         float bf[16];
+        if constexpr (B_ROWS) {
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const f32x4 v = *(const f32x4*)(sBt + j * kLD + kk + 4 * u);
-            bf[4 * u] = v.x; bf[4 * u + 1] = v.y; bf[4 * u + 2] = v.z; bf[4 * u + 3] = v.w;
+            for (int u = 0; u < 4; ++u) {
+                const f32x4 v = *(const f32x4*)(sB + j * kLD + kk + 4 * u);
+                bf[4 * u] = v.x; bf[4 * u + 1] = v.y; bf[4 * u + 2] = v.z; bf[4 * u + 3] = v.w;
+            }
+        } else {
+            const int c = rot_col(kk, j);
+#pragma unroll
+            for (int s = 0; s < 16; ++s) bf[s] = sB[(kk + s) * kLD + c];
         }
 #pragma unroll
         for (int s = 0; s < 16; ++s) acc[jt] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[s], bf[s], acc[jt], 0, 0, 0);
@@ -97,35 +142,51 @@ __device__ __forceinline__ void mfma_64x64x64(const float* sA, const float* sBt,
 
 __device__ __forceinline__ bool is_begin(const uint8_t* st, int64_t t) { return t == 0 || st[t] != 0; }
 
+// sum over the 16 lanes that share lane / 16
+__device__ __forceinline__ float sum16(float v) {
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
 // ---------------------------------------------------------------- summaries
 
-__global__ __launch_bounds__(256) void linattn_summary_kernel(const float* __restrict__ k,
-                                                              const float* __restrict__ v,
-                                                              const uint8_t* __restrict__ start,
-                                                              float* __restrict__ dS, uint8_t* __restrict__ R,
-                                                              int64_t T, int64_t H) {
-    __shared__ __attribute__((aligned(16))) float sKt[kC * kLD];
-    __shared__ __attribute__((aligned(16))) float sVt[kC * kLD];
+__global__ __launch_bounds__(256) void linattn_summary_kernel(LinSummaryArgs p) {
+    __shared__ __attribute__((aligned(16))) float sK[kC * kLD];   // phi(K), rotated
+    __shared__ __attribute__((aligned(16))) float sV[kC * kLD];   // V, rotated
     __shared__ int s_last;
     const int64_t c = blockIdx.x, h = blockIdx.y;
     const int64_t t0 = c * kC;
-    const int nvalid = (int)(T - t0 < kC ? T - t0 : kC);
+    const int nvalid = (int)(p.T - t0 < kC ? p.T - t0 : kC);
+
+    // workspace of the state scan and of the episode-index count words: the
+    // header is zeroed and the descriptors filled with all-ones bytes here,
+    // so that the later kernels find them initialised (stream order)
+    {
+        const int64_t nblk = (int64_t)gridDim.x * gridDim.y;
+        const int64_t gid = (int64_t)(blockIdx.y * gridDim.x + blockIdx.x) * 256 + threadIdx.x;
+        if (gid < 64) p.hdr[gid] = 0u;
+        const u32x4 ones = {kEmpty32, kEmpty32, kEmpty32, kEmpty32};
+        for (int64_t i = gid; i < p.fill16; i += nblk * 256) p.fill[i] = ones;
+    }
+
     if (threadIdx.x == 0) s_last = -1;
     __syncthreads();
-    if ((int)threadIdx.x < nvalid && is_begin(start, t0 + threadIdx.x)) atomicMax(&s_last, (int)threadIdx.x);
+    if ((int)threadIdx.x < nvalid && is_begin(p.start, t0 + threadIdx.x)) atomicMax(&s_last, (int)threadIdx.x);
     __syncthreads();
     const int last = s_last;
     const int lo = last > 0 ? last : 0;
-    stage<true, true>(sKt, k, t0, H, h, lo, nvalid);
-    stage<false, true>(sVt, v, t0, H, h, lo, nvalid);
+    stage<true, true>(sK, p.k, t0, p.H, h, lo, nvalid);
+    stage<false, true>(sV, p.v, t0, p.H, h, lo, nvalid);
     __syncthreads();
 
     f32x4 acc[4];
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) acc[jt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    mfma_64x64x64(sVt, sKt, acc);   // C[n][kd] = sum_j V[j][n] phi(K)[j][kd] = dS^T
+    // C[n][kd] = sum_j V[j][n] phi(K)[j][kd] = dS^T: A = V^T, B = phi(K), both k-major
+    mfma_64x64x64<false, false>(sV, sK, acc);
 
-    float* out = dS + (c * H + h) * kStateWords;
+    float* out = p.dS + (c * p.H + h) * kStateWords;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) {
@@ -138,38 +199,44 @@ __global__ __launch_bounds__(256) void linattn_summary_kernel(const float* __res
     }
     if (threadIdx.x < kC) {
         float z = 0.0f;
-        for (int j = 0; j < kC; ++j) z += sKt[threadIdx.x * kLD + j];
+        for (int j = 0; j < kC; ++j) z += sK[j * kLD + rot_col(j, threadIdx.x)];
         out[kC * kC + threadIdx.x] = z;
     }
-    if (h == 0 && threadIdx.x == 0) R[c] = last >= 0 ? 1 : 0;
+    if (h == 0 && threadIdx.x == 0) p.R[c] = last >= 0 ? 1 : 0;
 }
 
 // ------------------------------------------------------------------- output
 
-__global__ __launch_bounds__(256) void linattn_output_kernel(const float* __restrict__ q,
-                                                             const float* __restrict__ k,
-                                                             const float* __restrict__ v,
-                                                             const uint8_t* __restrict__ start,
-                                                             const float* __restrict__ Sinc,
-                                                             float* __restrict__ out, int64_t T, int64_t H) {
-    __shared__ __attribute__((aligned(16))) float sQ[kC * kLD];   // phi(Q), later V^T
-    __shared__ __attribute__((aligned(16))) float sK[kC * kLD];   // phi(K), later masked A
-    __shared__ __attribute__((aligned(16))) float sS[kC * kLD];   // S_in^T
-    __shared__ float sZ[kC], sQZ[kC], sDen[kC];
-    __shared__ int sR[kC];
-    __shared__ uint8_t sBeg[kC];
-    __shared__ int s_bad;
+__global__ __launch_bounds__(256) void linattn_output_kernel(LinOutputArgs p) {
+    __shared__ __attribute__((aligned(16))) float sQ[kC * kLD];   // phi(Q)
+    __shared__ __attribute__((aligned(16))) float sK[kC * kLD];   // phi(K), later the masked A
+    __shared__ __attribute__((aligned(16))) float sS[kC * kLD];   // S_in^T, later V (rotated)
+    __shared__ float sZ[kC];
+    float* const sV = sS;
 
     const int64_t c = blockIdx.x, h = blockIdx.y;
     const int64_t t0 = c * kC;
-    const int nvalid = (int)(T - t0 < kC ? T - t0 : kC);
-    const int tid = threadIdx.x;
-    if (tid < kC) sBeg[tid] = tid < nvalid && is_begin(start, t0 + tid);
-    if (tid == 0) s_bad = 0;
-    stage<true, false>(sQ, q, t0, H, h, 0, nvalid);
-    stage<true, false>(sK, k, t0, H, h, 0, nvalid);
+    const int nvalid = (int)(p.T - t0 < kC ? p.T - t0 : kC);
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+
+    // row `lane` of the chunk: begin flag, and the last begin at or before it
+    // (an inclusive max-scan across the wavefront; every wavefront has all 64)
+    const bool beg = lane < nvalid && is_begin(p.start, t0 + lane);
+    int rmax = beg ? lane : -1;
+#pragma unroll
+    for (int k = 1; k < 64; k <<= 1) {
+        const int o = __shfl_up(rmax, k, 64);
+        if (lane >= k) rmax = rmax > o ? rmax : o;
+    }
+
+    // V is fetched now (its loads overlap the first contractions) and moved
+    // into the S buffer once S has been used
+    f32x4 vreg[4];
+    const int bad = fetch_rows(vreg, p.v, t0, p.H, h, 0, nvalid);
+    stage<true, false>(sQ, p.q, t0, p.H, h, 0, nvalid);
+    stage<true, false>(sK, p.k, t0, p.H, h, 0, nvalid);
     if (c > 0) {
-        const float* src = Sinc + ((c - 1) * H + h) * kStateWords;
+        const float* src = p.Sinc + ((c - 1) * p.H + h) * kStateWords;
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             const int f = tid + 256 * u;
@@ -186,73 +253,88 @@ __global__ __launch_bounds__(256) void linattn_output_kernel(const float* __rest
         }
         if (tid < kC) sZ[tid] = 0.0f;
     }
-    __syncthreads();
+    const bool nonfinite_v = __syncthreads_or(bad) != 0;
 
-    if (tid < kC) {
-        int r = -1;
-        for (int j = tid; j >= 0; --j)
-            if (sBeg[j]) { r = j; break; }
-        sR[tid] = r;
-        float qz = 0.0f;
-        for (int kd = 0; kd < kC; ++kd) qz += sQ[tid * kLD + kd] * sZ[kd];
-        sQZ[tid] = qz;
+    // episode index of the chunk's steps (head-0 workgroups): wavefront 2
+    // publishes the chunk's own begin count at once, wavefront 1 looks back
+    // for the count before the chunk, publishes the running count and writes
+    // the indices (publishing and polling use different wavefronts)
+    if (p.idx != nullptr && h == 0 && (w == 1 || w == 2)) {
+        const uint64_t m = __ballot(beg);
+        const uint32_t c_chunk = (uint32_t)__builtin_popcountll(m);
+        if (w == 2) {
+            if (lane == 0) publish64(p.cnt + c, (c == 0 ? kCountIncl : kCountOwn) | c_chunk);
+        } else {
+            const uint32_t before = c == 0 ? 0u : count_lookback(p.cnt, c - 1, 1, p.timeout);
+            if (lane == 0 && c > 0) publish64(p.cnt + c, kCountIncl | (before + c_chunk));
+            const uint32_t upto = (uint32_t)__builtin_popcountll(m & ((2ull << lane) - 1ull));
+            if (lane < nvalid) p.idx[t0 + lane] = (int32_t)(before + upto) - 1;
+        }
     }
+
     f32x4 accA[4], accS[4];
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) {
         accA[jt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
         accS[jt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     }
-    mfma_64x64x64(sQ, sK, accA);    // A[i][j]   = phi(q_i) . phi(k_j)
-    mfma_64x64x64(sQ, sS, accS);    // QS[i][n]  = sum_kd phi(q_i)[kd] S_in[kd][n]
-    __syncthreads();
+    mfma_64x64x64<true, true>(sQ, sK, accA);    // A[i][j]  = phi(q_i) . phi(k_j)
+    mfma_64x64x64<true, true>(sQ, sS, accS);    // QS[i][n] = sum_kd phi(q_i)[kd] S_in[kd][n]
 
-    const int lane = tid & 63, w = tid >> 6;
-    // masked A into sK (select: excluded entries are exact zeros)
+    // mask A to each row's episode (a select: excluded entries are exact
+    // zeros), then the row sums and phi(q_i).z_in, reduced across lanes
+    int ri[4];
+    float den[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int i = 16 * w + 4 * (lane >> 4) + r;
+        ri[r] = __shfl(rmax, i, 64);
+        float rs = 0.0f;
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt) {
+            const int j = 16 * jt + (lane & 15);
+            const bool keep = i < nvalid && j <= i && j >= (ri[r] > 0 ? ri[r] : 0);
+            accA[jt][r] = keep ? accA[jt][r] : 0.0f;
+            rs += accA[jt][r];
+        }
+        const int kd = 4 * (lane & 15);
+        const f32x4 qv = *(const f32x4*)(sQ + i * kLD + kd);
+        float qz = qv.x * sZ[kd] + qv.y * sZ[kd + 1] + qv.z * sZ[kd + 2] + qv.w * sZ[kd + 3];
+        rs = sum16(rs);
+        qz = sum16(qz);
+        den[r] = rs + (ri[r] < 0 ? qz : 0.0f);
+    }
+    __syncthreads();                            // every wavefront is done with sK and sS
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int i = 16 * w + 4 * (lane >> 4) + r;
-            const int j = 16 * jt + (lane & 15);
-            const int ri = sR[i];
-            const bool keep = i < nvalid && j <= i && j >= (ri > 0 ? ri : 0);
-            sK[i * kLD + j] = keep ? accA[jt][r] : 0.0f;
-        }
+        for (int r = 0; r < 4; ++r) sK[(16 * w + 4 * (lane >> 4) + r) * kLD + 16 * jt + (lane & 15)] = accA[jt][r];
     }
-    const int bad = stage<false, true>(sQ, v, t0, H, h, 0, nvalid);   // V^T
-    if (bad) atomicOr(&s_bad, 1);
+    store_rows<true>(sV, vreg);
     __syncthreads();
 
-    if (tid < kC) {
-        float den = 0.0f;
-        for (int j = 0; j < kC; ++j) den += sK[tid * kLD + j];
-        sDen[tid] = den + (sR[tid] < 0 ? sQZ[tid] : 0.0f);
-    }
     f32x4 accO[4];
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) accO[jt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    const bool nonfinite_v = s_bad != 0;
     if (!nonfinite_v) {
-        mfma_64x64x64(sK, sQ, accO);    // num[i][n] = sum_j Am[i][j] V[j][n]
+        mfma_64x64x64<true, false>(sK, sV, accO);    // num[i][n] = sum_j A[i][j] V[j][n]
     } else {
         // A non-finite value in V would reach other episodes of this chunk
-        // through the dense product (0 * NaN = NaN); sum only each row's own
-        // episode instead.
+        // through the dense product (0 * NaN = NaN); sum each row's own
+        // episode explicitly instead.
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int i = 16 * w + 4 * (lane >> 4) + r;
                 const int n = 16 * jt + (lane & 15);
-                const int ri = sR[i];
                 float s = 0.0f;
-                for (int j = (ri > 0 ? ri : 0); j <= i && j < nvalid; ++j) s += sK[i * kLD + j] * sQ[n * kLD + j];
+                for (int j = (ri[r] > 0 ? ri[r] : 0); j <= i && j < nvalid; ++j)
+                    s += sK[i * kLD + j] * sV[j * kLD + rot_col(j, n)];
                 accO[jt][r] = s;
             }
         }
     }
-    __syncthreads();
 
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) {
@@ -261,40 +343,24 @@ __global__ __launch_bounds__(256) void linattn_output_kernel(const float* __rest
             const int i = 16 * w + 4 * (lane >> 4) + r;
             const int n = 16 * jt + (lane & 15);
             if (i < nvalid) {
-                const float num = accO[jt][r] + (sR[i] < 0 ? accS[jt][r] : 0.0f);
-                out[((t0 + i) * H + h) * kC + n] = num / sDen[i];
+                const float num = accO[jt][r] + (ri[r] < 0 ? accS[jt][r] : 0.0f);
+                p.out[((t0 + i) * p.H + h) * kC + n] = num / den[r];
             }
         }
     }
 }
 
-__global__ __launch_bounds__(256) void fill_f32_kernel(float* p, int64_t n, float value) {
-    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) p[i] = value;
-}
-
 // ------------------------------------------------------------------ launch
 
-hipError_t linattn_summary_launch(const float* k, const float* v, const uint8_t* start, float* dS, uint8_t* R,
-                                  int64_t T, int64_t H, hipStream_t s) {
-    const int64_t nch = (T + kC - 1) / kC;
-    hipLaunchKernelGGL(linattn_summary_kernel, dim3((unsigned)nch, (unsigned)H), dim3(256), 0, s, k, v, start, dS,
-                       R, T, H);
+hipError_t linattn_summary_launch(const LinSummaryArgs& a, hipStream_t s) {
+    const int64_t nch = (a.T + kC - 1) / kC;
+    hipLaunchKernelGGL(linattn_summary_kernel, dim3((unsigned)nch, (unsigned)a.H), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
-hipError_t linattn_output_launch(const float* q, const float* k, const float* v, const uint8_t* start,
-                                 const float* Sinc, float* out, int64_t T, int64_t H, hipStream_t s) {
-    const int64_t nch = (T + kC - 1) / kC;
-    hipLaunchKernelGGL(linattn_output_kernel, dim3((unsigned)nch, (unsigned)H), dim3(256), 0, s, q, k, v, start,
-                       Sinc, out, T, H);
-    return hipGetLastError();
-}
-
-hipError_t fill_f32_launch(float* p, int64_t n, float value, hipStream_t s) {
-    int64_t blocks = (n + 255) / 256;
-    if (blocks > 4096) blocks = 4096;
-    if (blocks < 1) blocks = 1;
-    hipLaunchKernelGGL(fill_f32_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p, n, value);
+hipError_t linattn_output_launch(const LinOutputArgs& a, hipStream_t s) {
+    const int64_t nch = (a.T + kC - 1) / kC;
+    hipLaunchKernelGGL(linattn_output_kernel, dim3((unsigned)nch, (unsigned)a.H), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
