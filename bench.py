@@ -16,6 +16,10 @@ Workloads (seeded, synthetic; laws in paper_2402_09900_amd.tapes):
   4  diag real, 64 tapes x T=16384, d=512, bf16 in / fp32 state / bf16 out
   5  diag real f32, T=1048576, d=256, lognormal(5, 1.5) episodes, forward + reverse
 
+Every buffer exists in several copies (at least 1 GiB cycled, at least 3) and
+step i uses copy i mod n, so inputs are read from HBM rather than from the
+256 MB last-level cache left warm by the previous step.
+
 value = tape timesteps x features per second of the whole step (B*T*d, or
 T*H*dv for linear attention).  roofline: the dominant kernel's algorithmic
 bytes (or flops) per launch over its average launch time, measured here with
@@ -78,71 +82,89 @@ def dev_tensor(torch, arr, kind):
     return torch.from_numpy(arr).cuda()
 
 
+def n_sets(set_bytes):
+    """Copies of every buffer to rotate through, so that a step does not find
+    its inputs in the 256 MB last-level cache (MALL) from an earlier step:
+    enough copies to cycle over at least 1 GiB, at least 3, at most 16."""
+    need = -(-(1 << 30) // max(int(set_bytes), 1))
+    return int(min(16, max(3, need)))
+
+
 def setup_diag(torch, mb, tapes, key):
     w = tapes.make_diag(key)
     kind = w.dtype
     code = {"f32": mb.F32, "bf16": mb.BF16, "c64": mb.C64}
     tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "c64": torch.complex64}
-    a, x, s = dev_tensor(torch, w.a, kind), dev_tensor(torch, w.x, kind), dev_tensor(torch, w.start, "u8")
-    B, T, d = w.B, w.T, w.d
-    h = torch.empty((B, T, d), dtype=tdt[w.out_dtype], device="cuda")
-    idx = torch.empty((B, T), dtype=torch.int32, device="cuda")
-    stride = 0 if w.a_invariant else d
-    nb = mb.memoroid_scan_diag_workspace_bytes(B, T, d, code[kind], code[w.out_dtype])
-    ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
     ebytes = {"f32": 4, "bf16": 2, "c64": 8}
+    B, T, d = w.B, w.T, w.d
     n = B * T * d
+    stride = 0 if w.a_invariant else d
     a_bytes = (d if w.a_invariant else n) * ebytes[kind]
-    calls = {}
-    bytes_per = {}
-    stream = lambda: torch.cuda.current_stream().cuda_stream  # noqa: E731
-
-    def fwd():
-        st = mb.memoroid_scan_diag(a.data_ptr(), stride, x.data_ptr(), s.data_ptr(), h.data_ptr(), idx.data_ptr(),
-                                   B, T, d, code[kind], code[w.out_dtype], ws.data_ptr(), ws.numel(), stream())
-        assert st == 0, mb.status_string(st)
-    calls["fwd"] = fwd
-    bytes_per["fwd"] = a_bytes + n * ebytes[kind] + n * ebytes[w.out_dtype] + B * T * (1 + 4)
+    nb = mb.memoroid_scan_diag_workspace_bytes(B, T, d, code[kind], code[w.out_dtype])
+    nbb = mb.memoroid_scan_diag_bwd_workspace_bytes(B, T, d, code[kind], stride) if w.g is not None else 0
+    da_bytes = (d if w.a_invariant else n) * ebytes[kind]
+    set_bytes = a_bytes + n * ebytes[kind] + n * ebytes[w.out_dtype] + B * T * 5 + nb
     if w.g is not None:
-        g = dev_tensor(torch, w.g, kind)
-        hb = h if w.out_dtype == kind else h.to(tdt[kind])
-        gx = torch.empty_like(g)
-        ga = torch.empty((d,) if w.a_invariant else (B, T, d), dtype=tdt[kind], device="cuda")
-        nbb = mb.memoroid_scan_diag_bwd_workspace_bytes(B, T, d, code[kind], stride)
-        wsb = torch.empty(nbb, dtype=torch.uint8, device="cuda")
+        set_bytes += 2 * n * ebytes[kind] + da_bytes + nbb
+    stream = lambda: torch.cuda.current_stream().cuda_stream  # noqa: E731
+    sets = []
+    for _ in range(n_sets(set_bytes)):
+        a, x, s = dev_tensor(torch, w.a, kind), dev_tensor(torch, w.x, kind), dev_tensor(torch, w.start, "u8")
+        h = torch.empty((B, T, d), dtype=tdt[w.out_dtype], device="cuda")
+        idx = torch.empty((B, T), dtype=torch.int32, device="cuda")
+        ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+        calls = {}
 
-        def bwd():
-            st = mb.memoroid_scan_diag_bwd(a.data_ptr(), stride, s.data_ptr(), hb.data_ptr(), g.data_ptr(),
-                                           gx.data_ptr(), ga.data_ptr(), B, T, d, code[kind], wsb.data_ptr(),
-                                           wsb.numel(), stream())
+        def fwd(a=a, x=x, s=s, h=h, idx=idx, ws=ws):
+            st = mb.memoroid_scan_diag(a.data_ptr(), stride, x.data_ptr(), s.data_ptr(), h.data_ptr(),
+                                       idx.data_ptr(), B, T, d, code[kind], code[w.out_dtype], ws.data_ptr(),
+                                       ws.numel(), stream())
             assert st == 0, mb.status_string(st)
-        calls["bwd"] = bwd
+        calls["fwd"] = fwd
+        if w.g is not None:
+            g = dev_tensor(torch, w.g, kind)
+            hb = h if w.out_dtype == kind else h.to(tdt[kind])
+            gx = torch.empty_like(g)
+            ga = torch.empty((d,) if w.a_invariant else (B, T, d), dtype=tdt[kind], device="cuda")
+            wsb = torch.empty(nbb, dtype=torch.uint8, device="cuda")
+
+            def bwd(a=a, s=s, hb=hb, g=g, gx=gx, ga=ga, wsb=wsb):
+                st = mb.memoroid_scan_diag_bwd(a.data_ptr(), stride, s.data_ptr(), hb.data_ptr(), g.data_ptr(),
+                                               gx.data_ptr(), ga.data_ptr(), B, T, d, code[kind], wsb.data_ptr(),
+                                               wsb.numel(), stream())
+                assert st == 0, mb.status_string(st)
+            calls["bwd"] = bwd
+        sets.append(calls)
+    bytes_per = {"fwd": a_bytes + n * ebytes[kind] + n * ebytes[w.out_dtype] + B * T * (1 + 4)}
+    if w.g is not None:
         # read a_{t+1}, g, h_{t-1}; write dx, da (da per step, or [d])
-        da_bytes = (d if w.a_invariant else n) * ebytes[kind]
         bytes_per["bwd"] = a_bytes + 3 * n * ebytes[kind] + da_bytes + B * T
-    return w, calls, bytes_per, n
+    return w, sets, bytes_per, n
 
 
 def setup_linattn(torch, mb, tapes):
     la = tapes.make_linattn()
-    q, k, v = (dev_tensor(torch, t, "f32") for t in (la.q, la.k, la.v))
-    s = dev_tensor(torch, la.start, "u8")
-    out = torch.empty_like(v)
-    idx = torch.empty((la.T,), dtype=torch.int32, device="cuda")
-    nb = mb.memoroid_scan_linattn_workspace_bytes(la.T, la.H, 64, 64, 64)
-    ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
-
-    def fwd():
-        st = mb.memoroid_scan_linattn(q.data_ptr(), k.data_ptr(), v.data_ptr(), s.data_ptr(), out.data_ptr(),
-                                      idx.data_ptr(), la.T, la.H, 64, 64, 64, ws.data_ptr(), ws.numel(),
-                                      torch.cuda.current_stream().cuda_stream)
-        assert st == 0, mb.status_string(st)
     n = la.T * la.H * la.dv
+    nb = mb.memoroid_scan_linattn_workspace_bytes(la.T, la.H, 64, 64, 64)
+    sets = []
+    for _ in range(n_sets(4 * n * 4 + la.T * 5 + nb)):
+        q, k, v = (dev_tensor(torch, t, "f32") for t in (la.q, la.k, la.v))
+        s = dev_tensor(torch, la.start, "u8")
+        out = torch.empty_like(v)
+        idx = torch.empty((la.T,), dtype=torch.int32, device="cuda")
+        ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+
+        def fwd(q=q, k=k, v=v, s=s, out=out, idx=idx, ws=ws):
+            st = mb.memoroid_scan_linattn(q.data_ptr(), k.data_ptr(), v.data_ptr(), s.data_ptr(), out.data_ptr(),
+                                          idx.data_ptr(), la.T, la.H, 64, 64, 64, ws.data_ptr(), ws.numel(),
+                                          torch.cuda.current_stream().cuda_stream)
+            assert st == 0, mb.status_string(st)
+        sets.append({"fwd": fwd})
     # algorithmic: q, k, v read and out written once (4 B each), flags, idx
     bytes_per = {"fwd": 4 * n * 4 + la.T * 5}
     # chunked-dense flops: 4 contractions of 2*64^3 per (chunk, head)
     flops = 4 * 2 * 64 ** 3 * (la.T // 64) * la.H
-    return la, {"fwd": fwd}, bytes_per, n, flops
+    return la, sets, bytes_per, n, flops
 
 
 def kernel_source_hash():
@@ -219,9 +241,10 @@ def main():
     wl = tapes.WORKLOADS[key]
     flops = None
     if wl.kind == "linattn":
-        w, calls, bytes_per, n, flops = setup_linattn(torch, mb, tapes)
+        w, sets, bytes_per, n, flops = setup_linattn(torch, mb, tapes)
     else:
-        w, calls, bytes_per, n = setup_diag(torch, mb, tapes, key)
+        w, sets, bytes_per, n = setup_diag(torch, mb, tapes, key)
+    calls = sets[0]
     timers = {name: Timer(torch) for name in calls}
 
     # calibration anchor for hardware byte counters: one plain device copy of
@@ -232,19 +255,19 @@ def main():
     torch.cuda.synchronize()
     del cal_src, cal_dst
 
-    def step(timed):
-        for name, fn in calls.items():
+    def step(i, timed):
+        for name, fn in sets[i % len(sets)].items():
             if timed:
                 timers[name](fn)
             else:
                 fn()
 
-    for _ in range(args.warmup):
-        step(False)
+    for i in range(args.warmup):
+        step(i, False)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step(True)
+    for i in range(args.steps):
+        step(args.warmup + i, True)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / max(args.steps, 1)
@@ -285,6 +308,7 @@ def main():
         "config": {"workload": wl.name, "B": wl.B, "T": wl.T,
                    ("heads" if wl.kind == "linattn" else "d"): wl.d,
                    "passes": list(calls.keys()),
+                   "buffer_sets": len(sets),
                    "ms_per_call": {k: round(v, 4) for k, v in per_call_ms.items()},
                    "GBps_per_call": {k: round(bytes_per[k] / (per_call_ms[k] * 1e-3) / 1e9, 1)
                                      for k in calls}},

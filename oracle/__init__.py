@@ -52,8 +52,12 @@ def _load():
         lib.oracle_phi.argtypes = [ctypes.c_double]
         lib.oracle_phi.restype = ctypes.c_double
         lib.oracle_linattn.argtypes = [P, P, P, P, I64, I64, I64, I64, P, P]
+        D = ctypes.c_double
+        lib.oracle_discounted_return.argtypes = [P, P, D, I64, I64, P, P]
+        lib.oracle_gae.argtypes = [P, P, P, P, P, D, D, I64, I64, P, P, P, P]
         for name in ("oracle_episode_idx", "oracle_diag_fwd", "oracle_diag_fwd_c",
-                     "oracle_diag_bwd", "oracle_diag_bwd_c", "oracle_linattn"):
+                     "oracle_diag_bwd", "oracle_diag_bwd_c", "oracle_linattn",
+                     "oracle_discounted_return", "oracle_gae"):
             getattr(lib, name).restype = None
         _lib = lib
     return _lib
@@ -153,3 +157,41 @@ def linattn(q, k, v, start):
     _load().oracle_linattn(_ptr(q), _ptr(k), _ptr(v), _ptr(s), T, H, dk, dv,
                            _ptr(out), _ptr(m))
     return out, m
+
+
+def _tape2(x, B=None, T=None):
+    x = np.asarray(x)
+    x2 = x.reshape(1, -1) if x.ndim == 1 else x
+    return np.ascontiguousarray(x2, dtype=np.float64)
+
+
+def discounted_return(r, start, gamma):
+    """G_t = discounted sum of rewards to the end of t's episode.
+
+    r, start: [B,T] (or [T]).  Returns (G, m) shaped like r."""
+    shape = np.shape(r)
+    r2 = _tape2(r)
+    B, T = r2.shape
+    s = _flags(start, B, T)
+    G = np.empty((B, T), dtype=np.float64)
+    m = np.empty((B, T), dtype=np.float64)
+    _load().oracle_discounted_return(_ptr(r2), _ptr(s), float(gamma), B, T, _ptr(G), _ptr(m))
+    return G.reshape(shape), m.reshape(shape)
+
+
+def gae(r, v, start, gamma, lam, vn=None, done=None):
+    """Generalized advantage estimate over a tape.
+
+    r, v, start (and vn, done if given): [B,T] (or [T]).  Returns
+    (adv, target, m_adv, m_target) shaped like r; target = adv + v."""
+    shape = np.shape(r)
+    r2 = _tape2(r)
+    B, T = r2.shape
+    v2 = _tape2(v).reshape(B, T)
+    vn2 = None if vn is None else _tape2(vn).reshape(B, T)
+    d2 = None if done is None else _flags(done, B, T)
+    s = _flags(start, B, T)
+    out = [np.empty((B, T), dtype=np.float64) for _ in range(4)]
+    _load().oracle_gae(_ptr(r2), _ptr(v2), _ptr(vn2), _ptr(d2), _ptr(s), float(gamma), float(lam), B, T,
+                       *[_ptr(o) for o in out])
+    return tuple(o.reshape(shape) for o in out)

@@ -210,3 +210,47 @@ void oracle_linattn(const double* q, const double* k, const double* v,
     free(kf);
     free(qf);
 }
+
+/* ------------------------------------------------------ returns and GAE */
+
+void oracle_discounted_return(const double* r, const uint8_t* start, double gamma,
+                              int64_t B, int64_t T, double* G, double* m) {
+    for (int64_t b = 0; b < B; ++b) {
+        const double* rb = r + b * T;
+        /* walk backwards: G_t = r_t + gamma * G_{t+1} inside an episode, and
+         * G_e = r_e at its last step (the sum above, evaluated by Horner) */
+        double g = 0.0, ga = 0.0;
+        for (int64_t t = T - 1; t >= 0; --t) {
+            const int last = (t == T - 1) || is_begin(start, T, b, t + 1);
+            g = last ? rb[t] : rb[t] + gamma * g;
+            ga = last ? fabs(rb[t]) : fabs(rb[t]) + gamma * ga;
+            G[b * T + t] = g;
+            if (m) m[b * T + t] = ga;
+        }
+    }
+}
+
+void oracle_gae(const double* r, const double* v, const double* vn, const uint8_t* done,
+                const uint8_t* start, double gamma, double lambda, int64_t B, int64_t T,
+                double* adv, double* target, double* m_adv, double* m_target) {
+    const double gl = gamma * lambda;
+    for (int64_t b = 0; b < B; ++b) {
+        double A = 0.0, Am = 0.0;
+        for (int64_t t = T - 1; t >= 0; --t) {
+            const int64_t i = b * T + t;
+            const int last = (t == T - 1) || is_begin(start, T, b, t + 1);
+            double next_v;
+            if (vn) next_v = vn[i];
+            else next_v = last ? 0.0 : v[i + 1];
+            const double keep = (done && done[i]) ? 0.0 : 1.0;
+            const double delta = r[i] + gamma * keep * next_v - v[i];
+            const double dmag = fabs(r[i]) + gamma * keep * fabs(next_v) + fabs(v[i]);
+            A = last ? delta : delta + gl * A;
+            Am = last ? dmag : dmag + gl * Am;
+            adv[i] = A;
+            if (target) target[i] = A + v[i];
+            if (m_adv) m_adv[i] = Am;
+            if (m_target) m_target[i] = Am + fabs(v[i]);
+        }
+    }
+}

@@ -102,6 +102,32 @@ void oracle_linattn(const double* q, const double* k, const double* v,
                     const uint8_t* start, int64_t T, int64_t H, int64_t dk, int64_t dv,
                     double* out, double* m);
 
+/* Discounted return over a tape (App. D, discounted-return memoroid; the
+ * done-flag convention of Section 2): for every step, the discounted sum of
+ * the rewards from that step to the end of its episode,
+ *   G_t = sum_{i=t}^{e} gamma^(i-t) r_i,
+ * where e is the last step of t's episode: the step before the next begin
+ * step of the tape, or T-1.  Nothing beyond an episode's last step enters
+ * (the episode is complete).  r, G: [B][T].
+ * m (optional, [B][T]): the same sum over |r_i|. */
+void oracle_discounted_return(const double* r, const uint8_t* start, double gamma,
+                              int64_t B, int64_t T, double* G, double* m);
+
+/* Generalized advantage estimate over a tape (App. E, GAE memoroid), with the
+ * terminal (done) flag of Section 2:
+ *   delta_t = r_t + gamma * [done_t == 0] * vn_t - v_t,
+ *   A_t     = sum_{l=0}^{e-t} (gamma*lambda)^l delta_{t+l},
+ * e as for the return.  vn_t is the value of the step's next state: vn[t] if
+ * vn is given, otherwise v[t+1] when step t+1 is in t's episode and 0 at the
+ * episode's last step.  done NULL means no step is terminal.
+ *   r, v, vn, adv, target: [B][T]; done, start: [B][T] bytes.
+ *   target (optional): A_t + v_t.
+ *   m_adv (optional): the same sums over |r_t| + gamma |vn_t| + |v_t|;
+ *   m_target (optional): m_adv + |v_t|. */
+void oracle_gae(const double* r, const double* v, const double* vn, const uint8_t* done,
+                const uint8_t* start, double gamma, double lambda, int64_t B, int64_t T,
+                double* adv, double* target, double* m_adv, double* m_target);
+
 #ifdef __cplusplus
 }
 #endif

@@ -529,3 +529,177 @@ def test_episode_idx_is_cumsum_of_begins_any_nonzero_byte():
     start[1, 0] = 0
     ref = np.cumsum(np.where(np.arange(T)[None] == 0, 1, start != 0), axis=1) - 1
     np.testing.assert_array_equal(oracle.episode_idx(start), ref)
+
+
+# ------------------------------------------------- discounted return and GAE
+# App. D / App. E: the return and the advantage are the memoroid
+#   (a, r) . (a', r') = (a a', a r' + r),  e_I = (1, 0),  f(r) = (gamma, r)
+# folded over the rewards (TD errors) from step t to the end of t's episode.
+
+
+def paper_return_fold(gamma, rewards, rnd):
+    """Second component of e_I . f(r_t) . ... . f(r_e) under a random
+    bracketing, in rational arithmetic (the monoid is associative)."""
+    def op(p, q):
+        return (p[0] * q[0], p[0] * q[1] + p[1])
+    items = [(Fraction(1), Fraction(0))] + [(gamma, Fraction(x)) for x in rewards]
+    while len(items) > 1:
+        k = rnd.randrange(len(items) - 1)
+        items[k:k + 2] = [op(items[k], items[k + 1])]
+    return items[0][1]
+
+
+def _episode_slices(flags):
+    T = len(flags)
+    begins = [0] + [t for t in range(1, T) if flags[t]] + [T]
+    return [(s, e) for s, e in zip(begins[:-1], begins[1:]) if e > s]
+
+
+def test_return_equals_paper_monoid_fold_exactly():
+    """Every G_t equals the App. D memoroid folded, under a random bracketing,
+    over r_t .. r_e of its episode; dyadic gamma and integer rewards keep the
+    fp64 oracle exact, so the comparison is bit-exact."""
+    rnd = random.Random(5)
+    for gamma in (Fraction(1, 2), Fraction(3, 4), Fraction(0), Fraction(1)):
+        T = 64
+        lengths = [rnd.randint(1, 16) for _ in range(16)]
+        flags = tapes.flags_from_lengths(np.array(lengths), T)
+        r = np.array([rnd.randint(-9, 9) for _ in range(T)], dtype=np.float64)
+        G, _ = oracle.discounted_return(r, flags, float(gamma))
+        for s, e in _episode_slices(flags):
+            for t in range(s, e):
+                ref = paper_return_fold(gamma, r[t:e], rnd)
+                assert G[t] == float(ref), (float(gamma), t)
+
+
+def test_return_closed_form_constant_reward():
+    """Constant reward c over an episode of n steps: G_t = c (1 - gamma^(n-t)) / (1 - gamma)."""
+    gamma, c, n = 0.97, 0.37, 500
+    flags = np.zeros(n, np.uint8)
+    G, _ = oracle.discounted_return(np.full(n, c), flags, gamma)
+    t = np.arange(n)
+    np.testing.assert_allclose(G, c * (1 - gamma ** (n - t)) / (1 - gamma), rtol=1e-13)
+
+
+def test_return_special_gammas():
+    """gamma = 0 gives G = r; gamma = 1 gives each episode's reversed cumulative sum."""
+    rng = np.random.default_rng(3)
+    T = 300
+    flags = tapes.flags_from_lengths(rng.integers(1, 40, size=40), T)
+    r = rng.standard_normal(T)
+    G0, _ = oracle.discounted_return(r, flags, 0.0)
+    assert np.array_equal(G0, r)
+    G1, _ = oracle.discounted_return(r, flags, 1.0)
+    ref = np.empty(T)
+    for s, e in _episode_slices(flags):
+        ref[s:e] = np.cumsum(r[s:e][::-1])[::-1]
+    np.testing.assert_allclose(G1, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_return_tapes_and_episodes_are_independent():
+    """B tapes equal B separate runs; each episode equals its own run."""
+    rng = np.random.default_rng(4)
+    B, T = 3, 200
+    flags = np.stack([tapes.flags_from_lengths(rng.integers(1, 60, size=20), T) for _ in range(B)])
+    flags[:, 0] = 0                      # t = 0 is a begin step whatever the byte says
+    r = rng.standard_normal((B, T))
+    G, _ = oracle.discounted_return(r, flags, 0.9)
+    for b in range(B):
+        Gb, _ = oracle.discounted_return(r[b], flags[b], 0.9)
+        assert np.array_equal(G[b], Gb)
+        for s, e in _episode_slices(flags[b]):
+            Ge, _ = oracle.discounted_return(r[b, s:e], np.zeros(e - s, np.uint8), 0.9)
+            assert np.array_equal(G[b, s:e], Ge)
+
+
+def test_return_nan_stays_inside_its_episode_and_companion_bounds():
+    rng = np.random.default_rng(6)
+    T = 100
+    flags = tapes.flags_from_lengths(np.array([30, 40, 30]), T)
+    r = rng.standard_normal(T)
+    G, m = oracle.discounted_return(r, flags, 0.95)
+    assert np.all(m >= np.abs(G) - 1e-12)
+    Gp, mp = oracle.discounted_return(np.abs(r), flags, 0.95)
+    np.testing.assert_allclose(mp, Gp, rtol=1e-15)
+    r[50] = np.nan
+    Gn, _ = oracle.discounted_return(r, flags, 0.95)
+    assert np.all(np.isnan(Gn[30:51])) and not np.any(np.isnan(Gn[51:]))
+    assert np.array_equal(Gn[:30], G[:30]) and np.array_equal(Gn[70:], G[70:])
+
+
+def _gae_reference(r, v, vn, done, flags, gamma, lam):
+    """App. E definition in rational arithmetic: A_t = sum_l (gamma lam)^l delta_{t+l}
+    over the rest of t's episode, delta_t = r_t + gamma [not done_t] V(s'_t) - V(s_t)."""
+    T = len(r)
+    F = [Fraction(float(x)) for x in r]
+    Vf = [Fraction(float(x)) for x in v]
+    out = [None] * T
+    for s, e in _episode_slices(flags):
+        delta = []
+        for t in range(s, e):
+            if vn is not None:
+                nxt = Fraction(float(vn[t]))
+            else:
+                nxt = Vf[t + 1] if t + 1 < e else Fraction(0)
+            keep = 0 if (done is not None and done[t]) else 1
+            delta.append(F[t] + gamma * keep * nxt - Vf[t])
+        for t in range(s, e):
+            acc, w = Fraction(0), Fraction(1)
+            for l in range(e - t):
+                acc += w * delta[t - s + l]
+                w *= gamma * lam
+            out[t] = acc
+    return out
+
+
+@pytest.mark.parametrize("with_vn", [False, True])
+@pytest.mark.parametrize("with_done", [False, True])
+def test_gae_equals_definition_exactly(with_vn, with_done):
+    """Dyadic gamma, lambda and half-integer values keep every fp64 step exact:
+    the oracle's advantages equal the definition's sums bit for bit."""
+    rnd = random.Random(7 + 2 * with_vn + with_done)
+    gamma, lam = Fraction(1, 2), Fraction(3, 4)
+    T = 48
+    flags = tapes.flags_from_lengths(np.array([rnd.randint(1, 12) for _ in range(12)]), T)
+    r = np.array([rnd.randint(-6, 6) for _ in range(T)], dtype=np.float64)
+    v = np.array([rnd.randint(-8, 8) / 2 for _ in range(T)], dtype=np.float64)
+    vn = np.array([rnd.randint(-8, 8) / 2 for _ in range(T)], dtype=np.float64) if with_vn else None
+    done = np.array([rnd.random() < 0.3 for _ in range(T)], dtype=np.uint8) if with_done else None
+    adv, target, _, _ = oracle.gae(r, v, flags, float(gamma), float(lam), vn=vn, done=done)
+    ref = _gae_reference(r, v, vn, done, flags, gamma, lam)
+    assert [float(x) for x in ref] == list(adv)
+    assert np.array_equal(target, adv + v)
+
+
+def test_gae_limits():
+    """lambda = 0: A_t = delta_t.  lambda = 1 with every episode ending in a
+    terminal state: A_t + V(s_t) is the discounted return (the value terms
+    telescope)."""
+    rng = np.random.default_rng(8)
+    T, gamma = 400, 0.99
+    flags = tapes.flags_from_lengths(rng.integers(1, 80, size=30), T)
+    r, v = rng.standard_normal(T), rng.standard_normal(T)
+    adv0, _, _, _ = oracle.gae(r, v, flags, gamma, 0.0)
+    nxt = np.zeros(T)
+    for s, e in _episode_slices(flags):
+        nxt[s:e - 1] = v[s + 1:e]
+    np.testing.assert_allclose(adv0, r + gamma * nxt - v, rtol=1e-14, atol=1e-14)
+    adv1, target1, _, _ = oracle.gae(r, v, flags, gamma, 1.0)
+    G, _ = oracle.discounted_return(r, flags, gamma)
+    np.testing.assert_allclose(target1, G, rtol=1e-11, atol=1e-11)
+
+
+def test_gae_done_cuts_bootstrap_only():
+    """A terminal step drops gamma V(s') from its own TD error but the
+    advantage recursion still stops only at episode ends."""
+    T = 5
+    r = np.array([1.0, 1.0, 1.0, 1.0, 1.0])
+    v = np.zeros(T)
+    vn = np.full(T, 10.0)
+    flags = np.zeros(T, np.uint8)
+    done = np.array([0, 0, 1, 0, 0], np.uint8)
+    adv, _, m, _ = oracle.gae(r, v, flags, 0.5, 1.0, vn=vn, done=done)
+    delta = np.array([6.0, 6.0, 1.0, 6.0, 6.0])
+    ref = [sum(0.5 ** l * delta[t + l] for l in range(T - t)) for t in range(T)]
+    assert list(adv) == ref
+    assert np.all(m >= np.abs(adv))
