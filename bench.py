@@ -6,7 +6,8 @@
 A step is one pass of the whole hot path over one synthetic tape already
 resident in HBM: for the diagonal workloads the forward scan (with episode
 indices) and, where the workload has one, the reverse (gradient) scan; for the
-linear-attention workload the chunked forward readout.  Prints ONE JSON line.
+linear-attention workload the chunked forward readout; for the RL-target
+workload the discounted return and the advantage estimate.  Prints ONE JSON line.
 
 Workloads (seeded, synthetic; laws in paper_2402_09900_amd.tapes):
   1  diag real f32, T=1024, d=32, 8 episodes, forward
@@ -15,6 +16,8 @@ Workloads (seeded, synthetic; laws in paper_2402_09900_amd.tapes):
   3  linear-transformer memoroid, T=32768, 4 heads x 64, Geometric(500), chunk 64
   4  diag real, 64 tapes x T=16384, d=512, bf16 in / fp32 state / bf16 out
   5  diag real f32, T=1048576, d=256, lognormal(5, 1.5) episodes, forward + reverse
+  6  discounted return + generalized advantage estimate, one tape of 2^24 steps,
+     U{1..1000} episodes, gamma 0.99, lambda 0.95
 
 Every buffer exists in several copies (at least 1 GiB cycled, at least 3) and
 step i uses copy i mod n, so inputs are read from HBM rather than from the
@@ -51,7 +54,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    p.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6])
     p.add_argument("--no-cpu-baseline", action="store_true")
     return p.parse_args()
 
@@ -167,6 +170,35 @@ def setup_linattn(torch, mb, tapes):
     return la, sets, bytes_per, n, flops
 
 
+def setup_discount(torch, mb, tapes, key):
+    tp = tapes.make_discount(key)
+    B, T = tp.B, tp.T
+    n = B * T
+    nb = mb.memoroid_discount_workspace_bytes(B, T)
+    stream = lambda: torch.cuda.current_stream().cuda_stream  # noqa: E731
+    sets = []
+    for _ in range(n_sets(n * (4 * 6 + 2) + 2 * nb)):
+        r, v, vn = dev_tensor(torch, tp.r, "f32"), dev_tensor(torch, tp.v, "f32"), dev_tensor(torch, tp.vn, "f32")
+        s, done = dev_tensor(torch, tp.start, "u8"), dev_tensor(torch, tp.done, "u8")
+        G, adv, tg = (torch.empty((B, T), dtype=torch.float32, device="cuda") for _ in range(3))
+        ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+
+        def ret(r=r, s=s, G=G, ws=ws):
+            st = mb.memoroid_discounted_return(r.data_ptr(), s.data_ptr(), tp.gamma, G.data_ptr(), B, T,
+                                               ws.data_ptr(), ws.numel(), stream())
+            assert st == 0, mb.status_string(st)
+
+        def gae(r=r, v=v, vn=vn, done=done, s=s, adv=adv, tg=tg, ws=ws):
+            st = mb.memoroid_gae(r.data_ptr(), v.data_ptr(), vn.data_ptr(), done.data_ptr(), s.data_ptr(),
+                                 tp.gamma, tp.lam, adv.data_ptr(), tg.data_ptr(), B, T, ws.data_ptr(), ws.numel(),
+                                 stream())
+            assert st == 0, mb.status_string(st)
+        sets.append({"return": ret, "gae": gae})
+    # return: read r, flags; write G.  gae: read r, V, V', done, flags; write adv, target
+    bytes_per = {"return": n * (4 + 1 + 4), "gae": n * (3 * 4 + 2 + 2 * 4)}
+    return tp, sets, bytes_per, n
+
+
 def kernel_source_hash():
     """sha256 over the library's HIP sources (same recipe as
     profiles/summarize.py), to tell whether recorded counters still apply."""
@@ -195,6 +227,17 @@ def cpu_baseline(key, tapes, budget_s=20.0):
     """The oracle as it stands, single thread, on a bounded sample."""
     import oracle
     w = tapes.WORKLOADS[key]
+    if w.kind == "discount":
+        T = min(w.T, 1 << 22)
+        tp = tapes.make_discount(key, T=T)
+        r, v, vn = (a.astype(np.float64) for a in (tp.r, tp.v, tp.vn))
+        g32, l32 = float(np.float32(tp.gamma)), float(np.float32(tp.lam))
+        t0 = time.perf_counter()
+        oracle.discounted_return(r, tp.start, g32)
+        oracle.gae(r, v, tp.start, g32, l32, vn=vn, done=tp.done)
+        dt = time.perf_counter() - t0
+        return {"value": tp.B * T / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
+                "sample": "first %d steps of the tape, return + advantage, fp64, %.1f s" % (T, dt)}
     if w.kind == "linattn":
         T = min(w.T, 4096)
         la = tapes.make_linattn(T=T)
@@ -242,6 +285,8 @@ def main():
     flops = None
     if wl.kind == "linattn":
         w, sets, bytes_per, n, flops = setup_linattn(torch, mb, tapes)
+    elif wl.kind == "discount":
+        w, sets, bytes_per, n = setup_discount(torch, mb, tapes, key)
     else:
         w, sets, bytes_per, n = setup_diag(torch, mb, tapes, key)
     calls = sets[0]
@@ -286,7 +331,8 @@ def main():
     roof["traffic"] = recorded_traffic(key, "linattn" if wl.kind == "linattn" else dom)
     roof["traffic_unit"] = "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
     roof["kernel"] = {"fwd": "memoroid_scan_diag" if wl.kind == "diag" else "memoroid_scan_linattn",
-                      "bwd": "memoroid_scan_diag_bwd"}[dom]
+                      "bwd": "memoroid_scan_diag_bwd", "return": "memoroid_discounted_return",
+                      "gae": "memoroid_gae"}[dom]
     roof["ms_per_launch"] = round(per_call_ms[dom], 4)
     roof["algorithmic_bytes_per_launch"] = int(bytes_per[dom])
     if flops is not None:
@@ -307,6 +353,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "B": wl.B, "T": wl.T,
                    ("heads" if wl.kind == "linattn" else "d"): wl.d,
+                   **({"gamma": wl.gamma, "lambda": wl.lam} if wl.kind == "discount" else {}),
                    "passes": list(calls.keys()),
                    "buffer_sets": len(sets),
                    "ms_per_call": {k: round(v, 4) for k, v in per_call_ms.items()},

@@ -34,7 +34,7 @@
  *    passed for both).
  *  - Every pointer must be aligned to its element size (4 bytes for f32, 2 for
  *    bf16, 8 for complex64, 4 for int32).  Rows whose pointers are 16-byte
- *    aligned and whose d is a multiple of the vector width (4 f32, 8 bf16,
+ *    aligned and whose d is a multiple of the vector width (4 f32, 4 bf16,
  *    2 complex64) take the vectorised kernels; other shapes take a scalar
  *    kernel with identical results.
  *  - The workspace is caller-allocated device memory of at least the size the
@@ -162,6 +162,58 @@ int memoroid_scan_linattn(const float* q, const float* k, const float* v,
                           const uint8_t* start, float* out, int32_t* episode_idx,
                           int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t chunk,
                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Discounted return over a tape (App. D, the discounted-return memoroid
+ * (a, r) . (a', r') = (a a', a r' + r) with f(r) = (gamma, r)), restarted at
+ * every episode: for each step, the sum of gamma^(i-t) r_i over the steps i
+ * from t to the last step of t's episode, which is the step before the next
+ * begin step or the tape's last step (episodes are complete: nothing is
+ * bootstrapped after them).
+ *
+ *   r          rewards [B][T] fp32.
+ *   start      start[B][T] begin flags (as above).
+ *   gamma      discount, 0 <= gamma <= 1 (MEMOROID_EINVAL otherwise, NaN too).
+ *   G          out [B][T] fp32; must not alias r or start.
+ *   Rows with T % 4 == 0 and 16-byte aligned r and G (4-byte aligned start)
+ *   take the vectorised kernel, other shapes a scalar one.
+ *   Workspace: memoroid_discount_workspace_bytes(B, T) bytes.
+ * ------------------------------------------------------------------------ */
+size_t memoroid_discount_workspace_bytes(int64_t B, int64_t T);
+
+int memoroid_discounted_return(const float* r, const uint8_t* start, float gamma, float* G,
+                               int64_t B, int64_t T,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Generalized advantage estimate over a tape (App. E, the GAE memoroid:
+ * the return's monoid with gamma*lambda as the discount and the TD error as
+ * the reward), restarted at every episode, with the terminal (done) flag of
+ * Section 2 removing the bootstrap value of a terminal transition:
+ *     delta_t = r_t + gamma * [done_t == 0] * vn_t - value_t
+ *     adv_t   = sum_{l=0}^{e-t} (gamma*lambda)^l delta_{t+l},  e = last step of t's episode
+ *     target_t = adv_t + value_t
+ *
+ *   r, value   [B][T] fp32: reward of the transition, V(s_t).
+ *   value_next optional [B][T] fp32: V(s'_t), the value of the transition's
+ *              next state (used at every step, episode ends included).  NULL:
+ *              vn_t = value_{t+1} when step t+1 is in t's episode, 0 at the
+ *              episode's last step.
+ *   done       optional [B][T] bytes, nonzero = the transition ends in a
+ *              terminal state; NULL = no terminal steps.
+ *   start      start[B][T] begin flags (as above).
+ *   gamma, lambda  in [0, 1] (MEMOROID_EINVAL otherwise).  The recurrence
+ *              runs with the fp32 product gamma*lambda.
+ *   adv        out [B][T] fp32;  target: optional out [B][T] fp32 (NULL skips).
+ *              Outputs must not alias any input or each other.
+ *   Vectorised when T % 4 == 0, every fp32 pointer is 16-byte aligned and
+ *   the flag pointers 4-byte aligned.
+ *   Workspace: memoroid_discount_workspace_bytes(B, T) bytes.
+ * ------------------------------------------------------------------------ */
+int memoroid_gae(const float* r, const float* value, const float* value_next, const uint8_t* done,
+                 const uint8_t* start, float gamma, float lambda, float* adv, float* target,
+                 int64_t B, int64_t T,
+                 void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Health of the last call that used `workspace`: synchronises `stream`,

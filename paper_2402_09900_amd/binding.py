@@ -59,6 +59,12 @@ def lib() -> ctypes.CDLL:
         L.memoroid_scan_linattn_workspace_bytes.argtypes = [I64, I64, I64, I64, I64]
         L.memoroid_scan_linattn.restype = I32
         L.memoroid_scan_linattn.argtypes = [P, P, P, P, P, P, I64, I64, I64, I64, I64, P, SZ, P]
+        L.memoroid_discount_workspace_bytes.restype = SZ
+        L.memoroid_discount_workspace_bytes.argtypes = [I64, I64]
+        L.memoroid_discounted_return.restype = I32
+        L.memoroid_discounted_return.argtypes = [P, P, ctypes.c_float, P, I64, I64, P, SZ, P]
+        L.memoroid_gae.restype = I32
+        L.memoroid_gae.argtypes = [P, P, P, P, P, ctypes.c_float, ctypes.c_float, P, P, I64, I64, P, SZ, P]
         L.memoroid_workspace_status.restype = I32
         L.memoroid_workspace_status.argtypes = [P, SZ, P]
         _lib = L
@@ -110,6 +116,20 @@ def memoroid_scan_linattn(q, k, v, start, out, episode_idx, T, H, dk, dv, chunk,
                           workspace, workspace_bytes, stream) -> int:
     return lib().memoroid_scan_linattn(q, k, v, start, out, episode_idx, T, H, dk, dv, chunk,
                                        workspace, workspace_bytes, stream)
+
+
+def memoroid_discount_workspace_bytes(B, T) -> int:
+    return lib().memoroid_discount_workspace_bytes(B, T)
+
+
+def memoroid_discounted_return(r, start, gamma, G, B, T, workspace, workspace_bytes, stream) -> int:
+    return lib().memoroid_discounted_return(r, start, gamma, G, B, T, workspace, workspace_bytes, stream)
+
+
+def memoroid_gae(r, value, value_next, done, start, gamma, lam, adv, target, B, T,
+                 workspace, workspace_bytes, stream) -> int:
+    return lib().memoroid_gae(r, value, value_next, done, start, gamma, lam, adv, target, B, T,
+                              workspace, workspace_bytes, stream)
 
 
 def memoroid_workspace_status(workspace, workspace_bytes, stream) -> int:
@@ -264,6 +284,60 @@ def scan_linattn(q, k, v, start, episode_idx: bool = False, chunk: int = 64, wor
                                      T, H, dk, dv, chunk, ws.data_ptr(), ws.numel(), _stream_ptr(dev))
     _raise(st, "memoroid_scan_linattn")
     return (out, idx) if episode_idx else out
+
+
+def _tape_shapes(r, *others):
+    if r.dim() == 1:
+        r = r.unsqueeze(0)
+    if r.dim() != 2:
+        raise ValueError("tape tensors must be [B, T] or [T]")
+    B, T = r.shape
+    return r, [None if o is None else o.reshape(B, T) for o in others], B, T
+
+
+def discounted_return(r, start, gamma: float, workspace=None):
+    """Discounted return of every step to the end of its episode (episodes end
+    before each begin step and at the tape end).  r: float32 [B,T] (or [T]);
+    start: uint8, same shape.  Returns G shaped like r."""
+    torch = _torch()
+    shape = r.shape
+    r, (start,), B, T = _tape_shapes(r, start)
+    dev = _check_cuda(r, start)
+    if r.dtype != torch.float32 or start.dtype != torch.uint8:
+        raise TypeError("r must be float32 and start uint8")
+    G = torch.empty((B, T), dtype=torch.float32, device=dev)
+    ws = _workspace(lib().memoroid_discount_workspace_bytes(B, T), dev, workspace)
+    st = lib().memoroid_discounted_return(r.data_ptr(), start.data_ptr(), float(gamma), G.data_ptr(), B, T,
+                                          ws.data_ptr(), ws.numel(), _stream_ptr(dev))
+    _raise(st, "memoroid_discounted_return")
+    return G.reshape(shape)
+
+
+def gae(r, value, start, gamma: float, lam: float, value_next=None, done=None, target: bool = True,
+        workspace=None):
+    """Generalized advantage estimate over a tape.  r, value (and value_next)
+    float32 [B,T] (or [T]); start (and done) uint8 of the same shape.
+    Returns (adv, target) with target = adv + value (None if not asked)."""
+    torch = _torch()
+    shape = r.shape
+    r, (value, value_next, done, start), B, T = _tape_shapes(r, value, value_next, done, start)
+    dev = _check_cuda(r, value, value_next, done, start)
+    for t in (r, value, value_next):
+        if t is not None and t.dtype != torch.float32:
+            raise TypeError("r, value and value_next must be float32")
+    for t in (start, done):
+        if t is not None and t.dtype != torch.uint8:
+            raise TypeError("start and done must be uint8")
+    adv = torch.empty((B, T), dtype=torch.float32, device=dev)
+    tg = torch.empty((B, T), dtype=torch.float32, device=dev) if target else None
+    ws = _workspace(lib().memoroid_discount_workspace_bytes(B, T), dev, workspace)
+    st = lib().memoroid_gae(r.data_ptr(), value.data_ptr(),
+                            value_next.data_ptr() if value_next is not None else None,
+                            done.data_ptr() if done is not None else None, start.data_ptr(),
+                            float(gamma), float(lam), adv.data_ptr(), tg.data_ptr() if tg is not None else None,
+                            B, T, ws.data_ptr(), ws.numel(), _stream_ptr(dev))
+    _raise(st, "memoroid_gae")
+    return adv.reshape(shape), (tg.reshape(shape) if tg is not None else None)
 
 
 def workspace_status(workspace) -> int:

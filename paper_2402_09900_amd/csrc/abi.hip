@@ -2,6 +2,7 @@
 // argument validation (before any HIP call), tiling plans, workspace layout
 // and kernel launches.
 #include <limits.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include "memoroid.h"
@@ -40,7 +41,7 @@ struct DiagPlan {
     int64_t nt = 0;
     int64_t nchains = 0;
     int64_t ntiles = 0;
-    size_t off_agg = 0, off_incl = 0, off_cnt = 0, off_part = 0, off_sum1 = 0, off_sum2 = 0;
+    size_t off_ctr = 0, off_agg = 0, off_incl = 0, off_cnt = 0, off_part = 0, off_sum1 = 0, off_sum2 = 0;
     size_t fill_bytes = 0;   // bytes from off_agg that must start as 0xFF
     size_t total = 0;
 };
@@ -69,6 +70,8 @@ bool plan_diag(int64_t B, int64_t T, int64_t d, int state_dtype, bool vec, int r
     if (!mul_ok(p->ntiles, p->Dp, &ndesc)) return false;
     if (ndesc > INT64_MAX / 32) return false;
     size_t off = kAlign;                                   // header
+    p->off_ctr = off;                                      // per-chain tile counters
+    off = align_up(off + (size_t)p->nchains * kCtrStride * 4);
     p->off_agg = off;
     off = align_up(off + (size_t)ndesc * agg_b);
     p->off_incl = off;
@@ -181,7 +184,7 @@ int memoroid_scan_diag(const void* a, int64_t a_stride_t, const void* x, const u
 
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
-    if (ws_init_launch(ws, ws + p.off_agg, p.fill_bytes, s) != hipSuccess) return MEMOROID_EHIP;
+    if (ws_init_launch(ws, p.off_agg, ws + p.off_agg, p.fill_bytes, s) != hipSuccess) return MEMOROID_EHIP;
     DiagFwdArgs args{};
     args.a = a;
     args.x = x;
@@ -195,6 +198,7 @@ int memoroid_scan_diag(const void* a, int64_t a_stride_t, const void* x, const u
     args.agg = ws + p.off_agg;
     args.incl = ws + p.off_incl;
     args.hdr = (WsHeader*)ws;
+    args.ctr = (uint32_t*)(ws + p.off_ctr);
     args.idx = episode_idx;
     args.cnt = (uint64_t*)(ws + p.off_cnt);
     const int ik = in_dtype == MEMOROID_F32 ? K_F32 : in_dtype == MEMOROID_BF16 ? K_BF16 : K_C64;
@@ -248,7 +252,7 @@ int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t, const uint8_t* sta
 
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
-    if (ws_init_launch(ws, ws + p.off_agg, p.fill_bytes, s) != hipSuccess) return MEMOROID_EHIP;
+    if (ws_init_launch(ws, p.off_agg, ws + p.off_agg, p.fill_bytes, s) != hipSuccess) return MEMOROID_EHIP;
     DiagBwdArgs args{};
     args.a = a;
     args.start = start;
@@ -266,6 +270,7 @@ int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t, const uint8_t* sta
     args.agg = ws + p.off_agg;
     args.incl = ws + p.off_incl;
     args.hdr = (WsHeader*)ws;
+    args.ctr = (uint32_t*)(ws + p.off_ctr);
     const int k = dtype == MEMOROID_F32 ? K_F32 : K_C64;
     const int64_t cols = d * (dtype == MEMOROID_C64 ? 2 : 1);
     if (diag_bwd_launch(k, vec, ainv, args, p.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
@@ -359,7 +364,8 @@ int memoroid_scan_linattn(const float* q, const float* k, const float* v, const 
     sa.R = R;
     sa.T = T;
     sa.H = H;
-    sa.hdr = (uint32_t*)sw;
+    sa.zero = (u32x4*)sw;
+    sa.zero16 = (int64_t)(p.scan.off_agg / 16);
     sa.fill = (u32x4*)(sw + p.scan.off_agg);
     sa.fill16 = (int64_t)((p.off_cnt + (size_t)p.nch * 8 - (p.off_scan + p.scan.off_agg) + 15) / 16);
     if (linattn_summary_launch(sa, s) != hipSuccess) return MEMOROID_EHIP;
@@ -376,6 +382,7 @@ int memoroid_scan_linattn(const float* q, const float* k, const float* v, const 
     args.agg = sw + p.scan.off_agg;
     args.incl = sw + p.scan.off_incl;
     args.hdr = (WsHeader*)sw;
+    args.ctr = (uint32_t*)(sw + p.scan.off_ctr);
     args.idx = nullptr;
     args.cnt = nullptr;
     if (diag_fwd_launch(K_F32, K_F32, true, true, args, p.scan.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
@@ -396,6 +403,117 @@ int memoroid_scan_linattn(const float* q, const float* k, const float* v, const 
 }
 
 // ------------------------------------------------------------------ status
+
+// ------------------------------------------- discounted return and GAE
+
+namespace {
+
+struct DiscPlan {
+    int64_t nt = 0, ntiles = 0;
+    size_t off_agg = 0, off_incl = 0, fill_bytes = 0, total = 0;
+};
+
+bool plan_disc(int64_t B, int64_t T, DiscPlan* p) {
+    p->nt = (T + kDiscTile - 1) / kDiscTile;
+    if (!mul_ok(B, p->nt, &p->ntiles) || p->ntiles >= (int64_t)INT32_MAX) return false;
+    size_t off = kAlign;
+    p->off_agg = off;
+    off = align_up(off + (size_t)p->ntiles * 8);
+    p->off_incl = off;
+    off = align_up(off + (size_t)p->ntiles * 8);
+    p->fill_bytes = off - p->off_agg;
+    p->total = off;
+    return true;
+}
+
+bool unit_interval(float v) { return v >= 0.0f && v <= 1.0f; }   // false for NaN
+
+// Polls of an awaited tile without progress before a look-back computes
+// that tile's aggregate from its inputs.  MEMOROID_FALLBACK_POLLS overrides
+// the default (tests set it to 0 to run the fallback on every wait).
+uint32_t fallback_polls() {
+    const char* e = getenv("MEMOROID_FALLBACK_POLLS");
+    if (e && *e) {
+        char* end = nullptr;
+        const unsigned long v = strtoul(e, &end, 10);
+        if (end && *end == 0 && v <= 0xFFFFFFFFul) return (uint32_t)v;
+    }
+    return 4096u;
+}
+
+int disc_run(const float* r, const float* value, const float* value_next, const uint8_t* done,
+             const uint8_t* start, float a, float gamma, float* out, float* target, int64_t B, int64_t T,
+             void* workspace, size_t workspace_bytes, void* stream, bool gae) {
+    int64_t BT;
+    if (!mul_ok(B, T, &BT) || BT > INT64_MAX / 16) return MEMOROID_EINVAL;
+    const float* fin[3] = {r, value, value_next};
+    const float* fout[2] = {out, target};
+    for (const float* q : fin)
+        if (q && !aligned(q, 4)) return MEMOROID_EINVAL;
+    for (const float* q : fout) {
+        if (q && !aligned(q, 4)) return MEMOROID_EINVAL;
+        if (q && (q == r || q == value || q == value_next || (const void*)q == (const void*)start ||
+                  (const void*)q == (const void*)done))
+            return MEMOROID_EINVAL;
+    }
+    if (target && target == out) return MEMOROID_EINVAL;
+    const bool vec = T % 4 == 0 && aligned(r, 16) && aligned(out, 16) && aligned(start, 4) &&
+                     (!value || aligned(value, 16)) && (!value_next || aligned(value_next, 16)) &&
+                     (!done || aligned(done, 4)) && (!target || aligned(target, 16));
+    DiscPlan p;
+    if (!plan_disc(B, T, &p)) return MEMOROID_EUNSUPPORTED;
+    if (!workspace || workspace_bytes < p.total) return MEMOROID_EWORKSPACE;
+    if (!aligned(workspace, 16)) return MEMOROID_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    if (ws_init_launch(ws, p.off_agg, ws + p.off_agg, p.fill_bytes, s) != hipSuccess) return MEMOROID_EHIP;
+    DiscArgs args{};
+    args.r = r;
+    args.v = value;
+    args.vn = value_next;
+    args.done = done;
+    args.start = start;
+    args.out = out;
+    args.target = target;
+    args.a = a;
+    args.gamma = gamma;
+    args.T = T;
+    args.nt = p.nt;
+    args.B = B;
+    args.fallback_polls = fallback_polls();
+    args.agg = (uint64_t*)(ws + p.off_agg);
+    args.incl = (uint64_t*)(ws + p.off_incl);
+    args.hdr = (WsHeader*)ws;
+    return check_hip(disc_launch(vec, gae, args, p.ntiles, s));
+}
+
+}  // namespace
+
+size_t memoroid_discount_workspace_bytes(int64_t B, int64_t T) {
+    if (B <= 0 || T <= 0) return 0;
+    DiscPlan p;
+    if (!plan_disc(B, T, &p)) return 0;
+    return p.total;
+}
+
+int memoroid_discounted_return(const float* r, const uint8_t* start, float gamma, float* G, int64_t B, int64_t T,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+    if (B < 0 || T < 0 || !unit_interval(gamma)) return MEMOROID_EINVAL;
+    if (B == 0 || T == 0) return MEMOROID_OK;
+    if (!r || !start || !G) return MEMOROID_EINVAL;
+    return disc_run(r, nullptr, nullptr, nullptr, start, gamma, gamma, G, nullptr, B, T, workspace,
+                    workspace_bytes, stream, false);
+}
+
+int memoroid_gae(const float* r, const float* value, const float* value_next, const uint8_t* done,
+                 const uint8_t* start, float gamma, float lambda, float* adv, float* target, int64_t B, int64_t T,
+                 void* workspace, size_t workspace_bytes, void* stream) {
+    if (B < 0 || T < 0 || !unit_interval(gamma) || !unit_interval(lambda)) return MEMOROID_EINVAL;
+    if (B == 0 || T == 0) return MEMOROID_OK;
+    if (!r || !value || !start || !adv) return MEMOROID_EINVAL;
+    return disc_run(r, value, value_next, done, start, gamma * lambda, gamma, adv, target, B, T, workspace,
+                    workspace_bytes, stream, true);
+}
 
 int memoroid_workspace_status(const void* workspace, size_t workspace_bytes, void* stream) {
     if (!workspace || workspace_bytes < sizeof(WsHeader)) return MEMOROID_EINVAL;

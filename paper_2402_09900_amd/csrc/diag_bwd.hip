@@ -37,11 +37,18 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     __shared__ LookbackLds<S, VEC> sLb;
 
     const int tid = threadIdx.x;
-    if (tid == 0) s_ticket = atomicAdd(&p.hdr->ticket, 1u);
+    // the workgroup's chain is fixed by its index (each run of nchains
+    // consecutive workgroups covers every chain once, rotated by one per run
+    // so that no chain stays on one XCD); its place in the chain comes from
+    // the chain's own counter, in the order tiles start
+    const uint32_t nch = (uint32_t)p.nchains;
+    const int chain = (int)((blockIdx.x % nch + blockIdx.x / nch) % nch);
+    if (tid == 0)
+        s_ticket = __hip_atomic_fetch_add(p.ctr + (size_t)chain * kCtrStride, 1u, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
-    const uint32_t ticket = s_ticket;
-    const int chain = (int)(ticket % (uint32_t)p.nchains);
-    const int64_t k = ticket / (uint32_t)p.nchains;
+    const int64_t k = s_ticket;
+    const uint32_t ticket = (uint32_t)(k * p.nchains + chain);
     const int64_t tile = p.nt - 1 - k;              // tiles run from the tape end
     const int b = chain / p.nfb;
     const int fb = chain - b * p.nfb;

@@ -16,10 +16,15 @@
 //            (lane = j * Qp + q) owns the VEC features at q and R consecutive
 //            steps; its group is w * Gw + j with Gw = 64 / Qp, groups being
 //            consecutive in time: L = 4 * Gw * R steps per tile.
-//   ticket = tiles are numbered by an atomic counter in launch order,
-//            interleaving chains (ticket = tile * nchains + chain), so every
-//            tile a workgroup waits for was handed to a workgroup that is
-//            already running or finished.
+//   ticket = workgroup g works on chain (g + g / nchains) mod nchains (every
+//            chain once per run of nchains workgroups, rotated so that no
+//            chain is tied to one XCD); its tile within the
+//            chain is drawn from that chain's own atomic counter in the order
+//            workgroups start, so every tile a workgroup waits for (an
+//            earlier tile of its chain) was handed to a workgroup that is
+//            already running or finished.  Descriptors are indexed by
+//            ticket = tile * nchains + chain.  One counter per chain, each on
+//            its own 128-byte line, keeps the counters from serialising.
 //
 // Per tile: (1) every load is issued up front: the begin flags of the lane's
 // steps, then a and x, one wide access per step; (2) each lane folds its R
@@ -58,11 +63,18 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     __shared__ uint32_t sCntBefore;        // begins on the tape before this tile
 
     const int tid = threadIdx.x;
-    if (tid == 0) s_ticket = atomicAdd(&p.hdr->ticket, 1u);
+    // the workgroup's chain is fixed by its index (each run of nchains
+    // consecutive workgroups covers every chain once, rotated by one per run
+    // so that no chain stays on one XCD); its place in the chain comes from
+    // the chain's own counter, in the order tiles start
+    const uint32_t nch = (uint32_t)p.nchains;
+    const int chain = (int)((blockIdx.x % nch + blockIdx.x / nch) % nch);
+    if (tid == 0)
+        s_ticket = __hip_atomic_fetch_add(p.ctr + (size_t)chain * kCtrStride, 1u, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
-    const uint32_t ticket = s_ticket;
-    const int chain = (int)(ticket % (uint32_t)p.nchains);
-    const int64_t tile = ticket / (uint32_t)p.nchains;
+    const int64_t tile = s_ticket;
+    const uint32_t ticket = (uint32_t)(tile * p.nchains + chain);
     const int b = chain / p.nfb;
     const int fb = chain - b * p.nfb;
     const int Qp = p.Qp;

@@ -1,0 +1,393 @@
+// discount.hip -- discounted return and generalized advantage estimate over a
+// tape of episodes, for gfx950.
+//
+// Both are the memoroid (a, r) . (a', r') = (a a', a r' + r) of App. D and
+// App. E folded over the rest of each step's episode, i.e. the reverse
+// resettable recurrence
+//     y_t = x_t                     if t is the last step of its episode
+//     y_t = a * y_{t+1} + x_t       otherwise,
+// with a = gamma, x = r for the return and a = gamma * lambda, x = delta
+// (the TD error, computed in the kernel) for the advantage.  A step is the
+// last of its episode when the next step begins an episode or the tape ends.
+//
+// One tape per row of [B][T]; a tile is 4096 consecutive steps of one tape,
+// handled by 4 wavefronts of 1024 steps.  In a wavefront, load u puts steps
+// 64*VEC*u + VEC*lane .. + VEC-1 into lane `lane` (so every load is one
+// contiguous, coalesced run).  The recurrence is carried as maps
+// "value at the run's first step = f ? H : A * (value after the run) + H";
+// lanes compose their own VEC steps, wavefronts scan the 64 lane maps of
+// each load with shuffles, and tiles find the value entering from their
+// right with a decoupled look-back over the tiles to their right.
+//
+// Tiles are numbered from the tape's end by their workgroup index, with no
+// ticket counter (a single counter serialises every workgroup on one memory
+// line).  Waiting for a tile that has not started could then deadlock, so a
+// look-back that sees no progress for a while computes the awaited tile's
+// aggregate itself from that tile's inputs (a "fallback") and moves on: no
+// wait depends on another workgroup having started, and in the usual
+// in-order dispatch the fallback never runs.
+#include "scan_common.hpp"
+#include "kernels.hpp"
+
+namespace memoroid {
+
+namespace {
+
+constexpr int kRows = kDiscRows;              // steps per lane
+constexpr int kSeg = 64 * kRows;              // steps per wavefront
+static_assert(kDiscTile == 4 * kSeg, "tile = 4 wavefronts");
+
+struct RMap {
+    float A, H;
+    bool f;
+};
+
+__device__ __forceinline__ RMap rmap_id() { return RMap{1.0f, 0.0f, false}; }
+
+// `left` covers the steps just before `right`; the value entering from the
+// right passes through `right` first.
+__device__ __forceinline__ RMap rmap_then(const RMap& left, const RMap& right) {
+    RMap o;
+    o.f = left.f || right.f;
+    o.H = left.f ? left.H : __builtin_fmaf(left.A, right.H, left.H);
+    o.A = left.A * right.A;
+    return o;
+}
+
+__device__ __forceinline__ float rmap_apply(const RMap& m, float after) {
+    return m.f ? m.H : __builtin_fmaf(m.A, after, m.H);
+}
+
+__device__ __forceinline__ RMap rmap_shfl_down(const RMap& m, int k) {
+    return RMap{__shfl_down(m.A, k, 64), __shfl_down(m.H, k, 64), __shfl_down((int)m.f, k, 64) != 0};
+}
+
+__device__ __forceinline__ RMap rmap_bcast(const RMap& m, int src) {
+    return RMap{__shfl(m.A, src, 64), __shfl(m.H, src, 64), __shfl((int)m.f, src, 64) != 0};
+}
+
+// Inclusive suffix composition over the wavefront: lane l ends with
+// m_l . m_{l+1} . ... . m_63.
+__device__ __forceinline__ RMap wave_suffix(RMap m) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int k = 1; k < 64; k <<= 1) {
+        const RMap o = rmap_shfl_down(m, k);
+        if (lane + k < 64) m = rmap_then(m, o);
+    }
+    return m;
+}
+
+template <int VEC>
+struct F;
+template <>
+struct F<4> {
+    typedef float __attribute__((ext_vector_type(4))) T;
+};
+template <>
+struct F<1> {
+    typedef float T;
+};
+
+template <int VEC>
+__device__ __forceinline__ float comp(const typename F<VEC>::T& v, int k) {
+    if constexpr (VEC == 1) {
+        return v;
+    } else {
+        return v[k];
+    }
+}
+
+template <int VEC>
+__device__ __forceinline__ void set_comp(typename F<VEC>::T& v, int k, float x) {
+    if constexpr (VEC == 1) {
+        v = x;
+    } else {
+        v[k] = x;
+    }
+}
+
+template <int VEC>
+__device__ __forceinline__ typename F<VEC>::T load_vec(const float* p) {
+    return *(const typename F<VEC>::T*)p;
+}
+
+template <int VEC>
+__device__ __forceinline__ uint32_t load_flags(const uint8_t* p) {
+    if constexpr (VEC == 1) {
+        return *p;
+    } else {
+        return *(const uint32_t*)p;
+    }
+}
+
+template <int VEC>
+__device__ __forceinline__ void store_vec(float* p, const typename F<VEC>::T& v) {
+    __builtin_nontemporal_store(v, (typename F<VEC>::T*)p);
+}
+
+// Inputs x (delta for the advantage, computed here in place) and the map of
+// one lane's VEC steps t0 .. t0+VEC-1.  next_fl / next_v: begin flag and
+// V(s) of the step after the lane's last step.  eb gets bit k set when step
+// k is the last of its episode.
+template <int VEC, bool GAE>
+__device__ __forceinline__ RMap lane_map(const DiscArgs& p, int64_t t0, typename F<VEC>::T& x,
+                                         const typename F<VEC>::T& vv, const typename F<VEC>::T& vn, uint32_t fl,
+                                         uint32_t dn, uint32_t next_fl, float next_v, uint32_t& eb) {
+    eb = 0;
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) {
+        const uint32_t nb = k + 1 < VEC ? ((fl >> (8 * (k + 1))) & 0xFFu) : (next_fl & 0xFFu);
+        const bool e = (t0 + k + 1 >= p.T) || nb != 0u;
+        eb |= (uint32_t)e << k;
+        if constexpr (GAE) {
+            float nxt;
+            if (p.vn) {
+                nxt = comp<VEC>(vn, k);
+            } else {
+                nxt = k + 1 < VEC ? comp<VEC>(vv, k + 1 < VEC ? k + 1 : k) : next_v;
+                nxt = e ? 0.0f : nxt;
+            }
+            const bool keep = ((dn >> (8 * k)) & 0xFFu) == 0u;
+            const float g = keep ? p.gamma : 0.0f;
+            set_comp<VEC>(x, k, __builtin_fmaf(g, nxt, comp<VEC>(x, k)) - comp<VEC>(vv, k));
+        }
+    }
+    RMap m = rmap_id();
+#pragma unroll
+    for (int k = VEC - 1; k >= 0; --k) m = rmap_then(RMap{p.a, comp<VEC>(x, k), ((eb >> k) & 1u) != 0u}, m);
+    return m;
+}
+
+// Aggregate map of tile `tile` of tape row `row`, computed by one wavefront
+// straight from the inputs (the look-back fallback).  Loads are taken one
+// run of 64*VEC steps at a time, right to left; each lane reads the flag and
+// value after its own steps directly.
+template <int VEC, bool GAE>
+__device__ __forceinline__ RMap tile_map_from_inputs(const DiscArgs& p, int64_t row, int64_t tile) {
+    typedef typename F<VEC>::T V;
+    const int lane = threadIdx.x & 63;
+    constexpr int runs = kDiscTile / (64 * VEC);
+    RMap TM = rmap_id();
+#pragma unroll 1
+    for (int s = runs - 1; s >= 0; --s) {
+        const int64_t t0 = tile * kDiscTile + (int64_t)64 * VEC * s + VEC * lane;
+        const bool ok = t0 < p.T;
+        V x{}, vv{}, vn{};
+        uint32_t fl = 0, dn = 0, next_fl = 1;
+        float next_v = 0.0f;
+        if (ok) {
+            fl = load_flags<VEC>(p.start + row + t0);
+            x = load_vec<VEC>(p.r + row + t0);
+            if (t0 + VEC < p.T) next_fl = p.start[row + t0 + VEC];
+            if constexpr (GAE) {
+                vv = load_vec<VEC>(p.v + row + t0);
+                if (p.vn) vn = load_vec<VEC>(p.vn + row + t0);
+                if (p.done) dn = load_flags<VEC>(p.done + row + t0);
+                if (!p.vn && t0 + VEC < p.T) next_v = p.v[row + t0 + VEC];
+            }
+        }
+        uint32_t eb;
+        const RMap m = lane_map<VEC, GAE>(p, t0, x, vv, vn, fl, dn, next_fl, next_v, eb);
+        TM = rmap_then(rmap_bcast(wave_suffix(m), 0), TM);
+    }
+    return TM;
+}
+
+}  // namespace
+
+template <int VEC, bool GAE>
+__global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
+    constexpr int NB = kRows / VEC;           // loads per lane
+    typedef typename F<VEC>::T V;
+    __shared__ float s_wA[4], s_wH[4];
+    __shared__ int s_wf[4];
+    __shared__ float s_carry;
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int64_t ticket = blockIdx.x;
+    const int64_t j = ticket / p.B;           // tiles counted from the tape's end
+    const int64_t b = ticket - j * p.B;
+    const int64_t i = p.nt - 1 - j;           // tile index from the tape's start
+    const int64_t T = p.T;
+    const int64_t row = b * T;
+    const int64_t t_seg = i * kDiscTile + (int64_t)w * kSeg;
+    const int64_t t_after = t_seg + kSeg;     // first step after this wavefront's steps
+
+    // ------------------------------------------------------------- loads
+    V x[NB], vv[NB] = {}, vn[NB] = {};
+    uint32_t fl[NB], dn[NB] = {};
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+        const int64_t t = t_seg + 64 * VEC * u + VEC * lane;
+        const bool ok = t < T;
+        fl[u] = ok ? load_flags<VEC>(p.start + row + t) : 0u;
+        x[u] = ok ? load_vec<VEC>(p.r + row + t) : V{};
+        if constexpr (GAE) {
+            vv[u] = ok ? load_vec<VEC>(p.v + row + t) : V{};
+            vn[u] = (ok && p.vn) ? load_vec<VEC>(p.vn + row + t) : V{};
+            dn[u] = (ok && p.done) ? load_flags<VEC>(p.done + row + t) : 0u;
+        }
+    }
+    // the step after this wavefront's run: its begin flag (and value)
+    const bool after_in = t_after < T;
+    const uint32_t fl_after = after_in ? p.start[row + t_after] : 1u;
+    float v_after = 0.0f;
+    if constexpr (GAE) {
+        if (after_in && !p.vn) v_after = p.v[row + t_after];
+    }
+
+    // -------------------------------------- per-step inputs and lane maps
+    // e bit k of load u: step is the last of its episode
+    uint32_t ebits[NB];
+    RMap E[NB];                               // exclusive suffix: lanes after this one, same load
+    RMap Bm[NB];                              // whole load (wave-uniform)
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+        const int64_t t0 = t_seg + 64 * VEC * u + VEC * lane;
+        // begin flag (and value) of the step after the lane's last step: the
+        // next lane's first step, or the next load's (or wavefront's) first
+        const uint32_t next_lane_fl = __shfl_down(fl[u], 1, 64);
+        const uint32_t fl_next_run = u + 1 < NB ? __shfl(fl[u + 1 < NB ? u + 1 : u], 0, 64) : fl_after;
+        const uint32_t next_fl = lane < 63 ? next_lane_fl : fl_next_run;
+        float next_v = 0.0f;
+        if constexpr (GAE) {
+            const float nl = __shfl_down(comp<VEC>(vv[u], 0), 1, 64);
+            const float nr = u + 1 < NB ? __shfl(comp<VEC>(vv[u + 1 < NB ? u + 1 : u], 0), 0, 64) : v_after;
+            next_v = lane < 63 ? nl : nr;
+        }
+        const RMap m = lane_map<VEC, GAE>(p, t0, x[u], vv[u], vn[u], fl[u], dn[u], next_fl, next_v, ebits[u]);
+        const RMap S = wave_suffix(m);
+        E[u] = rmap_shfl_down(S, 1);
+        if (lane == 63) E[u] = rmap_id();
+        Bm[u] = rmap_bcast(S, 0);
+    }
+    RMap W = Bm[NB - 1];
+#pragma unroll
+    for (int u = NB - 2; u >= 0; --u) W = rmap_then(Bm[u], W);
+    if (lane == 0) {
+        s_wA[w] = W.A;
+        s_wH[w] = W.H;
+        s_wf[w] = (int)W.f;
+    }
+    __syncthreads();
+    RMap Wt[4];
+#pragma unroll
+    for (int ww = 0; ww < 4; ++ww) Wt[ww] = RMap{s_wA[ww], s_wH[ww], s_wf[ww] != 0};
+    const RMap TM = rmap_then(Wt[0], rmap_then(Wt[1], rmap_then(Wt[2], Wt[3])));
+    const int64_t slot = b * p.nt + j;
+
+    // ------------------------------------------------ publish, look back
+    // Wavefront 3 publishes the tile's aggregate (or, when the tile holds an
+    // episode end, its value at the first step, which then needs nothing from
+    // the right); wavefront 0 polls, so no wavefront both stores and polls.
+    if (w == 3 && lane == 0) {
+        if (TM.f)
+            publish64(p.incl + slot, pack2(TM.H, 0.0f));
+        else
+            publish64(p.agg + slot, pack2(TM.H, TM.A));
+    }
+    if (w == 0) {
+        // a carry is needed unless the tile's last step ends an episode
+        const int64_t t_next_tile = (i + 1) * (int64_t)kDiscTile;
+        const bool need = j > 0 && p.start[row + t_next_tile] == 0;
+        float carry = 0.0f;
+        if (need) {
+            RMap acc = rmap_id();
+            int64_t base = j - 1;
+            uint32_t polls = 0;
+            while (true) {
+                const int64_t pj = base - lane;
+                uint64_t wi = pack2(0.0f, 0.0f), wa = kEmpty64;
+                if (pj >= 0) {
+                    wi = peek64(p.incl + b * p.nt + pj);
+                    if (wi == kEmpty64) wa = peek64(p.agg + b * p.nt + pj);
+                }
+                const bool term = wi != kEmpty64;
+                const bool ready = term || wa != kEmpty64;
+                const uint64_t m_term = __ballot(term);
+                const uint64_t m_nr = __ballot(!ready);
+                const int ft = m_term ? __builtin_ctzll(m_term) : 64;
+                const int fn = m_nr ? __builtin_ctzll(m_nr) : 64;
+                const int upto = ft < fn ? ft : fn;   // lanes before `upto` hold aggregates
+                RMap m = rmap_id();
+                if (lane < upto) m = RMap{unpack_hi(wa), unpack_lo(wa), false};
+                if (ft < fn && lane == ft) m = RMap{1.0f, unpack_lo(wi), true};
+                const RMap R = rmap_bcast(wave_suffix(m), 0);
+                acc = rmap_then(acc, R);
+                if (ft < fn) {
+                    carry = acc.H;
+                    break;
+                }
+                base -= fn;
+                if (fn > 0) {
+                    polls = 0;
+                } else if (++polls > p.fallback_polls) {
+                    // tile `base` has not published: fold its aggregate in
+                    // from its inputs (tile index from the tape's start)
+                    const RMap M = tile_map_from_inputs<VEC, GAE>(p, row, p.nt - 1 - base);
+                    acc = rmap_then(acc, M);
+                    if (M.f) {
+                        carry = acc.H;
+                        break;
+                    }
+                    base -= 1;
+                    polls = 0;
+                } else {
+                    __builtin_amdgcn_s_sleep(1);
+                }
+            }
+        }
+        if (!TM.f && lane == 0) publish64(p.incl + slot, pack2(rmap_apply(TM, carry), 0.0f));
+        if (lane == 0) s_carry = carry;
+    }
+    __syncthreads();
+
+    // ------------------------------------------------------------ outputs
+    float c = s_carry;
+#pragma unroll
+    for (int ww = 3; ww > 0; --ww)
+        if (ww > w) c = rmap_apply(Wt[ww], c);
+#pragma unroll
+    for (int u = NB - 1; u >= 0; --u) {
+        const int64_t t0 = t_seg + 64 * VEC * u + VEC * lane;
+        float y = rmap_apply(E[u], c);
+        V out;
+#pragma unroll
+        for (int k = VEC - 1; k >= 0; --k) {
+            const float xk = comp<VEC>(x[u], k);
+            y = ((ebits[u] >> k) & 1u) ? xk : __builtin_fmaf(p.a, y, xk);
+            set_comp<VEC>(out, k, y);
+        }
+        if (t0 < T) {
+            store_vec<VEC>(p.out + row + t0, out);
+            if constexpr (GAE) {
+                if (p.target) {
+                    V tg;
+#pragma unroll
+                    for (int k = 0; k < VEC; ++k) set_comp<VEC>(tg, k, comp<VEC>(out, k) + comp<VEC>(vv[u], k));
+                    store_vec<VEC>(p.target + row + t0, tg);
+                }
+            }
+        }
+        c = rmap_apply(Bm[u], c);
+    }
+}
+
+hipError_t disc_launch(bool vec, bool gae, const DiscArgs& a, int64_t ntiles, hipStream_t s) {
+    const dim3 grid((unsigned)ntiles), block(256);
+    if (vec) {
+        if (gae)
+            hipLaunchKernelGGL((disc_kernel<4, true>), grid, block, 0, s, a);
+        else
+            hipLaunchKernelGGL((disc_kernel<4, false>), grid, block, 0, s, a);
+    } else {
+        if (gae)
+            hipLaunchKernelGGL((disc_kernel<1, true>), grid, block, 0, s, a);
+        else
+            hipLaunchKernelGGL((disc_kernel<1, false>), grid, block, 0, s, a);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace memoroid

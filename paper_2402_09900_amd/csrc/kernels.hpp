@@ -48,6 +48,7 @@ struct DiagFwdArgs {
     void* agg;         // [tiles][Dp] aggregate descriptor words
     void* incl;        // [tiles][Dp] inclusive-prefix descriptor words
     WsHeader* hdr;
+    uint32_t* ctr;     // per-chain tile counters, kCtrStride words apart
     int32_t* idx;      // episode index out [B][T], or NULL
     uint64_t* cnt;     // [tiles per chain][B] begin-count descriptor words
 };
@@ -70,6 +71,7 @@ struct DiagBwdArgs {
     void* agg;
     void* incl;
     WsHeader* hdr;
+    uint32_t* ctr;     // per-chain tile counters, kCtrStride words apart
 };
 
 hipError_t diag_fwd_launch(int in_kind, int out_kind, bool vec, bool ainv,
@@ -83,7 +85,14 @@ hipError_t colsum_launch(const float* in, float* out, int64_t rows, int64_t cols
 // Fill `bytes` (multiple of 16, 16-byte aligned) at p with 0xFF, and zero the
 // 256-byte header at hdr.  A kernel, not hipMemsetAsync, so that a caller may
 // capture the call in a HIP graph.
-hipError_t ws_init_launch(void* hdr, void* p, size_t bytes, hipStream_t s);
+// Per-chain tile counters sit 128 bytes apart: atomics on one cache line
+// serialise (about 11 ns each on MI355X), atomics on distinct lines do not.
+constexpr int kCtrStride = 32;
+
+// Workspace set-up: zero `zero_bytes` from `zero` (header, counters) and fill
+// `ones_bytes` from `ones` with all-ones bytes (empty descriptors); both
+// sizes multiples of 16.
+hipError_t ws_init_launch(void* zero, size_t zero_bytes, void* ones, size_t ones_bytes, hipStream_t s);
 
 // Linear-attention memoroid: per-(chunk, head) state summaries, and outputs
 // from the scanned chunk states.  A state is S^T (64x64, row n holds column n
@@ -99,7 +108,8 @@ struct LinSummaryArgs {
     uint8_t* R;         // [chunks] chunk holds a begin step
     int64_t T;
     int64_t H;
-    uint32_t* hdr;      // state-scan workspace header (zeroed here)
+    u32x4* zero;        // state-scan header and counters, zeroed here (16-byte units)
+    int64_t zero16;
     u32x4* fill;        // descriptors to fill with all-ones bytes (16-byte units)
     int64_t fill16;
 };
@@ -120,5 +130,28 @@ struct LinOutputArgs {
 
 hipError_t linattn_summary_launch(const LinSummaryArgs& a, hipStream_t s);
 hipError_t linattn_output_launch(const LinOutputArgs& a, hipStream_t s);
+
+// ------------------------------------------- discounted return and GAE
+constexpr int kDiscRows = 16;                       // steps per lane
+constexpr int kDiscTile = 4 * 64 * kDiscRows;       // steps per tile (4 wavefronts)
+
+struct DiscArgs {
+    const float* r;          // [B][T] rewards
+    const float* v;          // [B][T] V(s_t) (advantage only)
+    const float* vn;         // [B][T] V(s'_t) or NULL (advantage only)
+    const uint8_t* done;     // [B][T] terminal flags or NULL (advantage only)
+    const uint8_t* start;    // [B][T] begin flags
+    float* out;              // [B][T] return or advantage
+    float* target;           // [B][T] advantage + V(s_t), or NULL
+    float a;                 // recurrence coefficient: gamma, or gamma * lambda
+    float gamma;             // discount of the TD error (advantage only)
+    int64_t T, nt, B;        // tape length, tiles per tape, tapes
+    uint32_t fallback_polls; // polls without progress before a look-back computes the awaited tile itself
+    uint64_t* agg;           // [B][nt] tile aggregates
+    uint64_t* incl;          // [B][nt] tile values at their first step
+    WsHeader* hdr;
+};
+
+hipError_t disc_launch(bool vec, bool gae, const DiscArgs& a, int64_t ntiles, hipStream_t s);
 
 }  // namespace memoroid

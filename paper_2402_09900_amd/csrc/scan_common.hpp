@@ -501,7 +501,7 @@ __device__ __forceinline__ uint32_t count_lookback(const uint64_t* desc, int64_t
 
 // Workspace header shared by the scan kernels (first 256 bytes).
 struct WsHeader {
-    uint32_t ticket;     // next tile ticket
+    uint32_t reserved;   // zero
     uint32_t timeout;    // nonzero: some wait gave up
     uint32_t pad[62];
 };

@@ -160,6 +160,8 @@ class Workload:
     dk: int = 0
     dv: int = 0
     chunk: int = 0
+    gamma: float = 0.0        # discount (returns / advantages)
+    lam: float = 0.0          # GAE lambda
 
     def describe(self) -> str:
         return self.name
@@ -176,6 +178,8 @@ WORKLOADS: Dict[int, Workload] = {
                 False, (0.8, 0.999), _uniform_int(10, 1000), False),
     5: Workload(5, "diag_real_f32_T1048576_d256_lognormal5_1.5_fwd_bwd", "diag", 1, 1 << 20, 256, "f32", "f32",
                 False, (0.5, 0.99), _lognormal(5.0, 1.5), True),
+    6: Workload(6, "return_gae_f32_T16777216_unif1_1000_g0.99_l0.95", "discount", 1, 1 << 24, 1, "f32", "f32",
+                False, (0.0, 0.0), _uniform_int(1, 1000), False, gamma=0.99, lam=0.95),
 }
 
 
@@ -307,3 +311,50 @@ def make_custom_diag(dtype: str, B: int, T: int, d: int, a_invariant: bool, seed
             g = None
     return DiagTape(a=a, x=x, start=start, g=g, dtype=dtype, out_dtype=out_dtype or dtype,
                     B=B, T=T, d=d, a_invariant=a_invariant)
+
+
+@dataclasses.dataclass
+class DiscountTape:
+    """Transitions of an RL tape for the return / advantage workloads.
+
+    r, v, vn: float32 [B,T] (reward, V(s_t), V(s'_t)); done, start: uint8 [B,T]."""
+    r: np.ndarray
+    v: np.ndarray
+    vn: np.ndarray
+    done: np.ndarray
+    start: np.ndarray
+    gamma: float
+    lam: float
+    B: int
+    T: int
+
+
+def make_discount(key: int = 6, seed: Optional[int] = None, B: Optional[int] = None, T: Optional[int] = None,
+                  episodes: Optional[Callable] = None, done_rate: float = 0.5) -> DiscountTape:
+    """Rewards and values of a tape of episodes.  Draw order: episode lengths
+    (per tape), rewards ~ N(0,1), values V(s_t) ~ N(0,1), the value of each
+    episode's final next state ~ N(0,1), then each episode end is terminal
+    with probability done_rate (except at the tape end, where the episode is
+    cut off, not finished).  Inside an episode V(s'_t) = V(s_{t+1})."""
+    w = WORKLOADS[key]
+    assert w.kind == "discount"
+    B = w.B if B is None else B
+    T = w.T if T is None else T
+    law = w.episodes if episodes is None else episodes
+    rng = np.random.Generator(np.random.PCG64(key if seed is None else seed))
+    start = (np.stack([law(rng, T) for _ in range(B)]) if T > 0 else np.zeros((B, 0), np.uint8))
+    start = start.reshape(B, T).astype(np.uint8)
+    r = _normal_f32(rng, (B, T))
+    v = _normal_f32(rng, (B, T))
+    boot = _normal_f32(rng, (B, T))
+    coin = rng.random((B, T)) < done_rate
+    ends = np.zeros((B, T), dtype=bool)
+    if T > 0:
+        ends[:, :-1] = start[:, 1:] != 0
+    vn = np.empty((B, T), dtype=np.float32)
+    if T > 0:
+        vn[:, :-1] = v[:, 1:]
+        vn[:, -1] = boot[:, -1]
+    vn[ends] = boot[ends]
+    done = (ends & coin).astype(np.uint8)
+    return DiscountTape(r=r, v=v, vn=vn, done=done, start=start, gamma=w.gamma, lam=w.lam, B=B, T=T)

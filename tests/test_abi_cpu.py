@@ -124,6 +124,36 @@ def test_linattn_validation():
     assert la(workspace_bytes=1000) == mb.EWORKSPACE
 
 
+def test_discount_validation():
+    def ret(**kw):
+        args = dict(r=A, start=S, gamma=0.99, G=H, B=2, T=100, workspace=W, workspace_bytes=1 << 30, stream=None)
+        args.update(kw)
+        return mb.memoroid_discounted_return(*args.values())
+
+    def gae(**kw):
+        args = dict(r=A, value=X, value_next=None, done=None, start=S, gamma=0.99, lam=0.95, adv=H, target=I,
+                    B=2, T=100, workspace=W, workspace_bytes=1 << 30, stream=None)
+        args.update(kw)
+        return mb.memoroid_gae(*args.values())
+    assert mb.memoroid_discount_workspace_bytes(1, 1 << 24) > mb.memoroid_discount_workspace_bytes(1, 4096) > 0
+    assert mb.memoroid_discount_workspace_bytes(0, 10) == 0
+    for f in (ret, gae):
+        assert f(B=-1) == mb.EINVAL
+        assert f(B=0) == mb.OK and f(T=0) == mb.OK
+        assert f(gamma=1.5) == mb.EINVAL and f(gamma=-0.1) == mb.EINVAL and f(gamma=float("nan")) == mb.EINVAL
+        assert f(r=None) == mb.EINVAL and f(start=None) == mb.EINVAL
+        assert f(r=A + 2) == mb.EINVAL                 # misaligned f32
+        assert f(workspace=None) == mb.EWORKSPACE
+        assert f(workspace_bytes=64) == mb.EWORKSPACE
+        assert f(B=1 << 40, T=1 << 40) == mb.EINVAL
+    assert ret(G=A) == mb.EINVAL                       # output aliases input
+    assert ret(G=None) == mb.EINVAL
+    assert gae(lam=2.0) == mb.EINVAL
+    assert gae(value=None) == mb.EINVAL and gae(adv=None) == mb.EINVAL
+    assert gae(adv=X) == mb.EINVAL and gae(target=A) == mb.EINVAL and gae(target=H) == mb.EINVAL
+    assert gae(value_next=0x70000, done=0x80000, target=None, B=0) == mb.OK
+
+
 def test_torch_layer_rejects_cpu_tensors():
     torch = pytest.importorskip("torch")
     a = torch.rand(4, 8)
