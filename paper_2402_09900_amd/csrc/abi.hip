@@ -64,6 +64,11 @@ bool plan_diag(int64_t B, int64_t T, int64_t d, int state_dtype, bool vec, int r
     if (!mul_ok(B, p->nfb, &p->nchains)) return false;
     if (!mul_ok(p->nt, p->nchains, &p->ntiles)) return false;
     if (p->ntiles >= (int64_t)INT32_MAX || p->nchains >= (int64_t)INT32_MAX) return false;
+    // a tile's rows (plus one step on each side) are addressed with 32-bit
+    // buffer offsets below 2^31
+    // (4 bytes at least: bf16 input may be written as f32)
+    const int64_t wb = elem_bytes(state_dtype) > 4 ? elem_bytes(state_dtype) : 4;
+    if ((p->L + 2) * d * wb >= (int64_t)INT32_MAX) return false;
     const bool cplx = state_dtype == MEMOROID_C64;
     const size_t agg_b = cplx ? 16 : 8, incl_b = cplx ? 8 : 4;
     int64_t ndesc;

@@ -47,7 +47,7 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
         s_ticket = __hip_atomic_fetch_add(p.ctr + (size_t)chain * kCtrStride, 1u, __ATOMIC_RELAXED,
                                           __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
-    const int64_t k = s_ticket;
+    const int64_t k = (int64_t)__builtin_amdgcn_readfirstlane(s_ticket);
     const uint32_t ticket = (uint32_t)(k * p.nchains + chain);
     const int64_t tile = p.nt - 1 - k;              // tiles run from the tape end
     const int b = chain / p.nfb;
@@ -69,32 +69,42 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     const int64_t rowbase = (int64_t)b * T;
     const bool want_da = AINV ? p.da_part != nullptr : p.da != nullptr;
 
-    // ---- loads.  The begin flags of the lane's steps t and t+1 (and of the
-    // step after the tile) first, by unconditional byte loads at clamped
-    // addresses, so that waiting for them leaves every data load in flight;
-    // then g_t, a_{t+1} and h_{t-1} of every step, one wide access each.
+    // ---- loads, through buffer resources based at the tile's first step of
+    // this tape: rows past T and lanes past d read zeros and their stores are
+    // dropped, and so are a_{t+1} at t + 1 = T and h_{t-1} at t = 0 (offsets
+    // out of range; both are unused there).  The begin flags of the lane's
+    // steps t and t+1 (and of the step after the tile) go first, so that
+    // waiting for them leaves every data load in flight; then g_t, a_{t+1}
+    // and h_{t-1} of every step, one wide access each.
+    const int64_t rows_left = T - tile_row0;
+    const int64_t tape_row0 = rowbase + tile_row0;
+    const int64_t rowB = p.d * EB;
+    const uint32_t lrow = (uint32_t)((wave * Gw + j) * R);
+    const Rsrc rs_st = make_rsrc(st + tile_row0, rows_left);
+    const Rsrc rs_g = make_rsrc((const char*)p.g + tape_row0 * rowB, rows_left * rowB);
+    const Rsrc rs_a = make_rsrc(AINV ? p.a : (const char*)p.a + tape_row0 * rowB, AINV ? 0 : rows_left * rowB);
+    // h_{t-1}: based one step before the tile (when there is one), so the
+    // tile's first step reads the previous tile's last h
+    const int64_t h_back = tile_row0 > 0 ? 1 : 0;
+    const Rsrc rs_h = make_rsrc(want_da ? (const char*)p.h + (tape_row0 - h_back) * rowB : p.g,
+                                want_da ? (rows_left + h_back) * rowB : 0);
+    const uint32_t step = active ? (uint32_t)rowB : 0u;
+    const uint32_t off0 = active ? (uint32_t)((int64_t)lrow * rowB + f0 * EB) : kOob;
     uint32_t fl[R + 1];
 #pragma unroll
-    for (int r = 0; r <= R; ++r) {
-        const int64_t t = row0 + r < T ? row0 + r : T - 1;
-        fl[r] = st[t];
-    }
+    for (int r = 0; r <= R; ++r) fl[r] = bload_u8(rs_st, lrow + r);
     const int64_t t_last = (tile_row0 + L < T ? tile_row0 + L : T) - 1;
-    const uint32_t fl_after = st[t_last + 1 < T ? t_last + 1 : T - 1];
+    const uint32_t fl_after = bload_u8(rs_st, (uint32_t)(t_last + 1 - tile_row0));
     __builtin_amdgcn_sched_barrier(0);
     RawVec<K, VEC> rg[R];
     RawVec<K, VEC> ra[AINV ? 1 : R];
     RawVec<K, VEC> rh[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-        const int64_t t = row0 + r;
-        if (active && t < T) {
-            raw_load(rg[r], (const char*)p.g + ((rowbase + t) * p.d + f0) * EB);
-            if constexpr (!AINV) {
-                if (t + 1 < T) raw_load(ra[r], (const char*)p.a + ((rowbase + t + 1) * p.d + f0) * EB);
-            }
-            if (want_da && t > 0) raw_load(rh[r], (const char*)p.h + ((rowbase + t - 1) * p.d + f0) * EB);
-        }
+        const uint32_t off = off0 + r * step;
+        raw_bload(rg[r], rs_g, off);
+        if constexpr (!AINV) raw_bload(ra[r], rs_a, off + step);
+        if (want_da) raw_bload(rh[r], rs_h, h_back ? off : off - step);
     }
     __builtin_amdgcn_sched_barrier(0);
     uint32_t ends = 0, begins = 0, valid = 0;
@@ -118,23 +128,21 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
         else return conj(C::get(ra[r], v));
     };
 
-    // ---- per-lane summary, walking its R steps backwards
+    // ---- per-lane summary, walking its R steps backwards.  Steps past T
+    // hold zeros and come before the tape's last step, which ends an episode,
+    // so they never reach a real output.
     SegT own = seg_identity<S, VEC>();
 #pragma unroll
     for (int r = R - 1; r >= 0; --r) {
-        if (!((valid >> r) & 1u)) continue;
         const bool e = (ends >> r) & 1u;
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {
             const S gv = C::get(rg[r], v);
-            if (e) {
-                own.A[v] = s_one<S>();
-                own.H[v] = gv;
-            } else {
-                const S cv = coef(r, v);
-                own.H[v] = mad(cv, own.H[v], gv);
-                own.A[v] = own.A[v] * cv;
-            }
+            const S cv = coef(r, v);
+            const S nh = mad(cv, own.H[v], gv);
+            const S na = own.A[v] * cv;
+            own.H[v] = e ? gv : nh;
+            own.A[v] = e ? s_one<S>() : na;
         }
     }
     own.f = ends != 0;
@@ -218,20 +226,20 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
                 lam[v] = e ? gv : mad(coef(r, v), lam[v], gv);
                 const S dav = bg ? s_zero<S>() : lam[v] * conj(C::get(rh[r], v));
                 if constexpr (AINV) {
-                    if ((valid >> r) & 1u) dsum[v] = dsum[v] + dav;
+                    dsum[v] = dsum[v] + dav;             // zero past T (h reads zeros there)
                 } else {
                     C::put(ra[r], v, dav);
                 }
                 C::put(rg[r], v, lam[v]);
             }
         }
+        const Rsrc rs_dx = make_rsrc((char*)p.dx + tape_row0 * rowB, rows_left * rowB);
+        const Rsrc rs_da = make_rsrc(AINV ? p.dx : (char*)p.da + tape_row0 * rowB, AINV ? 0 : rows_left * rowB);
 #pragma unroll
         for (int r = R - 1; r >= 0; --r) {
-            if (!((valid >> r) & 1u)) continue;
-            const int64_t off = ((rowbase + row0 + r) * p.d + f0) * EB;
-            raw_store_nt((char*)p.dx + off, rg[r]);
+            raw_bstore_nt(rs_dx, off0 + r * step, rg[r]);
             if constexpr (!AINV) {
-                if (want_da) raw_store_nt((char*)p.da + off, ra[r]);
+                if (want_da) raw_bstore_nt(rs_da, off0 + r * step, ra[r]);
             }
         }
     }

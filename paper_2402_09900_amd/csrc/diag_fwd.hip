@@ -73,7 +73,7 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
         s_ticket = __hip_atomic_fetch_add(p.ctr + (size_t)chain * kCtrStride, 1u, __ATOMIC_RELAXED,
                                           __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
-    const int64_t tile = s_ticket;
+    const int64_t tile = (int64_t)__builtin_amdgcn_readfirstlane(s_ticket);
     const uint32_t ticket = (uint32_t)(tile * p.nchains + chain);
     const int b = chain / p.nfb;
     const int fb = chain - b * p.nfb;
@@ -91,28 +91,31 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     const bool active = f0 < p.d;
     const uint8_t* st = p.start + (int64_t)b * p.T;
 
-    // ---- (1) loads.  Flags of the lane's own steps (and of the tile's first
-    // step) first, by unconditional byte loads at clamped addresses, so that
+    // ---- (1) loads, through buffer resources based at the tile's first
+    // step of this tape: rows past T and lanes past d read zeros (their
+    // offsets are out of range) and their stores are dropped.  Flags of the
+    // lane's own steps (and of the tile's first step) go first, so that
     // waiting for them leaves every data load in flight; then one wide access
     // per step and tensor.
+    const int64_t rows_left = p.T - tile_row0;             // steps from the tile's first to T
+    const int64_t tape_row0 = (int64_t)b * p.T + tile_row0;
+    const uint32_t lrow = (uint32_t)((wave * Gw + j) * R);  // lane's first step within the tile
+    const Rsrc rs_st = make_rsrc(st + tile_row0, rows_left);
+    const Rsrc rs_x = make_rsrc((const char*)p.x + tape_row0 * p.d * IB, rows_left * p.d * IB);
+    const Rsrc rs_a = make_rsrc(AINV ? p.a : (const char*)p.a + tape_row0 * p.d * IB, AINV ? 0 : rows_left * p.d * IB);
+    const uint32_t in_step = active ? (uint32_t)(p.d * IB) : 0u;
+    const uint32_t in_off = active ? (uint32_t)((int64_t)lrow * p.d * IB + f0 * IB) : kOob;
     uint32_t fl[R];
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const int64_t t = row0 + r < p.T ? row0 + r : p.T - 1;
-        fl[r] = st[t];
-    }
-    const uint32_t fl_tile0 = st[tile_row0];
+    for (int r = 0; r < R; ++r) fl[r] = bload_u8(rs_st, lrow + r);
+    const uint32_t fl_tile0 = bload_u8(rs_st, 0);
     __builtin_amdgcn_sched_barrier(0);
     RawVec<IN, VEC> ra[AINV ? 1 : R];
     RawVec<IN, VEC> rx[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-        const int64_t t = row0 + r;
-        if (active && t < p.T) {
-            const int64_t off = ((int64_t)b * p.T + t) * p.d + f0;
-            raw_load(rx[r], (const char*)p.x + off * IB);
-            if constexpr (!AINV) raw_load(ra[r], (const char*)p.a + off * IB);
-        }
+        raw_bload(rx[r], rs_x, in_off + r * in_step);
+        if constexpr (!AINV) raw_bload(ra[r], rs_a, in_off + r * in_step);
     }
     __builtin_amdgcn_sched_barrier(0);
     uint32_t begins = 0, valid = 0;
@@ -138,23 +141,21 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
         else return CIn::get(ra[r], v);
     };
 
-    // ---- (2) per-lane summary of its R steps (steps past T are identities)
+    // ---- (2) per-lane summary of its R steps.  Steps past T hold zeros and
+    // come after every real step, so they only touch summaries that no real
+    // output uses.
     SegT own = seg_identity<S, VEC>();
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-        if (!((valid >> r) & 1u)) continue;
         const bool bg = (begins >> r) & 1u;
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {
             const S xv = CIn::get(rx[r], v);
-            if (bg) {
-                own.A[v] = s_one<S>();
-                own.H[v] = xv;
-            } else {
-                const S av = a_at(r, v);
-                own.H[v] = mad(av, own.H[v], xv);
-                own.A[v] = own.A[v] * av;
-            }
+            const S av = a_at(r, v);
+            const S nh = mad(av, own.H[v], xv);
+            const S na = own.A[v] * av;
+            own.H[v] = bg ? xv : nh;
+            own.A[v] = bg ? s_one<S>() : na;
         }
     }
     own.f = begins != 0;
@@ -270,7 +271,6 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
             }
         }
     }
-    if (!active) return;
     constexpr bool kInPlace = (int)IN == (int)OUT;
     RawVec<OUT, VEC> o[kInPlace ? 1 : R];
 #pragma unroll
@@ -280,16 +280,17 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
         for (int v = 0; v < VEC; ++v) {
             const S xv = CIn::get(rx[r], v);
             hv[v] = bg ? xv : mad(a_at(r, v), hv[v], xv);
-            if constexpr (kInPlace) CIn::put(rx[r], v, hv[v]);
-            else COut::put(o[r], v, hv[v]);
         }
+        if constexpr (kInPlace) CIn::put_all(rx[r], hv);
+        else COut::put_all(o[r], hv);
     }
+    const Rsrc rs_h = make_rsrc((char*)p.h + tape_row0 * p.d * OB, rows_left * p.d * OB);
+    const uint32_t out_step = active ? (uint32_t)(p.d * OB) : 0u;
+    const uint32_t out_off = active ? (uint32_t)((int64_t)lrow * p.d * OB + f0 * OB) : kOob;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-        if (!((valid >> r) & 1u)) continue;
-        const int64_t off = ((int64_t)b * p.T + row0 + r) * p.d + f0;
-        if constexpr (kInPlace) raw_store_nt((char*)p.h + off * OB, rx[r]);
-        else raw_store_nt((char*)p.h + off * OB, o[r]);
+        if constexpr (kInPlace) raw_bstore_nt(rs_h, out_off + r * out_step, rx[r]);
+        else raw_bstore_nt(rs_h, out_off + r * out_step, o[r]);
     }
 }
 

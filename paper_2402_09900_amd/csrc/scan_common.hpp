@@ -57,12 +57,16 @@ template <> struct StateOf<K_C64> { using type = cf; };
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-// float -> bf16 bits, round to nearest even; NaN stays a quiet NaN.
-__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x0040u;
-    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+// float -> bf16 bits, round to nearest even (NaN stays NaN), by the
+// hardware conversion; f32x2_to_bf16x2 converts two values with one
+// instruction and packs them, the first in the low half.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t f32x2_to_bf16x2(float lo, float hi) {
+    const f32x2_t f = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
 }
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) { return f32x2_to_bf16x2(f, 0.0f) & 0xFFFFu; }
 
 // -------------------------------------------------------------- raw vectors
 // RawVec<K, VEC> holds VEC elements of kind K in their storage format, in
@@ -74,9 +78,36 @@ template <Kind K, int VEC> struct RawVec {
     uint32_t w[WORDS];
 };
 
+// ------------------------------------------------------- buffer access
+// Raw buffer loads and stores: 32-bit byte offsets from a base held in
+// scalar registers, with the range check done by the memory pipeline -- a
+// load at or past the resource's byte count returns zeros and a store there
+// is dropped -- so the edges of a tile need no branches or masks.  Every
+// offset goes in the per-lane (range-checked) operand; the scalar offset,
+// which the check does not cover, is always 0.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr int kRsrcWord3 = 0x00020000;       // gfx9 raw buffer, 32-bit data format
+constexpr uint32_t kOob = 0x80000000u;       // an offset past every resource's range
+constexpr int kNt = 2;                       // cache policy: non-temporal
+
+__device__ __forceinline__ Rsrc make_rsrc(const void* base, int64_t bytes) {
+    const int n = bytes >= 0x7FFFFFFF ? 0x7FFFFFFF : (bytes <= 0 ? 0 : (int)bytes);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, kRsrcWord3);
+}
+
+__device__ __forceinline__ uint32_t bload_u8(Rsrc r, uint32_t off) {
+    return (uint32_t)__builtin_amdgcn_raw_buffer_load_b8(r, (int)off, 0, 0);
+}
+
 template <int BYTES> struct WideAccess;
 
 template <> struct WideAccess<2> {
+    template <int W> __device__ static void bload(uint32_t (&w)[W], Rsrc r, uint32_t off) {
+        w[0] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0);
+    }
+    template <int W> __device__ static void bstore_nt(Rsrc r, uint32_t off, const uint32_t (&w)[W]) {
+        __builtin_amdgcn_raw_buffer_store_b16((unsigned short)w[0], r, (int)off, 0, kNt);
+    }
     template <int W> __device__ static void load(uint32_t (&w)[W], const void* p) {
         w[0] = *(const uint16_t*)p;
     }
@@ -85,6 +116,12 @@ template <> struct WideAccess<2> {
     }
 };
 template <> struct WideAccess<4> {
+    template <int W> __device__ static void bload(uint32_t (&w)[W], Rsrc r, uint32_t off) {
+        w[0] = __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0);
+    }
+    template <int W> __device__ static void bstore_nt(Rsrc r, uint32_t off, const uint32_t (&w)[W]) {
+        __builtin_amdgcn_raw_buffer_store_b32(w[0], r, (int)off, 0, kNt);
+    }
     template <int W> __device__ static void load(uint32_t (&w)[W], const void* p) {
         w[0] = *(const uint32_t*)p;
     }
@@ -93,6 +130,14 @@ template <> struct WideAccess<4> {
     }
 };
 template <> struct WideAccess<8> {
+    template <int W> __device__ static void bload(uint32_t (&w)[W], Rsrc r, uint32_t off) {
+        const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0);
+        w[0] = v.x; w[1] = v.y;
+    }
+    template <int W> __device__ static void bstore_nt(Rsrc r, uint32_t off, const uint32_t (&w)[W]) {
+        const u32x2 v = {w[0], w[1]};
+        __builtin_amdgcn_raw_buffer_store_b64(v, r, (int)off, 0, kNt);
+    }
     template <int W> __device__ static void load(uint32_t (&w)[W], const void* p) {
         u32x2 v = *(const u32x2*)p;
         w[0] = v.x; w[1] = v.y;
@@ -103,6 +148,14 @@ template <> struct WideAccess<8> {
     }
 };
 template <> struct WideAccess<16> {
+    template <int W> __device__ static void bload(uint32_t (&w)[W], Rsrc r, uint32_t off) {
+        const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+        w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+    }
+    template <int W> __device__ static void bstore_nt(Rsrc r, uint32_t off, const uint32_t (&w)[W]) {
+        const u32x4 v = {w[0], w[1], w[2], w[3]};
+        __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)off, 0, kNt);
+    }
     template <int W> __device__ static void load(uint32_t (&w)[W], const void* p) {
         u32x4 v = *(const u32x4*)p;
         w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
@@ -113,6 +166,18 @@ template <> struct WideAccess<16> {
     }
 };
 template <> struct WideAccess<32> {
+    template <int W> __device__ static void bload(uint32_t (&w)[W], Rsrc r, uint32_t off) {
+        const u32x4 v0 = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+        const u32x4 v1 = __builtin_amdgcn_raw_buffer_load_b128(r, (int)(off + 16u), 0, 0);
+        w[0] = v0.x; w[1] = v0.y; w[2] = v0.z; w[3] = v0.w;
+        w[4] = v1.x; w[5] = v1.y; w[6] = v1.z; w[7] = v1.w;
+    }
+    template <int W> __device__ static void bstore_nt(Rsrc r, uint32_t off, const uint32_t (&w)[W]) {
+        const u32x4 v0 = {w[0], w[1], w[2], w[3]};
+        const u32x4 v1 = {w[4], w[5], w[6], w[7]};
+        __builtin_amdgcn_raw_buffer_store_b128(v0, r, (int)off, 0, kNt);
+        __builtin_amdgcn_raw_buffer_store_b128(v1, r, (int)(off + 16u), 0, kNt);
+    }
     template <int W> __device__ static void load(uint32_t (&w)[W], const void* p) {
         u32x4 v0 = ((const u32x4*)p)[0];
         u32x4 v1 = ((const u32x4*)p)[1];
@@ -137,12 +202,26 @@ __device__ __forceinline__ void raw_store_nt(void* p, const RawVec<K, VEC>& r) {
     WideAccess<RawVec<K, VEC>::BYTES>::store_nt(p, r.w);
 }
 
+template <Kind K, int VEC>
+__device__ __forceinline__ void raw_bload(RawVec<K, VEC>& r, Rsrc rs, uint32_t off) {
+    WideAccess<RawVec<K, VEC>::BYTES>::bload(r.w, rs, off);
+}
+
+template <Kind K, int VEC>
+__device__ __forceinline__ void raw_bstore_nt(Rsrc rs, uint32_t off, const RawVec<K, VEC>& r) {
+    WideAccess<RawVec<K, VEC>::BYTES>::bstore_nt(rs, off, r.w);
+}
+
 // decode element i of a raw vector into its state type
 template <Kind K, int VEC> struct Codec;
 
 template <int VEC> struct Codec<K_F32, VEC> {
     __device__ static float get(const RawVec<K_F32, VEC>& r, int i) { return __uint_as_float(r.w[i]); }
     __device__ static void put(RawVec<K_F32, VEC>& r, int i, float v) { r.w[i] = __float_as_uint(v); }
+    __device__ static void put_all(RawVec<K_F32, VEC>& r, const float (&v)[VEC]) {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) r.w[i] = __float_as_uint(v[i]);
+    }
 };
 template <int VEC> struct Codec<K_BF16, VEC> {
     __device__ static float get(const RawVec<K_BF16, VEC>& r, int i) {
@@ -153,6 +232,14 @@ template <int VEC> struct Codec<K_BF16, VEC> {
         if (i & 1) r.w[i >> 1] = (r.w[i >> 1] & 0x0000FFFFu) | (b << 16);
         else r.w[i >> 1] = (r.w[i >> 1] & 0xFFFF0000u) | b;
     }
+    __device__ static void put_all(RawVec<K_BF16, VEC>& r, const float (&v)[VEC]) {
+        if constexpr (VEC == 1) {
+            r.w[0] = f32_to_bf16(v[0]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < VEC / 2; ++i) r.w[i] = f32x2_to_bf16x2(v[2 * i], v[2 * i + 1]);
+        }
+    }
 };
 template <int VEC> struct Codec<K_C64, VEC> {
     __device__ static cf get(const RawVec<K_C64, VEC>& r, int i) {
@@ -161,6 +248,10 @@ template <int VEC> struct Codec<K_C64, VEC> {
     __device__ static void put(RawVec<K_C64, VEC>& r, int i, cf v) {
         r.w[2 * i] = __float_as_uint(v.re);
         r.w[2 * i + 1] = __float_as_uint(v.im);
+    }
+    __device__ static void put_all(RawVec<K_C64, VEC>& r, const cf (&v)[VEC]) {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) put(r, i, v[i]);
     }
 };
 
