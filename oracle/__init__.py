@@ -55,9 +55,10 @@ def _load():
         D = ctypes.c_double
         lib.oracle_discounted_return.argtypes = [P, P, D, I64, I64, P, P]
         lib.oracle_gae.argtypes = [P, P, P, P, P, D, D, I64, I64, P, P, P, P]
+        lib.oracle_ffm.argtypes = [P, P, P, P, I64, I64, I64, I64, P, P]
         for name in ("oracle_episode_idx", "oracle_diag_fwd", "oracle_diag_fwd_c",
                      "oracle_diag_bwd", "oracle_diag_bwd_c", "oracle_linattn",
-                     "oracle_discounted_return", "oracle_gae"):
+                     "oracle_discounted_return", "oracle_gae", "oracle_ffm"):
             getattr(lib, name).restype = None
         _lib = lib
     return _lib
@@ -195,3 +196,27 @@ def gae(r, v, start, gamma, lam, vn=None, done=None):
     _load().oracle_gae(_ptr(r2), _ptr(v2), _ptr(vn2), _ptr(d2), _ptr(s), float(gamma), float(lam), B, T,
                        *[_ptr(o) for o in out])
     return tuple(o.reshape(shape) for o in out)
+
+
+def ffm(alpha, omega, x, start):
+    """FFM aggregator state.  alpha [m], omega [c], x [B,T,m] (or [T,m]) real,
+    start [B,T].  Returns (S, m) with S complex128 [B,T,m,c] and m its
+    magnitude companion (float64, same shape)."""
+    x = np.asarray(x, dtype=np.float64)
+    squeeze = x.ndim == 2
+    if squeeze:
+        x = x[None]
+    B, T, m = x.shape
+    alpha = np.ascontiguousarray(alpha, dtype=np.float64)
+    omega = np.ascontiguousarray(omega, dtype=np.float64)
+    if alpha.shape != (m,):
+        raise ValueError("alpha must have shape [m]")
+    c = omega.shape[0]
+    x = np.ascontiguousarray(x)
+    s = _flags(start, B, T)
+    S = np.empty((B, T, m, c), dtype=np.complex128)
+    mo = np.empty((B, T, m, c), dtype=np.float64)
+    _load().oracle_ffm(_ptr(alpha), _ptr(omega), _ptr(x), _ptr(s), B, T, m, c, _ptr(S), _ptr(mo))
+    if squeeze:
+        return S[0], mo[0]
+    return S, mo

@@ -254,3 +254,33 @@ void oracle_gae(const double* r, const double* v, const double* vn, const uint8_
         }
     }
 }
+
+/* ---------------------------------------------------------------- FFM */
+
+void oracle_ffm(const double* alpha, const double* omega, const double* x, const uint8_t* start,
+                int64_t B, int64_t T, int64_t m, int64_t c, double* S, double* m_out) {
+    for (int64_t b = 0; b < B; ++b) {
+        for (int64_t j = 0; j < m; ++j) {
+            const double mag = exp(-fabs(alpha[j]));
+            for (int64_t k = 0; k < c; ++k) {
+                const double complex g = mag * cexp(I * omega[k]);
+                double complex s = 0.0;
+                double sm = 0.0;
+                for (int64_t t = 0; t < T; ++t) {
+                    const double xv = x[(b * T + t) * m + j];
+                    if (is_begin(start, T, b, t)) {
+                        s = xv;
+                        sm = fabs(xv);
+                    } else {
+                        s = s * g + xv;
+                        sm = sm * mag + fabs(xv);
+                    }
+                    const int64_t o = ((b * T + t) * m + j) * c + k;
+                    S[2 * o] = creal(s);
+                    S[2 * o + 1] = cimag(s);
+                    if (m_out) m_out[o] = sm;
+                }
+            }
+        }
+    }
+}

@@ -102,6 +102,18 @@ void oracle_linattn(const double* q, const double* k, const double* v,
                     const uint8_t* start, int64_t T, int64_t H, int64_t dk, int64_t dv,
                     double* out, double* m);
 
+/* Fast-and-forgetful-memory aggregator (App. G.4, FFM memoroid): per step a
+ * complex m x c state
+ *   S_t = x_t 1_c^T                          at a begin step,
+ *   S_t = S_{t-1} (.) gamma + x_t 1_c^T      otherwise,
+ * with gamma[j][k] = exp(-|alpha_j| + i omega_k) (the outer sum of the paper's
+ * memoroid, one step of its time count).  x: [B][T][m] real; S: [B][T][m][c]
+ * interleaved complex; alpha[m], omega[c].
+ * m_out (optional, [B][T][m][c]): magnitude companion, the same recurrence on
+ * |gamma| = exp(-|alpha_j|) and |x|. */
+void oracle_ffm(const double* alpha, const double* omega, const double* x, const uint8_t* start,
+                int64_t B, int64_t T, int64_t m, int64_t c, double* S, double* m_out);
+
 /* Discounted return over a tape (App. D, discounted-return memoroid; the
  * done-flag convention of Section 2): for every step, the discounted sum of
  * the rewards from that step to the end of its episode,

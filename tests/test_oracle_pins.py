@@ -703,3 +703,66 @@ def test_gae_done_cuts_bootstrap_only():
     ref = [sum(0.5 ** l * delta[t + l] for l in range(T - t)) for t in range(T)]
     assert list(adv) == ref
     assert np.all(m >= np.abs(adv))
+
+
+# ------------------------------------------------------------------ FFM
+# App. G.4: (X, t) . (X', t') = (X (.) exp(t' (-|alpha| (+) i omega)) + X', t + t'),
+# e_I = (0, 0), f(x) = (x 1_c^T, 1): the state decays by the step count of the
+# later operand.
+
+
+def ffm_paper_fold(alpha, omega, xs, rnd):
+    """e_I . f(x_0) . ... . f(x_n) under a random bracketing, evaluated with
+    the time-count form of the paper (exp of t' times the exponent)."""
+    expo = -np.abs(alpha)[:, None] + 1j * omega[None, :]
+
+    def op(p, q):
+        (X, t), (X2, t2) = p, q
+        return (X * np.exp(t2 * expo) + X2, t + t2)
+    m, c = len(alpha), len(omega)
+    items = [(np.zeros((m, c), complex), 0)] + [(np.repeat(x[:, None], c, axis=1).astype(complex), 1) for x in xs]
+    while len(items) > 1:
+        k = rnd.randrange(len(items) - 1)
+        items[k:k + 2] = [op(items[k], items[k + 1])]
+    return items[0][0]
+
+
+def test_ffm_equals_paper_time_count_monoid():
+    rnd = random.Random(12)
+    rng = np.random.default_rng(12)
+    m, c, T = 3, 4, 60
+    alpha = rng.uniform(-0.3, 0.3, m)
+    omega = rng.uniform(-3, 3, c)
+    flags = tapes.flags_from_lengths(rng.integers(1, 25, size=10), T)
+    x = rng.standard_normal((T, m))
+    S, _ = oracle.ffm(alpha, omega, x, flags)
+    for s, e in _episode_slices(flags):
+        for t in range(s, e):
+            ref = ffm_paper_fold(alpha, omega, x[s:t + 1], rnd)
+            np.testing.assert_allclose(S[t], ref, rtol=1e-12, atol=1e-12)
+
+
+def test_ffm_constant_input_geometric_series():
+    """x = 1 through one episode: S_n = (1 - gamma^(n+1)) / (1 - gamma)."""
+    alpha, omega = np.array([0.01, 0.5]), np.array([0.2, -1.3, 2.9])
+    T = 400
+    S, m = oracle.ffm(alpha, omega, np.ones((T, 2)), np.zeros(T, np.uint8))
+    g = np.exp(-np.abs(alpha)[:, None] + 1j * omega[None, :])
+    n = np.arange(T)[:, None, None]
+    np.testing.assert_allclose(S, (1 - g[None] ** (n + 1)) / (1 - g[None]), rtol=1e-12, atol=1e-12)
+    assert np.all(m >= np.abs(S) - 1e-12)
+
+
+def test_ffm_without_rotation_is_the_real_diagonal_scan():
+    """omega = 0: every column is the real diagonal recurrence with
+    a = exp(-|alpha|) on the broadcast input."""
+    rng = np.random.default_rng(13)
+    B, T, m, c = 2, 150, 3, 2
+    alpha = rng.uniform(-1, 1, m)
+    flags = np.stack([tapes.flags_from_lengths(rng.integers(1, 40, size=10), T) for _ in range(B)])
+    x = rng.standard_normal((B, T, m))
+    S, _ = oracle.ffm(alpha, np.zeros(c), x, flags)
+    h, _ = oracle.diag_fwd(np.exp(-np.abs(alpha)), x, flags)
+    for k in range(c):
+        np.testing.assert_allclose(S[..., k].real, h, rtol=1e-13, atol=1e-13)
+        assert np.all(S[..., k].imag == 0)
