@@ -18,6 +18,7 @@ Workloads (seeded, synthetic; laws in paper_2402_09900_amd.tapes):
   5  diag real f32, T=1048576, d=256, lognormal(5, 1.5) episodes, forward + reverse
   6  discounted return + generalized advantage estimate, one tape of 2^24 steps,
      U{1..1000} episodes, gamma 0.99, lambda 0.95
+  7  FFM aggregator, T=262144, m=32 x c=8 complex state, Geometric(200) episodes
 
 Every buffer exists in several copies (at least 1 GiB cycled, at least 3) and
 step i uses copy i mod n, so inputs are read from HBM rather than from the
@@ -54,7 +55,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6])
+    p.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6, 7])
     p.add_argument("--no-cpu-baseline", action="store_true")
     return p.parse_args()
 
@@ -199,6 +200,30 @@ def setup_discount(torch, mb, tapes, key):
     return tp, sets, bytes_per, n
 
 
+def setup_ffm(torch, mb, tapes, key):
+    f = tapes.make_ffm(key)
+    B, T, m, c = f.B, f.T, f.m, f.c
+    n = B * T * m * c
+    nb = mb.memoroid_scan_ffm_workspace_bytes(B, T, m, c)
+    stream = lambda: torch.cuda.current_stream().cuda_stream  # noqa: E731
+    sets = []
+    for _ in range(n_sets(n * 8 + B * T * (m * 4 + 5) + nb)):
+        al, om, x, s = (dev_tensor(torch, a, k) for a, k in ((f.alpha, "f32"), (f.omega, "f32"), (f.x, "f32"),
+                                                              (f.start, "u8")))
+        S = torch.empty((B, T, m, c), dtype=torch.complex64, device="cuda")
+        idx = torch.empty((B, T), dtype=torch.int32, device="cuda")
+        ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+
+        def fwd(al=al, om=om, x=x, s=s, S=S, idx=idx, ws=ws):
+            st = mb.memoroid_scan_ffm(al.data_ptr(), om.data_ptr(), x.data_ptr(), s.data_ptr(), S.data_ptr(),
+                                      idx.data_ptr(), B, T, m, c, ws.data_ptr(), ws.numel(), stream())
+            assert st == 0, mb.status_string(st)
+        sets.append({"fwd": fwd})
+    # read x (real, m per step) and flags; write S (complex, m*c per step) and idx
+    bytes_per = {"fwd": B * T * (m * 4 + 1 + 4) + n * 8}
+    return f, sets, bytes_per, n
+
+
 def kernel_source_hash():
     """sha256 over the library's HIP sources (same recipe as
     profiles/summarize.py), to tell whether recorded counters still apply."""
@@ -227,6 +252,14 @@ def cpu_baseline(key, tapes, budget_s=20.0):
     """The oracle as it stands, single thread, on a bounded sample."""
     import oracle
     w = tapes.WORKLOADS[key]
+    if w.kind == "ffm":
+        T = min(w.T, 1 << 16)
+        f = tapes.make_ffm(key, T=T)
+        t0 = time.perf_counter()
+        oracle.ffm(f.alpha.astype(np.float64), f.omega.astype(np.float64), f.x.astype(np.float64), f.start)
+        dt = time.perf_counter() - t0
+        return {"value": f.B * T * f.m * f.c / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
+                "sample": "first %d steps of the tape, all %d x %d features, fp64, %.1f s" % (T, f.m, f.c, dt)}
     if w.kind == "discount":
         T = min(w.T, 1 << 22)
         tp = tapes.make_discount(key, T=T)
@@ -287,6 +320,8 @@ def main():
         w, sets, bytes_per, n, flops = setup_linattn(torch, mb, tapes)
     elif wl.kind == "discount":
         w, sets, bytes_per, n = setup_discount(torch, mb, tapes, key)
+    elif wl.kind == "ffm":
+        w, sets, bytes_per, n = setup_ffm(torch, mb, tapes, key)
     else:
         w, sets, bytes_per, n = setup_diag(torch, mb, tapes, key)
     calls = sets[0]
@@ -330,7 +365,8 @@ def main():
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None}
     roof["traffic"] = recorded_traffic(key, "linattn" if wl.kind == "linattn" else dom)
     roof["traffic_unit"] = "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
-    roof["kernel"] = {"fwd": "memoroid_scan_diag" if wl.kind == "diag" else "memoroid_scan_linattn",
+    roof["kernel"] = {"fwd": {"diag": "memoroid_scan_diag", "linattn": "memoroid_scan_linattn",
+                              "ffm": "memoroid_scan_ffm"}.get(wl.kind),
                       "bwd": "memoroid_scan_diag_bwd", "return": "memoroid_discounted_return",
                       "gae": "memoroid_gae"}[dom]
     roof["ms_per_launch"] = round(per_call_ms[dom], 4)
@@ -353,6 +389,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "B": wl.B, "T": wl.T,
                    ("heads" if wl.kind == "linattn" else "d"): wl.d,
+                   **({"m": wl.dk, "c": wl.dv} if wl.kind == "ffm" else {}),
                    **({"gamma": wl.gamma, "lambda": wl.lam} if wl.kind == "discount" else {}),
                    "passes": list(calls.keys()),
                    "buffer_sets": len(sets),

@@ -141,6 +141,31 @@ int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t,
                            void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * FFM aggregator (App. G.4, the fast-and-forgetful-memory memoroid): a
+ * complex m x c state per step,
+ *     S_t = x_t 1_c^T                          at a begin step,
+ *     S_t = S_{t-1} (.) gamma + x_t 1_c^T      otherwise,
+ * gamma[j][k] = exp(-|alpha_j| + i omega_k), i.e. the paper's time-count
+ * monoid (X, t) . (X', t') = (X (.) exp(t' (-|alpha| (+) i omega)) + X', t + t')
+ * advanced one step at a time.  gamma is generated in the kernel (fp32
+ * exp/sincos); the input gate x = (W1 o + b1) (.) sigma(W2 o + b2) and the
+ * readout g are left to the caller.
+ *
+ *   alpha      [m] fp32;  omega: [c] fp32.
+ *   x          [B][T][m] fp32, real; broadcast over the c columns.
+ *   start      start[B][T] (as above).
+ *   S          out [B][T][m][c] complex64, interleaved (re, im).
+ *   episode_idx  optional out int32[B][T]; NULL skips it.
+ *   Vectorised when m * c is even and S is 16-byte aligned.
+ * ------------------------------------------------------------------------ */
+size_t memoroid_scan_ffm_workspace_bytes(int64_t B, int64_t T, int64_t m, int64_t c);
+
+int memoroid_scan_ffm(const float* alpha, const float* omega, const float* x,
+                      const uint8_t* start, void* S, int32_t* episode_idx,
+                      int64_t B, int64_t T, int64_t m, int64_t c,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Linear-transformer memoroid (App. G.1), forward readout, one tape of T
  * steps with H independent heads.  Per head, with S (dk x dv) and z (dk)
  * reset to zero at every begin step:

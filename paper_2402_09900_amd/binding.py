@@ -59,6 +59,10 @@ def lib() -> ctypes.CDLL:
         L.memoroid_scan_linattn_workspace_bytes.argtypes = [I64, I64, I64, I64, I64]
         L.memoroid_scan_linattn.restype = I32
         L.memoroid_scan_linattn.argtypes = [P, P, P, P, P, P, I64, I64, I64, I64, I64, P, SZ, P]
+        L.memoroid_scan_ffm_workspace_bytes.restype = SZ
+        L.memoroid_scan_ffm_workspace_bytes.argtypes = [I64, I64, I64, I64]
+        L.memoroid_scan_ffm.restype = I32
+        L.memoroid_scan_ffm.argtypes = [P, P, P, P, P, P, I64, I64, I64, I64, P, SZ, P]
         L.memoroid_discount_workspace_bytes.restype = SZ
         L.memoroid_discount_workspace_bytes.argtypes = [I64, I64]
         L.memoroid_discounted_return.restype = I32
@@ -116,6 +120,16 @@ def memoroid_scan_linattn(q, k, v, start, out, episode_idx, T, H, dk, dv, chunk,
                           workspace, workspace_bytes, stream) -> int:
     return lib().memoroid_scan_linattn(q, k, v, start, out, episode_idx, T, H, dk, dv, chunk,
                                        workspace, workspace_bytes, stream)
+
+
+def memoroid_scan_ffm_workspace_bytes(B, T, m, c) -> int:
+    return lib().memoroid_scan_ffm_workspace_bytes(B, T, m, c)
+
+
+def memoroid_scan_ffm(alpha, omega, x, start, S, episode_idx, B, T, m, c, workspace, workspace_bytes,
+                      stream) -> int:
+    return lib().memoroid_scan_ffm(alpha, omega, x, start, S, episode_idx, B, T, m, c, workspace,
+                                   workspace_bytes, stream)
 
 
 def memoroid_discount_workspace_bytes(B, T) -> int:
@@ -284,6 +298,38 @@ def scan_linattn(q, k, v, start, episode_idx: bool = False, chunk: int = 64, wor
                                      T, H, dk, dv, chunk, ws.data_ptr(), ws.numel(), _stream_ptr(dev))
     _raise(st, "memoroid_scan_linattn")
     return (out, idx) if episode_idx else out
+
+
+def scan_ffm(alpha, omega, x, start, episode_idx: bool = False, workspace=None):
+    """FFM aggregator state.  alpha float32 [m], omega float32 [c], x float32
+    [B,T,m] (or [T,m]), start uint8 [B,T].  Returns S complex64 [B,T,m,c]
+    (and the int32 episode index [B,T] when asked)."""
+    torch = _torch()
+    squeeze = x.dim() == 2
+    if squeeze:
+        x = x.unsqueeze(0)
+    B, T, m = x.shape
+    c = omega.shape[0]
+    if alpha.shape != (m,):
+        raise ValueError("alpha must have shape [m]")
+    start = start.reshape(B, T)
+    dev = _check_cuda(alpha, omega, x, start)
+    for t in (alpha, omega, x):
+        if t.dtype != torch.float32:
+            raise TypeError("alpha, omega and x must be float32")
+    if start.dtype != torch.uint8:
+        raise TypeError("start must be uint8")
+    S = torch.empty((B, T, m, c), dtype=torch.complex64, device=dev)
+    idx = torch.empty((B, T), dtype=torch.int32, device=dev) if episode_idx else None
+    ws = _workspace(lib().memoroid_scan_ffm_workspace_bytes(B, T, m, c), dev, workspace)
+    st = lib().memoroid_scan_ffm(alpha.data_ptr(), omega.data_ptr(), x.data_ptr(), start.data_ptr(), S.data_ptr(),
+                                 idx.data_ptr() if idx is not None else None, B, T, m, c, ws.data_ptr(), ws.numel(),
+                                 _stream_ptr(dev))
+    _raise(st, "memoroid_scan_ffm")
+    if squeeze:
+        S = S[0]
+        idx = idx[0] if idx is not None else None
+    return (S, idx) if episode_idx else S
 
 
 def _tape_shapes(r, *others):

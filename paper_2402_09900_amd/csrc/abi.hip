@@ -212,6 +212,70 @@ int memoroid_scan_diag(const void* a, int64_t a_stride_t, const void* x, const u
     return MEMOROID_OK;
 }
 
+// ------------------------------------------------------------------- FFM
+
+size_t memoroid_scan_ffm_workspace_bytes(int64_t B, int64_t T, int64_t m, int64_t c) {
+    int64_t d;
+    if (B <= 0 || T <= 0 || m <= 0 || c <= 0 || !mul_ok(m, c, &d)) return 0;
+    size_t best = 0;
+    for (int vec = 0; vec < 2; ++vec) {
+        DiagPlan p;
+        if (!plan_diag(B, T, d, MEMOROID_C64, vec, diag_rows(false, true), false, true, false, &p)) return 0;
+        if (p.total > best) best = p.total;
+    }
+    return best;
+}
+
+int memoroid_scan_ffm(const float* alpha, const float* omega, const float* x, const uint8_t* start, void* S,
+                      int32_t* episode_idx, int64_t B, int64_t T, int64_t m, int64_t c, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+    if (B < 0 || T < 0 || m < 0 || c < 0) return MEMOROID_EINVAL;
+    if (B == 0 || T == 0 || m == 0 || c == 0) return MEMOROID_OK;
+    int64_t d, BT, BTd;
+    if (!mul_ok(m, c, &d) || !mul_ok(B, T, &BT) || !mul_ok(BT, d, &BTd) || BTd > INT64_MAX / 16)
+        return MEMOROID_EINVAL;
+    if (!alpha || !omega || !x || !start || !S) return MEMOROID_EINVAL;
+    if (!aligned(alpha, 4) || !aligned(omega, 4) || !aligned(x, 4) || !aligned(S, 8) ||
+        (episode_idx && !aligned(episode_idx, 4)))
+        return MEMOROID_EINVAL;
+    if (S == (const void*)x || S == (const void*)alpha || S == (const void*)omega || S == (const void*)start ||
+        (const void*)episode_idx == S || (const void*)episode_idx == (const void*)x ||
+        (const void*)episode_idx == (const void*)start)
+        return MEMOROID_EINVAL;
+    const bool vec = d % 2 == 0 && aligned(S, 16);
+    DiagPlan p;
+    if (!plan_diag(B, T, d, MEMOROID_C64, vec, diag_rows(false, true), false, true, false, &p))
+        return MEMOROID_EUNSUPPORTED;
+    if (!workspace) return MEMOROID_EWORKSPACE;
+    if (workspace_bytes < memoroid_scan_ffm_workspace_bytes(B, T, m, c) || workspace_bytes < p.total)
+        return MEMOROID_EWORKSPACE;
+    if (!aligned(workspace, 16)) return MEMOROID_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    if (ws_init_launch(ws, p.off_agg, ws + p.off_agg, p.fill_bytes, s) != hipSuccess) return MEMOROID_EHIP;
+    DiagFwdArgs args{};
+    args.a = nullptr;
+    args.x = x;
+    args.start = start;
+    args.h = S;
+    args.T = T;
+    args.d = d;
+    args.Qp = p.Qp;
+    args.nfb = p.nfb;
+    args.nchains = (int32_t)p.nchains;
+    args.agg = ws + p.off_agg;
+    args.incl = ws + p.off_incl;
+    args.hdr = (WsHeader*)ws;
+    args.ctr = (uint32_t*)(ws + p.off_ctr);
+    args.idx = episode_idx;
+    args.cnt = (uint64_t*)(ws + p.off_cnt);
+    args.alpha = alpha;
+    args.omega = omega;
+    args.ffm_m = m;
+    args.ffm_c = c;
+    return check_hip(ffm_fwd_launch(vec, args, p.ntiles, s));
+}
+
 // ------------------------------------------------------------ diag backward
 
 size_t memoroid_scan_diag_bwd_workspace_bytes(int64_t B, int64_t T, int64_t d, int dtype, int64_t a_stride_t) {

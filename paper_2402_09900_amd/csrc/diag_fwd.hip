@@ -37,13 +37,16 @@
 // (5) the tile's inclusive prefix is published, and every lane replays its
 // steps from its carry-in and streams h out.  a and x are read from HBM once
 // and h written once; cross-tile traffic is a few bytes per feature per tile.
+#include <type_traits>
+
 #include "scan_common.hpp"
 #include "kernels.hpp"
 
 namespace memoroid {
 
-template <Kind IN, Kind OUT, int VEC, int R, bool AINV>
+template <Kind IN, Kind OUT, int VEC, int R, bool AINV, bool FFM = false>
 __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
+    static_assert(!FFM || (IN == K_C64 && OUT == K_C64 && AINV), "FFM: complex state, generated a");
     using S = typename StateOf<IN>::type;
     using CIn = Codec<IN, VEC>;
     using COut = Codec<OUT, VEC>;
@@ -112,10 +115,30 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     __builtin_amdgcn_sched_barrier(0);
     RawVec<IN, VEC> ra[AINV ? 1 : R];
     RawVec<IN, VEC> rx[R];
+    if constexpr (FFM) {
+        // real x[B][T][m] read once per feature's row j and broadcast over
+        // the row's c columns (imaginary parts zero)
+        const int64_t m = p.ffm_m;
+        const Rsrc rs_xf = make_rsrc((const char*)p.x + tape_row0 * m * 4, rows_left * m * 4);
+        uint32_t xo[VEC];
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-        raw_bload(rx[r], rs_x, in_off + r * in_step);
-        if constexpr (!AINV) raw_bload(ra[r], rs_a, in_off + r * in_step);
+        for (int v = 0; v < VEC; ++v)
+            xo[v] = active && f0 + v < p.d ? (uint32_t)(((int64_t)lrow * m + (f0 + v) / p.ffm_c) * 4) : kOob;
+        const uint32_t xstep = active ? (uint32_t)(m * 4) : 0u;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) {
+                rx[r].w[2 * v] = __builtin_amdgcn_raw_buffer_load_b32(rs_xf, (int)(xo[v] + r * xstep), 0, 0);
+                rx[r].w[2 * v + 1] = 0u;
+            }
+        }
+    } else {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            raw_bload(rx[r], rs_x, in_off + r * in_step);
+            if constexpr (!AINV) raw_bload(ra[r], rs_a, in_off + r * in_step);
+        }
     }
     __builtin_amdgcn_sched_barrier(0);
     uint32_t begins = 0, valid = 0;
@@ -127,7 +150,20 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
         begins |= (in & ((t == 0 ? 1u : 0u) | (fl[r] != 0u ? 1u : 0u))) << r;
     }
     S ainv[VEC];
-    if constexpr (AINV) {
+    if constexpr (FFM) {
+        // a = exp(-|alpha_j|) (cos omega_k + i sin omega_k), f = j * c + k,
+        // evaluated in double and rounded once to float: with |a| near 1 the
+        // error of a is amplified by up to the episode length
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+            const int64_t f = f0 + v < p.d ? f0 + v : 0;
+            const int64_t jj = f / p.ffm_c, kk = f - jj * p.ffm_c;
+            const double mag = exp(-fabs((double)p.alpha[jj]));
+            double sn, cs;
+            sincos((double)p.omega[kk], &sn, &cs);
+            if constexpr (std::is_same<S, cf>::value) ainv[v] = cf{(float)(mag * cs), (float)(mag * sn)};
+        }
+    } else if constexpr (AINV) {
         // a NULL time-invariant a stands for a = 1 (the sum monoid, used by
         // the linear-attention state scan)
         RawVec<IN, VEC> r0;
@@ -302,6 +338,18 @@ static hipError_t launch_fwd(const DiagFwdArgs& args, int64_t ntiles, bool ainv,
         hipLaunchKernelGGL((diag_fwd_kernel<IN, OUT, VEC, R, true>), dim3((unsigned)ntiles), dim3(256), 0, s, args);
     else
         hipLaunchKernelGGL((diag_fwd_kernel<IN, OUT, VEC, R, false>), dim3((unsigned)ntiles), dim3(256), 0, s, args);
+    return hipGetLastError();
+}
+
+hipError_t ffm_fwd_launch(bool vec, const DiagFwdArgs& args, int64_t ntiles, hipStream_t s) {
+    constexpr int R = kFwdRows;
+    constexpr int VC = KindInfo<K_C64>::vec;
+    if (vec)
+        hipLaunchKernelGGL((diag_fwd_kernel<K_C64, K_C64, VC, R, true, true>), dim3((unsigned)ntiles), dim3(256), 0, s,
+                           args);
+    else
+        hipLaunchKernelGGL((diag_fwd_kernel<K_C64, K_C64, 1, R, true, true>), dim3((unsigned)ntiles), dim3(256), 0, s,
+                           args);
     return hipGetLastError();
 }
 

@@ -51,6 +51,12 @@ struct DiagFwdArgs {
     uint32_t* ctr;     // per-chain tile counters, kCtrStride words apart
     int32_t* idx;      // episode index out [B][T], or NULL
     uint64_t* cnt;     // [tiles per chain][B] begin-count descriptor words
+    // FFM aggregator (complex state, d = m * c): a[j*c + k] =
+    // exp(-|alpha_j| + i omega_k) is generated in the kernel and x is real
+    // [B][T][m], broadcast over the c columns
+    const float* alpha;
+    const float* omega;
+    int64_t ffm_m, ffm_c;
 };
 
 struct DiagBwdArgs {
@@ -76,6 +82,7 @@ struct DiagBwdArgs {
 
 hipError_t diag_fwd_launch(int in_kind, int out_kind, bool vec, bool ainv,
                            const DiagFwdArgs& args, int64_t ntiles, hipStream_t s);
+hipError_t ffm_fwd_launch(bool vec, const DiagFwdArgs& args, int64_t ntiles, hipStream_t s);
 hipError_t diag_bwd_launch(int kind, bool vec, bool ainv, const DiagBwdArgs& args,
                            int64_t ntiles, hipStream_t s);
 // out[r / (4 rpw)][c] = sum over rows r .. r + 4 rpw - 1 of in[r][c], in a

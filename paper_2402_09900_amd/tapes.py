@@ -180,6 +180,8 @@ WORKLOADS: Dict[int, Workload] = {
                 False, (0.5, 0.99), _lognormal(5.0, 1.5), True),
     6: Workload(6, "return_gae_f32_T16777216_unif1_1000_g0.99_l0.95", "discount", 1, 1 << 24, 1, "f32", "f32",
                 False, (0.0, 0.0), _uniform_int(1, 1000), False, gamma=0.99, lam=0.95),
+    7: Workload(7, "ffm_c64_T262144_m32_c8_geom200_fwd", "ffm", 1, 1 << 18, 32, "c64", "c64",
+                True, (0.5, 0.995), _geometric(200.0), False, dk=32, dv=8),
 }
 
 
@@ -358,3 +360,42 @@ def make_discount(key: int = 6, seed: Optional[int] = None, B: Optional[int] = N
     vn[ends] = boot[ends]
     done = (ends & coin).astype(np.uint8)
     return DiscountTape(r=r, v=v, vn=vn, done=done, start=start, gamma=w.gamma, lam=w.lam, B=B, T=T)
+
+
+@dataclasses.dataclass
+class FfmTape:
+    """Inputs of the FFM aggregator: alpha [m], omega [c], x [B,T,m] float32,
+    start [B,T] uint8."""
+    alpha: np.ndarray
+    omega: np.ndarray
+    x: np.ndarray
+    start: np.ndarray
+    B: int
+    T: int
+    m: int
+    c: int
+
+
+def make_ffm(key: int = 7, seed: Optional[int] = None, B: Optional[int] = None, T: Optional[int] = None,
+             m: Optional[int] = None, c: Optional[int] = None, episodes: Optional[Callable] = None) -> FfmTape:
+    """FFM inputs.  |gamma_j| = exp(-|alpha_j|) is spread log-uniformly in
+    decay time between the workload's |a| bounds (signs of alpha random),
+    omega_k evenly spaced in [0, pi), x ~ N(0, 1).  Draw order: episode
+    lengths (per tape), alpha signs, x."""
+    w = WORKLOADS[key]
+    assert w.kind == "ffm"
+    B = w.B if B is None else B
+    T = w.T if T is None else T
+    m = w.dk if m is None else m
+    c = w.dv if c is None else c
+    law = w.episodes if episodes is None else episodes
+    rng = np.random.Generator(np.random.PCG64(key if seed is None else seed))
+    start = (np.stack([law(rng, T) for _ in range(B)]) if T > 0 else np.zeros((B, 0), np.uint8))
+    start = start.reshape(B, T).astype(np.uint8)
+    lo, hi = w.a_range
+    tau = np.exp(np.linspace(np.log(-1.0 / np.log(lo)), np.log(-1.0 / np.log(hi)), m))  # decay times
+    sign = np.where(rng.random(m) < 0.5, -1.0, 1.0)
+    alpha = (sign / tau).astype(np.float32)
+    omega = (np.pi * np.arange(c) / max(c, 1)).astype(np.float32)
+    x = _normal_f32(rng, (B, T, m))
+    return FfmTape(alpha=alpha, omega=omega, x=x, start=start, B=B, T=T, m=m, c=c)

@@ -124,6 +124,26 @@ def test_linattn_validation():
     assert la(workspace_bytes=1000) == mb.EWORKSPACE
 
 
+def test_ffm_validation():
+    def ffm(**kw):
+        args = dict(alpha=A, omega=X, x=S, start=H + 0x100, S=I, episode_idx=None, B=2, T=100, m=4, c=3,
+                    workspace=W, workspace_bytes=1 << 30, stream=None)
+        args.update(kw)
+        return mb.memoroid_scan_ffm(*args.values())
+    assert mb.memoroid_scan_ffm_workspace_bytes(1, 1 << 18, 32, 8) > 0
+    assert mb.memoroid_scan_ffm_workspace_bytes(1, 100, 0, 8) == 0
+    assert ffm(B=-1) == mb.EINVAL
+    assert ffm(T=0) == mb.OK and ffm(m=0) == mb.OK and ffm(c=0) == mb.OK
+    assert ffm(alpha=None) == mb.EINVAL and ffm(omega=None) == mb.EINVAL and ffm(x=None) == mb.EINVAL
+    assert ffm(S=None) == mb.EINVAL and ffm(start=None) == mb.EINVAL
+    assert ffm(S=I + 4) == mb.EINVAL                    # complex64 needs 8-byte alignment
+    assert ffm(x=S + 2) == mb.EINVAL
+    assert ffm(S=S) == mb.EINVAL                        # output aliases x
+    assert ffm(workspace=None) == mb.EWORKSPACE
+    assert ffm(workspace_bytes=100) == mb.EWORKSPACE
+    assert ffm(m=1 << 30, c=1 << 30) == mb.EINVAL       # extent overflow
+
+
 def test_discount_validation():
     def ret(**kw):
         args = dict(r=A, start=S, gamma=0.99, G=H, B=2, T=100, workspace=W, workspace_bytes=1 << 30, stream=None)

@@ -1,0 +1,82 @@
+"""Parity of the FFM aggregator kernel (through the C ABI) with the fp64
+oracle: conditioned relative error (|y - r| / max(|r|, m), m the oracle's
+magnitude companion) at most 1e-4 (fp32 arithmetic), episode indices
+bit-exact.  The full workload is compared on every element."""
+import numpy as np
+import pytest
+
+import oracle
+from conftest import announce, cond_err
+from paper_2402_09900_amd import tapes
+
+torch = pytest.importorskip("torch")
+from paper_2402_09900_amd import binding as mb  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+TOL = 1e-4
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def check(f, label, x_override=None):
+    announce("ffm %s B=%d T=%d m=%d c=%d" % (label, f.B, f.T, f.m, f.c))
+    x = f.x if x_override is None else x_override
+    S, idx = mb.scan_ffm(dev(f.alpha), dev(f.omega), dev(x), dev(f.start), episode_idx=True)
+    torch.cuda.synchronize()
+    ref, m = oracle.ffm(f.alpha.astype(np.float64), f.omega.astype(np.float64), x.astype(np.float64), f.start)
+    got = S.cpu().numpy()
+    e = cond_err(got, ref, m)
+    assert e <= TOL, (label, e)
+    np.testing.assert_array_equal(idx.cpu().numpy(), oracle.episode_idx(f.start))
+    return got, ref
+
+
+def test_workload7_full():
+    check(tapes.make_ffm(7), "workload7")
+
+
+# m * c odd -> scalar kernel; c = 1; m = 1; ragged T around the 512-step tile
+SHAPES = [(1, 1, 1, 1), (1, 5, 1, 3), (2, 513, 3, 5), (1, 1000, 32, 8), (3, 2049, 7, 2), (2, 4096, 1, 16),
+          (1, 777, 16, 1), (4, 3000, 5, 4)]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "B%dT%dm%dc%d" % s)
+def test_shapes(shape):
+    B, T, m, c = shape
+    check(tapes.make_ffm(7, seed=200 + T + m * c, B=B, T=T, m=m, c=c, episodes=tapes._geometric(150.0)), "shape")
+
+
+def test_misaligned_output_takes_scalar_kernel():
+    f = tapes.make_ffm(7, seed=211, B=2, T=1500, m=4, c=4)
+    announce("ffm misaligned output")
+    n = f.B * f.T * f.m * f.c
+    big = torch.empty(n + 1, dtype=torch.complex64, device=DEV)
+    ws = torch.empty(mb.memoroid_scan_ffm_workspace_bytes(f.B, f.T, f.m, f.c), dtype=torch.uint8, device=DEV)
+    S = big[1:]
+    al, om, x, s = dev(f.alpha), dev(f.omega), dev(f.x), dev(f.start)     # held until the kernel has run
+    st = mb.memoroid_scan_ffm(al.data_ptr(), om.data_ptr(), x.data_ptr(), s.data_ptr(), S.data_ptr(), None,
+                              f.B, f.T, f.m, f.c, ws.data_ptr(), ws.numel(), torch.cuda.current_stream().cuda_stream)
+    assert st == mb.OK
+    torch.cuda.synchronize()
+    ref, m = oracle.ffm(f.alpha.astype(np.float64), f.omega.astype(np.float64), f.x.astype(np.float64), f.start)
+    assert cond_err(S.cpu().numpy().reshape(ref.shape), ref, m) <= TOL
+
+
+def test_nan_stays_in_its_episode():
+    f = tapes.make_ffm(7, seed=212, B=1, T=3000, m=4, c=2)
+    s = np.zeros((1, f.T), np.uint8)
+    s[0, [0, 1000, 1700, 2500]] = 1
+    f.start = s
+    x = f.x.copy()
+    x[0, 1200, 1] = np.nan
+    announce("ffm nan")
+    S = mb.scan_ffm(dev(f.alpha), dev(f.omega), dev(x), dev(s)).cpu().numpy()
+    ref, m = oracle.ffm(f.alpha.astype(np.float64), f.omega.astype(np.float64), x.astype(np.float64), s)
+    bad = np.isnan(ref)
+    assert np.array_equal(np.isnan(S), bad)
+    assert bad[0, 1200:1700, 1].all() and not bad[0, 1700:].any()
+    assert cond_err(S[~bad], ref[~bad], m[~bad]) <= TOL
