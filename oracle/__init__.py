@@ -56,6 +56,10 @@ def _load():
         lib.oracle_discounted_return.argtypes = [P, P, D, I64, I64, P, P]
         lib.oracle_gae.argtypes = [P, P, P, P, P, D, D, I64, I64, P, P, P, P]
         lib.oracle_ffm.argtypes = [P, P, P, P, I64, I64, I64, I64, P, P]
+        lib.oracle_tbb_begin_indices.argtypes = [P, I64, I64, P]
+        lib.oracle_tbb_begin_indices.restype = I64
+        lib.oracle_tbb_sample.argtypes = [P, I64, I64, P, I64, P, I64, I64, P, P, P]
+        lib.oracle_tbb_sample.restype = I64
         for name in ("oracle_episode_idx", "oracle_diag_fwd", "oracle_diag_fwd_c",
                      "oracle_diag_bwd", "oracle_diag_bwd_c", "oracle_linattn",
                      "oracle_discounted_return", "oracle_gae", "oracle_ffm"):
@@ -220,3 +224,32 @@ def ffm(alpha, omega, x, start):
     if squeeze:
         return S[0], mo[0]
     return S, mo
+
+
+def tbb_begin_indices(start, offset=0):
+    """I = offset + where(start != 0) (Alg. 1); step 0 is not forced."""
+    s = np.ascontiguousarray(start, dtype=np.uint8).reshape(-1)
+    out = np.empty(max(s.size, 1), dtype=np.int64)
+    k = _load().oracle_tbb_begin_indices(_ptr(s), s.size, int(offset), _ptr(out))
+    return out[:k].copy()
+
+
+def tbb_sample(D, I, draws, batch):
+    """Alg. 2 batch: D is [n_D, ...] (any dtype; rows are its first axis), I
+    the begin indices, draws the sampled positions in I.  Returns (out,
+    out_start, out_src, filled) with out shaped [batch, ...] like D's rows."""
+    D = np.ascontiguousarray(D)
+    n_D = D.shape[0]
+    row_shape = D.shape[1:]
+    row_bytes = int(D.dtype.itemsize * int(np.prod(row_shape, dtype=np.int64)))
+    I = np.ascontiguousarray(I, dtype=np.int64)
+    draws = np.ascontiguousarray(draws, dtype=np.int64)
+    if draws.size and (draws.min() < 0 or draws.max() >= I.size):
+        raise ValueError("draws must index I")
+    out = np.empty((batch,) + row_shape, dtype=D.dtype)
+    out_start = np.empty(batch, dtype=np.uint8)
+    out_src = np.empty(batch, dtype=np.int64)
+    filled = _load().oracle_tbb_sample(D.ctypes.data_as(ctypes.c_void_p), n_D, row_bytes, _ptr(I), I.size,
+                                       _ptr(draws), draws.size, int(batch),
+                                       out.ctypes.data_as(ctypes.c_void_p), _ptr(out_start), _ptr(out_src))
+    return out, out_start, out_src, int(filled)

@@ -284,3 +284,35 @@ void oracle_ffm(const double* alpha, const double* omega, const double* x, const
         }
     }
 }
+
+/* ------------------------------------------------- tape-based batching */
+
+int64_t oracle_tbb_begin_indices(const uint8_t* start, int64_t n, int64_t offset, int64_t* out) {
+    int64_t k = 0;
+    for (int64_t t = 0; t < n; ++t)
+        if (start[t] != 0) out[k++] = offset + t;
+    return k;
+}
+
+int64_t oracle_tbb_sample(const uint8_t* D, int64_t n_D, int64_t row_bytes, const int64_t* begins, int64_t n_I,
+                          const int64_t* draws, int64_t n_draws, int64_t batch,
+                          uint8_t* out, uint8_t* out_start, int64_t* out_src) {
+    int64_t len = 0;                       /* rows in the batch so far */
+    for (int64_t k = 0; k < n_draws && len < batch; ++k) {
+        const int64_t i = draws[k];
+        const int64_t lo = begins[i];
+        const int64_t hi = i + 1 < n_I ? begins[i + 1] : n_D;
+        for (int64_t r = lo; r < hi && len < batch; ++r) {
+            memcpy(out + len * row_bytes, D + r * row_bytes, (size_t)row_bytes);
+            out_start[len] = r == lo ? 1 : 0;
+            out_src[len] = r;
+            len += 1;
+        }
+    }
+    for (int64_t t = len; t < batch; ++t) {
+        memset(out + t * row_bytes, 0, (size_t)row_bytes);
+        out_start[t] = 0;
+        out_src[t] = -1;
+    }
+    return len;
+}

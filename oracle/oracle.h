@@ -114,6 +114,23 @@ void oracle_linattn(const double* q, const double* k, const double* v,
 void oracle_ffm(const double* alpha, const double* omega, const double* x, const uint8_t* start,
                 int64_t B, int64_t T, int64_t m, int64_t c, double* S, double* m_out);
 
+/* Tape-Based Batching insertion (Alg. 1): the begin indices of a rollout,
+ * I = offset + where(b).  Every step whose flag byte is nonzero is listed,
+ * in order; step 0 is NOT forced (a rollout may continue the episode in
+ * flight).  out has room for n entries; returns the count. */
+int64_t oracle_tbb_begin_indices(const uint8_t* start, int64_t n, int64_t offset, int64_t* out);
+
+/* Tape-Based Batching sampling (Alg. 2): concatenate the episodes
+ * D[I[i] : I[i+1]] (I = begins, I[n_I] standing for n_D) for i = draws[0], draws[1], ...
+ * until the batch holds `batch` transitions, then cut it to exactly `batch`.
+ * D holds n_D rows of row_bytes bytes.  Outputs per batch row: the row
+ * (out), 1 at the first row of every appended episode (out_start), and the
+ * source row in D (out_src).  If the draws run out first, the remaining rows
+ * are zero, with out_start 0 and out_src -1.  Returns the rows filled. */
+int64_t oracle_tbb_sample(const uint8_t* D, int64_t n_D, int64_t row_bytes, const int64_t* begins, int64_t n_I,
+                          const int64_t* draws, int64_t n_draws, int64_t batch,
+                          uint8_t* out, uint8_t* out_start, int64_t* out_src);
+
 /* Discounted return over a tape (App. D, discounted-return memoroid; the
  * done-flag convention of Section 2): for every step, the discounted sum of
  * the rewards from that step to the end of its episode,

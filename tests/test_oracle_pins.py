@@ -766,3 +766,82 @@ def test_ffm_without_rotation_is_the_real_diagonal_scan():
     for k in range(c):
         np.testing.assert_allclose(S[..., k].real, h, rtol=1e-13, atol=1e-13)
         assert np.all(S[..., k].imag == 0)
+
+
+# ---------------------------------------------------- tape-based batching
+# Alg. 1 (insertion: I = where(b)) and Alg. 2 (sampling: concatenate the
+# drawn episodes D[I[i]:I[i+1]] and cut the batch to B transitions).
+
+
+def test_fig2_sampling_example():
+    """Fig. 2: drawing the I-entries holding 4 and 7 with B = 4 gives the batch
+    concat(E1, E2) = rows 4, 5, 7, 8 of D, an episode beginning at 4 and at 7."""
+    g = read_golden("fig2_tape.txt")
+    flags = np.array([int(v) for v in g["begin_flags"][0]], np.uint8)
+    I = oracle.tbb_begin_indices(flags)
+    assert list(I) == [int(v) for v in g["begin_indices"][0]]
+    want_pos = [int(v) for v in g["sampled_begin_positions"][0]]
+    draws = [list(I).index(p) for p in want_pos]
+    D = np.arange(len(flags), dtype=np.int64)[:, None] * 10 + np.arange(3)[None, :]   # row r holds 10 r + col
+    out, out_start, out_src, filled = oracle.tbb_sample(D, I, draws, int(g["batch_size"][0][0]))
+    rows = [int(v) for v in g["sampled_batch_rows"][0]]
+    assert filled == len(rows) and list(out_src) == rows
+    assert np.array_equal(out, D[rows])
+    assert list(out_start) == [1 if r in want_pos else 0 for r in rows]
+
+
+def test_begin_indices_is_flatnonzero_with_offset():
+    rng = np.random.default_rng(21)
+    for n in (0, 1, 17, 5000):
+        f = (rng.random(n) < 0.05).astype(np.uint8) * rng.integers(1, 256, size=n).astype(np.uint8)
+        if n:
+            f[0] = 0                                     # step 0 is not forced
+        np.testing.assert_array_equal(oracle.tbb_begin_indices(f, offset=123), np.flatnonzero(f) + 123)
+
+
+def test_sampling_every_episode_in_order_rebuilds_the_buffer():
+    """Drawing every episode once, in order, with B = card(D), returns D itself
+    and begin flags that mark exactly I."""
+    rng = np.random.default_rng(22)
+    n = 3000
+    flags = tapes.flags_from_lengths(rng.integers(1, 100, size=100), n)
+    I = oracle.tbb_begin_indices(flags)
+    D = rng.standard_normal((n, 5)).astype(np.float32)
+    out, out_start, out_src, filled = oracle.tbb_sample(D, I, np.arange(I.size), n)
+    assert filled == n
+    assert np.array_equal(out, D) and np.array_equal(out_src, np.arange(n))
+    assert np.array_equal(out_start, (flags != 0).astype(np.uint8))
+
+
+def test_sampled_batch_is_a_concatenation_of_drawn_episodes():
+    """Structure of any Alg. 2 batch: consecutive runs of D rows, each starting
+    at the begin index of the next draw and running to its episode end, the
+    last one cut at B; the episode index over the batch counts the draws."""
+    rng = np.random.default_rng(23)
+    n = 5000
+    flags = tapes.flags_from_lengths(rng.integers(1, 300, size=60), n)
+    I = oracle.tbb_begin_indices(flags)
+    D = np.arange(n, dtype=np.int32)
+    draws = rng.integers(0, I.size, size=200)
+    Bsz = 2500
+    out, out_start, out_src, filled = oracle.tbb_sample(D, I, draws, Bsz)
+    assert filled == Bsz and np.array_equal(out, out_src.astype(np.int32))
+    ends = np.append(I[1:], n)
+    t, k = 0, 0
+    while t < Bsz:
+        lo, hi = I[draws[k]], ends[draws[k]]
+        run = min(hi - lo, Bsz - t)
+        assert out_start[t] == 1 and np.all(out_start[t + 1:t + run] == 0)
+        np.testing.assert_array_equal(out_src[t:t + run], np.arange(lo, lo + run))
+        t += run
+        k += 1
+    assert oracle.episode_idx(out_start)[-1] == k - 1
+
+
+def test_sampling_with_too_few_draws_leaves_the_tail_empty():
+    I = np.array([0, 3])
+    D = np.arange(5, dtype=np.int64)
+    out, out_start, out_src, filled = oracle.tbb_sample(D, I, [1], 6)
+    assert filled == 2
+    assert list(out[:2]) == [3, 4] and list(out_src) == [3, 4, -1, -1, -1, -1]
+    assert list(out_start) == [1, 0, 0, 0, 0, 0] and not out[2:].any()
