@@ -845,3 +845,11 @@ def test_sampling_with_too_few_draws_leaves_the_tail_empty():
     assert filled == 2
     assert list(out[:2]) == [3, 4] and list(out_src) == [3, 4, -1, -1, -1, -1]
     assert list(out_start) == [1, 0, 0, 0, 0, 0] and not out[2:].any()
+
+
+def test_sampling_fills_the_last_row_after_an_episode_ends_one_short():
+    """An episode ending one row short of B: the next draw supplies the last row."""
+    I = np.array([0, 3])
+    D = np.arange(5, dtype=np.int64)
+    out, out_start, out_src, filled = oracle.tbb_sample(D, I, [0, 1], 4)
+    assert filled == 4 and list(out_src) == [0, 1, 2, 3] and list(out_start) == [1, 0, 0, 1]
