@@ -19,6 +19,8 @@ Workloads (seeded, synthetic; laws in paper_2402_09900_amd.tapes):
   6  discounted return + generalized advantage estimate, one tape of 2^24 steps,
      U{1..1000} episodes, gamma 0.99, lambda 0.95
   7  FFM aggregator, T=262144, m=32 x c=8 complex state, Geometric(200) episodes
+  8  tape-based batching: begin indices of a 2^24-transition buffer (64-byte
+     rows, U{1..1000} episodes) and a sampled batch of 2^20 rows
 
 Every buffer exists in several copies (at least 1 GiB cycled, at least 3) and
 step i uses copy i mod n, so inputs are read from HBM rather than from the
@@ -55,7 +57,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6, 7])
+    p.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6, 7, 8])
     p.add_argument("--no-cpu-baseline", action="store_true")
     return p.parse_args()
 
@@ -224,6 +226,47 @@ def setup_ffm(torch, mb, tapes, key):
     return f, sets, bytes_per, n
 
 
+def setup_tbb(torch, mb, tapes, key):
+    tb = tapes.make_tbb(key)
+    n, row = tb.D.shape
+    K = tb.draws.size
+    nbi = mb.memoroid_tbb_begin_indices_workspace_bytes(n)
+    nbs = mb.memoroid_tbb_sample_workspace_bytes(K)
+    stream = lambda: torch.cuda.current_stream().cuda_stream  # noqa: E731
+    row_bytes = row * 4
+    sets = []
+    set_bytes = n * (row_bytes + 1 + 8) + tb.batch * (row_bytes + 9) + K * 8 * 2 + nbi + nbs
+    for _ in range(n_sets(set_bytes)):
+        D, s, I, draws = dev_tensor(torch, tb.D, "f32"), dev_tensor(torch, tb.start, "u8"), \
+            dev_tensor(torch, tb.begins, "i64"), dev_tensor(torch, tb.draws, "i64")
+        idx = torch.empty(n, dtype=torch.int64, device="cuda")
+        cnt = torch.empty(1, dtype=torch.int64, device="cuda")
+        out = torch.empty((tb.batch, row), dtype=torch.float32, device="cuda")
+        ost = torch.empty(tb.batch, dtype=torch.uint8, device="cuda")
+        osrc = torch.empty(tb.batch, dtype=torch.int64, device="cuda")
+        filled = torch.empty(1, dtype=torch.int64, device="cuda")
+        wsi = torch.empty(nbi, dtype=torch.uint8, device="cuda")
+        wss = torch.empty(nbs, dtype=torch.uint8, device="cuda")
+
+        def insert(s=s, idx=idx, cnt=cnt, wsi=wsi):
+            st = mb.memoroid_tbb_begin_indices(s.data_ptr(), n, 0, idx.data_ptr(), cnt.data_ptr(), wsi.data_ptr(),
+                                               wsi.numel(), stream())
+            assert st == 0, mb.status_string(st)
+
+        def sample(D=D, I=I, draws=draws, out=out, ost=ost, osrc=osrc, filled=filled, wss=wss):
+            st = mb.memoroid_tbb_sample(D.data_ptr(), n, row_bytes, I.data_ptr(), I.numel(), draws.data_ptr(), K,
+                                        tb.batch, out.data_ptr(), ost.data_ptr(), osrc.data_ptr(), filled.data_ptr(),
+                                        wss.data_ptr(), wss.numel(), stream())
+            assert st == 0, mb.status_string(st)
+        sets.append({"insert": insert, "sample": sample})
+    n_I = tb.begins.size
+    # insert: read the flags, write the begin indices.  sample: read the draws
+    # and their I entries, read and write the batch rows, write flags and
+    # source rows
+    bytes_per = {"insert": n + 8 * n_I, "sample": K * (8 + 16) + tb.batch * (2 * row_bytes + 1 + 8)}
+    return tb, sets, bytes_per, tb.batch
+
+
 def kernel_source_hash():
     """sha256 over the library's HIP sources (same recipe as
     profiles/summarize.py), to tell whether recorded counters still apply."""
@@ -252,6 +295,15 @@ def cpu_baseline(key, tapes, budget_s=20.0):
     """The oracle as it stands, single thread, on a bounded sample."""
     import oracle
     w = tapes.WORKLOADS[key]
+    if w.kind == "tbb":
+        tb = tapes.make_tbb(key)
+        t0 = time.perf_counter()
+        I = oracle.tbb_begin_indices(tb.start)
+        oracle.tbb_sample(tb.D, I, tb.draws, tb.batch)
+        dt = time.perf_counter() - t0
+        return {"value": tb.batch / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
+                "sample": "the whole workload (begin indices of %d flags, batch of %d rows), %.1f s"
+                          % (tb.start.size, tb.batch, dt)}
     if w.kind == "ffm":
         T = min(w.T, 1 << 16)
         f = tapes.make_ffm(key, T=T)
@@ -322,6 +374,8 @@ def main():
         w, sets, bytes_per, n = setup_discount(torch, mb, tapes, key)
     elif wl.kind == "ffm":
         w, sets, bytes_per, n = setup_ffm(torch, mb, tapes, key)
+    elif wl.kind == "tbb":
+        w, sets, bytes_per, n = setup_tbb(torch, mb, tapes, key)
     else:
         w, sets, bytes_per, n = setup_diag(torch, mb, tapes, key)
     calls = sets[0]
@@ -368,7 +422,8 @@ def main():
     roof["kernel"] = {"fwd": {"diag": "memoroid_scan_diag", "linattn": "memoroid_scan_linattn",
                               "ffm": "memoroid_scan_ffm"}.get(wl.kind),
                       "bwd": "memoroid_scan_diag_bwd", "return": "memoroid_discounted_return",
-                      "gae": "memoroid_gae"}[dom]
+                      "gae": "memoroid_gae", "insert": "memoroid_tbb_begin_indices",
+                      "sample": "memoroid_tbb_sample"}[dom]
     roof["ms_per_launch"] = round(per_call_ms[dom], 4)
     roof["algorithmic_bytes_per_launch"] = int(bytes_per[dom])
     if flops is not None:

@@ -241,6 +241,56 @@ int memoroid_gae(const float* r, const float* value, const float* value_next, co
                  void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Tape-Based Batching, insertion (Alg. 1): the begin indices of a rollout,
+ *     indices[0 .. count) = offset + where(start[0 .. n) != 0),
+ * in increasing order.  Step 0 is NOT treated as a begin here: a rollout
+ * may continue the episode that the previous one left unfinished, and only
+ * its flag byte decides.
+ *
+ *   start      [n] flag bytes.
+ *   offset     added to every index (card(D) before the rollout is appended).
+ *   indices    out, room for n int64 values (only count are written).
+ *   count      out, one int64 in device memory.
+ *   n < 2^31 (MEMOROID_EUNSUPPORTED otherwise); n == 0 writes count = 0.
+ *   Workspace: memoroid_tbb_begin_indices_workspace_bytes(n).
+ * ------------------------------------------------------------------------ */
+size_t memoroid_tbb_begin_indices_workspace_bytes(int64_t n);
+
+int memoroid_tbb_begin_indices(const uint8_t* start, int64_t n, int64_t offset,
+                               int64_t* indices, int64_t* count,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Tape-Based Batching, sampling (Alg. 2): the batch is the concatenation of
+ * the episodes D[I[i] : I[i+1]] for i = draws[0], draws[1], ... (I[n_I]
+ * standing for n_D), cut to exactly `batch` rows.  The random positions are
+ * drawn by the caller (Alg. 2 draws them uniformly from 0 .. n_I - 1).
+ *
+ *   D          [n_D][row_bytes] transitions (any payload).
+ *   I          [n_I] int64 begin indices, increasing, in [0, n_D]; values
+ *              outside that range are clamped (an episode never reads past D).
+ *   draws      [n_draws] int64 positions in I, clamped to [0, n_I).
+ *   out        out [batch][row_bytes].
+ *   out_start  out [batch] bytes: 1 at the first row of every appended
+ *              episode (the begin flags of the batch as a tape), else 0.
+ *   out_src    optional out [batch] int64: source row in D, -1 if unfilled.
+ *   filled     optional out int64 (device): rows filled, min(batch, total
+ *              length of the drawn episodes).  Rows past it are zero, with
+ *              out_start 0.  Since every episode has at least one row,
+ *              n_draws >= batch always fills the batch.
+ *   n_draws <= 2^24 and row_bytes <= 2^24 (MEMOROID_EUNSUPPORTED otherwise).
+ *   Rows move in 16-byte
+ *   units when row_bytes % 16 == 0 and D, out are 16-byte aligned.
+ *   Workspace: memoroid_tbb_sample_workspace_bytes(n_draws) (0 when n_draws is 0).
+ * ------------------------------------------------------------------------ */
+size_t memoroid_tbb_sample_workspace_bytes(int64_t n_draws);
+
+int memoroid_tbb_sample(const void* D, int64_t n_D, int64_t row_bytes,
+                        const int64_t* I, int64_t n_I, const int64_t* draws, int64_t n_draws,
+                        int64_t batch, void* out, uint8_t* out_start, int64_t* out_src,
+                        int64_t* filled, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Health of the last call that used `workspace`: synchronises `stream`,
  * then returns MEMOROID_OK, or MEMOROID_ETIMEOUT if a kernel's bounded wait
  * for a predecessor tile gave up (its outputs are then invalid), or

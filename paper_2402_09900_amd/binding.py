@@ -63,6 +63,14 @@ def lib() -> ctypes.CDLL:
         L.memoroid_scan_ffm_workspace_bytes.argtypes = [I64, I64, I64, I64]
         L.memoroid_scan_ffm.restype = I32
         L.memoroid_scan_ffm.argtypes = [P, P, P, P, P, P, I64, I64, I64, I64, P, SZ, P]
+        L.memoroid_tbb_begin_indices_workspace_bytes.restype = SZ
+        L.memoroid_tbb_begin_indices_workspace_bytes.argtypes = [I64]
+        L.memoroid_tbb_begin_indices.restype = I32
+        L.memoroid_tbb_begin_indices.argtypes = [P, I64, I64, P, P, P, SZ, P]
+        L.memoroid_tbb_sample_workspace_bytes.restype = SZ
+        L.memoroid_tbb_sample_workspace_bytes.argtypes = [I64]
+        L.memoroid_tbb_sample.restype = I32
+        L.memoroid_tbb_sample.argtypes = [P, I64, I64, P, I64, P, I64, I64, P, P, P, P, P, SZ, P]
         L.memoroid_discount_workspace_bytes.restype = SZ
         L.memoroid_discount_workspace_bytes.argtypes = [I64, I64]
         L.memoroid_discounted_return.restype = I32
@@ -130,6 +138,24 @@ def memoroid_scan_ffm(alpha, omega, x, start, S, episode_idx, B, T, m, c, worksp
                       stream) -> int:
     return lib().memoroid_scan_ffm(alpha, omega, x, start, S, episode_idx, B, T, m, c, workspace,
                                    workspace_bytes, stream)
+
+
+def memoroid_tbb_begin_indices_workspace_bytes(n) -> int:
+    return lib().memoroid_tbb_begin_indices_workspace_bytes(n)
+
+
+def memoroid_tbb_begin_indices(start, n, offset, indices, count, workspace, workspace_bytes, stream) -> int:
+    return lib().memoroid_tbb_begin_indices(start, n, offset, indices, count, workspace, workspace_bytes, stream)
+
+
+def memoroid_tbb_sample_workspace_bytes(n_draws) -> int:
+    return lib().memoroid_tbb_sample_workspace_bytes(n_draws)
+
+
+def memoroid_tbb_sample(D, n_D, row_bytes, I, n_I, draws, n_draws, batch, out, out_start, out_src, filled,
+                        workspace, workspace_bytes, stream) -> int:
+    return lib().memoroid_tbb_sample(D, n_D, row_bytes, I, n_I, draws, n_draws, batch, out, out_start, out_src,
+                                     filled, workspace, workspace_bytes, stream)
 
 
 def memoroid_discount_workspace_bytes(B, T) -> int:
@@ -330,6 +356,47 @@ def scan_ffm(alpha, omega, x, start, episode_idx: bool = False, workspace=None):
         S = S[0]
         idx = idx[0] if idx is not None else None
     return (S, idx) if episode_idx else S
+
+
+def tbb_begin_indices(start, offset: int = 0, workspace=None):
+    """Alg. 1's I = offset + where(start) of a rollout (step 0 not forced).
+    start: uint8 [n].  Returns (indices int64 [n] of which the first `count`
+    are valid, count int64 [1]); both stay on the device."""
+    torch = _torch()
+    dev = _check_cuda(start)
+    if start.dtype != torch.uint8:
+        raise TypeError("start must be uint8")
+    n = start.numel()
+    idx = torch.empty(max(n, 1), dtype=torch.int64, device=dev)
+    count = torch.empty(1, dtype=torch.int64, device=dev)
+    ws = _workspace(lib().memoroid_tbb_begin_indices_workspace_bytes(n), dev, workspace)
+    st = lib().memoroid_tbb_begin_indices(start.data_ptr(), n, int(offset), idx.data_ptr(), count.data_ptr(),
+                                          ws.data_ptr(), ws.numel(), _stream_ptr(dev))
+    _raise(st, "memoroid_tbb_begin_indices")
+    return idx, count
+
+
+def tbb_sample(D, I, draws, batch: int, workspace=None):
+    """Alg. 2 batch: D [n_D, ...] (rows on the first axis, any dtype), I int64
+    begin indices, draws int64 positions in I.  Returns (out [batch, ...],
+    out_start uint8 [batch], out_src int64 [batch], filled int64 [1])."""
+    torch = _torch()
+    dev = _check_cuda(D, I, draws)
+    if I.dtype != torch.int64 or draws.dtype != torch.int64:
+        raise TypeError("I and draws must be int64")
+    n_D = D.shape[0]
+    row_bytes = D.element_size() * (D[0].numel() if n_D else int(torch.tensor(D.shape[1:]).prod().item()))
+    out = torch.empty((batch,) + tuple(D.shape[1:]), dtype=D.dtype, device=dev)
+    out_start = torch.empty(batch, dtype=torch.uint8, device=dev)
+    out_src = torch.empty(batch, dtype=torch.int64, device=dev)
+    filled = torch.empty(1, dtype=torch.int64, device=dev)
+    nd = draws.numel()
+    ws = _workspace(lib().memoroid_tbb_sample_workspace_bytes(nd), dev, workspace)
+    st = lib().memoroid_tbb_sample(D.data_ptr(), n_D, row_bytes, I.data_ptr(), I.numel(), draws.data_ptr(), nd,
+                                   batch, out.data_ptr(), out_start.data_ptr(), out_src.data_ptr(),
+                                   filled.data_ptr(), ws.data_ptr(), ws.numel(), _stream_ptr(dev))
+    _raise(st, "memoroid_tbb_sample")
+    return out, out_start, out_src, filled
 
 
 def _tape_shapes(r, *others):

@@ -584,6 +584,101 @@ int memoroid_gae(const float* r, const float* value, const float* value_next, co
                     workspace_bytes, stream, true);
 }
 
+// ------------------------------------------------- tape-based batching
+
+size_t memoroid_tbb_begin_indices_workspace_bytes(int64_t n) {
+    if (n <= 0 || n > (int64_t)INT32_MAX) return 0;
+    const int64_t ntiles = (n + kTbbBeginTile - 1) / kTbbBeginTile;
+    return align_up(kAlign + (size_t)ntiles * 8);
+}
+
+int memoroid_tbb_begin_indices(const uint8_t* start, int64_t n, int64_t offset, int64_t* indices, int64_t* count,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+    if (n < 0) return MEMOROID_EINVAL;
+    if (n > (int64_t)INT32_MAX) return MEMOROID_EUNSUPPORTED;
+    if (!count) return MEMOROID_EINVAL;
+    if (!aligned(count, 8) || (indices && !aligned(indices, 8))) return MEMOROID_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    if (n == 0) {
+        // nothing to scan, but the count is still an output
+        return check_hip(store_i64_launch(count, 0, s));
+    }
+    if (!start || !indices) return MEMOROID_EINVAL;
+    if ((const void*)indices == (const void*)start || (const void*)count == (const void*)start ||
+        (const void*)count == (const void*)indices)
+        return MEMOROID_EINVAL;
+    if (offset > INT64_MAX - n || offset < INT64_MIN + 1) return MEMOROID_EINVAL;
+    const size_t need = memoroid_tbb_begin_indices_workspace_bytes(n);
+    if (!workspace || workspace_bytes < need) return MEMOROID_EWORKSPACE;
+    if (!aligned(workspace, 16)) return MEMOROID_EINVAL;
+    char* ws = (char*)workspace;
+    const int64_t ntiles = (n + kTbbBeginTile - 1) / kTbbBeginTile;
+    if (ws_init_launch(ws, kAlign, ws + kAlign, need - kAlign, s) != hipSuccess) return MEMOROID_EHIP;
+    TbbBeginArgs a{};
+    a.start = start;
+    a.n = n;
+    a.offset = offset;
+    a.indices = indices;
+    a.count = count;
+    a.cnt = (uint64_t*)(ws + kAlign);
+    a.fallback_polls = fallback_polls();
+    const bool vec = aligned(start, 16) && n % 16 == 0;
+    return check_hip(tbb_begins_launch(vec, a, ntiles, s));
+}
+
+size_t memoroid_tbb_sample_workspace_bytes(int64_t n_draws) {
+    if (n_draws < 0 || n_draws > ((int64_t)1 << 24)) return 0;
+    const int64_t nb = (n_draws + kTbbDrawBlock - 1) / kTbbDrawBlock;
+    return align_up((size_t)n_draws * 8) + 2 * align_up((size_t)(nb > 0 ? nb : 1) * 8);
+}
+
+int memoroid_tbb_sample(const void* D, int64_t n_D, int64_t row_bytes, const int64_t* I, int64_t n_I,
+                        const int64_t* draws, int64_t n_draws, int64_t batch, void* out, uint8_t* out_start,
+                        int64_t* out_src, int64_t* filled, void* workspace, size_t workspace_bytes, void* stream) {
+    if (n_D < 0 || row_bytes <= 0 || n_I < 0 || n_draws < 0 || batch < 0) return MEMOROID_EINVAL;
+    if (n_draws > ((int64_t)1 << 24) || row_bytes > ((int64_t)1 << 24)) return MEMOROID_EUNSUPPORTED;
+    int64_t tmp;
+    if (!mul_ok(batch, row_bytes, &tmp) || !mul_ok(n_D, row_bytes, &tmp)) return MEMOROID_EINVAL;
+    if (n_draws > 0 && (!I || !draws || n_I == 0)) return MEMOROID_EINVAL;
+    if (n_draws > 0 && n_D > 0 && !D) return MEMOROID_EINVAL;
+    if (batch > 0 && (!out || !out_start)) return MEMOROID_EINVAL;
+    if ((I && !aligned(I, 8)) || (draws && !aligned(draws, 8)) || (out_src && !aligned(out_src, 8)) ||
+        (filled && !aligned(filled, 8)))
+        return MEMOROID_EINVAL;
+    if (batch > 0 && (out == D || (const void*)out == (const void*)I || (const void*)out == (const void*)draws ||
+                      (const void*)out_start == (const void*)out || (const void*)out_src == (const void*)out))
+        return MEMOROID_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    if (batch == 0) return filled ? check_hip(store_i64_launch(filled, 0, s)) : MEMOROID_OK;
+    const size_t need = memoroid_tbb_sample_workspace_bytes(n_draws);
+    if (n_draws > 0 && (!workspace || workspace_bytes < need)) return MEMOROID_EWORKSPACE;
+    if (workspace && !aligned(workspace, 16)) return MEMOROID_EINVAL;
+    const int64_t nb = (n_draws + kTbbDrawBlock - 1) / kTbbDrawBlock;
+    char* ws = (char*)workspace;
+    TbbSampleArgs a{};
+    a.D = D;
+    a.n_D = n_D;
+    a.row_bytes = row_bytes;
+    a.I = I;
+    a.n_I = n_I;
+    a.draws = draws;
+    a.n_draws = n_draws;
+    a.batch = batch;
+    a.out = out;
+    a.out_start = out_start;
+    a.out_src = out_src;
+    a.filled = filled;
+    a.nblocks = nb;
+    if (n_draws > 0) {
+        a.ends = (int64_t*)ws;
+        a.block_tot = (int64_t*)(ws + align_up((size_t)n_draws * 8));
+        a.block_off = (int64_t*)(ws + align_up((size_t)n_draws * 8) + align_up((size_t)nb * 8));
+    }
+    const int unit = (row_bytes % 16 == 0 && aligned(out, 16) && (!D || aligned(D, 16))) ? 16
+                     : (row_bytes % 4 == 0 && aligned(out, 4) && (!D || aligned(D, 4))) ? 4 : 1;
+    return check_hip(tbb_sample_launch(unit, a, s));
+}
+
 int memoroid_workspace_status(const void* workspace, size_t workspace_bytes, void* stream) {
     if (!workspace || workspace_bytes < sizeof(WsHeader)) return MEMOROID_EINVAL;
     uint32_t hdr[2] = {0, 0};

@@ -100,6 +100,7 @@ constexpr int kCtrStride = 32;
 // `ones_bytes` from `ones` with all-ones bytes (empty descriptors); both
 // sizes multiples of 16.
 hipError_t ws_init_launch(void* zero, size_t zero_bytes, void* ones, size_t ones_bytes, hipStream_t s);
+hipError_t store_i64_launch(int64_t* p, int64_t v, hipStream_t s);
 
 // Linear-attention memoroid: per-(chunk, head) state summaries, and outputs
 // from the scanned chunk states.  A state is S^T (64x64, row n holds column n
@@ -160,5 +161,42 @@ struct DiscArgs {
 };
 
 hipError_t disc_launch(bool vec, bool gae, const DiscArgs& a, int64_t ntiles, hipStream_t s);
+
+// ------------------------------------------------ tape-based batching
+constexpr int kTbbBeginTile = 16384;      // flags per workgroup of the compaction
+constexpr int kTbbDrawBlock = 1024;       // draws per workgroup of the length sums
+constexpr int kTbbRowsPerGroup = 1024;    // output rows per workgroup of the gather
+
+struct TbbBeginArgs {
+    const uint8_t* start;    // [n] begin flags
+    int64_t n;
+    int64_t offset;          // added to every index
+    int64_t* indices;        // out, room for n
+    int64_t* count;          // out, one value (may be NULL)
+    uint64_t* cnt;           // [tiles] count descriptor words
+    uint32_t fallback_polls;
+};
+
+hipError_t tbb_begins_launch(bool vec, const TbbBeginArgs& a, int64_t ntiles, hipStream_t s);
+
+struct TbbSampleArgs {
+    const void* D;           // [n_D][row_bytes]
+    int64_t n_D, row_bytes;
+    const int64_t* I;        // [n_I] begin indices
+    int64_t n_I;
+    const int64_t* draws;    // [n_draws] positions in I
+    int64_t n_draws;
+    int64_t batch;
+    void* out;               // [batch][row_bytes]
+    uint8_t* out_start;      // [batch]
+    int64_t* out_src;        // [batch] or NULL
+    int64_t* filled;         // one value or NULL
+    int64_t* ends;           // [n_draws] workspace: running ends within blocks
+    int64_t* block_tot;      // [nblocks] workspace
+    int64_t* block_off;      // [nblocks] workspace
+    int64_t nblocks;
+};
+
+hipError_t tbb_sample_launch(int unit, const TbbSampleArgs& a, hipStream_t s);
 
 }  // namespace memoroid

@@ -26,4 +26,15 @@ hipError_t ws_init_launch(void* zero, size_t zero_bytes, void* ones, size_t ones
     return hipGetLastError();
 }
 
+// One int64 store: outputs that must be written even when there is no work
+// (a fill kernel rather than a memset, so that the call can be captured).
+__global__ void store_i64_kernel(int64_t* p, int64_t v) {
+    if (threadIdx.x == 0) *p = v;
+}
+
+hipError_t store_i64_launch(int64_t* p, int64_t v, hipStream_t s) {
+    hipLaunchKernelGGL(store_i64_kernel, dim3(1), dim3(64), 0, s, p, v);
+    return hipGetLastError();
+}
+
 }  // namespace memoroid

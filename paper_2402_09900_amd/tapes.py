@@ -147,7 +147,7 @@ class Workload:
     """One synthetic workload: shape, dtypes and the laws it is drawn from."""
     key: int
     name: str
-    kind: str                 # "diag" or "linattn"
+    kind: str                 # "diag", "linattn", "discount", "ffm" or "tbb"
     B: int
     T: int
     d: int                    # features (diag) or heads (linattn)
@@ -182,6 +182,8 @@ WORKLOADS: Dict[int, Workload] = {
                 False, (0.0, 0.0), _uniform_int(1, 1000), False, gamma=0.99, lam=0.95),
     7: Workload(7, "ffm_c64_T262144_m32_c8_geom200_fwd", "ffm", 1, 1 << 18, 32, "c64", "c64",
                 True, (0.5, 0.995), _geometric(200.0), False, dk=32, dv=8),
+    8: Workload(8, "tbb_D16777216_row64B_batch1048576_unif1_1000", "tbb", 1, 1 << 24, 16, "f32", "f32",
+                False, (0.0, 0.0), _uniform_int(1, 1000), False, chunk=1 << 20),
 }
 
 
@@ -399,3 +401,35 @@ def make_ffm(key: int = 7, seed: Optional[int] = None, B: Optional[int] = None, 
     omega = (np.pi * np.arange(c) / max(c, 1)).astype(np.float32)
     x = _normal_f32(rng, (B, T, m))
     return FfmTape(alpha=alpha, omega=omega, x=x, start=start, B=B, T=T, m=m, c=c)
+
+
+@dataclasses.dataclass
+class TbbBuffer:
+    """A replay buffer D of n_D transitions (rows of `row` float32 values),
+    the begin flags it was filled with, the begin positions used to place
+    them (as the generator laid the episodes out), and uniform draws of
+    positions in that list (Alg. 2 samples them from U(0, card(I) - 1))."""
+    D: np.ndarray
+    start: np.ndarray
+    begins: np.ndarray
+    draws: np.ndarray
+    batch: int
+
+
+def make_tbb(key: int = 8, seed: Optional[int] = None, n: Optional[int] = None, row: Optional[int] = None,
+             batch: Optional[int] = None, n_draws: Optional[int] = None,
+             episodes: Optional[Callable] = None) -> TbbBuffer:
+    """Draw order: episode lengths, D ~ N(0, 1), draws."""
+    w = WORKLOADS[key]
+    assert w.kind == "tbb"
+    n = w.T if n is None else n
+    row = w.d if row is None else row
+    batch = w.chunk if batch is None else batch
+    law = w.episodes if episodes is None else episodes
+    rng = np.random.Generator(np.random.PCG64(key if seed is None else seed))
+    start = law(rng, n) if n > 0 else np.zeros(0, np.uint8)
+    begins = np.flatnonzero(start).astype(np.int64)        # where the generator placed each episode
+    D = _normal_f32(rng, (n, row))
+    nd = batch if n_draws is None else n_draws
+    draws = rng.integers(0, max(begins.size, 1), size=nd).astype(np.int64)
+    return TbbBuffer(D=D, start=start.astype(np.uint8), begins=begins, draws=draws, batch=batch)

@@ -144,6 +144,34 @@ def test_ffm_validation():
     assert ffm(m=1 << 30, c=1 << 30) == mb.EINVAL       # extent overflow
 
 
+def test_tbb_validation():
+    def bi(**kw):
+        args = dict(start=S, n=1000, offset=0, indices=I, count=A, workspace=W, workspace_bytes=1 << 30,
+                    stream=None)
+        args.update(kw)
+        return mb.memoroid_tbb_begin_indices(*args.values())
+
+    def sm(**kw):
+        args = dict(D=A, n_D=1000, row_bytes=64, I=X, n_I=10, draws=S, n_draws=100, batch=500, out=H,
+                    out_start=I, out_src=None, filled=None, workspace=W, workspace_bytes=1 << 30, stream=None)
+        args.update(kw)
+        return mb.memoroid_tbb_sample(*args.values())
+    assert mb.memoroid_tbb_begin_indices_workspace_bytes(1 << 24) > 256
+    assert mb.memoroid_tbb_sample_workspace_bytes(0) > 0 and mb.memoroid_tbb_sample_workspace_bytes(-1) == 0
+    assert bi(n=-1) == mb.EINVAL and bi(n=1 << 31) == mb.EUNSUPPORTED
+    assert bi(count=None) == mb.EINVAL and bi(start=None) == mb.EINVAL and bi(indices=None) == mb.EINVAL
+    assert bi(count=A + 4) == mb.EINVAL and bi(indices=S) == mb.EINVAL
+    assert bi(workspace=None) == mb.EWORKSPACE and bi(workspace_bytes=16) == mb.EWORKSPACE
+    assert sm(row_bytes=0) == mb.EINVAL and sm(batch=-1) == mb.EINVAL and sm(n_draws=-1) == mb.EINVAL
+    assert sm(n_draws=(1 << 24) + 1) == mb.EUNSUPPORTED
+    assert sm(I=None) == mb.EINVAL and sm(draws=None) == mb.EINVAL and sm(n_I=0) == mb.EINVAL
+    assert sm(out=None) == mb.EINVAL and sm(out_start=None) == mb.EINVAL
+    assert sm(out=A) == mb.EINVAL                       # batch aliases D
+    assert sm(I=X + 4) == mb.EINVAL
+    assert sm(workspace=None) == mb.EWORKSPACE and sm(workspace_bytes=8) == mb.EWORKSPACE
+    assert sm(batch=1 << 62) == mb.EINVAL               # batch * row_bytes overflows
+
+
 def test_discount_validation():
     def ret(**kw):
         args = dict(r=A, start=S, gamma=0.99, G=H, B=2, T=100, workspace=W, workspace_bytes=1 << 30, stream=None)
