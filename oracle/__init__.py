@@ -56,6 +56,8 @@ def _load():
         lib.oracle_discounted_return.argtypes = [P, P, D, I64, I64, P, P]
         lib.oracle_gae.argtypes = [P, P, P, P, P, D, D, I64, I64, P, P, P, P]
         lib.oracle_ffm.argtypes = [P, P, P, P, I64, I64, I64, I64, P, P]
+        lib.oracle_linattn_bwd.argtypes = [P, P, P, P, P, I64, I64, I64, I64, P, P, P, P, P, P]
+        lib.oracle_linattn_bwd.restype = None
         lib.oracle_tbb_begin_indices.argtypes = [P, I64, I64, P]
         lib.oracle_tbb_begin_indices.restype = I64
         lib.oracle_tbb_sample.argtypes = [P, I64, I64, P, I64, P, I64, I64, P, P, P]
@@ -253,3 +255,24 @@ def tbb_sample(D, I, draws, batch):
                                        _ptr(draws), draws.size, int(batch),
                                        out.ctypes.data_as(ctypes.c_void_p), _ptr(out_start), _ptr(out_src))
     return out, out_start, out_src, int(filled)
+
+
+def linattn_bwd(q, k, v, start, g):
+    """Gradient of the linear-attention readout w.r.t. the raw q, k, v.
+
+    q, k: [T,H,dk]; v, g: [T,H,dv]; start: [T].  Returns (dq, dk, dv, m_dq,
+    m_dk, m_dv), all float64, the last three the magnitude companions."""
+    q = np.ascontiguousarray(q, dtype=np.float64)
+    k = np.ascontiguousarray(k, dtype=np.float64)
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    g = np.ascontiguousarray(g, dtype=np.float64)
+    T, H, dk = q.shape
+    dv = v.shape[2]
+    if k.shape != (T, H, dk) or v.shape[:2] != (T, H) or g.shape != v.shape:
+        raise ValueError("q, k must be [T,H,dk]; v, g [T,H,dv]")
+    s = _flags(start, 1, T)
+    outs = [np.empty((T, H, dk)), np.empty((T, H, dk)), np.empty((T, H, dv)),
+            np.empty((T, H, dk)), np.empty((T, H, dk)), np.empty((T, H, dv))]
+    _load().oracle_linattn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(s), _ptr(g), T, H, dk, dv,
+                               *[_ptr(o) for o in outs])
+    return tuple(outs)

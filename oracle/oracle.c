@@ -211,6 +211,128 @@ void oracle_linattn(const double* q, const double* k, const double* v,
     free(qf);
 }
 
+/* ----------------------------------------------- linear attention, grad */
+
+static double phi_prime(double u) { return u > 0.0 ? 1.0 : exp(u); }
+
+void oracle_linattn_bwd(const double* q, const double* k, const double* v, const uint8_t* start,
+                        const double* g, int64_t T, int64_t H, int64_t dk, int64_t dv,
+                        double* dq, double* dk_out, double* dv_out,
+                        double* m_dq, double* m_dk, double* m_dv) {
+    const size_t nS = (size_t)(dk * dv > 0 ? dk * dv : 1);
+    const size_t nk = (size_t)(dk > 0 ? dk : 1), nv = (size_t)(dv > 0 ? dv : 1);
+    double* S = (double*)malloc(nS * sizeof(double));
+    double* Sa = (double*)malloc(nS * sizeof(double));
+    double* z = (double*)malloc(nk * sizeof(double));
+    double* U = (double*)malloc(nS * sizeof(double));
+    double* Ua = (double*)malloc(nS * sizeof(double));
+    double* w = (double*)malloc(nk * sizeof(double));
+    double* wa = (double*)malloc(nk * sizeof(double));
+    double* Qf = (double*)malloc(nk * sizeof(double));
+    double* Kf = (double*)malloc(nk * sizeof(double));
+    const size_t steps = (size_t)(T > 0 ? T : 1);
+    /* per step of one head: dnum (dv), dden, and their companions */
+    double* dnum = (double*)malloc(steps * nv * sizeof(double));
+    double* mdnum = (double*)malloc(steps * nv * sizeof(double));
+    double* dden = (double*)malloc(steps * sizeof(double));
+    double* mdden = (double*)malloc(steps * sizeof(double));
+    for (int64_t hh = 0; hh < H; ++hh) {
+        /* forward in time: the states (S, z), the readout, dnum, dden, dq */
+        for (int64_t t = 0; t < T; ++t) {
+            if (is_begin(start, T, 0, t)) {
+                memset(S, 0, nS * sizeof(double));
+                memset(Sa, 0, nS * sizeof(double));
+                memset(z, 0, nk * sizeof(double));
+            }
+            const double* qt = q + (t * H + hh) * dk;
+            const double* kt = k + (t * H + hh) * dk;
+            const double* vt = v + (t * H + hh) * dv;
+            const double* gt = g + (t * H + hh) * dv;
+            for (int64_t i = 0; i < dk; ++i) {
+                Qf[i] = oracle_phi(qt[i]);
+                Kf[i] = oracle_phi(kt[i]);
+            }
+            for (int64_t i = 0; i < dk; ++i) {
+                z[i] += Kf[i];
+                for (int64_t j = 0; j < dv; ++j) {
+                    S[i * dv + j] += Kf[i] * vt[j];
+                    Sa[i * dv + j] += Kf[i] * fabs(vt[j]);
+                }
+            }
+            double den = 0.0;
+            for (int64_t i = 0; i < dk; ++i) den += Qf[i] * z[i];
+            double go = 0.0, gm = 0.0;
+            for (int64_t j = 0; j < dv; ++j) {
+                double num = 0.0, numa = 0.0;
+                for (int64_t i = 0; i < dk; ++i) {
+                    num += Qf[i] * S[i * dv + j];
+                    numa += Qf[i] * Sa[i * dv + j];
+                }
+                go += gt[j] * (num / den);
+                gm += fabs(gt[j]) * (numa / den);
+                dnum[t * dv + j] = gt[j] / den;
+                mdnum[t * dv + j] = fabs(gt[j]) / den;
+            }
+            dden[t] = -go / den;
+            mdden[t] = gm / den;
+            for (int64_t i = 0; i < dk; ++i) {
+                double a = dden[t] * z[i], am = mdden[t] * z[i];
+                for (int64_t j = 0; j < dv; ++j) {
+                    a += S[i * dv + j] * dnum[t * dv + j];
+                    am += Sa[i * dv + j] * mdnum[t * dv + j];
+                }
+                const double d = phi_prime(qt[i]);
+                dq[(t * H + hh) * dk + i] = a * d;
+                if (m_dq) m_dq[(t * H + hh) * dk + i] = am * d;
+            }
+        }
+        /* backward in time: the reverse states (U, w), dk and dv */
+        for (int64_t t = T - 1; t >= 0; --t) {
+            const int last = (t == T - 1) || is_begin(start, T, 0, t + 1);
+            if (last) {
+                memset(U, 0, nS * sizeof(double));
+                memset(Ua, 0, nS * sizeof(double));
+                memset(w, 0, nk * sizeof(double));
+                memset(wa, 0, nk * sizeof(double));
+            }
+            const double* qt = q + (t * H + hh) * dk;
+            const double* kt = k + (t * H + hh) * dk;
+            const double* vt = v + (t * H + hh) * dv;
+            for (int64_t i = 0; i < dk; ++i) {
+                Qf[i] = oracle_phi(qt[i]);
+                Kf[i] = oracle_phi(kt[i]);
+                w[i] += dden[t] * Qf[i];
+                wa[i] += mdden[t] * Qf[i];
+                for (int64_t j = 0; j < dv; ++j) {
+                    U[i * dv + j] += Qf[i] * dnum[t * dv + j];
+                    Ua[i * dv + j] += Qf[i] * mdnum[t * dv + j];
+                }
+            }
+            for (int64_t i = 0; i < dk; ++i) {
+                double a = w[i], am = wa[i];
+                for (int64_t j = 0; j < dv; ++j) {
+                    a += U[i * dv + j] * vt[j];
+                    am += Ua[i * dv + j] * fabs(vt[j]);
+                }
+                const double d = phi_prime(kt[i]);
+                dk_out[(t * H + hh) * dk + i] = a * d;
+                if (m_dk) m_dk[(t * H + hh) * dk + i] = am * d;
+            }
+            for (int64_t j = 0; j < dv; ++j) {
+                double a = 0.0, am = 0.0;
+                for (int64_t i = 0; i < dk; ++i) {
+                    a += U[i * dv + j] * Kf[i];
+                    am += Ua[i * dv + j] * Kf[i];
+                }
+                dv_out[(t * H + hh) * dv + j] = a;
+                if (m_dv) m_dv[(t * H + hh) * dv + j] = am;
+            }
+        }
+    }
+    free(S); free(Sa); free(z); free(U); free(Ua); free(w); free(wa); free(Qf); free(Kf);
+    free(dnum); free(mdnum); free(dden); free(mdden);
+}
+
 /* ------------------------------------------------------ returns and GAE */
 
 void oracle_discounted_return(const double* r, const uint8_t* start, double gamma,

@@ -102,6 +102,24 @@ void oracle_linattn(const double* q, const double* k, const double* v,
                     const uint8_t* start, int64_t T, int64_t H, int64_t dk, int64_t dv,
                     double* out, double* m);
 
+/* Gradient of the linear-transformer memoroid readout (App. G.1; the paper
+ * differentiates it automatically, Alg. 3 trains through it).  With
+ * Q = phi(q), K = phi(k), the state (S, z) of the forward routine, num_t =
+ * Q_t^T S_t, den_t = Q_t^T z_t, out_t = num_t / den_t and g = dL/dout:
+ *   dnum_t = g_t / den_t,  dden_t = -(g_t . out_t) / den_t,
+ *   dQ_t   = S_t dnum_t + dden_t z_t,
+ *   U_t    = sum over steps s >= t of t's episode of Q_s dnum_s^T   (dk x dv),
+ *   w_t    = sum over the same steps of dden_s Q_s,
+ *   dK_t   = U_t v_t + w_t,  dV_t = U_t^T K_t,
+ *   dq = dQ (.) phi'(q), dk = dK (.) phi'(k), phi'(u) = 1 (u > 0) or exp(u).
+ * q, k, dq, dk: [T][H][dk]; v, g, dv: [T][H][dv].
+ * m_dq, m_dk, m_dv (optional): magnitude companions, the same sums over
+ * |v|, |g| and the companion of out. */
+void oracle_linattn_bwd(const double* q, const double* k, const double* v, const uint8_t* start,
+                        const double* g, int64_t T, int64_t H, int64_t dk, int64_t dv,
+                        double* dq, double* dk_out, double* dv_out,
+                        double* m_dq, double* m_dk, double* m_dv);
+
 /* Fast-and-forgetful-memory aggregator (App. G.4, FFM memoroid): per step a
  * complex m x c state
  *   S_t = x_t 1_c^T                          at a begin step,

@@ -853,3 +853,70 @@ def test_sampling_fills_the_last_row_after_an_episode_ends_one_short():
     D = np.arange(5, dtype=np.int64)
     out, out_start, out_src, filled = oracle.tbb_sample(D, I, [0, 1], 4)
     assert filled == 4 and list(out_src) == [0, 1, 2, 3] and list(out_start) == [1, 0, 0, 1]
+
+
+# ------------------------------------------------- linear attention, grad
+
+
+def _torch_linattn_grads(q, k, v, start, g):
+    """Gradients of sum(g * out) through the masked attention form of the
+    readout (App. G.1), by torch autograd in float64."""
+    import torch
+    T, H, dk = q.shape
+    qt, kt, vt = (torch.tensor(a, dtype=torch.float64, requires_grad=True) for a in (q, k, v))
+    ep = torch.tensor(np.cumsum(np.asarray(start, dtype=np.int64) != 0) + (1 if start[0] == 0 else 0))
+    same = ep[:, None] == ep[None, :]
+    causal = torch.tril(torch.ones(T, T, dtype=torch.bool))
+    mask = (same & causal).to(torch.float64)
+    Q = torch.nn.functional.elu(qt) + 1.0
+    K = torch.nn.functional.elu(kt) + 1.0
+    outs = []
+    for h in range(H):
+        W = (Q[:, h, :] @ K[:, h, :].T) * mask
+        outs.append((W @ vt[:, h, :]) / W.sum(dim=1, keepdim=True))
+    out = torch.stack(outs, dim=1)
+    (out * torch.tensor(g)).sum().backward()
+    return qt.grad.numpy(), kt.grad.numpy(), vt.grad.numpy()
+
+
+@pytest.mark.parametrize("dk,dv", [(4, 4), (3, 5)])
+def test_linattn_grad_matches_autograd(dk, dv):
+    rng = np.random.default_rng(90 + dk)
+    T, H = 40, 2
+    flags = tapes.flags_from_lengths(rng.integers(1, 12, size=10), T)
+    q, k = rng.standard_normal((T, H, dk)), rng.standard_normal((T, H, dk))
+    v, g = rng.standard_normal((T, H, dv)), rng.standard_normal((T, H, dv))
+    dq, dk_, dv_, mq, mk, mv = oracle.linattn_bwd(q, k, v, flags, g)
+    rq, rk, rv = _torch_linattn_grads(q, k, v, flags, g)
+    np.testing.assert_allclose(dq, rq, rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(dk_, rk, rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(dv_, rv, rtol=1e-11, atol=1e-12)
+    assert np.all(mq >= np.abs(dq) - 1e-12) and np.all(mk >= np.abs(dk_) - 1e-12) and np.all(mv >= np.abs(dv_) - 1e-12)
+
+
+def test_linattn_grad_finite_differences():
+    rng = np.random.default_rng(95)
+    T, H, d = 12, 1, 3
+    flags = tapes.flags_from_lengths(np.array([5, 4, 3]), T)
+    q, k, v, g = (rng.standard_normal((T, H, d)) for _ in range(4))
+    dq, dk_, dv_, _, _, _ = oracle.linattn_bwd(q, k, v, flags, g)
+    loss = lambda q_, k_, v_: float(np.sum(oracle.linattn(q_, k_, v_, flags)[0] * g))  # noqa: E731
+    eps = 1e-6
+    for arr, grad, which in ((q, dq, 0), (k, dk_, 1), (v, dv_, 2)):
+        for idx in [(0, 0, 1), (6, 0, 2), (11, 0, 0)]:
+            plus, minus = [a.copy() for a in (q, k, v)], [a.copy() for a in (q, k, v)]
+            plus[which][idx] += eps
+            minus[which][idx] -= eps
+            fd = (loss(*plus) - loss(*minus)) / (2 * eps)
+            assert abs(fd - grad[idx]) < 1e-7 * max(1.0, abs(fd)), (which, idx)
+
+
+def test_linattn_grad_single_step_episodes():
+    """Every step its own episode: out_t = v_t exactly, so dv = g and the
+    gradients w.r.t. q and k vanish."""
+    rng = np.random.default_rng(96)
+    T, H, d = 20, 2, 4
+    q, k, v, g = (rng.standard_normal((T, H, d)) for _ in range(4))
+    dq, dk_, dv_, _, _, _ = oracle.linattn_bwd(q, k, v, np.ones(T, np.uint8), g)
+    np.testing.assert_allclose(dv_, g, rtol=1e-14, atol=1e-15)
+    assert np.allclose(dq, 0.0, atol=1e-14) and np.allclose(dk_, 0.0, atol=1e-14)
