@@ -21,6 +21,7 @@ Workloads (seeded, synthetic; laws in paper_2402_09900_amd.tapes):
   7  FFM aggregator, T=262144, m=32 x c=8 complex state, Geometric(200) episodes
   8  tape-based batching: begin indices of a 2^24-transition buffer (64-byte
      rows, U{1..1000} episodes) and a sampled batch of 2^20 rows
+  9  workload 3 with the gradient of the readout (dq, dk, dv)
 
 Every buffer exists in several copies (at least 1 GiB cycled, at least 3) and
 step i uses copy i mod n, so inputs are read from HBM rather than from the
@@ -57,7 +58,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6, 7, 8])
+    p.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6, 7, 8, 9])
     p.add_argument("--no-cpu-baseline", action="store_true")
     return p.parse_args()
 
@@ -148,12 +149,16 @@ def setup_diag(torch, mb, tapes, key):
     return w, sets, bytes_per, n
 
 
-def setup_linattn(torch, mb, tapes):
-    la = tapes.make_linattn()
+def setup_linattn(torch, mb, tapes, key=3):
+    wl = tapes.WORKLOADS[key]
+    la = tapes.make_linattn(key)
     n = la.T * la.H * la.dv
     nb = mb.memoroid_scan_linattn_workspace_bytes(la.T, la.H, 64, 64, 64)
+    nbb = mb.memoroid_scan_linattn_bwd_workspace_bytes(la.T, la.H, 64, 64, 64) if wl.backward else 0
+    g_host = np.random.Generator(np.random.PCG64(key + 100)).standard_normal(la.v.shape, dtype=np.float32)
+    stream = lambda: torch.cuda.current_stream().cuda_stream  # noqa: E731
     sets = []
-    for _ in range(n_sets(4 * n * 4 + la.T * 5 + nb)):
+    for _ in range(n_sets((4 + (5 if wl.backward else 0)) * n * 4 + la.T * 5 + nb + nbb)):
         q, k, v = (dev_tensor(torch, t, "f32") for t in (la.q, la.k, la.v))
         s = dev_tensor(torch, la.start, "u8")
         out = torch.empty_like(v)
@@ -163,13 +168,31 @@ def setup_linattn(torch, mb, tapes):
         def fwd(q=q, k=k, v=v, s=s, out=out, idx=idx, ws=ws):
             st = mb.memoroid_scan_linattn(q.data_ptr(), k.data_ptr(), v.data_ptr(), s.data_ptr(), out.data_ptr(),
                                           idx.data_ptr(), la.T, la.H, 64, 64, 64, ws.data_ptr(), ws.numel(),
-                                          torch.cuda.current_stream().cuda_stream)
+                                          stream())
             assert st == 0, mb.status_string(st)
-        sets.append({"fwd": fwd})
-    # algorithmic: q, k, v read and out written once (4 B each), flags, idx
-    bytes_per = {"fwd": 4 * n * 4 + la.T * 5}
-    # chunked-dense flops: 4 contractions of 2*64^3 per (chunk, head)
-    flops = 4 * 2 * 64 ** 3 * (la.T // 64) * la.H
+        calls = {"fwd": fwd}
+        if wl.backward:
+            g = dev_tensor(torch, g_host, "f32")
+            gq, gk, gv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+            wsb = torch.empty(nbb, dtype=torch.uint8, device="cuda")
+
+            def bwd(q=q, k=k, v=v, s=s, out=out, g=g, gq=gq, gk=gk, gv=gv, wsb=wsb):
+                st = mb.memoroid_scan_linattn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), s.data_ptr(),
+                                                  out.data_ptr(), g.data_ptr(), gq.data_ptr(), gk.data_ptr(),
+                                                  gv.data_ptr(), la.T, la.H, 64, 64, 64, wsb.data_ptr(), wsb.numel(),
+                                                  stream())
+                assert st == 0, mb.status_string(st)
+            calls["bwd"] = bwd
+        sets.append(calls)
+    # algorithmic: q, k, v read and out written once (4 B each), flags, idx;
+    # backward: q, k, v, out, grad read and dq, dk, dv written once
+    bytes_per = {"fwd": 4 * n * 4 + la.T * 5, "bwd": 8 * n * 4 + la.T}
+    # chunked-dense flops per (chunk, head), 2*64^3 each: forward 4
+    # contractions (QK^T, A V, Q S_in, the chunk summary); backward 10 (the
+    # forward chunk summary, A, dP = dnum V^T, two for dq, two for dk, two
+    # for dv, and the reverse chunk summary)
+    unit = 2 * 64 ** 3 * (la.T // 64) * la.H
+    flops = {"fwd": 4 * unit, "bwd": 10 * unit}
     return la, sets, bytes_per, n, flops
 
 
@@ -325,12 +348,16 @@ def cpu_baseline(key, tapes, budget_s=20.0):
                 "sample": "first %d steps of the tape, return + advantage, fp64, %.1f s" % (T, dt)}
     if w.kind == "linattn":
         T = min(w.T, 4096)
-        la = tapes.make_linattn(T=T)
+        la = tapes.make_linattn(key, T=T)
+        q, k, v = la.q.astype(np.float64), la.k.astype(np.float64), la.v.astype(np.float64)
         t0 = time.perf_counter()
-        oracle.linattn(la.q.astype(np.float64), la.k.astype(np.float64), la.v.astype(np.float64), la.start)
+        oracle.linattn(q, k, v, la.start)
+        if w.backward:
+            oracle.linattn_bwd(q, k, v, la.start, np.ones_like(v))
         dt = time.perf_counter() - t0
+        what = "forward readout and its gradient" if w.backward else "forward readout"
         return {"value": T * la.H * la.dv / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
-                "sample": "first %d steps of the tape, all %d heads, forward readout" % (T, la.H)}
+                "sample": "first %d steps of the tape, all %d heads, %s" % (T, la.H, what)}
     # diagonal: whole tapes of the workload's law, capped so the oracle runs
     # for about budget_s seconds at most
     T = w.T
@@ -369,7 +396,7 @@ def main():
     wl = tapes.WORKLOADS[key]
     flops = None
     if wl.kind == "linattn":
-        w, sets, bytes_per, n, flops = setup_linattn(torch, mb, tapes)
+        w, sets, bytes_per, n, flops = setup_linattn(torch, mb, tapes, key)
     elif wl.kind == "discount":
         w, sets, bytes_per, n = setup_discount(torch, mb, tapes, key)
     elif wl.kind == "ffm":
@@ -410,24 +437,24 @@ def main():
     per_call_ms = {name: timers[name].mean_ms() for name in calls}
     dom = max(per_call_ms, key=per_call_ms.get)
     if flops is not None:
-        achieved = flops / (per_call_ms[dom] * 1e-3) / 1e12
+        achieved = flops[dom] / (per_call_ms[dom] * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": FP32_MFMA_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": None}
     else:
         achieved = bytes_per[dom] / (per_call_ms[dom] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None}
-    roof["traffic"] = recorded_traffic(key, "linattn" if wl.kind == "linattn" else dom)
+    roof["traffic"] = recorded_traffic(key, ("linattn_" + dom) if wl.kind == "linattn" else dom)
     roof["traffic_unit"] = "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
     roof["kernel"] = {"fwd": {"diag": "memoroid_scan_diag", "linattn": "memoroid_scan_linattn",
                               "ffm": "memoroid_scan_ffm"}.get(wl.kind),
-                      "bwd": "memoroid_scan_diag_bwd", "return": "memoroid_discounted_return",
+                      "bwd": "memoroid_scan_linattn_bwd" if wl.kind == "linattn" else "memoroid_scan_diag_bwd", "return": "memoroid_discounted_return",
                       "gae": "memoroid_gae", "insert": "memoroid_tbb_begin_indices",
                       "sample": "memoroid_tbb_sample"}[dom]
     roof["ms_per_launch"] = round(per_call_ms[dom], 4)
     roof["algorithmic_bytes_per_launch"] = int(bytes_per[dom])
     if flops is not None:
-        roof["algorithmic_flops_per_launch"] = int(flops)
+        roof["algorithmic_flops_per_launch"] = int(flops[dom])
 
     result = {
         "metric": METRIC,

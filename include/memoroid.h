@@ -189,6 +189,34 @@ int memoroid_scan_linattn(const float* q, const float* k, const float* v,
                           void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Gradient of the linear-transformer memoroid readout (App. G.1; Alg. 3
+ * trains through it).  With Q = phi(q), K = phi(k) and g = dL/dout:
+ *     dnum_t = g_t / den_t,  dden_t = -(g_t . out_t) / den_t,
+ *     dQ_t = S_t dnum_t + dden_t z_t,
+ *     dK_t = U_t v_t + w_t,  dV_t = U_t^T K_t,
+ * where (S, z) are the forward states and U_t, w_t sum Q_s dnum_s^T and
+ * dden_s Q_s over the steps s >= t of t's episode; dq = dQ (.) phi'(q),
+ * dk = dK (.) phi'(k).  Chunked like the forward pass (chunk states are
+ * recomputed, so only the forward output is needed).
+ *
+ *   q, k, v, start  as for memoroid_scan_linattn.
+ *   out        the forward output [T][H][dv] for the same inputs.
+ *   grad_out   dL/dout [T][H][dv].
+ *   grad_q, grad_k, grad_v  out [T][H][64] fp32, distinct from every input.
+ *   dk == dv == chunk == 64 (MEMOROID_EUNSUPPORTED otherwise); 16-byte
+ *   aligned fp32 arrays.
+ *   Workspace: memoroid_scan_linattn_bwd_workspace_bytes(T, H, dk, dv, chunk).
+ * ------------------------------------------------------------------------ */
+size_t memoroid_scan_linattn_bwd_workspace_bytes(int64_t T, int64_t H, int64_t dk,
+                                                 int64_t dv, int64_t chunk);
+
+int memoroid_scan_linattn_bwd(const float* q, const float* k, const float* v,
+                              const uint8_t* start, const float* out, const float* grad_out,
+                              float* grad_q, float* grad_k, float* grad_v,
+                              int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t chunk,
+                              void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Discounted return over a tape (App. D, the discounted-return memoroid
  * (a, r) . (a', r') = (a a', a r' + r) with f(r) = (gamma, r)), restarted at
  * every episode: for each step, the sum of gamma^(i-t) r_i over the steps i

@@ -59,6 +59,10 @@ def lib() -> ctypes.CDLL:
         L.memoroid_scan_linattn_workspace_bytes.argtypes = [I64, I64, I64, I64, I64]
         L.memoroid_scan_linattn.restype = I32
         L.memoroid_scan_linattn.argtypes = [P, P, P, P, P, P, I64, I64, I64, I64, I64, P, SZ, P]
+        L.memoroid_scan_linattn_bwd_workspace_bytes.restype = SZ
+        L.memoroid_scan_linattn_bwd_workspace_bytes.argtypes = [I64, I64, I64, I64, I64]
+        L.memoroid_scan_linattn_bwd.restype = I32
+        L.memoroid_scan_linattn_bwd.argtypes = [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, I64, P, SZ, P]
         L.memoroid_scan_ffm_workspace_bytes.restype = SZ
         L.memoroid_scan_ffm_workspace_bytes.argtypes = [I64, I64, I64, I64]
         L.memoroid_scan_ffm.restype = I32
@@ -128,6 +132,16 @@ def memoroid_scan_linattn(q, k, v, start, out, episode_idx, T, H, dk, dv, chunk,
                           workspace, workspace_bytes, stream) -> int:
     return lib().memoroid_scan_linattn(q, k, v, start, out, episode_idx, T, H, dk, dv, chunk,
                                        workspace, workspace_bytes, stream)
+
+
+def memoroid_scan_linattn_bwd_workspace_bytes(T, H, dk, dv, chunk) -> int:
+    return lib().memoroid_scan_linattn_bwd_workspace_bytes(T, H, dk, dv, chunk)
+
+
+def memoroid_scan_linattn_bwd(q, k, v, start, out, grad_out, grad_q, grad_k, grad_v, T, H, dk, dv, chunk,
+                              workspace, workspace_bytes, stream) -> int:
+    return lib().memoroid_scan_linattn_bwd(q, k, v, start, out, grad_out, grad_q, grad_k, grad_v, T, H, dk, dv,
+                                           chunk, workspace, workspace_bytes, stream)
 
 
 def memoroid_scan_ffm_workspace_bytes(B, T, m, c) -> int:
@@ -453,6 +467,27 @@ def gae(r, value, start, gamma: float, lam: float, value_next=None, done=None, t
     return adv.reshape(shape), (tg.reshape(shape) if tg is not None else None)
 
 
+def scan_linattn_bwd(q, k, v, start, out, grad_out, chunk: int = 64, workspace=None):
+    """Gradient of the linear-attention readout: (dq, dk, dv), each like q /
+    k / v.  out is the forward output for the same inputs."""
+    torch = _torch()
+    dev = _check_cuda(q, k, v, start, out, grad_out)
+    T, H, dk = q.shape
+    dv = v.shape[2]
+    for t in (q, k, v, out, grad_out):
+        if t.dtype != torch.float32:
+            raise TypeError("q, k, v, out and grad_out must be float32")
+    if out.shape != v.shape or grad_out.shape != v.shape or k.shape != q.shape:
+        raise ValueError("q, k must be [T,H,dk]; v, out, grad_out [T,H,dv]")
+    gq, gk, gv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    ws = _workspace(lib().memoroid_scan_linattn_bwd_workspace_bytes(T, H, dk, dv, chunk), dev, workspace)
+    st = lib().memoroid_scan_linattn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), start.data_ptr(), out.data_ptr(),
+                                         grad_out.data_ptr(), gq.data_ptr(), gk.data_ptr(), gv.data_ptr(), T, H,
+                                         dk, dv, chunk, ws.data_ptr(), ws.numel(), _stream_ptr(dev))
+    _raise(st, "memoroid_scan_linattn_bwd")
+    return gq, gk, gv
+
+
 def workspace_status(workspace) -> int:
     """Synchronise and report whether the last call on `workspace` timed out
     in a cross-tile wait (ETIMEOUT) or completed normally (OK)."""
@@ -493,3 +528,35 @@ def diag_scan(a, x, start):
     if _DiagScan is None:
         _DiagScan = _make_autograd()
     return _DiagScan.apply(a, x, start)
+
+
+def _make_linattn_autograd():
+    torch = _torch()
+
+    class LinAttn(torch.autograd.Function):
+        """Differentiable linear-attention readout over a tape with resets."""
+
+        @staticmethod
+        def forward(ctx, q, k, v, start):
+            out = scan_linattn(q, k, v, start)
+            ctx.save_for_backward(q, k, v, start, out)
+            return out
+
+        @staticmethod
+        def backward(ctx, grad_out):
+            q, k, v, start, out = ctx.saved_tensors
+            gq, gk, gv = scan_linattn_bwd(q, k, v, start, out, grad_out.contiguous())
+            return gq, gk, gv, None
+
+    return LinAttn
+
+
+_LinAttn = None
+
+
+def linattn(q, k, v, start):
+    """Autograd-aware scan_linattn."""
+    global _LinAttn
+    if _LinAttn is None:
+        _LinAttn = _make_linattn_autograd()
+    return _LinAttn.apply(q, k, v, start)

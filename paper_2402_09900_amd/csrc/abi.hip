@@ -471,6 +471,164 @@ int memoroid_scan_linattn(const float* q, const float* k, const float* v, const 
     return MEMOROID_OK;
 }
 
+// ------------------------------------------------- linear attention, grad
+
+namespace {
+
+struct LinBwdPlan {
+    LinPlan fwd;                 // the forward summaries and state scan, from offset 0
+    DiagPlan rscan;              // the reverse chunk-state scan
+    size_t off_dnum = 0, off_dden = 0, off_dU = 0, off_Y = 0, off_Rs = 0, off_rscan = 0, total = 0;
+};
+
+bool plan_linattn_bwd(int64_t T, int64_t H, LinBwdPlan* p) {
+    if (!plan_linattn(T, H, &p->fwd)) return false;
+    const int64_t nch = p->fwd.nch;
+    const size_t states = (size_t)nch * (size_t)p->fwd.dstate * 4;
+    size_t off = align_up(p->fwd.total);
+    p->off_dnum = off;
+    off = align_up(off + (size_t)T * (size_t)H * kLinChunk * 4);
+    p->off_dden = off;
+    off = align_up(off + (size_t)T * (size_t)H * 4);
+    p->off_dU = off;
+    off = align_up(off + states);
+    p->off_Y = off;
+    off = align_up(off + states);
+    p->off_Rs = off;
+    off = align_up(off + (size_t)nch);
+    if (!plan_diag(1, nch, p->fwd.dstate, MEMOROID_F32, true, diag_rows(true, true), true, true, false, &p->rscan))
+        return false;
+    p->off_rscan = off;
+    off = align_up(off + p->rscan.total);
+    p->total = off;
+    return true;
+}
+
+}  // namespace
+
+size_t memoroid_scan_linattn_bwd_workspace_bytes(int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t chunk) {
+    if (T <= 0 || H <= 0 || dk != 64 || dv != 64 || chunk != 64) return 0;
+    if (T > (int64_t)INT32_MAX / 2 || H > 65535) return 0;
+    LinBwdPlan p;
+    if (!plan_linattn_bwd(T, H, &p)) return 0;
+    return p.total;
+}
+
+int memoroid_scan_linattn_bwd(const float* q, const float* k, const float* v, const uint8_t* start,
+                              const float* out, const float* grad_out, float* grad_q, float* grad_k, float* grad_v,
+                              int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t chunk, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+    if (T < 0 || H < 0 || dk < 0 || dv < 0 || chunk < 0) return MEMOROID_EINVAL;
+    if (dk != 64 || dv != 64 || chunk != 64) return MEMOROID_EUNSUPPORTED;
+    if (T == 0 || H == 0) return MEMOROID_OK;
+    if (T > (int64_t)INT32_MAX / 2 || H > 65535) return MEMOROID_EUNSUPPORTED;
+    const float* ins[6] = {q, k, v, out, grad_out, nullptr};
+    float* outs[3] = {grad_q, grad_k, grad_v};
+    for (int i = 0; i < 5; ++i)
+        if (!ins[i] || !aligned(ins[i], 16)) return MEMOROID_EINVAL;
+    if (!start) return MEMOROID_EINVAL;
+    for (int o = 0; o < 3; ++o) {
+        if (!outs[o] || !aligned(outs[o], 16)) return MEMOROID_EINVAL;
+        for (int i = 0; i < 5; ++i)
+            if ((const float*)outs[o] == ins[i]) return MEMOROID_EINVAL;
+        for (int o2 = 0; o2 < o; ++o2)
+            if (outs[o] == outs[o2]) return MEMOROID_EINVAL;
+    }
+    LinBwdPlan p;
+    if (!plan_linattn_bwd(T, H, &p)) return MEMOROID_EUNSUPPORTED;
+    if (!workspace || workspace_bytes < p.total) return MEMOROID_EWORKSPACE;
+    if (!aligned(workspace, 256)) return MEMOROID_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    const LinPlan& f = p.fwd;
+    char* sw = ws + f.off_scan;
+    float* dS = (float*)(ws + f.off_dS);
+    float* Sinc = (float*)(ws + f.off_Sinc);
+    uint8_t* R = (uint8_t*)(ws + f.off_R);
+
+    // forward chunk states (as in the forward pass, without the readout)
+    LinSummaryArgs sa{};
+    sa.k = k;
+    sa.v = v;
+    sa.start = start;
+    sa.dS = dS;
+    sa.R = R;
+    sa.T = T;
+    sa.H = H;
+    sa.zero = (u32x4*)sw;
+    sa.zero16 = (int64_t)(f.scan.off_agg / 16);
+    sa.fill = (u32x4*)(sw + f.scan.off_agg);
+    sa.fill16 = (int64_t)((f.off_cnt + (size_t)f.nch * 8 - (f.off_scan + f.scan.off_agg) + 15) / 16);
+    if (linattn_summary_launch(sa, s) != hipSuccess) return MEMOROID_EHIP;
+    DiagFwdArgs fa{};
+    fa.a = nullptr;
+    fa.x = dS;
+    fa.start = R;
+    fa.h = Sinc;
+    fa.T = f.nch;
+    fa.d = f.dstate;
+    fa.Qp = f.scan.Qp;
+    fa.nfb = f.scan.nfb;
+    fa.nchains = (int32_t)f.scan.nchains;
+    fa.agg = sw + f.scan.off_agg;
+    fa.incl = sw + f.scan.off_incl;
+    fa.hdr = (WsHeader*)sw;
+    fa.ctr = (uint32_t*)(sw + f.scan.off_ctr);
+    if (diag_fwd_launch(K_F32, K_F32, true, true, fa, f.scan.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
+
+    // backward summaries (and the reverse scan's workspace set-up)
+    char* rw = ws + p.off_rscan;
+    LinBwdArgs ba{};
+    ba.q = q;
+    ba.k = k;
+    ba.v = v;
+    ba.out = out;
+    ba.g = grad_out;
+    ba.start = start;
+    ba.Sinc = Sinc;
+    ba.dnum = (float*)(ws + p.off_dnum);
+    ba.dden = (float*)(ws + p.off_dden);
+    ba.dU = (float*)(ws + p.off_dU);
+    ba.Rs = (uint8_t*)(ws + p.off_Rs);
+    ba.Y = (const float*)(ws + p.off_Y);
+    ba.dq = grad_q;
+    ba.dk = grad_k;
+    ba.dv = grad_v;
+    ba.T = T;
+    ba.H = H;
+    ba.nch = f.nch;
+    ba.zero = (u32x4*)rw;
+    ba.zero16 = (int64_t)(p.rscan.off_agg / 16);
+    ba.fill = (u32x4*)(rw + p.rscan.off_agg);
+    ba.fill16 = (int64_t)(p.rscan.fill_bytes / 16);
+    if (linattn_bwd_summary_launch(ba, s) != hipSuccess) return MEMOROID_EHIP;
+
+    // reverse chunk-state scan: Y_c = dU_c + [chunk c holds no begin] Y_{c+1}
+    // (the reverse diagonal scan with a = 1, cut by the shifted chunk flags);
+    // a wait that gives up flags the timeout word of the forward header
+    DiagBwdArgs ra{};
+    ra.a = nullptr;
+    ra.start = ba.Rs;
+    ra.h = nullptr;
+    ra.g = ba.dU;
+    ra.dx = (void*)ba.Y;
+    ra.da = nullptr;
+    ra.da_part = nullptr;
+    ra.T = f.nch;
+    ra.d = f.dstate;
+    ra.nt = p.rscan.nt;
+    ra.Qp = p.rscan.Qp;
+    ra.nfb = p.rscan.nfb;
+    ra.nchains = (int32_t)p.rscan.nchains;
+    ra.agg = rw + p.rscan.off_agg;
+    ra.incl = rw + p.rscan.off_incl;
+    ra.hdr = (WsHeader*)sw;
+    ra.ctr = (uint32_t*)(rw + p.rscan.off_ctr);
+    if (diag_bwd_launch(K_F32, true, true, ra, p.rscan.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
+
+    return check_hip(linattn_bwd_grad_launch(ba, s));
+}
+
 // ------------------------------------------------------------------ status
 
 // ------------------------------------------- discounted return and GAE

@@ -82,7 +82,7 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     const uint32_t lrow = (uint32_t)((wave * Gw + j) * R);
     const Rsrc rs_st = make_rsrc(st + tile_row0, rows_left);
     const Rsrc rs_g = make_rsrc((const char*)p.g + tape_row0 * rowB, rows_left * rowB);
-    const Rsrc rs_a = make_rsrc(AINV ? p.a : (const char*)p.a + tape_row0 * rowB, AINV ? 0 : rows_left * rowB);
+    const Rsrc rs_a = make_rsrc(AINV ? p.g : (const char*)p.a + tape_row0 * rowB, AINV ? 0 : rows_left * rowB);
     // h_{t-1}: based one step before the tile (when there is one), so the
     // tile's first step reads the previous tile's last h
     const int64_t h_back = tile_row0 > 0 ? 1 : 0;
@@ -118,10 +118,13 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     }
     S ainv[VEC];
     if constexpr (AINV) {
+        // a NULL time-invariant a stands for a = 1 (the reverse sum, used by
+        // the linear-attention gradient's state scan)
         RawVec<K, VEC> r0;
-        if (active) raw_load(r0, (const char*)p.a + f0 * EB);
+        const bool have = active && p.a != nullptr;
+        if (have) raw_load(r0, (const char*)p.a + f0 * EB);
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) ainv[v] = active ? conj(C::get(r0, v)) : s_one<S>();
+        for (int v = 0; v < VEC; ++v) ainv[v] = have ? conj(C::get(r0, v)) : s_one<S>();
     }
     auto coef = [&](int r, int v) -> S {      // conj(a_{t+1})
         if constexpr (AINV) return ainv[v];

@@ -139,6 +139,32 @@ struct LinOutputArgs {
 hipError_t linattn_summary_launch(const LinSummaryArgs& a, hipStream_t s);
 hipError_t linattn_output_launch(const LinOutputArgs& a, hipStream_t s);
 
+struct LinBwdArgs {
+    const float* q;
+    const float* k;
+    const float* v;
+    const float* out;   // forward readout [T][H][64]
+    const float* g;     // dL/dout [T][H][64]
+    const uint8_t* start;
+    const float* Sinc;  // forward chunk states after each chunk [chunks][H][kLinStateWords]
+    float* dnum;        // workspace [T][H][64]
+    float* dden;        // workspace [T][H]
+    float* dU;          // reverse chunk summaries [chunks][H][kLinStateWords] (U [kd][n], then w)
+    uint8_t* Rs;        // [chunks] reverse-scan flags: Rs[c] = chunk c - 1 holds a begin
+    const float* Y;     // reverse-scanned states [chunks][H][kLinStateWords]
+    float* dq;
+    float* dk;
+    float* dv;
+    int64_t T, H, nch;
+    u32x4* zero;        // reverse-scan workspace to zero (header, counters), 16-byte units
+    int64_t zero16;
+    u32x4* fill;        // reverse-scan descriptors to fill with all-ones bytes
+    int64_t fill16;
+};
+
+hipError_t linattn_bwd_summary_launch(const LinBwdArgs& a, hipStream_t s);
+hipError_t linattn_bwd_grad_launch(const LinBwdArgs& a, hipStream_t s);
+
 // ------------------------------------------- discounted return and GAE
 constexpr int kDiscRows = 16;                       // steps per lane
 constexpr int kDiscTile = 4 * 64 * kDiscRows;       // steps per tile (4 wavefronts)

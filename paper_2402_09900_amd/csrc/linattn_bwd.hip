@@ -1,0 +1,351 @@
+// linattn_bwd.hip -- gradient of the linear-transformer memoroid readout
+// (App. G.1) over a tape with resets, chunked like the forward pass, for
+// gfx950.
+//
+// With Q = phi(q), K = phi(k), the forward states (S, z) and g = dL/dout:
+//   dnum_i = g_i / den_i,  dden_i = -(g_i . out_i) / den_i,
+//   dP     = (dnum V^T + dden 1^T) masked to the forward pattern M (j <= i,
+//            j >= r_i: row i's episode inside the chunk),
+//   dQ     = dP K + [r_i < 0] (S_in dnum_i + dden_i z_in),
+//   dK     = dP^T Q + [row j's episode runs past the chunk] (U_out v_j + w_out),
+//   dV     = (A (.) M)^T dnum + [same] U_out^T K_j,
+// where (U, w) are reverse states: sums of Q_t dnum_t^T and dden_t Q_t over
+// the later steps of the episode.  Per chunk the reverse summary is
+// dU = sum of Q_i dnum_i^T over the rows before the chunk's first begin step
+// (the rows whose episode continues into the previous chunk), and the chunk
+// states are scanned right to left with the resettable reverse scan (a = 1),
+// cut at every chunk that holds a begin step.
+//
+// Kernels: the forward summary and state scan (shared with the forward
+// pass) give S_in, z_in; the backward summary computes den, dnum, dden for
+// every row (kept in the workspace) and dU; the reverse state scan gives
+// U_out; then one kernel forms dq and one forms dk and dv.  Each workgroup
+// (one chunk of one head) uses four 64x64 LDS tiles, restaged between
+// contractions in the layout each operand needs.
+#include "linattn_common.hpp"
+
+namespace memoroid {
+
+namespace {
+
+__device__ __forceinline__ float phi_prime(float u) { return u > 0.0f ? 1.0f : __expf(u); }
+
+// Row `lane` of the chunk: its begin flag and the last begin at or before it
+// (an inclusive max-scan across the wavefront; every wavefront has all 64).
+__device__ __forceinline__ int row_last_begin(const uint8_t* start, int64_t t0, int nvalid, bool& beg) {
+    const int lane = threadIdx.x & 63;
+    beg = lane < nvalid && is_begin(start, t0 + lane);
+    int rmax = beg ? lane : -1;
+#pragma unroll
+    for (int k = 1; k < 64; k <<= 1) {
+        const int o = __shfl_up(rmax, k, 64);
+        if (lane >= k) rmax = rmax > o ? rmax : o;
+    }
+    return rmax;
+}
+
+// Mask of the forward pattern for the accumulator element (i, j) of this
+// lane: j <= i, j >= max(r_i, 0), i a valid row.
+__device__ __forceinline__ bool keep_ij(int i, int j, int ri, int nvalid) {
+    return i < nvalid && j <= i && j >= (ri > 0 ? ri : 0);
+}
+
+// Write a 64x64 accumulator tile (acc[jt][r] = C[16w + 4(lane/16) + r][16 jt + lane%16])
+// to LDS, natural or rotated.
+template <bool ROT>
+__device__ __forceinline__ void acc_to_lds(float* s, const f32x4 (&acc)[4]) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int row = 16 * w + 4 * (lane >> 4) + r, col = 16 * jt + (lane & 15);
+            s[row * kLD + (ROT ? rot_col(row, col) : col)] = acc[jt][r];
+        }
+}
+
+// Stage a 64x64 state block stored row-major at src (64 rows of 64 floats)
+// into LDS, natural or rotated; zeros if src is NULL.
+template <bool ROT>
+__device__ __forceinline__ void stage_state(float* s, const float* src) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int f = threadIdx.x + 256 * u;
+        const int row = f >> 4, c4 = (f & 15) * 4;
+        f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
+        if (src) v = *(const f32x4*)(src + row * kC + c4);
+        *(f32x4*)(s + row * kLD + (ROT ? rot_col(row, c4) : c4)) = v;
+    }
+}
+
+__device__ __forceinline__ void zero_acc(f32x4 (&acc)[4]) {
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt) acc[jt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+}
+
+}  // namespace
+
+// ------------------------------------------------------------- summaries
+// den, dnum, dden of every row (to the workspace), the reverse summary
+// (dU, dw) of the rows before the chunk's first begin, and the shifted chunk
+// flag of the reverse scan.  Also initialises the reverse scan's workspace.
+__global__ __launch_bounds__(256) void linattn_bwd_summary_kernel(LinBwdArgs p) {
+    __shared__ __attribute__((aligned(16))) float sQ[kC * kLD];   // phi(Q), later rotated rows < fb
+    __shared__ __attribute__((aligned(16))) float sK[kC * kLD];   // phi(K), later dnum rotated rows < fb
+    __shared__ float sZ[kC], sDen[kC], sDd[kC];
+    const int64_t c = blockIdx.x, h = blockIdx.y;
+    const int64_t t0 = c * kC;
+    const int nvalid = (int)(p.T - t0 < kC ? p.T - t0 : kC);
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+
+    {   // reverse-scan workspace: header and counters zeroed, descriptors all-ones
+        const int64_t nblk = (int64_t)gridDim.x * gridDim.y;
+        const int64_t gid = (int64_t)(blockIdx.y * gridDim.x + blockIdx.x) * 256 + tid;
+        const u32x4 zeros = {0u, 0u, 0u, 0u};
+        for (int64_t i = gid; i < p.zero16; i += nblk * 256) p.zero[i] = zeros;
+        const u32x4 ones = {kEmpty32, kEmpty32, kEmpty32, kEmpty32};
+        for (int64_t i = gid; i < p.fill16; i += nblk * 256) p.fill[i] = ones;
+    }
+
+    bool beg;
+    const int rmax = row_last_begin(p.start, t0, nvalid, beg);
+    const uint64_t mb = __ballot(beg);
+    const int fb = mb ? __builtin_ctzll(mb) : kC;        // first begin row (64: none)
+
+    stage<true, false>(sQ, p.q, t0, p.H, h, 0, nvalid);
+    stage<true, false>(sK, p.k, t0, p.H, h, 0, nvalid);
+    if (tid < kC) sZ[tid] = c > 0 ? p.Sinc[((c - 1) * p.H + h) * kStateWords + kC * kC + tid] : 0.0f;
+    __syncthreads();
+
+    f32x4 accA[4];
+    zero_acc(accA);
+    mfma_64x64x64<true, true>(sQ, sK, accA);               // A[i][j] = phi(q_i) . phi(k_j)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int i = 16 * w + 4 * (lane >> 4) + r;
+        const int ri = __shfl(rmax, i, 64);
+        float rs = 0.0f;
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt)
+            rs += keep_ij(i, 16 * jt + (lane & 15), ri, nvalid) ? accA[jt][r] : 0.0f;
+        const int kd = 4 * (lane & 15);
+        const f32x4 qv = *(const f32x4*)(sQ + i * kLD + kd);
+        float qz = qv.x * sZ[kd] + qv.y * sZ[kd + 1] + qv.z * sZ[kd + 2] + qv.w * sZ[kd + 3];
+        rs = sum16(rs);
+        qz = sum16(qz);
+        if ((lane & 15) == 0) sDen[i] = rs + (ri < 0 ? qz : 0.0f);
+    }
+    __syncthreads();                                         // den ready; sQ/sK reads done
+
+    // dnum = g / den and dden = -(g . out) / den: four threads per row, 16
+    // columns each
+    {
+        const int row = tid >> 2, c0 = (tid & 3) * 16;
+        f32x4 gv[4], ov[4];
+        float dot = 0.0f;
+        const bool ok = row < nvalid;
+        const int64_t base = ((t0 + row) * p.H + h) * kC + c0;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            gv[u] = ok ? *(const f32x4*)(p.g + base + 4 * u) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            ov[u] = ok ? *(const f32x4*)(p.out + base + 4 * u) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            dot += gv[u].x * ov[u].x + gv[u].y * ov[u].y + gv[u].z * ov[u].z + gv[u].w * ov[u].w;
+        }
+        dot += __shfl_xor(dot, 1, 64);
+        dot += __shfl_xor(dot, 2, 64);
+        const float den = sDen[row];
+        const float dd = -dot / den;
+        const bool in_du = row < fb;                         // row's episode continues to the left
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            f32x4 dn;
+            dn.x = gv[u].x / den; dn.y = gv[u].y / den; dn.z = gv[u].z / den; dn.w = gv[u].w / den;
+            if (ok) *(f32x4*)(p.dnum + base + 4 * u) = dn;
+            const f32x4 zz = {0.0f, 0.0f, 0.0f, 0.0f};
+            *(f32x4*)(sK + row * kLD + rot_col(row, c0 + 4 * u)) = (ok && in_du) ? dn : zz;
+        }
+        if ((tid & 3) == 0) {
+            if (ok) p.dden[(t0 + row) * p.H + h] = dd;
+            sDd[row] = (ok && in_du) ? dd : 0.0f;
+        }
+    }
+    stage<true, true>(sQ, p.q, t0, p.H, h, 0, fb < nvalid ? fb : nvalid);   // phi(Q) rows < fb, rotated
+    __syncthreads();
+
+    f32x4 accU[4];
+    zero_acc(accU);
+    // dU[kd][n] = sum_i Q[i][kd] dnum[i][n]: A = Q^T, B = dnum, both k-major
+    mfma_64x64x64<false, false>(sQ, sK, accU);
+    float* du = p.dU + (c * p.H + h) * kStateWords;
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            du[(16 * w + 4 * (lane >> 4) + r) * kC + 16 * jt + (lane & 15)] = accU[jt][r];
+    if (tid < kC) {
+        float s = 0.0f;
+        for (int i = 0; i < kC; ++i) s += sDd[i] * sQ[i * kLD + rot_col(i, tid)];
+        du[kC * kC + tid] = s;
+    }
+    if (h == 0 && tid == 0) {
+        if (c == 0) p.Rs[0] = 1;
+        if (c + 1 < p.nch) p.Rs[c + 1] = mb ? 1 : 0;
+    }
+}
+
+// ------------------------------------------------------------------- dq
+__global__ __launch_bounds__(256) void linattn_bwd_dq_kernel(LinBwdArgs p) {
+    __shared__ __attribute__((aligned(16))) float X0[kC * kLD];   // dP (natural)
+    __shared__ __attribute__((aligned(16))) float X1[kC * kLD];   // phi(K), rotated
+    __shared__ __attribute__((aligned(16))) float X2[kC * kLD];   // dnum (natural)
+    __shared__ __attribute__((aligned(16))) float X3[kC * kLD];   // V (natural), later S_in^T rotated
+    __shared__ float sZ[kC];
+    const int64_t c = blockIdx.x, h = blockIdx.y;
+    const int64_t t0 = c * kC;
+    const int nvalid = (int)(p.T - t0 < kC ? p.T - t0 : kC);
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    bool beg;
+    const int rmax = row_last_begin(p.start, t0, nvalid, beg);
+
+    stage<false, false>(X2, p.dnum, t0, p.H, h, 0, nvalid);
+    stage<false, false>(X3, p.v, t0, p.H, h, 0, nvalid);
+    stage<true, true>(X1, p.k, t0, p.H, h, 0, nvalid);
+    __syncthreads();
+
+    f32x4 acc[4];
+    zero_acc(acc);
+    mfma_64x64x64<true, true>(X2, X3, acc);                  // dnum_i . v_j
+    int ri[4];
+    float dd[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int i = 16 * w + 4 * (lane >> 4) + r;
+        ri[r] = __shfl(rmax, i, 64);
+        dd[r] = i < nvalid ? p.dden[(t0 + i) * p.H + h] : 0.0f;
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt)
+            acc[jt][r] = keep_ij(i, 16 * jt + (lane & 15), ri[r], nvalid) ? acc[jt][r] + dd[r] : 0.0f;
+    }
+    acc_to_lds<false>(X0, acc);
+    __syncthreads();                                         // X3 (V) free
+    stage_state<true>(X3, c > 0 ? p.Sinc + ((c - 1) * p.H + h) * kStateWords : nullptr);   // S_in^T [n][kd]
+    if (tid < kC) sZ[tid] = c > 0 ? p.Sinc[((c - 1) * p.H + h) * kStateWords + kC * kC + tid] : 0.0f;
+    __syncthreads();
+
+    f32x4 accQ[4], accS[4];
+    zero_acc(accQ);
+    zero_acc(accS);
+    mfma_64x64x64<true, false>(X0, X1, accQ);                // sum_j dP[i][j] K[j][kd]
+    mfma_64x64x64<true, false>(X2, X3, accS);                // sum_n dnum[i][n] S_in[kd][n]
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int i = 16 * w + 4 * (lane >> 4) + r, kd = 16 * jt + (lane & 15);
+            if (i < nvalid) {
+                const float dQ = accQ[jt][r] + (ri[r] < 0 ? accS[jt][r] + dd[r] * sZ[kd] : 0.0f);
+                const int64_t o = ((t0 + i) * p.H + h) * kC + kd;
+                p.dq[o] = dQ * phi_prime(p.q[o]);
+            }
+        }
+}
+
+// --------------------------------------------------------------- dk, dv
+__global__ __launch_bounds__(256) void linattn_bwd_dkv_kernel(LinBwdArgs p) {
+    __shared__ __attribute__((aligned(16))) float X0[kC * kLD];
+    __shared__ __attribute__((aligned(16))) float X1[kC * kLD];   // phi(K) natural throughout
+    __shared__ __attribute__((aligned(16))) float X2[kC * kLD];
+    __shared__ __attribute__((aligned(16))) float X3[kC * kLD];
+    __shared__ float sW[kC];
+    const int64_t c = blockIdx.x, h = blockIdx.y;
+    const int64_t t0 = c * kC;
+    const int nvalid = (int)(p.T - t0 < kC ? p.T - t0 : kC);
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    bool beg;
+    const int rmax = row_last_begin(p.start, t0, nvalid, beg);
+    const uint64_t mb = __ballot(beg);
+    const int lastb = mb ? 63 - __builtin_clzll(mb) : -1;    // rows >= lastb continue past the chunk
+    const float* uo = c + 1 < p.nch ? p.Y + ((c + 1) * p.H + h) * kStateWords : nullptr;
+
+    stage<true, false>(X0, p.q, t0, p.H, h, 0, nvalid);
+    stage<true, false>(X1, p.k, t0, p.H, h, 0, nvalid);
+    stage<false, false>(X2, p.dnum, t0, p.H, h, 0, nvalid);
+    stage<false, false>(X3, p.v, t0, p.H, h, 0, nvalid);
+    __syncthreads();
+
+    f32x4 accA[4], accP[4];
+    zero_acc(accA);
+    zero_acc(accP);
+    mfma_64x64x64<true, true>(X0, X1, accA);                 // A = Q K^T
+    mfma_64x64x64<true, true>(X2, X3, accP);                 // dnum_i . v_j
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int i = 16 * w + 4 * (lane >> 4) + r;
+        const int ri = __shfl(rmax, i, 64);
+        const float dd = i < nvalid ? p.dden[(t0 + i) * p.H + h] : 0.0f;
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt) {
+            const bool keep = keep_ij(i, 16 * jt + (lane & 15), ri, nvalid);
+            accA[jt][r] = keep ? accA[jt][r] : 0.0f;
+            accP[jt][r] = keep ? accP[jt][r] + dd : 0.0f;
+        }
+    }
+    __syncthreads();                                         // X0 (Q), X2 (dnum) free
+    stage<true, true>(X0, p.q, t0, p.H, h, 0, nvalid);       // phi(Q) rotated
+    acc_to_lds<true>(X2, accP);                              // dP rotated
+    __syncthreads();
+
+    f32x4 accK[4];
+    zero_acc(accK);
+    mfma_64x64x64<false, false>(X2, X0, accK);               // sum_i dP[i][j] Q[i][kd]
+    __syncthreads();                                         // X0, X2 free
+    stage_state<false>(X0, uo);                              // U_out [kd][n], natural
+    if (tid < kC) sW[tid] = uo ? uo[kC * kC + tid] : 0.0f;
+    acc_to_lds<true>(X2, accA);                              // A (masked) rotated
+    __syncthreads();
+
+    f32x4 accK2[4];
+    zero_acc(accK2);
+    mfma_64x64x64<true, true>(X3, X0, accK2);                // sum_n V[j][n] U[kd][n]
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int j = 16 * w + 4 * (lane >> 4) + r, kd = 16 * jt + (lane & 15);
+            if (j < nvalid) {
+                const float dK = accK[jt][r] + (j >= lastb ? accK2[jt][r] + sW[kd] : 0.0f);
+                const int64_t o = ((t0 + j) * p.H + h) * kC + kd;
+                p.dk[o] = dK * phi_prime(p.k[o]);
+            }
+        }
+    __syncthreads();                                         // X0, X3 free
+    stage<false, true>(X3, p.dnum, t0, p.H, h, 0, nvalid);   // dnum rotated
+    stage_state<true>(X0, uo);                               // U_out rotated
+    __syncthreads();
+
+    f32x4 accV[4], accV2[4];
+    zero_acc(accV);
+    zero_acc(accV2);
+    mfma_64x64x64<false, false>(X2, X3, accV);               // sum_i A[i][j] dnum[i][n]
+    mfma_64x64x64<true, false>(X1, X0, accV2);               // sum_kd K[j][kd] U[kd][n]
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int j = 16 * w + 4 * (lane >> 4) + r, n = 16 * jt + (lane & 15);
+            if (j < nvalid) p.dv[((t0 + j) * p.H + h) * kC + n] = accV[jt][r] + (j >= lastb ? accV2[jt][r] : 0.0f);
+        }
+}
+
+hipError_t linattn_bwd_summary_launch(const LinBwdArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL(linattn_bwd_summary_kernel, dim3((unsigned)a.nch, (unsigned)a.H), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t linattn_bwd_grad_launch(const LinBwdArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL(linattn_bwd_dq_kernel, dim3((unsigned)a.nch, (unsigned)a.H), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(linattn_bwd_dkv_kernel, dim3((unsigned)a.nch, (unsigned)a.H), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace memoroid

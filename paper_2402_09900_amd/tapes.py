@@ -184,6 +184,8 @@ WORKLOADS: Dict[int, Workload] = {
                 True, (0.5, 0.995), _geometric(200.0), False, dk=32, dv=8),
     8: Workload(8, "tbb_D16777216_row64B_batch1048576_unif1_1000", "tbb", 1, 1 << 24, 16, "f32", "f32",
                 False, (0.0, 0.0), _uniform_int(1, 1000), False, chunk=1 << 20),
+    9: Workload(9, "linattn_f32_T32768_H4_dk64_dv64_geom500_chunk64_fwd_bwd", "linattn", 1, 32768, 4, "f32", "f32",
+                False, (0.0, 0.0), _geometric(500.0), True, dk=64, dv=64, chunk=64),
 }
 
 

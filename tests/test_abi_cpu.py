@@ -124,6 +124,23 @@ def test_linattn_validation():
     assert la(workspace_bytes=1000) == mb.EWORKSPACE
 
 
+def test_linattn_bwd_validation():
+    def lb(**kw):
+        args = dict(q=A, k=X, v=S, start=H + 0x100, out=I, grad_out=W + 0x100000, grad_q=0x90000, grad_k=0xA0000,
+                    grad_v=0xB0000, T=1000, H=4, dk=64, dv=64, chunk=64, workspace=W, workspace_bytes=1 << 30,
+                    stream=None)
+        args.update(kw)
+        return mb.memoroid_scan_linattn_bwd(*args.values())
+    assert mb.memoroid_scan_linattn_bwd_workspace_bytes(32768, 4, 64, 64, 64) > \
+        mb.memoroid_scan_linattn_workspace_bytes(32768, 4, 64, 64, 64)
+    assert lb(dk=32) == mb.EUNSUPPORTED and lb(chunk=32) == mb.EUNSUPPORTED
+    assert lb(T=0) == mb.OK and lb(T=-1) == mb.EINVAL
+    assert lb(q=None) == mb.EINVAL and lb(grad_out=None) == mb.EINVAL and lb(grad_v=None) == mb.EINVAL
+    assert lb(grad_q=A) == mb.EINVAL and lb(grad_k=0x90000) == mb.EINVAL     # aliasing
+    assert lb(q=A + 4) == mb.EINVAL
+    assert lb(workspace=None) == mb.EWORKSPACE and lb(workspace_bytes=4096) == mb.EWORKSPACE
+
+
 def test_ffm_validation():
     def ffm(**kw):
         args = dict(alpha=A, omega=X, x=S, start=H + 0x100, S=I, episode_idx=None, B=2, T=100, m=4, c=3,

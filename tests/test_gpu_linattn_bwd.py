@@ -1,0 +1,89 @@
+"""Parity of the linear-attention gradient kernels (through the C ABI) with
+the fp64 oracle: conditioned relative error (|y - r| / max(|r|, m), m the
+oracle's magnitude companion) at most 1e-4 for dq, dk and dv (fp32
+arithmetic).  The full workload is compared on every element."""
+import numpy as np
+import pytest
+
+import oracle
+from conftest import announce, cond_err
+from paper_2402_09900_amd import tapes
+
+torch = pytest.importorskip("torch")
+from paper_2402_09900_amd import binding as mb  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+TOL = 1e-4
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def grad_input(la, seed):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return rng.standard_normal(la.v.shape, dtype=np.float32)
+
+
+def check(la, label, seed=1):
+    announce("linattn bwd %s T=%d H=%d" % (label, la.T, la.H))
+    g = grad_input(la, seed)
+    q, k, v, s = dev(la.q), dev(la.k), dev(la.v), dev(la.start)
+    out = mb.scan_linattn(q, k, v, s)
+    gq, gk, gv = mb.scan_linattn_bwd(q, k, v, s, out, dev(g))
+    torch.cuda.synchronize()
+    rq, rk, rv, mq, mk, mv = oracle.linattn_bwd(la.q.astype(np.float64), la.k.astype(np.float64),
+                                                la.v.astype(np.float64), la.start, g.astype(np.float64))
+    for name, got, ref, m in (("dq", gq, rq, mq), ("dk", gk, rk, mk), ("dv", gv, rv, mv)):
+        e = cond_err(got.cpu().numpy(), ref, m)
+        assert e <= TOL, (label, name, e)
+
+
+def test_workload3_full():
+    check(tapes.make_linattn(3), "workload3")
+
+
+@pytest.mark.parametrize("T", [1, 63, 64, 65, 1000, 4097])
+def test_ragged_lengths(T):
+    check(tapes.make_linattn(3, seed=300 + T, T=T, H=2), "ragged")
+
+
+def _with_flags(la, flags):
+    la.start = flags.astype(np.uint8)
+    return la
+
+
+@pytest.mark.parametrize("kind", ["short", "all_begins", "single_episode", "chunk_starts", "chunk_second_rows",
+                                  "flag_bytes"])
+def test_flag_patterns(kind):
+    rng = np.random.default_rng(17)
+    T = 3 * 1024 + 17
+    la = tapes.make_linattn(3, seed=77, T=T, H=2)
+    f = np.zeros(T, np.uint8)
+    if kind == "short":
+        f = tapes.flags_from_lengths(rng.integers(1, 40, size=T), T)
+    elif kind == "all_begins":
+        f[:] = 1
+    elif kind == "chunk_starts":
+        f[::64] = 1
+    elif kind == "chunk_second_rows":
+        f[1::64] = 1
+    elif kind == "flag_bytes":
+        f = (rng.random(T) < 0.01).astype(np.uint8) * rng.integers(1, 256, size=T).astype(np.uint8)
+    check(_with_flags(la, f), kind)
+
+
+def test_autograd_function():
+    la = tapes.make_linattn(3, seed=88, T=700, H=2)
+    announce("linattn autograd T=700")
+    q, k, v = (dev(a).requires_grad_(True) for a in (la.q, la.k, la.v))
+    g = grad_input(la, 5)
+    out = mb.linattn(q, k, v, dev(la.start))
+    (out * dev(g)).sum().backward()
+    rq, rk, rv, mq, mk, mv = oracle.linattn_bwd(la.q.astype(np.float64), la.k.astype(np.float64),
+                                                la.v.astype(np.float64), la.start, g.astype(np.float64))
+    assert cond_err(q.grad.cpu().numpy(), rq, mq) <= TOL
+    assert cond_err(k.grad.cpu().numpy(), rk, mk) <= TOL
+    assert cond_err(v.grad.cpu().numpy(), rv, mv) <= TOL
