@@ -57,6 +57,8 @@ def _load():
         lib.oracle_gae.argtypes = [P, P, P, P, P, D, D, I64, I64, P, P, P, P]
         lib.oracle_ffm.argtypes = [P, P, P, P, I64, I64, I64, I64, P, P]
         lib.oracle_linattn_bwd.argtypes = [P, P, P, P, P, I64, I64, I64, I64, P, P, P, P, P, P]
+        lib.oracle_ffm_bwd.argtypes = [P, P, P, P, P, I64, I64, I64, I64, P, P, P, P, P, P]
+        lib.oracle_ffm_bwd.restype = None
         lib.oracle_linattn_bwd.restype = None
         lib.oracle_tbb_begin_indices.argtypes = [P, I64, I64, P]
         lib.oracle_tbb_begin_indices.restype = I64
@@ -276,3 +278,24 @@ def linattn_bwd(q, k, v, start, g):
     _load().oracle_linattn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(s), _ptr(g), T, H, dk, dv,
                                *[_ptr(o) for o in outs])
     return tuple(outs)
+
+
+def ffm_bwd(alpha, omega, start, S, G):
+    """Gradient of the FFM aggregator: S (forward output) and G = dL/dS are
+    complex [B,T,m,c] (or [T,m,c]).  Returns (dx [B,T,m], dalpha [m],
+    domega [c], m_dx, m_dalpha, m_domega), all float64."""
+    S = np.asarray(S)
+    squeeze = S.ndim == 3
+    S = np.ascontiguousarray(S[None] if squeeze else S, dtype=np.complex128)
+    G = np.ascontiguousarray(np.asarray(G).reshape(S.shape), dtype=np.complex128)
+    B, T, m, c = S.shape
+    alpha = np.ascontiguousarray(alpha, dtype=np.float64)
+    omega = np.ascontiguousarray(omega, dtype=np.float64)
+    s = _flags(start, B, T)
+    dx, mdx = np.empty((B, T, m)), np.empty((B, T, m))
+    da, mda, dw, mdw = np.empty(m), np.empty(m), np.empty(c), np.empty(c)
+    _load().oracle_ffm_bwd(_ptr(alpha), _ptr(omega), _ptr(s), _ptr(S), _ptr(G), B, T, m, c,
+                           _ptr(dx), _ptr(da), _ptr(dw), _ptr(mdx), _ptr(mda), _ptr(mdw))
+    if squeeze:
+        dx, mdx = dx[0], mdx[0]
+    return dx, da, dw, mdx, mda, mdw

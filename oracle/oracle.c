@@ -438,3 +438,52 @@ int64_t oracle_tbb_sample(const uint8_t* D, int64_t n_D, int64_t row_bytes, cons
     }
     return len;
 }
+
+void oracle_ffm_bwd(const double* alpha, const double* omega, const uint8_t* start, const double* S,
+                    const double* G, int64_t B, int64_t T, int64_t m, int64_t c,
+                    double* dx, double* dalpha, double* domega,
+                    double* m_dx, double* m_dalpha, double* m_domega) {
+    memset(dx, 0, (size_t)(B * T * m) * sizeof(double));
+    if (m_dx) memset(m_dx, 0, (size_t)(B * T * m) * sizeof(double));
+    for (int64_t j = 0; j < m; ++j) {
+        if (dalpha) dalpha[j] = 0.0;
+        if (m_dalpha) m_dalpha[j] = 0.0;
+    }
+    for (int64_t k = 0; k < c; ++k) {
+        if (domega) domega[k] = 0.0;
+        if (m_domega) m_domega[k] = 0.0;
+    }
+    for (int64_t j = 0; j < m; ++j) {
+        const double mag = exp(-fabs(alpha[j]));
+        const double sgn = alpha[j] > 0.0 ? 1.0 : (alpha[j] < 0.0 ? -1.0 : 0.0);
+        for (int64_t k = 0; k < c; ++k) {
+            const double complex g = mag * cexp(I * omega[k]);
+            double complex da = 0.0;
+            double mda = 0.0;
+            for (int64_t b = 0; b < B; ++b) {
+                double complex lam = 0.0;
+                double ml = 0.0;
+                for (int64_t t = T - 1; t >= 0; --t) {
+                    const int64_t o = ((b * T + t) * m + j) * c + k;
+                    const double complex gt = G[2 * o] + I * G[2 * o + 1];
+                    const int cont = (t + 1 < T) && !is_begin(start, T, b, t + 1);
+                    lam = cont ? gt + conj(g) * lam : gt;
+                    ml = cont ? cabs(gt) + mag * ml : cabs(gt);
+                    dx[(b * T + t) * m + j] += creal(lam);
+                    if (m_dx) m_dx[(b * T + t) * m + j] += ml;
+                    if (!is_begin(start, T, b, t)) {
+                        const int64_t p = ((b * T + t - 1) * m + j) * c + k;
+                        const double complex sp = S[2 * p] + I * S[2 * p + 1];
+                        da += lam * conj(sp);
+                        mda += ml * cabs(sp);
+                    }
+                }
+            }
+            const double complex w = conj(g) * da;
+            if (dalpha) dalpha[j] += -sgn * creal(w);
+            if (domega) domega[k] += cimag(w);
+            if (m_dalpha) m_dalpha[j] += mag * mda;
+            if (m_domega) m_domega[k] += mag * mda;
+        }
+    }
+}

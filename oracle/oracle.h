@@ -149,6 +149,21 @@ int64_t oracle_tbb_sample(const uint8_t* D, int64_t n_D, int64_t row_bytes, cons
                           const int64_t* draws, int64_t n_draws, int64_t batch,
                           uint8_t* out, uint8_t* out_start, int64_t* out_src);
 
+/* Gradient of the FFM aggregator (App. G.4) with the conjugate convention
+ * of complex autograd.  G = dL/dS [B][T][m][c] (complex), S the forward
+ * output.  Per feature (j, k), with gamma as in oracle_ffm:
+ *   lam_t = G_t + [step t+1 exists and is not a begin step] conj(gamma) lam_{t+1}
+ *   dx[b][t][j] = sum_k Re(lam_t[j][k])                       (x is real)
+ *   da[j][k]    = sum over b, t not a begin step of lam_t conj(S_{t-1})
+ *   dalpha[j]   = -sign(alpha_j) sum_k Re(conj(gamma_jk) da_jk)
+ *   domega[k]   = sum_j Im(conj(gamma_jk) da_jk)
+ * dx: [B][T][m]; dalpha: [m]; domega: [c] (NULL skips the parameter grads).
+ * m_dx, m_dalpha, m_domega (optional): magnitude companions (|gamma|, |G|, |S|). */
+void oracle_ffm_bwd(const double* alpha, const double* omega, const uint8_t* start, const double* S,
+                    const double* G, int64_t B, int64_t T, int64_t m, int64_t c,
+                    double* dx, double* dalpha, double* domega,
+                    double* m_dx, double* m_dalpha, double* m_domega);
+
 /* Discounted return over a tape (App. D, discounted-return memoroid; the
  * done-flag convention of Section 2): for every step, the discounted sum of
  * the rewards from that step to the end of its episode,

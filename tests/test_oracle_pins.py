@@ -920,3 +920,43 @@ def test_linattn_grad_single_step_episodes():
     dq, dk_, dv_, _, _, _ = oracle.linattn_bwd(q, k, v, np.ones(T, np.uint8), g)
     np.testing.assert_allclose(dv_, g, rtol=1e-14, atol=1e-15)
     assert np.allclose(dq, 0.0, atol=1e-14) and np.allclose(dk_, 0.0, atol=1e-14)
+
+
+def test_ffm_grad_matches_autograd():
+    """The FFM gradient w.r.t. the real input and the real parameters alpha,
+    omega, against torch autograd (complex128) through the sequential
+    aggregator, for a loss mixing real and imaginary parts."""
+    import torch
+    rng = np.random.default_rng(97)
+    B, T, m, c = 2, 30, 3, 4
+    alpha = rng.uniform(-1, 1, m)
+    omega = rng.uniform(-3, 3, c)
+    flags = np.stack([tapes.flags_from_lengths(rng.integers(1, 12, size=8), T) for _ in range(B)])
+    x = rng.standard_normal((B, T, m))
+    W = rng.standard_normal((B, T, m, c)) + 1j * rng.standard_normal((B, T, m, c))
+    al = torch.tensor(alpha, requires_grad=True)
+    om = torch.tensor(omega, requires_grad=True)
+    xt = torch.tensor(x, requires_grad=True)
+    gam = torch.exp((-al.abs())[:, None] + 1j * om[None, :])
+    outs = []
+    for b in range(B):
+        s = torch.zeros(m, c, dtype=torch.complex128)
+        row = []
+        for t in range(T):
+            xb = xt[b, t][:, None].to(torch.complex128)
+            s = xb.expand(m, c) if (t == 0 or flags[b, t]) else s * gam + xb
+            row.append(s)
+        outs.append(torch.stack(row))
+    S = torch.stack(outs)
+    L = (S * torch.tensor(W)).real.sum() + 0.05 * (S.abs() ** 2).sum()
+    L.backward()
+    # the upstream gradient dL/dS in autograd's convention, from autograd itself
+    St = S.detach().clone().requires_grad_(True)
+    L2 = (St * torch.tensor(W)).real.sum() + 0.05 * (St.abs() ** 2).sum()
+    L2.backward()
+    G = St.grad.numpy()
+    dx, da, dw, mdx, mda, mdw = oracle.ffm_bwd(alpha, omega, flags, S.detach().numpy(), G)
+    np.testing.assert_allclose(dx, xt.grad.numpy(), rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(da, al.grad.numpy(), rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(dw, om.grad.numpy(), rtol=1e-11, atol=1e-12)
+    assert np.all(mdx >= np.abs(dx) - 1e-12) and np.all(mda >= np.abs(da) - 1e-12) and np.all(mdw >= np.abs(dw) - 1e-12)
