@@ -18,7 +18,8 @@ Workloads (seeded, synthetic; laws in paper_2402_09900_amd.tapes):
   5  diag real f32, T=1048576, d=256, lognormal(5, 1.5) episodes, forward + reverse
   6  discounted return + generalized advantage estimate, one tape of 2^24 steps,
      U{1..1000} episodes, gamma 0.99, lambda 0.95
-  7  FFM aggregator, T=262144, m=32 x c=8 complex state, Geometric(200) episodes
+  7  FFM aggregator, T=262144, m=32 x c=8 complex state, Geometric(200) episodes,
+     forward + gradient (x, alpha, omega)
   8  tape-based batching: begin indices of a 2^24-transition buffer (64-byte
      rows, U{1..1000} episodes) and a sampled batch of 2^20 rows
   9  workload 3 with the gradient of the readout (dq, dk, dv)
@@ -226,13 +227,20 @@ def setup_discount(torch, mb, tapes, key):
 
 
 def setup_ffm(torch, mb, tapes, key):
+    wl = tapes.WORKLOADS[key]
     f = tapes.make_ffm(key)
     B, T, m, c = f.B, f.T, f.m, f.c
     n = B * T * m * c
     nb = mb.memoroid_scan_ffm_workspace_bytes(B, T, m, c)
+    nbb = mb.memoroid_scan_ffm_bwd_workspace_bytes(B, T, m, c) if wl.backward else 0
+    g_host = None
+    if wl.backward:
+        rng = np.random.Generator(np.random.PCG64(key + 100))
+        g_host = (rng.standard_normal((B, T, m, c), dtype=np.float32)
+                  + 1j * rng.standard_normal((B, T, m, c), dtype=np.float32)).astype(np.complex64)
     stream = lambda: torch.cuda.current_stream().cuda_stream  # noqa: E731
     sets = []
-    for _ in range(n_sets(n * 8 + B * T * (m * 4 + 5) + nb)):
+    for _ in range(n_sets(n * (16 if wl.backward else 8) + B * T * (m * 8 + 5) + nb + nbb)):
         al, om, x, s = (dev_tensor(torch, a, k) for a, k in ((f.alpha, "f32"), (f.omega, "f32"), (f.x, "f32"),
                                                               (f.start, "u8")))
         S = torch.empty((B, T, m, c), dtype=torch.complex64, device="cuda")
@@ -243,9 +251,25 @@ def setup_ffm(torch, mb, tapes, key):
             st = mb.memoroid_scan_ffm(al.data_ptr(), om.data_ptr(), x.data_ptr(), s.data_ptr(), S.data_ptr(),
                                       idx.data_ptr(), B, T, m, c, ws.data_ptr(), ws.numel(), stream())
             assert st == 0, mb.status_string(st)
-        sets.append({"fwd": fwd})
-    # read x (real, m per step) and flags; write S (complex, m*c per step) and idx
-    bytes_per = {"fwd": B * T * (m * 4 + 1 + 4) + n * 8}
+        calls = {"fwd": fwd}
+        if wl.backward:
+            G = dev_tensor(torch, g_host, "c64")
+            gx = torch.empty((B, T, m), dtype=torch.float32, device="cuda")
+            ga = torch.empty(m, dtype=torch.float32, device="cuda")
+            gw = torch.empty(c, dtype=torch.float32, device="cuda")
+            wsb = torch.empty(nbb, dtype=torch.uint8, device="cuda")
+
+            def bwd(al=al, om=om, s=s, S=S, G=G, gx=gx, ga=ga, gw=gw, wsb=wsb):
+                st = mb.memoroid_scan_ffm_bwd(al.data_ptr(), om.data_ptr(), s.data_ptr(), S.data_ptr(), G.data_ptr(),
+                                              gx.data_ptr(), ga.data_ptr(), gw.data_ptr(), B, T, m, c,
+                                              wsb.data_ptr(), wsb.numel(), stream())
+                assert st == 0, mb.status_string(st)
+            calls["bwd"] = bwd
+        sets.append(calls)
+    # fwd: read x (real, m per step) and flags; write S (complex, m*c per
+    # step) and idx.  bwd: read dL/dS and S_{t-1}, flags; write dx (real, m per
+    # step); the parameter gradients are a reduction to m + c values
+    bytes_per = {"fwd": B * T * (m * 4 + 1 + 4) + n * 8, "bwd": n * 16 + B * T * (1 + m * 4)}
     return f, sets, bytes_per, n
 
 
@@ -330,11 +354,16 @@ def cpu_baseline(key, tapes, budget_s=20.0):
     if w.kind == "ffm":
         T = min(w.T, 1 << 16)
         f = tapes.make_ffm(key, T=T)
+        al, om = f.alpha.astype(np.float64), f.omega.astype(np.float64)
         t0 = time.perf_counter()
-        oracle.ffm(f.alpha.astype(np.float64), f.omega.astype(np.float64), f.x.astype(np.float64), f.start)
+        S, _ = oracle.ffm(al, om, f.x.astype(np.float64), f.start)
+        if w.backward:
+            oracle.ffm_bwd(al, om, f.start, S, np.ones_like(S))
         dt = time.perf_counter() - t0
+        what = "forward + gradient" if w.backward else "forward"
         return {"value": f.B * T * f.m * f.c / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
-                "sample": "first %d steps of the tape, all %d x %d features, fp64, %.1f s" % (T, f.m, f.c, dt)}
+                "sample": "first %d steps of the tape, all %d x %d features, %s, fp64, %.1f s"
+                          % (T, f.m, f.c, what, dt)}
     if w.kind == "discount":
         T = min(w.T, 1 << 22)
         tp = tapes.make_discount(key, T=T)
@@ -448,7 +477,8 @@ def main():
     roof["traffic_unit"] = "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
     roof["kernel"] = {"fwd": {"diag": "memoroid_scan_diag", "linattn": "memoroid_scan_linattn",
                               "ffm": "memoroid_scan_ffm"}.get(wl.kind),
-                      "bwd": "memoroid_scan_linattn_bwd" if wl.kind == "linattn" else "memoroid_scan_diag_bwd", "return": "memoroid_discounted_return",
+                      "bwd": {"linattn": "memoroid_scan_linattn_bwd", "ffm": "memoroid_scan_ffm_bwd"}.get(
+                          wl.kind, "memoroid_scan_diag_bwd"), "return": "memoroid_discounted_return",
                       "gae": "memoroid_gae", "insert": "memoroid_tbb_begin_indices",
                       "sample": "memoroid_tbb_sample"}[dom]
     roof["ms_per_launch"] = round(per_call_ms[dom], 4)

@@ -166,6 +166,33 @@ int memoroid_scan_ffm(const float* alpha, const float* omega, const float* x,
                       void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Gradient of the FFM aggregator (App. G.4), conjugate (PyTorch) convention
+ * for the complex upstream gradient.  Per feature (j, k):
+ *     lam_t = G_t + [step t+1 is not a begin step] conj(gamma_jk) lam_{t+1}
+ *     grad_x[b][t][j] = sum_k Re(lam_t[j][k])
+ *     da_jk = sum over tapes and non-begin steps of lam_t conj(S_{t-1})
+ *     grad_alpha[j] = -sign(alpha_j) sum_k Re(conj(gamma_jk) da_jk)
+ *     grad_omega[k] = sum_j Im(conj(gamma_jk) da_jk)
+ *
+ *   alpha, omega, start  as for memoroid_scan_ffm.
+ *   S          the forward output [B][T][m][c] complex64 (needed only for the
+ *              parameter gradients; may be NULL when both are NULL).
+ *   grad_S     dL/dS [B][T][m][c] complex64.
+ *   grad_x     out [B][T][m] fp32.
+ *   grad_alpha optional out [m] fp32;  grad_omega: optional out [c] fp32.
+ *   c must be a power of two no larger than 16 (MEMOROID_EUNSUPPORTED
+ *   otherwise): the input gradient is reduced over c inside the kernel.
+ *   Workspace: memoroid_scan_ffm_bwd_workspace_bytes(B, T, m, c).
+ * ------------------------------------------------------------------------ */
+size_t memoroid_scan_ffm_bwd_workspace_bytes(int64_t B, int64_t T, int64_t m, int64_t c);
+
+int memoroid_scan_ffm_bwd(const float* alpha, const float* omega, const uint8_t* start,
+                          const void* S, const void* grad_S, float* grad_x,
+                          float* grad_alpha, float* grad_omega,
+                          int64_t B, int64_t T, int64_t m, int64_t c,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Linear-transformer memoroid (App. G.1), forward readout, one tape of T
  * steps with H independent heads.  Per head, with S (dk x dv) and z (dk)
  * reset to zero at every begin step:

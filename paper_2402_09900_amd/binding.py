@@ -63,6 +63,10 @@ def lib() -> ctypes.CDLL:
         L.memoroid_scan_linattn_bwd_workspace_bytes.argtypes = [I64, I64, I64, I64, I64]
         L.memoroid_scan_linattn_bwd.restype = I32
         L.memoroid_scan_linattn_bwd.argtypes = [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, I64, P, SZ, P]
+        L.memoroid_scan_ffm_bwd_workspace_bytes.restype = SZ
+        L.memoroid_scan_ffm_bwd_workspace_bytes.argtypes = [I64, I64, I64, I64]
+        L.memoroid_scan_ffm_bwd.restype = I32
+        L.memoroid_scan_ffm_bwd.argtypes = [P, P, P, P, P, P, P, P, I64, I64, I64, I64, P, SZ, P]
         L.memoroid_scan_ffm_workspace_bytes.restype = SZ
         L.memoroid_scan_ffm_workspace_bytes.argtypes = [I64, I64, I64, I64]
         L.memoroid_scan_ffm.restype = I32
@@ -170,6 +174,16 @@ def memoroid_tbb_sample(D, n_D, row_bytes, I, n_I, draws, n_draws, batch, out, o
                         workspace, workspace_bytes, stream) -> int:
     return lib().memoroid_tbb_sample(D, n_D, row_bytes, I, n_I, draws, n_draws, batch, out, out_start, out_src,
                                      filled, workspace, workspace_bytes, stream)
+
+
+def memoroid_scan_ffm_bwd_workspace_bytes(B, T, m, c) -> int:
+    return lib().memoroid_scan_ffm_bwd_workspace_bytes(B, T, m, c)
+
+
+def memoroid_scan_ffm_bwd(alpha, omega, start, S, grad_S, grad_x, grad_alpha, grad_omega, B, T, m, c, workspace,
+                          workspace_bytes, stream) -> int:
+    return lib().memoroid_scan_ffm_bwd(alpha, omega, start, S, grad_S, grad_x, grad_alpha, grad_omega, B, T, m, c,
+                                       workspace, workspace_bytes, stream)
 
 
 def memoroid_discount_workspace_bytes(B, T) -> int:
@@ -411,6 +425,32 @@ def tbb_sample(D, I, draws, batch: int, workspace=None):
                                    filled.data_ptr(), ws.data_ptr(), ws.numel(), _stream_ptr(dev))
     _raise(st, "memoroid_tbb_sample")
     return out, out_start, out_src, filled
+
+
+def scan_ffm_bwd(alpha, omega, start, S, grad_S, params: bool = True, workspace=None):
+    """Gradient of the FFM aggregator: returns (grad_x [B,T,m], grad_alpha [m],
+    grad_omega [c]); the parameter gradients are None when params is false."""
+    torch = _torch()
+    squeeze = grad_S.dim() == 3
+    if squeeze:
+        grad_S = grad_S.unsqueeze(0)
+        S = S.unsqueeze(0) if S is not None else None
+    B, T, m, c = grad_S.shape
+    start = start.reshape(B, T)
+    dev = _check_cuda(alpha, omega, start, S, grad_S)
+    if grad_S.dtype != torch.complex64 or (S is not None and S.dtype != torch.complex64):
+        raise TypeError("S and grad_S must be complex64")
+    gx = torch.empty((B, T, m), dtype=torch.float32, device=dev)
+    ga = torch.empty(m, dtype=torch.float32, device=dev) if params else None
+    gw = torch.empty(c, dtype=torch.float32, device=dev) if params else None
+    ws = _workspace(lib().memoroid_scan_ffm_bwd_workspace_bytes(B, T, m, c), dev, workspace)
+    st = lib().memoroid_scan_ffm_bwd(alpha.data_ptr(), omega.data_ptr(), start.data_ptr(),
+                                     S.data_ptr() if S is not None else None, grad_S.data_ptr(), gx.data_ptr(),
+                                     ga.data_ptr() if ga is not None else None,
+                                     gw.data_ptr() if gw is not None else None, B, T, m, c, ws.data_ptr(),
+                                     ws.numel(), _stream_ptr(dev))
+    _raise(st, "memoroid_scan_ffm_bwd")
+    return (gx[0] if squeeze else gx), ga, gw
 
 
 def _tape_shapes(r, *others):

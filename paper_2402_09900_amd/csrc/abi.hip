@@ -276,6 +276,105 @@ int memoroid_scan_ffm(const float* alpha, const float* omega, const float* x, co
     return check_hip(ffm_fwd_launch(vec, args, p.ntiles, s));
 }
 
+// ------------------------------------------------------------ FFM gradient
+
+namespace {
+
+bool ffm_bwd_plan(int64_t B, int64_t T, int64_t m, int64_t c, bool vec, bool params, DiagPlan* p,
+                  size_t* off_da, size_t* total) {
+    int64_t d;
+    if (!mul_ok(m, c, &d)) return false;
+    if (!plan_diag(B, T, d, MEMOROID_C64, vec, diag_rows(true, true), true, true, params, p)) return false;
+    *off_da = align_up(p->total);
+    *total = align_up(*off_da + (size_t)(params ? d : 1) * 8);
+    return true;
+}
+
+bool pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
+
+}  // namespace
+
+size_t memoroid_scan_ffm_bwd_workspace_bytes(int64_t B, int64_t T, int64_t m, int64_t c) {
+    if (B <= 0 || T <= 0 || m <= 0 || c <= 0) return 0;
+    size_t best = 0;
+    for (int vec = 0; vec < 2; ++vec) {
+        DiagPlan p;
+        size_t off_da, total;
+        if (!ffm_bwd_plan(B, T, m, c, vec, true, &p, &off_da, &total)) return 0;
+        if (total > best) best = total;
+    }
+    return best;
+}
+
+int memoroid_scan_ffm_bwd(const float* alpha, const float* omega, const uint8_t* start, const void* S,
+                          const void* grad_S, float* grad_x, float* grad_alpha, float* grad_omega, int64_t B,
+                          int64_t T, int64_t m, int64_t c, void* workspace, size_t workspace_bytes, void* stream) {
+    if (B < 0 || T < 0 || m < 0 || c < 0) return MEMOROID_EINVAL;
+    if (B == 0 || T == 0 || m == 0 || c == 0) return MEMOROID_OK;
+    int64_t d, BT, BTd;
+    if (!mul_ok(m, c, &d) || !mul_ok(B, T, &BT) || !mul_ok(BT, d, &BTd) || BTd > INT64_MAX / 16)
+        return MEMOROID_EINVAL;
+    const bool params = grad_alpha || grad_omega;
+    if (!alpha || !omega || !start || !grad_S || !grad_x || (params && !S)) return MEMOROID_EINVAL;
+    if (!aligned(alpha, 4) || !aligned(omega, 4) || !aligned(grad_S, 8) || !aligned(grad_x, 4) ||
+        (S && !aligned(S, 8)) || (grad_alpha && !aligned(grad_alpha, 4)) || (grad_omega && !aligned(grad_omega, 4)))
+        return MEMOROID_EINVAL;
+    const void* ins[5] = {alpha, omega, start, S, grad_S};
+    const void* outs[3] = {grad_x, grad_alpha, grad_omega};
+    for (int o = 0; o < 3; ++o) {
+        if (!outs[o]) continue;
+        for (int i = 0; i < 5; ++i)
+            if (ins[i] && outs[o] == ins[i]) return MEMOROID_EINVAL;
+        for (int o2 = 0; o2 < o; ++o2)
+            if (outs[o2] && outs[o] == outs[o2]) return MEMOROID_EINVAL;
+    }
+    const bool vec = d % 2 == 0 && aligned(grad_S, 16) && (!S || aligned(S, 16));
+    DiagPlan p;
+    size_t off_da, total;
+    if (!ffm_bwd_plan(B, T, m, c, vec, params, &p, &off_da, &total)) return MEMOROID_EUNSUPPORTED;
+    // the real input's gradient is reduced over the c columns inside the
+    // kernel: c must be a power of two that divides the chain width
+    if (!pow2(c) || c > p.Dp) return MEMOROID_EUNSUPPORTED;
+    if (!workspace || workspace_bytes < total) return MEMOROID_EWORKSPACE;
+    if (!aligned(workspace, 16)) return MEMOROID_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    if (ws_init_launch(ws, p.off_agg, ws + p.off_agg, p.fill_bytes, s) != hipSuccess) return MEMOROID_EHIP;
+    DiagBwdArgs args{};
+    args.a = nullptr;
+    args.start = start;
+    args.h = S;
+    args.g = grad_S;
+    args.dx = nullptr;
+    args.da = nullptr;
+    args.da_part = params ? ws + p.off_part : nullptr;
+    args.T = T;
+    args.d = d;
+    args.nt = p.nt;
+    args.Qp = p.Qp;
+    args.nfb = p.nfb;
+    args.nchains = (int32_t)p.nchains;
+    args.agg = ws + p.off_agg;
+    args.incl = ws + p.off_incl;
+    args.hdr = (WsHeader*)ws;
+    args.ctr = (uint32_t*)(ws + p.off_ctr);
+    args.alpha = alpha;
+    args.omega = omega;
+    args.ffm_m = m;
+    args.ffm_c = c;
+    args.dxr = grad_x;
+    if (ffm_bwd_launch(vec, args, p.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
+    if (params) {
+        float* da = (float*)(ws + off_da);
+        const int st = reduce_rows((const float*)(ws + p.off_part), (float*)(ws + p.off_sum1),
+                                   (float*)(ws + p.off_sum2), da, p.nt * B, 2 * d, s);
+        if (st != MEMOROID_OK) return st;
+        if (ffm_param_grad_launch(alpha, omega, da, m, c, grad_alpha, grad_omega, s) != hipSuccess)
+            return MEMOROID_EHIP;
+    }
+    return MEMOROID_OK;
+}
+
 // ------------------------------------------------------------ diag backward
 
 size_t memoroid_scan_diag_bwd_workspace_bytes(int64_t B, int64_t T, int64_t d, int dtype, int64_t a_stride_t) {

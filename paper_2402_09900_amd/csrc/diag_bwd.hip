@@ -15,13 +15,16 @@
 // writes one partial per feature, summed inside the tile in a fixed order, and
 // colsum kernels (below) add the partials up in a fixed order too, so the
 // result does not depend on timing.
+#include <type_traits>
+
 #include "scan_common.hpp"
 #include "kernels.hpp"
 
 namespace memoroid {
 
-template <Kind K, int VEC, int R, bool AINV>
+template <Kind K, int VEC, int R, bool AINV, bool FFM = false>
 __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
+    static_assert(!FFM || (K == K_C64 && AINV), "FFM: complex state, generated a");
     using S = typename StateOf<K>::type;
     using C = Codec<K, VEC>;
     using SegT = Seg<S, VEC>;
@@ -117,7 +120,19 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
         ends |= (in & ((t + 1 == T ? 1u : 0u) | (fl[r + 1] != 0u ? 1u : 0u))) << r;
     }
     S ainv[VEC];
-    if constexpr (AINV) {
+    if constexpr (FFM) {
+        // conj(a), a = exp(-|alpha_j|) (cos omega_k + i sin omega_k), f = j * c + k,
+        // evaluated as in the forward pass
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+            const int64_t f = f0 + v < p.d ? f0 + v : 0;
+            const int64_t jj = f / p.ffm_c, kk = f - jj * p.ffm_c;
+            const double mag = exp(-fabs((double)p.alpha[jj]));
+            double sn, cs;
+            sincos((double)p.omega[kk], &sn, &cs);
+            if constexpr (std::is_same<S, cf>::value) ainv[v] = cf{(float)(mag * cs), -(float)(mag * sn)};
+        }
+    } else if constexpr (AINV) {
         // a NULL time-invariant a stands for a = 1 (the reverse sum, used by
         // the linear-attention gradient's state scan)
         RawVec<K, VEC> r0;
@@ -236,13 +251,38 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
                 C::put(rg[r], v, lam[v]);
             }
         }
-        const Rsrc rs_dx = make_rsrc((char*)p.dx + tape_row0 * rowB, rows_left * rowB);
-        const Rsrc rs_da = make_rsrc(AINV ? p.dx : (char*)p.da + tape_row0 * rowB, AINV ? 0 : rows_left * rowB);
+        if constexpr (FFM) {
+            // x is real and broadcast over the c columns of its row j: its
+            // gradient is the sum of Re(lam) over those columns.  c is a power
+            // of two: with c >= VEC a lane's features share one j and groups
+            // of c / VEC lanes are combined by shuffles; with c < VEC each
+            // feature is its own j.
+            const int64_t cc = p.ffm_c;
 #pragma unroll
-        for (int r = R - 1; r >= 0; --r) {
-            raw_bstore_nt(rs_dx, off0 + r * step, rg[r]);
-            if constexpr (!AINV) {
-                if (want_da) raw_bstore_nt(rs_da, off0 + r * step, ra[r]);
+            for (int r = R - 1; r >= 0; --r) {
+                const int64_t t = row0 + r;
+                const bool in = t < T;
+                if (cc >= VEC) {
+                    float part = 0.0f;
+#pragma unroll
+                    for (int v = 0; v < VEC; ++v) part += C::get(rg[r], v).re;
+                    for (int off = 1; off < (int)(cc / VEC); off <<= 1) part += __shfl_xor(part, off, 64);
+                    if (in && (q % (int)(cc / VEC)) == 0) p.dxr[(rowbase + t) * p.ffm_m + f0 / cc] = part;
+                } else {
+#pragma unroll
+                    for (int v = 0; v < VEC; ++v)
+                        if (in && f0 + v < p.d) p.dxr[(rowbase + t) * p.ffm_m + (f0 + v) / cc] = C::get(rg[r], v).re;
+                }
+            }
+        } else {
+            const Rsrc rs_dx = make_rsrc((char*)p.dx + tape_row0 * rowB, rows_left * rowB);
+            const Rsrc rs_da = make_rsrc(AINV ? p.dx : (char*)p.da + tape_row0 * rowB, AINV ? 0 : rows_left * rowB);
+#pragma unroll
+            for (int r = R - 1; r >= 0; --r) {
+                raw_bstore_nt(rs_dx, off0 + r * step, rg[r]);
+                if constexpr (!AINV) {
+                    if (want_da) raw_bstore_nt(rs_da, off0 + r * step, ra[r]);
+                }
             }
         }
     }
@@ -308,6 +348,51 @@ static hipError_t launch_bwd(const DiagBwdArgs& args, int64_t ntiles, bool ainv,
         hipLaunchKernelGGL((diag_bwd_kernel<K, VEC, R, true>), dim3((unsigned)ntiles), dim3(256), 0, s, args);
     else
         hipLaunchKernelGGL((diag_bwd_kernel<K, VEC, R, false>), dim3((unsigned)ntiles), dim3(256), 0, s, args);
+    return hipGetLastError();
+}
+
+hipError_t ffm_bwd_launch(bool vec, const DiagBwdArgs& args, int64_t ntiles, hipStream_t s) {
+    constexpr int RI = diag_rows(true, true);
+    if (vec)
+        hipLaunchKernelGGL((diag_bwd_kernel<K_C64, KindInfo<K_C64>::vec, RI, true, true>), dim3((unsigned)ntiles),
+                           dim3(256), 0, s, args);
+    else
+        hipLaunchKernelGGL((diag_bwd_kernel<K_C64, 1, RI, true, true>), dim3((unsigned)ntiles), dim3(256), 0, s, args);
+    return hipGetLastError();
+}
+
+// One workgroup: thread j < m forms dalpha[j], thread k < c forms domega[k]
+// (loops over the other index), from the summed complex da[m][c].
+__global__ __launch_bounds__(256) void ffm_param_grad_kernel(const float* alpha, const float* omega, const float* da,
+                                                             int64_t m, int64_t c, float* dalpha, float* domega) {
+    for (int64_t j = threadIdx.x; dalpha && j < m; j += 256) {
+        const double mag = exp(-fabs((double)alpha[j]));
+        const double sgn = alpha[j] > 0.0f ? 1.0 : (alpha[j] < 0.0f ? -1.0 : 0.0);
+        double acc = 0.0;
+        for (int64_t k = 0; k < c; ++k) {
+            double sn, cs;
+            sincos((double)omega[k], &sn, &cs);
+            const double dr = da[2 * (j * c + k)], di = da[2 * (j * c + k) + 1];
+            acc += mag * (cs * dr + sn * di);                 // Re(conj(a) da)
+        }
+        dalpha[j] = (float)(-sgn * acc);
+    }
+    for (int64_t k = threadIdx.x; domega && k < c; k += 256) {
+        double sn, cs;
+        sincos((double)omega[k], &sn, &cs);
+        double acc = 0.0;
+        for (int64_t j = 0; j < m; ++j) {
+            const double mag = exp(-fabs((double)alpha[j]));
+            const double dr = da[2 * (j * c + k)], di = da[2 * (j * c + k) + 1];
+            acc += mag * (cs * di - sn * dr);                 // Im(conj(a) da)
+        }
+        domega[k] = (float)acc;
+    }
+}
+
+hipError_t ffm_param_grad_launch(const float* alpha, const float* omega, const float* da, int64_t m, int64_t c,
+                                 float* dalpha, float* domega, hipStream_t s) {
+    hipLaunchKernelGGL(ffm_param_grad_kernel, dim3(1), dim3(256), 0, s, alpha, omega, da, m, c, dalpha, domega);
     return hipGetLastError();
 }
 

@@ -78,11 +78,22 @@ struct DiagBwdArgs {
     void* incl;
     WsHeader* hdr;
     uint32_t* ctr;     // per-chain tile counters, kCtrStride words apart
+    // FFM aggregator gradient: a generated from alpha, omega (as in the
+    // forward pass); dx is reduced over the c columns of each row j into the
+    // real dxr[B][T][m] instead of being stored per feature
+    const float* alpha;
+    const float* omega;
+    int64_t ffm_m, ffm_c;
+    float* dxr;
 };
 
 hipError_t diag_fwd_launch(int in_kind, int out_kind, bool vec, bool ainv,
                            const DiagFwdArgs& args, int64_t ntiles, hipStream_t s);
 hipError_t ffm_fwd_launch(bool vec, const DiagFwdArgs& args, int64_t ntiles, hipStream_t s);
+hipError_t ffm_bwd_launch(bool vec, const DiagBwdArgs& args, int64_t ntiles, hipStream_t s);
+// dalpha[j] = -sign(alpha_j) sum_k Re(conj(a_jk) da_jk), domega[k] = sum_j Im(conj(a_jk) da_jk)
+hipError_t ffm_param_grad_launch(const float* alpha, const float* omega, const float* da, int64_t m, int64_t c,
+                                 float* dalpha, float* domega, hipStream_t s);
 hipError_t diag_bwd_launch(int kind, bool vec, bool ainv, const DiagBwdArgs& args,
                            int64_t ntiles, hipStream_t s);
 // out[r / (4 rpw)][c] = sum over rows r .. r + 4 rpw - 1 of in[r][c], in a

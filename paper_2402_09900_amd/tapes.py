@@ -180,8 +180,8 @@ WORKLOADS: Dict[int, Workload] = {
                 False, (0.5, 0.99), _lognormal(5.0, 1.5), True),
     6: Workload(6, "return_gae_f32_T16777216_unif1_1000_g0.99_l0.95", "discount", 1, 1 << 24, 1, "f32", "f32",
                 False, (0.0, 0.0), _uniform_int(1, 1000), False, gamma=0.99, lam=0.95),
-    7: Workload(7, "ffm_c64_T262144_m32_c8_geom200_fwd", "ffm", 1, 1 << 18, 32, "c64", "c64",
-                True, (0.5, 0.995), _geometric(200.0), False, dk=32, dv=8),
+    7: Workload(7, "ffm_c64_T262144_m32_c8_geom200_fwd_bwd", "ffm", 1, 1 << 18, 32, "c64", "c64",
+                True, (0.5, 0.995), _geometric(200.0), True, dk=32, dv=8),
     8: Workload(8, "tbb_D16777216_row64B_batch1048576_unif1_1000", "tbb", 1, 1 << 24, 16, "f32", "f32",
                 False, (0.0, 0.0), _uniform_int(1, 1000), False, chunk=1 << 20),
     9: Workload(9, "linattn_f32_T32768_H4_dk64_dv64_geom500_chunk64_fwd_bwd", "linattn", 1, 32768, 4, "f32", "f32",

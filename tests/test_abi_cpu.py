@@ -189,6 +189,22 @@ def test_tbb_validation():
     assert sm(batch=1 << 62) == mb.EINVAL               # batch * row_bytes overflows
 
 
+def test_ffm_bwd_validation():
+    def fb(**kw):
+        args = dict(alpha=A, omega=X, start=S, S=H, grad_S=I, grad_x=0x90000, grad_alpha=0xA0000,
+                    grad_omega=0xB0000, B=1, T=100, m=4, c=4, workspace=W, workspace_bytes=1 << 30, stream=None)
+        args.update(kw)
+        return mb.memoroid_scan_ffm_bwd(*args.values())
+    assert mb.memoroid_scan_ffm_bwd_workspace_bytes(1, 1 << 18, 32, 8) > 0
+    assert fb(T=0) == mb.OK and fb(B=-1) == mb.EINVAL
+    assert fb(c=3) == mb.EUNSUPPORTED and fb(c=32) == mb.EUNSUPPORTED
+    assert fb(S=None) == mb.EINVAL                           # parameter grads need S
+    assert fb(grad_x=None) == mb.EINVAL and fb(grad_S=None) == mb.EINVAL
+    assert fb(grad_x=I) == mb.EINVAL and fb(grad_alpha=0x90000) == mb.EINVAL   # aliasing
+    assert fb(grad_S=I + 4) == mb.EINVAL
+    assert fb(workspace=None) == mb.EWORKSPACE and fb(workspace_bytes=64) == mb.EWORKSPACE
+
+
 def test_discount_validation():
     def ret(**kw):
         args = dict(r=A, start=S, gamma=0.99, G=H, B=2, T=100, workspace=W, workspace_bytes=1 << 30, stream=None)

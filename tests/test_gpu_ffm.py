@@ -80,3 +80,50 @@ def test_nan_stays_in_its_episode():
     assert np.array_equal(np.isnan(S), bad)
     assert bad[0, 1200:1700, 1].all() and not bad[0, 1700:].any()
     assert cond_err(S[~bad], ref[~bad], m[~bad]) <= TOL
+
+
+# ----------------------------------------------------------------- gradient
+
+GTOL = 1e-4
+
+
+def check_grad(f, label, seed=3):
+    announce("ffm bwd %s B=%d T=%d m=%d c=%d" % (label, f.B, f.T, f.m, f.c))
+    rng = np.random.Generator(np.random.PCG64(seed))
+    G = (rng.standard_normal((f.B, f.T, f.m, f.c), dtype=np.float32)
+         + 1j * rng.standard_normal((f.B, f.T, f.m, f.c), dtype=np.float32)).astype(np.complex64)
+    al, om, x, s = dev(f.alpha), dev(f.omega), dev(f.x), dev(f.start)
+    S = mb.scan_ffm(al, om, x, s)
+    gx, ga, gw = mb.scan_ffm_bwd(al, om, s, S, dev(G))
+    torch.cuda.synchronize()
+    rdx, rda, rdw, mdx, mda, mdw = oracle.ffm_bwd(f.alpha.astype(np.float64), f.omega.astype(np.float64), f.start,
+                                                  S.cpu().numpy().astype(np.complex128), G.astype(np.complex128))
+    assert cond_err(gx.cpu().numpy(), rdx, mdx) <= GTOL, label
+    assert cond_err(ga.cpu().numpy(), rda, mda) <= GTOL, label
+    assert cond_err(gw.cpu().numpy(), rdw, mdw) <= GTOL, label
+
+
+def test_grad_workload7_full():
+    check_grad(tapes.make_ffm(7), "workload7")
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 1, 1), (2, 513, 3, 4), (1, 1000, 32, 8), (3, 2049, 7, 2), (2, 4096, 1, 16),
+                                   (1, 777, 16, 1), (4, 3000, 5, 4)], ids=lambda s: "B%dT%dm%dc%d" % s)
+def test_grad_shapes(shape):
+    B, T, m, c = shape
+    check_grad(tapes.make_ffm(7, seed=400 + T + m * c, B=B, T=T, m=m, c=c, episodes=tapes._geometric(150.0)),
+               "shape")
+
+
+def test_grad_without_parameter_gradients():
+    f = tapes.make_ffm(7, seed=401, B=2, T=2000, m=8, c=4)
+    announce("ffm bwd x only")
+    rng = np.random.Generator(np.random.PCG64(9))
+    G = (rng.standard_normal((2, 2000, 8, 4), dtype=np.float32)
+         + 1j * rng.standard_normal((2, 2000, 8, 4), dtype=np.float32)).astype(np.complex64)
+    gx, ga, gw = mb.scan_ffm_bwd(dev(f.alpha), dev(f.omega), dev(f.start), None, dev(G), params=False)
+    assert ga is None and gw is None
+    S = np.zeros((2, 2000, 8, 4), np.complex128)          # unused by the input gradient
+    rdx, _, _, mdx, _, _ = oracle.ffm_bwd(f.alpha.astype(np.float64), f.omega.astype(np.float64), f.start, S,
+                                          G.astype(np.complex128))
+    assert cond_err(gx.cpu().numpy(), rdx, mdx) <= GTOL
