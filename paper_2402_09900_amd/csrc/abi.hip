@@ -43,6 +43,7 @@ struct DiagPlan {
     int64_t ntiles = 0;
     size_t off_ctr = 0, off_agg = 0, off_incl = 0, off_cnt = 0, off_part = 0, off_sum1 = 0, off_sum2 = 0;
     size_t fill_bytes = 0;   // bytes from off_agg that must start as 0xFF
+    bool fused_da = false;   // one tape: da summed inside the reverse kernel
     size_t total = 0;
 };
 
@@ -84,7 +85,14 @@ bool plan_diag(int64_t B, int64_t T, int64_t d, int state_dtype, bool vec, int r
     p->off_cnt = off;                                      // begin-count words, [tiles per chain][B]
     if (!bwd) off = align_up(off + (size_t)p->nt * (size_t)B * 8);
     p->fill_bytes = off - p->off_agg;
-    if (bwd && ainv && want_grad_a) {
+    if (bwd && ainv && want_grad_a && B == 1) {
+        // one tape: the partial rows are self-validating 64-bit words, filled
+        // with the descriptors, and the chain's last tile sums them
+        p->fused_da = true;
+        p->off_part = off;
+        off = align_up(off + (size_t)p->nt * (size_t)d * 8);
+        p->fill_bytes = off - p->off_agg;
+    } else if (bwd && ainv && want_grad_a) {
         const size_t sb = cplx ? 8 : 4;
         const int64_t rows_part = p->nt * B;
         p->off_part = off;
@@ -348,6 +356,7 @@ int memoroid_scan_ffm_bwd(const float* alpha, const float* omega, const uint8_t*
     args.dx = nullptr;
     args.da = nullptr;
     args.da_part = params ? ws + p.off_part : nullptr;
+    args.da_out = (params && p.fused_da) ? ws + off_da : nullptr;
     args.T = T;
     args.d = d;
     args.nt = p.nt;
@@ -366,9 +375,11 @@ int memoroid_scan_ffm_bwd(const float* alpha, const float* omega, const uint8_t*
     if (ffm_bwd_launch(vec, args, p.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
     if (params) {
         float* da = (float*)(ws + off_da);
-        const int st = reduce_rows((const float*)(ws + p.off_part), (float*)(ws + p.off_sum1),
-                                   (float*)(ws + p.off_sum2), da, p.nt * B, 2 * d, s);
-        if (st != MEMOROID_OK) return st;
+        if (!p.fused_da) {
+            const int st = reduce_rows((const float*)(ws + p.off_part), (float*)(ws + p.off_sum1),
+                                       (float*)(ws + p.off_sum2), da, p.nt * B, 2 * d, s);
+            if (st != MEMOROID_OK) return st;
+        }
         if (ffm_param_grad_launch(alpha, omega, da, m, c, grad_alpha, grad_omega, s) != hipSuccess)
             return MEMOROID_EHIP;
     }
@@ -429,6 +440,7 @@ int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t, const uint8_t* sta
     args.dx = grad_x;
     args.da = ainv ? nullptr : grad_a;
     args.da_part = (ainv && grad_a) ? ws + p.off_part : nullptr;
+    args.da_out = (ainv && grad_a && p.fused_da) ? grad_a : nullptr;
     args.T = T;
     args.d = d;
     args.nt = p.nt;
@@ -442,7 +454,7 @@ int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t, const uint8_t* sta
     const int k = dtype == MEMOROID_F32 ? K_F32 : K_C64;
     const int64_t cols = d * (dtype == MEMOROID_C64 ? 2 : 1);
     if (diag_bwd_launch(k, vec, ainv, args, p.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
-    if (ainv && grad_a) {
+    if (ainv && grad_a && !p.fused_da) {
         const int st = reduce_rows((const float*)(ws + p.off_part), (float*)(ws + p.off_sum1),
                                    (float*)(ws + p.off_sum2), (float*)grad_a, p.nt * B, cols, s);
         if (st != MEMOROID_OK) return st;

@@ -296,16 +296,72 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
             __syncthreads();
             if (wave == 0 && j == 0 && active) {
                 RawVec<K, VEC> o;
+                S sv[VEC];
 #pragma unroll
                 for (int v = 0; v < VEC; ++v) {
                     S s = s_zero<S>();
                     for (int w = 0; w < NW; ++w)
                         for (int jj = 0; jj < Gw; ++jj) s = s + sWH[w][(jj * Qp + q) * VEC + v];
+                    sv[v] = s;
                     C::put(o, v, s);
                 }
                 // partial row = (tile, tape); columns = the d features
                 const int64_t prow = tile * (p.nchains / p.nfb) + b;
-                raw_store_nt((char*)p.da_part + (prow * p.d + f0) * EB, o);
+                if (p.da_out) {
+#pragma unroll
+                    for (int v = 0; v < VEC; ++v) publish64((uint64_t*)p.da_part + prow * p.d + f0 + v, pack_state(sv[v]));
+                } else {
+                    raw_store_nt((char*)p.da_part + (prow * p.d + f0) * EB, o);
+                }
+            }
+            if (p.da_out && k == p.nt - 1) {
+                // the chain's last tile (its ticket was handed out last, so
+                // every other tile of the chain is running or done) sums the
+                // chain's partial rows.  Thread (group g, slot fs) takes the
+                // feature fb * Dp + fs of tiles g, g + G, ... (G = 256 / Dp),
+                // eight loads in flight at a time; the groups are then added
+                // in order through LDS, so the result does not depend on timing.
+                const int fs = tid % Dp, G = NT / Dp, grp = tid / Dp;
+                const int64_t f = (int64_t)fb * Dp + fs;
+                const bool fin = f < p.d;
+                S acc = s_zero<S>();
+                uint32_t polls = 0;
+                for (int64_t base = grp; base < p.nt; base += 8 * (int64_t)G) {
+                    uint64_t wd[8];
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        const int64_t tl = base + (int64_t)i * G;
+                        wd[i] = (fin && tl < p.nt) ? peek64((const uint64_t*)p.da_part + tl * p.d + f) : 0ull;
+                    }
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        const int64_t tl = base + (int64_t)i * G;
+                        while (wd[i] == kEmpty64) {
+                            if (++polls > kMaxPolls) {
+                                __hip_atomic_store(&p.hdr->timeout, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                                wd[i] = 0ull;
+                            } else {
+                                __builtin_amdgcn_s_sleep(1);
+                                wd[i] = peek64((const uint64_t*)p.da_part + tl * p.d + f);
+                            }
+                        }
+                        acc = acc + unpack_state<S>(wd[i]);
+                    }
+                }
+                __syncthreads();                     // sWH is free again
+                S* red = &sWH[0][0];
+                red[tid] = acc;
+                __syncthreads();
+                if (grp == 0 && fin) {
+                    S tot2 = s_zero<S>();
+                    for (int g2 = 0; g2 < G; ++g2) tot2 = tot2 + red[g2 * Dp + fs];
+                    if constexpr (std::is_same<S, cf>::value) {
+                        ((float*)p.da_out)[2 * f] = tot2.re;
+                        ((float*)p.da_out)[2 * f + 1] = tot2.im;
+                    } else {
+                        ((float*)p.da_out)[f] = tot2;
+                    }
+                }
             }
         }
     }

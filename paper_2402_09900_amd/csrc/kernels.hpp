@@ -67,6 +67,8 @@ struct DiagBwdArgs {
     void* dx;
     void* da;          // per-step da, or NULL
     void* da_part;     // time-invariant a: [tiles per chain * B][d] partial sums
+    void* da_out;      // time-invariant a with one tape: da [d], summed in the kernel from
+                       // partial words [tiles per chain][d] (64-bit, self-validating) in da_part
     int64_t T;
     int64_t d;
     int64_t nt;        // tiles per chain

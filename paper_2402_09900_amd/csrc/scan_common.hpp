@@ -288,6 +288,16 @@ __device__ __forceinline__ uint32_t peek32(const uint32_t* p) {
     return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// A state value as one self-validating 64-bit word (real: (v, 0); complex:
+// (re, im)), and back.
+__device__ __forceinline__ uint64_t pack_state(float v) { return pack2(v, 0.0f); }
+__device__ __forceinline__ uint64_t pack_state(cf v) { return pack2(v.re, v.im); }
+template <class S> __device__ __forceinline__ S unpack_state(uint64_t w);
+template <> __device__ __forceinline__ float unpack_state<float>(uint64_t w) { return unpack_lo(w); }
+template <> __device__ __forceinline__ cf unpack_state<cf>(uint64_t w) { return cf{unpack_lo(w), unpack_hi(w)}; }
+__device__ __forceinline__ float shfl_xor_state(float v, int m) { return __shfl_xor(v, m, 64); }
+__device__ __forceinline__ cf shfl_xor_state(cf v, int m) { return cf{__shfl_xor(v.re, m, 64), __shfl_xor(v.im, m, 64)}; }
+
 // Per-feature tile summary of the scan state, in the two forms a successor
 // can use.  AGG: (A, H) of a tile without a begin step, i.e. h_end =
 // A * h_before + H.  INCL: h_end itself (the tile's inclusive prefix).

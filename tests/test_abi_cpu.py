@@ -52,7 +52,8 @@ def test_workspace_queries():
     assert f(-1, 100, 8, mb.F32, mb.F32) == 0
     assert f(0, 100, 8, mb.F32, mb.F32) == 0            # empty problem needs nothing
     g = mb.memoroid_scan_diag_bwd_workspace_bytes
-    assert g(1, 65536, 256, mb.C64, 0) > g(1, 65536, 256, mb.C64, 256) > 0   # da partials
+    assert g(1, 65536, 256, mb.C64, 0) > 0 and g(1, 65536, 256, mb.C64, 256) > 0
+    assert g(4, 65536, 256, mb.C64, 0) > 4 * g(1, 65536, 256, mb.C64, 0) // 2   # da partial rows per tape
     assert g(1, 100, 8, mb.BF16, 8) == 0
     h = mb.memoroid_scan_linattn_workspace_bytes
     assert h(32768, 4, 64, 64, 64) > 0
