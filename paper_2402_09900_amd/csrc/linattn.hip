@@ -90,7 +90,7 @@ __global__ __launch_bounds__(256) void linattn_summary_kernel(LinSummaryArgs p) 
 
 // ------------------------------------------------------------------- output
 
-__global__ __launch_bounds__(256) void linattn_output_kernel(LinOutputArgs p) {
+__global__ __launch_bounds__(256, 3) void linattn_output_kernel(LinOutputArgs p) {
     __shared__ __attribute__((aligned(16))) float sQ[kC * kLD];   // phi(Q)
     __shared__ __attribute__((aligned(16))) float sK[kC * kLD];   // phi(K), later the masked A
     __shared__ __attribute__((aligned(16))) float sS[kC * kLD];   // S_in^T, later V (rotated)
@@ -112,30 +112,34 @@ __global__ __launch_bounds__(256) void linattn_output_kernel(LinOutputArgs p) {
         if (lane >= k) rmax = rmax > o ? rmax : o;
     }
 
-    // V is fetched now (its loads overlap the first contractions) and moved
-    // into the S buffer once S has been used
-    f32x4 vreg[4];
+    // every global load of the workgroup is issued before any LDS store: q,
+    // k, v and S_in into registers (V is kept there and moved into the S
+    // buffer once S has been used)
+    f32x4 qreg[4], kreg[4], vreg[4], sreg[4];
+    fetch_rows(qreg, p.q, t0, p.H, h, 0, nvalid);
+    fetch_rows(kreg, p.k, t0, p.H, h, 0, nvalid);
     const int bad = fetch_rows(vreg, p.v, t0, p.H, h, 0, nvalid);
-    stage<true, false>(sQ, p.q, t0, p.H, h, 0, nvalid);
-    stage<true, false>(sK, p.k, t0, p.H, h, 0, nvalid);
-    if (c > 0) {
-        const float* src = p.Sinc + ((c - 1) * p.H + h) * kStateWords;
+    const float* src = c > 0 ? p.Sinc + ((c - 1) * p.H + h) * kStateWords : nullptr;
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int f = tid + 256 * u;
-            const int row = f >> 4, c4 = (f & 15) * 4;
-            *(f32x4*)(sS + row * kLD + c4) = *(const f32x4*)(src + row * kC + c4);
-        }
-        if (tid < kC) sZ[tid] = src[kC * kC + tid];
-    } else {
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int f = tid + 256 * u;
-            const int row = f >> 4, c4 = (f & 15) * 4;
-            *(f32x4*)(sS + row * kLD + c4) = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-        }
-        if (tid < kC) sZ[tid] = 0.0f;
+    for (int u = 0; u < 4; ++u) {
+        const int f = tid + 256 * u;
+        sreg[u] = src ? *(const f32x4*)(src + (f >> 4) * kC + (f & 15) * 4) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     }
+    const float zin = (src && tid < kC) ? src[kC * kC + tid] : 0.0f;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int f = tid + 256 * u;
+        const int row = f >> 4, c4 = (f & 15) * 4;
+        f32x4 qv = qreg[u], kv = kreg[u];
+        if (row < nvalid) {
+            qv.x = phi(qv.x); qv.y = phi(qv.y); qv.z = phi(qv.z); qv.w = phi(qv.w);
+            kv.x = phi(kv.x); kv.y = phi(kv.y); kv.z = phi(kv.z); kv.w = phi(kv.w);
+        }
+        *(f32x4*)(sQ + row * kLD + c4) = qv;
+        *(f32x4*)(sK + row * kLD + c4) = kv;
+        *(f32x4*)(sS + row * kLD + c4) = sreg[u];
+    }
+    if (tid < kC) sZ[tid] = zin;
     const bool nonfinite_v = __syncthreads_or(bad) != 0;
 
     // episode index of the chunk's steps (head-0 workgroups): wavefront 2
@@ -219,15 +223,19 @@ __global__ __launch_bounds__(256) void linattn_output_kernel(LinOutputArgs p) {
         }
     }
 
+    // one reciprocal per row (correctly rounded) and a product per output
+    float rden[4];
 #pragma unroll
-    for (int jt = 0; jt < 4; ++jt) {
+    for (int r = 0; r < 4; ++r) rden[r] = 1.0f / den[r];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int i = 16 * w + 4 * (lane >> 4) + r;
-            const int n = 16 * jt + (lane & 15);
-            if (i < nvalid) {
+    for (int r = 0; r < 4; ++r) {
+        const int i = 16 * w + 4 * (lane >> 4) + r;
+        if (i < nvalid) {
+            float* orow = p.out + ((t0 + i) * p.H + h) * kC + (lane & 15);
+#pragma unroll
+            for (int jt = 0; jt < 4; ++jt) {
                 const float num = accO[jt][r] + (ri[r] < 0 ? accS[jt][r] : 0.0f);
-                p.out[((t0 + i) * p.H + h) * kC + n] = num / den[r];
+                orow[16 * jt] = num * rden[r];
             }
         }
     }
