@@ -38,9 +38,29 @@
  *    2 complex64) take the vectorised kernels; other shapes take a scalar
  *    kernel with identical results.
  *  - The workspace is caller-allocated device memory of at least the size the
- *    matching *_workspace_bytes query returns for the same arguments.  Its
- *    contents are undefined on entry and on exit; the call initialises what it
- *    needs on `stream`.  Concurrent calls must use distinct workspaces.
+ *    matching *_workspace_bytes query returns for the same arguments, 16-byte
+ *    aligned (256 for linear attention).  Concurrent calls must use distinct
+ *    workspaces.  Two kinds of call:
+ *      * PREPARED (memoroid_scan_diag, _diag_bwd, _ffm, _ffm_bwd,
+ *        memoroid_discounted_return, memoroid_gae,
+ *        memoroid_tbb_begin_indices): the call is one kernel launch and
+ *        initialises nothing.  The workspace must have been prepared with
+ *        memoroid_workspace_prepare() (on a stream ordered before the call)
+ *        and then used only by calls of this library.  The first call binds
+ *        it to that entry point and those sizes (discounted return and GAE
+ *        count as one entry point); every later call with the same entry
+ *        point, sizes and flags finds it ready again, with no preparation in
+ *        between.  The binding also covers: the dtypes; whether the
+ *        vectorised kernels run (pointer alignment, d); a time-invariant a;
+ *        whether grad_a / the FFM parameter gradients are asked for.  A call
+ *        that differs in any of these returns MEMOROID_OK but computes
+ *        nothing: memoroid_workspace_status() then reports
+ *        MEMOROID_EMISMATCH, and the workspace must be prepared again before
+ *        any further use.  Prepare it again as well after
+ *        MEMOROID_ETIMEOUT, and after any other writes to its memory.
+ *      * SELF-INITIALISING (memoroid_scan_linattn, _linattn_bwd,
+ *        memoroid_tbb_sample): contents undefined on entry and on exit; the
+ *        call initialises what it needs on `stream`.
  */
 #ifndef MEMOROID_H
 #define MEMOROID_H
@@ -52,7 +72,7 @@
 extern "C" {
 #endif
 
-#define MEMOROID_ABI_VERSION 1
+#define MEMOROID_ABI_VERSION 2
 
 typedef enum {
     MEMOROID_OK = 0,
@@ -60,7 +80,9 @@ typedef enum {
     MEMOROID_EUNSUPPORTED = -2, /* valid but unsupported dtype pair or shape */
     MEMOROID_EWORKSPACE = -3,   /* workspace NULL or smaller than the query's size */
     MEMOROID_EHIP = -4,         /* a HIP runtime call or kernel launch failed */
-    MEMOROID_ETIMEOUT = -5      /* memoroid_workspace_status: a cross-tile wait gave up */
+    MEMOROID_ETIMEOUT = -5,     /* memoroid_workspace_status: a cross-tile wait gave up */
+    MEMOROID_EMISMATCH = -6     /* memoroid_workspace_status: the workspace was bound to
+                                   another call (or not prepared); prepare it again */
 } memoroid_status;
 
 typedef enum {
@@ -99,6 +121,7 @@ const char* memoroid_status_string(int status);
  *              bf16 inputs are decoded exactly and the state is carried in
  *              fp32; bf16 outputs are rounded to nearest even.  Other pairs:
  *              EUNSUPPORTED.
+ *   Workspace (prepared): memoroid_scan_diag_workspace_bytes(B, T, d, in_dtype, out_dtype).
  * ------------------------------------------------------------------------ */
 size_t memoroid_scan_diag_workspace_bytes(int64_t B, int64_t T, int64_t d,
                                           int in_dtype, int out_dtype);
@@ -130,6 +153,7 @@ int memoroid_scan_diag(const void* a, int64_t a_stride_t,
  *   grad_a     out [B][T][d] when a_stride_t == d; out [d], summed over every
  *              tape and step, when a_stride_t == 0.  NULL skips it.
  *   dtype      MEMOROID_F32 or MEMOROID_C64 (all tensors of that dtype).
+ *   Workspace (prepared): memoroid_scan_diag_bwd_workspace_bytes(B, T, d, dtype, a_stride_t).
  * ------------------------------------------------------------------------ */
 size_t memoroid_scan_diag_bwd_workspace_bytes(int64_t B, int64_t T, int64_t d,
                                               int dtype, int64_t a_stride_t);
@@ -157,6 +181,7 @@ int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t,
  *   S          out [B][T][m][c] complex64, interleaved (re, im).
  *   episode_idx  optional out int32[B][T]; NULL skips it.
  *   Vectorised when m * c is even and S is 16-byte aligned.
+ *   Workspace (prepared): memoroid_scan_ffm_workspace_bytes(B, T, m, c).
  * ------------------------------------------------------------------------ */
 size_t memoroid_scan_ffm_workspace_bytes(int64_t B, int64_t T, int64_t m, int64_t c);
 
@@ -182,7 +207,7 @@ int memoroid_scan_ffm(const float* alpha, const float* omega, const float* x,
  *   grad_alpha optional out [m] fp32;  grad_omega: optional out [c] fp32.
  *   c must be a power of two no larger than 16 (MEMOROID_EUNSUPPORTED
  *   otherwise): the input gradient is reduced over c inside the kernel.
- *   Workspace: memoroid_scan_ffm_bwd_workspace_bytes(B, T, m, c).
+ *   Workspace (prepared): memoroid_scan_ffm_bwd_workspace_bytes(B, T, m, c).
  * ------------------------------------------------------------------------ */
 size_t memoroid_scan_ffm_bwd_workspace_bytes(int64_t B, int64_t T, int64_t m, int64_t c);
 
@@ -206,6 +231,7 @@ int memoroid_scan_ffm_bwd(const float* alpha, const float* omega, const uint8_t*
  *   episode_idx  optional out int32[T] (as above); NULL skips it.
  *   dk, dv, chunk: this version supports dk == dv == 64 and chunk == 64
  *              (EUNSUPPORTED otherwise).
+ *   Workspace (self-initialising): memoroid_scan_linattn_workspace_bytes(T, H, dk, dv, chunk).
  * ------------------------------------------------------------------------ */
 size_t memoroid_scan_linattn_workspace_bytes(int64_t T, int64_t H, int64_t dk,
                                              int64_t dv, int64_t chunk);
@@ -232,7 +258,7 @@ int memoroid_scan_linattn(const float* q, const float* k, const float* v,
  *   grad_q, grad_k, grad_v  out [T][H][64] fp32, distinct from every input.
  *   dk == dv == chunk == 64 (MEMOROID_EUNSUPPORTED otherwise); 16-byte
  *   aligned fp32 arrays.
- *   Workspace: memoroid_scan_linattn_bwd_workspace_bytes(T, H, dk, dv, chunk).
+ *   Workspace (self-initialising): memoroid_scan_linattn_bwd_workspace_bytes(T, H, dk, dv, chunk).
  * ------------------------------------------------------------------------ */
 size_t memoroid_scan_linattn_bwd_workspace_bytes(int64_t T, int64_t H, int64_t dk,
                                                  int64_t dv, int64_t chunk);
@@ -257,7 +283,7 @@ int memoroid_scan_linattn_bwd(const float* q, const float* k, const float* v,
  *   G          out [B][T] fp32; must not alias r or start.
  *   Rows with T % 4 == 0 and 16-byte aligned r and G (4-byte aligned start)
  *   take the vectorised kernel, other shapes a scalar one.
- *   Workspace: memoroid_discount_workspace_bytes(B, T) bytes.
+ *   Workspace (prepared): memoroid_discount_workspace_bytes(B, T) bytes.
  * ------------------------------------------------------------------------ */
 size_t memoroid_discount_workspace_bytes(int64_t B, int64_t T);
 
@@ -288,7 +314,7 @@ int memoroid_discounted_return(const float* r, const uint8_t* start, float gamma
  *              Outputs must not alias any input or each other.
  *   Vectorised when T % 4 == 0, every fp32 pointer is 16-byte aligned and
  *   the flag pointers 4-byte aligned.
- *   Workspace: memoroid_discount_workspace_bytes(B, T) bytes.
+ *   Workspace (prepared): memoroid_discount_workspace_bytes(B, T) bytes.
  * ------------------------------------------------------------------------ */
 int memoroid_gae(const float* r, const float* value, const float* value_next, const uint8_t* done,
                  const uint8_t* start, float gamma, float lambda, float* adv, float* target,
@@ -307,7 +333,7 @@ int memoroid_gae(const float* r, const float* value, const float* value_next, co
  *   indices    out, room for n int64 values (only count are written).
  *   count      out, one int64 in device memory.
  *   n < 2^31 (MEMOROID_EUNSUPPORTED otherwise); n == 0 writes count = 0.
- *   Workspace: memoroid_tbb_begin_indices_workspace_bytes(n).
+ *   Workspace (prepared): memoroid_tbb_begin_indices_workspace_bytes(n).
  * ------------------------------------------------------------------------ */
 size_t memoroid_tbb_begin_indices_workspace_bytes(int64_t n);
 
@@ -336,7 +362,7 @@ int memoroid_tbb_begin_indices(const uint8_t* start, int64_t n, int64_t offset,
  *   n_draws <= 2^24 and row_bytes <= 2^24 (MEMOROID_EUNSUPPORTED otherwise).
  *   Rows move in 16-byte
  *   units when row_bytes % 16 == 0 and D, out are 16-byte aligned.
- *   Workspace: memoroid_tbb_sample_workspace_bytes(n_draws) (0 when n_draws is 0).
+ *   Workspace (self-initialising): memoroid_tbb_sample_workspace_bytes(n_draws) (0 when n_draws is 0).
  * ------------------------------------------------------------------------ */
 size_t memoroid_tbb_sample_workspace_bytes(int64_t n_draws);
 
@@ -346,10 +372,25 @@ int memoroid_tbb_sample(const void* D, int64_t n_D, int64_t row_bytes,
                         int64_t* filled, void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
- * Health of the last call that used `workspace`: synchronises `stream`,
- * then returns MEMOROID_OK, or MEMOROID_ETIMEOUT if a kernel's bounded wait
- * for a predecessor tile gave up (its outputs are then invalid), or
- * MEMOROID_EHIP if the copy failed.  Intended for tests and debugging.
+ * Prepare a workspace for the PREPARED calls (see the conventions above):
+ * enqueues on `stream` one kernel that fills the first workspace_bytes
+ * (rounded down to a multiple of 16) with all-ones bytes: an unbound
+ * workspace, with no tile counted and no descriptor published.  workspace
+ * must be 16-byte aligned and at least 256 bytes (MEMOROID_EINVAL
+ * otherwise).  Not needed by the SELF-INITIALISING calls.  The caller keeps
+ * ownership; nothing is allocated.
+ * ------------------------------------------------------------------------ */
+int memoroid_workspace_prepare(void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Health of the calls that used `workspace` since it was prepared (for a
+ * SELF-INITIALISING call: of the last call): synchronises `stream`, then
+ * returns MEMOROID_OK; MEMOROID_EMISMATCH if a call found the workspace
+ * bound to another call (that call's outputs are invalid); MEMOROID_ETIMEOUT
+ * if a kernel's bounded wait for a predecessor tile gave up (its outputs are
+ * then invalid); MEMOROID_EHIP if the copy failed.  Meaningless for a
+ * memoroid_tbb_sample workspace, which holds no header.  Intended for tests
+ * and debugging.
  * ------------------------------------------------------------------------ */
 int memoroid_workspace_status(const void* workspace, size_t workspace_bytes, void* stream);
 

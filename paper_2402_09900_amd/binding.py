@@ -5,10 +5,15 @@ runs in the library's HIP kernels:
 
 * ``memoroid_*`` functions with the C names and signatures (plain integers
   for pointers), for callers that manage device memory themselves;
-* ``scan_diag``, ``scan_diag_bwd``, ``scan_linattn`` taking torch CUDA
-  tensors: they check shapes, dtypes and contiguity, allocate outputs and the
-  workspace with ``torch.empty`` and launch on the current torch stream.
-  ``DiagScan`` wraps the diagonal pair as a ``torch.autograd.Function``.
+* ``scan_diag``, ``scan_diag_bwd``, ``scan_linattn`` ... taking torch CUDA
+  tensors: they check shapes, dtypes and contiguity, allocate outputs with
+  ``torch.empty`` and launch on the current torch stream.  Workspaces of the
+  prepared entry points (one kernel per call, see include/memoroid.h) come
+  from a small cache of prepared workspaces, one per (device, stream, entry
+  point, sizes, flags, operand alignment): after the first call with a key,
+  a call launches exactly one kernel.  A workspace tensor passed in
+  explicitly is prepared on every call.  ``DiagScan`` wraps the diagonal pair
+  as a ``torch.autograd.Function``.
 
 Loading fails loudly (``MemoroidError``) if the shared library is missing:
 there is no fallback implementation.
@@ -22,7 +27,7 @@ from typing import Optional, Tuple
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmemoroid.so")
 
-OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP, ETIMEOUT = 0, -1, -2, -3, -4, -5
+OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP, ETIMEOUT, EMISMATCH = 0, -1, -2, -3, -4, -5, -6
 F32, BF16, C64 = 0, 1, 2
 
 _lib = None
@@ -87,6 +92,8 @@ def lib() -> ctypes.CDLL:
         L.memoroid_gae.argtypes = [P, P, P, P, P, ctypes.c_float, ctypes.c_float, P, P, I64, I64, P, SZ, P]
         L.memoroid_workspace_status.restype = I32
         L.memoroid_workspace_status.argtypes = [P, SZ, P]
+        L.memoroid_workspace_prepare.restype = I32
+        L.memoroid_workspace_prepare.argtypes = [P, SZ, P]
         _lib = L
     return _lib
 
@@ -204,6 +211,10 @@ def memoroid_workspace_status(workspace, workspace_bytes, stream) -> int:
     return lib().memoroid_workspace_status(workspace, workspace_bytes, stream)
 
 
+def memoroid_workspace_prepare(workspace, workspace_bytes, stream) -> int:
+    return lib().memoroid_workspace_prepare(workspace, workspace_bytes, stream)
+
+
 # ------------------------------------------------------------- torch layer
 
 def _torch():
@@ -249,10 +260,42 @@ def _raise(status: int, where: str):
 
 
 def _workspace(nbytes: int, device, workspace=None):
+    """Workspace of a self-initialising entry point."""
     torch = _torch()
     if workspace is not None and workspace.numel() >= nbytes:
         return workspace
     return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+_PREPARED = None            # OrderedDict: key -> prepared workspace tensor
+_PREPARED_MAX = 32
+
+
+def _prepared(nbytes: int, device, key, operands, workspace=None):
+    """Workspace of a prepared entry point.  `key` names the entry point and
+    the sizes and flags its layout depends on; the alignment of the operands
+    (which selects the vectorised kernels) is added here.  A workspace given
+    by the caller is prepared again on every call."""
+    global _PREPARED
+    torch = _torch()
+    stream = _stream_ptr(device)
+    if workspace is not None and workspace.numel() >= nbytes:
+        _raise(lib().memoroid_workspace_prepare(workspace.data_ptr(), workspace.numel(), stream),
+               "memoroid_workspace_prepare")
+        return workspace
+    import collections
+    if _PREPARED is None:
+        _PREPARED = collections.OrderedDict()
+    full = (device.index, stream, key, tuple(t.data_ptr() % 16 == 0 for t in operands if t is not None))
+    ws = _PREPARED.get(full)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        _raise(lib().memoroid_workspace_prepare(ws.data_ptr(), ws.numel(), stream), "memoroid_workspace_prepare")
+        _PREPARED[full] = ws
+        while len(_PREPARED) > _PREPARED_MAX:
+            _PREPARED.popitem(last=False)
+    _PREPARED.move_to_end(full)
+    return ws
 
 
 def _diag_shapes(a, x, start):
@@ -292,7 +335,7 @@ def scan_diag(a, x, start, out_dtype=None, episode_idx: bool = False, workspace=
     h = torch.empty((B, T, d), dtype=out_torch, device=dev)
     idx = torch.empty((B, T), dtype=torch.int32, device=dev) if episode_idx else None
     nbytes = lib().memoroid_scan_diag_workspace_bytes(B, T, d, in_dt, out_dt)
-    ws = _workspace(nbytes, dev, workspace)
+    ws = _prepared(nbytes, dev, ("diag", B, T, d, in_dt, out_dt, stride), (a, x, h), workspace)
     st = lib().memoroid_scan_diag(a.data_ptr(), stride, x.data_ptr(), start.data_ptr(), h.data_ptr(),
                                   idx.data_ptr() if idx is not None else None, B, T, d, in_dt, out_dt,
                                   ws.data_ptr(), ws.numel(), _stream_ptr(dev))
@@ -320,7 +363,7 @@ def scan_diag_bwd(a, start, h, grad_h, need_grad_a: bool = True, workspace=None)
     if need_grad_a:
         ga = torch.empty((B, T, d) if stride else (d,), dtype=grad_h.dtype, device=dev)
     nbytes = lib().memoroid_scan_diag_bwd_workspace_bytes(B, T, d, dt, stride)
-    ws = _workspace(nbytes, dev, workspace)
+    ws = _prepared(nbytes, dev, ("diag_bwd", B, T, d, dt, stride, need_grad_a), (a, h, grad_h, gx, ga), workspace)
     st = lib().memoroid_scan_diag_bwd(a.data_ptr(), stride, start.data_ptr(),
                                       h.data_ptr() if h is not None else None, grad_h.data_ptr(),
                                       gx.data_ptr(), ga.data_ptr() if ga is not None else None,
@@ -375,7 +418,7 @@ def scan_ffm(alpha, omega, x, start, episode_idx: bool = False, workspace=None):
         raise TypeError("start must be uint8")
     S = torch.empty((B, T, m, c), dtype=torch.complex64, device=dev)
     idx = torch.empty((B, T), dtype=torch.int32, device=dev) if episode_idx else None
-    ws = _workspace(lib().memoroid_scan_ffm_workspace_bytes(B, T, m, c), dev, workspace)
+    ws = _prepared(lib().memoroid_scan_ffm_workspace_bytes(B, T, m, c), dev, ("ffm", B, T, m, c), (S,), workspace)
     st = lib().memoroid_scan_ffm(alpha.data_ptr(), omega.data_ptr(), x.data_ptr(), start.data_ptr(), S.data_ptr(),
                                  idx.data_ptr() if idx is not None else None, B, T, m, c, ws.data_ptr(), ws.numel(),
                                  _stream_ptr(dev))
@@ -397,7 +440,7 @@ def tbb_begin_indices(start, offset: int = 0, workspace=None):
     n = start.numel()
     idx = torch.empty(max(n, 1), dtype=torch.int64, device=dev)
     count = torch.empty(1, dtype=torch.int64, device=dev)
-    ws = _workspace(lib().memoroid_tbb_begin_indices_workspace_bytes(n), dev, workspace)
+    ws = _prepared(lib().memoroid_tbb_begin_indices_workspace_bytes(n), dev, ("tbb_begins", n), (), workspace)
     st = lib().memoroid_tbb_begin_indices(start.data_ptr(), n, int(offset), idx.data_ptr(), count.data_ptr(),
                                           ws.data_ptr(), ws.numel(), _stream_ptr(dev))
     _raise(st, "memoroid_tbb_begin_indices")
@@ -443,7 +486,8 @@ def scan_ffm_bwd(alpha, omega, start, S, grad_S, params: bool = True, workspace=
     gx = torch.empty((B, T, m), dtype=torch.float32, device=dev)
     ga = torch.empty(m, dtype=torch.float32, device=dev) if params else None
     gw = torch.empty(c, dtype=torch.float32, device=dev) if params else None
-    ws = _workspace(lib().memoroid_scan_ffm_bwd_workspace_bytes(B, T, m, c), dev, workspace)
+    ws = _prepared(lib().memoroid_scan_ffm_bwd_workspace_bytes(B, T, m, c), dev, ("ffm_bwd", B, T, m, c, params),
+                   (S, grad_S), workspace)
     st = lib().memoroid_scan_ffm_bwd(alpha.data_ptr(), omega.data_ptr(), start.data_ptr(),
                                      S.data_ptr() if S is not None else None, grad_S.data_ptr(), gx.data_ptr(),
                                      ga.data_ptr() if ga is not None else None,
@@ -473,7 +517,7 @@ def discounted_return(r, start, gamma: float, workspace=None):
     if r.dtype != torch.float32 or start.dtype != torch.uint8:
         raise TypeError("r must be float32 and start uint8")
     G = torch.empty((B, T), dtype=torch.float32, device=dev)
-    ws = _workspace(lib().memoroid_discount_workspace_bytes(B, T), dev, workspace)
+    ws = _prepared(lib().memoroid_discount_workspace_bytes(B, T), dev, ("discount", B, T), (), workspace)
     st = lib().memoroid_discounted_return(r.data_ptr(), start.data_ptr(), float(gamma), G.data_ptr(), B, T,
                                           ws.data_ptr(), ws.numel(), _stream_ptr(dev))
     _raise(st, "memoroid_discounted_return")
@@ -497,7 +541,7 @@ def gae(r, value, start, gamma: float, lam: float, value_next=None, done=None, t
             raise TypeError("start and done must be uint8")
     adv = torch.empty((B, T), dtype=torch.float32, device=dev)
     tg = torch.empty((B, T), dtype=torch.float32, device=dev) if target else None
-    ws = _workspace(lib().memoroid_discount_workspace_bytes(B, T), dev, workspace)
+    ws = _prepared(lib().memoroid_discount_workspace_bytes(B, T), dev, ("discount", B, T), (), workspace)
     st = lib().memoroid_gae(r.data_ptr(), value.data_ptr(),
                             value_next.data_ptr() if value_next is not None else None,
                             done.data_ptr() if done is not None else None, start.data_ptr(),
@@ -529,8 +573,9 @@ def scan_linattn_bwd(q, k, v, start, out, grad_out, chunk: int = 64, workspace=N
 
 
 def workspace_status(workspace) -> int:
-    """Synchronise and report whether the last call on `workspace` timed out
-    in a cross-tile wait (ETIMEOUT) or completed normally (OK)."""
+    """Synchronise and report OK, ETIMEOUT (a cross-tile wait gave up) or
+    EMISMATCH (the workspace was bound to another call) for the calls that
+    used `workspace` since it was prepared."""
     return lib().memoroid_workspace_status(workspace.data_ptr(), workspace.numel(),
                                            _stream_ptr(workspace.device))
 

@@ -2,6 +2,7 @@
 // argument validation (before any HIP call), tiling plans, workspace layout
 // and kernel launches.
 #include <limits.h>
+#include <initializer_list>
 #include <stdlib.h>
 #include <string.h>
 
@@ -41,11 +42,29 @@ struct DiagPlan {
     int64_t nt = 0;
     int64_t nchains = 0;
     int64_t ntiles = 0;
+    // offsets of the counters and of bank 0's regions (bank 1: + bank_bytes)
     size_t off_ctr = 0, off_agg = 0, off_incl = 0, off_cnt = 0, off_part = 0, off_sum1 = 0, off_sum2 = 0;
-    size_t fill_bytes = 0;   // bytes from off_agg that must start as 0xFF
+    size_t bank_bytes = 0;
     bool fused_da = false;   // one tape: da summed inside the reverse kernel
     size_t total = 0;
 };
+
+// Signature of a call's workspace layout (FNV-1a over the values that fix
+// it); never all ones (a fresh workspace) or kSigPoisoned.
+uint64_t layout_sig(std::initializer_list<int64_t> vals) {
+    uint64_t h = 0xcbf29ce484222325ull;
+    for (int64_t v : vals)
+        for (int i = 0; i < 8; ++i) {
+            h ^= (uint64_t)(v >> (8 * i)) & 0xFFu;
+            h *= 0x100000001b3ull;
+        }
+    if (h == kEmpty64 || h == kSigPoisoned) h ^= 0x9E3779B97F4A7C15ull;
+    return h;
+}
+
+// entry points in a signature
+enum SigKind : int64_t { kSigDiag = 1, kSigDiagBwd, kSigFfm, kSigFfmBwd, kSigDiscount, kSigTbbBegins,
+                         kSigLinattn, kSigLinattnBwd };
 
 // Tiling and workspace layout of a diagonal scan.  `vec` selects the
 // vectorised lane width; `state_complex` picks the descriptor size.
@@ -78,21 +97,25 @@ bool plan_diag(int64_t B, int64_t T, int64_t d, int state_dtype, bool vec, int r
     size_t off = kAlign;                                   // header
     p->off_ctr = off;                                      // per-chain tile counters
     off = align_up(off + (size_t)p->nchains * kCtrStride * 4);
+    // bank 0 of the self-validating words, then bank 1 with the same layout
+    const size_t bank0 = off;
     p->off_agg = off;
     off = align_up(off + (size_t)ndesc * agg_b);
     p->off_incl = off;
     off = align_up(off + (size_t)ndesc * incl_b);
     p->off_cnt = off;                                      // begin-count words, [tiles per chain][B]
     if (!bwd) off = align_up(off + (size_t)p->nt * (size_t)B * 8);
-    p->fill_bytes = off - p->off_agg;
-    if (bwd && ainv && want_grad_a && B == 1) {
-        // one tape: the partial rows are self-validating 64-bit words, filled
+    const bool fused = bwd && ainv && want_grad_a && B == 1;
+    if (fused) {
+        // one tape: the partial rows are self-validating 64-bit words, banked
         // with the descriptors, and the chain's last tile sums them
         p->fused_da = true;
         p->off_part = off;
         off = align_up(off + (size_t)p->nt * (size_t)d * 8);
-        p->fill_bytes = off - p->off_agg;
-    } else if (bwd && ainv && want_grad_a) {
+    }
+    p->bank_bytes = off - bank0;
+    off += p->bank_bytes;
+    if (bwd && ainv && want_grad_a && !fused) {
         const size_t sb = cplx ? 8 : 4;
         const int64_t rows_part = p->nt * B;
         p->off_part = off;
@@ -108,6 +131,19 @@ bool plan_diag(int64_t B, int64_t T, int64_t d, int state_dtype, bool vec, int r
 }
 
 int check_hip(hipError_t e) { return e == hipSuccess ? MEMOROID_OK : MEMOROID_EHIP; }
+
+// Workspace fields of a diagonal scan's arguments: counters and bank-0
+// descriptor regions at `base` (the plan's offset 0), header at `hdr`.
+template <class Args>
+void set_scan_ws(Args& a, const DiagPlan& p, char* base, WsHeader* hdr, uint64_t sig) {
+    a.nt = p.nt;
+    a.agg = base + p.off_agg;
+    a.incl = base + p.off_incl;
+    a.bank = (int64_t)p.bank_bytes;
+    a.hdr = hdr;
+    a.sig = sig;
+    a.ctr = (uint32_t*)(base + p.off_ctr);
+}
 
 bool diag_dtypes_ok(int in_dt, int out_dt) {
     return (in_dt == MEMOROID_F32 && out_dt == MEMOROID_F32) || (in_dt == MEMOROID_BF16 && out_dt == MEMOROID_BF16) ||
@@ -147,6 +183,8 @@ const char* memoroid_status_string(int status) {
         case MEMOROID_EWORKSPACE: return "workspace missing or too small";
         case MEMOROID_EHIP: return "HIP runtime error";
         case MEMOROID_ETIMEOUT: return "a cross-tile wait gave up; outputs are invalid";
+        case MEMOROID_EMISMATCH:
+            return "workspace prepared for (bound to) another call; outputs are invalid, prepare it again";
         default: return "unknown status";
     }
 }
@@ -197,7 +235,6 @@ int memoroid_scan_diag(const void* a, int64_t a_stride_t, const void* x, const u
 
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
-    if (ws_init_launch(ws, p.off_agg, ws + p.off_agg, p.fill_bytes, s) != hipSuccess) return MEMOROID_EHIP;
     DiagFwdArgs args{};
     args.a = a;
     args.x = x;
@@ -208,10 +245,7 @@ int memoroid_scan_diag(const void* a, int64_t a_stride_t, const void* x, const u
     args.Qp = p.Qp;
     args.nfb = p.nfb;
     args.nchains = (int32_t)p.nchains;
-    args.agg = ws + p.off_agg;
-    args.incl = ws + p.off_incl;
-    args.hdr = (WsHeader*)ws;
-    args.ctr = (uint32_t*)(ws + p.off_ctr);
+    set_scan_ws(args, p, ws, (WsHeader*)ws, layout_sig({kSigDiag, B, T, d, sd, vec, ainv}));
     args.idx = episode_idx;
     args.cnt = (uint64_t*)(ws + p.off_cnt);
     const int ik = in_dtype == MEMOROID_F32 ? K_F32 : in_dtype == MEMOROID_BF16 ? K_BF16 : K_C64;
@@ -260,7 +294,6 @@ int memoroid_scan_ffm(const float* alpha, const float* omega, const float* x, co
     if (!aligned(workspace, 16)) return MEMOROID_EINVAL;
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
-    if (ws_init_launch(ws, p.off_agg, ws + p.off_agg, p.fill_bytes, s) != hipSuccess) return MEMOROID_EHIP;
     DiagFwdArgs args{};
     args.a = nullptr;
     args.x = x;
@@ -271,10 +304,7 @@ int memoroid_scan_ffm(const float* alpha, const float* omega, const float* x, co
     args.Qp = p.Qp;
     args.nfb = p.nfb;
     args.nchains = (int32_t)p.nchains;
-    args.agg = ws + p.off_agg;
-    args.incl = ws + p.off_incl;
-    args.hdr = (WsHeader*)ws;
-    args.ctr = (uint32_t*)(ws + p.off_ctr);
+    set_scan_ws(args, p, ws, (WsHeader*)ws, layout_sig({kSigFfm, B, T, m, c, vec}));
     args.idx = episode_idx;
     args.cnt = (uint64_t*)(ws + p.off_cnt);
     args.alpha = alpha;
@@ -347,7 +377,6 @@ int memoroid_scan_ffm_bwd(const float* alpha, const float* omega, const uint8_t*
     if (!aligned(workspace, 16)) return MEMOROID_EINVAL;
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
-    if (ws_init_launch(ws, p.off_agg, ws + p.off_agg, p.fill_bytes, s) != hipSuccess) return MEMOROID_EHIP;
     DiagBwdArgs args{};
     args.a = nullptr;
     args.start = start;
@@ -359,14 +388,10 @@ int memoroid_scan_ffm_bwd(const float* alpha, const float* omega, const uint8_t*
     args.da_out = (params && p.fused_da) ? ws + off_da : nullptr;
     args.T = T;
     args.d = d;
-    args.nt = p.nt;
     args.Qp = p.Qp;
     args.nfb = p.nfb;
     args.nchains = (int32_t)p.nchains;
-    args.agg = ws + p.off_agg;
-    args.incl = ws + p.off_incl;
-    args.hdr = (WsHeader*)ws;
-    args.ctr = (uint32_t*)(ws + p.off_ctr);
+    set_scan_ws(args, p, ws, (WsHeader*)ws, layout_sig({kSigFfmBwd, B, T, m, c, vec, params}));
     args.alpha = alpha;
     args.omega = omega;
     args.ffm_m = m;
@@ -431,7 +456,6 @@ int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t, const uint8_t* sta
 
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
-    if (ws_init_launch(ws, p.off_agg, ws + p.off_agg, p.fill_bytes, s) != hipSuccess) return MEMOROID_EHIP;
     DiagBwdArgs args{};
     args.a = a;
     args.start = start;
@@ -443,14 +467,11 @@ int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t, const uint8_t* sta
     args.da_out = (ainv && grad_a && p.fused_da) ? grad_a : nullptr;
     args.T = T;
     args.d = d;
-    args.nt = p.nt;
     args.Qp = p.Qp;
     args.nfb = p.nfb;
     args.nchains = (int32_t)p.nchains;
-    args.agg = ws + p.off_agg;
-    args.incl = ws + p.off_incl;
-    args.hdr = (WsHeader*)ws;
-    args.ctr = (uint32_t*)(ws + p.off_ctr);
+    set_scan_ws(args, p, ws, (WsHeader*)ws,
+                layout_sig({kSigDiagBwd, B, T, d, dtype, vec, ainv, grad_a != nullptr}));
     const int k = dtype == MEMOROID_F32 ? K_F32 : K_C64;
     const int64_t cols = d * (dtype == MEMOROID_C64 ? 2 : 1);
     if (diag_bwd_launch(k, vec, ainv, args, p.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
@@ -544,10 +565,10 @@ int memoroid_scan_linattn(const float* q, const float* k, const float* v, const 
     sa.R = R;
     sa.T = T;
     sa.H = H;
-    sa.zero = (u32x4*)sw;
-    sa.zero16 = (int64_t)(p.scan.off_agg / 16);
-    sa.fill = (u32x4*)(sw + p.scan.off_agg);
-    sa.fill16 = (int64_t)((p.off_cnt + (size_t)p.nch * 8 - (p.off_scan + p.scan.off_agg) + 15) / 16);
+    // the summary kernel prepares the state scan's workspace and the count
+    // words (one contiguous run from offset 0) on every call
+    sa.fill = (u32x4*)sw;
+    sa.fill16 = (int64_t)((p.off_cnt + (size_t)p.nch * 8 - p.off_scan + 15) / 16);
     if (linattn_summary_launch(sa, s) != hipSuccess) return MEMOROID_EHIP;
     DiagFwdArgs args{};
     args.a = nullptr;            // a = 1: the state scan is a resettable sum
@@ -559,10 +580,7 @@ int memoroid_scan_linattn(const float* q, const float* k, const float* v, const 
     args.Qp = p.scan.Qp;
     args.nfb = p.scan.nfb;
     args.nchains = (int32_t)p.scan.nchains;
-    args.agg = sw + p.scan.off_agg;
-    args.incl = sw + p.scan.off_incl;
-    args.hdr = (WsHeader*)sw;
-    args.ctr = (uint32_t*)(sw + p.scan.off_ctr);
+    set_scan_ws(args, p.scan, sw, (WsHeader*)sw, layout_sig({kSigLinattn, T, H}));
     args.idx = nullptr;
     args.cnt = nullptr;
     if (diag_fwd_launch(K_F32, K_F32, true, true, args, p.scan.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
@@ -666,11 +684,10 @@ int memoroid_scan_linattn_bwd(const float* q, const float* k, const float* v, co
     sa.R = R;
     sa.T = T;
     sa.H = H;
-    sa.zero = (u32x4*)sw;
-    sa.zero16 = (int64_t)(f.scan.off_agg / 16);
-    sa.fill = (u32x4*)(sw + f.scan.off_agg);
-    sa.fill16 = (int64_t)((f.off_cnt + (size_t)f.nch * 8 - (f.off_scan + f.scan.off_agg) + 15) / 16);
+    sa.fill = (u32x4*)sw;
+    sa.fill16 = (int64_t)((f.off_cnt + (size_t)f.nch * 8 - f.off_scan + 15) / 16);
     if (linattn_summary_launch(sa, s) != hipSuccess) return MEMOROID_EHIP;
+    const uint64_t sig = layout_sig({kSigLinattnBwd, T, H});
     DiagFwdArgs fa{};
     fa.a = nullptr;
     fa.x = dS;
@@ -681,10 +698,7 @@ int memoroid_scan_linattn_bwd(const float* q, const float* k, const float* v, co
     fa.Qp = f.scan.Qp;
     fa.nfb = f.scan.nfb;
     fa.nchains = (int32_t)f.scan.nchains;
-    fa.agg = sw + f.scan.off_agg;
-    fa.incl = sw + f.scan.off_incl;
-    fa.hdr = (WsHeader*)sw;
-    fa.ctr = (uint32_t*)(sw + f.scan.off_ctr);
+    set_scan_ws(fa, f.scan, sw, (WsHeader*)sw, sig);
     if (diag_fwd_launch(K_F32, K_F32, true, true, fa, f.scan.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
 
     // backward summaries (and the reverse scan's workspace set-up)
@@ -708,10 +722,8 @@ int memoroid_scan_linattn_bwd(const float* q, const float* k, const float* v, co
     ba.T = T;
     ba.H = H;
     ba.nch = f.nch;
-    ba.zero = (u32x4*)rw;
-    ba.zero16 = (int64_t)(p.rscan.off_agg / 16);
-    ba.fill = (u32x4*)(rw + p.rscan.off_agg);
-    ba.fill16 = (int64_t)(p.rscan.fill_bytes / 16);
+    ba.fill = (u32x4*)rw;
+    ba.fill16 = (int64_t)(p.rscan.total / 16);
     if (linattn_bwd_summary_launch(ba, s) != hipSuccess) return MEMOROID_EHIP;
 
     // reverse chunk-state scan: Y_c = dU_c + [chunk c holds no begin] Y_{c+1}
@@ -727,14 +739,10 @@ int memoroid_scan_linattn_bwd(const float* q, const float* k, const float* v, co
     ra.da_part = nullptr;
     ra.T = f.nch;
     ra.d = f.dstate;
-    ra.nt = p.rscan.nt;
     ra.Qp = p.rscan.Qp;
     ra.nfb = p.rscan.nfb;
     ra.nchains = (int32_t)p.rscan.nchains;
-    ra.agg = rw + p.rscan.off_agg;
-    ra.incl = rw + p.rscan.off_incl;
-    ra.hdr = (WsHeader*)sw;
-    ra.ctr = (uint32_t*)(rw + p.rscan.off_ctr);
+    set_scan_ws(ra, p.rscan, rw, (WsHeader*)sw, sig);
     if (diag_bwd_launch(K_F32, true, true, ra, p.rscan.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
 
     return check_hip(linattn_bwd_grad_launch(ba, s));
@@ -748,19 +756,23 @@ namespace {
 
 struct DiscPlan {
     int64_t nt = 0, ntiles = 0;
-    size_t off_agg = 0, off_incl = 0, fill_bytes = 0, total = 0;
+    size_t off_epoch = 0, off_agg = 0, off_incl = 0, bank_bytes = 0, total = 0;
 };
 
+// header, per-tile epoch words, then two banks of tile words
 bool plan_disc(int64_t B, int64_t T, DiscPlan* p) {
     p->nt = (T + kDiscTile - 1) / kDiscTile;
     if (!mul_ok(B, p->nt, &p->ntiles) || p->ntiles >= (int64_t)INT32_MAX) return false;
     size_t off = kAlign;
+    p->off_epoch = off;
+    off = align_up(off + (size_t)p->ntiles * 4);
+    const size_t bank0 = off;
     p->off_agg = off;
     off = align_up(off + (size_t)p->ntiles * 8);
     p->off_incl = off;
     off = align_up(off + (size_t)p->ntiles * 8);
-    p->fill_bytes = off - p->off_agg;
-    p->total = off;
+    p->bank_bytes = off - bank0;
+    p->total = off + p->bank_bytes;
     return true;
 }
 
@@ -804,7 +816,6 @@ int disc_run(const float* r, const float* value, const float* value_next, const 
     if (!aligned(workspace, 16)) return MEMOROID_EINVAL;
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
-    if (ws_init_launch(ws, p.off_agg, ws + p.off_agg, p.fill_bytes, s) != hipSuccess) return MEMOROID_EHIP;
     DiscArgs args{};
     args.r = r;
     args.v = value;
@@ -821,7 +832,11 @@ int disc_run(const float* r, const float* value, const float* value_next, const 
     args.fallback_polls = fallback_polls();
     args.agg = (uint64_t*)(ws + p.off_agg);
     args.incl = (uint64_t*)(ws + p.off_incl);
+    args.bank = (int64_t)p.bank_bytes;
     args.hdr = (WsHeader*)ws;
+    // the return and the advantage share one layout (and may share a workspace)
+    args.sig = layout_sig({kSigDiscount, B, T});
+    args.epoch = (uint32_t*)(ws + p.off_epoch);
     return check_hip(disc_launch(vec, gae, args, p.ntiles, s));
 }
 
@@ -855,10 +870,29 @@ int memoroid_gae(const float* r, const float* value, const float* value_next, co
 
 // ------------------------------------------------- tape-based batching
 
+namespace {
+
+// header, per-tile epoch words, then two banks of count words
+struct TbbPlan {
+    int64_t ntiles = 0;
+    size_t off_epoch = 0, off_cnt = 0, bank_bytes = 0, total = 0;
+};
+
+void plan_tbb(int64_t n, TbbPlan* p) {
+    p->ntiles = (n + kTbbBeginTile - 1) / kTbbBeginTile;
+    p->off_epoch = kAlign;
+    p->off_cnt = align_up(p->off_epoch + (size_t)p->ntiles * 4);
+    p->bank_bytes = align_up((size_t)p->ntiles * 8);
+    p->total = p->off_cnt + 2 * p->bank_bytes;
+}
+
+}  // namespace
+
 size_t memoroid_tbb_begin_indices_workspace_bytes(int64_t n) {
     if (n <= 0 || n > (int64_t)INT32_MAX) return 0;
-    const int64_t ntiles = (n + kTbbBeginTile - 1) / kTbbBeginTile;
-    return align_up(kAlign + (size_t)ntiles * 8);
+    TbbPlan p;
+    plan_tbb(n, &p);
+    return p.total;
 }
 
 int memoroid_tbb_begin_indices(const uint8_t* start, int64_t n, int64_t offset, int64_t* indices, int64_t* count,
@@ -881,18 +915,22 @@ int memoroid_tbb_begin_indices(const uint8_t* start, int64_t n, int64_t offset, 
     if (!workspace || workspace_bytes < need) return MEMOROID_EWORKSPACE;
     if (!aligned(workspace, 16)) return MEMOROID_EINVAL;
     char* ws = (char*)workspace;
-    const int64_t ntiles = (n + kTbbBeginTile - 1) / kTbbBeginTile;
-    if (ws_init_launch(ws, kAlign, ws + kAlign, need - kAlign, s) != hipSuccess) return MEMOROID_EHIP;
+    TbbPlan p;
+    plan_tbb(n, &p);
     TbbBeginArgs a{};
     a.start = start;
     a.n = n;
     a.offset = offset;
     a.indices = indices;
     a.count = count;
-    a.cnt = (uint64_t*)(ws + kAlign);
+    a.cnt = (uint64_t*)(ws + p.off_cnt);
+    a.bank = (int64_t)p.bank_bytes;
+    a.hdr = (WsHeader*)ws;
+    a.sig = layout_sig({kSigTbbBegins, n});
+    a.epoch = (uint32_t*)(ws + p.off_epoch);
     a.fallback_polls = fallback_polls();
     const bool vec = aligned(start, 16) && n % 16 == 0;
-    return check_hip(tbb_begins_launch(vec, a, ntiles, s));
+    return check_hip(tbb_begins_launch(vec, a, p.ntiles, s));
 }
 
 size_t memoroid_tbb_sample_workspace_bytes(int64_t n_draws) {
@@ -948,13 +986,19 @@ int memoroid_tbb_sample(const void* D, int64_t n_D, int64_t row_bytes, const int
     return check_hip(tbb_sample_launch(unit, a, s));
 }
 
+int memoroid_workspace_prepare(void* workspace, size_t workspace_bytes, void* stream) {
+    if (!workspace || workspace_bytes < sizeof(WsHeader) || !aligned(workspace, 16)) return MEMOROID_EINVAL;
+    return check_hip(ws_init_launch(nullptr, 0, workspace, workspace_bytes / 16 * 16, (hipStream_t)stream));
+}
+
 int memoroid_workspace_status(const void* workspace, size_t workspace_bytes, void* stream) {
     if (!workspace || workspace_bytes < sizeof(WsHeader)) return MEMOROID_EINVAL;
-    uint32_t hdr[2] = {0, 0};
+    WsHeader hdr;
     hipStream_t s = (hipStream_t)stream;
-    if (hipMemcpyAsync(hdr, workspace, sizeof(hdr), hipMemcpyDeviceToHost, s) != hipSuccess) return MEMOROID_EHIP;
+    if (hipMemcpyAsync(&hdr, workspace, 16, hipMemcpyDeviceToHost, s) != hipSuccess) return MEMOROID_EHIP;
     if (hipStreamSynchronize(s) != hipSuccess) return MEMOROID_EHIP;
-    return hdr[1] ? MEMOROID_ETIMEOUT : MEMOROID_OK;
+    if (hdr.sig == kSigPoisoned) return MEMOROID_EMISMATCH;
+    return hdr.timeout != kEmpty32 ? MEMOROID_ETIMEOUT : MEMOROID_OK;
 }
 
 }  // extern "C"

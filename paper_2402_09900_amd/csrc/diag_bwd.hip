@@ -9,7 +9,8 @@
 // begin step; then dx_t = lam_t and da_t = [t not a begin] lam_t conj(h_{t-1}).
 // This is the forward scan's machinery (diag_fwd.hip) mirrored in time: the
 // same tiles, handed out from the end of the tape, each step's coefficient
-// taken from the step after it, and episode ends acting as resets.
+// taken from the step after it, and episode ends acting as resets; the same
+// never-reset counters, epoch banks and workspace binding.
 //
 // For a time-invariant a, da is the sum over all tapes and steps; each tile
 // writes one partial per feature, summed inside the tile in a fixed order, and
@@ -32,7 +33,8 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     constexpr int NW = NT / 64;
     constexpr int EB = KindInfo<K>::bytes;
 
-    __shared__ uint32_t s_ticket;
+    __shared__ uint32_t s_ticket;          // place in the chain; all ones: stand down
+    __shared__ uint32_t s_bank;
     __shared__ S sWA[NW][64 * VEC];
     __shared__ S sWH[NW][64 * VEC];
     __shared__ uint32_t sWF[NW];
@@ -46,12 +48,24 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     // the chain's own counter, in the order tiles start
     const uint32_t nch = (uint32_t)p.nchains;
     const int chain = (int)((blockIdx.x % nch + blockIdx.x / nch) % nch);
-    if (tid == 0)
-        s_ticket = __hip_atomic_fetch_add(p.ctr + (size_t)chain * kCtrStride, 1u, __ATOMIC_RELAXED,
-                                          __HIP_MEMORY_SCOPE_AGENT);
+    if (tid == 0) {
+        // the signature load goes first: the compiler waits for the atomic's
+        // result right after issuing it, and both round trips then overlap
+        const uint64_t seen = peek_sig(p.hdr);
+        const Claim c = claim_of(take_ticket(p.ctr + (size_t)chain * kCtrStride, (uint32_t)p.nt), (uint32_t)p.nt);
+        const bool bound = ws_bound_to(p.hdr, p.sig, seen, chain == 0 && c.pos == 0);
+        s_ticket = bound ? c.pos : kEmpty32;
+        s_bank = c.bank;
+    }
     __syncthreads();
-    const int64_t k = (int64_t)__builtin_amdgcn_readfirstlane(s_ticket);
+    const uint32_t claimed = __builtin_amdgcn_readfirstlane(s_ticket);
+    if (claimed == kEmpty32) return;       // workspace bound to another call: every tile stands down
+    const int64_t k = (int64_t)claimed;
     const uint32_t ticket = (uint32_t)(k * p.nchains + chain);
+    const int64_t boff = __builtin_amdgcn_readfirstlane(s_bank) ? p.bank : 0;
+    const int64_t bidle = p.bank - boff;
+    void* const agg = (char*)p.agg + boff;
+    void* const incl = (char*)p.incl + boff;
     const int64_t tile = p.nt - 1 - k;              // tiles run from the tape end
     const int b = chain / p.nfb;
     const int fb = chain - b * p.nfb;
@@ -110,12 +124,11 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
         if (want_da) raw_bload(rh[r], rs_h, h_back ? off : off - step);
     }
     __builtin_amdgcn_sched_barrier(0);
-    uint32_t ends = 0, begins = 0, valid = 0;
+    uint32_t ends = 0, begins = 0;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         const int64_t t = row0 + r;
         const uint32_t in = t < T ? 1u : 0u;
-        valid |= in << r;
         begins |= (in & ((t == 0 ? 1u : 0u) | (fl[r] != 0u ? 1u : 0u))) << r;
         ends |= (in & ((t + 1 == T ? 1u : 0u) | (fl[r + 1] != 0u ? 1u : 0u))) << r;
     }
@@ -202,15 +215,18 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
         if (summary_lane) {
 #pragma unroll
             for (int v = 0; v < VEC; ++v) {
-                if (tot.f) Desc<S>::put_incl(p.incl, desc_slot(ticket, Dp, Qp, q, v), tot.H[v]);
-                else Desc<S>::put_agg(p.agg, desc_slot(ticket, Dp, Qp, q, v), tot.A[v], tot.H[v]);
+                if (tot.f) Desc<S>::put_incl(incl, desc_slot(ticket, Dp, Qp, q, v), tot.H[v]);
+                else Desc<S>::put_agg(agg, desc_slot(ticket, Dp, Qp, q, v), tot.A[v], tot.H[v]);
             }
+#pragma unroll
+            for (int v = 0; v < VEC; ++v)
+                Desc<S>::clear((char*)p.agg + bidle, (char*)p.incl + bidle, desc_slot(ticket, Dp, Qp, q, v));
         }
     }
     if (wave == NW - 1) {
         const bool need_carry = !((t_last + 1 == T) || fl_after != 0);
         S carry[VEC];
-        lookback<S, VEC>(p.agg, p.incl, (int64_t)ticket - p.nchains, p.nchains, Dp, Qp, need_carry && active, carry,
+        lookback<S, VEC>(agg, incl, (int64_t)ticket - p.nchains, p.nchains, Dp, Qp, need_carry && active, carry,
                          sLb, &p.hdr->timeout);
         if (j == 0) {
 #pragma unroll
@@ -227,7 +243,7 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     for (int v = 0; v < VEC; ++v) {
         const S c = sCarry[q * VEC + v];
         if (summary_lane && !tot.f)
-            Desc<S>::put_incl(p.incl, desc_slot(ticket, Dp, Qp, q, v), mad(tot.A[v], c, tot.H[v]));
+            Desc<S>::put_incl(incl, desc_slot(ticket, Dp, Qp, q, v), mad(tot.A[v], c, tot.H[v]));
         lam[v] = seg_apply<S, VEC>(pre, v, c);
     }
     S dsum[VEC];
@@ -308,8 +324,14 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
                 // partial row = (tile, tape); columns = the d features
                 const int64_t prow = tile * (p.nchains / p.nfb) + b;
                 if (p.da_out) {
+                    // self-validating words, banked like the descriptors
+                    uint64_t* const cur = (uint64_t*)((char*)p.da_part + boff);
+                    uint64_t* const idle = (uint64_t*)((char*)p.da_part + bidle);
 #pragma unroll
-                    for (int v = 0; v < VEC; ++v) publish64((uint64_t*)p.da_part + prow * p.d + f0 + v, pack_state(sv[v]));
+                    for (int v = 0; v < VEC; ++v) {
+                        publish64(cur + prow * p.d + f0 + v, pack_state(sv[v]));
+                        idle[prow * p.d + f0 + v] = kEmpty64;
+                    }
                 } else {
                     raw_store_nt((char*)p.da_part + (prow * p.d + f0) * EB, o);
                 }
@@ -324,6 +346,7 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
                 const int fs = tid % Dp, G = NT / Dp, grp = tid / Dp;
                 const int64_t f = (int64_t)fb * Dp + fs;
                 const bool fin = f < p.d;
+                const uint64_t* const part = (const uint64_t*)((const char*)p.da_part + boff);
                 S acc = s_zero<S>();
                 uint32_t polls = 0;
                 for (int64_t base = grp; base < p.nt; base += 8 * (int64_t)G) {
@@ -331,18 +354,18 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
 #pragma unroll
                     for (int i = 0; i < 8; ++i) {
                         const int64_t tl = base + (int64_t)i * G;
-                        wd[i] = (fin && tl < p.nt) ? peek64((const uint64_t*)p.da_part + tl * p.d + f) : 0ull;
+                        wd[i] = (fin && tl < p.nt) ? peek64(part + tl * p.d + f) : 0ull;
                     }
 #pragma unroll
                     for (int i = 0; i < 8; ++i) {
                         const int64_t tl = base + (int64_t)i * G;
                         while (wd[i] == kEmpty64) {
                             if (++polls > kMaxPolls) {
-                                __hip_atomic_store(&p.hdr->timeout, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                                flag_timeout(&p.hdr->timeout);
                                 wd[i] = 0ull;
                             } else {
                                 __builtin_amdgcn_s_sleep(1);
-                                wd[i] = peek64((const uint64_t*)p.da_part + tl * p.d + f);
+                                wd[i] = peek64(part + tl * p.d + f);
                             }
                         }
                         acc = acc + unpack_state<S>(wd[i]);

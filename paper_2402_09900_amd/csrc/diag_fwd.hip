@@ -25,6 +25,10 @@
 //            already running or finished.  Descriptors are indexed by
 //            ticket = tile * nchains + chain.  One counter per chain, each on
 //            its own 128-byte line, keeps the counters from serialising.
+//            The counters are never reset: they wrap every two calls, so a
+//            ticket also tells the call's epoch parity, which picks the
+//            descriptor bank (the tile clears its words of the other bank
+//            for the next call).
 //
 // Per tile: (1) every load is issued up front: the begin flags of the lane's
 // steps, then a and x, one wide access per step; (2) each lane folds its R
@@ -56,7 +60,8 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     constexpr int IB = KindInfo<IN>::bytes;
     constexpr int OB = KindInfo<OUT>::bytes;
 
-    __shared__ uint32_t s_ticket;
+    __shared__ uint32_t s_ticket;          // place in the chain; all ones: stand down
+    __shared__ uint32_t s_bank;
     __shared__ S sWA[NW][64 * VEC];        // wavefront totals, per feature of the block
     __shared__ S sWH[NW][64 * VEC];
     __shared__ uint32_t sWF[NW];
@@ -72,12 +77,26 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     // the chain's own counter, in the order tiles start
     const uint32_t nch = (uint32_t)p.nchains;
     const int chain = (int)((blockIdx.x % nch + blockIdx.x / nch) % nch);
-    if (tid == 0)
-        s_ticket = __hip_atomic_fetch_add(p.ctr + (size_t)chain * kCtrStride, 1u, __ATOMIC_RELAXED,
-                                          __HIP_MEMORY_SCOPE_AGENT);
+    if (tid == 0) {
+        // the signature load goes first: the compiler waits for the atomic's
+        // result right after issuing it, and both round trips then overlap
+        const uint64_t seen = peek_sig(p.hdr);
+        const Claim c = claim_of(take_ticket(p.ctr + (size_t)chain * kCtrStride, (uint32_t)p.nt), (uint32_t)p.nt);
+        const bool bound = ws_bound_to(p.hdr, p.sig, seen, chain == 0 && c.pos == 0);
+        s_ticket = bound ? c.pos : kEmpty32;
+        s_bank = c.bank;
+    }
     __syncthreads();
-    const int64_t tile = (int64_t)__builtin_amdgcn_readfirstlane(s_ticket);
+    const uint32_t claimed = __builtin_amdgcn_readfirstlane(s_ticket);
+    if (claimed == kEmpty32) return;       // workspace bound to another call: every tile stands down
+    const int64_t tile = (int64_t)claimed;
     const uint32_t ticket = (uint32_t)(tile * p.nchains + chain);
+    // descriptor banks: this call's (epoch parity) and the idle one
+    const int64_t boff = __builtin_amdgcn_readfirstlane(s_bank) ? p.bank : 0;
+    const int64_t bidle = p.bank - boff;
+    void* const agg = (char*)p.agg + boff;
+    void* const incl = (char*)p.incl + boff;
+    uint64_t* const cnt = p.cnt ? (uint64_t*)((char*)p.cnt + boff) : nullptr;
     const int b = chain / p.nfb;
     const int fb = chain - b * p.nfb;
     const int Qp = p.Qp;
@@ -250,10 +269,16 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
         if (summary_lane) {
 #pragma unroll
             for (int v = 0; v < VEC; ++v) {
-                if (tot.f) Desc<S>::put_incl(p.incl, desc_slot(ticket, Dp, Qp, q, v), tot.H[v]);
-                else Desc<S>::put_agg(p.agg, desc_slot(ticket, Dp, Qp, q, v), tot.A[v], tot.H[v]);
+                if (tot.f) Desc<S>::put_incl(incl, desc_slot(ticket, Dp, Qp, q, v), tot.H[v]);
+                else Desc<S>::put_agg(agg, desc_slot(ticket, Dp, Qp, q, v), tot.A[v], tot.H[v]);
             }
+#pragma unroll
+            for (int v = 0; v < VEC; ++v)
+                Desc<S>::clear((char*)p.agg + bidle, (char*)p.incl + bidle, desc_slot(ticket, Dp, Qp, q, v));
         }
+        // the count word of the idle bank, whether or not this call counts
+        if (p.cnt != nullptr && fb == 0 && lane == 0)
+            ((uint64_t*)((char*)p.cnt + bidle))[tile * (p.nchains / p.nfb) + b] = kEmpty64;
     }
     uint32_t c_before = 0, c_tile = 0;           // begins before this wavefront / in the tile
     if (want_idx) {
@@ -262,17 +287,17 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
             c_tile += sWC[w];
         }
         if (wave == NW - 1 && lane == 0)
-            publish64(p.cnt + tile * B + b, (tile == 0 ? kCountIncl : kCountOwn) | c_tile);
+            publish64(cnt + tile * B + b, (tile == 0 ? kCountIncl : kCountOwn) | c_tile);
         if (wave == 1) {
             const uint32_t before_tile =
-                tile == 0 ? 0u : count_lookback(p.cnt, (tile - 1) * B + b, B, &p.hdr->timeout);
+                tile == 0 ? 0u : count_lookback(cnt, (tile - 1) * B + b, B, &p.hdr->timeout);
             if (lane == 0) sCntBefore = before_tile;
         }
     }
     if (wave == 0) {
         const bool need_carry = !(tile_row0 == 0 || fl_tile0 != 0);
         S carry[VEC];
-        lookback<S, VEC>(p.agg, p.incl, (int64_t)ticket - p.nchains, p.nchains, Dp, Qp, need_carry && active, carry,
+        lookback<S, VEC>(agg, incl, (int64_t)ticket - p.nchains, p.nchains, Dp, Qp, need_carry && active, carry,
                          sLb, &p.hdr->timeout);
         if (j == 0) {
 #pragma unroll
@@ -291,12 +316,12 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     for (int v = 0; v < VEC; ++v) {
         const S c = sCarry[q * VEC + v];
         if (summary_lane && !tot.f)
-            Desc<S>::put_incl(p.incl, desc_slot(ticket, Dp, Qp, q, v), mad(tot.A[v], c, tot.H[v]));
+            Desc<S>::put_incl(incl, desc_slot(ticket, Dp, Qp, q, v), mad(tot.A[v], c, tot.H[v]));
         hv[v] = seg_apply<S, VEC>(pre, v, c);
     }
     if (want_idx) {
         const uint32_t base_cnt = sCntBefore;
-        if (wave == NW - 1 && lane == 0 && tile > 0) publish64(p.cnt + tile * B + b, kCountIncl | (base_cnt + c_tile));
+        if (wave == NW - 1 && lane == 0 && tile > 0) publish64(cnt + tile * B + b, kCountIncl | (base_cnt + c_tile));
         if (q == 0) {
             uint32_t run = base_cnt + c_before + (c_inc - c_own);
 #pragma unroll

@@ -25,7 +25,8 @@
 // look-back that sees no progress for a while computes the awaited tile's
 // aggregate itself from that tile's inputs (a "fallback") and moves on: no
 // wait depends on another workgroup having started, and in the usual
-// in-order dispatch the fallback never runs.
+// in-order dispatch the fallback never runs.  The descriptor words are
+// banked by epoch (see scan_common.hpp); each tile keeps its own epoch word.
 #include "scan_common.hpp"
 #include "kernels.hpp"
 
@@ -203,9 +204,14 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
     __shared__ float s_wA[4], s_wH[4];
     __shared__ int s_wf[4];
     __shared__ float s_carry;
+    __shared__ uint32_t s_bank;               // epoch parity; all ones: stand down
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int64_t ticket = blockIdx.x;
+    // workspace binding: the signature is loaded first, checked after the loads
+    uint64_t sig_seen = 0;
+    uint32_t epoch = 0;
+    if (tid == 0) sig_seen = peek_sig(p.hdr);
     const int64_t j = ticket / p.B;           // tiles counted from the tape's end
     const int64_t b = ticket - j * p.B;
     const int64_t i = p.nt - 1 - j;           // tile index from the tape's start
@@ -229,6 +235,9 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
             dn[u] = (ok && p.done) ? load_flags<VEC>(p.done + row + t) : 0u;
         }
     }
+    // the tile's epoch, behind its loads (waiting for the epoch word then
+    // leaves them in flight)
+    if (tid == 0) epoch = read_epoch(p.epoch + ticket);
     // the step after this wavefront's run: its begin flag (and value)
     const bool after_in = t_after < T;
     const uint32_t fl_after = after_in ? p.start[row + t_after] : 1u;
@@ -270,7 +279,12 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
         s_wH[w] = W.H;
         s_wf[w] = (int)W.f;
     }
+    if (tid == 0) s_bank = ws_bound_to(p.hdr, p.sig, sig_seen, ticket == 0) ? (epoch & 1u) : kEmpty32;
     __syncthreads();
+    const uint32_t bank = __builtin_amdgcn_readfirstlane(s_bank);
+    if (bank == kEmpty32) return;             // workspace bound to another call: every tile stands down
+    uint64_t* const agg = (uint64_t*)((char*)p.agg + (bank ? p.bank : 0));
+    uint64_t* const incl = (uint64_t*)((char*)p.incl + (bank ? p.bank : 0));
     RMap Wt[4];
 #pragma unroll
     for (int ww = 0; ww < 4; ++ww) Wt[ww] = RMap{s_wA[ww], s_wH[ww], s_wf[ww] != 0};
@@ -283,9 +297,13 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
     // the right); wavefront 0 polls, so no wavefront both stores and polls.
     if (w == 3 && lane == 0) {
         if (TM.f)
-            publish64(p.incl + slot, pack2(TM.H, 0.0f));
+            publish64(incl + slot, pack2(TM.H, 0.0f));
         else
-            publish64(p.agg + slot, pack2(TM.H, TM.A));
+            publish64(agg + slot, pack2(TM.H, TM.A));
+        // this tile's words of the idle bank, for the next call
+        const int64_t idle = bank ? 0 : p.bank;
+        ((uint64_t*)((char*)p.agg + idle))[slot] = kEmpty64;
+        ((uint64_t*)((char*)p.incl + idle))[slot] = kEmpty64;
     }
     if (w == 0) {
         // a carry is needed unless the tile's last step ends an episode
@@ -300,8 +318,8 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
                 const int64_t pj = base - lane;
                 uint64_t wi = pack2(0.0f, 0.0f), wa = kEmpty64;
                 if (pj >= 0) {
-                    wi = peek64(p.incl + b * p.nt + pj);
-                    if (wi == kEmpty64) wa = peek64(p.agg + b * p.nt + pj);
+                    wi = peek64(incl + b * p.nt + pj);
+                    if (wi == kEmpty64) wa = peek64(agg + b * p.nt + pj);
                 }
                 const bool term = wi != kEmpty64;
                 const bool ready = term || wa != kEmpty64;
@@ -338,7 +356,7 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
                 }
             }
         }
-        if (!TM.f && lane == 0) publish64(p.incl + slot, pack2(rmap_apply(TM, carry), 0.0f));
+        if (!TM.f && lane == 0) publish64(incl + slot, pack2(rmap_apply(TM, carry), 0.0f));
         if (lane == 0) s_carry = carry;
     }
     __syncthreads();
@@ -372,6 +390,7 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
         }
         c = rmap_apply(Bm[u], c);
     }
+    if (tid == 0) write_epoch(p.epoch + ticket, epoch);
 }
 
 hipError_t disc_launch(bool vec, bool gae, const DiscArgs& a, int64_t ntiles, hipStream_t s) {

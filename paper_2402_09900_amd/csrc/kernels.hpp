@@ -45,12 +45,16 @@ struct DiagFwdArgs {
     int32_t nfb;       // feature blocks per tape
     int32_t nchains;   // tapes * feature blocks
     int32_t pad0;
+    int64_t nt;        // tiles per chain
+    // descriptor words, bank 0 (bank 1 lies `bank` bytes further on)
     void* agg;         // [tiles][Dp] aggregate descriptor words
     void* incl;        // [tiles][Dp] inclusive-prefix descriptor words
+    uint64_t* cnt;     // [tiles per chain][B] begin-count descriptor words, or NULL
+    int64_t bank;
     WsHeader* hdr;
+    uint64_t sig;      // signature of the call (workspace binding)
     uint32_t* ctr;     // per-chain tile counters, kCtrStride words apart
     int32_t* idx;      // episode index out [B][T], or NULL
-    uint64_t* cnt;     // [tiles per chain][B] begin-count descriptor words
     // FFM aggregator (complex state, d = m * c): a[j*c + k] =
     // exp(-|alpha_j| + i omega_k) is generated in the kernel and x is real
     // [B][T][m], broadcast over the c columns
@@ -68,7 +72,8 @@ struct DiagBwdArgs {
     void* da;          // per-step da, or NULL
     void* da_part;     // time-invariant a: [tiles per chain * B][d] partial sums
     void* da_out;      // time-invariant a with one tape: da [d], summed in the kernel from
-                       // partial words [tiles per chain][d] (64-bit, self-validating) in da_part
+                       // partial words [tiles per chain][d] (64-bit, self-validating, banked
+                       // like the descriptors) in da_part
     int64_t T;
     int64_t d;
     int64_t nt;        // tiles per chain
@@ -76,9 +81,11 @@ struct DiagBwdArgs {
     int32_t nfb;
     int32_t nchains;
     int32_t pad0;
-    void* agg;
+    void* agg;         // bank 0, as in DiagFwdArgs
     void* incl;
+    int64_t bank;
     WsHeader* hdr;
+    uint64_t sig;
     uint32_t* ctr;     // per-chain tile counters, kCtrStride words apart
     // FFM aggregator gradient: a generated from alpha, omega (as in the
     // forward pass); dx is reduced over the c columns of each row j into the
@@ -102,16 +109,13 @@ hipError_t diag_bwd_launch(int kind, bool vec, bool ainv, const DiagBwdArgs& arg
 // fixed order (rpw: rows per wavefront).
 hipError_t colsum_launch(const float* in, float* out, int64_t rows, int64_t cols, int64_t rpw, hipStream_t s);
 
-// Fill `bytes` (multiple of 16, 16-byte aligned) at p with 0xFF, and zero the
-// 256-byte header at hdr.  A kernel, not hipMemsetAsync, so that a caller may
-// capture the call in a HIP graph.
 // Per-chain tile counters sit 128 bytes apart: atomics on one cache line
 // serialise (about 11 ns each on MI355X), atomics on distinct lines do not.
 constexpr int kCtrStride = 32;
 
-// Workspace set-up: zero `zero_bytes` from `zero` (header, counters) and fill
-// `ones_bytes` from `ones` with all-ones bytes (empty descriptors); both
-// sizes multiples of 16.
+// Zero `zero_bytes` from `zero` and fill `ones_bytes` from `ones` with
+// all-ones bytes; both sizes multiples of 16.  A kernel, not
+// hipMemsetAsync, so that a caller may capture the call in a HIP graph.
 hipError_t ws_init_launch(void* zero, size_t zero_bytes, void* ones, size_t ones_bytes, hipStream_t s);
 hipError_t store_i64_launch(int64_t* p, int64_t v, hipStream_t s);
 
@@ -129,9 +133,7 @@ struct LinSummaryArgs {
     uint8_t* R;         // [chunks] chunk holds a begin step
     int64_t T;
     int64_t H;
-    u32x4* zero;        // state-scan header and counters, zeroed here (16-byte units)
-    int64_t zero16;
-    u32x4* fill;        // descriptors to fill with all-ones bytes (16-byte units)
+    u32x4* fill;        // state-scan workspace to prepare (all-ones bytes, 16-byte units)
     int64_t fill16;
 };
 
@@ -169,9 +171,7 @@ struct LinBwdArgs {
     float* dk;
     float* dv;
     int64_t T, H, nch;
-    u32x4* zero;        // reverse-scan workspace to zero (header, counters), 16-byte units
-    int64_t zero16;
-    u32x4* fill;        // reverse-scan descriptors to fill with all-ones bytes
+    u32x4* fill;        // reverse-scan workspace to prepare (all-ones bytes)
     int64_t fill16;
 };
 
@@ -194,9 +194,12 @@ struct DiscArgs {
     float gamma;             // discount of the TD error (advantage only)
     int64_t T, nt, B;        // tape length, tiles per tape, tapes
     uint32_t fallback_polls; // polls without progress before a look-back computes the awaited tile itself
-    uint64_t* agg;           // [B][nt] tile aggregates
-    uint64_t* incl;          // [B][nt] tile values at their first step
+    uint64_t* agg;           // [B][nt] tile aggregates (bank 0)
+    uint64_t* incl;          // [B][nt] tile values at their first step (bank 0)
+    int64_t bank;            // bytes from bank 0 to bank 1
     WsHeader* hdr;
+    uint64_t sig;
+    uint32_t* epoch;         // [B][nt] per-tile epoch words
 };
 
 hipError_t disc_launch(bool vec, bool gae, const DiscArgs& a, int64_t ntiles, hipStream_t s);
@@ -212,7 +215,11 @@ struct TbbBeginArgs {
     int64_t offset;          // added to every index
     int64_t* indices;        // out, room for n
     int64_t* count;          // out, one value (may be NULL)
-    uint64_t* cnt;           // [tiles] count descriptor words
+    uint64_t* cnt;           // [tiles] count descriptor words (bank 0)
+    int64_t bank;            // bytes from bank 0 to bank 1
+    WsHeader* hdr;
+    uint64_t sig;
+    uint32_t* epoch;         // [tiles] per-tile epoch words
     uint32_t fallback_polls;
 };
 

@@ -40,15 +40,12 @@ __global__ __launch_bounds__(256) void linattn_summary_kernel(LinSummaryArgs p) 
     const int64_t t0 = c * kC;
     const int nvalid = (int)(p.T - t0 < kC ? p.T - t0 : kC);
 
-    // workspace of the state scan and of the episode-index count words: the
-    // header and tile counters are zeroed and the descriptors filled with
-    // all-ones bytes here,
-    // so that the later kernels find them initialised (stream order)
+    // workspace of the state scan and the episode-index count words are
+    // prepared (all-ones bytes) here, so that the later kernels find them
+    // ready (stream order)
     {
         const int64_t nblk = (int64_t)gridDim.x * gridDim.y;
         const int64_t gid = (int64_t)(blockIdx.y * gridDim.x + blockIdx.x) * 256 + threadIdx.x;
-        const u32x4 zeros = {0u, 0u, 0u, 0u};
-        for (int64_t i = gid; i < p.zero16; i += nblk * 256) p.zero[i] = zeros;
         const u32x4 ones = {kEmpty32, kEmpty32, kEmpty32, kEmpty32};
         for (int64_t i = gid; i < p.fill16; i += nblk * 256) p.fill[i] = ones;
     }

@@ -98,11 +98,9 @@ __global__ __launch_bounds__(256) void linattn_bwd_summary_kernel(LinBwdArgs p) 
     const int nvalid = (int)(p.T - t0 < kC ? p.T - t0 : kC);
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
 
-    {   // reverse-scan workspace: header and counters zeroed, descriptors all-ones
+    {   // reverse-scan workspace prepared: all-ones bytes
         const int64_t nblk = (int64_t)gridDim.x * gridDim.y;
         const int64_t gid = (int64_t)(blockIdx.y * gridDim.x + blockIdx.x) * 256 + tid;
-        const u32x4 zeros = {0u, 0u, 0u, 0u};
-        for (int64_t i = gid; i < p.zero16; i += nblk * 256) p.zero[i] = zeros;
         const u32x4 ones = {kEmpty32, kEmpty32, kEmpty32, kEmpty32};
         for (int64_t i = gid; i < p.fill16; i += nblk * 256) p.fill[i] = ones;
     }

@@ -258,11 +258,19 @@ template <int VEC> struct Codec<K_C64, VEC> {
 // ------------------------------------------------------- descriptor words
 // Cross-tile communication of the single-pass scan.  Every word is written
 // once per call with a relaxed agent-scope atomic store and read with relaxed
-// agent-scope atomic loads, and validates itself: the workspace is filled with
-// all-ones bytes before the scan, and a published value never has that bit
-// pattern because every float is canonicalised (any NaN becomes 0x7FC00000)
-// before it is stored.  No fence is needed: a reader that sees a valid word
-// sees the whole value, and no other memory is ordered against it.
+// agent-scope atomic loads, and validates itself: an unpublished word holds
+// all-ones bytes, and a published value never has that bit pattern because
+// every float is canonicalised (any NaN becomes 0x7FC00000) before it is
+// stored.  No fence is needed: a reader that sees a valid word sees the whole
+// value, and no other memory is ordered against it.
+//
+// The words live in two banks.  A call publishes into the bank of its epoch's
+// parity and every tile resets its own words of the other bank to all ones,
+// so the next call (epoch + 1) finds its bank clean without any fill pass:
+// a prepared workspace (all ones) stays ready from call to call.  The epoch
+// comes from the tile counters, which are never reset: a call takes exactly
+// n tickets from a counter that hands out n per call, so ticket / n is the
+// number of calls before it.
 
 constexpr uint32_t kEmpty32 = 0xFFFFFFFFu;
 constexpr uint64_t kEmpty64 = 0xFFFFFFFFFFFFFFFFull;
@@ -325,6 +333,12 @@ template <> struct Desc<float> {
         H = __uint_as_float(w);
         return w != kEmpty32;
     }
+    // back to unpublished (words of the idle bank; plain stores, read only
+    // after the kernel has ended)
+    __device__ static void clear(void* agg, void* incl, int64_t i) {
+        ((uint64_t*)agg)[i] = kEmpty64;
+        ((uint32_t*)incl)[i] = kEmpty32;
+    }
 };
 
 template <> struct Desc<cf> {
@@ -349,6 +363,11 @@ template <> struct Desc<cf> {
         H = cf{unpack_lo(w), unpack_hi(w)};
         return w != kEmpty64;
     }
+    __device__ static void clear(void* agg, void* incl, int64_t i) {
+        ((uint64_t*)agg)[2 * i] = kEmpty64;
+        ((uint64_t*)agg)[2 * i + 1] = kEmpty64;
+        ((uint64_t*)incl)[i] = kEmpty64;
+    }
 };
 
 // Descriptor slot of feature v of lane q inside tile `ticket`'s block of Dp
@@ -365,6 +384,12 @@ __device__ __forceinline__ int64_t desc_slot(int64_t ticket, int Dp, int Qp, int
 // ticketed tile order guarantees every awaited tile is running or done, so
 // the bound only matters if that guarantee were broken.
 constexpr uint32_t kMaxPolls = 1u << 22;
+
+// The header's timeout word reads all ones until a wait gives up.
+constexpr uint32_t kTimedOut = 0u;
+__device__ __forceinline__ void flag_timeout(uint32_t* timeout) {
+    __hip_atomic_store(timeout, kTimedOut, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 // ------------------------------------------------------------- look-back
 // Carry-in of a tile: the chain's state just before the tile, found by
@@ -457,7 +482,7 @@ __device__ __forceinline__ void lookback(const void* agg, const void* incl, int6
                 done = true;
             } else if (consumed == 0) {
                 if (++polls > kMaxPolls) {
-                    __hip_atomic_store(timeout, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    flag_timeout(timeout);
                     done = true;
                 } else {
                     __builtin_amdgcn_s_sleep(1);
@@ -592,7 +617,7 @@ __device__ __forceinline__ uint32_t count_lookback(const uint64_t* desc, int64_t
         base -= (int64_t)first_empty * stride;
         if (first_empty == 0) {
             if (++polls > kMaxPolls) {
-                __hip_atomic_store(timeout, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                flag_timeout(timeout);
                 return acc;
             }
             __builtin_amdgcn_s_sleep(1);
@@ -600,11 +625,78 @@ __device__ __forceinline__ uint32_t count_lookback(const uint64_t* desc, int64_t
     }
 }
 
-// Workspace header shared by the scan kernels (first 256 bytes).
+// Workspace header shared by the scan kernels (first 256 bytes).  Prepared
+// state: all ones.
 struct WsHeader {
-    uint32_t reserved;   // zero
-    uint32_t timeout;    // nonzero: some wait gave up
-    uint32_t pad[62];
+    uint32_t reserved;
+    uint32_t timeout;    // kTimedOut: some wait gave up
+    uint64_t sig;        // signature of the call the workspace is bound to
+    uint32_t pad[60];
 };
+
+// Signature word: all ones = not bound yet; kSigPoisoned = a call with
+// another signature found the workspace (it must be prepared again).
+constexpr uint64_t kSigPoisoned = 0ull;
+
+// The signature word as a tile reads it: a cacheable load (workgroup
+// scope), so that thousands of tiles reading the one word are served by the
+// caches instead of queueing at one memory channel.  Within a call the word
+// only changes from all ones to the call's own signature, or to
+// kSigPoisoned in a call that finds a foreign signature (whose tiles all
+// stand down whichever of the values they see); between calls the kernel
+// boundary makes the last value visible.
+__device__ __forceinline__ uint64_t peek_sig(const WsHeader* hdr) {
+    // one aligned 8-byte raw buffer load (never torn): an ordinary cached
+    // load, which the compiler need not order after the counter atomic
+    // issued just before it
+    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+    const Rsrc r = make_rsrc(hdr, sizeof(WsHeader));
+    const u32x2 w = __builtin_amdgcn_raw_buffer_load_b64(r, (int)offsetof(WsHeader, sig), 0, 0);
+    return (uint64_t)w.x | ((uint64_t)w.y << 32);
+}
+
+// Binding check of a tile (one thread), given the signature word it read
+// (`w`, loaded beside the tile's counter atomic so that the check costs no
+// extra round trip): a fresh workspace is bound to the first call's
+// signature (written by one designated tile of that call); a call with
+// another signature poisons it and all of its tiles stand down (every tile
+// of that call sees a foreign or poisoned signature, so they agree).
+__device__ __forceinline__ bool ws_bound_to(WsHeader* hdr, uint64_t sig, uint64_t w, bool designated) {
+    if (w == sig) return true;
+    if (w == kEmpty64) {
+        if (designated) publish64(&hdr->sig, sig);
+        return true;
+    }
+    publish64(&hdr->sig, kSigPoisoned);
+    return false;
+}
+
+// Ticket of a tile from a counter that is never reset: a wrapping atomic
+// increment (new = old >= 2n - 1 ? 0 : old + 1, n tickets per call) cycles
+// the counter through 0 .. 2n - 1, two calls per cycle, starting from the
+// prepared value (all ones wraps to 0).  new < n: position new in an
+// even-epoch call (bank 0); otherwise position new - n in an odd one
+// (bank 1).  No division and no reset.
+struct Claim {
+    uint32_t pos;
+    uint32_t bank;
+};
+__device__ __forceinline__ uint32_t take_ticket(uint32_t* ctr, uint32_t per_call) {
+    const uint32_t top = 2u * per_call - 1u;
+    const uint32_t old = __builtin_amdgcn_atomic_inc32(ctr, top, __ATOMIC_RELAXED, "agent");
+    return old >= top ? 0u : old + 1u;
+}
+__device__ __forceinline__ Claim claim_of(uint32_t t, uint32_t per_call) {
+    return t < per_call ? Claim{t, 0u} : Claim{t - per_call, 1u};
+}
+
+// Epoch of a tile that is ordered by its workgroup index: every tile owns
+// one 32-bit epoch word, reads it (plus one: this call's epoch, the prepared
+// value all ones reading as epoch 0) and stores the new value back at its
+// end, where no later wait of the storing wavefront covers the store.  Only
+// the owner touches the word and calls are ordered by the stream, so plain
+// accesses suffice and nothing is contended.
+__device__ __forceinline__ uint32_t read_epoch(const uint32_t* word) { return *word + 1u; }
+__device__ __forceinline__ void write_epoch(uint32_t* word, uint32_t e) { *word = e; }
 
 }  // namespace memoroid

@@ -5,9 +5,10 @@
 // flags.  One pass: a tile (256 lanes x 64 flags) counts its begin steps,
 // publishes the count at once, finds the count before it with a look-back
 // over earlier tiles and writes its indices.  Tiles are ordered by workgroup
-// index, with no ticket counter; a look-back that sees no progress counts
-// the awaited tile's flags itself (a fallback), so no wait depends on
-// another workgroup having started.
+// index; a look-back that sees no progress counts the awaited tile's flags
+// itself (a fallback), so no wait depends on another workgroup having
+// started.  The count words are banked by epoch (see scan_common.hpp);
+// each tile keeps its own epoch word.
 //
 // Sampling concatenates the drawn episodes D[I[i] : I[i+1]] and cuts the
 // batch to B rows.  Three kernels: episode lengths with block-local
@@ -66,16 +67,26 @@ template <bool VEC>
 __global__ __launch_bounds__(256) void tbb_begins_kernel(TbbBeginArgs p) {
     __shared__ uint32_t s_wave[4];
     __shared__ uint32_t s_before;
+    __shared__ uint32_t s_bank;               // epoch parity; all ones: stand down
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int64_t tile = blockIdx.x;
+    // workspace binding and epoch, as in the discounted-return kernel
+    uint64_t sig_seen = 0;
+    uint32_t epoch = 0;
+    if (tid == 0) sig_seen = peek_sig(p.hdr);
     const int64_t t0 = tile * kIdxTile;
     const Rsrc rs = make_rsrc(p.start + t0, p.n - t0);
     const uint32_t loff = (uint32_t)(tid * kFlagsPerLane);
     const uint64_t mask = lane_begin_mask<VEC>(rs, loff);
+    if (tid == 0) epoch = read_epoch(p.epoch + tile);
     const uint32_t mine = (uint32_t)__builtin_popcountll(mask);
     const uint32_t incl = wave_incl_sum(mine);
     if (lane == 63) s_wave[w] = incl;
+    if (tid == 0) s_bank = ws_bound_to(p.hdr, p.sig, sig_seen, tile == 0) ? (epoch & 1u) : kEmpty32;
     __syncthreads();
+    const uint32_t bank = __builtin_amdgcn_readfirstlane(s_bank);
+    if (bank == kEmpty32) return;             // workspace bound to another call: every tile stands down
+    uint64_t* const cnt = (uint64_t*)((char*)p.cnt + (bank ? p.bank : 0));
     const uint32_t own = s_wave[0] + s_wave[1] + s_wave[2] + s_wave[3];
     uint32_t before_wave = 0;
 #pragma unroll
@@ -84,7 +95,10 @@ __global__ __launch_bounds__(256) void tbb_begins_kernel(TbbBeginArgs p) {
 
     // wavefront 3 publishes the tile's own count (inclusive for tile 0);
     // wavefront 0 looks back (publishing and polling use different waves)
-    if (w == 3 && lane == 0) publish64(p.cnt + tile, (tile == 0 ? kCountIncl : kCountOwn) | own);
+    if (w == 3 && lane == 0) {
+        publish64(cnt + tile, (tile == 0 ? kCountIncl : kCountOwn) | own);
+        ((uint64_t*)((char*)p.cnt + (bank ? 0 : p.bank)))[tile] = kEmpty64;   // idle bank, next call
+    }
     if (w == 0) {
         uint32_t acc = 0;
         if (tile > 0) {
@@ -92,7 +106,7 @@ __global__ __launch_bounds__(256) void tbb_begins_kernel(TbbBeginArgs p) {
             uint32_t polls = 0;
             while (true) {
                 const int64_t i = base - lane;
-                const uint64_t word = i >= 0 ? peek64(p.cnt + i) : kCountIncl;
+                const uint64_t word = i >= 0 ? peek64(cnt + i) : kCountIncl;
                 const bool empty = word == kEmpty64;
                 const bool inc = !empty && (word & kCountIncl) != 0;
                 const uint64_t m_empty = __ballot(empty), m_incl = __ballot(inc);
@@ -122,7 +136,7 @@ __global__ __launch_bounds__(256) void tbb_begins_kernel(TbbBeginArgs p) {
                     __builtin_amdgcn_s_sleep(1);
                 }
             }
-            if (lane == 0) publish64(p.cnt + tile, kCountIncl | (acc + own));
+            if (lane == 0) publish64(cnt + tile, kCountIncl | (acc + own));
         }
         if (lane == 0) {
             s_before = acc;
@@ -137,6 +151,7 @@ __global__ __launch_bounds__(256) void tbb_begins_kernel(TbbBeginArgs p) {
         p.indices[k++] = p.offset + t0 + loff + b;
         m &= m - 1;
     }
+    if (tid == 0) write_epoch(p.epoch + tile, epoch);
 }
 
 hipError_t tbb_begins_launch(bool vec, const TbbBeginArgs& a, int64_t ntiles, hipStream_t s) {

@@ -36,10 +36,29 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert mb.memoroid_abi_version() == 1
-    for s in (mb.OK, mb.EINVAL, mb.EUNSUPPORTED, mb.EWORKSPACE, mb.EHIP, mb.ETIMEOUT):
+    assert mb.memoroid_abi_version() == 2
+    for s in (mb.OK, mb.EINVAL, mb.EUNSUPPORTED, mb.EWORKSPACE, mb.EHIP, mb.ETIMEOUT, mb.EMISMATCH):
         assert mb.status_string(s) and mb.status_string(s) != "unknown status"
     assert mb.status_string(12345) == "unknown status"
+
+
+def test_workspace_prepare_validation():
+    # argument errors are found before any HIP call
+    assert mb.memoroid_workspace_prepare(None, 4096, None) == mb.EINVAL
+    assert mb.memoroid_workspace_prepare(W, 255, None) == mb.EINVAL        # smaller than the header
+    assert mb.memoroid_workspace_prepare(W + 8, 4096, None) == mb.EINVAL   # not 16-byte aligned
+    assert mb.memoroid_workspace_status(None, 4096, None) == mb.EINVAL
+
+
+def test_prepared_workspaces_hold_two_banks():
+    """The prepared entry points keep two banks of descriptor words, so their
+    workspaces grow with the tile count roughly twice as fast as one bank
+    would."""
+    small = mb.memoroid_scan_diag_workspace_bytes(1, 1 << 16, 256, mb.C64, mb.C64)
+    large = mb.memoroid_scan_diag_workspace_bytes(1, 1 << 20, 256, mb.C64, mb.C64)
+    # 16x the tiles: 16 (tiles per chain) * 16 chains * 16 features * 24 bytes per bank
+    per_tile_pair = (large - small) / ((1 << 20) - (1 << 16)) * 512
+    assert per_tile_pair >= 2 * 16 * 16 * 24 * 0.99
 
 
 def test_workspace_queries():

@@ -56,6 +56,7 @@ def test_misaligned_output_takes_scalar_kernel():
     n = f.B * f.T * f.m * f.c
     big = torch.empty(n + 1, dtype=torch.complex64, device=DEV)
     ws = torch.empty(mb.memoroid_scan_ffm_workspace_bytes(f.B, f.T, f.m, f.c), dtype=torch.uint8, device=DEV)
+    assert mb.memoroid_workspace_prepare(ws.data_ptr(), ws.numel(), torch.cuda.current_stream().cuda_stream) == mb.OK
     S = big[1:]
     al, om, x, s = dev(f.alpha), dev(f.omega), dev(f.x), dev(f.start)     # held until the kernel has run
     st = mb.memoroid_scan_ffm(al.data_ptr(), om.data_ptr(), x.data_ptr(), s.data_ptr(), S.data_ptr(), None,

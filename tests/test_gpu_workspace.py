@@ -1,0 +1,227 @@
+"""The prepared-workspace protocol of the single-kernel entry points, through
+the C ABI: one preparation, then many calls with the same sizes and no
+initialisation in between (the descriptor words alternate between two banks
+from call to call, so four calls use each bank twice); a workspace shared by
+the discounted return and GAE; a call with other sizes on a bound workspace
+(stands down and reports MEMOROID_EMISMATCH); memory that was never prepared.
+Every result is compared with the fp64 oracle (conditioned relative error,
+1e-4 for fp32 arithmetic; indices bit-exact)."""
+import numpy as np
+import pytest
+
+import oracle
+from conftest import announce, cond_err
+from paper_2402_09900_amd import tapes
+
+torch = pytest.importorskip("torch")
+from paper_2402_09900_amd import binding as mb  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+TOL = 1e-4
+CALLS = 4
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def prepared(nbytes):
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=DEV)
+    assert mb.memoroid_workspace_prepare(ws.data_ptr(), ws.numel(), stream()) == mb.OK
+    return ws
+
+
+def status(ws):
+    return mb.memoroid_workspace_status(ws.data_ptr(), ws.numel(), stream())
+
+
+def diag_call(w, ws, idx=None):
+    code = {"f32": mb.F32, "c64": mb.C64}[w.dtype]
+    a, x, s = dev(w.a), dev(w.x), dev(w.start)
+    h = torch.empty((w.B, w.T, w.d), dtype=x.dtype, device=DEV)
+    st = mb.memoroid_scan_diag(a.data_ptr(), 0 if w.a_invariant else w.d, x.data_ptr(), s.data_ptr(), h.data_ptr(),
+                               idx.data_ptr() if idx is not None else None, w.B, w.T, w.d, code, code,
+                               ws.data_ptr(), ws.numel(), stream())
+    assert st == mb.OK
+    torch.cuda.synchronize()
+    return h.cpu().numpy()
+
+
+@pytest.mark.parametrize("dtype,a_inv,B,T,d", [("f32", False, 2, 3000, 40), ("c64", True, 1, 20000, 64),
+                                              ("f32", True, 3, 1500, 7)])
+def test_diag_forward_repeated_calls(dtype, a_inv, B, T, d):
+    nb = mb.memoroid_scan_diag_workspace_bytes(B, T, d, {"f32": mb.F32, "c64": mb.C64}[dtype],
+                                               {"f32": mb.F32, "c64": mb.C64}[dtype])
+    ws = prepared(nb)
+    for call in range(CALLS):
+        w = tapes.make_custom_diag(dtype, B, T, d, a_inv, seed=500 + call, with_grad=False)
+        announce("workspace diag fwd %s B=%d T=%d d=%d call %d" % (dtype, B, T, d, call))
+        idx = torch.empty((B, T), dtype=torch.int32, device=DEV) if call % 2 == 0 else None
+        got = diag_call(w, ws, idx)
+        ref, m = oracle.diag_fwd(w.a, w.x, w.start)
+        assert cond_err(got, ref, m) <= TOL, call
+        if idx is not None:
+            np.testing.assert_array_equal(idx.cpu().numpy(), oracle.episode_idx(w.start))
+    assert status(ws) == mb.OK
+
+
+@pytest.mark.parametrize("dtype,a_inv,B,T,d", [("c64", True, 1, 20000, 64), ("f32", False, 2, 3000, 40),
+                                              ("f32", True, 3, 2000, 12)])
+def test_diag_reverse_repeated_calls(dtype, a_inv, B, T, d):
+    code = {"f32": mb.F32, "c64": mb.C64}[dtype]
+    ws = prepared(mb.memoroid_scan_diag_bwd_workspace_bytes(B, T, d, code, 0 if a_inv else d))
+    for call in range(CALLS):
+        w = tapes.make_custom_diag(dtype, B, T, d, a_inv, seed=600 + call)
+        announce("workspace diag bwd %s B=%d T=%d d=%d call %d" % (dtype, B, T, d, call))
+        h, _ = oracle.diag_fwd(w.a, w.x, w.start)
+        h32 = h.astype(w.x.dtype)
+        a, s, hd, g = dev(w.a), dev(w.start), dev(h32), dev(w.g)
+        gx = torch.empty_like(g)
+        ga = torch.empty((d,) if a_inv else (B, T, d), dtype=g.dtype, device=DEV)
+        st = mb.memoroid_scan_diag_bwd(a.data_ptr(), 0 if a_inv else d, s.data_ptr(), hd.data_ptr(), g.data_ptr(),
+                                       gx.data_ptr(), ga.data_ptr(), B, T, d, code, ws.data_ptr(), ws.numel(),
+                                       stream())
+        assert st == mb.OK
+        torch.cuda.synchronize()
+        dx, da, mdx, mda = oracle.diag_bwd(w.a, w.start, h32, w.g)
+        assert cond_err(gx.cpu().numpy(), dx, mdx) <= TOL, call
+        assert cond_err(ga.cpu().numpy(), da, mda) <= TOL, call
+    assert status(ws) == mb.OK
+
+
+def test_ffm_forward_and_gradient_repeated_calls():
+    B, T, m, c = 1, 9000, 8, 4
+    wsf = prepared(mb.memoroid_scan_ffm_workspace_bytes(B, T, m, c))
+    wsb = prepared(mb.memoroid_scan_ffm_bwd_workspace_bytes(B, T, m, c))
+    for call in range(CALLS):
+        f = tapes.make_ffm(7, seed=700 + call, B=B, T=T, m=m, c=c)
+        announce("workspace ffm call %d" % call)
+        al, om, x, s = dev(f.alpha), dev(f.omega), dev(f.x), dev(f.start)
+        S = torch.empty((B, T, m, c), dtype=torch.complex64, device=DEV)
+        assert mb.memoroid_scan_ffm(al.data_ptr(), om.data_ptr(), x.data_ptr(), s.data_ptr(), S.data_ptr(), None,
+                                    B, T, m, c, wsf.data_ptr(), wsf.numel(), stream()) == mb.OK
+        rng = np.random.Generator(np.random.PCG64(800 + call))
+        G = (rng.standard_normal((B, T, m, c), dtype=np.float32)
+             + 1j * rng.standard_normal((B, T, m, c), dtype=np.float32)).astype(np.complex64)
+        Gd = dev(G)
+        gx = torch.empty((B, T, m), dtype=torch.float32, device=DEV)
+        ga = torch.empty(m, dtype=torch.float32, device=DEV)
+        gw = torch.empty(c, dtype=torch.float32, device=DEV)
+        assert mb.memoroid_scan_ffm_bwd(al.data_ptr(), om.data_ptr(), s.data_ptr(), S.data_ptr(), Gd.data_ptr(),
+                                        gx.data_ptr(), ga.data_ptr(), gw.data_ptr(), B, T, m, c, wsb.data_ptr(),
+                                        wsb.numel(), stream()) == mb.OK
+        torch.cuda.synchronize()
+        ref, mag = oracle.ffm(f.alpha.astype(np.float64), f.omega.astype(np.float64), f.x.astype(np.float64),
+                              f.start)
+        Sg = S.cpu().numpy()
+        assert cond_err(Sg, ref, mag) <= TOL, call
+        rdx, rda, rdw, mdx, mda, mdw = oracle.ffm_bwd(f.alpha.astype(np.float64), f.omega.astype(np.float64),
+                                                      f.start, Sg.astype(np.complex128), G.astype(np.complex128))
+        assert cond_err(gx.cpu().numpy(), rdx, mdx) <= TOL, call
+        assert cond_err(ga.cpu().numpy(), rda, mda) <= TOL, call
+        assert cond_err(gw.cpu().numpy(), rdw, mdw) <= TOL, call
+    assert status(wsf) == mb.OK and status(wsb) == mb.OK
+
+
+def test_return_and_gae_share_a_prepared_workspace():
+    B, T = 2, 70000
+    ws = prepared(mb.memoroid_discount_workspace_bytes(B, T))
+    for call in range(CALLS):
+        tp = tapes.make_discount(6, seed=900 + call, B=B, T=T)
+        r, v, vn, dn, s = dev(tp.r), dev(tp.v), dev(tp.vn), dev(tp.done), dev(tp.start)
+        out = torch.empty((B, T), dtype=torch.float32, device=DEV)
+        if call % 2 == 0:
+            announce("workspace return call %d" % call)
+            assert mb.memoroid_discounted_return(r.data_ptr(), s.data_ptr(), 0.97, out.data_ptr(), B, T,
+                                                 ws.data_ptr(), ws.numel(), stream()) == mb.OK
+            ref, m = oracle.discounted_return(tp.r.astype(np.float64), tp.start, float(np.float32(0.97)))
+        else:
+            announce("workspace gae call %d" % call)
+            assert mb.memoroid_gae(r.data_ptr(), v.data_ptr(), vn.data_ptr(), dn.data_ptr(), s.data_ptr(), 0.99,
+                                   0.95, out.data_ptr(), None, B, T, ws.data_ptr(), ws.numel(),
+                                   stream()) == mb.OK
+            ref, _, m, _ = oracle.gae(tp.r.astype(np.float64), tp.v.astype(np.float64), tp.start,
+                                      float(np.float32(0.99)), float(np.float32(0.95)),
+                                      vn=tp.vn.astype(np.float64), done=tp.done)
+        torch.cuda.synchronize()
+        assert cond_err(out.cpu().numpy(), ref, m) <= TOL, call
+    assert status(ws) == mb.OK
+
+
+def test_begin_indices_repeated_calls():
+    n = 300000
+    ws = prepared(mb.memoroid_tbb_begin_indices_workspace_bytes(n))
+    for call in range(CALLS):
+        rng = np.random.Generator(np.random.PCG64(1000 + call))
+        flags = (rng.random(n) < 0.01).astype(np.uint8)
+        announce("workspace begin indices call %d" % call)
+        s = dev(flags)
+        idx = torch.empty(n, dtype=torch.int64, device=DEV)
+        cnt = torch.empty(1, dtype=torch.int64, device=DEV)
+        assert mb.memoroid_tbb_begin_indices(s.data_ptr(), n, 5, idx.data_ptr(), cnt.data_ptr(), ws.data_ptr(),
+                                             ws.numel(), stream()) == mb.OK
+        torch.cuda.synchronize()
+        ref = oracle.tbb_begin_indices(flags, 5)
+        k = int(cnt.item())
+        assert k == ref.size
+        np.testing.assert_array_equal(idx.cpu().numpy()[:k], ref)
+    assert status(ws) == mb.OK
+
+
+def test_other_sizes_on_a_bound_workspace_report_mismatch():
+    """A bound workspace used with other sizes: the call computes nothing and
+    the status says so; after a new preparation the same call is correct."""
+    d = 32
+    nb = max(mb.memoroid_scan_diag_workspace_bytes(1, T, d, mb.F32, mb.F32) for T in (4000, 5000))
+    ws = prepared(nb)
+    w1 = tapes.make_custom_diag("f32", 1, 4000, d, False, seed=1101, with_grad=False)
+    w2 = tapes.make_custom_diag("f32", 1, 5000, d, False, seed=1102, with_grad=False)
+    announce("workspace mismatch: bind T=4000")
+    ref1, m1 = oracle.diag_fwd(w1.a, w1.x, w1.start)
+    assert cond_err(diag_call(w1, ws), ref1, m1) <= TOL
+    assert status(ws) == mb.OK
+    announce("workspace mismatch: T=5000 on the bound workspace")
+    diag_call(w2, ws)
+    assert status(ws) == mb.EMISMATCH
+    announce("workspace mismatch: T=4000 after the mismatch")
+    diag_call(w1, ws)                       # still poisoned: stands down too
+    assert status(ws) == mb.EMISMATCH
+    assert mb.memoroid_workspace_prepare(ws.data_ptr(), ws.numel(), stream()) == mb.OK
+    announce("workspace mismatch: T=5000 after preparing again")
+    ref2, m2 = oracle.diag_fwd(w2.a, w2.x, w2.start)
+    assert cond_err(diag_call(w2, ws), ref2, m2) <= TOL
+    assert status(ws) == mb.OK
+
+
+def test_unprepared_workspace_computes_nothing():
+    """Zeroed memory reads as a poisoned workspace: every tile stands down,
+    the output keeps its previous contents and the status reports it."""
+    w = tapes.make_custom_diag("f32", 1, 3000, 16, True, seed=1201, with_grad=False)
+    ws = torch.zeros(mb.memoroid_scan_diag_workspace_bytes(1, 3000, 16, mb.F32, mb.F32), dtype=torch.uint8,
+                     device=DEV)
+    announce("workspace unprepared")
+    a, x, s = dev(w.a), dev(w.x), dev(w.start)
+    h = torch.full((1, 3000, 16), 7.0, dtype=torch.float32, device=DEV)
+    assert mb.memoroid_scan_diag(a.data_ptr(), 0, x.data_ptr(), s.data_ptr(), h.data_ptr(), None, 1, 3000, 16,
+                                 mb.F32, mb.F32, ws.data_ptr(), ws.numel(), stream()) == mb.OK
+    assert status(ws) == mb.EMISMATCH
+    assert bool((h == 7.0).all())
+
+
+def test_binding_cache_reuses_prepared_workspaces():
+    """The torch layer's cache: repeated calls with one key run one kernel
+    each on the same prepared workspace and stay correct."""
+    w = tapes.make_custom_diag("c64", 2, 5000, 24, False, seed=1301, with_grad=False)
+    ref, m = oracle.diag_fwd(w.a, w.x, w.start)
+    a, x, s = dev(w.a), dev(w.x), dev(w.start)
+    for call in range(CALLS):
+        announce("workspace binding cache call %d" % call)
+        h = mb.scan_diag(a, x, s)
+        torch.cuda.synchronize()
+        assert cond_err(h.cpu().numpy(), ref, m) <= TOL, call
