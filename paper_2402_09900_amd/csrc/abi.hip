@@ -318,13 +318,19 @@ int memoroid_scan_ffm(const float* alpha, const float* omega, const float* x, co
 
 namespace {
 
+// The scan's workspace, then the summed da (complex [m][c]), then the
+// chain-major input gradient [B][nfb][T][Dp / c] (floats).
 bool ffm_bwd_plan(int64_t B, int64_t T, int64_t m, int64_t c, bool vec, bool params, DiagPlan* p,
-                  size_t* off_da, size_t* total) {
+                  size_t* off_da, size_t* off_dxw, size_t* total) {
     int64_t d;
     if (!mul_ok(m, c, &d)) return false;
     if (!plan_diag(B, T, d, MEMOROID_C64, vec, diag_rows(true, true), true, true, params, p)) return false;
     *off_da = align_up(p->total);
-    *total = align_up(*off_da + (size_t)(params ? d : 1) * 8);
+    *off_dxw = align_up(*off_da + (size_t)(params ? d : 1) * 8);
+    const int64_t jpc = c <= p->Dp ? p->Dp / c : 1;
+    int64_t n;
+    if (!mul_ok(B * (int64_t)p->nfb, T, &n) || !mul_ok(n, jpc, &n) || n > INT64_MAX / 8) return false;
+    *total = align_up(*off_dxw + (size_t)n * 4);
     return true;
 }
 
@@ -337,8 +343,8 @@ size_t memoroid_scan_ffm_bwd_workspace_bytes(int64_t B, int64_t T, int64_t m, in
     size_t best = 0;
     for (int vec = 0; vec < 2; ++vec) {
         DiagPlan p;
-        size_t off_da, total;
-        if (!ffm_bwd_plan(B, T, m, c, vec, true, &p, &off_da, &total)) return 0;
+        size_t off_da, off_dxw, total;
+        if (!ffm_bwd_plan(B, T, m, c, vec, true, &p, &off_da, &off_dxw, &total)) return 0;
         if (total > best) best = total;
     }
     return best;
@@ -368,8 +374,8 @@ int memoroid_scan_ffm_bwd(const float* alpha, const float* omega, const uint8_t*
     }
     const bool vec = d % 2 == 0 && aligned(grad_S, 16) && (!S || aligned(S, 16));
     DiagPlan p;
-    size_t off_da, total;
-    if (!ffm_bwd_plan(B, T, m, c, vec, params, &p, &off_da, &total)) return MEMOROID_EUNSUPPORTED;
+    size_t off_da, off_dxw, total;
+    if (!ffm_bwd_plan(B, T, m, c, vec, params, &p, &off_da, &off_dxw, &total)) return MEMOROID_EUNSUPPORTED;
     // the real input's gradient is reduced over the c columns inside the
     // kernel: c must be a power of two that divides the chain width
     if (!pow2(c) || c > p.Dp) return MEMOROID_EUNSUPPORTED;
@@ -396,19 +402,28 @@ int memoroid_scan_ffm_bwd(const float* alpha, const float* omega, const uint8_t*
     args.omega = omega;
     args.ffm_m = m;
     args.ffm_c = c;
-    args.dxr = grad_x;
+    args.dxr = (float*)(ws + off_dxw);
     if (ffm_bwd_launch(vec, args, p.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
-    if (params) {
-        float* da = (float*)(ws + off_da);
-        if (!p.fused_da) {
-            const int st = reduce_rows((const float*)(ws + p.off_part), (float*)(ws + p.off_sum1),
-                                       (float*)(ws + p.off_sum2), da, p.nt * B, 2 * d, s);
-            if (st != MEMOROID_OK) return st;
-        }
-        if (ffm_param_grad_launch(alpha, omega, da, m, c, grad_alpha, grad_omega, s) != hipSuccess)
-            return MEMOROID_EHIP;
+    float* da = (float*)(ws + off_da);
+    if (params && !p.fused_da) {
+        const int st = reduce_rows((const float*)(ws + p.off_part), (float*)(ws + p.off_sum1),
+                                   (float*)(ws + p.off_sum2), da, p.nt * B, 2 * d, s);
+        if (st != MEMOROID_OK) return st;
     }
-    return MEMOROID_OK;
+    FfmFinishArgs fa{};
+    fa.dxw = (const float*)(ws + off_dxw);
+    fa.dx = grad_x;
+    fa.B = B;
+    fa.T = T;
+    fa.m = m;
+    fa.c = c;
+    fa.jpc = p.Dp / c;
+    fa.alpha = alpha;
+    fa.omega = omega;
+    fa.da = da;
+    fa.dalpha = params ? grad_alpha : nullptr;
+    fa.domega = params ? grad_omega : nullptr;
+    return check_hip(ffm_bwd_finish_launch(fa, s));
 }
 
 // ------------------------------------------------------------ diag backward

@@ -40,6 +40,7 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     __shared__ uint32_t sWF[NW];
     __shared__ S sCarry[64 * VEC];
     __shared__ LookbackLds<S, VEC> sLb;
+    __shared__ cf sFfm[FFM ? 64 : 1];      // FFM conj(a) of the chain's features
 
     const int tid = threadIdx.x;
     // the workgroup's chain is fixed by its index (each run of nchains
@@ -134,16 +135,13 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     }
     S ainv[VEC];
     if constexpr (FFM) {
-        // conj(a), a = exp(-|alpha_j|) (cos omega_k + i sin omega_k), f = j * c + k,
-        // evaluated as in the forward pass
+        // conj(a) of the chain's features, evaluated once per tile as in the
+        // forward pass
+        if constexpr (std::is_same<S, cf>::value) {
+            ffm_table(sFfm, p.alpha, p.omega, p.d, p.ffm_c, (int64_t)fb * Dp, Dp, true);
+            __syncthreads();
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) {
-            const int64_t f = f0 + v < p.d ? f0 + v : 0;
-            const int64_t jj = f / p.ffm_c, kk = f - jj * p.ffm_c;
-            const double mag = exp(-fabs((double)p.alpha[jj]));
-            double sn, cs;
-            sincos((double)p.omega[kk], &sn, &cs);
-            if constexpr (std::is_same<S, cf>::value) ainv[v] = cf{(float)(mag * cs), -(float)(mag * sn)};
+            for (int v = 0; v < VEC; ++v) ainv[v] = sFfm[q * VEC + v];
         }
     } else if constexpr (AINV) {
         // a NULL time-invariant a stands for a = 1 (the reverse sum, used by
@@ -272,8 +270,12 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
             // gradient is the sum of Re(lam) over those columns.  c is a power
             // of two: with c >= VEC a lane's features share one j and groups
             // of c / VEC lanes are combined by shuffles; with c < VEC each
-            // feature is its own j.
+            // feature is its own j.  The chain's jpc = Dp / c rows go to the
+            // chain-major workspace [chain][T][jpc], so that a tile writes
+            // whole lines (ffm_bwd_finish_kernel puts them in [B][T][m] order).
             const int64_t cc = p.ffm_c;
+            const int64_t jpc = Dp / cc;
+            float* const dxw = p.dxr + (int64_t)chain * T * jpc;
 #pragma unroll
             for (int r = R - 1; r >= 0; --r) {
                 const int64_t t = row0 + r;
@@ -283,11 +285,11 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
 #pragma unroll
                     for (int v = 0; v < VEC; ++v) part += C::get(rg[r], v).re;
                     for (int off = 1; off < (int)(cc / VEC); off <<= 1) part += __shfl_xor(part, off, 64);
-                    if (in && (q % (int)(cc / VEC)) == 0) p.dxr[(rowbase + t) * p.ffm_m + f0 / cc] = part;
+                    if (in && (q % (int)(cc / VEC)) == 0) dxw[t * jpc + (q * VEC) / cc] = part;
                 } else {
 #pragma unroll
                     for (int v = 0; v < VEC; ++v)
-                        if (in && f0 + v < p.d) p.dxr[(rowbase + t) * p.ffm_m + (f0 + v) / cc] = C::get(rg[r], v).re;
+                        if (in && f0 + v < p.d) dxw[t * jpc + (q * VEC + v) / cc] = C::get(rg[r], v).re;
                 }
             }
         } else {
@@ -442,8 +444,8 @@ hipError_t ffm_bwd_launch(bool vec, const DiagBwdArgs& args, int64_t ntiles, hip
 
 // One workgroup: thread j < m forms dalpha[j], thread k < c forms domega[k]
 // (loops over the other index), from the summed complex da[m][c].
-__global__ __launch_bounds__(256) void ffm_param_grad_kernel(const float* alpha, const float* omega, const float* da,
-                                                             int64_t m, int64_t c, float* dalpha, float* domega) {
+__device__ void ffm_param_grad(const float* alpha, const float* omega, const float* da, int64_t m, int64_t c,
+                               float* dalpha, float* domega) {
     for (int64_t j = threadIdx.x; dalpha && j < m; j += 256) {
         const double mag = exp(-fabs((double)alpha[j]));
         const double sgn = alpha[j] > 0.0f ? 1.0 : (alpha[j] < 0.0f ? -1.0 : 0.0);
@@ -469,9 +471,47 @@ __global__ __launch_bounds__(256) void ffm_param_grad_kernel(const float* alpha,
     }
 }
 
-hipError_t ffm_param_grad_launch(const float* alpha, const float* omega, const float* da, int64_t m, int64_t c,
-                                 float* dalpha, float* domega, hipStream_t s) {
-    hipLaunchKernelGGL(ffm_param_grad_kernel, dim3(1), dim3(256), 0, s, alpha, omega, da, m, c, dalpha, domega);
+// The FFM gradient's last step: workgroups below nblk copy the chain-major
+// input gradient dxw[B][nfb][T][jpc] into dx[B][T][m], 256 steps of one tape
+// each (the chains' rows of those steps are whole lines, read once); the
+// last workgroup forms the parameter gradients from the summed da when asked.
+__global__ __launch_bounds__(256) void ffm_bwd_finish_kernel(FfmFinishArgs p) {
+    const int64_t nblk_t = (p.T + 255) / 256;
+    if ((int64_t)blockIdx.x == p.B * nblk_t) {
+        if (p.dalpha || p.domega) ffm_param_grad(p.alpha, p.omega, p.da, p.m, p.c, p.dalpha, p.domega);
+        return;
+    }
+    const int64_t b = blockIdx.x / nblk_t;
+    const int64_t t0 = (blockIdx.x - b * nblk_t) * 256;
+    const int rows = (int)(p.T - t0 < 256 ? p.T - t0 : 256);
+    const int64_t nfb = (p.m + p.jpc - 1) / p.jpc;
+    // thread (r0, j) copies column j of rows r0, r0 + per, ...; for m > 256
+    // one row per pass and several columns per thread
+    const int64_t per = p.m <= 256 ? 256 / p.m : 1;
+    const int64_t r0 = p.m <= 256 ? threadIdx.x / p.m : 0;
+    if (r0 >= per) return;
+    for (int64_t j = p.m <= 256 ? threadIdx.x % p.m : threadIdx.x; j < p.m; j += 256) {
+        const int64_t fb = j / p.jpc;
+        const float* src = p.dxw + ((b * nfb + fb) * p.T + t0) * p.jpc + (j - fb * p.jpc);
+        float* dst = p.dx + (b * p.T + t0) * p.m + j;
+        const int64_t ss = p.jpc, ds = p.m;
+        int64_t r = r0;
+        for (; r + 3 * per < rows; r += 4 * per) {
+            const float v0 = src[r * ss], v1 = src[(r + per) * ss];
+            const float v2 = src[(r + 2 * per) * ss], v3 = src[(r + 3 * per) * ss];
+            dst[r * ds] = v0;
+            dst[(r + per) * ds] = v1;
+            dst[(r + 2 * per) * ds] = v2;
+            dst[(r + 3 * per) * ds] = v3;
+        }
+        for (; r < rows; r += per) dst[r * ds] = src[r * ss];
+        if (p.m <= 256) break;
+    }
+}
+
+hipError_t ffm_bwd_finish_launch(const FfmFinishArgs& a, hipStream_t s) {
+    const int64_t nblk = a.B * ((a.T + 255) / 256) + 1;
+    hipLaunchKernelGGL(ffm_bwd_finish_kernel, dim3((unsigned)nblk), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

@@ -69,6 +69,7 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     __shared__ LookbackLds<S, VEC> sLb;
     __shared__ uint32_t sWC[NW];           // begin counts per wavefront (episode index)
     __shared__ uint32_t sCntBefore;        // begins on the tape before this tile
+    __shared__ cf sFfm[FFM ? 64 : 1];      // FFM transitions of the chain's features
 
     const int tid = threadIdx.x;
     // the workgroup's chain is fixed by its index (each run of nchains
@@ -170,17 +171,13 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     }
     S ainv[VEC];
     if constexpr (FFM) {
-        // a = exp(-|alpha_j|) (cos omega_k + i sin omega_k), f = j * c + k,
-        // evaluated in double and rounded once to float: with |a| near 1 the
-        // error of a is amplified by up to the episode length
+        // the chain's transitions, evaluated once per tile by wavefront 0
+        // while the loads are in flight
+        if constexpr (std::is_same<S, cf>::value) {
+            ffm_table(sFfm, p.alpha, p.omega, p.d, p.ffm_c, (int64_t)fb * Dp, Dp, false);
+            __syncthreads();
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) {
-            const int64_t f = f0 + v < p.d ? f0 + v : 0;
-            const int64_t jj = f / p.ffm_c, kk = f - jj * p.ffm_c;
-            const double mag = exp(-fabs((double)p.alpha[jj]));
-            double sn, cs;
-            sincos((double)p.omega[kk], &sn, &cs);
-            if constexpr (std::is_same<S, cf>::value) ainv[v] = cf{(float)(mag * cs), (float)(mag * sn)};
+            for (int v = 0; v < VEC; ++v) ainv[v] = sFfm[q * VEC + v];
         }
     } else if constexpr (AINV) {
         // a NULL time-invariant a stands for a = 1 (the sum monoid, used by

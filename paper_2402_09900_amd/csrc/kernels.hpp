@@ -93,16 +93,29 @@ struct DiagBwdArgs {
     const float* alpha;
     const float* omega;
     int64_t ffm_m, ffm_c;
-    float* dxr;
+    float* dxr;        // chain-major input gradient [chains][T][Dp / c] (workspace)
+};
+
+// Last step of the FFM gradient: dx[B][T][m] from the chain-major dxw, and
+// dalpha / domega from the summed da[m][c] (complex), when not NULL.
+struct FfmFinishArgs {
+    const float* dxw;  // [B][nfb][T][jpc], nfb = ceil(m / jpc)
+    float* dx;
+    int64_t B, T, m, c, jpc;
+    const float* alpha;
+    const float* omega;
+    const float* da;
+    float* dalpha;
+    float* domega;
 };
 
 hipError_t diag_fwd_launch(int in_kind, int out_kind, bool vec, bool ainv,
                            const DiagFwdArgs& args, int64_t ntiles, hipStream_t s);
 hipError_t ffm_fwd_launch(bool vec, const DiagFwdArgs& args, int64_t ntiles, hipStream_t s);
 hipError_t ffm_bwd_launch(bool vec, const DiagBwdArgs& args, int64_t ntiles, hipStream_t s);
-// dalpha[j] = -sign(alpha_j) sum_k Re(conj(a_jk) da_jk), domega[k] = sum_j Im(conj(a_jk) da_jk)
-hipError_t ffm_param_grad_launch(const float* alpha, const float* omega, const float* da, int64_t m, int64_t c,
-                                 float* dalpha, float* domega, hipStream_t s);
+// dx from the chain-major workspace; dalpha[j] = -sign(alpha_j) sum_k
+// Re(conj(a_jk) da_jk), domega[k] = sum_j Im(conj(a_jk) da_jk)
+hipError_t ffm_bwd_finish_launch(const FfmFinishArgs& a, hipStream_t s);
 hipError_t diag_bwd_launch(int kind, bool vec, bool ainv, const DiagBwdArgs& args,
                            int64_t ntiles, hipStream_t s);
 // out[r / (4 rpw)][c] = sum over rows r .. r + 4 rpw - 1 of in[r][c], in a

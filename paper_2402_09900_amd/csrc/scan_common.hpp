@@ -370,6 +370,27 @@ template <> struct Desc<cf> {
     }
 };
 
+// FFM transition of a chain's Dp features, a_jk = exp(-|alpha_j|) (cos omega_k
+// + i sin omega_k) for feature f = j * c + k, evaluated once per tile: lane
+// l < Dp (Dp <= 64, so wavefront 0 alone) takes feature f_base + l, in double
+// and rounded once to float (with |a| near 1 the error of a is amplified by up
+// to the episode length), into tab[l].  conj_a stores conj(a) (the reverse
+// scan's coefficient).  Features past d get a valid, unused value.  The caller
+// synchronises the workgroup before reading tab.
+__device__ __forceinline__ void ffm_table(cf* tab, const float* alpha, const float* omega, int64_t d, int64_t c,
+                                          int64_t f_base, int Dp, bool conj_a) {
+    const int l = threadIdx.x;
+    if (l < Dp) {
+        const int64_t f = f_base + l < d ? f_base + l : 0;
+        const int64_t jj = f / c, kk = f - jj * c;
+        const double mag = exp(-fabs((double)alpha[jj]));
+        double sn, cs;
+        sincos((double)omega[kk], &sn, &cs);
+        const float im = (float)(mag * sn);
+        tab[l] = cf{(float)(mag * cs), conj_a ? -im : im};
+    }
+}
+
 // Descriptor slot of feature v of lane q inside tile `ticket`'s block of Dp
 // features: lanes are contiguous for a fixed v, so the accesses of a
 // wavefront coalesce.
