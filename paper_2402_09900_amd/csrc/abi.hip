@@ -324,7 +324,7 @@ bool ffm_bwd_plan(int64_t B, int64_t T, int64_t m, int64_t c, bool vec, bool par
                   size_t* off_da, size_t* off_dxw, size_t* total) {
     int64_t d;
     if (!mul_ok(m, c, &d)) return false;
-    if (!plan_diag(B, T, d, MEMOROID_C64, vec, diag_rows(true, true), true, true, params, p)) return false;
+    if (!plan_diag(B, T, d, MEMOROID_C64, vec, kFfmBwdRows, true, true, params, p)) return false;
     *off_da = align_up(p->total);
     *off_dxw = align_up(*off_da + (size_t)(params ? d : 1) * 8);
     const int64_t jpc = c <= p->Dp ? p->Dp / c : 1;

@@ -433,7 +433,7 @@ static hipError_t launch_bwd(const DiagBwdArgs& args, int64_t ntiles, bool ainv,
 }
 
 hipError_t ffm_bwd_launch(bool vec, const DiagBwdArgs& args, int64_t ntiles, hipStream_t s) {
-    constexpr int RI = diag_rows(true, true);
+    constexpr int RI = kFfmBwdRows;
     if (vec)
         hipLaunchKernelGGL((diag_bwd_kernel<K_C64, KindInfo<K_C64>::vec, RI, true, true>), dim3((unsigned)ntiles),
                            dim3(256), 0, s, args);

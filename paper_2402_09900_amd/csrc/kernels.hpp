@@ -33,6 +33,12 @@ constexpr int kBwdRowsPerStepA = MEMOROID_BWD_ROWS_PER_STEP_A;
 // Bytes of a feature row one chain covers (one 128-byte line by default).
 constexpr int64_t kChainRowBytes = MEMOROID_CHAIN_ROW_BYTES;
 constexpr int diag_rows(bool bwd, bool ainv) { return !bwd ? kFwdRows : (ainv ? kBwdRows : kBwdRowsPerStepA); }
+// The FFM gradient keeps more per-tile state (the input-gradient reduction)
+// and runs fastest with shorter tiles and more workgroups per CU.
+#ifndef MEMOROID_FFM_BWD_ROWS
+#define MEMOROID_FFM_BWD_ROWS 8
+#endif
+constexpr int kFfmBwdRows = MEMOROID_FFM_BWD_ROWS;
 
 struct DiagFwdArgs {
     const void* a;
