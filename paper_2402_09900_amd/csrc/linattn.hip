@@ -116,22 +116,26 @@ __global__ __launch_bounds__(256, 3) void linattn_output_kernel(LinOutputArgs p)
     fetch_rows(qreg, p.q, t0, p.H, h, 0, nvalid);
     fetch_rows(kreg, p.k, t0, p.H, h, 0, nvalid);
     const int bad = fetch_rows(vreg, p.v, t0, p.H, h, 0, nvalid);
-    const float* src = c > 0 ? p.Sinc + ((c - 1) * p.H + h) * kStateWords : nullptr;
+    // S_in: the state after the previous chunk (an empty range, read as
+    // zeros, for the first chunk)
+    const Rsrc rs_s = make_rsrc(p.Sinc + (c > 0 ? ((c - 1) * p.H + h) * kStateWords : 0),
+                                c > 0 ? kStateWords * 4 : 0);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
         const int f = tid + 256 * u;
-        sreg[u] = src ? *(const f32x4*)(src + (f >> 4) * kC + (f & 15) * 4) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        const u32x4 wv = __builtin_amdgcn_raw_buffer_load_b128(rs_s, ((f >> 4) * kC + (f & 15) * 4) * 4, 0, 0);
+        sreg[u] = f32x4{__uint_as_float(wv.x), __uint_as_float(wv.y), __uint_as_float(wv.z), __uint_as_float(wv.w)};
     }
-    const float zin = (src && tid < kC) ? src[kC * kC + tid] : 0.0f;
+    const float zin = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs_s, (kC * kC + (tid & (kC - 1))) * 4, 0, 0));
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
         const int f = tid + 256 * u;
         const int row = f >> 4, c4 = (f & 15) * 4;
+        // phi of every row: rows past T read zeros (phi = 1), and their
+        // entries are masked out of A or belong to outputs never stored
         f32x4 qv = qreg[u], kv = kreg[u];
-        if (row < nvalid) {
-            qv.x = phi(qv.x); qv.y = phi(qv.y); qv.z = phi(qv.z); qv.w = phi(qv.w);
-            kv.x = phi(kv.x); kv.y = phi(kv.y); kv.z = phi(kv.z); kv.w = phi(kv.w);
-        }
+        qv.x = phi(qv.x); qv.y = phi(qv.y); qv.z = phi(qv.z); qv.w = phi(qv.w);
+        kv.x = phi(kv.x); kv.y = phi(kv.y); kv.z = phi(kv.z); kv.w = phi(kv.w);
         *(f32x4*)(sQ + row * kLD + c4) = qv;
         *(f32x4*)(sK + row * kLD + c4) = kv;
         *(f32x4*)(sS + row * kLD + c4) = sreg[u];

@@ -28,22 +28,45 @@ __device__ __forceinline__ float phi(float u) { return u > 0.0f ? u + 1.0f : __e
 // column of element (row, col) in a rotated buffer
 __device__ __forceinline__ int rot_col(int row, int col) { return (col + 16 * (row >> 4)) & (kC - 1); }
 
+// Rows [lo, hi) of one chunk of a [T][H][64] tensor as a buffer resource
+// based at row lo: a row outside the range has an offset past the end (rows
+// below lo wrap to huge unsigned offsets), so the hardware reads it as zeros
+// and no load needs a branch.  off(row, c4) is the byte offset.
+struct ChunkRows {
+    Rsrc r;
+    uint32_t row_bytes;
+    int lo;
+    __device__ __forceinline__ uint32_t off(int row, int c4) const {
+        return (uint32_t)(row - lo) * row_bytes + (uint32_t)c4 * 4u;
+    }
+    __device__ __forceinline__ f32x4 load(int row, int c4) const {
+        const u32x4 w = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off(row, c4), 0, 0);
+        return f32x4{__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z), __uint_as_float(w.w)};
+    }
+};
+__device__ __forceinline__ ChunkRows chunk_rows(const float* src, int64_t t0, int64_t H, int64_t h, int lo, int hi) {
+    const uint32_t rb = (uint32_t)(H * kC * 4);
+    const int n = hi > lo ? hi - lo : 0;
+    const int64_t bytes = n > 0 ? (int64_t)(n - 1) * rb + kC * 4 : 0;
+    return ChunkRows{make_rsrc(src + ((t0 + lo) * H + h) * kC, bytes), rb, lo};
+}
+
+__device__ __forceinline__ bool finite4(f32x4 v) {
+    return __builtin_isfinite(v.x) && __builtin_isfinite(v.y) && __builtin_isfinite(v.z) && __builtin_isfinite(v.w);
+}
+
 // Fetch one chunk of a [T][H][64] tensor into registers (4 float4 per
 // thread, rows outside [lo, hi) as zeros) and write it to LDS later with
 // store_rows; returns nonzero if a value is not finite.
 __device__ __forceinline__ int fetch_rows(f32x4 (&v)[4], const float* src, int64_t t0, int64_t H, int64_t h, int lo,
                                           int hi) {
+    const ChunkRows cr = chunk_rows(src, t0, H, h, lo, hi);
     int bad = 0;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
         const int f = threadIdx.x + 256 * u;
-        const int row = f >> 4, c4 = (f & 15) * 4;
-        v[u] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-        if (row >= lo && row < hi) {
-            v[u] = *(const f32x4*)(src + ((t0 + row) * H + h) * kC + c4);
-            bad |= !(__builtin_isfinite(v[u].x) && __builtin_isfinite(v[u].y) && __builtin_isfinite(v[u].z) &&
-                     __builtin_isfinite(v[u].w));
-        }
+        v[u] = cr.load(f >> 4, (f & 15) * 4);
+        bad |= !finite4(v[u]);
     }
     return bad;
 }
@@ -64,21 +87,28 @@ __device__ __forceinline__ void store_rows(float* s, const f32x4 (&v)[4]) {
 // each row as rot_col does.  Returns nonzero if a staged value is not finite.
 template <bool PHI, bool ROT>
 __device__ __forceinline__ int stage(float* s, const float* src, int64_t t0, int64_t H, int64_t h, int lo, int hi) {
-    int bad = 0;
+    const ChunkRows cr = chunk_rows(src, t0, H, h, lo, hi);
+    f32x4 v[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
         const int f = threadIdx.x + 256 * u;   // float4 index within the 64x64 tile
+        v[u] = cr.load(f >> 4, (f & 15) * 4);
+    }
+    int bad = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int f = threadIdx.x + 256 * u;
         const int row = f >> 4, c4 = (f & 15) * 4;
-        f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
-        if (row >= lo && row < hi) {
-            v = *(const f32x4*)(src + ((t0 + row) * H + h) * kC + c4);
-            if (PHI) {
-                v.x = phi(v.x); v.y = phi(v.y); v.z = phi(v.z); v.w = phi(v.w);
-            }
-            bad |= !(__builtin_isfinite(v.x) && __builtin_isfinite(v.y) && __builtin_isfinite(v.z) &&
-                     __builtin_isfinite(v.w));
+        if (PHI) {
+            // phi(0) = 1: rows outside the range are selected back to zeros
+            const bool in = row >= lo && row < hi;
+            v[u].x = in ? phi(v[u].x) : 0.0f;
+            v[u].y = in ? phi(v[u].y) : 0.0f;
+            v[u].z = in ? phi(v[u].z) : 0.0f;
+            v[u].w = in ? phi(v[u].w) : 0.0f;
         }
-        *(f32x4*)(s + row * kLD + (ROT ? rot_col(row, c4) : c4)) = v;
+        bad |= !finite4(v[u]);
+        *(f32x4*)(s + row * kLD + (ROT ? rot_col(row, c4) : c4)) = v[u];
     }
     return bad;
 }
@@ -125,10 +155,19 @@ __device__ __forceinline__ void mfma_64x64x64(const float* sA, const float* sB, 
 
 __device__ __forceinline__ bool is_begin(const uint8_t* st, int64_t t) { return t == 0 || st[t] != 0; }
 
-// sum over the 16 lanes that share lane / 16
+// sum over the 16 lanes that share lane / 16, with DPP moves inside each
+// 16-lane row: lane ^ 1, lane ^ 2 (quad permutations), then the mirror of
+// each 8-lane half and of the row; every step adds two equal partial sums in
+// either order, so all 16 lanes hold the bit-identical total
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
 __device__ __forceinline__ float sum16(float v) {
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) v += __shfl_xor(v, off, 64);
+    v += dpp_f32<0xB1>(v);     // quad_perm [1, 0, 3, 2]
+    v += dpp_f32<0x4E>(v);     // quad_perm [2, 3, 0, 1]
+    v += dpp_f32<0x141>(v);    // row_half_mirror
+    v += dpp_f32<0x140>(v);    // row_mirror
     return v;
 }
 
