@@ -35,7 +35,6 @@ namespace memoroid {
 __global__ __launch_bounds__(256) void linattn_summary_kernel(LinSummaryArgs p) {
     __shared__ __attribute__((aligned(16))) float sK[kC * kLD];   // phi(K), rotated
     __shared__ __attribute__((aligned(16))) float sV[kC * kLD];   // V, rotated
-    __shared__ int s_last;
     const int64_t c = blockIdx.x, h = blockIdx.y;
     const int64_t t0 = c * kC;
     const int nvalid = (int)(p.T - t0 < kC ? p.T - t0 : kC);
@@ -50,14 +49,29 @@ __global__ __launch_bounds__(256) void linattn_summary_kernel(LinSummaryArgs p) 
         for (int64_t i = gid; i < p.fill16; i += nblk * 256) p.fill[i] = ones;
     }
 
-    if (threadIdx.x == 0) s_last = -1;
-    __syncthreads();
-    if ((int)threadIdx.x < nvalid && is_begin(p.start, t0 + threadIdx.x)) atomicMax(&s_last, (int)threadIdx.x);
-    __syncthreads();
-    const int last = s_last;
+    // K, V rows and the begin flags are all loaded at once; every wavefront
+    // finds the chunk's last begin step with one ballot (lane = row), and
+    // rows before it are then selected to zeros in both phi(K) and V (a
+    // select, so non-finite values there never enter)
+    f32x4 kreg[4], vreg[4];
+    fetch_rows(kreg, p.k, t0, p.H, h, 0, nvalid);
+    fetch_rows(vreg, p.v, t0, p.H, h, 0, nvalid);
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const uint64_t bm = __ballot(lane < nvalid && is_begin(p.start, t0 + lane));
+    const int last = bm ? 63 - __builtin_clzll(bm) : -1;
     const int lo = last > 0 ? last : 0;
-    stage<true, true>(sK, p.k, t0, p.H, h, lo, nvalid);
-    stage<false, true>(sV, p.v, t0, p.H, h, lo, nvalid);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int f = threadIdx.x + 256 * u;
+        const int row = f >> 4, c4 = (f & 15) * 4;
+        const bool in = row >= lo && row < nvalid;
+        f32x4 kv = kreg[u], vv = vreg[u];
+        kv.x = in ? phi(kv.x) : 0.0f; kv.y = in ? phi(kv.y) : 0.0f;
+        kv.z = in ? phi(kv.z) : 0.0f; kv.w = in ? phi(kv.w) : 0.0f;
+        vv.x = in ? vv.x : 0.0f; vv.y = in ? vv.y : 0.0f; vv.z = in ? vv.z : 0.0f; vv.w = in ? vv.w : 0.0f;
+        *(f32x4*)(sK + row * kLD + rot_col(row, c4)) = kv;
+        *(f32x4*)(sV + row * kLD + rot_col(row, c4)) = vv;
+    }
     __syncthreads();
 
     f32x4 acc[4];
@@ -67,7 +81,6 @@ __global__ __launch_bounds__(256) void linattn_summary_kernel(LinSummaryArgs p) 
     mfma_64x64x64<false, false>(sV, sK, acc);
 
     float* out = p.dS + (c * p.H + h) * kStateWords;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) {
 #pragma unroll
@@ -87,12 +100,12 @@ __global__ __launch_bounds__(256) void linattn_summary_kernel(LinSummaryArgs p) 
 
 // ------------------------------------------------------------------- output
 
-__global__ __launch_bounds__(256, 3) void linattn_output_kernel(LinOutputArgs p) {
-    __shared__ __attribute__((aligned(16))) float sQ[kC * kLD];   // phi(Q)
-    __shared__ __attribute__((aligned(16))) float sK[kC * kLD];   // phi(K), later the masked A
-    __shared__ __attribute__((aligned(16))) float sS[kC * kLD];   // S_in^T, later V (rotated)
+__global__ __launch_bounds__(256, 4) void linattn_output_kernel(LinOutputArgs p) {
+    // two LDS tiles, reused in turn: (phi(Q), phi(K)) -> (phi(Q), S_in^T) ->
+    // (masked A, V rotated); 35 KB per workgroup, four workgroups per CU
+    __shared__ __attribute__((aligned(16))) float X0[kC * kLD];
+    __shared__ __attribute__((aligned(16))) float X1[kC * kLD];
     __shared__ float sZ[kC];
-    float* const sV = sS;
 
     const int64_t c = blockIdx.x, h = blockIdx.y;
     const int64_t t0 = c * kC;
@@ -110,8 +123,7 @@ __global__ __launch_bounds__(256, 3) void linattn_output_kernel(LinOutputArgs p)
     }
 
     // every global load of the workgroup is issued before any LDS store: q,
-    // k, v and S_in into registers (V is kept there and moved into the S
-    // buffer once S has been used)
+    // k, v and S_in into registers (S and V wait there for their turn in LDS)
     f32x4 qreg[4], kreg[4], vreg[4], sreg[4];
     fetch_rows(qreg, p.q, t0, p.H, h, 0, nvalid);
     fetch_rows(kreg, p.k, t0, p.H, h, 0, nvalid);
@@ -136,9 +148,8 @@ __global__ __launch_bounds__(256, 3) void linattn_output_kernel(LinOutputArgs p)
         f32x4 qv = qreg[u], kv = kreg[u];
         qv.x = phi(qv.x); qv.y = phi(qv.y); qv.z = phi(qv.z); qv.w = phi(qv.w);
         kv.x = phi(kv.x); kv.y = phi(kv.y); kv.z = phi(kv.z); kv.w = phi(kv.w);
-        *(f32x4*)(sQ + row * kLD + c4) = qv;
-        *(f32x4*)(sK + row * kLD + c4) = kv;
-        *(f32x4*)(sS + row * kLD + c4) = sreg[u];
+        *(f32x4*)(X0 + row * kLD + c4) = qv;
+        *(f32x4*)(X1 + row * kLD + c4) = kv;
     }
     if (tid < kC) sZ[tid] = zin;
     const bool nonfinite_v = __syncthreads_or(bad) != 0;
@@ -166,8 +177,15 @@ __global__ __launch_bounds__(256, 3) void linattn_output_kernel(LinOutputArgs p)
         accA[jt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
         accS[jt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     }
-    mfma_64x64x64<true, true>(sQ, sK, accA);    // A[i][j]  = phi(q_i) . phi(k_j)
-    mfma_64x64x64<true, true>(sQ, sS, accS);    // QS[i][n] = sum_kd phi(q_i)[kd] S_in[kd][n]
+    mfma_64x64x64<true, true>(X0, X1, accA);    // A[i][j]  = phi(q_i) . phi(k_j)
+    __syncthreads();                            // every wavefront is done with phi(K)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int f = tid + 256 * u;
+        *(f32x4*)(X1 + (f >> 4) * kLD + (f & 15) * 4) = sreg[u];
+    }
+    __syncthreads();
+    mfma_64x64x64<true, true>(X0, X1, accS);    // QS[i][n] = sum_kd phi(q_i)[kd] S_in[kd][n]
 
     // mask A to each row's episode (a select: excluded entries are exact
     // zeros), then the row sums and phi(q_i).z_in, reduced across lanes
@@ -186,17 +204,19 @@ __global__ __launch_bounds__(256, 3) void linattn_output_kernel(LinOutputArgs p)
             rs += accA[jt][r];
         }
         const int kd = 4 * (lane & 15);
-        const f32x4 qv = *(const f32x4*)(sQ + i * kLD + kd);
+        const f32x4 qv = *(const f32x4*)(X0 + i * kLD + kd);
         float qz = qv.x * sZ[kd] + qv.y * sZ[kd + 1] + qv.z * sZ[kd + 2] + qv.w * sZ[kd + 3];
         rs = sum16(rs);
         qz = sum16(qz);
         den[r] = rs + (ri[r] < 0 ? qz : 0.0f);
     }
-    __syncthreads();                            // every wavefront is done with sK and sS
+    __syncthreads();                            // every wavefront is done with phi(Q) and S
+    float* const sA = X0;
+    float* const sV = X1;
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) sK[(16 * w + 4 * (lane >> 4) + r) * kLD + 16 * jt + (lane & 15)] = accA[jt][r];
+        for (int r = 0; r < 4; ++r) sA[(16 * w + 4 * (lane >> 4) + r) * kLD + 16 * jt + (lane & 15)] = accA[jt][r];
     }
     store_rows<true>(sV, vreg);
     __syncthreads();
@@ -205,7 +225,7 @@ __global__ __launch_bounds__(256, 3) void linattn_output_kernel(LinOutputArgs p)
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) accO[jt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     if (!nonfinite_v) {
-        mfma_64x64x64<true, false>(sK, sV, accO);    // num[i][n] = sum_j A[i][j] V[j][n]
+        mfma_64x64x64<true, false>(sA, sV, accO);    // num[i][n] = sum_j A[i][j] V[j][n]
     } else {
         // A non-finite value in V would reach other episodes of this chunk
         // through the dense product (0 * NaN = NaN); sum each row's own
@@ -218,7 +238,7 @@ __global__ __launch_bounds__(256, 3) void linattn_output_kernel(LinOutputArgs p)
                 const int n = 16 * jt + (lane & 15);
                 float s = 0.0f;
                 for (int j = (ri[r] > 0 ? ri[r] : 0); j <= i && j < nvalid; ++j)
-                    s += sK[i * kLD + j] * sV[j * kLD + rot_col(j, n)];
+                    s += sA[i * kLD + j] * sV[j * kLD + rot_col(j, n)];
                 accO[jt][r] = s;
             }
         }

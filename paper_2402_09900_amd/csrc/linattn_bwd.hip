@@ -64,19 +64,39 @@ __device__ __forceinline__ void acc_to_lds(float* s, const f32x4 (&acc)[4]) {
         }
 }
 
-// Stage a 64x64 state block stored row-major at src (64 rows of 64 floats)
-// into LDS, natural or rotated; zeros if src is NULL.
-template <bool ROT>
-__device__ __forceinline__ void stage_state(float* s, const float* src) {
+// Load a 64x64 state block stored row-major at src into registers (the
+// fetch_rows layout); zeros when `have` is false.
+__device__ __forceinline__ void fetch_state(f32x4 (&v)[4], const float* src, bool have) {
+    const Rsrc r = make_rsrc(src, have ? kC * kC * 4 : 0);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
         const int f = threadIdx.x + 256 * u;
-        const int row = f >> 4, c4 = (f & 15) * 4;
-        f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
-        if (src) v = *(const f32x4*)(src + row * kC + c4);
-        *(f32x4*)(s + row * kLD + (ROT ? rot_col(row, c4) : c4)) = v;
+        const u32x4 wv = __builtin_amdgcn_raw_buffer_load_b128(r, ((f >> 4) * kC + (f & 15) * 4) * 4, 0, 0);
+        v[u] = f32x4{__uint_as_float(wv.x), __uint_as_float(wv.y), __uint_as_float(wv.z), __uint_as_float(wv.w)};
     }
 }
+
+// phi of a fetched tile, rows outside [lo, hi) selected to zeros
+__device__ __forceinline__ void phi_rows(f32x4 (&v)[4], int lo, int hi) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int row = (threadIdx.x + 256 * u) >> 4;
+        const bool in = row >= lo && row < hi;
+        v[u].x = in ? phi(v[u].x) : 0.0f; v[u].y = in ? phi(v[u].y) : 0.0f;
+        v[u].z = in ? phi(v[u].z) : 0.0f; v[u].w = in ? phi(v[u].w) : 0.0f;
+    }
+}
+
+// rows outside [lo, hi) selected to zeros (store_rows writes the result)
+__device__ __forceinline__ f32x4 rows_in(const f32x4& v, int u, int lo, int hi) {
+    const int row = (threadIdx.x + 256 * u) >> 4;
+    const bool in = row >= lo && row < hi;
+    return f32x4{in ? v.x : 0.0f, in ? v.y : 0.0f, in ? v.z : 0.0f, in ? v.w : 0.0f};
+}
+
+// phi'(u) from phi(u): 1 for u > 0 (phi = u + 1 >= 1), exp(u) = phi(u) <= 1
+// otherwise, i.e. min(phi(u), 1), bit for bit; a NaN stays NaN
+__device__ __forceinline__ float phi_prime_of_phi(float ph) { return ph > 1.0f ? 1.0f : ph; }
 
 __device__ __forceinline__ void zero_acc(f32x4 (&acc)[4]) {
 #pragma unroll
@@ -110,9 +130,27 @@ __global__ __launch_bounds__(256) void linattn_bwd_summary_kernel(LinBwdArgs p) 
     const uint64_t mb = __ballot(beg);
     const int fb = mb ? __builtin_ctzll(mb) : kC;        // first begin row (64: none)
 
-    stage<true, false>(sQ, p.q, t0, p.H, h, 0, nvalid);
-    stage<true, false>(sK, p.k, t0, p.H, h, 0, nvalid);
-    if (tid < kC) sZ[tid] = c > 0 ? p.Sinc[((c - 1) * p.H + h) * kStateWords + kC * kC + tid] : 0.0f;
+    // every global load up front: q, k, z_in; g and out of this thread's
+    // row quarter (four threads per row, 16 columns each)
+    f32x4 qreg[4], kreg[4], gv[4], ov[4];
+    fetch_rows(qreg, p.q, t0, p.H, h, 0, nvalid);
+    fetch_rows(kreg, p.k, t0, p.H, h, 0, nvalid);
+    const float zin = tid < kC && c > 0 ? p.Sinc[((c - 1) * p.H + h) * kStateWords + kC * kC + tid] : 0.0f;
+    const int grow = tid >> 2, gc0 = (tid & 3) * 16;
+    {
+        const ChunkRows cr_g = chunk_rows(p.g, t0, p.H, h, 0, nvalid);
+        const ChunkRows cr_o = chunk_rows(p.out, t0, p.H, h, 0, nvalid);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            gv[u] = cr_g.load(grow, gc0 + 4 * u);
+            ov[u] = cr_o.load(grow, gc0 + 4 * u);
+        }
+    }
+    phi_rows(qreg, 0, nvalid);
+    phi_rows(kreg, 0, nvalid);
+    store_rows<false>(sQ, qreg);
+    store_rows<false>(sK, kreg);
+    if (tid < kC) sZ[tid] = zin;
     __syncthreads();
 
     f32x4 accA[4];
@@ -138,17 +176,13 @@ __global__ __launch_bounds__(256) void linattn_bwd_summary_kernel(LinBwdArgs p) 
     // dnum = g / den and dden = -(g . out) / den: four threads per row, 16
     // columns each
     {
-        const int row = tid >> 2, c0 = (tid & 3) * 16;
-        f32x4 gv[4], ov[4];
+        const int row = grow, c0 = gc0;
         float dot = 0.0f;
         const bool ok = row < nvalid;
         const int64_t base = ((t0 + row) * p.H + h) * kC + c0;
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            gv[u] = ok ? *(const f32x4*)(p.g + base + 4 * u) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-            ov[u] = ok ? *(const f32x4*)(p.out + base + 4 * u) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int u = 0; u < 4; ++u)
             dot += gv[u].x * ov[u].x + gv[u].y * ov[u].y + gv[u].z * ov[u].z + gv[u].w * ov[u].w;
-        }
         dot += __shfl_xor(dot, 1, 64);
         dot += __shfl_xor(dot, 2, 64);
         const float den = sDen[row];
@@ -167,7 +201,13 @@ __global__ __launch_bounds__(256) void linattn_bwd_summary_kernel(LinBwdArgs p) 
             sDd[row] = (ok && in_du) ? dd : 0.0f;
         }
     }
-    stage<true, true>(sQ, p.q, t0, p.H, h, 0, fb < nvalid ? fb : nvalid);   // phi(Q) rows < fb, rotated
+    {   // phi(Q) rows < fb, rotated, from the registers
+        const int hi = fb < nvalid ? fb : nvalid;
+        f32x4 qr[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) qr[u] = rows_in(qreg[u], u, 0, hi);
+        store_rows<true>(sQ, qr);
+    }
     __syncthreads();
 
     f32x4 accU[4];
@@ -205,29 +245,45 @@ __global__ __launch_bounds__(256) void linattn_bwd_dq_kernel(LinBwdArgs p) {
     bool beg;
     const int rmax = row_last_begin(p.start, t0, nvalid, beg);
 
-    stage<false, false>(X2, p.dnum, t0, p.H, h, 0, nvalid);
-    stage<false, false>(X3, p.v, t0, p.H, h, 0, nvalid);
-    stage<true, true>(X1, p.k, t0, p.H, h, 0, nvalid);
+    // every global load up front: dnum, v, k, S_in, z_in, the rows' dden,
+    // and q at this lane's output elements (for phi')
+    f32x4 dnreg[4], vreg[4], kreg[4], sreg[4];
+    fetch_rows(dnreg, p.dnum, t0, p.H, h, 0, nvalid);
+    fetch_rows(vreg, p.v, t0, p.H, h, 0, nvalid);
+    fetch_rows(kreg, p.k, t0, p.H, h, 0, nvalid);
+    fetch_state(sreg, p.Sinc + (c > 0 ? ((c - 1) * p.H + h) * kStateWords : 0), c > 0);
+    const float zin = tid < kC && c > 0 ? p.Sinc[((c - 1) * p.H + h) * kStateWords + kC * kC + tid] : 0.0f;
+    int ri[4];
+    float dd[4], qo[4][4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int i = 16 * w + 4 * (lane >> 4) + r;
+        dd[r] = i < nvalid ? p.dden[(t0 + i) * p.H + h] : 0.0f;
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt)
+            qo[jt][r] = i < nvalid ? p.q[((t0 + i) * p.H + h) * kC + 16 * jt + (lane & 15)] : 0.0f;
+    }
+    phi_rows(kreg, 0, nvalid);
+    store_rows<false>(X2, dnreg);
+    store_rows<false>(X3, vreg);
+    store_rows<true>(X1, kreg);
     __syncthreads();
 
     f32x4 acc[4];
     zero_acc(acc);
     mfma_64x64x64<true, true>(X2, X3, acc);                  // dnum_i . v_j
-    int ri[4];
-    float dd[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int i = 16 * w + 4 * (lane >> 4) + r;
         ri[r] = __shfl(rmax, i, 64);
-        dd[r] = i < nvalid ? p.dden[(t0 + i) * p.H + h] : 0.0f;
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt)
             acc[jt][r] = keep_ij(i, 16 * jt + (lane & 15), ri[r], nvalid) ? acc[jt][r] + dd[r] : 0.0f;
     }
     acc_to_lds<false>(X0, acc);
     __syncthreads();                                         // X3 (V) free
-    stage_state<true>(X3, c > 0 ? p.Sinc + ((c - 1) * p.H + h) * kStateWords : nullptr);   // S_in^T [n][kd]
-    if (tid < kC) sZ[tid] = c > 0 ? p.Sinc[((c - 1) * p.H + h) * kStateWords + kC * kC + tid] : 0.0f;
+    store_rows<true>(X3, sreg);                              // S_in^T [n][kd], rotated
+    if (tid < kC) sZ[tid] = zin;
     __syncthreads();
 
     f32x4 accQ[4], accS[4];
@@ -242,8 +298,7 @@ __global__ __launch_bounds__(256) void linattn_bwd_dq_kernel(LinBwdArgs p) {
             const int i = 16 * w + 4 * (lane >> 4) + r, kd = 16 * jt + (lane & 15);
             if (i < nvalid) {
                 const float dQ = accQ[jt][r] + (ri[r] < 0 ? accS[jt][r] + dd[r] * sZ[kd] : 0.0f);
-                const int64_t o = ((t0 + i) * p.H + h) * kC + kd;
-                p.dq[o] = dQ * phi_prime(p.q[o]);
+                p.dq[((t0 + i) * p.H + h) * kC + kd] = dQ * phi_prime(qo[jt][r]);
             }
         }
 }
@@ -263,12 +318,30 @@ __global__ __launch_bounds__(256) void linattn_bwd_dkv_kernel(LinBwdArgs p) {
     const int rmax = row_last_begin(p.start, t0, nvalid, beg);
     const uint64_t mb = __ballot(beg);
     const int lastb = mb ? 63 - __builtin_clzll(mb) : -1;    // rows >= lastb continue past the chunk
-    const float* uo = c + 1 < p.nch ? p.Y + ((c + 1) * p.H + h) * kStateWords : nullptr;
+    const bool have_u = c + 1 < p.nch;
+    const float* uo = p.Y + (have_u ? ((c + 1) * p.H + h) * kStateWords : 0);
 
-    stage<true, false>(X0, p.q, t0, p.H, h, 0, nvalid);
-    stage<true, false>(X1, p.k, t0, p.H, h, 0, nvalid);
-    stage<false, false>(X2, p.dnum, t0, p.H, h, 0, nvalid);
-    stage<false, false>(X3, p.v, t0, p.H, h, 0, nvalid);
+    // every global load up front: q, k, dnum, v, U_out, w_out and the rows'
+    // dden; q, dnum and U_out stay in registers for their second layout
+    f32x4 qreg[4], kreg[4], dnreg[4], vreg[4], ureg[4];
+    fetch_rows(qreg, p.q, t0, p.H, h, 0, nvalid);
+    fetch_rows(kreg, p.k, t0, p.H, h, 0, nvalid);
+    fetch_rows(dnreg, p.dnum, t0, p.H, h, 0, nvalid);
+    fetch_rows(vreg, p.v, t0, p.H, h, 0, nvalid);
+    fetch_state(ureg, uo, have_u);
+    const float wout = tid < kC && have_u ? uo[kC * kC + tid] : 0.0f;
+    float ddr[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int i = 16 * w + 4 * (lane >> 4) + r;
+        ddr[r] = i < nvalid ? p.dden[(t0 + i) * p.H + h] : 0.0f;
+    }
+    phi_rows(qreg, 0, nvalid);
+    phi_rows(kreg, 0, nvalid);
+    store_rows<false>(X0, qreg);
+    store_rows<false>(X1, kreg);
+    store_rows<false>(X2, dnreg);
+    store_rows<false>(X3, vreg);
     __syncthreads();
 
     f32x4 accA[4], accP[4];
@@ -280,16 +353,15 @@ __global__ __launch_bounds__(256) void linattn_bwd_dkv_kernel(LinBwdArgs p) {
     for (int r = 0; r < 4; ++r) {
         const int i = 16 * w + 4 * (lane >> 4) + r;
         const int ri = __shfl(rmax, i, 64);
-        const float dd = i < nvalid ? p.dden[(t0 + i) * p.H + h] : 0.0f;
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt) {
             const bool keep = keep_ij(i, 16 * jt + (lane & 15), ri, nvalid);
             accA[jt][r] = keep ? accA[jt][r] : 0.0f;
-            accP[jt][r] = keep ? accP[jt][r] + dd : 0.0f;
+            accP[jt][r] = keep ? accP[jt][r] + ddr[r] : 0.0f;
         }
     }
     __syncthreads();                                         // X0 (Q), X2 (dnum) free
-    stage<true, true>(X0, p.q, t0, p.H, h, 0, nvalid);       // phi(Q) rotated
+    store_rows<true>(X0, qreg);                              // phi(Q) rotated
     acc_to_lds<true>(X2, accP);                              // dP rotated
     __syncthreads();
 
@@ -297,8 +369,8 @@ __global__ __launch_bounds__(256) void linattn_bwd_dkv_kernel(LinBwdArgs p) {
     zero_acc(accK);
     mfma_64x64x64<false, false>(X2, X0, accK);               // sum_i dP[i][j] Q[i][kd]
     __syncthreads();                                         // X0, X2 free
-    stage_state<false>(X0, uo);                              // U_out [kd][n], natural
-    if (tid < kC) sW[tid] = uo ? uo[kC * kC + tid] : 0.0f;
+    store_rows<false>(X0, ureg);                             // U_out [kd][n], natural
+    if (tid < kC) sW[tid] = wout;
     acc_to_lds<true>(X2, accA);                              // A (masked) rotated
     __syncthreads();
 
@@ -312,13 +384,13 @@ __global__ __launch_bounds__(256) void linattn_bwd_dkv_kernel(LinBwdArgs p) {
             const int j = 16 * w + 4 * (lane >> 4) + r, kd = 16 * jt + (lane & 15);
             if (j < nvalid) {
                 const float dK = accK[jt][r] + (j >= lastb ? accK2[jt][r] + sW[kd] : 0.0f);
-                const int64_t o = ((t0 + j) * p.H + h) * kC + kd;
-                p.dk[o] = dK * phi_prime(p.k[o]);
+                // phi'(k) from phi(K), which X1 holds throughout
+                p.dk[((t0 + j) * p.H + h) * kC + kd] = dK * phi_prime_of_phi(X1[j * kLD + kd]);
             }
         }
     __syncthreads();                                         // X0, X3 free
-    stage<false, true>(X3, p.dnum, t0, p.H, h, 0, nvalid);   // dnum rotated
-    stage_state<true>(X0, uo);                               // U_out rotated
+    store_rows<true>(X3, dnreg);                             // dnum rotated
+    store_rows<true>(X0, ureg);                              // U_out rotated
     __syncthreads();
 
     f32x4 accV[4], accV2[4];
