@@ -177,7 +177,9 @@ __global__ __launch_bounds__(256, 4) void linattn_output_kernel(LinOutputArgs p)
         accA[jt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
         accS[jt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     }
-    mfma_64x64x64<true, true>(X0, X1, accA);    // A[i][j]  = phi(q_i) . phi(k_j)
+    // A[i][j] = phi(q_i) . phi(k_j); column tiles above the diagonal are
+    // masked out entirely and skipped
+    mfma_64x64x64<true, true>(X0, X1, accA, w);
     __syncthreads();                            // every wavefront is done with phi(K)
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -185,7 +187,11 @@ __global__ __launch_bounds__(256, 4) void linattn_output_kernel(LinOutputArgs p)
         *(f32x4*)(X1 + (f >> 4) * kLD + (f & 15) * 4) = sreg[u];
     }
     __syncthreads();
-    mfma_64x64x64<true, true>(X0, X1, accS);    // QS[i][n] = sum_kd phi(q_i)[kd] S_in[kd][n]
+    // QS[i][n] = sum_kd phi(q_i)[kd] S_in[kd][n], needed only by rows before
+    // the chunk's first begin (their episode started in an earlier chunk)
+    const uint64_t bmask = __ballot(beg);
+    const int fbeg = bmask ? __builtin_ctzll(bmask) : kC;
+    if (16 * w < fbeg) mfma_64x64x64<true, true>(X0, X1, accS);
 
     // mask A to each row's episode (a select: excluded entries are exact
     // zeros), then the row sums and phi(q_i).z_in, reduced across lanes

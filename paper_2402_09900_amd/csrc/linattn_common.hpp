@@ -117,8 +117,10 @@ __device__ __forceinline__ int stage(float* s, const float* src, int64_t t0, int
 // return acc[jt][r] = C[16w + 4*(lane/16) + r][16*jt + lane%16].
 //   A_ROWS: A[i][k] = sA[i*kLD + k]          else A[i][k] = sA[k*kLD + rot_col(k, i)]
 //   B_ROWS: B[k][j] = sB[j*kLD + k]          else B[k][j] = sB[k*kLD + rot_col(k, j)]
+// jt_last < 3 leaves the output column tiles past it untouched (a wave of a
+// causally masked product skips the tiles above the diagonal).
 template <bool A_ROWS, bool B_ROWS>
-__device__ __forceinline__ void mfma_64x64x64(const float* sA, const float* sB, f32x4 acc[4]) {
+__device__ __forceinline__ void mfma_64x64x64(const float* sA, const float* sB, f32x4 acc[4], int jt_last = 3) {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int i = 16 * w + (lane & 15), kk = (lane >> 4) * 16;
     float af[16];
@@ -135,6 +137,7 @@ __device__ __forceinline__ void mfma_64x64x64(const float* sA, const float* sB, 
     }
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) {
+        if (jt > jt_last) break;
         const int j = 16 * jt + (lane & 15);
         float bf[16];
         if constexpr (B_ROWS) {
