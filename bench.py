@@ -218,20 +218,21 @@ def setup_discount(torch, mb, tapes, key):
     nb = mb.memoroid_discount_workspace_bytes(B, T)
     stream = lambda: torch.cuda.current_stream().cuda_stream  # noqa: E731
     sets = []
-    for _ in range(n_sets(n * (4 * 6 + 2) + 2 * nb)):
+    for _ in range(n_sets(n * (4 * 6 + 2) + 4 * nb)):
         r, v, vn = dev_tensor(torch, tp.r, "f32"), dev_tensor(torch, tp.v, "f32"), dev_tensor(torch, tp.vn, "f32")
         s, done = dev_tensor(torch, tp.start, "u8"), dev_tensor(torch, tp.done, "u8")
         G, adv, tg = (torch.empty((B, T), dtype=torch.float32, device="cuda") for _ in range(3))
-        ws = prepared_ws(torch, mb, nb)
+        ws = prepared_ws(torch, mb, nb)       # the return and the advantage bind one workspace each
+        wsg = prepared_ws(torch, mb, nb)
 
         def ret(r=r, s=s, G=G, ws=ws):
             st = mb.memoroid_discounted_return(r.data_ptr(), s.data_ptr(), tp.gamma, G.data_ptr(), B, T,
                                                ws.data_ptr(), ws.numel(), stream())
             assert st == 0, mb.status_string(st)
 
-        def gae(r=r, v=v, vn=vn, done=done, s=s, adv=adv, tg=tg, ws=ws):
+        def gae(r=r, v=v, vn=vn, done=done, s=s, adv=adv, tg=tg, wsg=wsg):
             st = mb.memoroid_gae(r.data_ptr(), v.data_ptr(), vn.data_ptr(), done.data_ptr(), s.data_ptr(),
-                                 tp.gamma, tp.lam, adv.data_ptr(), tg.data_ptr(), B, T, ws.data_ptr(), ws.numel(),
+                                 tp.gamma, tp.lam, adv.data_ptr(), tg.data_ptr(), B, T, wsg.data_ptr(), wsg.numel(),
                                  stream())
             assert st == 0, mb.status_string(st)
         sets.append({"return": ret, "gae": gae})

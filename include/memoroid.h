@@ -47,8 +47,7 @@
  *        initialises nothing.  The workspace must have been prepared with
  *        memoroid_workspace_prepare() (on a stream ordered before the call)
  *        and then used only by calls of this library.  The first call binds
- *        it to that entry point and those sizes (discounted return and GAE
- *        count as one entry point); every later call with the same entry
+ *        it to that entry point and those sizes; every later call with the same entry
  *        point, sizes and flags finds it ready again, with no preparation in
  *        between.  The binding also covers: the dtypes; whether the
  *        vectorised kernels run (pointer alignment, d); a time-invariant a;

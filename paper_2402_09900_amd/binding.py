@@ -517,7 +517,7 @@ def discounted_return(r, start, gamma: float, workspace=None):
     if r.dtype != torch.float32 or start.dtype != torch.uint8:
         raise TypeError("r must be float32 and start uint8")
     G = torch.empty((B, T), dtype=torch.float32, device=dev)
-    ws = _prepared(lib().memoroid_discount_workspace_bytes(B, T), dev, ("discount", B, T), (), workspace)
+    ws = _prepared(lib().memoroid_discount_workspace_bytes(B, T), dev, ("return", B, T), (), workspace)
     st = lib().memoroid_discounted_return(r.data_ptr(), start.data_ptr(), float(gamma), G.data_ptr(), B, T,
                                           ws.data_ptr(), ws.numel(), _stream_ptr(dev))
     _raise(st, "memoroid_discounted_return")
@@ -541,7 +541,7 @@ def gae(r, value, start, gamma: float, lam: float, value_next=None, done=None, t
             raise TypeError("start and done must be uint8")
     adv = torch.empty((B, T), dtype=torch.float32, device=dev)
     tg = torch.empty((B, T), dtype=torch.float32, device=dev) if target else None
-    ws = _prepared(lib().memoroid_discount_workspace_bytes(B, T), dev, ("discount", B, T), (), workspace)
+    ws = _prepared(lib().memoroid_discount_workspace_bytes(B, T), dev, ("gae", B, T), (), workspace)
     st = lib().memoroid_gae(r.data_ptr(), value.data_ptr(),
                             value_next.data_ptr() if value_next is not None else None,
                             done.data_ptr() if done is not None else None, start.data_ptr(),

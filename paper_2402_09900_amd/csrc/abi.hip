@@ -775,8 +775,8 @@ struct DiscPlan {
 };
 
 // header, per-tile epoch words, then two banks of tile words
-bool plan_disc(int64_t B, int64_t T, DiscPlan* p) {
-    p->nt = (T + kDiscTile - 1) / kDiscTile;
+bool plan_disc(int64_t B, int64_t T, bool gae, DiscPlan* p) {
+    p->nt = (T + disc_tile(gae) - 1) / disc_tile(gae);
     if (!mul_ok(B, p->nt, &p->ntiles) || p->ntiles >= (int64_t)INT32_MAX) return false;
     size_t off = kAlign;
     p->off_epoch = off;
@@ -826,7 +826,7 @@ int disc_run(const float* r, const float* value, const float* value_next, const 
                      (!value || aligned(value, 16)) && (!value_next || aligned(value_next, 16)) &&
                      (!done || aligned(done, 4)) && (!target || aligned(target, 16));
     DiscPlan p;
-    if (!plan_disc(B, T, &p)) return MEMOROID_EUNSUPPORTED;
+    if (!plan_disc(B, T, gae, &p)) return MEMOROID_EUNSUPPORTED;
     if (!workspace || workspace_bytes < p.total) return MEMOROID_EWORKSPACE;
     if (!aligned(workspace, 16)) return MEMOROID_EINVAL;
     hipStream_t s = (hipStream_t)stream;
@@ -849,8 +849,8 @@ int disc_run(const float* r, const float* value, const float* value_next, const 
     args.incl = (uint64_t*)(ws + p.off_incl);
     args.bank = (int64_t)p.bank_bytes;
     args.hdr = (WsHeader*)ws;
-    // the return and the advantage share one layout (and may share a workspace)
-    args.sig = layout_sig({kSigDiscount, B, T});
+    // the return and the advantage tile differently: each binds its own workspace
+    args.sig = layout_sig({kSigDiscount, B, T, gae});
     args.epoch = (uint32_t*)(ws + p.off_epoch);
     return check_hip(disc_launch(vec, gae, args, p.ntiles, s));
 }
@@ -859,9 +859,9 @@ int disc_run(const float* r, const float* value, const float* value_next, const 
 
 size_t memoroid_discount_workspace_bytes(int64_t B, int64_t T) {
     if (B <= 0 || T <= 0) return 0;
-    DiscPlan p;
-    if (!plan_disc(B, T, &p)) return 0;
-    return p.total;
+    DiscPlan pr, pg;
+    if (!plan_disc(B, T, false, &pr) || !plan_disc(B, T, true, &pg)) return 0;
+    return pr.total > pg.total ? pr.total : pg.total;
 }
 
 int memoroid_discounted_return(const float* r, const uint8_t* start, float gamma, float* G, int64_t B, int64_t T,

@@ -34,9 +34,6 @@ namespace memoroid {
 
 namespace {
 
-constexpr int kRows = kDiscRows;              // steps per lane
-constexpr int kSeg = 64 * kRows;              // steps per wavefront
-static_assert(kDiscTile == 4 * kSeg, "tile = 4 wavefronts");
 
 struct RMap {
     float A, H;
@@ -168,11 +165,12 @@ template <int VEC, bool GAE>
 __device__ __forceinline__ RMap tile_map_from_inputs(const DiscArgs& p, int64_t row, int64_t tile) {
     typedef typename F<VEC>::T V;
     const int lane = threadIdx.x & 63;
-    constexpr int runs = kDiscTile / (64 * VEC);
+    constexpr int kTile = disc_tile(GAE);
+    constexpr int runs = kTile / (64 * VEC);
     RMap TM = rmap_id();
 #pragma unroll 1
     for (int s = runs - 1; s >= 0; --s) {
-        const int64_t t0 = tile * kDiscTile + (int64_t)64 * VEC * s + VEC * lane;
+        const int64_t t0 = tile * kTile + (int64_t)64 * VEC * s + VEC * lane;
         const bool ok = t0 < p.T;
         V x{}, vv{}, vn{};
         uint32_t fl = 0, dn = 0, next_fl = 1;
@@ -199,6 +197,9 @@ __device__ __forceinline__ RMap tile_map_from_inputs(const DiscArgs& p, int64_t 
 
 template <int VEC, bool GAE>
 __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
+    constexpr int kRows = disc_rows(GAE);     // steps per lane
+    constexpr int kSeg = 64 * kRows;          // steps per wavefront
+    constexpr int kTile = disc_tile(GAE);
     constexpr int NB = kRows / VEC;           // loads per lane
     typedef typename F<VEC>::T V;
     __shared__ float s_wA[4], s_wH[4];
@@ -217,7 +218,7 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
     const int64_t i = p.nt - 1 - j;           // tile index from the tape's start
     const int64_t T = p.T;
     const int64_t row = b * T;
-    const int64_t t_seg = i * kDiscTile + (int64_t)w * kSeg;
+    const int64_t t_seg = i * kTile + (int64_t)w * kSeg;
     const int64_t t_after = t_seg + kSeg;     // first step after this wavefront's steps
 
     // ------------------------------------------------------------- loads
@@ -307,7 +308,7 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
     }
     if (w == 0) {
         // a carry is needed unless the tile's last step ends an episode
-        const int64_t t_next_tile = (i + 1) * (int64_t)kDiscTile;
+        const int64_t t_next_tile = (i + 1) * (int64_t)kTile;
         const bool need = j > 0 && p.start[row + t_next_tile] == 0;
         float carry = 0.0f;
         if (need) {

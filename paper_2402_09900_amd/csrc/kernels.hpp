@@ -198,8 +198,10 @@ hipError_t linattn_bwd_summary_launch(const LinBwdArgs& a, hipStream_t s);
 hipError_t linattn_bwd_grad_launch(const LinBwdArgs& a, hipStream_t s);
 
 // ------------------------------------------- discounted return and GAE
-constexpr int kDiscRows = 16;                       // steps per lane
-constexpr int kDiscTile = 4 * 64 * kDiscRows;       // steps per tile (4 wavefronts)
+// Steps per lane: 32 for the return (two streams in registers), 16 for the
+// advantage (four); a tile is 4 wavefronts of 64 lanes.
+constexpr int disc_rows(bool gae) { return gae ? 16 : 32; }
+constexpr int disc_tile(bool gae) { return 4 * 64 * disc_rows(gae); }
 
 struct DiscArgs {
     const float* r;          // [B][T] rewards

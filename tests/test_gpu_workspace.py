@@ -1,8 +1,8 @@
 """The prepared-workspace protocol of the single-kernel entry points, through
 the C ABI: one preparation, then many calls with the same sizes and no
 initialisation in between (the descriptor words alternate between two banks
-from call to call, so four calls use each bank twice); a workspace shared by
-the discounted return and GAE; a call with other sizes on a bound workspace
+from call to call, so four calls use each bank twice); return and GAE calls
+interleaved on their own workspaces; a call with other sizes on a bound workspace
 (stands down and reports MEMOROID_EMISMATCH); memory that was never prepared.
 Every result is compared with the fp64 oracle (conditioned relative error,
 1e-4 for fp32 arithmetic; indices bit-exact)."""
@@ -129,29 +129,51 @@ def test_ffm_forward_and_gradient_repeated_calls():
     assert status(wsf) == mb.OK and status(wsb) == mb.OK
 
 
-def test_return_and_gae_share_a_prepared_workspace():
+def _return_call(tp, ws, B, T):
+    r, s = dev(tp.r), dev(tp.start)
+    out = torch.empty((B, T), dtype=torch.float32, device=DEV)
+    assert mb.memoroid_discounted_return(r.data_ptr(), s.data_ptr(), 0.97, out.data_ptr(), B, T, ws.data_ptr(),
+                                         ws.numel(), stream()) == mb.OK
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def _gae_call(tp, ws, B, T):
+    r, v, vn, dn, s = dev(tp.r), dev(tp.v), dev(tp.vn), dev(tp.done), dev(tp.start)
+    out = torch.empty((B, T), dtype=torch.float32, device=DEV)
+    assert mb.memoroid_gae(r.data_ptr(), v.data_ptr(), vn.data_ptr(), dn.data_ptr(), s.data_ptr(), 0.99, 0.95,
+                           out.data_ptr(), None, B, T, ws.data_ptr(), ws.numel(), stream()) == mb.OK
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def test_return_and_gae_repeated_calls_interleaved():
+    """The return and the advantage tile differently, so each binds its own
+    workspace; their calls interleave on the same stream."""
     B, T = 2, 70000
-    ws = prepared(mb.memoroid_discount_workspace_bytes(B, T))
+    wsr = prepared(mb.memoroid_discount_workspace_bytes(B, T))
+    wsg = prepared(mb.memoroid_discount_workspace_bytes(B, T))
     for call in range(CALLS):
         tp = tapes.make_discount(6, seed=900 + call, B=B, T=T)
-        r, v, vn, dn, s = dev(tp.r), dev(tp.v), dev(tp.vn), dev(tp.done), dev(tp.start)
-        out = torch.empty((B, T), dtype=torch.float32, device=DEV)
-        if call % 2 == 0:
-            announce("workspace return call %d" % call)
-            assert mb.memoroid_discounted_return(r.data_ptr(), s.data_ptr(), 0.97, out.data_ptr(), B, T,
-                                                 ws.data_ptr(), ws.numel(), stream()) == mb.OK
-            ref, m = oracle.discounted_return(tp.r.astype(np.float64), tp.start, float(np.float32(0.97)))
-        else:
-            announce("workspace gae call %d" % call)
-            assert mb.memoroid_gae(r.data_ptr(), v.data_ptr(), vn.data_ptr(), dn.data_ptr(), s.data_ptr(), 0.99,
-                                   0.95, out.data_ptr(), None, B, T, ws.data_ptr(), ws.numel(),
-                                   stream()) == mb.OK
-            ref, _, m, _ = oracle.gae(tp.r.astype(np.float64), tp.v.astype(np.float64), tp.start,
-                                      float(np.float32(0.99)), float(np.float32(0.95)),
-                                      vn=tp.vn.astype(np.float64), done=tp.done)
-        torch.cuda.synchronize()
-        assert cond_err(out.cpu().numpy(), ref, m) <= TOL, call
+        announce("workspace return and gae call %d" % call)
+        ref, m = oracle.discounted_return(tp.r.astype(np.float64), tp.start, float(np.float32(0.97)))
+        assert cond_err(_return_call(tp, wsr, B, T), ref, m) <= TOL, call
+        ref, _, m, _ = oracle.gae(tp.r.astype(np.float64), tp.v.astype(np.float64), tp.start,
+                                  float(np.float32(0.99)), float(np.float32(0.95)),
+                                  vn=tp.vn.astype(np.float64), done=tp.done)
+        assert cond_err(_gae_call(tp, wsg, B, T), ref, m) <= TOL, call
+    assert status(wsr) == mb.OK and status(wsg) == mb.OK
+
+
+def test_gae_on_a_return_workspace_reports_mismatch():
+    B, T = 1, 50000
+    ws = prepared(mb.memoroid_discount_workspace_bytes(B, T))
+    tp = tapes.make_discount(6, seed=950, B=B, T=T)
+    announce("workspace return binds, gae mismatches")
+    _return_call(tp, ws, B, T)
     assert status(ws) == mb.OK
+    _gae_call(tp, ws, B, T)
+    assert status(ws) == mb.EMISMATCH
 
 
 def test_begin_indices_repeated_calls():
