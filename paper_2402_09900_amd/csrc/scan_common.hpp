@@ -601,9 +601,11 @@ __device__ __forceinline__ void wave_group_scan(Seg<S, VEC>& inc, Seg<S, VEC>& e
 // minus one), carried by one 64-bit word per tile: all ones = not yet
 // published, bit 62 = the tile's own count, bit 63 = the count through the
 // end of the tile; the low 32 bits hold the value.  A count never resets, so
-// the walk always goes back to an inclusive word; one wavefront polls 64
-// predecessors per round trip (lane l: predecessor base - l * stride) and the
-// ready prefix of the window is summed with cross-lane reductions.
+// the walk always goes back to an inclusive word; one wavefront polls a
+// window of 256 predecessors per round trip (position o = 64 k + lane is
+// predecessor base - o * stride) and the ready prefix of the window is summed
+// with cross-lane reductions.  The wide window matters when a thousand tiles
+// run at once: a running count then crosses them in a few round trips.
 constexpr uint64_t kCountOwn = 1ull << 62;
 constexpr uint64_t kCountIncl = 2ull << 62;
 
@@ -613,30 +615,52 @@ __device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
     return v;
 }
 
+constexpr int kCountWin = 4;      // blocks of 64 predecessors per round trip
+
+// One round trip of a count look-back from predecessor `base`: `sum` gets the
+// counts of the window's ready prefix (through the nearest inclusive word, or
+// up to the nearest unpublished one) and `used` the positions consumed;
+// returns true when an inclusive word closed the walk.  Positions before the
+// first tile of the tape read as an inclusive zero.
+__device__ __forceinline__ bool count_window(const uint64_t* desc, int64_t base, int64_t stride, uint32_t& sum,
+                                             int& used) {
+    const int lane = threadIdx.x & 63;
+    uint64_t w[kCountWin];
+#pragma unroll
+    for (int k = 0; k < kCountWin; ++k) {
+        const int64_t i = base - (int64_t)(64 * k + lane) * stride;
+        w[k] = i >= 0 ? peek64(desc + i) : kCountIncl;
+    }
+    int fi = 64 * kCountWin, fe = 64 * kCountWin;       // first inclusive / unpublished position
+#pragma unroll
+    for (int k = kCountWin - 1; k >= 0; --k) {          // the nearest block wins
+        const bool empty = w[k] == kEmpty64;
+        const uint64_t me = __ballot(empty);
+        const uint64_t mi = __ballot(!empty && (w[k] & kCountIncl) != 0);
+        if (me) fe = 64 * k + __builtin_ctzll(me);
+        if (mi) fi = 64 * k + __builtin_ctzll(mi);
+    }
+    const bool stop = fi < fe;
+    used = stop ? fi + 1 : fe;
+    uint32_t mine = 0;
+#pragma unroll
+    for (int k = 0; k < kCountWin; ++k) mine += 64 * k + lane < used ? (uint32_t)w[k] : 0u;
+    sum = wave_sum_u32(mine);
+    return stop;
+}
+
 __device__ __forceinline__ uint32_t count_lookback(const uint64_t* desc, int64_t first_pred, int64_t stride,
                                                    uint32_t* timeout) {
-    const int lane = threadIdx.x & 63;
     uint32_t acc = 0;
     int64_t base = first_pred;
     uint32_t polls = 0;
     while (true) {
-        const int64_t i = base - (int64_t)lane * stride;
-        // before the first tile of the tape the count is an inclusive zero
-        const uint64_t w = i >= 0 ? peek64(desc + i) : kCountIncl;
-        const bool empty = w == kEmpty64;
-        const bool incl = !empty && (w & kCountIncl) != 0;
-        const uint64_t m_empty = __ballot(empty);
-        const uint64_t m_incl = __ballot(incl);
-        const int first_incl = m_incl ? __builtin_ctzll(m_incl) : 64;
-        const int first_empty = m_empty ? __builtin_ctzll(m_empty) : 64;
-        if (first_incl < first_empty) {
-            const uint32_t mine = lane <= first_incl ? (uint32_t)w : 0u;
-            return acc + wave_sum_u32(mine);
-        }
-        const uint32_t mine = lane < first_empty ? (uint32_t)w : 0u;
-        acc += wave_sum_u32(mine);
-        base -= (int64_t)first_empty * stride;
-        if (first_empty == 0) {
+        uint32_t s;
+        int used;
+        if (count_window(desc, base, stride, s, used)) return acc + s;
+        acc += s;
+        base -= (int64_t)used * stride;
+        if (used == 0) {
             if (++polls > kMaxPolls) {
                 flag_timeout(timeout);
                 return acc;

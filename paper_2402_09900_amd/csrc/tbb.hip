@@ -105,18 +105,11 @@ __global__ __launch_bounds__(256) void tbb_begins_kernel(TbbBeginArgs p) {
             int64_t base = tile - 1;
             uint32_t polls = 0;
             while (true) {
-                const int64_t i = base - lane;
-                const uint64_t word = i >= 0 ? peek64(cnt + i) : kCountIncl;
-                const bool empty = word == kEmpty64;
-                const bool inc = !empty && (word & kCountIncl) != 0;
-                const uint64_t m_empty = __ballot(empty), m_incl = __ballot(inc);
-                const int fi = m_incl ? __builtin_ctzll(m_incl) : 64;
-                const int fe = m_empty ? __builtin_ctzll(m_empty) : 64;
-                if (fi < fe) {
-                    acc += wave_sum_u32(lane <= fi ? (uint32_t)word : 0u);
-                    break;
-                }
-                acc += wave_sum_u32(lane < fe ? (uint32_t)word : 0u);
+                uint32_t sum;
+                int fe;
+                const bool stop = count_window(cnt, base, 1, sum, fe);
+                acc += sum;
+                if (stop) break;
                 base -= fe;
                 if (fe > 0) {
                     polls = 0;
