@@ -293,7 +293,7 @@ def setup_tbb(torch, mb, tapes, key):
     n, row = tb.D.shape
     K = tb.draws.size
     nbi = mb.memoroid_tbb_begin_indices_workspace_bytes(n)
-    nbs = mb.memoroid_tbb_sample_workspace_bytes(K)
+    nbs = mb.memoroid_tbb_sample_workspace_bytes(K, tb.batch)
     stream = lambda: torch.cuda.current_stream().cuda_stream  # noqa: E731
     row_bytes = row * 4
     sets = []
@@ -308,7 +308,7 @@ def setup_tbb(torch, mb, tapes, key):
         osrc = torch.empty(tb.batch, dtype=torch.int64, device="cuda")
         filled = torch.empty(1, dtype=torch.int64, device="cuda")
         wsi = prepared_ws(torch, mb, nbi)
-        wss = torch.empty(nbs, dtype=torch.uint8, device="cuda")
+        wss = prepared_ws(torch, mb, nbs)
 
         def insert(s=s, idx=idx, cnt=cnt, wsi=wsi):
             st = mb.memoroid_tbb_begin_indices(s.data_ptr(), n, 0, idx.data_ptr(), cnt.data_ptr(), wsi.data_ptr(),

@@ -43,8 +43,9 @@
  *    workspaces.  Two kinds of call:
  *      * PREPARED (memoroid_scan_diag, _diag_bwd, _ffm, _ffm_bwd,
  *        memoroid_discounted_return, memoroid_gae,
- *        memoroid_tbb_begin_indices): the call is one kernel launch and
- *        initialises nothing.  The workspace must have been prepared with
+ *        memoroid_tbb_begin_indices, memoroid_tbb_sample): the call
+ *        initialises nothing in the workspace (sampling runs two kernels,
+ *        the others one).  The workspace must have been prepared with
  *        memoroid_workspace_prepare() (on a stream ordered before the call)
  *        and then used only by calls of this library.  The first call binds
  *        it to that entry point and those sizes; every later call with the same entry
@@ -57,9 +58,9 @@
  *        MEMOROID_EMISMATCH, and the workspace must be prepared again before
  *        any further use.  Prepare it again as well after
  *        MEMOROID_ETIMEOUT, and after any other writes to its memory.
- *      * SELF-INITIALISING (memoroid_scan_linattn, _linattn_bwd,
- *        memoroid_tbb_sample): contents undefined on entry and on exit; the
- *        call initialises what it needs on `stream`.
+ *      * SELF-INITIALISING (memoroid_scan_linattn, _linattn_bwd): contents
+ *        undefined on entry and on exit; the call initialises what it needs
+ *        on `stream`.
  */
 #ifndef MEMOROID_H
 #define MEMOROID_H
@@ -71,7 +72,7 @@
 extern "C" {
 #endif
 
-#define MEMOROID_ABI_VERSION 2
+#define MEMOROID_ABI_VERSION 3
 
 typedef enum {
     MEMOROID_OK = 0,
@@ -358,12 +359,17 @@ int memoroid_tbb_begin_indices(const uint8_t* start, int64_t n, int64_t offset,
  *              length of the drawn episodes).  Rows past it are zero, with
  *              out_start 0.  Since every episode has at least one row,
  *              n_draws >= batch always fills the batch.
- *   n_draws <= 2^24 and row_bytes <= 2^24 (MEMOROID_EUNSUPPORTED otherwise).
- *   Rows move in 16-byte
- *   units when row_bytes % 16 == 0 and D, out are 16-byte aligned.
- *   Workspace (self-initialising): memoroid_tbb_sample_workspace_bytes(n_draws) (0 when n_draws is 0).
+ *   n_draws <= 2^24, row_bytes <= 2^24, batch < 2^47 and n_D < 2^47
+ *   (MEMOROID_EUNSUPPORTED otherwise).  Rows move in 16-byte units when
+ *   row_bytes % 16 == 0 and D, out are 16-byte aligned.
+ *   Workspace (prepared, bound to n_draws and batch):
+ *   memoroid_tbb_sample_workspace_bytes(n_draws, batch); not used when
+ *   n_draws or batch is 0.  It holds, per call, where each draw starts in
+ *   the batch and which draw holds the first row of each group of 256
+ *   output rows.  A call that finds it bound to other sizes writes no
+ *   output (memoroid_workspace_status reports MEMOROID_EMISMATCH).
  * ------------------------------------------------------------------------ */
-size_t memoroid_tbb_sample_workspace_bytes(int64_t n_draws);
+size_t memoroid_tbb_sample_workspace_bytes(int64_t n_draws, int64_t batch);
 
 int memoroid_tbb_sample(const void* D, int64_t n_D, int64_t row_bytes,
                         const int64_t* I, int64_t n_I, const int64_t* draws, int64_t n_draws,
@@ -387,9 +393,8 @@ int memoroid_workspace_prepare(void* workspace, size_t workspace_bytes, void* st
  * returns MEMOROID_OK; MEMOROID_EMISMATCH if a call found the workspace
  * bound to another call (that call's outputs are invalid); MEMOROID_ETIMEOUT
  * if a kernel's bounded wait for a predecessor tile gave up (its outputs are
- * then invalid); MEMOROID_EHIP if the copy failed.  Meaningless for a
- * memoroid_tbb_sample workspace, which holds no header.  Intended for tests
- * and debugging.
+ * then invalid); MEMOROID_EHIP if the copy failed.  Intended for tests and
+ * debugging.
  * ------------------------------------------------------------------------ */
 int memoroid_workspace_status(const void* workspace, size_t workspace_bytes, void* stream);
 

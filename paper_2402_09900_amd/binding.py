@@ -81,7 +81,7 @@ def lib() -> ctypes.CDLL:
         L.memoroid_tbb_begin_indices.restype = I32
         L.memoroid_tbb_begin_indices.argtypes = [P, I64, I64, P, P, P, SZ, P]
         L.memoroid_tbb_sample_workspace_bytes.restype = SZ
-        L.memoroid_tbb_sample_workspace_bytes.argtypes = [I64]
+        L.memoroid_tbb_sample_workspace_bytes.argtypes = [I64, I64]
         L.memoroid_tbb_sample.restype = I32
         L.memoroid_tbb_sample.argtypes = [P, I64, I64, P, I64, P, I64, I64, P, P, P, P, P, SZ, P]
         L.memoroid_discount_workspace_bytes.restype = SZ
@@ -173,8 +173,8 @@ def memoroid_tbb_begin_indices(start, n, offset, indices, count, workspace, work
     return lib().memoroid_tbb_begin_indices(start, n, offset, indices, count, workspace, workspace_bytes, stream)
 
 
-def memoroid_tbb_sample_workspace_bytes(n_draws) -> int:
-    return lib().memoroid_tbb_sample_workspace_bytes(n_draws)
+def memoroid_tbb_sample_workspace_bytes(n_draws, batch) -> int:
+    return lib().memoroid_tbb_sample_workspace_bytes(n_draws, batch)
 
 
 def memoroid_tbb_sample(D, n_D, row_bytes, I, n_I, draws, n_draws, batch, out, out_start, out_src, filled,
@@ -462,7 +462,8 @@ def tbb_sample(D, I, draws, batch: int, workspace=None):
     out_src = torch.empty(batch, dtype=torch.int64, device=dev)
     filled = torch.empty(1, dtype=torch.int64, device=dev)
     nd = draws.numel()
-    ws = _workspace(lib().memoroid_tbb_sample_workspace_bytes(nd), dev, workspace)
+    ws = _prepared(lib().memoroid_tbb_sample_workspace_bytes(nd, batch), dev, ("tbb_sample", nd, batch), (),
+                   workspace)
     st = lib().memoroid_tbb_sample(D.data_ptr(), n_D, row_bytes, I.data_ptr(), I.numel(), draws.data_ptr(), nd,
                                    batch, out.data_ptr(), out_start.data_ptr(), out_src.data_ptr(),
                                    filled.data_ptr(), ws.data_ptr(), ws.numel(), _stream_ptr(dev))

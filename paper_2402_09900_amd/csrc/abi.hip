@@ -64,7 +64,7 @@ uint64_t layout_sig(std::initializer_list<int64_t> vals) {
 
 // entry points in a signature
 enum SigKind : int64_t { kSigDiag = 1, kSigDiagBwd, kSigFfm, kSigFfmBwd, kSigDiscount, kSigTbbBegins,
-                         kSigLinattn, kSigLinattnBwd };
+                         kSigLinattn, kSigLinattnBwd, kSigTbbSample };
 
 // Tiling and workspace layout of a diagonal scan.  `vec` selects the
 // vectorised lane width; `state_complex` picks the descriptor size.
@@ -901,6 +901,30 @@ void plan_tbb(int64_t n, TbbPlan* p) {
     p->total = p->off_cnt + 2 * p->bank_bytes;
 }
 
+// Sampling workspace: header, epoch words, two banks of row-sum words, the
+// rows filled and draws inside the batch, the group table, and each draw's
+// first batch row and source shift.
+struct SamplePlan {
+    int64_t ntiles = 0, groups = 0;
+    size_t off_epoch = 0, off_cnt = 0, bank_bytes = 0, off_meta = 0, off_first = 0, off_row0 = 0, off_shift = 0,
+           total = 0;
+};
+
+constexpr int64_t kSampleMaxRows = (int64_t)1 << 47;   // batch and n_D bound: row sums stay below 2^48
+
+void plan_sample(int64_t n_draws, int64_t batch, SamplePlan* p) {
+    p->ntiles = (n_draws + kTbbDrawTile - 1) / kTbbDrawTile;
+    p->groups = (batch + kTbbRowsPerGroup - 1) / kTbbRowsPerGroup;
+    p->off_epoch = kAlign;
+    p->off_cnt = align_up(p->off_epoch + (size_t)p->ntiles * 4);
+    p->bank_bytes = align_up((size_t)p->ntiles * 8);
+    p->off_meta = p->off_cnt + 2 * p->bank_bytes;
+    p->off_first = align_up(p->off_meta + 16);
+    p->off_row0 = align_up(p->off_first + (size_t)p->groups * 8);
+    p->off_shift = align_up(p->off_row0 + (size_t)n_draws * 8);
+    p->total = align_up(p->off_shift + (size_t)n_draws * 8);
+}
+
 }  // namespace
 
 size_t memoroid_tbb_begin_indices_workspace_bytes(int64_t n) {
@@ -948,10 +972,11 @@ int memoroid_tbb_begin_indices(const uint8_t* start, int64_t n, int64_t offset, 
     return check_hip(tbb_begins_launch(vec, a, p.ntiles, s));
 }
 
-size_t memoroid_tbb_sample_workspace_bytes(int64_t n_draws) {
-    if (n_draws < 0 || n_draws > ((int64_t)1 << 24)) return 0;
-    const int64_t nb = (n_draws + kTbbDrawBlock - 1) / kTbbDrawBlock;
-    return align_up((size_t)n_draws * 8) + 2 * align_up((size_t)(nb > 0 ? nb : 1) * 8);
+size_t memoroid_tbb_sample_workspace_bytes(int64_t n_draws, int64_t batch) {
+    if (n_draws < 0 || n_draws > ((int64_t)1 << 24) || batch < 0 || batch >= kSampleMaxRows) return 0;
+    SamplePlan p;
+    plan_sample(n_draws, batch, &p);
+    return p.total;
 }
 
 int memoroid_tbb_sample(const void* D, int64_t n_D, int64_t row_bytes, const int64_t* I, int64_t n_I,
@@ -961,6 +986,7 @@ int memoroid_tbb_sample(const void* D, int64_t n_D, int64_t row_bytes, const int
     if (n_draws > ((int64_t)1 << 24) || row_bytes > ((int64_t)1 << 24)) return MEMOROID_EUNSUPPORTED;
     int64_t tmp;
     if (!mul_ok(batch, row_bytes, &tmp) || !mul_ok(n_D, row_bytes, &tmp)) return MEMOROID_EINVAL;
+    if (batch >= kSampleMaxRows || n_D >= kSampleMaxRows) return MEMOROID_EUNSUPPORTED;
     if (n_draws > 0 && (!I || !draws || n_I == 0)) return MEMOROID_EINVAL;
     if (n_draws > 0 && n_D > 0 && !D) return MEMOROID_EINVAL;
     if (batch > 0 && (!out || !out_start)) return MEMOROID_EINVAL;
@@ -972,11 +998,10 @@ int memoroid_tbb_sample(const void* D, int64_t n_D, int64_t row_bytes, const int
         return MEMOROID_EINVAL;
     hipStream_t s = (hipStream_t)stream;
     if (batch == 0) return filled ? check_hip(store_i64_launch(filled, 0, s)) : MEMOROID_OK;
-    const size_t need = memoroid_tbb_sample_workspace_bytes(n_draws);
-    if (n_draws > 0 && (!workspace || workspace_bytes < need)) return MEMOROID_EWORKSPACE;
+    SamplePlan p;
+    plan_sample(n_draws, batch, &p);
+    if (n_draws > 0 && (!workspace || workspace_bytes < p.total)) return MEMOROID_EWORKSPACE;
     if (workspace && !aligned(workspace, 16)) return MEMOROID_EINVAL;
-    const int64_t nb = (n_draws + kTbbDrawBlock - 1) / kTbbDrawBlock;
-    char* ws = (char*)workspace;
     TbbSampleArgs a{};
     a.D = D;
     a.n_D = n_D;
@@ -990,15 +1015,22 @@ int memoroid_tbb_sample(const void* D, int64_t n_D, int64_t row_bytes, const int
     a.out_start = out_start;
     a.out_src = out_src;
     a.filled = filled;
-    a.nblocks = nb;
     if (n_draws > 0) {
-        a.ends = (int64_t*)ws;
-        a.block_tot = (int64_t*)(ws + align_up((size_t)n_draws * 8));
-        a.block_off = (int64_t*)(ws + align_up((size_t)n_draws * 8) + align_up((size_t)nb * 8));
+        char* ws = (char*)workspace;
+        a.hdr = (WsHeader*)ws;
+        a.sig = layout_sig({kSigTbbSample, n_draws, batch});
+        a.epoch = (uint32_t*)(ws + p.off_epoch);
+        a.cnt = (uint64_t*)(ws + p.off_cnt);
+        a.bank = (int64_t)p.bank_bytes;
+        a.meta = (int64_t*)(ws + p.off_meta);
+        a.first = (int64_t*)(ws + p.off_first);
+        a.row0 = (int64_t*)(ws + p.off_row0);
+        a.shift = (int64_t*)(ws + p.off_shift);
+        a.fallback_polls = fallback_polls();
     }
     const int unit = (row_bytes % 16 == 0 && aligned(out, 16) && (!D || aligned(D, 16))) ? 16
                      : (row_bytes % 4 == 0 && aligned(out, 4) && (!D || aligned(D, 4))) ? 4 : 1;
-    return check_hip(tbb_sample_launch(unit, a, s));
+    return check_hip(tbb_sample_launch(unit, a, p.ntiles, s));
 }
 
 int memoroid_workspace_prepare(void* workspace, size_t workspace_bytes, void* stream) {

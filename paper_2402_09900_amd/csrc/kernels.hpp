@@ -227,8 +227,14 @@ hipError_t disc_launch(bool vec, bool gae, const DiscArgs& a, int64_t ntiles, hi
 
 // ------------------------------------------------ tape-based batching
 constexpr int kTbbBeginTile = 16384;      // flags per workgroup of the compaction
-constexpr int kTbbDrawBlock = 1024;       // draws per workgroup of the length sums
-constexpr int kTbbRowsPerGroup = 1024;    // output rows per workgroup of the gather
+#ifndef MEMOROID_TBB_DRAW_TILE
+#define MEMOROID_TBB_DRAW_TILE 2048
+#endif
+#ifndef MEMOROID_TBB_ROWS_PER_GROUP
+#define MEMOROID_TBB_ROWS_PER_GROUP 256
+#endif
+constexpr int kTbbDrawTile = MEMOROID_TBB_DRAW_TILE;          // draws per workgroup of the row sums
+constexpr int kTbbRowsPerGroup = MEMOROID_TBB_ROWS_PER_GROUP; // output rows per workgroup of the gather
 
 struct TbbBeginArgs {
     const uint8_t* start;    // [n] begin flags
@@ -258,12 +264,19 @@ struct TbbSampleArgs {
     uint8_t* out_start;      // [batch]
     int64_t* out_src;        // [batch] or NULL
     int64_t* filled;         // one value or NULL
-    int64_t* ends;           // [n_draws] workspace: running ends within blocks
-    int64_t* block_tot;      // [nblocks] workspace
-    int64_t* block_off;      // [nblocks] workspace
-    int64_t nblocks;
+    // workspace
+    WsHeader* hdr;
+    uint64_t sig;
+    uint32_t* epoch;         // [tiles] per-tile epoch words
+    uint64_t* cnt;           // [tiles] row-sum descriptor words (bank 0)
+    int64_t bank;            // bytes from bank 0 to bank 1
+    int64_t* meta;           // [2]: rows filled; draws whose first row is inside the batch
+    int64_t* first;          // [groups]: the draw holding each gather group's first row
+    int64_t* row0;           // [n_draws]: first batch row of each draw (draws inside the batch)
+    int64_t* shift;          // [n_draws]: source row minus batch row (same draws)
+    uint32_t fallback_polls;
 };
 
-hipError_t tbb_sample_launch(int unit, const TbbSampleArgs& a, hipStream_t s);
+hipError_t tbb_sample_launch(int unit, const TbbSampleArgs& a, int64_t ntiles, hipStream_t s);
 
 }  // namespace memoroid

@@ -600,20 +600,31 @@ __device__ __forceinline__ void wave_group_scan(Seg<S, VEC>& inc, Seg<S, VEC>& e
 // Running count of begin steps before a tile (the episode index is that count
 // minus one), carried by one 64-bit word per tile: all ones = not yet
 // published, bit 62 = the tile's own count, bit 63 = the count through the
-// end of the tile; the low 32 bits hold the value.  A count never resets, so
-// the walk always goes back to an inclusive word; one wavefront polls a
-// window of 256 predecessors per round trip (position o = 64 k + lane is
-// predecessor base - o * stride) and the ready prefix of the window is summed
-// with cross-lane reductions.  The wide window matters when a thousand tiles
-// run at once: a running count then crosses them in a few round trips.
+// end of the tile; the low 62 bits hold the value (under 2^32 for a count
+// of begin steps, under 2^48 for the row sums of batch sampling).  A count
+// never resets, so the walk always goes back to an inclusive word; one
+// wavefront polls a window of 256 predecessors per round trip (position
+// o = 64 k + lane is predecessor base - o * stride) and the ready prefix of
+// the window is summed with cross-lane reductions.  The wide window matters
+// when a thousand tiles run at once: a running count then crosses them in a
+// few round trips.
 constexpr uint64_t kCountOwn = 1ull << 62;
 constexpr uint64_t kCountIncl = 2ull << 62;
+constexpr uint64_t kCountValue = kCountOwn - 1;
 
 __device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) v += (uint32_t)__shfl_xor((int)v, off, 64);
     return v;
 }
+
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += (uint64_t)__shfl_xor((long long)v, off, 64);
+    return v;
+}
+__device__ __forceinline__ uint32_t wave_sum(uint32_t v) { return wave_sum_u32(v); }
+__device__ __forceinline__ uint64_t wave_sum(uint64_t v) { return wave_sum_u64(v); }
 
 constexpr int kCountWin = 4;      // blocks of 64 predecessors per round trip
 
@@ -622,8 +633,8 @@ constexpr int kCountWin = 4;      // blocks of 64 predecessors per round trip
 // up to the nearest unpublished one) and `used` the positions consumed;
 // returns true when an inclusive word closed the walk.  Positions before the
 // first tile of the tape read as an inclusive zero.
-__device__ __forceinline__ bool count_window(const uint64_t* desc, int64_t base, int64_t stride, uint32_t& sum,
-                                             int& used) {
+template <typename V>
+__device__ __forceinline__ bool count_window(const uint64_t* desc, int64_t base, int64_t stride, V& sum, int& used) {
     const int lane = threadIdx.x & 63;
     uint64_t w[kCountWin];
 #pragma unroll
@@ -642,10 +653,10 @@ __device__ __forceinline__ bool count_window(const uint64_t* desc, int64_t base,
     }
     const bool stop = fi < fe;
     used = stop ? fi + 1 : fe;
-    uint32_t mine = 0;
+    V mine = 0;
 #pragma unroll
-    for (int k = 0; k < kCountWin; ++k) mine += 64 * k + lane < used ? (uint32_t)w[k] : 0u;
-    sum = wave_sum_u32(mine);
+    for (int k = 0; k < kCountWin; ++k) mine += 64 * k + lane < used ? (V)(w[k] & kCountValue) : (V)0;
+    sum = wave_sum(mine);
     return stop;
 }
 

@@ -11,10 +11,12 @@
 // each tile keeps its own epoch word.
 //
 // Sampling concatenates the drawn episodes D[I[i] : I[i+1]] and cuts the
-// batch to B rows.  Three kernels: episode lengths with block-local
-// inclusive sums; a one-workgroup scan of the block totals; a gather in
-// which every output row finds its episode by binary search over the
-// running ends and copies its row.
+// batch to B rows.  Two kernels: a row-sum pass over the draws (the same
+// one-pass look-back, on sums saturated at B) that records where each draw
+// starts in the batch and which draw holds the first row of each group of
+// 256 output rows; then a gather in which every group reads its first draw
+// from that table, every row finds its draw by binary search over the next
+// 256 draws' first rows, and the workgroup copies the rows.
 #include <type_traits>
 
 #include "scan_common.hpp"
@@ -159,25 +161,24 @@ hipError_t tbb_begins_launch(bool vec, const TbbBeginArgs& a, int64_t ntiles, hi
 
 namespace {
 
-__device__ __forceinline__ int64_t draw_at(const TbbSampleArgs& p, int64_t k) {
+constexpr int kDrawsPerLane = kTbbDrawTile / 256;
+static_assert(kDrawsPerLane * 256 == kTbbDrawTile, "draw tile");
+
+// Episode of draw k: first source row `lo` and length `len` (0 past the last
+// draw).  The position is clamped into [0, n_I) and the episode's rows into
+// [0, n_D], so no index in I or draws can send a read outside D.
+__device__ __forceinline__ void draw_rows(const TbbSampleArgs& p, int64_t k, int64_t& lo, int64_t& len) {
+    lo = 0;
+    len = 0;
+    if (k >= p.n_draws) return;
     int64_t i = p.draws[k];
     i = i < 0 ? 0 : (i >= p.n_I ? p.n_I - 1 : i);
-    return i;
-}
-
-// Rows [lo, hi) of episode i, clamped into [0, n_D] so that no index in I
-// can send a read outside D.
-__device__ __forceinline__ void episode_rows(const TbbSampleArgs& p, int64_t i, int64_t& lo, int64_t& hi) {
-    lo = p.I[i];
-    hi = i + 1 < p.n_I ? p.I[i + 1] : p.n_D;
-    lo = lo < 0 ? 0 : (lo > p.n_D ? p.n_D : lo);
-    hi = hi < lo ? lo : (hi > p.n_D ? p.n_D : hi);
-}
-
-__device__ __forceinline__ int64_t episode_len(const TbbSampleArgs& p, int64_t i) {
-    int64_t lo, hi;
-    episode_rows(p, i, lo, hi);
-    return hi - lo;
+    int64_t a = p.I[i];
+    int64_t b = i + 1 < p.n_I ? p.I[i + 1] : p.n_D;
+    a = a < 0 ? 0 : (a > p.n_D ? p.n_D : a);
+    b = b < a ? a : (b > p.n_D ? p.n_D : b);
+    lo = a;
+    len = b - a;
 }
 
 __device__ __forceinline__ int64_t wave_incl_sum64(int64_t v) {
@@ -190,129 +191,191 @@ __device__ __forceinline__ int64_t wave_incl_sum64(int64_t v) {
     return v;
 }
 
-// running end of draw k's episode inside the batch (rows before + its length)
-__device__ __forceinline__ int64_t end_at(const TbbSampleArgs& p, int64_t k) {
-    return p.ends[k] + p.block_off[k / kTbbDrawBlock];
-}
+__device__ __forceinline__ uint64_t min_u64(uint64_t a, uint64_t b) { return a < b ? a : b; }
 
 }  // namespace
 
-// Episode lengths of the draws and their inclusive sums within blocks of
-// kTbbDrawBlock draws (256 lanes x 16 consecutive draws).
-__global__ __launch_bounds__(256) void tbb_lengths_kernel(TbbSampleArgs p) {
+// Row sums of the draws: tile = kTbbDrawTile consecutive draws (8 per
+// lane).  Each tile sums its episode lengths, publishes the sum, looks back
+// over earlier tiles for the rows before it (ordered by workgroup index, with
+// the same fallback as the compaction: an awaited tile that has not
+// published is summed here), and then, for every draw whose first row falls
+// inside the batch, writes that row and the source-row shift, the gather
+// groups whose first row it holds, and -- for the draw that reaches the end
+// of the batch, or the last tile if the draws fall short -- the rows filled.
+// Sums saturate at the batch size (min(a + b, batch) is associative), so they
+// stay exact below it and never overflow.
+__global__ __launch_bounds__(256) void tbb_rows_kernel(TbbSampleArgs p) {
+    constexpr int RW = kTbbRowsPerGroup;
     __shared__ int64_t s_wave[4];
-    constexpr int PER = kTbbDrawBlock / 256;
+    __shared__ uint64_t s_before;
+    __shared__ uint32_t s_bank;               // epoch parity; all ones: stand down
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int64_t k0 = (int64_t)blockIdx.x * kTbbDrawBlock + (int64_t)tid * PER;
-    int64_t len[PER];
+    const int64_t tile = blockIdx.x;
+    const uint64_t cap = (uint64_t)p.batch;
+    uint64_t sig_seen = 0;
+    uint32_t epoch = 0;
+    if (tid == 0) sig_seen = peek_sig(p.hdr);
+    const int64_t k0 = tile * kTbbDrawTile + (int64_t)tid * kDrawsPerLane;
+    int64_t lo[kDrawsPerLane], len[kDrawsPerLane];
     int64_t run = 0;
 #pragma unroll
-    for (int e = 0; e < PER; ++e) {
-        const int64_t k = k0 + e;
-        len[e] = k < p.n_draws ? episode_len(p, draw_at(p, k)) : 0;
+    for (int e = 0; e < kDrawsPerLane; ++e) {
+        draw_rows(p, k0 + e, lo[e], len[e]);
         run += len[e];
     }
+    if (tid == 0) epoch = read_epoch(p.epoch + tile);
     const int64_t incl = wave_incl_sum64(run);
     if (lane == 63) s_wave[w] = incl;
+    if (tid == 0) s_bank = ws_bound_to(p.hdr, p.sig, sig_seen, tile == 0) ? (epoch & 1u) : kEmpty32;
     __syncthreads();
-    int64_t before = incl - run;
-    for (int ww = 0; ww < w; ++ww) before += s_wave[ww];
+    const uint32_t bank = __builtin_amdgcn_readfirstlane(s_bank);
+    if (bank == kEmpty32) return;             // workspace bound to another call: every tile stands down
+    uint64_t* const cnt = (uint64_t*)((char*)p.cnt + (bank ? p.bank : 0));
+    const uint64_t own = min_u64((uint64_t)(s_wave[0] + s_wave[1] + s_wave[2] + s_wave[3]), cap);
+    int64_t before_wave = 0;
 #pragma unroll
-    for (int e = 0; e < PER; ++e) {
-        before += len[e];
-        if (k0 + e < p.n_draws) p.ends[k0 + e] = before;
-    }
-    if (tid == 255) p.block_tot[blockIdx.x] = before;
-}
+    for (int ww = 0; ww < 4; ++ww)
+        if (ww < w) before_wave += s_wave[ww];
 
-// Exclusive scan of the block totals (one workgroup of 1024 threads), and
-// the number of batch rows the draws fill.
-__global__ __launch_bounds__(1024) void tbb_block_scan_kernel(TbbSampleArgs p) {
-    __shared__ int64_t s_wave[16];
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int64_t nb = p.nblocks;
-    const int64_t per = (nb + 1023) / 1024;
-    const int64_t b0 = (int64_t)tid * per;
-    int64_t run = 0;
-    for (int64_t e = 0; e < per; ++e)
-        if (b0 + e < nb) run += p.block_tot[b0 + e];
-    const int64_t incl = wave_incl_sum64(run);
-    if (lane == 63) s_wave[w] = incl;
-    __syncthreads();
-    int64_t before = incl - run;
-    for (int ww = 0; ww < w; ++ww) before += s_wave[ww];
-    for (int64_t e = 0; e < per; ++e) {
-        if (b0 + e < nb) {
-            p.block_off[b0 + e] = before;
-            before += p.block_tot[b0 + e];
+    // wavefront 3 publishes the tile's own sum (inclusive for tile 0);
+    // wavefront 0 looks back
+    if (w == 3 && lane == 0) {
+        publish64(cnt + tile, (tile == 0 ? kCountIncl : kCountOwn) | own);
+        ((uint64_t*)((char*)p.cnt + (bank ? 0 : p.bank)))[tile] = kEmpty64;   // idle bank, next call
+    }
+    if (w == 0) {
+        uint64_t acc = 0;
+        if (tile > 0) {
+            int64_t base = tile - 1;
+            uint32_t polls = 0;
+            while (true) {
+                uint64_t sum;
+                int fe;
+                const bool stop = count_window(cnt, base, 1, sum, fe);
+                acc = min_u64(acc + sum, cap);
+                if (stop) break;
+                base -= fe;
+                if (fe > 0) {
+                    polls = 0;
+                } else if (++polls > p.fallback_polls) {
+                    // tile `base` has not published: sum its episode lengths here
+                    uint64_t r = 0;
+#pragma unroll 1
+                    for (int e = 0; e < kTbbDrawTile / 64; ++e) {
+                        int64_t l, n;
+                        draw_rows(p, base * kTbbDrawTile + 64 * e + lane, l, n);
+                        r += (uint64_t)n;
+                    }
+                    acc = min_u64(acc + min_u64(wave_sum_u64(r), cap), cap);
+                    base -= 1;
+                    polls = 0;
+                } else {
+                    __builtin_amdgcn_s_sleep(1);
+                }
+            }
+            if (lane == 0) publish64(cnt + tile, kCountIncl | min_u64(acc + own, cap));
+        }
+        if (lane == 0) {
+            s_before = acc;
+            const uint64_t total = min_u64(acc + own, cap);
+            if (tile == (int64_t)gridDim.x - 1 && total < cap) {
+                // the draws end inside the batch
+                p.meta[0] = (int64_t)total;
+                p.meta[1] = p.n_draws;
+                if (p.filled) *p.filled = (int64_t)total;
+            }
         }
     }
-    if (tid == 1023 && p.filled) *p.filled = before < p.batch ? before : p.batch;
+    __syncthreads();
+
+    // first batch row of each of the lane's draws, and the groups whose
+    // first row g * RW lies in [row, min(row + length, batch)): a lane writes
+    // up to kFewGroups of them itself; the whole wavefront serves a draw
+    // whose episode holds more
+    constexpr int64_t kFewGroups = 8;
+    uint64_t r = min_u64(s_before + (uint64_t)(before_wave + incl - run), cap);
+#pragma unroll
+    for (int e = 0; e < kDrawsPerLane; ++e) {
+        const int64_t k = k0 + e;
+        int64_t ga = 0, gb = 0;
+        if (k < p.n_draws && r < cap) {
+            const uint64_t end = r + (uint64_t)len[e];
+            p.row0[k] = (int64_t)r;
+            p.shift[k] = lo[e] - (int64_t)r;
+            if (end >= cap) {
+                // the draw that reaches the end of the batch
+                p.meta[0] = (int64_t)cap;
+                p.meta[1] = k + 1;
+                if (p.filled) *p.filled = (int64_t)cap;
+            }
+            ga = (int64_t)((r + RW - 1) / RW);
+            gb = (int64_t)((min_u64(end, cap) + RW - 1) / RW);
+            if (gb - ga <= kFewGroups)
+                for (int64_t g = ga; g < gb; ++g) p.first[g] = k;
+        }
+        uint64_t many = __ballot(gb - ga > kFewGroups);
+        while (many) {
+            const int L = __builtin_ctzll(many);
+            many &= many - 1;
+            const int64_t a = __shfl(ga, L, 64), b = __shfl(gb, L, 64), kk = __shfl(k, L, 64);
+            for (int64_t g = a + lane; g < b; g += 64) p.first[g] = kk;
+        }
+        r = min_u64(r + (uint64_t)len[e], cap);
+    }
+    if (tid == 0) write_epoch(p.epoch + tile, epoch);
 }
 
-// Output rows in groups of kTbbRowsPerGroup (kRowsPerThread per thread).
-// The group's first draw -- the first whose running end passes the group's
-// first row -- is found by a 256-way search over the running ends (a few
-// rounds of one probe per thread); the ends and first source rows of the
-// next kTbbRowsPerGroup draws go to LDS, where every row finds its own draw
-// by binary search; then the workgroup copies the rows in units of U bytes.
+// Output rows in groups of kTbbRowsPerGroup (RW / 256 per thread).
+// The group's first draw comes from the row-sum kernel's table; the first
+// rows and shifts of the next kTbbRowsPerGroup draws go to LDS, where every
+// row finds its own draw (the last one starting at or before it) by binary
+// search; then the workgroup copies the rows in units of U bytes.
 template <int U>
 __global__ __launch_bounds__(256) void tbb_gather_kernel(TbbSampleArgs p) {
     constexpr int RW = kTbbRowsPerGroup;
     constexpr int RPT = RW / 256;                  // rows (and window draws) per thread
-    __shared__ int64_t s_q[256];
-    __shared__ int s_first;
-    __shared__ int64_t s_end[RW];      // running ends of draws k0 .. k0 + RW - 1
-    __shared__ int64_t s_lo[RW];       // source row minus batch row for those draws
+    __shared__ int64_t s_row0[RW];     // first batch rows of draws k0 .. k0 + RW - 1
+    __shared__ int64_t s_shift[RW];    // source row minus batch row for those draws
     __shared__ int64_t s_src[RW];
+    __shared__ int64_t s_head[4];      // rows filled, k0, draws inside the batch, go
     const int tid = threadIdx.x;
-    const int64_t r0 = (int64_t)blockIdx.x * RW;
+    const int64_t g = blockIdx.x, r0 = g * RW;
     const int64_t nd = p.n_draws;
 
-    // ---- k0 = first k with end(k) > r0 (nd if none).  Invariant: the answer
-    // lies in [lo, hi], and position hi is either nd or known to qualify.
-    int64_t lo = 0, hi = nd;
-    while (hi > lo) {
-        const int64_t span = hi - lo;
-        const bool last_round = span <= 256;
-        const int64_t q = last_round ? lo + tid : lo + (((int64_t)tid + 1) * span) / 256 - 1;
-        const bool ok = q < hi && end_at(p, q) > r0;
-        if (tid == 0) s_first = 256;
-        s_q[tid] = q;
-        __syncthreads();
-        if (ok) atomicMin(&s_first, tid);
-        __syncthreads();
-        const int f = s_first;
-        if (last_round) {
-            hi = f < 256 ? s_q[f] : hi;
-            lo = hi;
-        } else if (f == 256) {
-            lo = hi;                      // nothing in [lo, hi) qualifies
-        } else {
-            lo = f == 0 ? lo : s_q[f - 1] + 1;
-            hi = s_q[f];
+    if (tid == 0) {
+        int64_t fill = 0, k0 = 0, klim = 0, go = 1;
+        if (nd > 0) {
+            const uint64_t sig = p.hdr->sig;
+            const int64_t f = p.meta[0], kl = p.meta[1], first = p.first[g];
+            go = sig == p.sig;                     // else the row sums stood down
+            // clamped so that even a workspace left stale by an abandoned
+            // call keeps every access in bounds
+            fill = f < 0 ? 0 : (f > p.batch ? p.batch : f);
+            klim = kl < 0 ? 0 : (kl > nd ? nd : kl);
+            k0 = r0 < fill ? (first < 0 ? 0 : (first > klim ? klim : first)) : klim;
+        } else if (g == 0 && p.filled) {
+            *p.filled = 0;
         }
-        __syncthreads();
+        s_head[0] = fill;
+        s_head[1] = k0;
+        s_head[2] = klim;
+        s_head[3] = go;
     }
-    const int64_t k0 = hi;
+    __syncthreads();
+    if (!s_head[3]) return;
+    const int64_t fill = s_head[0], k0 = s_head[1], klim = s_head[2];
 
     // ---- the window of draws k0 .. k0 + RW - 1
 #pragma unroll
     for (int j = 0; j < RPT; ++j) {
         const int w = tid + 256 * j;
         const int64_t k = k0 + w;
-        int64_t e = INT64_MAX, l = 0;
-        if (k < nd) {
-            int64_t elo, ehi;
-            episode_rows(p, draw_at(p, k), elo, ehi);
-            e = end_at(p, k);
-            l = elo - (e - (ehi - elo));     // source row minus batch row, constant over the episode
-        }
-        s_end[w] = e;
-        s_lo[w] = l;
+        const bool in = k < klim;
+        s_row0[w] = in ? p.row0[k] : INT64_MAX;
+        s_shift[w] = in ? p.shift[k] : 0;
     }
     __syncthreads();
-    const int64_t prev0 = k0 > 0 && k0 <= nd ? end_at(p, k0 - 1) : 0;   // end of the draw before the window
 
     // ---- each row's draw and source row
 #pragma unroll
@@ -322,39 +385,38 @@ __global__ __launch_bounds__(256) void tbb_gather_kernel(TbbSampleArgs p) {
         int64_t src = -1;
         if (t < p.batch) {
             uint8_t st = 0;
-            if (k0 < nd) {
-                int a = 0, b = RW;              // first window slot with end > t
+            if (t < fill) {
+                int a = 0, b = RW;                 // first window slot starting after t
                 while (a < b) {
                     const int mid = (a + b) >> 1;
-                    if (s_end[mid] > t) b = mid;
+                    if (s_row0[mid] > t) b = mid;
                     else a = mid + 1;
                 }
-                if (a < RW && k0 + a < nd) {
-                    src = t + s_lo[a];
-                    st = (a > 0 ? s_end[a - 1] : prev0) == t ? 1 : 0;
-                } else if (a == RW) {
-                    // more than RW draws end inside this group (empty
+                int64_t row0 = -1, shift = 0;
+                if (a == RW && k0 + RW < klim) {
+                    // more than RW draws begin inside this group (empty
                     // episodes): search the remaining draws directly
-                    int64_t gl = k0 + RW, gh = nd;
+                    int64_t gl = k0 + RW, gh = klim;
                     while (gl < gh) {
                         const int64_t mid = (gl + gh) >> 1;
-                        if (end_at(p, mid) > t) gh = mid;
+                        if (p.row0[mid] > t) gh = mid;
                         else gl = mid + 1;
                     }
-                    if (gl < nd) {
-                        int64_t elo, ehi;
-                        episode_rows(p, draw_at(p, gl), elo, ehi);
-                        src = elo + (t - (end_at(p, gl) - (ehi - elo)));
-                        st = src == elo ? 1 : 0;
-                    }
+                    row0 = p.row0[gl - 1];
+                    shift = p.shift[gl - 1];
+                } else if (a > 0) {
+                    row0 = s_row0[a - 1];
+                    shift = s_shift[a - 1];
                 }
+                src = t + shift;
+                if (row0 < 0 || src < 0 || src >= p.n_D) src = -1;
+                st = src >= 0 && row0 == t ? 1 : 0;
             }
             p.out_start[t] = st;
             if (p.out_src) p.out_src[t] = src;
         }
         s_src[rr] = src;
     }
-    if (blockIdx.x == 0 && tid == 0 && nd == 0 && p.filled) *p.filled = 0;
     __syncthreads();
 
     // ---- copy the rows: up to 8 units per thread in flight (loads first,
@@ -387,11 +449,8 @@ __global__ __launch_bounds__(256) void tbb_gather_kernel(TbbSampleArgs p) {
     }
 }
 
-hipError_t tbb_sample_launch(int unit, const TbbSampleArgs& a, hipStream_t s) {
-    if (a.n_draws > 0) {
-        hipLaunchKernelGGL(tbb_lengths_kernel, dim3((unsigned)a.nblocks), dim3(256), 0, s, a);
-        hipLaunchKernelGGL(tbb_block_scan_kernel, dim3(1), dim3(1024), 0, s, a);
-    }
+hipError_t tbb_sample_launch(int unit, const TbbSampleArgs& a, int64_t ntiles, hipStream_t s) {
+    if (a.n_draws > 0) hipLaunchKernelGGL(tbb_rows_kernel, dim3((unsigned)ntiles), dim3(256), 0, s, a);
     const unsigned groups = (unsigned)((a.batch + kTbbRowsPerGroup - 1) / kTbbRowsPerGroup);
     if (unit == 16)
         hipLaunchKernelGGL(tbb_gather_kernel<16>, dim3(groups), dim3(256), 0, s, a);

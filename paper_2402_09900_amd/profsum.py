@@ -106,7 +106,7 @@ CALLS = {
     6: {"return": ["disc_kernel<4, false>"], "gae": ["disc_kernel<4, true>"]},
     7: {"fwd": ["diag_fwd_kernel"], "bwd": ["diag_bwd_kernel", "ffm_bwd_finish_kernel"]},
     8: {"insert": ["tbb_begins_kernel"],
-        "sample": ["tbb_lengths_kernel", "tbb_block_scan_kernel", "tbb_gather_kernel"]},
+        "sample": ["tbb_rows_kernel", "tbb_gather_kernel"]},
     3: {"linattn_fwd": _LIN_FWD},
     9: {"linattn_fwd": _LIN_FWD,
         "linattn_bwd": ["linattn_summary_kernel", "diag_fwd_kernel", "linattn_bwd_summary_kernel", "diag_bwd_kernel",

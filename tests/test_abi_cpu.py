@@ -36,7 +36,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert mb.memoroid_abi_version() == 2
+    assert mb.memoroid_abi_version() == 3
     for s in (mb.OK, mb.EINVAL, mb.EUNSUPPORTED, mb.EWORKSPACE, mb.EHIP, mb.ETIMEOUT, mb.EMISMATCH):
         assert mb.status_string(s) and mb.status_string(s) != "unknown status"
     assert mb.status_string(12345) == "unknown status"
@@ -194,7 +194,9 @@ def test_tbb_validation():
         args.update(kw)
         return mb.memoroid_tbb_sample(*args.values())
     assert mb.memoroid_tbb_begin_indices_workspace_bytes(1 << 24) > 256
-    assert mb.memoroid_tbb_sample_workspace_bytes(0) > 0 and mb.memoroid_tbb_sample_workspace_bytes(-1) == 0
+    assert mb.memoroid_tbb_sample_workspace_bytes(0, 10) > 0 and mb.memoroid_tbb_sample_workspace_bytes(-1, 10) == 0
+    assert mb.memoroid_tbb_sample_workspace_bytes(10, -1) == 0 and mb.memoroid_tbb_sample_workspace_bytes(10, 1 << 47) == 0
+    assert mb.memoroid_tbb_sample_workspace_bytes(1 << 20, 1 << 20) >= (1 << 20) * 16
     assert bi(n=-1) == mb.EINVAL and bi(n=1 << 31) == mb.EUNSUPPORTED
     assert bi(count=None) == mb.EINVAL and bi(start=None) == mb.EINVAL and bi(indices=None) == mb.EINVAL
     assert bi(count=A + 4) == mb.EINVAL and bi(indices=S) == mb.EINVAL
@@ -207,6 +209,8 @@ def test_tbb_validation():
     assert sm(I=X + 4) == mb.EINVAL
     assert sm(workspace=None) == mb.EWORKSPACE and sm(workspace_bytes=8) == mb.EWORKSPACE
     assert sm(batch=1 << 62) == mb.EINVAL               # batch * row_bytes overflows
+    assert sm(batch=1 << 47, row_bytes=1) == mb.EUNSUPPORTED and sm(n_D=1 << 47, row_bytes=1) == mb.EUNSUPPORTED
+    assert sm(workspace_bytes=mb.memoroid_tbb_sample_workspace_bytes(100, 500) - 1) == mb.EWORKSPACE
 
 
 def test_ffm_bwd_validation():

@@ -35,8 +35,10 @@ def check_sample(D, I, draws, batch, label):
                                                                       len(draws), batch))
     out, st, src, filled = mb.tbb_sample(dev(D), dev(I), dev(np.asarray(draws, np.int64)), batch)
     torch.cuda.synchronize()
+    # the kernels clamp positions into I and episode rows into D; the oracle
+    # takes the clamped values
     clamped = np.clip(np.asarray(draws, np.int64), 0, max(I.size - 1, 0))
-    r_out, r_st, r_src, r_filled = oracle.tbb_sample(D, I, clamped, batch)
+    r_out, r_st, r_src, r_filled = oracle.tbb_sample(D, np.clip(I, 0, D.shape[0]), clamped, batch)
     assert int(filled.item()) == r_filled
     np.testing.assert_array_equal(src.cpu().numpy(), r_src)
     np.testing.assert_array_equal(st.cpu().numpy(), r_st)
@@ -114,3 +116,39 @@ def test_sample_many_draws_cross_blocks():
 def test_sample_workload8():
     tb = tapes.make_tbb(8)
     check_sample(tb.D, tb.begins, tb.draws, tb.batch, "workload8")
+
+
+def test_sample_group_table_edge_cases():
+    """Where the batch rows meet the draws: more than 1024 draws starting
+    inside one group of 1024 rows (runs of empty episodes), one episode
+    spanning many groups, draws that fill the batch exactly, episode bounds
+    outside D (clamped)."""
+    rng = np.random.default_rng(41)
+    n = 50000
+    D = rng.standard_normal((n, 4)).astype(np.float32)
+    # begins: 3000 empty episodes at row 100, then episodes of 1..5 rows,
+    # one of 20000 rows, more short ones
+    short = np.cumsum(rng.integers(1, 6, size=2000)) + 100
+    I = np.concatenate([[0], np.full(3000, 100), short, [short[-1] + 20000],
+                        short[-1] + 20000 + np.cumsum(rng.integers(1, 6, size=2000))]).astype(np.int64)
+    I = I[I <= n]
+    k_long = 1 + 3000 + 2000 - 1            # position of the 20000-row episode
+    draws = np.arange(I.size)
+    check_sample(D, I, draws, 30000, "empty runs")
+    check_sample(D, I, np.concatenate([[k_long], draws]), 45000, "long episode first")
+    lens = np.diff(np.append(I, n))
+    exact = int(lens[:4000].sum())
+    check_sample(D, I, np.arange(4000), exact, "exact fill")
+    check_sample(D, I, np.arange(4000), exact + 1, "one row short")
+    check_sample(D, I, np.arange(4000), exact - 1, "one row over")
+    bad = np.array([-40, 5, 17, 17, n - 10, n + 30], np.int64)
+    check_sample(D, bad, [0, 1, 2, 3, 4, 5, 0], 200, "bounds outside D")
+
+
+def test_sample_many_tiles_and_fallback(monkeypatch):
+    """Row sums over many draw tiles, with the look-back's fallback forced
+    (every awaited tile's sum computed by the waiting tile)."""
+    tb = tapes.make_tbb(8, seed=34, n=300000, batch=200000, n_draws=150000, episodes=tapes._uniform_int(1, 3))
+    check_sample(tb.D, tb.begins, tb.draws, tb.batch, "many tiles")
+    monkeypatch.setenv("MEMOROID_FALLBACK_POLLS", "0")
+    check_sample(tb.D, tb.begins, tb.draws, tb.batch, "many tiles fallback")

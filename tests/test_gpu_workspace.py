@@ -196,6 +196,44 @@ def test_begin_indices_repeated_calls():
     assert status(ws) == mb.OK
 
 
+def _sample_call(tb, draws, batch, ws):
+    D, I, dr = dev(tb.D), dev(tb.begins), dev(np.asarray(draws, np.int64))
+    row_bytes = tb.D.shape[1] * 4
+    out = torch.empty((batch, tb.D.shape[1]), dtype=torch.float32, device=DEV)
+    ost = torch.empty(batch, dtype=torch.uint8, device=DEV)
+    osrc = torch.empty(batch, dtype=torch.int64, device=DEV)
+    filled = torch.full((1,), -3, dtype=torch.int64, device=DEV)
+    assert mb.memoroid_tbb_sample(D.data_ptr(), tb.D.shape[0], row_bytes, I.data_ptr(), I.numel(), dr.data_ptr(),
+                                  dr.numel(), batch, out.data_ptr(), ost.data_ptr(), osrc.data_ptr(),
+                                  filled.data_ptr(), ws.data_ptr(), ws.numel(), stream()) == mb.OK
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), ost.cpu().numpy(), osrc.cpu().numpy(), int(filled.item())
+
+
+def test_sample_repeated_calls_and_mismatch():
+    """Sampling on one prepared workspace: four calls with new draws each
+    (row sums alternate banks; the group table and draw rows are rewritten),
+    then a call with another batch size stands down and writes nothing."""
+    tb = tapes.make_tbb(8, seed=35, n=200000, batch=60000, n_draws=40000)
+    K, batch = 40000, 60000
+    ws = prepared(mb.memoroid_tbb_sample_workspace_bytes(K, batch))
+    for call in range(CALLS):
+        rng = np.random.Generator(np.random.PCG64(1400 + call))
+        draws = rng.integers(0, tb.begins.size, size=K)
+        announce("workspace sample call %d" % call)
+        out, ost, osrc, filled = _sample_call(tb, draws, batch, ws)
+        r_out, r_st, r_src, r_filled = oracle.tbb_sample(tb.D, tb.begins, draws, batch)
+        assert filled == r_filled
+        np.testing.assert_array_equal(osrc, r_src)
+        np.testing.assert_array_equal(ost, r_st)
+        assert np.array_equal(out.view(np.uint8), r_out.view(np.uint8))
+    assert status(ws) == mb.OK
+    announce("workspace sample: other batch on the bound workspace")
+    out, ost, osrc, filled = _sample_call(tb, draws, batch - 5000, ws)
+    assert status(ws) == mb.EMISMATCH
+    assert filled == -3
+
+
 def test_other_sizes_on_a_bound_workspace_report_mismatch():
     """A bound workspace used with other sizes: the call computes nothing and
     the status says so; after a new preparation the same call is correct."""
