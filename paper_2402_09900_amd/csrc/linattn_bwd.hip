@@ -19,16 +19,14 @@
 // Kernels: the forward summary and state scan (shared with the forward
 // pass) give S_in, z_in; the backward summary computes den, dnum, dden for
 // every row (kept in the workspace) and dU; the reverse state scan gives
-// U_out; then one kernel forms dq and one forms dk and dv.  Each workgroup
-// (one chunk of one head) uses four 64x64 LDS tiles, restaged between
-// contractions in the layout each operand needs.
+// U_out; then one kernel forms dq, dk and dv.  Each of its workgroups (one
+// chunk of one head) uses four 64x64 LDS tiles, all stored rotated so that
+// either index of a tile can serve as the contraction index.
 #include "linattn_common.hpp"
 
 namespace memoroid {
 
 namespace {
-
-__device__ __forceinline__ float phi_prime(float u) { return u > 0.0f ? 1.0f : __expf(u); }
 
 // Row `lane` of the chunk: its begin flag and the last begin at or before it
 // (an inclusive max-scan across the wavefront; every wavefront has all 64).
@@ -231,85 +229,67 @@ __global__ __launch_bounds__(256) void linattn_bwd_summary_kernel(LinBwdArgs p) 
     }
 }
 
-// ------------------------------------------------------------------- dq
-__global__ __launch_bounds__(256) void linattn_bwd_dq_kernel(LinBwdArgs p) {
-    __shared__ __attribute__((aligned(16))) float X0[kC * kLD];   // dP (natural)
-    __shared__ __attribute__((aligned(16))) float X1[kC * kLD];   // phi(K), rotated
-    __shared__ __attribute__((aligned(16))) float X2[kC * kLD];   // dnum (natural)
-    __shared__ __attribute__((aligned(16))) float X3[kC * kLD];   // V (natural), later S_in^T rotated
-    __shared__ float sZ[kC];
-    const int64_t c = blockIdx.x, h = blockIdx.y;
-    const int64_t t0 = c * kC;
-    const int nvalid = (int)(p.T - t0 < kC ? p.T - t0 : kC);
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    bool beg;
-    const int rmax = row_last_begin(p.start, t0, nvalid, beg);
-
-    // every global load up front: dnum, v, k, S_in, z_in, the rows' dden,
-    // and q at this lane's output elements (for phi')
-    f32x4 dnreg[4], vreg[4], kreg[4], sreg[4];
-    fetch_rows(dnreg, p.dnum, t0, p.H, h, 0, nvalid);
-    fetch_rows(vreg, p.v, t0, p.H, h, 0, nvalid);
-    fetch_rows(kreg, p.k, t0, p.H, h, 0, nvalid);
-    fetch_state(sreg, p.Sinc + (c > 0 ? ((c - 1) * p.H + h) * kStateWords : 0), c > 0);
-    const float zin = tid < kC && c > 0 ? p.Sinc[((c - 1) * p.H + h) * kStateWords + kC * kC + tid] : 0.0f;
-    int ri[4];
-    float dd[4], qo[4][4];
+// ------------------------------------------------------------- dq, dk, dv
+// acc += A * B for 64x64 LDS tiles that are all stored rotated (rot_col).
+//   A_ROWS: A[i][k] is element (i, k) of the A tile, else element (k, i);
+//   B_ROWS: B[k][j] is element (j, k) of the B tile, else element (k, j).
+// Read along its rows, a rotated tile still gives 16-byte runs (the rotation
+// moves whole 16-column blocks, the same for the 16 rows of a wavefront), so
+// either index of a tile can be the contraction index and no tile is staged
+// twice.  jt_last as in mfma_64x64x64.
+template <bool A_ROWS, bool B_ROWS>
+__device__ __forceinline__ void mfma_rot(const float* sA, const float* sB, f32x4 acc[4], int jt_last = 3) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int i = 16 * w + (lane & 15), kk = (lane >> 4) * 16;
+    float af[16];
+    if constexpr (A_ROWS) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int i = 16 * w + 4 * (lane >> 4) + r;
-        dd[r] = i < nvalid ? p.dden[(t0 + i) * p.H + h] : 0.0f;
-#pragma unroll
-        for (int jt = 0; jt < 4; ++jt)
-            qo[jt][r] = i < nvalid ? p.q[((t0 + i) * p.H + h) * kC + 16 * jt + (lane & 15)] : 0.0f;
-    }
-    phi_rows(kreg, 0, nvalid);
-    store_rows<false>(X2, dnreg);
-    store_rows<false>(X3, vreg);
-    store_rows<true>(X1, kreg);
-    __syncthreads();
-
-    f32x4 acc[4];
-    zero_acc(acc);
-    mfma_64x64x64<true, true>(X2, X3, acc);                  // dnum_i . v_j
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int i = 16 * w + 4 * (lane >> 4) + r;
-        ri[r] = __shfl(rmax, i, 64);
-#pragma unroll
-        for (int jt = 0; jt < 4; ++jt)
-            acc[jt][r] = keep_ij(i, 16 * jt + (lane & 15), ri[r], nvalid) ? acc[jt][r] + dd[r] : 0.0f;
-    }
-    acc_to_lds<false>(X0, acc);
-    __syncthreads();                                         // X3 (V) free
-    store_rows<true>(X3, sreg);                              // S_in^T [n][kd], rotated
-    if (tid < kC) sZ[tid] = zin;
-    __syncthreads();
-
-    f32x4 accQ[4], accS[4];
-    zero_acc(accQ);
-    zero_acc(accS);
-    mfma_64x64x64<true, false>(X0, X1, accQ);                // sum_j dP[i][j] K[j][kd]
-    mfma_64x64x64<true, false>(X2, X3, accS);                // sum_n dnum[i][n] S_in[kd][n]
-#pragma unroll
-    for (int jt = 0; jt < 4; ++jt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int i = 16 * w + 4 * (lane >> 4) + r, kd = 16 * jt + (lane & 15);
-            if (i < nvalid) {
-                const float dQ = accQ[jt][r] + (ri[r] < 0 ? accS[jt][r] + dd[r] * sZ[kd] : 0.0f);
-                p.dq[((t0 + i) * p.H + h) * kC + kd] = dQ * phi_prime(qo[jt][r]);
-            }
+        for (int u = 0; u < 4; ++u) {
+            const f32x4 v = *(const f32x4*)(sA + i * kLD + rot_col(i, kk + 4 * u));
+            af[4 * u] = v.x; af[4 * u + 1] = v.y; af[4 * u + 2] = v.z; af[4 * u + 3] = v.w;
         }
+    } else {
+        const int c = rot_col(kk, i);
+#pragma unroll
+        for (int s = 0; s < 16; ++s) af[s] = sA[(kk + s) * kLD + c];
+    }
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt) {
+        if (jt > jt_last) break;
+        const int j = 16 * jt + (lane & 15);
+        float bf[16];
+        if constexpr (B_ROWS) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const f32x4 v = *(const f32x4*)(sB + j * kLD + rot_col(j, kk + 4 * u));
+                bf[4 * u] = v.x; bf[4 * u + 1] = v.y; bf[4 * u + 2] = v.z; bf[4 * u + 3] = v.w;
+            }
+        } else {
+            const int c = rot_col(kk, j);
+#pragma unroll
+            for (int s = 0; s < 16; ++s) bf[s] = sB[(kk + s) * kLD + c];
+        }
+#pragma unroll
+        for (int s = 0; s < 16; ++s) acc[jt] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[s], bf[s], acc[jt], 0, 0, 0);
+    }
 }
 
-// --------------------------------------------------------------- dk, dv
-__global__ __launch_bounds__(256) void linattn_bwd_dkv_kernel(LinBwdArgs p) {
-    __shared__ __attribute__((aligned(16))) float X0[kC * kLD];
-    __shared__ __attribute__((aligned(16))) float X1[kC * kLD];   // phi(K) natural throughout
-    __shared__ __attribute__((aligned(16))) float X2[kC * kLD];
-    __shared__ __attribute__((aligned(16))) float X3[kC * kLD];
-    __shared__ float sW[kC];
+// One workgroup per (chunk, head) forms dq, dk and dv from four rotated LDS
+// tiles, each written once per phase:
+//   phase 1 (U_out, phi(K), V, dnum): dK2 = V U_out^T, dV2 = phi(K) U_out,
+//                                     dP = (dnum V^T + dden) masked
+//   phase 2 (phi(Q), phi(K), dP, dnum): A = phi(Q) phi(K)^T masked,
+//                                       dQ1 = dP phi(K), dK1 = dP^T phi(Q) -> dk
+//   phase 3 (S_in^T, phi(K), A, dnum): dV1 = A^T dnum -> dv, dQ2 = dnum S_in^T -> dq
+// The state products are skipped by wavefronts none of whose rows take them
+// (dK2, dV2: rows at or after the chunk's last begin; dQ2: rows before its
+// first), and dP, A skip their column tiles above the diagonal.
+__global__ __launch_bounds__(256, 2) void linattn_bwd_grad_kernel(LinBwdArgs p) {
+    __shared__ __attribute__((aligned(16))) float X0[kC * kLD];   // U_out [kd][n], then phi(Q), then S_in^T [n][kd]
+    __shared__ __attribute__((aligned(16))) float X1[kC * kLD];   // phi(K)
+    __shared__ __attribute__((aligned(16))) float X2[kC * kLD];   // V, then dP, then A
+    __shared__ __attribute__((aligned(16))) float X3[kC * kLD];   // dnum
+    __shared__ float sW[kC], sZ[kC];
     const int64_t c = blockIdx.x, h = blockIdx.y;
     const int64_t t0 = c * kC;
     const int nvalid = (int)(p.T - t0 < kC ? p.T - t0 : kC);
@@ -318,92 +298,105 @@ __global__ __launch_bounds__(256) void linattn_bwd_dkv_kernel(LinBwdArgs p) {
     const int rmax = row_last_begin(p.start, t0, nvalid, beg);
     const uint64_t mb = __ballot(beg);
     const int lastb = mb ? 63 - __builtin_clzll(mb) : -1;    // rows >= lastb continue past the chunk
-    const bool have_u = c + 1 < p.nch;
+    const int firstb = mb ? __builtin_ctzll(mb) : kC;        // rows < firstb continue from the previous chunk
+    const bool have_u = c + 1 < p.nch, have_s = c > 0;
     const float* uo = p.Y + (have_u ? ((c + 1) * p.H + h) * kStateWords : 0);
+    const float* si = p.Sinc + (have_s ? ((c - 1) * p.H + h) * kStateWords : 0);
 
-    // every global load up front: q, k, dnum, v, U_out, w_out and the rows'
-    // dden; q, dnum and U_out stay in registers for their second layout
-    f32x4 qreg[4], kreg[4], dnreg[4], vreg[4], ureg[4];
-    fetch_rows(qreg, p.q, t0, p.H, h, 0, nvalid);
-    fetch_rows(kreg, p.k, t0, p.H, h, 0, nvalid);
-    fetch_rows(dnreg, p.dnum, t0, p.H, h, 0, nvalid);
-    fetch_rows(vreg, p.v, t0, p.H, h, 0, nvalid);
+    // every global load up front
+    f32x4 ureg[4], kreg[4], vreg[4], dnreg[4], qreg[4], sreg[4];
     fetch_state(ureg, uo, have_u);
-    const float wout = tid < kC && have_u ? uo[kC * kC + tid] : 0.0f;
-    float ddr[4];
+    fetch_rows(kreg, p.k, t0, p.H, h, 0, nvalid);
+    fetch_rows(vreg, p.v, t0, p.H, h, 0, nvalid);
+    fetch_rows(dnreg, p.dnum, t0, p.H, h, 0, nvalid);
+    fetch_rows(qreg, p.q, t0, p.H, h, 0, nvalid);
+    fetch_state(sreg, si, have_s);
+    if (tid < kC) {
+        sW[tid] = have_u ? uo[kC * kC + tid] : 0.0f;
+        sZ[tid] = have_s ? si[kC * kC + tid] : 0.0f;
+    }
+    float dd[4];
+    int ri[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int i = 16 * w + 4 * (lane >> 4) + r;
-        ddr[r] = i < nvalid ? p.dden[(t0 + i) * p.H + h] : 0.0f;
+        dd[r] = i < nvalid ? p.dden[(t0 + i) * p.H + h] : 0.0f;
+        ri[r] = __shfl(rmax, i, 64);
+    }
+    phi_rows(kreg, 0, nvalid);
+    store_rows<true>(X0, ureg);
+    store_rows<true>(X1, kreg);
+    store_rows<true>(X2, vreg);
+    store_rows<true>(X3, dnreg);
+    __syncthreads();
+
+    // ---- phase 1
+    f32x4 accK2[4], accV2[4], accP[4];
+    zero_acc(accK2);
+    zero_acc(accV2);
+    zero_acc(accP);
+    if (have_u && 16 * w + 15 >= lastb) {
+        mfma_rot<true, true>(X2, X0, accK2);                 // sum_n V[j][n] U[kd][n]
+        mfma_rot<true, false>(X1, X0, accV2);                // sum_kd K[j][kd] U[kd][n]
+    }
+    mfma_rot<true, true>(X3, X2, accP, w);                   // sum_n dnum[i][n] V[j][n]
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int i = 16 * w + 4 * (lane >> 4) + r;
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt)
+            accP[jt][r] = keep_ij(i, 16 * jt + (lane & 15), ri[r], nvalid) ? accP[jt][r] + dd[r] : 0.0f;
     }
     phi_rows(qreg, 0, nvalid);
-    phi_rows(kreg, 0, nvalid);
-    store_rows<false>(X0, qreg);
-    store_rows<false>(X1, kreg);
-    store_rows<false>(X2, dnreg);
-    store_rows<false>(X3, vreg);
+    __syncthreads();                                         // X0 (U_out), X2 (V) free
+    store_rows<true>(X0, qreg);
+    acc_to_lds<true>(X2, accP);
     __syncthreads();
 
-    f32x4 accA[4], accP[4];
+    // ---- phase 2
+    f32x4 accA[4], accQ1[4], accK1[4];
     zero_acc(accA);
-    zero_acc(accP);
-    mfma_64x64x64<true, true>(X0, X1, accA);                 // A = Q K^T
-    mfma_64x64x64<true, true>(X2, X3, accP);                 // dnum_i . v_j
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int i = 16 * w + 4 * (lane >> 4) + r;
-        const int ri = __shfl(rmax, i, 64);
-#pragma unroll
-        for (int jt = 0; jt < 4; ++jt) {
-            const bool keep = keep_ij(i, 16 * jt + (lane & 15), ri, nvalid);
-            accA[jt][r] = keep ? accA[jt][r] : 0.0f;
-            accP[jt][r] = keep ? accP[jt][r] + ddr[r] : 0.0f;
-        }
-    }
-    __syncthreads();                                         // X0 (Q), X2 (dnum) free
-    store_rows<true>(X0, qreg);                              // phi(Q) rotated
-    acc_to_lds<true>(X2, accP);                              // dP rotated
-    __syncthreads();
-
-    f32x4 accK[4];
-    zero_acc(accK);
-    mfma_64x64x64<false, false>(X2, X0, accK);               // sum_i dP[i][j] Q[i][kd]
-    __syncthreads();                                         // X0, X2 free
-    store_rows<false>(X0, ureg);                             // U_out [kd][n], natural
-    if (tid < kC) sW[tid] = wout;
-    acc_to_lds<true>(X2, accA);                              // A (masked) rotated
-    __syncthreads();
-
-    f32x4 accK2[4];
-    zero_acc(accK2);
-    mfma_64x64x64<true, true>(X3, X0, accK2);                // sum_n V[j][n] U[kd][n]
+    zero_acc(accQ1);
+    zero_acc(accK1);
+    mfma_rot<true, true>(X0, X1, accA, w);                   // sum_kd Q[i][kd] K[j][kd]
+    mfma_rot<true, false>(X2, X1, accQ1);                    // sum_j dP[i][j] K[j][kd]
+    mfma_rot<false, false>(X2, X0, accK1);                   // sum_i dP[i][j] Q[i][kd]
+    // this lane's accumulator elements (row, col): A masked; phi'(q) kept for
+    // dq; dk (rows j, columns kd) written, with phi'(k) from phi(K)
+    float pq[4][4];
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const int j = 16 * w + 4 * (lane >> 4) + r, kd = 16 * jt + (lane & 15);
-            if (j < nvalid) {
-                const float dK = accK[jt][r] + (j >= lastb ? accK2[jt][r] + sW[kd] : 0.0f);
-                // phi'(k) from phi(K), which X1 holds throughout
-                p.dk[((t0 + j) * p.H + h) * kC + kd] = dK * phi_prime_of_phi(X1[j * kLD + kd]);
+            const int row = 16 * w + 4 * (lane >> 4) + r, col = 16 * jt + (lane & 15);
+            accA[jt][r] = keep_ij(row, col, ri[r], nvalid) ? accA[jt][r] : 0.0f;
+            pq[jt][r] = phi_prime_of_phi(X0[row * kLD + rot_col(row, col)]);
+            if (row < nvalid) {
+                const float dK = accK1[jt][r] + (row >= lastb ? accK2[jt][r] + sW[col] : 0.0f);
+                p.dk[((t0 + row) * p.H + h) * kC + col] = dK * phi_prime_of_phi(X1[row * kLD + rot_col(row, col)]);
             }
         }
-    __syncthreads();                                         // X0, X3 free
-    store_rows<true>(X3, dnreg);                             // dnum rotated
-    store_rows<true>(X0, ureg);                              // U_out rotated
+    __syncthreads();                                         // X0 (phi(Q)), X2 (dP) free
+    store_rows<true>(X0, sreg);
+    acc_to_lds<true>(X2, accA);
     __syncthreads();
 
-    f32x4 accV[4], accV2[4];
-    zero_acc(accV);
-    zero_acc(accV2);
-    mfma_64x64x64<false, false>(X2, X3, accV);               // sum_i A[i][j] dnum[i][n]
-    mfma_64x64x64<true, false>(X1, X0, accV2);               // sum_kd K[j][kd] U[kd][n]
+    // ---- phase 3
+    f32x4 accV1[4], accQ2[4];
+    zero_acc(accV1);
+    zero_acc(accQ2);
+    mfma_rot<false, false>(X2, X3, accV1);                   // sum_i A[i][j] dnum[i][n]
+    if (have_s && 16 * w < firstb) mfma_rot<true, false>(X3, X0, accQ2);   // sum_n dnum[i][n] S_in[kd][n]
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const int j = 16 * w + 4 * (lane >> 4) + r, n = 16 * jt + (lane & 15);
-            if (j < nvalid) p.dv[((t0 + j) * p.H + h) * kC + n] = accV[jt][r] + (j >= lastb ? accV2[jt][r] : 0.0f);
+            const int i = 16 * w + 4 * (lane >> 4) + r, col = 16 * jt + (lane & 15);
+            if (i < nvalid) {
+                p.dv[((t0 + i) * p.H + h) * kC + col] = accV1[jt][r] + (i >= lastb ? accV2[jt][r] : 0.0f);
+                const float dQ = accQ1[jt][r] + (ri[r] < 0 ? accQ2[jt][r] + dd[r] * sZ[col] : 0.0f);
+                p.dq[((t0 + i) * p.H + h) * kC + col] = dQ * pq[jt][r];
+            }
         }
 }
 
@@ -413,8 +406,7 @@ hipError_t linattn_bwd_summary_launch(const LinBwdArgs& a, hipStream_t s) {
 }
 
 hipError_t linattn_bwd_grad_launch(const LinBwdArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL(linattn_bwd_dq_kernel, dim3((unsigned)a.nch, (unsigned)a.H), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(linattn_bwd_dkv_kernel, dim3((unsigned)a.nch, (unsigned)a.H), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(linattn_bwd_grad_kernel, dim3((unsigned)a.nch, (unsigned)a.H), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

@@ -110,7 +110,7 @@ CALLS = {
     3: {"linattn_fwd": _LIN_FWD},
     9: {"linattn_fwd": _LIN_FWD,
         "linattn_bwd": ["linattn_summary_kernel", "diag_fwd_kernel", "linattn_bwd_summary_kernel", "diag_bwd_kernel",
-                        "linattn_bwd_dq_kernel", "linattn_bwd_dkv_kernel"]},
+                        "linattn_bwd_grad_kernel"]},
 }
 
 
