@@ -62,18 +62,6 @@ __device__ __forceinline__ void acc_to_lds(float* s, const f32x4 (&acc)[4]) {
         }
 }
 
-// Load a 64x64 state block stored row-major at src into registers (the
-// fetch_rows layout); zeros when `have` is false.
-__device__ __forceinline__ void fetch_state(f32x4 (&v)[4], const float* src, bool have) {
-    const Rsrc r = make_rsrc(src, have ? kC * kC * 4 : 0);
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int f = threadIdx.x + 256 * u;
-        const u32x4 wv = __builtin_amdgcn_raw_buffer_load_b128(r, ((f >> 4) * kC + (f & 15) * 4) * 4, 0, 0);
-        v[u] = f32x4{__uint_as_float(wv.x), __uint_as_float(wv.y), __uint_as_float(wv.z), __uint_as_float(wv.w)};
-    }
-}
-
 // phi of a fetched tile, rows outside [lo, hi) selected to zeros
 __device__ __forceinline__ void phi_rows(f32x4 (&v)[4], int lo, int hi) {
 #pragma unroll
@@ -230,17 +218,90 @@ __global__ __launch_bounds__(256) void linattn_bwd_summary_kernel(LinBwdArgs p) 
 }
 
 // ------------------------------------------------------------- dq, dk, dv
-// acc += A * B for 64x64 LDS tiles that are all stored rotated (rot_col).
+// The gradient kernel runs eight wavefronts per (chunk, head): wavefront w
+// owns rows 16 rb .. 16 rb + 15 and the column half ch = w / 4 (column tiles
+// 2 ch, 2 ch + 1) of every 64x64 product, with rb = w % 4 for ch = 0 and
+// 3 - w % 4 for ch = 1.  The hardware places wavefront w on SIMD w % 4, so
+// each SIMD gets one row block from each end of the causal triangle and the
+// triangular products (dP, A) load the four SIMDs about evenly.  Eight
+// wavefronts with at most 128 VGPRs each give two workgroups, four
+// wavefronts per SIMD, on a CU.
+constexpr int kGradThreads = 512;
+constexpr int kGradPer = kC * kC / 4 / kGradThreads;    // float4 per thread per 64x64 tile
+
+__device__ __forceinline__ void grad_block(int& rb, int& ch) {
+    const int w = threadIdx.x >> 6;
+    ch = w >> 2;
+    rb = ch ? 3 - (w & 3) : (w & 3);
+}
+
+// rows [0, nvalid) of one chunk of a [T][H][64] tensor (zeros past them)
+__device__ __forceinline__ void grad_fetch_rows(f32x4 (&v)[kGradPer], const float* src, int64_t t0, int64_t H,
+                                                int64_t h, int nvalid) {
+    const ChunkRows cr = chunk_rows(src, t0, H, h, 0, nvalid);
+#pragma unroll
+    for (int u = 0; u < kGradPer; ++u) {
+        const int f = threadIdx.x + kGradThreads * u;
+        v[u] = cr.load(f >> 4, (f & 15) * 4);
+    }
+}
+
+// a 64x64 state block stored row-major (zeros when `have` is false)
+__device__ __forceinline__ void grad_fetch_state(f32x4 (&v)[kGradPer], const float* src, bool have) {
+    const Rsrc r = make_rsrc(src, have ? kC * kC * 4 : 0);
+#pragma unroll
+    for (int u = 0; u < kGradPer; ++u) {
+        const int f = threadIdx.x + kGradThreads * u;
+        const u32x4 wv = __builtin_amdgcn_raw_buffer_load_b128(r, ((f >> 4) * kC + (f & 15) * 4) * 4, 0, 0);
+        v[u] = f32x4{__uint_as_float(wv.x), __uint_as_float(wv.y), __uint_as_float(wv.z), __uint_as_float(wv.w)};
+    }
+}
+
+// phi of fetched rows, rows at or past nvalid selected to zeros
+__device__ __forceinline__ void grad_phi(f32x4 (&v)[kGradPer], int nvalid) {
+#pragma unroll
+    for (int u = 0; u < kGradPer; ++u) {
+        const bool in = ((threadIdx.x + kGradThreads * u) >> 4) < nvalid;
+        v[u].x = in ? phi(v[u].x) : 0.0f; v[u].y = in ? phi(v[u].y) : 0.0f;
+        v[u].z = in ? phi(v[u].z) : 0.0f; v[u].w = in ? phi(v[u].w) : 0.0f;
+    }
+}
+
+__device__ __forceinline__ void grad_store(float* s, const f32x4 (&v)[kGradPer]) {
+#pragma unroll
+    for (int u = 0; u < kGradPer; ++u) {
+        const int f = threadIdx.x + kGradThreads * u;
+        const int row = f >> 4, c4 = (f & 15) * 4;
+        *(f32x4*)(s + row * kLD + rot_col(row, c4)) = v[u];
+    }
+}
+
+// acc[jj][r] = C[16 rb + 4 (lane / 16) + r][16 (2 ch + jj) + lane % 16]
+__device__ __forceinline__ void grad_acc_to_lds(float* s, const f32x4 (&acc)[2], int rb, int ch) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int row = 16 * rb + 4 * (lane >> 4) + r, col = 16 * (2 * ch + jj) + (lane & 15);
+            s[row * kLD + rot_col(row, col)] = acc[jj][r];
+        }
+}
+
+// acc += A * B on this wavefront's row block and column half, for 64x64 LDS
+// tiles all stored rotated (rot_col).
 //   A_ROWS: A[i][k] is element (i, k) of the A tile, else element (k, i);
 //   B_ROWS: B[k][j] is element (j, k) of the B tile, else element (k, j).
 // Read along its rows, a rotated tile still gives 16-byte runs (the rotation
-// moves whole 16-column blocks, the same for the 16 rows of a wavefront), so
-// either index of a tile can be the contraction index and no tile is staged
-// twice.  jt_last as in mfma_64x64x64.
+// moves whole 16-column blocks, the same for the 16 rows a wavefront
+// reads), so either index of a tile can be the contraction index and no
+// tile is staged twice.  Column tiles past jt_last are left untouched.
 template <bool A_ROWS, bool B_ROWS>
-__device__ __forceinline__ void mfma_rot(const float* sA, const float* sB, f32x4 acc[4], int jt_last = 3) {
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int i = 16 * w + (lane & 15), kk = (lane >> 4) * 16;
+__device__ __forceinline__ void grad_mfma(const float* sA, const float* sB, f32x4 (&acc)[2], int rb, int ch,
+                                          int jt_last = 3) {
+    if (2 * ch > jt_last) return;
+    const int lane = threadIdx.x & 63;
+    const int i = 16 * rb + (lane & 15), kk = (lane >> 4) * 16;
     float af[16];
     if constexpr (A_ROWS) {
 #pragma unroll
@@ -254,7 +315,8 @@ __device__ __forceinline__ void mfma_rot(const float* sA, const float* sB, f32x4
         for (int s = 0; s < 16; ++s) af[s] = sA[(kk + s) * kLD + c];
     }
 #pragma unroll
-    for (int jt = 0; jt < 4; ++jt) {
+    for (int jj = 0; jj < 2; ++jj) {
+        const int jt = 2 * ch + jj;
         if (jt > jt_last) break;
         const int j = 16 * jt + (lane & 15);
         float bf[16];
@@ -270,8 +332,13 @@ __device__ __forceinline__ void mfma_rot(const float* sA, const float* sB, f32x4
             for (int s = 0; s < 16; ++s) bf[s] = sB[(kk + s) * kLD + c];
         }
 #pragma unroll
-        for (int s = 0; s < 16; ++s) acc[jt] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[s], bf[s], acc[jt], 0, 0, 0);
+        for (int s = 0; s < 16; ++s) acc[jj] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[s], bf[s], acc[jj], 0, 0, 0);
     }
+}
+
+__device__ __forceinline__ void zero2(f32x4 (&acc)[2]) {
+    acc[0] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    acc[1] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 }
 
 // One workgroup per (chunk, head) forms dq, dk and dv from four rotated LDS
@@ -284,7 +351,7 @@ __device__ __forceinline__ void mfma_rot(const float* sA, const float* sB, f32x4
 // The state products are skipped by wavefronts none of whose rows take them
 // (dK2, dV2: rows at or after the chunk's last begin; dQ2: rows before its
 // first), and dP, A skip their column tiles above the diagonal.
-__global__ __launch_bounds__(256, 2) void linattn_bwd_grad_kernel(LinBwdArgs p) {
+__global__ __launch_bounds__(kGradThreads, 2) void linattn_bwd_grad_kernel(LinBwdArgs p) {
     __shared__ __attribute__((aligned(16))) float X0[kC * kLD];   // U_out [kd][n], then phi(Q), then S_in^T [n][kd]
     __shared__ __attribute__((aligned(16))) float X1[kC * kLD];   // phi(K)
     __shared__ __attribute__((aligned(16))) float X2[kC * kLD];   // V, then dP, then A
@@ -293,7 +360,9 @@ __global__ __launch_bounds__(256, 2) void linattn_bwd_grad_kernel(LinBwdArgs p) 
     const int64_t c = blockIdx.x, h = blockIdx.y;
     const int64_t t0 = c * kC;
     const int nvalid = (int)(p.T - t0 < kC ? p.T - t0 : kC);
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    int rb, ch;
+    grad_block(rb, ch);
     bool beg;
     const int rmax = row_last_begin(p.start, t0, nvalid, beg);
     const uint64_t mb = __ballot(beg);
@@ -304,13 +373,13 @@ __global__ __launch_bounds__(256, 2) void linattn_bwd_grad_kernel(LinBwdArgs p) 
     const float* si = p.Sinc + (have_s ? ((c - 1) * p.H + h) * kStateWords : 0);
 
     // every global load up front
-    f32x4 ureg[4], kreg[4], vreg[4], dnreg[4], qreg[4], sreg[4];
-    fetch_state(ureg, uo, have_u);
-    fetch_rows(kreg, p.k, t0, p.H, h, 0, nvalid);
-    fetch_rows(vreg, p.v, t0, p.H, h, 0, nvalid);
-    fetch_rows(dnreg, p.dnum, t0, p.H, h, 0, nvalid);
-    fetch_rows(qreg, p.q, t0, p.H, h, 0, nvalid);
-    fetch_state(sreg, si, have_s);
+    f32x4 ureg[kGradPer], kreg[kGradPer], vreg[kGradPer], dnreg[kGradPer], qreg[kGradPer], sreg[kGradPer];
+    grad_fetch_state(ureg, uo, have_u);
+    grad_fetch_rows(kreg, p.k, t0, p.H, h, nvalid);
+    grad_fetch_rows(vreg, p.v, t0, p.H, h, nvalid);
+    grad_fetch_rows(dnreg, p.dnum, t0, p.H, h, nvalid);
+    grad_fetch_rows(qreg, p.q, t0, p.H, h, nvalid);
+    grad_fetch_state(sreg, si, have_s);
     if (tid < kC) {
         sW[tid] = have_u ? uo[kC * kC + tid] : 0.0f;
         sZ[tid] = have_s ? si[kC * kC + tid] : 0.0f;
@@ -319,83 +388,83 @@ __global__ __launch_bounds__(256, 2) void linattn_bwd_grad_kernel(LinBwdArgs p) 
     int ri[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-        const int i = 16 * w + 4 * (lane >> 4) + r;
+        const int i = 16 * rb + 4 * (lane >> 4) + r;
         dd[r] = i < nvalid ? p.dden[(t0 + i) * p.H + h] : 0.0f;
         ri[r] = __shfl(rmax, i, 64);
     }
-    phi_rows(kreg, 0, nvalid);
-    store_rows<true>(X0, ureg);
-    store_rows<true>(X1, kreg);
-    store_rows<true>(X2, vreg);
-    store_rows<true>(X3, dnreg);
+    grad_phi(kreg, nvalid);
+    grad_store(X0, ureg);
+    grad_store(X1, kreg);
+    grad_store(X2, vreg);
+    grad_store(X3, dnreg);
     __syncthreads();
 
     // ---- phase 1
-    f32x4 accK2[4], accV2[4], accP[4];
-    zero_acc(accK2);
-    zero_acc(accV2);
-    zero_acc(accP);
-    if (have_u && 16 * w + 15 >= lastb) {
-        mfma_rot<true, true>(X2, X0, accK2);                 // sum_n V[j][n] U[kd][n]
-        mfma_rot<true, false>(X1, X0, accV2);                // sum_kd K[j][kd] U[kd][n]
+    f32x4 accK2[2], accV2[2], accP[2];
+    zero2(accK2);
+    zero2(accV2);
+    zero2(accP);
+    if (have_u && 16 * rb + 15 >= lastb) {
+        grad_mfma<true, true>(X2, X0, accK2, rb, ch);        // sum_n V[j][n] U[kd][n]
+        grad_mfma<true, false>(X1, X0, accV2, rb, ch);       // sum_kd K[j][kd] U[kd][n]
     }
-    mfma_rot<true, true>(X3, X2, accP, w);                   // sum_n dnum[i][n] V[j][n]
+    grad_mfma<true, true>(X3, X2, accP, rb, ch, rb);         // sum_n dnum[i][n] V[j][n]
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int i = 16 * w + 4 * (lane >> 4) + r;
+    for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
-        for (int jt = 0; jt < 4; ++jt)
-            accP[jt][r] = keep_ij(i, 16 * jt + (lane & 15), ri[r], nvalid) ? accP[jt][r] + dd[r] : 0.0f;
-    }
-    phi_rows(qreg, 0, nvalid);
+        for (int r = 0; r < 4; ++r) {
+            const int row = 16 * rb + 4 * (lane >> 4) + r, col = 16 * (2 * ch + jj) + (lane & 15);
+            accP[jj][r] = keep_ij(row, col, ri[r], nvalid) ? accP[jj][r] + dd[r] : 0.0f;
+        }
+    grad_phi(qreg, nvalid);
     __syncthreads();                                         // X0 (U_out), X2 (V) free
-    store_rows<true>(X0, qreg);
-    acc_to_lds<true>(X2, accP);
+    grad_store(X0, qreg);
+    grad_acc_to_lds(X2, accP, rb, ch);
     __syncthreads();
 
     // ---- phase 2
-    f32x4 accA[4], accQ1[4], accK1[4];
-    zero_acc(accA);
-    zero_acc(accQ1);
-    zero_acc(accK1);
-    mfma_rot<true, true>(X0, X1, accA, w);                   // sum_kd Q[i][kd] K[j][kd]
-    mfma_rot<true, false>(X2, X1, accQ1);                    // sum_j dP[i][j] K[j][kd]
-    mfma_rot<false, false>(X2, X0, accK1);                   // sum_i dP[i][j] Q[i][kd]
+    f32x4 accA[2], accQ1[2], accK1[2];
+    zero2(accA);
+    zero2(accQ1);
+    zero2(accK1);
+    grad_mfma<true, true>(X0, X1, accA, rb, ch, rb);         // sum_kd Q[i][kd] K[j][kd]
+    grad_mfma<true, false>(X2, X1, accQ1, rb, ch);           // sum_j dP[i][j] K[j][kd]
+    grad_mfma<false, false>(X2, X0, accK1, rb, ch);          // sum_i dP[i][j] Q[i][kd]
     // this lane's accumulator elements (row, col): A masked; phi'(q) kept for
     // dq; dk (rows j, columns kd) written, with phi'(k) from phi(K)
-    float pq[4][4];
+    float pq[2][4];
 #pragma unroll
-    for (int jt = 0; jt < 4; ++jt)
+    for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const int row = 16 * w + 4 * (lane >> 4) + r, col = 16 * jt + (lane & 15);
-            accA[jt][r] = keep_ij(row, col, ri[r], nvalid) ? accA[jt][r] : 0.0f;
-            pq[jt][r] = phi_prime_of_phi(X0[row * kLD + rot_col(row, col)]);
+            const int row = 16 * rb + 4 * (lane >> 4) + r, col = 16 * (2 * ch + jj) + (lane & 15);
+            accA[jj][r] = keep_ij(row, col, ri[r], nvalid) ? accA[jj][r] : 0.0f;
+            pq[jj][r] = phi_prime_of_phi(X0[row * kLD + rot_col(row, col)]);
             if (row < nvalid) {
-                const float dK = accK1[jt][r] + (row >= lastb ? accK2[jt][r] + sW[col] : 0.0f);
+                const float dK = accK1[jj][r] + (row >= lastb ? accK2[jj][r] + sW[col] : 0.0f);
                 p.dk[((t0 + row) * p.H + h) * kC + col] = dK * phi_prime_of_phi(X1[row * kLD + rot_col(row, col)]);
             }
         }
     __syncthreads();                                         // X0 (phi(Q)), X2 (dP) free
-    store_rows<true>(X0, sreg);
-    acc_to_lds<true>(X2, accA);
+    grad_store(X0, sreg);
+    grad_acc_to_lds(X2, accA, rb, ch);
     __syncthreads();
 
     // ---- phase 3
-    f32x4 accV1[4], accQ2[4];
-    zero_acc(accV1);
-    zero_acc(accQ2);
-    mfma_rot<false, false>(X2, X3, accV1);                   // sum_i A[i][j] dnum[i][n]
-    if (have_s && 16 * w < firstb) mfma_rot<true, false>(X3, X0, accQ2);   // sum_n dnum[i][n] S_in[kd][n]
+    f32x4 accV1[2], accQ2[2];
+    zero2(accV1);
+    zero2(accQ2);
+    grad_mfma<false, false>(X2, X3, accV1, rb, ch);          // sum_i A[i][j] dnum[i][n]
+    if (have_s && 16 * rb < firstb) grad_mfma<true, false>(X3, X0, accQ2, rb, ch);   // sum_n dnum[i][n] S_in[kd][n]
 #pragma unroll
-    for (int jt = 0; jt < 4; ++jt)
+    for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const int i = 16 * w + 4 * (lane >> 4) + r, col = 16 * jt + (lane & 15);
+            const int i = 16 * rb + 4 * (lane >> 4) + r, col = 16 * (2 * ch + jj) + (lane & 15);
             if (i < nvalid) {
-                p.dv[((t0 + i) * p.H + h) * kC + col] = accV1[jt][r] + (i >= lastb ? accV2[jt][r] : 0.0f);
-                const float dQ = accQ1[jt][r] + (ri[r] < 0 ? accQ2[jt][r] + dd[r] * sZ[col] : 0.0f);
-                p.dq[((t0 + i) * p.H + h) * kC + col] = dQ * pq[jt][r];
+                p.dv[((t0 + i) * p.H + h) * kC + col] = accV1[jj][r] + (i >= lastb ? accV2[jj][r] : 0.0f);
+                const float dQ = accQ1[jj][r] + (ri[r] < 0 ? accQ2[jj][r] + dd[r] * sZ[col] : 0.0f);
+                p.dq[((t0 + i) * p.H + h) * kC + col] = dQ * pq[jj][r];
             }
         }
 }
@@ -406,7 +475,7 @@ hipError_t linattn_bwd_summary_launch(const LinBwdArgs& a, hipStream_t s) {
 }
 
 hipError_t linattn_bwd_grad_launch(const LinBwdArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL(linattn_bwd_grad_kernel, dim3((unsigned)a.nch, (unsigned)a.H), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(linattn_bwd_grad_kernel, dim3((unsigned)a.nch, (unsigned)a.H), dim3(kGradThreads), 0, s, a);
     return hipGetLastError();
 }
 
