@@ -71,11 +71,12 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     const int b = chain / p.nfb;
     const int fb = chain - b * p.nfb;
     const int Qp = p.Qp;
-    const int Gw = 64 / Qp;
+    const int qsh = __builtin_ctz((unsigned)Qp);   // Qp is a power of two
+    const int Gw = 64 >> qsh;
     const int wave = tid >> 6;
     const int lane = tid & 63;
     const int q = lane & (Qp - 1);
-    const int j = lane / Qp;
+    const int j = lane >> qsh;
     const int Dp = Qp * VEC;
     const int64_t L = (int64_t)NW * Gw * R;
     const int64_t tile_row0 = tile * L;
@@ -274,7 +275,8 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
             // chain-major workspace [chain][T][jpc], so that a tile writes
             // whole lines (ffm_bwd_finish_kernel puts them in [B][T][m] order).
             const int64_t cc = p.ffm_c;
-            const int64_t jpc = Dp / cc;
+            const int csh = __builtin_ctzll((uint64_t)cc);  // c is a power of two here
+            const int64_t jpc = Dp >> csh;
             float* const dxw = p.dxr + (int64_t)chain * T * jpc;
 #pragma unroll
             for (int r = R - 1; r >= 0; --r) {
@@ -285,11 +287,11 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
 #pragma unroll
                     for (int v = 0; v < VEC; ++v) part += C::get(rg[r], v).re;
                     for (int off = 1; off < (int)(cc / VEC); off <<= 1) part += __shfl_xor(part, off, 64);
-                    if (in && (q % (int)(cc / VEC)) == 0) dxw[t * jpc + (q * VEC) / cc] = part;
+                    if (in && (q & ((int)(cc / VEC) - 1)) == 0) dxw[t * jpc + ((q * VEC) >> csh)] = part;
                 } else {
 #pragma unroll
                     for (int v = 0; v < VEC; ++v)
-                        if (in && f0 + v < p.d) dxw[t * jpc + (q * VEC + v) / cc] = C::get(rg[r], v).re;
+                        if (in && f0 + v < p.d) dxw[t * jpc + ((q * VEC + v) >> csh)] = C::get(rg[r], v).re;
                 }
             }
         } else {

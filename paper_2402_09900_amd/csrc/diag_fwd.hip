@@ -101,11 +101,12 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     const int b = chain / p.nfb;
     const int fb = chain - b * p.nfb;
     const int Qp = p.Qp;
-    const int Gw = 64 / Qp;
+    const int qsh = __builtin_ctz((unsigned)Qp);   // Qp is a power of two
+    const int Gw = 64 >> qsh;
     const int wave = tid >> 6;
     const int lane = tid & 63;
     const int q = lane & (Qp - 1);
-    const int j = lane / Qp;
+    const int j = lane >> qsh;
     const int Dp = Qp * VEC;
     const int64_t L = (int64_t)NW * Gw * R;
     const int64_t tile_row0 = tile * L;
@@ -143,7 +144,9 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
         uint32_t xo[VEC];
 #pragma unroll
         for (int v = 0; v < VEC; ++v)
-            xo[v] = active && f0 + v < p.d ? (uint32_t)(((int64_t)lrow * m + (f0 + v) / p.ffm_c) * 4) : kOob;
+            xo[v] = active && f0 + v < p.d
+                        ? (uint32_t)(((int64_t)lrow * m + (int64_t)((uint32_t)(f0 + v) / (uint32_t)p.ffm_c)) * 4)
+                        : kOob;
         const uint32_t xstep = active ? (uint32_t)(m * 4) : 0u;
 #pragma unroll
         for (int r = 0; r < R; ++r) {

@@ -436,9 +436,10 @@ __device__ __forceinline__ void lookback(const void* agg, const void* incl, int6
                                          int Dp, int Qp, bool need, S (&carry)[VEC], LookbackLds<S, VEC>& lds,
                                          uint32_t* timeout) {
     const int lane = threadIdx.x & 63;
+    const int qsh = __builtin_ctz((unsigned)Qp);   // Qp is a power of two
     const int q = lane & (Qp - 1);
-    const int j = lane / Qp;
-    const int Gw = 64 / Qp;
+    const int j = lane >> qsh;
+    const int Gw = 64 >> qsh;
     S accA[VEC], accH[VEC];
 #pragma unroll
     for (int v = 0; v < VEC; ++v) {
@@ -583,8 +584,9 @@ __device__ __forceinline__ Seg<S, VEC> seg_shfl(const Seg<S, VEC>& x, int src) {
 template <class S, int VEC, bool REV>
 __device__ __forceinline__ void wave_group_scan(Seg<S, VEC>& inc, Seg<S, VEC>& exc, int Qp) {
     const int lane = threadIdx.x & 63;
-    const int j = lane / Qp;
-    const int Gw = 64 / Qp;
+    const int qsh = __builtin_ctz((unsigned)Qp);   // Qp is a power of two
+    const int j = lane >> qsh;
+    const int Gw = 64 >> qsh;
     for (int k = 1; k < Gw; k <<= 1) {
         const int src = REV ? lane + k * Qp : lane - k * Qp;
         const bool has = REV ? (j + k < Gw) : (j >= k);
