@@ -29,10 +29,15 @@ step i uses copy i mod n, so inputs are read from HBM rather than from the
 256 MB last-level cache left warm by the previous step.
 
 value = tape timesteps x features per second of the whole step (B*T*d, or
-T*H*dv for linear attention).  roofline: the dominant kernel's algorithmic
-bytes (or flops) per launch over its average launch time, measured here with
-HIP events on the launch stream.  cpu_baseline: the fp64 oracle timed on this
-host on a bounded sample of the same workload.
+T*H*dv for linear attention), from the wall time of the K timed steps.
+roofline: the dominant call's algorithmic bytes (or flops) per launch over
+its average launch time, measured in the timed steps with HIP events on the
+launch stream.  The dominant call is the slowest one in the warmup steps,
+which carry events on every call; in the timed steps only it does (an event
+pair costs the GPU a few microseconds of idle time between calls), and the
+other calls' times in config.ms_per_call come from as many steps again after
+the timed ones.  cpu_baseline: the fp64 oracle timed on this host on a
+bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -81,6 +86,9 @@ class Timer:
 
     def mean_ms(self):
         return float(np.mean([a.elapsed_time(b) for a, b in self.pairs])) if self.pairs else 0.0
+
+    def median_ms(self):
+        return float(np.median([a.elapsed_time(b) for a, b in self.pairs])) if self.pairs else 0.0
 
 
 def dev_tensor(torch, arr, kind):
@@ -450,6 +458,10 @@ def main():
     else:
         w, sets, bytes_per, n = setup_diag(torch, mb, tapes, key)
     calls = sets[0]
+    # the warmup steps carry HIP events on every call; the slowest call is
+    # the dominant one, and in the timed steps only it carries events (each
+    # event pair left the GPU idle for a few microseconds between calls)
+    warm = {name: Timer(torch) for name in calls}
     timers = {name: Timer(torch) for name in calls}
 
     # calibration anchor for hardware byte counters: one plain device copy of
@@ -460,21 +472,27 @@ def main():
     torch.cuda.synchronize()
     del cal_src, cal_dst
 
-    def step(i, timed):
+    def step(i, tm, which):
         for name, fn in sets[i % len(sets)].items():
-            if timed:
-                timers[name](fn)
+            if name in which:
+                tm[name](fn)
             else:
                 fn()
 
-    for i in range(args.warmup):
-        step(i, False)
+    for i in range(max(args.warmup, 1)):      # with no warmup, one untimed step picks the dominant call
+        step(i, warm, calls)
     torch.cuda.synchronize()
+    dom = max(calls, key=lambda k: warm[k].median_ms())   # the median ignores a slow first call
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(args.warmup + i, True)
+        step(args.warmup + i, timers, (dom,))
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    # the other calls' durations, from as many steps again after the timed
+    # region, with events on every call
+    for i in range(args.steps):
+        step(args.warmup + args.steps + i, timers, tuple(k for k in calls if k != dom))
+    torch.cuda.synchronize()
     ms_per_step = wall * 1e3 / max(args.steps, 1)
     value = n / (ms_per_step * 1e-3)
     # every call on a prepared workspace ran (no mismatch) and no wait gave up
@@ -485,7 +503,6 @@ def main():
             sys.exit(1)
 
     per_call_ms = {name: timers[name].mean_ms() for name in calls}
-    dom = max(per_call_ms, key=per_call_ms.get)
     if flops is not None:
         achieved = flops[dom] / (per_call_ms[dom] * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": FP32_MFMA_PEAK_TFLOPS,

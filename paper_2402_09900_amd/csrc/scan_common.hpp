@@ -635,18 +635,18 @@ constexpr int kCountWin = 4;      // blocks of 64 predecessors per round trip
 // up to the nearest unpublished one) and `used` the positions consumed;
 // returns true when an inclusive word closed the walk.  Positions before the
 // first tile of the tape read as an inclusive zero.
-template <typename V>
+template <typename V, int WIN = kCountWin>
 __device__ __forceinline__ bool count_window(const uint64_t* desc, int64_t base, int64_t stride, V& sum, int& used) {
     const int lane = threadIdx.x & 63;
-    uint64_t w[kCountWin];
+    uint64_t w[WIN];
 #pragma unroll
-    for (int k = 0; k < kCountWin; ++k) {
+    for (int k = 0; k < WIN; ++k) {
         const int64_t i = base - (int64_t)(64 * k + lane) * stride;
         w[k] = i >= 0 ? peek64(desc + i) : kCountIncl;
     }
-    int fi = 64 * kCountWin, fe = 64 * kCountWin;       // first inclusive / unpublished position
+    int fi = 64 * WIN, fe = 64 * WIN;                   // first inclusive / unpublished position
 #pragma unroll
-    for (int k = kCountWin - 1; k >= 0; --k) {          // the nearest block wins
+    for (int k = WIN - 1; k >= 0; --k) {                // the nearest block wins
         const bool empty = w[k] == kEmpty64;
         const uint64_t me = __ballot(empty);
         const uint64_t mi = __ballot(!empty && (w[k] & kCountIncl) != 0);
@@ -657,7 +657,7 @@ __device__ __forceinline__ bool count_window(const uint64_t* desc, int64_t base,
     used = stop ? fi + 1 : fe;
     V mine = 0;
 #pragma unroll
-    for (int k = 0; k < kCountWin; ++k) mine += 64 * k + lane < used ? (V)(w[k] & kCountValue) : (V)0;
+    for (int k = 0; k < WIN; ++k) mine += 64 * k + lane < used ? (V)(w[k] & kCountValue) : (V)0;
     sum = wave_sum(mine);
     return stop;
 }

@@ -152,3 +152,24 @@ def test_sample_many_tiles_and_fallback(monkeypatch):
     check_sample(tb.D, tb.begins, tb.draws, tb.batch, "many tiles")
     monkeypatch.setenv("MEMOROID_FALLBACK_POLLS", "0")
     check_sample(tb.D, tb.begins, tb.draws, tb.batch, "many tiles fallback")
+
+
+def test_sample_without_optional_outputs():
+    """out_src and filled are optional (NULL): the batch and its begin flags
+    are still exact."""
+    tb = tapes.make_tbb(8, seed=36, n=60000, batch=20000, n_draws=300)
+    announce("tbb sample without out_src / filled")
+    D, I, dr = dev(tb.D), dev(tb.begins), dev(tb.draws)
+    K, batch = tb.draws.size, tb.batch
+    ws = torch.empty(mb.memoroid_tbb_sample_workspace_bytes(K, batch), dtype=torch.uint8, device=DEV)
+    s = torch.cuda.current_stream().cuda_stream
+    assert mb.memoroid_workspace_prepare(ws.data_ptr(), ws.numel(), s) == mb.OK
+    out = torch.empty((batch, tb.D.shape[1]), dtype=torch.float32, device=DEV)
+    ost = torch.empty(batch, dtype=torch.uint8, device=DEV)
+    assert mb.memoroid_tbb_sample(D.data_ptr(), tb.D.shape[0], tb.D.shape[1] * 4, I.data_ptr(), I.numel(),
+                                  dr.data_ptr(), K, batch, out.data_ptr(), ost.data_ptr(), None, None,
+                                  ws.data_ptr(), ws.numel(), s) == mb.OK
+    assert mb.memoroid_workspace_status(ws.data_ptr(), ws.numel(), s) == mb.OK
+    r_out, r_st, _, _ = oracle.tbb_sample(tb.D, tb.begins, tb.draws, batch)
+    np.testing.assert_array_equal(ost.cpu().numpy(), r_st)
+    assert np.array_equal(out.cpu().numpy().view(np.uint8), r_out.view(np.uint8))
