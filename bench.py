@@ -90,6 +90,30 @@ class Timer:
     def median_ms(self):
         return float(np.median([a.elapsed_time(b) for a, b in self.pairs])) if self.pairs else 0.0
 
+    def percentiles_ms(self, qs=(10, 50, 90)):
+        v = [a.elapsed_time(b) for a, b in self.pairs]
+        return [round(float(np.percentile(v, q)), 4) for q in qs] if v else None
+
+
+COPY_PROBE_BYTES = 1 << 30     # plain read + write kernel, larger than the 256 MB last-level cache
+
+
+def copy_probe_gbps(torch, reps=5):
+    """Bandwidth of a plain device copy kernel (a torch elementwise negation
+    of a 1 GiB float32 buffer: read 1 GiB, write 1 GiB), median of `reps`
+    event-timed runs; the attainable ceiling the scans are compared with."""
+    src = torch.empty(COPY_PROBE_BYTES // 4, dtype=torch.float32, device="cuda")
+    src.fill_(1.0)
+    dst = torch.empty_like(src)
+    tm = Timer(torch)
+    torch.neg(src, out=dst)
+    for _ in range(reps):
+        tm(lambda: torch.neg(src, out=dst))
+    torch.cuda.synchronize()
+    ms = tm.median_ms()
+    del src, dst
+    return 2 * COPY_PROBE_BYTES / (ms * 1e-3) / 1e9
+
 
 def dev_tensor(torch, arr, kind):
     arr = np.ascontiguousarray(arr)
@@ -520,6 +544,13 @@ def main():
                       "gae": "memoroid_gae", "insert": "memoroid_tbb_begin_indices",
                       "sample": "memoroid_tbb_sample"}[dom]
     roof["ms_per_launch"] = round(per_call_ms[dom], 4)
+    roof["ms_per_launch_p10_p50_p90"] = timers[dom].percentiles_ms()
+    if flops is None:
+        # the fraction of what a plain copy kernel reaches on this GPU, from
+        # the same harness (after the timed steps)
+        cgbps = copy_probe_gbps(torch)
+        roof["copy_probe_GBps"] = round(cgbps, 1)
+        roof["frac_of_copy_probe"] = round(achieved / cgbps, 4)
     roof["algorithmic_bytes_per_launch"] = int(bytes_per[dom])
     if flops is not None:
         roof["algorithmic_flops_per_launch"] = int(flops[dom])

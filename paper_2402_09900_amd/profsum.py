@@ -45,6 +45,11 @@ def trace(db, title, cmd):
     if COPY_KERNEL in agg:
         notes.append("`%s`: input uploads and the byte-counter calibration copy, before the timed steps."
                      % COPY_KERNEL)
+    torch_kernels = [k for k in agg if not k.startswith(("memoroid::", "void memoroid::")) and k != COPY_KERNEL]
+    if torch_kernels:
+        notes.append("other kernels (%s): bench.py's own buffer fills and its copy-bandwidth probe (a 1 GiB "
+                     "elementwise negation), outside the timed steps." % ", ".join("`%s`" % short(k, 40)
+                                                                                   for k in torch_kernels))
     if notes:
         print()
         for n in notes:
