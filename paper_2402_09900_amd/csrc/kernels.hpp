@@ -226,7 +226,11 @@ struct DiscArgs {
 hipError_t disc_launch(bool vec, bool gae, const DiscArgs& a, int64_t ntiles, hipStream_t s);
 
 // ------------------------------------------------ tape-based batching
-constexpr int kTbbBeginTile = 16384;      // flags per workgroup of the compaction
+#ifndef MEMOROID_TBB_BEGIN_BLOCKS
+#define MEMOROID_TBB_BEGIN_BLOCKS 2
+#endif
+constexpr int kTbbBeginBlocks = MEMOROID_TBB_BEGIN_BLOCKS;    // blocks of 16384 flags per compaction workgroup
+constexpr int kTbbBeginTile = 16384 * kTbbBeginBlocks;        // flags per workgroup of the compaction
 #ifndef MEMOROID_TBB_DRAW_TILE
 #define MEMOROID_TBB_DRAW_TILE 2048
 #endif

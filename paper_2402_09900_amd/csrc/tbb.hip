@@ -2,13 +2,13 @@
 // gfx950.
 //
 // Insertion needs I = offset + where(b): a stream compaction of the begin
-// flags.  One pass: a tile (256 lanes x 64 flags) counts its begin steps,
-// publishes the count at once, finds the count before it with a look-back
-// over earlier tiles and writes its indices.  Tiles are ordered by workgroup
-// index; a look-back that sees no progress counts the awaited tile's flags
-// itself (a fallback), so no wait depends on another workgroup having
-// started.  The count words are banked by epoch (see scan_common.hpp);
-// each tile keeps its own epoch word.
+// flags.  One pass: a tile (kIdxBlocks blocks of 256 lanes x 64 flags)
+// counts its begin steps, publishes the count at once, finds the count
+// before it with a look-back over earlier tiles and writes its indices.
+// Tiles are ordered by workgroup index; a look-back that sees no progress
+// counts the awaited tile's flags itself (a fallback), so no wait depends on
+// another workgroup having started.  The count words are banked by epoch
+// (see scan_common.hpp); each tile keeps its own epoch word.
 //
 // Sampling concatenates the drawn episodes D[I[i] : I[i+1]] and cuts the
 // batch to B rows.  Two kernels: a row-sum pass over the draws (the same
@@ -26,8 +26,10 @@ namespace memoroid {
 
 namespace {
 
-constexpr int kFlagsPerLane = 64;
-constexpr int kIdxTile = 256 * kFlagsPerLane;      // flags per workgroup
+constexpr int kFlagsPerLane = 64;                  // flags per lane and block
+constexpr int kIdxBlocks = kTbbBeginBlocks;         // blocks per tile
+constexpr int kIdxBlock = 256 * kFlagsPerLane;      // flags per block (one per lane of the workgroup)
+constexpr int kIdxTile = kIdxBlocks * kIdxBlock;    // flags per workgroup
 static_assert(kIdxTile == kTbbBeginTile, "compaction tile");
 
 // Bit i set when byte i of the lane's 64 flags is nonzero.
@@ -67,7 +69,8 @@ __device__ __forceinline__ uint32_t wave_incl_sum(uint32_t v) {
 
 template <bool VEC>
 __global__ __launch_bounds__(256) void tbb_begins_kernel(TbbBeginArgs p) {
-    __shared__ uint32_t s_wave[4];
+    constexpr int NB = kIdxBlocks;
+    __shared__ uint32_t s_wave[NB][4];
     __shared__ uint32_t s_before;
     __shared__ uint32_t s_bank;               // epoch parity; all ones: stand down
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -78,22 +81,36 @@ __global__ __launch_bounds__(256) void tbb_begins_kernel(TbbBeginArgs p) {
     if (tid == 0) sig_seen = peek_sig(p.hdr);
     const int64_t t0 = tile * kIdxTile;
     const Rsrc rs = make_rsrc(p.start + t0, p.n - t0);
-    const uint32_t loff = (uint32_t)(tid * kFlagsPerLane);
-    const uint64_t mask = lane_begin_mask<VEC>(rs, loff);
+    // block b of the tile: lane tid holds flags (b * 256 + tid) * 64 .. + 63,
+    // so that each block is one contiguous, coalesced 16 KB read
+    uint64_t mask[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) mask[b] = lane_begin_mask<VEC>(rs, (uint32_t)((b * 256 + tid) * kFlagsPerLane));
     if (tid == 0) epoch = read_epoch(p.epoch + tile);
-    const uint32_t mine = (uint32_t)__builtin_popcountll(mask);
-    const uint32_t incl = wave_incl_sum(mine);
-    if (lane == 63) s_wave[w] = incl;
+    uint32_t mine[NB], incl[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        mine[b] = (uint32_t)__builtin_popcountll(mask[b]);
+        incl[b] = wave_incl_sum(mine[b]);
+        if (lane == 63) s_wave[b][w] = incl[b];
+    }
     if (tid == 0) s_bank = ws_bound_to(p.hdr, p.sig, sig_seen, tile == 0) ? (epoch & 1u) : kEmpty32;
     __syncthreads();
     const uint32_t bank = __builtin_amdgcn_readfirstlane(s_bank);
     if (bank == kEmpty32) return;             // workspace bound to another call: every tile stands down
     uint64_t* const cnt = (uint64_t*)((char*)p.cnt + (bank ? p.bank : 0));
-    const uint32_t own = s_wave[0] + s_wave[1] + s_wave[2] + s_wave[3];
-    uint32_t before_wave = 0;
+    // begin steps of the tile, and those before this lane's chunk of block b
+    // (earlier blocks, then earlier wavefronts of block b)
+    uint32_t own = 0, before[NB];
 #pragma unroll
-    for (int ww = 0; ww < 4; ++ww)
-        if (ww < w) before_wave += s_wave[ww];
+    for (int b = 0; b < NB; ++b) {
+        before[b] = own;
+#pragma unroll
+        for (int ww = 0; ww < 4; ++ww) {
+            if (ww < w) before[b] += s_wave[b][ww];
+            own += s_wave[b][ww];
+        }
+    }
 
     // wavefront 3 publishes the tile's own count (inclusive for tile 0);
     // wavefront 0 looks back (publishing and polling use different waves)
@@ -121,7 +138,7 @@ __global__ __launch_bounds__(256) void tbb_begins_kernel(TbbBeginArgs p) {
                     const Rsrc rb = make_rsrc(p.start + tb, p.n - tb);
                     uint32_t c = 0;
 #pragma unroll 1
-                    for (int part = 0; part < 4; ++part)
+                    for (int part = 0; part < 4 * NB; ++part)
                         c += (uint32_t)__builtin_popcountll(
                             lane_begin_mask<VEC>(rb, (uint32_t)((part * 64 + lane) * kFlagsPerLane)));
                     acc += wave_sum_u32(c);
@@ -139,12 +156,16 @@ __global__ __launch_bounds__(256) void tbb_begins_kernel(TbbBeginArgs p) {
         }
     }
     __syncthreads();
-    uint64_t m = mask;
-    int64_t k = (int64_t)s_before + before_wave + (incl - mine);
-    while (m) {
-        const int b = __builtin_ctzll(m);
-        p.indices[k++] = p.offset + t0 + loff + b;
-        m &= m - 1;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        uint64_t m = mask[b];
+        int64_t k = (int64_t)s_before + before[b] + (incl[b] - mine[b]);
+        const int64_t f0 = p.offset + t0 + (int64_t)(b * 256 + tid) * kFlagsPerLane;
+        while (m) {
+            const int bit = __builtin_ctzll(m);
+            p.indices[k++] = f0 + bit;
+            m &= m - 1;
+        }
     }
     if (tid == 0) write_epoch(p.epoch + tile, epoch);
 }
