@@ -4,6 +4,7 @@
     python -m paper_2402_09900_amd.profsum trace  <kernel_trace results.db> <title> <command>
     python -m paper_2402_09900_amd.profsum traffic <FETCH_SIZE results.db> <WRITE_SIZE results.db> <title> <command>
     python -m paper_2402_09900_amd.profsum json <out.json> <command> <workload>=<FETCH db>,<WRITE db> ...
+    python -m paper_2402_09900_amd.profsum mfma <SQ counter db> <kernel trace db> <title> <command> <kernel>=<wavefronts> ...
 
 `trace` prints per-kernel dispatch counts and durations.  `traffic` prints,
 per kernel, the FETCH_SIZE / WRITE_SIZE counters (KiB per dispatch) and the
@@ -119,6 +120,40 @@ CALLS = {
 }
 
 
+MFMA_FLOPS = 2 * 16 * 16 * 4      # one v_mfma_f32_16x16x4_f32
+FP32_MFMA_PEAK = 157.3e12
+
+
+def mfma(pmc_db, trace_db, waves_per_kernel, title, cmd):
+    """MFMA use of the linear-attention kernels from SQ counters.  The SQ
+    block samples one shader engine, so the counters give MFMA instructions
+    per wavefront (SQ_INSTS_VALU_MFMA_F32 / SQ_WAVES); flops issued = that x
+    the launch's wavefronts x 2048, over the kernel's mean traced duration
+    and the fp32 MFMA peak."""
+    c = {}
+    con = sqlite3.connect(pmc_db)
+    for k, name, v in con.execute("select name, counter_name, counter_value from pmc_events"):
+        c.setdefault(k, {}).setdefault(name, []).append(v)
+    con = sqlite3.connect(trace_db)
+    dur = {}
+    for k, s0, e0 in con.execute("select name, start, end from kernels"):
+        dur.setdefault(k, []).append((e0 - s0) * 1e-9)
+    print("# %s\n\ncommand: `%s`\n" % (title, cmd))
+    print("| kernel | wavefronts / launch | MFMA instr / wavefront | flops issued / launch | mean duration us "
+          "| issued TFLOP/s | % of fp32 MFMA peak |")
+    print("|---|---:|---:|---:|---:|---:|---:|")
+    for k, nw in waves_per_kernel:
+        full = [kk for kk in c if kk.startswith(k) or kk.startswith("void " + k)]
+        if not full:
+            continue
+        d = c[full[0]]
+        per_wave = sum(d["SQ_INSTS_VALU_MFMA_F32"]) / max(sum(d["SQ_WAVES"]), 1)
+        flops = per_wave * nw * MFMA_FLOPS
+        t = statistics.mean(next(v for kk, v in dur.items() if kk.startswith(k) or kk.startswith("void " + k)))
+        print("| %s | %d | %.1f | %.3g | %.1f | %.1f | %.1f |" % (short(full[0]), nw, per_wave, flops, t * 1e6,
+                                                                 flops / t / 1e12, 100 * flops / t / FP32_MFMA_PEAK))
+
+
 def per_dispatch_bytes(fdb, wdb):
     """Scaled bytes per dispatch of every kernel in a pair of counter runs."""
     f, w = counters(fdb), counters(wdb)
@@ -166,6 +201,10 @@ def write_json(out, cmd, specs):
 if __name__ == "__main__":
     if sys.argv[1] == "trace":
         trace(sys.argv[2], sys.argv[3], sys.argv[4])
+    elif sys.argv[1] == "mfma":
+        # mfma <pmc db> <trace db> <title> <command> <kernel>=<wavefronts per launch> ...
+        specs = [(a.split("=")[0], int(a.split("=")[1])) for a in sys.argv[6:]]
+        mfma(sys.argv[2], sys.argv[3], specs, sys.argv[4], sys.argv[5])
     elif sys.argv[1] == "traffic":
         traffic(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5])
     else:
