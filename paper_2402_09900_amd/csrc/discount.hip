@@ -360,15 +360,14 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
         if (!TM.f && lane == 0) publish64(incl + slot, pack2(rmap_apply(TM, carry), 0.0f));
         if (lane == 0) s_carry = carry;
     }
-    __syncthreads();
 
     // ------------------------------------------------------------ outputs
-    float c = s_carry;
-#pragma unroll
-    for (int ww = 3; ww > 0; --ww)
-        if (ww > w) c = rmap_apply(Wt[ww], c);
-#pragma unroll
-    for (int u = NB - 1; u >= 0; --u) {
+    // Block u of a lane starts from the carry passed through the later
+    // wavefronts' and blocks' maps; where one of those maps holds a reset the
+    // value no longer depends on the carry, and such blocks are formed and
+    // stored before the carry is known (wavefronts 1-3 do it while wavefront
+    // 0 looks back), so their stores overlap the wait.
+    auto emit = [&](int u, float c) {
         const int64_t t0 = t_seg + 64 * VEC * u + VEC * lane;
         float y = rmap_apply(E[u], c);
         V out;
@@ -389,6 +388,35 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
                 }
             }
         }
+    };
+    uint32_t stored = 0;
+    {
+        float c = 0.0f;                       // exact wherever `dep` is false
+        bool dep = true;
+#pragma unroll
+        for (int ww = 3; ww > 0; --ww)
+            if (ww > w) {
+                dep = dep && !Wt[ww].f;
+                c = rmap_apply(Wt[ww], c);
+            }
+#pragma unroll
+        for (int u = NB - 1; u >= 0; --u) {
+            if (!dep || E[u].f) {
+                emit(u, c);
+                stored |= 1u << u;
+            }
+            dep = dep && !Bm[u].f;
+            c = rmap_apply(Bm[u], c);
+        }
+    }
+    __syncthreads();
+    float c = s_carry;
+#pragma unroll
+    for (int ww = 3; ww > 0; --ww)
+        if (ww > w) c = rmap_apply(Wt[ww], c);
+#pragma unroll
+    for (int u = NB - 1; u >= 0; --u) {
+        if (!((stored >> u) & 1u)) emit(u, c);
         c = rmap_apply(Bm[u], c);
     }
     if (tid == 0) write_epoch(p.epoch + ticket, epoch);
