@@ -48,20 +48,6 @@ __device__ __forceinline__ bool keep_ij(int i, int j, int ri, int nvalid) {
     return i < nvalid && j <= i && j >= (ri > 0 ? ri : 0);
 }
 
-// Write a 64x64 accumulator tile (acc[jt][r] = C[16w + 4(lane/16) + r][16 jt + lane%16])
-// to LDS, natural or rotated.
-template <bool ROT>
-__device__ __forceinline__ void acc_to_lds(float* s, const f32x4 (&acc)[4]) {
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-#pragma unroll
-    for (int jt = 0; jt < 4; ++jt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int row = 16 * w + 4 * (lane >> 4) + r, col = 16 * jt + (lane & 15);
-            s[row * kLD + (ROT ? rot_col(row, col) : col)] = acc[jt][r];
-        }
-}
-
 // phi of a fetched tile, rows outside [lo, hi) selected to zeros
 __device__ __forceinline__ void phi_rows(f32x4 (&v)[4], int lo, int hi) {
 #pragma unroll
@@ -261,7 +247,7 @@ __device__ __forceinline__ void grad_fetch_state(f32x4 (&v)[kGradPer], const flo
 __device__ __forceinline__ void grad_phi(f32x4 (&v)[kGradPer], int nvalid) {
 #pragma unroll
     for (int u = 0; u < kGradPer; ++u) {
-        const bool in = ((threadIdx.x + kGradThreads * u) >> 4) < nvalid;
+        const bool in = (int)((threadIdx.x + kGradThreads * u) >> 4) < nvalid;
         v[u].x = in ? phi(v[u].x) : 0.0f; v[u].y = in ? phi(v[u].y) : 0.0f;
         v[u].z = in ? phi(v[u].z) : 0.0f; v[u].w = in ? phi(v[u].w) : 0.0f;
     }
