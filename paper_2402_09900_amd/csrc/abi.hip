@@ -902,12 +902,12 @@ void plan_tbb(int64_t n, TbbPlan* p) {
 }
 
 // Sampling workspace: header, epoch words, two banks of row-sum words, the
-// rows filled and draws inside the batch, the group table, and each draw's
-// first batch row and source shift.
+// rows filled and draws inside the batch, the lead tiles' verdict words, the
+// group table, and each draw's first batch row and source shift.
 struct SamplePlan {
     int64_t ntiles = 0, groups = 0;
-    size_t off_epoch = 0, off_cnt = 0, bank_bytes = 0, off_meta = 0, off_first = 0, off_row0 = 0, off_shift = 0,
-           total = 0;
+    size_t off_epoch = 0, off_cnt = 0, bank_bytes = 0, off_meta = 0, off_dec = 0, off_first = 0, off_row0 = 0,
+           off_shift = 0, total = 0;
 };
 
 constexpr int64_t kSampleMaxRows = (int64_t)1 << 47;   // batch and n_D bound: row sums stay below 2^48
@@ -919,7 +919,8 @@ void plan_sample(int64_t n_draws, int64_t batch, SamplePlan* p) {
     p->off_cnt = align_up(p->off_epoch + (size_t)p->ntiles * 4);
     p->bank_bytes = align_up((size_t)p->ntiles * 8);
     p->off_meta = p->off_cnt + 2 * p->bank_bytes;
-    p->off_first = align_up(p->off_meta + 16);
+    p->off_dec = align_up(p->off_meta + 16);
+    p->off_first = align_up(p->off_dec + 64 * 128);    // 64 verdict words, one per 128-byte line
     p->off_row0 = align_up(p->off_first + (size_t)p->groups * 8);
     p->off_shift = align_up(p->off_row0 + (size_t)n_draws * 8);
     p->total = align_up(p->off_shift + (size_t)n_draws * 8);
@@ -1023,6 +1024,7 @@ int memoroid_tbb_sample(const void* D, int64_t n_D, int64_t row_bytes, const int
         a.cnt = (uint64_t*)(ws + p.off_cnt);
         a.bank = (int64_t)p.bank_bytes;
         a.meta = (int64_t*)(ws + p.off_meta);
+        a.dec = (uint64_t*)(ws + p.off_dec);
         a.first = (int64_t*)(ws + p.off_first);
         a.row0 = (int64_t*)(ws + p.off_row0);
         a.shift = (int64_t*)(ws + p.off_shift);
@@ -1030,6 +1032,17 @@ int memoroid_tbb_sample(const void* D, int64_t n_D, int64_t row_bytes, const int
     }
     const int unit = (row_bytes % 16 == 0 && aligned(out, 16) && (!D || aligned(D, 16))) ? 16
                      : (row_bytes % 4 == 0 && aligned(out, 4) && (!D || aligned(D, 4))) ? 4 : 1;
+    // Draws are taken in order until the batch is full: about batch / (mean
+    // episode length) = batch * n_I / n_D of them.  The row-sum tiles that
+    // twice that many draws need run at once; the later ones wait for them
+    // and skip their loads if the batch is already full.
+    a.lead = p.ntiles;
+    if (n_draws > 0 && n_D > 0) {
+        const double need = 2.0 * (double)batch * (double)n_I / (double)n_D;
+        const double tiles = need / (double)kTbbDrawTile + 1.0;
+        a.lead = tiles < (double)p.ntiles ? (int64_t)tiles : p.ntiles;
+        if (a.lead < 1) a.lead = 1;
+    }
     return check_hip(tbb_sample_launch(unit, a, p.ntiles, s));
 }
 

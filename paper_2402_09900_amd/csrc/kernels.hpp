@@ -275,6 +275,8 @@ struct TbbSampleArgs {
     uint64_t* cnt;           // [tiles] row-sum descriptor words (bank 0)
     int64_t bank;            // bytes from bank 0 to bank 1
     int64_t* meta;           // [2]: rows filled; draws whose first row is inside the batch
+    int64_t lead;            // row-sum tiles that run without first waiting for the earlier ones
+    uint64_t* dec;           // [64 words, 128 bytes apart]: (epoch << 32) | 1 batch full within the lead tiles, | 2 not
     int64_t* first;          // [groups]: the draw holding each gather group's first row
     int64_t* row0;           // [n_draws]: first batch row of each draw (draws inside the batch)
     int64_t* shift;          // [n_draws]: source row minus batch row (same draws)

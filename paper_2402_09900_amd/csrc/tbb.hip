@@ -16,7 +16,10 @@
 // starts in the batch and which draw holds the first row of each group of
 // 256 output rows; then a gather in which every group reads its first draw
 // from that table, every row finds its draw by binary search over the next
-// 256 draws' first rows, and the workgroup copies the rows.
+// 256 draws' first rows, and the workgroup copies the rows.  The draws are
+// used in order until the batch is full, so the row-sum tiles past the few
+// that should fill it (from the buffer's mean episode length) wait for those
+// tiles' verdict and, if the batch is already full, skip their loads.
 #include <type_traits>
 
 #include "scan_common.hpp"
@@ -231,12 +234,54 @@ __global__ __launch_bounds__(256) void tbb_rows_kernel(TbbSampleArgs p) {
     __shared__ int64_t s_wave[4];
     __shared__ uint64_t s_before;
     __shared__ uint32_t s_bank;               // epoch parity; all ones: stand down
+    __shared__ uint32_t s_skip, s_epoch;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int64_t tile = blockIdx.x;
     const uint64_t cap = (uint64_t)p.batch;
     uint64_t sig_seen = 0;
     uint32_t epoch = 0;
     if (tid == 0) sig_seen = peek_sig(p.hdr);
+    if (tile >= p.lead) {
+        // a tile past the lead ones waits (one lane, bounded) for the last
+        // lead tile's verdict; if the lead tiles already fill the batch, every
+        // draw here starts past its end and the tile only publishes the
+        // saturated sum, with no loads
+        if (tid == 0) {
+            epoch = read_epoch(p.epoch + tile);
+            const bool bound = ws_bound_to(p.hdr, p.sig, sig_seen, false);
+            uint32_t skip = 0;
+            if (bound) {
+                // the last lead tile posts its verdict in 64 copies, one per
+                // cache line, so that the waiting tiles do not all poll one
+                // memory location
+                const uint64_t* dw = p.dec + 16 * (tile & 63);
+                uint32_t polls = 0;
+                while (true) {
+                    const uint64_t v = peek64(dw);
+                    if ((uint32_t)(v >> 32) == epoch && (uint32_t)v != kEmpty32) {
+                        skip = (uint32_t)v == 1u ? 1u : 0u;
+                        break;
+                    }
+                    if (++polls > p.fallback_polls) break;          // go on without it
+                    __builtin_amdgcn_s_sleep(4);
+                }
+            }
+            s_skip = skip;
+            s_bank = bound ? (epoch & 1u) : kEmpty32;
+        }
+        __syncthreads();
+        const uint32_t bank = __builtin_amdgcn_readfirstlane(s_bank);
+        if (bank == kEmpty32) return;
+        if (s_skip) {
+            if (tid == 0) {
+                publish64((uint64_t*)((char*)p.cnt + (bank ? p.bank : 0)) + tile, kCountIncl | cap);
+                ((uint64_t*)((char*)p.cnt + (bank ? 0 : p.bank)))[tile] = kEmpty64;
+                write_epoch(p.epoch + tile, epoch);
+            }
+            return;
+        }
+        __syncthreads();                      // s_bank is rewritten below
+    }
     const int64_t k0 = tile * kTbbDrawTile + (int64_t)tid * kDrawsPerLane;
     int64_t lo[kDrawsPerLane], len[kDrawsPerLane];
     int64_t run = 0;
@@ -245,10 +290,13 @@ __global__ __launch_bounds__(256) void tbb_rows_kernel(TbbSampleArgs p) {
         draw_rows(p, k0 + e, lo[e], len[e]);
         run += len[e];
     }
-    if (tid == 0) epoch = read_epoch(p.epoch + tile);
+    if (tid == 0 && tile < p.lead) epoch = read_epoch(p.epoch + tile);
     const int64_t incl = wave_incl_sum64(run);
     if (lane == 63) s_wave[w] = incl;
-    if (tid == 0) s_bank = ws_bound_to(p.hdr, p.sig, sig_seen, tile == 0) ? (epoch & 1u) : kEmpty32;
+    if (tid == 0) {
+        s_bank = ws_bound_to(p.hdr, p.sig, sig_seen, tile == 0) ? (epoch & 1u) : kEmpty32;
+        s_epoch = epoch;
+    }
     __syncthreads();
     const uint32_t bank = __builtin_amdgcn_readfirstlane(s_bank);
     if (bank == kEmpty32) return;             // workspace bound to another call: every tile stands down
@@ -297,10 +345,15 @@ __global__ __launch_bounds__(256) void tbb_rows_kernel(TbbSampleArgs p) {
             }
             if (lane == 0) publish64(cnt + tile, kCountIncl | min_u64(acc + own, cap));
         }
+        if (tile == p.lead - 1 && p.lead < (int64_t)gridDim.x) {
+            // the verdict for the tiles past the lead: is the batch full?
+            const uint64_t v = ((uint64_t)s_epoch << 32) | (min_u64(acc + own, cap) >= cap ? 1u : 2u);
+            __hip_atomic_store(p.dec + 16 * lane, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
         if (lane == 0) {
             s_before = acc;
             const uint64_t total = min_u64(acc + own, cap);
-            if (tile == (int64_t)gridDim.x - 1 && total < cap) {
+            if (tile == (p.n_draws - 1) / kTbbDrawTile && total < cap) {
                 // the draws end inside the batch
                 p.meta[0] = (int64_t)total;
                 p.meta[1] = p.n_draws;
