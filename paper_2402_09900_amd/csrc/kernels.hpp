@@ -239,6 +239,9 @@ constexpr int kTbbBeginTile = 16384 * kTbbBeginBlocks;        // flags per workg
 #endif
 constexpr int kTbbDrawTile = MEMOROID_TBB_DRAW_TILE;          // draws per workgroup of the row sums
 constexpr int kTbbRowsPerGroup = MEMOROID_TBB_ROWS_PER_GROUP; // output rows per workgroup of the gather
+// each of the gather's 256 threads owns RW / 256 rows and window draws
+static_assert(kTbbRowsPerGroup >= 256 && kTbbRowsPerGroup % 256 == 0, "gather group: a multiple of 256 rows");
+static_assert(kTbbDrawTile >= 256 && kTbbDrawTile % 256 == 0, "row-sum tile: a multiple of 256 draws");
 
 struct TbbBeginArgs {
     const uint8_t* start;    // [n] begin flags
