@@ -173,3 +173,18 @@ def test_sample_without_optional_outputs():
     r_out, r_st, _, _ = oracle.tbb_sample(tb.D, tb.begins, tb.draws, batch)
     np.testing.assert_array_equal(ost.cpu().numpy(), r_st)
     assert np.array_equal(out.cpu().numpy().view(np.uint8), r_out.view(np.uint8))
+
+
+def test_sample_lead_estimate_too_small():
+    """The row-sum pass sizes its lead tiles from the buffer's mean episode
+    length; draws of episodes much shorter than the mean leave the batch
+    unfilled after the lead, and the remaining tiles must then sum their
+    draws themselves."""
+    n = 1_000_000
+    rng = np.random.default_rng(43)
+    D = rng.standard_normal((n, 4)).astype(np.float32)
+    # one episode of 900 000 rows, then 100 000 one-row episodes
+    I = np.concatenate([[0], 900_000 + np.arange(100_000)]).astype(np.int64)
+    draws = rng.integers(1, I.size, size=60_000)          # one-row episodes only
+    check_sample(D, I, draws, 50_000, "short draws, long mean")
+    check_sample(D, I, np.concatenate([[0], draws]), 50_000, "long episode first")
