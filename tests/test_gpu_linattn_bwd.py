@@ -50,6 +50,13 @@ def test_ragged_lengths(T):
     check(tapes.make_linattn(3, seed=300 + T, T=T, H=2), "ragged")
 
 
+@pytest.mark.parametrize("H", [1, 3, 5])
+def test_head_counts(H):
+    """Odd head counts: the grid is (chunks, heads) and each head's rows are
+    a 256-byte slice of every [T][H][64] row."""
+    check(tapes.make_linattn(3, seed=400 + H, T=1000 + 13 * H, H=H), "heads")
+
+
 def _with_flags(la, flags):
     la.start = flags.astype(np.uint8)
     return la
