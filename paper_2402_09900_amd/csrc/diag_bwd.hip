@@ -446,15 +446,42 @@ hipError_t ffm_bwd_launch(bool vec, const DiagBwdArgs& args, int64_t ntiles, hip
 
 // One workgroup: thread j < m forms dalpha[j], thread k < c forms domega[k]
 // (loops over the other index), from the summed complex da[m][c].
-__device__ void ffm_param_grad(const float* alpha, const float* omega, const float* da, int64_t m, int64_t c,
+// dα_j = -sign(α_j) Σ_k Re(conj(γ_jk) da_jk) and dω_k = Σ_j Im(conj(γ_jk) da_jk)
+// with γ_jk = exp(-|α_j|) e^{iω_k}, in double.  One workgroup (all 256
+// threads call it): |γ| per row and (cos, sin) per column are evaluated once
+// into LDS, in parallel, so that the sums are plain multiply-adds (the same
+// operations in the same order as evaluating them inside the sums).
+constexpr int kParamRows = 1024, kParamCols = 256, kParamDa = 4096;
+__device__ void ffm_param_grad(const float* alpha, const float* omega, const float* da_g, int64_t m, int64_t c,
                                float* dalpha, float* domega) {
+    __shared__ double s_mag[kParamRows], s_cs[kParamCols], s_sn[kParamCols];
+    __shared__ float s_da[kParamDa];       // da as well, when it fits (loaded once, coalesced)
+    const bool tab = m <= kParamRows && c <= kParamCols;
+    const bool lds_da = 2 * m * c <= kParamDa;
+    if (tab) {
+        for (int64_t j = threadIdx.x; j < m; j += 256) s_mag[j] = exp(-fabs((double)alpha[j]));
+        for (int64_t k = threadIdx.x; k < c; k += 256) sincos((double)omega[k], &s_sn[k], &s_cs[k]);
+    }
+    if (lds_da)
+        for (int64_t e = threadIdx.x; e < 2 * m * c; e += 256) s_da[e] = da_g[e];
+    __syncthreads();
+    const float* da = lds_da ? s_da : da_g;
+    auto mag_of = [&](int64_t j) { return tab ? s_mag[j] : exp(-fabs((double)alpha[j])); };
+    auto trig_of = [&](int64_t k, double& sn, double& cs) {
+        if (tab) {
+            sn = s_sn[k];
+            cs = s_cs[k];
+        } else {
+            sincos((double)omega[k], &sn, &cs);
+        }
+    };
     for (int64_t j = threadIdx.x; dalpha && j < m; j += 256) {
-        const double mag = exp(-fabs((double)alpha[j]));
+        const double mag = mag_of(j);
         const double sgn = alpha[j] > 0.0f ? 1.0 : (alpha[j] < 0.0f ? -1.0 : 0.0);
         double acc = 0.0;
         for (int64_t k = 0; k < c; ++k) {
             double sn, cs;
-            sincos((double)omega[k], &sn, &cs);
+            trig_of(k, sn, cs);
             const double dr = da[2 * (j * c + k)], di = da[2 * (j * c + k) + 1];
             acc += mag * (cs * dr + sn * di);                 // Re(conj(a) da)
         }
@@ -462,10 +489,10 @@ __device__ void ffm_param_grad(const float* alpha, const float* omega, const flo
     }
     for (int64_t k = threadIdx.x; domega && k < c; k += 256) {
         double sn, cs;
-        sincos((double)omega[k], &sn, &cs);
+        trig_of(k, sn, cs);
         double acc = 0.0;
         for (int64_t j = 0; j < m; ++j) {
-            const double mag = exp(-fabs((double)alpha[j]));
+            const double mag = mag_of(j);
             const double dr = da[2 * (j * c + k)], di = da[2 * (j * c + k) + 1];
             acc += mag * (cs * di - sn * dr);                 // Im(conj(a) da)
         }
