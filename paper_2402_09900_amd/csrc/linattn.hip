@@ -35,6 +35,7 @@ namespace memoroid {
 __global__ __launch_bounds__(256) void linattn_summary_kernel(LinSummaryArgs p) {
     __shared__ __attribute__((aligned(16))) float sK[kC * kLD];   // phi(K), rotated
     __shared__ __attribute__((aligned(16))) float sV[kC * kLD];   // V, rotated
+    __shared__ __attribute__((aligned(16))) float sZ[4][kC];      // dz, one partial per wavefront
     const int64_t c = blockIdx.x, h = blockIdx.y;
     const int64_t t0 = c * kC;
     const int nvalid = (int)(p.T - t0 < kC ? p.T - t0 : kC);
@@ -60,6 +61,9 @@ __global__ __launch_bounds__(256) void linattn_summary_kernel(LinSummaryArgs p) 
     const uint64_t bm = __ballot(lane < nvalid && is_begin(p.start, t0 + lane));
     const int last = bm ? 63 - __builtin_clzll(bm) : -1;
     const int lo = last > 0 ? last : 0;
+    // dz: each thread sums its four rows of phi(K) per column, then the four
+    // lanes of a wavefront that hold the same columns (lane ^ 16, lane ^ 32)
+    f32x4 zp = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
         const int f = threadIdx.x + 256 * u;
@@ -71,7 +75,14 @@ __global__ __launch_bounds__(256) void linattn_summary_kernel(LinSummaryArgs p) 
         vv.x = in ? vv.x : 0.0f; vv.y = in ? vv.y : 0.0f; vv.z = in ? vv.z : 0.0f; vv.w = in ? vv.w : 0.0f;
         *(f32x4*)(sK + row * kLD + rot_col(row, c4)) = kv;
         *(f32x4*)(sV + row * kLD + rot_col(row, c4)) = vv;
+        zp.x += kv.x; zp.y += kv.y; zp.z += kv.z; zp.w += kv.w;
     }
+#pragma unroll
+    for (int m = 16; m < 64; m <<= 1) {
+        zp.x += __shfl_xor(zp.x, m, 64); zp.y += __shfl_xor(zp.y, m, 64);
+        zp.z += __shfl_xor(zp.z, m, 64); zp.w += __shfl_xor(zp.w, m, 64);
+    }
+    if (lane < 16) *(f32x4*)(&sZ[w][lane * 4]) = zp;
     __syncthreads();
 
     f32x4 acc[4];
@@ -91,9 +102,8 @@ __global__ __launch_bounds__(256) void linattn_summary_kernel(LinSummaryArgs p) 
         }
     }
     if (threadIdx.x < kC) {
-        float z = 0.0f;
-        for (int j = 0; j < kC; ++j) z += sK[j * kLD + rot_col(j, threadIdx.x)];
-        out[kC * kC + threadIdx.x] = z;
+        const int t = threadIdx.x;
+        out[kC * kC + t] = (sZ[0][t] + sZ[1][t]) + (sZ[2][t] + sZ[3][t]);
     }
     if (h == 0 && threadIdx.x == 0) p.R[c] = last >= 0 ? 1 : 0;
 }
@@ -111,6 +121,11 @@ __global__ __launch_bounds__(256, 4) void linattn_output_kernel(LinOutputArgs p)
     const int64_t t0 = c * kC;
     const int nvalid = (int)(p.T - t0 < kC ? p.T - t0 : kC);
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    // the causal products give the wavefront of row block rb (rb + 1) / 4 of
+    // a full product's work, and wavefront w of a workgroup usually runs on
+    // SIMD w: row blocks rotate with the chunk so that the SIMDs of a CU
+    // share the triangle evenly across its workgroups
+    const int rb = (w + (int)blockIdx.x) & 3;
 
     // row `lane` of the chunk: begin flag, and the last begin at or before it
     // (an inclusive max-scan across the wavefront; every wavefront has all 64)
@@ -179,7 +194,7 @@ __global__ __launch_bounds__(256, 4) void linattn_output_kernel(LinOutputArgs p)
     }
     // A[i][j] = phi(q_i) . phi(k_j); column tiles above the diagonal are
     // masked out entirely and skipped
-    mfma_64x64x64<true, true>(X0, X1, accA, w);
+    mfma_64x64x64<true, true>(X0, X1, accA, rb, rb);
     __syncthreads();                            // every wavefront is done with phi(K)
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -191,7 +206,7 @@ __global__ __launch_bounds__(256, 4) void linattn_output_kernel(LinOutputArgs p)
     // the chunk's first begin (their episode started in an earlier chunk)
     const uint64_t bmask = __ballot(beg);
     const int fbeg = bmask ? __builtin_ctzll(bmask) : kC;
-    if (16 * w < fbeg) mfma_64x64x64<true, true>(X0, X1, accS);
+    if (16 * rb < fbeg) mfma_64x64x64<true, true>(X0, X1, accS, 3, rb);
 
     // mask A to each row's episode (a select: excluded entries are exact
     // zeros), then the row sums and phi(q_i).z_in, reduced across lanes
@@ -199,7 +214,7 @@ __global__ __launch_bounds__(256, 4) void linattn_output_kernel(LinOutputArgs p)
     float den[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-        const int i = 16 * w + 4 * (lane >> 4) + r;
+        const int i = 16 * rb + 4 * (lane >> 4) + r;
         ri[r] = __shfl(rmax, i, 64);
         float rs = 0.0f;
 #pragma unroll
@@ -222,7 +237,7 @@ __global__ __launch_bounds__(256, 4) void linattn_output_kernel(LinOutputArgs p)
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) sA[(16 * w + 4 * (lane >> 4) + r) * kLD + 16 * jt + (lane & 15)] = accA[jt][r];
+        for (int r = 0; r < 4; ++r) sA[(16 * rb + 4 * (lane >> 4) + r) * kLD + 16 * jt + (lane & 15)] = accA[jt][r];
     }
     store_rows<true>(sV, vreg);
     __syncthreads();
@@ -231,7 +246,7 @@ __global__ __launch_bounds__(256, 4) void linattn_output_kernel(LinOutputArgs p)
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) accO[jt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     if (!nonfinite_v) {
-        mfma_64x64x64<true, false>(sA, sV, accO);    // num[i][n] = sum_j A[i][j] V[j][n]
+        mfma_64x64x64_tril(sA, sV, accO, rb);       // num[i][n] = sum_{j <= i} A[i][j] V[j][n]
     } else {
         // A non-finite value in V would reach other episodes of this chunk
         // through the dense product (0 * NaN = NaN); sum each row's own
@@ -240,7 +255,7 @@ __global__ __launch_bounds__(256, 4) void linattn_output_kernel(LinOutputArgs p)
         for (int jt = 0; jt < 4; ++jt) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int i = 16 * w + 4 * (lane >> 4) + r;
+                const int i = 16 * rb + 4 * (lane >> 4) + r;
                 const int n = 16 * jt + (lane & 15);
                 float s = 0.0f;
                 for (int j = (ri[r] > 0 ? ri[r] : 0); j <= i && j < nvalid; ++j)
@@ -256,7 +271,7 @@ __global__ __launch_bounds__(256, 4) void linattn_output_kernel(LinOutputArgs p)
     for (int r = 0; r < 4; ++r) rden[r] = 1.0f / den[r];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-        const int i = 16 * w + 4 * (lane >> 4) + r;
+        const int i = 16 * rb + 4 * (lane >> 4) + r;
         if (i < nvalid) {
             float* orow = p.out + ((t0 + i) * p.H + h) * kC + (lane & 15);
 #pragma unroll

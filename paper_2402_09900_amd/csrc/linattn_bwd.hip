@@ -85,10 +85,14 @@ __global__ __launch_bounds__(256) void linattn_bwd_summary_kernel(LinBwdArgs p) 
     __shared__ __attribute__((aligned(16))) float sQ[kC * kLD];   // phi(Q), later rotated rows < fb
     __shared__ __attribute__((aligned(16))) float sK[kC * kLD];   // phi(K), later dnum rotated rows < fb
     __shared__ float sZ[kC], sDen[kC], sDd[kC];
+    __shared__ __attribute__((aligned(16))) float sDw[4][kC];      // dw, one partial per wavefront
     const int64_t c = blockIdx.x, h = blockIdx.y;
     const int64_t t0 = c * kC;
     const int nvalid = (int)(p.T - t0 < kC ? p.T - t0 : kC);
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    // row block of the causal product A, rotated with the chunk so that the
+    // triangle's uneven work spreads over the SIMDs of a CU
+    const int rb = (w + (int)blockIdx.x) & 3;
 
     {   // reverse-scan workspace prepared: all-ones bytes
         const int64_t nblk = (int64_t)gridDim.x * gridDim.y;
@@ -127,10 +131,11 @@ __global__ __launch_bounds__(256) void linattn_bwd_summary_kernel(LinBwdArgs p) 
 
     f32x4 accA[4];
     zero_acc(accA);
-    mfma_64x64x64<true, true>(sQ, sK, accA);               // A[i][j] = phi(q_i) . phi(k_j)
+    // A[i][j] = phi(q_i) . phi(k_j), only the column tiles that reach j <= i
+    mfma_64x64x64<true, true>(sQ, sK, accA, rb, rb);
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-        const int i = 16 * w + 4 * (lane >> 4) + r;
+        const int i = 16 * rb + 4 * (lane >> 4) + r;
         const int ri = __shfl(rmax, i, 64);
         float rs = 0.0f;
 #pragma unroll
@@ -173,14 +178,30 @@ __global__ __launch_bounds__(256) void linattn_bwd_summary_kernel(LinBwdArgs p) 
             sDd[row] = (ok && in_du) ? dd : 0.0f;
         }
     }
-    {   // phi(Q) rows < fb, rotated, from the registers
+    // phi(Q) rows < fb, rotated, from the registers
+    f32x4 qr[4];
+    {
         const int hi = fb < nvalid ? fb : nvalid;
-        f32x4 qr[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) qr[u] = rows_in(qreg[u], u, 0, hi);
         store_rows<true>(sQ, qr);
     }
     __syncthreads();
+    {   // dw[kd] = sum_i dden_i phi(Q)[i][kd]: each thread's four rows, then
+        // the lanes holding the same columns (lane ^ 16, lane ^ 32)
+        f32x4 zp = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const float d = sDd[(tid >> 4) + 16 * u];
+            zp.x += d * qr[u].x; zp.y += d * qr[u].y; zp.z += d * qr[u].z; zp.w += d * qr[u].w;
+        }
+#pragma unroll
+        for (int m = 16; m < 64; m <<= 1) {
+            zp.x += __shfl_xor(zp.x, m, 64); zp.y += __shfl_xor(zp.y, m, 64);
+            zp.z += __shfl_xor(zp.z, m, 64); zp.w += __shfl_xor(zp.w, m, 64);
+        }
+        if (lane < 16) *(f32x4*)(&sDw[w][lane * 4]) = zp;
+    }
 
     f32x4 accU[4];
     zero_acc(accU);
@@ -192,11 +213,8 @@ __global__ __launch_bounds__(256) void linattn_bwd_summary_kernel(LinBwdArgs p) 
 #pragma unroll
         for (int r = 0; r < 4; ++r)
             du[(16 * w + 4 * (lane >> 4) + r) * kC + 16 * jt + (lane & 15)] = accU[jt][r];
-    if (tid < kC) {
-        float s = 0.0f;
-        for (int i = 0; i < kC; ++i) s += sDd[i] * sQ[i * kLD + rot_col(i, tid)];
-        du[kC * kC + tid] = s;
-    }
+    __syncthreads();                                         // dw partials ready
+    if (tid < kC) du[kC * kC + tid] = (sDw[0][tid] + sDw[1][tid]) + (sDw[2][tid] + sDw[3][tid]);
     if (h == 0 && tid == 0) {
         if (c == 0) p.Rs[0] = 1;
         if (c + 1 < p.nch) p.Rs[c + 1] = mb ? 1 : 0;

@@ -113,15 +113,17 @@ __device__ __forceinline__ int stage(float* s, const float* src, int64_t t0, int
     return bad;
 }
 
-// acc += A * B for 64x64 LDS tiles.  Wave w computes rows 16w .. 16w+15; on
+// acc += A * B for 64x64 LDS tiles.  The wavefront computes rows 16w .. 16w+15
+// of C, w = rb if given (else the wavefront's index in the workgroup); on
 // return acc[jt][r] = C[16w + 4*(lane/16) + r][16*jt + lane%16].
 //   A_ROWS: A[i][k] = sA[i*kLD + k]          else A[i][k] = sA[k*kLD + rot_col(k, i)]
 //   B_ROWS: B[k][j] = sB[j*kLD + k]          else B[k][j] = sB[k*kLD + rot_col(k, j)]
 // jt_last < 3 leaves the output column tiles past it untouched (a wave of a
 // causally masked product skips the tiles above the diagonal).
 template <bool A_ROWS, bool B_ROWS>
-__device__ __forceinline__ void mfma_64x64x64(const float* sA, const float* sB, f32x4 acc[4], int jt_last = 3) {
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+__device__ __forceinline__ void mfma_64x64x64(const float* sA, const float* sB, f32x4 acc[4], int jt_last = 3,
+                                              int rb = -1) {
+    const int lane = threadIdx.x & 63, w = rb >= 0 ? rb : (int)(threadIdx.x >> 6);
     const int i = 16 * w + (lane & 15), kk = (lane >> 4) * 16;
     float af[16];
     if constexpr (A_ROWS) {
@@ -153,6 +155,36 @@ __device__ __forceinline__ void mfma_64x64x64(const float* sA, const float* sB, 
         }
 #pragma unroll
         for (int s = 0; s < 16; ++s) acc[jt] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[s], bf[s], acc[jt], 0, 0, 0);
+    }
+}
+
+// acc += A * B for a lower-triangular A (A[i][k] = 0 for k > i), rows
+// 16rb .. 16rb+15 of C as above; A row-major, B stored with k as its row
+// index (rotated).  Here MFMA number 4q + r takes k = 16q + 4*(lane/16) + r in
+// its four k-slots, so each k-block q holds whole columns of A and the blocks
+// past the row block (all zeros in its rows) are skipped.  The A reads are
+// 16-byte loads; for the B reads the four k-slots sit 4 rows apart, which the
+// 68-float row stride already places in different LDS banks.
+__device__ __forceinline__ void mfma_64x64x64_tril(const float* sA, const float* sB, f32x4 acc[4], int rb) {
+    const int lane = threadIdx.x & 63;
+    const int i = 16 * rb + (lane & 15), g = lane >> 4;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        if (q > rb) break;
+        const f32x4 a4 = *(const f32x4*)(sA + i * kLD + 16 * q + 4 * g);
+        const float af[4] = {a4.x, a4.y, a4.z, a4.w};
+        float bf[4][4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int k = 16 * q + 4 * g + r;
+#pragma unroll
+            for (int jt = 0; jt < 4; ++jt) bf[r][jt] = sB[k * kLD + rot_col(k, 16 * jt + (lane & 15))];
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+#pragma unroll
+            for (int jt = 0; jt < 4; ++jt) acc[jt] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[r], bf[r][jt], acc[jt], 0, 0, 0);
+        }
     }
 }
 
