@@ -340,6 +340,50 @@ __device__ __forceinline__ void grad_mfma(const float* sA, const float* sB, f32x
     }
 }
 
+// grad_mfma over the k-blocks q_lo .. q_hi only (k in [16 q_lo, 16 q_hi + 16)),
+// for products whose A is zero outside them in this row block (a causal
+// factor: dP or A, read along either index).  MFMA number 4q + r takes k = 16q
+// + 4 (lane / 16) + r in its four k-slots, so each k-block is whole in its
+// own four MFMAs; A_ROWS reads stay 16-byte runs (4 (lane / 16) + 3 < 16, and
+// the rotation moves whole 16-column blocks), and the k-rows read by the
+// other mode sit 4 rows apart, which the 68-float stride puts in different
+// LDS banks.
+template <bool A_ROWS, bool B_ROWS>
+__device__ __forceinline__ void grad_mfma_kblocks(const float* sA, const float* sB, f32x4 (&acc)[2], int rb, int ch,
+                                                  int q_lo, int q_hi) {
+    const int lane = threadIdx.x & 63, g = lane >> 4;
+    const int i = 16 * rb + (lane & 15);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        if (q < q_lo || q > q_hi) continue;
+        const int k0 = 16 * q + 4 * g;
+        float af[4], bf[4][2];
+        if constexpr (A_ROWS) {
+            const f32x4 v = *(const f32x4*)(sA + i * kLD + rot_col(i, k0));
+            af[0] = v.x; af[1] = v.y; af[2] = v.z; af[3] = v.w;
+        } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) af[r] = sA[(k0 + r) * kLD + rot_col(k0 + r, i)];
+        }
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) {
+            const int j = 16 * (2 * ch + jj) + (lane & 15);
+            if constexpr (B_ROWS) {
+                const f32x4 v = *(const f32x4*)(sB + j * kLD + rot_col(j, k0));
+                bf[0][jj] = v.x; bf[1][jj] = v.y; bf[2][jj] = v.z; bf[3][jj] = v.w;
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) bf[r][jj] = sB[(k0 + r) * kLD + rot_col(k0 + r, j)];
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int jj = 0; jj < 2; ++jj)
+                acc[jj] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[r], bf[r][jj], acc[jj], 0, 0, 0);
+    }
+}
+
 __device__ __forceinline__ void zero2(f32x4 (&acc)[2]) {
     acc[0] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     acc[1] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
@@ -354,7 +398,8 @@ __device__ __forceinline__ void zero2(f32x4 (&acc)[2]) {
 //   phase 3 (S_in^T, phi(K), A, dnum): dV1 = A^T dnum -> dv, dQ2 = dnum S_in^T -> dq
 // The state products are skipped by wavefronts none of whose rows take them
 // (dK2, dV2: rows at or after the chunk's last begin; dQ2: rows before its
-// first), and dP, A skip their column tiles above the diagonal.
+// first), dP, A skip their column tiles above the diagonal, and dQ1, dK1,
+// dV1 the k-blocks where their causal factor is zero.
 __global__ __launch_bounds__(kGradThreads, 2) void linattn_bwd_grad_kernel(LinBwdArgs p) {
     __shared__ __attribute__((aligned(16))) float X0[kC * kLD];   // U_out [kd][n], then phi(Q), then S_in^T [n][kd]
     __shared__ __attribute__((aligned(16))) float X1[kC * kLD];   // phi(K)
@@ -432,8 +477,10 @@ __global__ __launch_bounds__(kGradThreads, 2) void linattn_bwd_grad_kernel(LinBw
     zero2(accQ1);
     zero2(accK1);
     grad_mfma<true, true>(X0, X1, accA, rb, ch, rb);         // sum_kd Q[i][kd] K[j][kd]
-    grad_mfma<true, false>(X2, X1, accQ1, rb, ch);           // sum_j dP[i][j] K[j][kd]
-    grad_mfma<false, false>(X2, X0, accK1, rb, ch);          // sum_i dP[i][j] Q[i][kd]
+    // dP[i][j] = 0 for j > i: row block rb of dQ1 takes j < 16 rb + 16, and
+    // of dK1 (rows j) takes i >= 16 rb
+    grad_mfma_kblocks<true, false>(X2, X1, accQ1, rb, ch, 0, rb);    // sum_j dP[i][j] K[j][kd]
+    grad_mfma_kblocks<false, false>(X2, X0, accK1, rb, ch, rb, 3);   // sum_i dP[i][j] Q[i][kd]
     // this lane's accumulator elements (row, col): A masked; phi'(q) kept for
     // dq; dk (rows j, columns kd) written, with phi'(k) from phi(K)
     float pq[2][4];
@@ -458,7 +505,7 @@ __global__ __launch_bounds__(kGradThreads, 2) void linattn_bwd_grad_kernel(LinBw
     f32x4 accV1[2], accQ2[2];
     zero2(accV1);
     zero2(accQ2);
-    grad_mfma<false, false>(X2, X3, accV1, rb, ch);          // sum_i A[i][j] dnum[i][n]
+    grad_mfma_kblocks<false, false>(X2, X3, accV1, rb, ch, rb, 3);   // sum_{i >= j} A[i][j] dnum[i][n]
     if (have_s && 16 * rb < firstb) grad_mfma<true, false>(X3, X0, accQ2, rb, ch);   // sum_n dnum[i][n] S_in[kd][n]
 #pragma unroll
     for (int jj = 0; jj < 2; ++jj)
