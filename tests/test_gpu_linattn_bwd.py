@@ -1,7 +1,7 @@
 """Parity of the linear-attention gradient kernels (through the C ABI) with
 the fp64 oracle: conditioned relative error (|y - r| / max(|r|, m), m the
-oracle's magnitude companion) at most 1e-4 for dq, dk and dv (fp32
-arithmetic).  The full workload is compared on every element."""
+oracle's magnitude companion) at most 1e-4 for dq, dk and dv, and for the
+forward output they are taken at (fp32 arithmetic).  The full workload is compared on every element."""
 import numpy as np
 import pytest
 
@@ -34,6 +34,11 @@ def check(la, label, seed=1):
     out = mb.scan_linattn(q, k, v, s)
     gq, gk, gv = mb.scan_linattn_bwd(q, k, v, s, out, dev(g))
     torch.cuda.synchronize()
+    # the forward output these gradients are taken at, on the same flag
+    # patterns, lengths and head counts
+    ro, mo = oracle.linattn(la.q.astype(np.float64), la.k.astype(np.float64), la.v.astype(np.float64), la.start)
+    e = cond_err(out.cpu().numpy(), ro, mo)
+    assert e <= TOL, (label, "out", e)
     rq, rk, rv, mq, mk, mv = oracle.linattn_bwd(la.q.astype(np.float64), la.k.astype(np.float64),
                                                 la.v.astype(np.float64), la.start, g.astype(np.float64))
     for name, got, ref, m in (("dq", gq, rq, mq), ("dk", gk, rk, mk), ("dv", gv, rv, mv)):
