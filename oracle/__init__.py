@@ -13,8 +13,10 @@ described in ``oracle.h``.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
+import shutil
 import subprocess
 
 import numpy as np
@@ -25,16 +27,51 @@ _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 
+def _compile(src: str, out: str) -> None:
+    """gcc, plain -O2, no fast-math and no FP contraction, so every
+    expression is evaluated as written."""
+    cmd = ["gcc", "-std=c99", "-O2", "-ffp-contract=off", "-fno-fast-math",
+           "-fPIC", "-shared", "-Wall", "-o", out, src, "-lm"]
+    subprocess.run(cmd, check=True)
+
+
 def build(force: bool = True) -> str:
-    """Compile oracle.c into liboracle.so with gcc (plain -O2, no fast-math,
-    no FP contraction, so every expression is evaluated as written)."""
+    """Compile oracle.c into liboracle.so."""
     if force or not os.path.exists(_LIB_PATH):
         tmp = _LIB_PATH + ".tmp%d" % os.getpid()
-        cmd = ["gcc", "-std=c99", "-O2", "-ffp-contract=off", "-fno-fast-math",
-               "-fPIC", "-shared", "-Wall", "-o", tmp, _SRC, "-lm"]
-        subprocess.run(cmd, check=True)
+        _compile(_SRC, tmp)
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
+
+
+def _bind(lib):
+    """Declare the argument and result types of every oracle function."""
+    P, I64 = ctypes.c_void_p, ctypes.c_int64
+    lib.oracle_episode_idx.argtypes = [P, I64, I64, P]
+    for name in ("oracle_diag_fwd", "oracle_diag_fwd_c"):
+        getattr(lib, name).argtypes = [P, I64, P, P, I64, I64, I64, P, P]
+    for name in ("oracle_diag_bwd", "oracle_diag_bwd_c"):
+        getattr(lib, name).argtypes = [P, I64, P, P, P, I64, I64, I64, P, P, P, P]
+    lib.oracle_phi.argtypes = [ctypes.c_double]
+    lib.oracle_phi.restype = ctypes.c_double
+    lib.oracle_linattn.argtypes = [P, P, P, P, I64, I64, I64, I64, P, P]
+    D = ctypes.c_double
+    lib.oracle_discounted_return.argtypes = [P, P, D, I64, I64, P, P]
+    lib.oracle_gae.argtypes = [P, P, P, P, P, D, D, I64, I64, P, P, P, P]
+    lib.oracle_ffm.argtypes = [P, P, P, P, I64, I64, I64, I64, P, P]
+    lib.oracle_linattn_bwd.argtypes = [P, P, P, P, P, I64, I64, I64, I64, P, P, P, P, P, P]
+    lib.oracle_ffm_bwd.argtypes = [P, P, P, P, P, I64, I64, I64, I64, P, P, P, P, P, P]
+    lib.oracle_ffm_bwd.restype = None
+    lib.oracle_linattn_bwd.restype = None
+    lib.oracle_tbb_begin_indices.argtypes = [P, I64, I64, P]
+    lib.oracle_tbb_begin_indices.restype = I64
+    lib.oracle_tbb_sample.argtypes = [P, I64, I64, P, I64, P, I64, I64, P, P, P]
+    lib.oracle_tbb_sample.restype = I64
+    for name in ("oracle_episode_idx", "oracle_diag_fwd", "oracle_diag_fwd_c",
+                 "oracle_diag_bwd", "oracle_diag_bwd_c", "oracle_linattn",
+                 "oracle_discounted_return", "oracle_gae", "oracle_ffm"):
+        getattr(lib, name).restype = None
+    return lib
 
 
 def _load():
@@ -42,34 +79,35 @@ def _load():
     if _lib is None:
         if not os.path.exists(_LIB_PATH):
             build(force=True)
-        lib = ctypes.CDLL(_LIB_PATH)
-        P, I64 = ctypes.c_void_p, ctypes.c_int64
-        lib.oracle_episode_idx.argtypes = [P, I64, I64, P]
-        for name in ("oracle_diag_fwd", "oracle_diag_fwd_c"):
-            getattr(lib, name).argtypes = [P, I64, P, P, I64, I64, I64, P, P]
-        for name in ("oracle_diag_bwd", "oracle_diag_bwd_c"):
-            getattr(lib, name).argtypes = [P, I64, P, P, P, I64, I64, I64, P, P, P, P]
-        lib.oracle_phi.argtypes = [ctypes.c_double]
-        lib.oracle_phi.restype = ctypes.c_double
-        lib.oracle_linattn.argtypes = [P, P, P, P, I64, I64, I64, I64, P, P]
-        D = ctypes.c_double
-        lib.oracle_discounted_return.argtypes = [P, P, D, I64, I64, P, P]
-        lib.oracle_gae.argtypes = [P, P, P, P, P, D, D, I64, I64, P, P, P, P]
-        lib.oracle_ffm.argtypes = [P, P, P, P, I64, I64, I64, I64, P, P]
-        lib.oracle_linattn_bwd.argtypes = [P, P, P, P, P, I64, I64, I64, I64, P, P, P, P, P, P]
-        lib.oracle_ffm_bwd.argtypes = [P, P, P, P, P, I64, I64, I64, I64, P, P, P, P, P, P]
-        lib.oracle_ffm_bwd.restype = None
-        lib.oracle_linattn_bwd.restype = None
-        lib.oracle_tbb_begin_indices.argtypes = [P, I64, I64, P]
-        lib.oracle_tbb_begin_indices.restype = I64
-        lib.oracle_tbb_sample.argtypes = [P, I64, I64, P, I64, P, I64, I64, P, P, P]
-        lib.oracle_tbb_sample.restype = I64
-        for name in ("oracle_episode_idx", "oracle_diag_fwd", "oracle_diag_fwd_c",
-                     "oracle_diag_bwd", "oracle_diag_bwd_c", "oracle_linattn",
-                     "oracle_discounted_return", "oracle_gae", "oracle_ffm"):
-            getattr(lib, name).restype = None
-        _lib = lib
+        _lib = _bind(ctypes.CDLL(_LIB_PATH))
     return _lib
+
+
+def source() -> str:
+    """Text of oracle.c (for tests that compile altered copies of it)."""
+    with open(_SRC) as f:
+        return f.read()
+
+
+@contextlib.contextmanager
+def variant(src_text: str, workdir: str):
+    """Compile `src_text` (an altered copy of oracle.c, e.g. with a mistake
+    planted on purpose) into `workdir` and route every wrapper of this
+    module through it for the duration of the block.  Used by the tests
+    that check the pins fail on a wrong oracle."""
+    global _lib
+    src = os.path.join(workdir, "oracle_variant.c")
+    with open(src, "w") as f:
+        f.write(src_text)
+    shutil.copy(os.path.join(_HERE, "oracle.h"), os.path.join(workdir, "oracle.h"))
+    out = os.path.join(workdir, "liboracle_variant.so")
+    _compile(src, out)
+    saved = _lib
+    _lib = _bind(ctypes.CDLL(out))
+    try:
+        yield
+    finally:
+        _lib = saved
 
 
 def _ptr(arr):
