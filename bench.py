@@ -12,10 +12,11 @@ workload the discounted return and the advantage estimate.  Prints ONE JSON line
 Workloads (seeded, synthetic; laws in paper_2402_09900_amd.tapes):
   1  diag real f32, T=1024, d=32, 8 episodes, forward
   2  diag complex64 (LRU-style, time-invariant a), T=65536, d=256, Geometric(200)
-     episodes, forward + reverse                                   [default]
+     episodes, forward + reverse
   3  linear-transformer memoroid, T=32768, 4 heads x 64, Geometric(500), chunk 64
   4  diag real, 64 tapes x T=16384, d=512, bf16 in / fp32 state / bf16 out
   5  diag real f32, T=1048576, d=256, lognormal(5, 1.5) episodes, forward + reverse
+     (the largest single-GPU configuration)                        [default]
   6  discounted return + generalized advantage estimate, one tape of 2^24 steps,
      U{1..1000} episodes, gamma 0.99, lambda 0.95
   7  FFM aggregator, T=262144, m=32 x c=8 complex state, Geometric(200) episodes,
@@ -29,15 +30,28 @@ step i uses copy i mod n, so inputs are read from HBM rather than from the
 256 MB last-level cache left warm by the previous step.
 
 value = tape timesteps x features per second of the whole step (B*T*d, or
-T*H*dv for linear attention), from the wall time of the K timed steps.
+T*H*dv for linear attention), from the wall time of the K timed steps.  The
+timed calls are the *_prepared entry points on workspaces prepared once
+before timing (one kernel per call); config.self_init_ms_per_step is the
+same step through the self-initialising entry points (which add a fill of
+each call's workspace header, counters and first descriptor bank).
 roofline: the dominant call's algorithmic bytes (or flops) per launch over
 its average launch time, measured in the timed steps with HIP events on the
 launch stream.  The dominant call is the slowest one in the warmup steps,
 which carry events on every call; in the timed steps only it does (an event
 pair costs the GPU a few microseconds of idle time between calls), and the
 other calls' times in config.ms_per_call come from as many steps again after
-the timed ones.  cpu_baseline: the fp64 oracle timed on this host on a
-bounded sample of the same workload.
+the timed ones.  roofline.step_frac puts the whole step's algorithmic bytes
+(or flops) over the step time.
+
+cpu_baseline: the fp64 oracle, unchanged, timed on this host on the very
+input arrays the GPU steps read (the whole workload; the flags' SHA-256 is in
+config), median of 3 runs, on one thread and on N threads.  The N-thread
+figure runs the same oracle functions on N independent slices of the
+problem at once (feature blocks or tapes of a diagonal scan, heads of linear
+attention, trace rows of FFM), through ctypes, which releases the GIL for
+each call; N is this process's CPU share, at most 16.  Input decoding to
+fp64 and slicing happen before timing.
 """
 from __future__ import annotations
 
@@ -64,7 +78,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6, 7, 8, 9])
+    p.add_argument("--workload", type=int, default=5, choices=[1, 2, 3, 4, 5, 6, 7, 8, 9])
     p.add_argument("--no-cpu-baseline", action="store_true")
     return p.parse_args()
 
@@ -131,6 +145,12 @@ def n_sets(set_bytes):
 
 
 PREPARED = []
+SUFFIX = ["_prepared"]      # "" switches every call to the self-initialising entry points
+
+
+def entry(mb, name):
+    """The entry point `name` of the current mode (prepared or self-initialising)."""
+    return getattr(mb, name + SUFFIX[0])
 
 
 def prepared_ws(torch, mb, nbytes):
@@ -170,7 +190,7 @@ def setup_diag(torch, mb, tapes, key):
         calls = {}
 
         def fwd(a=a, x=x, s=s, h=h, idx=idx, ws=ws):
-            st = mb.memoroid_scan_diag(a.data_ptr(), stride, x.data_ptr(), s.data_ptr(), h.data_ptr(),
+            st = entry(mb, "memoroid_scan_diag")(a.data_ptr(), stride, x.data_ptr(), s.data_ptr(), h.data_ptr(),
                                        idx.data_ptr(), B, T, d, code[kind], code[w.out_dtype], ws.data_ptr(),
                                        ws.numel(), stream())
             assert st == 0, mb.status_string(st)
@@ -183,7 +203,7 @@ def setup_diag(torch, mb, tapes, key):
             wsb = prepared_ws(torch, mb, nbb)
 
             def bwd(a=a, s=s, hb=hb, g=g, gx=gx, ga=ga, wsb=wsb):
-                st = mb.memoroid_scan_diag_bwd(a.data_ptr(), stride, s.data_ptr(), hb.data_ptr(), g.data_ptr(),
+                st = entry(mb, "memoroid_scan_diag_bwd")(a.data_ptr(), stride, s.data_ptr(), hb.data_ptr(), g.data_ptr(),
                                                gx.data_ptr(), ga.data_ptr(), B, T, d, code[kind], wsb.data_ptr(),
                                                wsb.numel(), stream())
                 assert st == 0, mb.status_string(st)
@@ -203,6 +223,7 @@ def setup_linattn(torch, mb, tapes, key=3):
     nb = mb.memoroid_scan_linattn_workspace_bytes(la.T, la.H, 64, 64, 64)
     nbb = mb.memoroid_scan_linattn_bwd_workspace_bytes(la.T, la.H, 64, 64, 64) if wl.backward else 0
     g_host = np.random.Generator(np.random.PCG64(key + 100)).standard_normal(la.v.shape, dtype=np.float32)
+    la.g_host = g_host
     stream = lambda: torch.cuda.current_stream().cuda_stream  # noqa: E731
     sets = []
     for _ in range(n_sets((4 + (5 if wl.backward else 0)) * n * 4 + la.T * 5 + nb + nbb)):
@@ -258,12 +279,12 @@ def setup_discount(torch, mb, tapes, key):
         wsg = prepared_ws(torch, mb, nb)
 
         def ret(r=r, s=s, G=G, ws=ws):
-            st = mb.memoroid_discounted_return(r.data_ptr(), s.data_ptr(), tp.gamma, G.data_ptr(), B, T,
+            st = entry(mb, "memoroid_discounted_return")(r.data_ptr(), s.data_ptr(), tp.gamma, G.data_ptr(), B, T,
                                                ws.data_ptr(), ws.numel(), stream())
             assert st == 0, mb.status_string(st)
 
         def gae(r=r, v=v, vn=vn, done=done, s=s, adv=adv, tg=tg, wsg=wsg):
-            st = mb.memoroid_gae(r.data_ptr(), v.data_ptr(), vn.data_ptr(), done.data_ptr(), s.data_ptr(),
+            st = entry(mb, "memoroid_gae")(r.data_ptr(), v.data_ptr(), vn.data_ptr(), done.data_ptr(), s.data_ptr(),
                                  tp.gamma, tp.lam, adv.data_ptr(), tg.data_ptr(), B, T, wsg.data_ptr(), wsg.numel(),
                                  stream())
             assert st == 0, mb.status_string(st)
@@ -285,6 +306,7 @@ def setup_ffm(torch, mb, tapes, key):
         rng = np.random.Generator(np.random.PCG64(key + 100))
         g_host = (rng.standard_normal((B, T, m, c), dtype=np.float32)
                   + 1j * rng.standard_normal((B, T, m, c), dtype=np.float32)).astype(np.complex64)
+    f.g_host = g_host
     stream = lambda: torch.cuda.current_stream().cuda_stream  # noqa: E731
     sets = []
     for _ in range(n_sets(n * (16 if wl.backward else 8) + B * T * (m * 8 + 5) + nb + nbb)):
@@ -295,7 +317,7 @@ def setup_ffm(torch, mb, tapes, key):
         ws = prepared_ws(torch, mb, nb)
 
         def fwd(al=al, om=om, x=x, s=s, S=S, idx=idx, ws=ws):
-            st = mb.memoroid_scan_ffm(al.data_ptr(), om.data_ptr(), x.data_ptr(), s.data_ptr(), S.data_ptr(),
+            st = entry(mb, "memoroid_scan_ffm")(al.data_ptr(), om.data_ptr(), x.data_ptr(), s.data_ptr(), S.data_ptr(),
                                       idx.data_ptr(), B, T, m, c, ws.data_ptr(), ws.numel(), stream())
             assert st == 0, mb.status_string(st)
         calls = {"fwd": fwd}
@@ -307,7 +329,7 @@ def setup_ffm(torch, mb, tapes, key):
             wsb = prepared_ws(torch, mb, nbb)
 
             def bwd(al=al, om=om, s=s, S=S, G=G, gx=gx, ga=ga, gw=gw, wsb=wsb):
-                st = mb.memoroid_scan_ffm_bwd(al.data_ptr(), om.data_ptr(), s.data_ptr(), S.data_ptr(), G.data_ptr(),
+                st = entry(mb, "memoroid_scan_ffm_bwd")(al.data_ptr(), om.data_ptr(), s.data_ptr(), S.data_ptr(), G.data_ptr(),
                                               gx.data_ptr(), ga.data_ptr(), gw.data_ptr(), B, T, m, c,
                                               wsb.data_ptr(), wsb.numel(), stream())
                 assert st == 0, mb.status_string(st)
@@ -343,12 +365,12 @@ def setup_tbb(torch, mb, tapes, key):
         wss = prepared_ws(torch, mb, nbs)
 
         def insert(s=s, idx=idx, cnt=cnt, wsi=wsi):
-            st = mb.memoroid_tbb_begin_indices(s.data_ptr(), n, 0, idx.data_ptr(), cnt.data_ptr(), wsi.data_ptr(),
+            st = entry(mb, "memoroid_tbb_begin_indices")(s.data_ptr(), n, 0, idx.data_ptr(), cnt.data_ptr(), wsi.data_ptr(),
                                                wsi.numel(), stream())
             assert st == 0, mb.status_string(st)
 
         def sample(D=D, I=I, draws=draws, out=out, ost=ost, osrc=osrc, filled=filled, wss=wss):
-            st = mb.memoroid_tbb_sample(D.data_ptr(), n, row_bytes, I.data_ptr(), I.numel(), draws.data_ptr(), K,
+            st = entry(mb, "memoroid_tbb_sample")(D.data_ptr(), n, row_bytes, I.data_ptr(), I.numel(), draws.data_ptr(), K,
                                         tb.batch, out.data_ptr(), ost.data_ptr(), osrc.data_ptr(), filled.data_ptr(),
                                         wss.data_ptr(), wss.numel(), stream())
             assert st == 0, mb.status_string(st)
@@ -385,77 +407,159 @@ def recorded_traffic(key, call):
     return rec.get("workloads", {}).get(str(key), {}).get(call)
 
 
-def cpu_baseline(key, tapes, budget_s=20.0):
-    """The oracle as it stands, single thread, on a bounded sample."""
+def _cpu_share():
+    """CPU model of this host and the threads this process may use (at most
+    16: the CPU share of one GPU on the boxes this runs on)."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = os.cpu_count() or 1
+    return model, max(1, min(avail, 16))
+
+
+def _median_seconds(fn, reps=3):
+    ts = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        fn()
+        ts.append(time.perf_counter() - t0)
+    return float(np.median(ts))
+
+
+def _run_parallel(jobs, threads):
+    """Run the oracle calls in `jobs` on `threads` threads (each a ctypes
+    call into the oracle, which runs without the GIL)."""
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        list(ex.map(lambda job: job(), jobs))
+
+
+def _bounds(n, parts):
+    parts = max(1, min(parts, n))
+    edges = [n * i // parts for i in range(parts + 1)]
+    return [(edges[i], edges[i + 1]) for i in range(parts) if edges[i + 1] > edges[i]]
+
+
+def cpu_baseline(key, tapes, w):
+    """The oracle as it stands, on the workload's own inputs (the arrays the
+    GPU steps were built from), on 1 thread and on N threads over independent
+    slices; the figure reported as value is the N-thread one."""
     import oracle
-    w = tapes.WORKLOADS[key]
-    if w.kind == "tbb":
-        tb = tapes.make_tbb(key)
-        t0 = time.perf_counter()
-        I = oracle.tbb_begin_indices(tb.start)
-        oracle.tbb_sample(tb.D, I, tb.draws, tb.batch)
-        dt = time.perf_counter() - t0
-        return {"value": tb.batch / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
-                "sample": "the whole workload (begin indices of %d flags, batch of %d rows), %.1f s"
-                          % (tb.start.size, tb.batch, dt)}
-    if w.kind == "ffm":
-        T = min(w.T, 1 << 16)
-        f = tapes.make_ffm(key, T=T)
-        al, om = f.alpha.astype(np.float64), f.omega.astype(np.float64)
-        t0 = time.perf_counter()
-        S, _ = oracle.ffm(al, om, f.x.astype(np.float64), f.start)
-        if w.backward:
-            oracle.ffm_bwd(al, om, f.start, S, np.ones_like(S))
-        dt = time.perf_counter() - t0
-        what = "forward + gradient" if w.backward else "forward"
-        return {"value": f.B * T * f.m * f.c / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
-                "sample": "first %d steps of the tape, all %d x %d features, %s, fp64, %.1f s"
-                          % (T, f.m, f.c, what, dt)}
-    if w.kind == "discount":
-        T = min(w.T, 1 << 22)
-        tp = tapes.make_discount(key, T=T)
-        r, v, vn = (a.astype(np.float64) for a in (tp.r, tp.v, tp.vn))
-        g32, l32 = float(np.float32(tp.gamma)), float(np.float32(tp.lam))
-        t0 = time.perf_counter()
-        oracle.discounted_return(r, tp.start, g32)
-        oracle.gae(r, v, tp.start, g32, l32, vn=vn, done=tp.done)
-        dt = time.perf_counter() - t0
-        return {"value": tp.B * T / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
-                "sample": "first %d steps of the tape, return + advantage, fp64, %.1f s" % (T, dt)}
-    if w.kind == "linattn":
-        T = min(w.T, 4096)
-        la = tapes.make_linattn(key, T=T)
-        q, k, v = la.q.astype(np.float64), la.k.astype(np.float64), la.v.astype(np.float64)
-        t0 = time.perf_counter()
-        oracle.linattn(q, k, v, la.start)
-        if w.backward:
-            oracle.linattn_bwd(q, k, v, la.start, np.ones_like(v))
-        dt = time.perf_counter() - t0
-        what = "forward readout and its gradient" if w.backward else "forward readout"
-        return {"value": T * la.H * la.dv / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
-                "sample": "first %d steps of the tape, all %d heads, %s" % (T, la.H, what)}
-    # diagonal: whole tapes of the workload's law, capped so the oracle runs
-    # for about budget_s seconds at most
-    T = w.T
-    B = w.B
-    d = w.d
-    cap = 64 << 20 if w.dtype != "c64" else 24 << 20
-    if B * T * d > cap:
-        if B > 1:
-            B = max(1, cap // (T * d))
+    wl = tapes.WORKLOADS[key]
+    model, threads = _cpu_share()
+    one, jobs, units, what, lanes = None, [], 0, "", ""
+    if wl.kind == "tbb":
+        units = w.batch
+        one = lambda: oracle.tbb_sample(w.D, oracle.tbb_begin_indices(w.start), w.draws, w.batch)  # noqa: E731
+        what = "begin indices of %d flags and a batch of %d rows" % (w.start.size, w.batch)
+        lanes = None
+    elif wl.kind == "ffm":
+        al, om, x = w.alpha.astype(np.float64), w.omega.astype(np.float64), w.x.astype(np.float64)
+        G = w.g_host.astype(np.complex128) if wl.backward else None
+        units = w.B * w.T * w.m * w.c
+
+        def one():
+            S, _ = oracle.ffm(al, om, x, w.start)
+            if G is not None:
+                oracle.ffm_bwd(al, om, w.start, S, G)
+        for j0, j1 in _bounds(w.m, threads):
+            xs = np.ascontiguousarray(x[:, :, j0:j1])
+            Gs = np.ascontiguousarray(G[:, :, j0:j1]) if G is not None else None
+
+            def job(j0=j0, j1=j1, xs=xs, Gs=Gs):
+                S, _ = oracle.ffm(al[j0:j1], om, xs, w.start)
+                if Gs is not None:
+                    oracle.ffm_bwd(al[j0:j1], om, w.start, S, Gs)
+            jobs.append(job)
+        what = ("forward + gradient" if wl.backward else "forward") + ", fp64"
+        lanes = "trace rows j of the m x c state"
+    elif wl.kind == "discount":
+        r, v, vn = (a.astype(np.float64) for a in (w.r, w.v, w.vn))
+        g32, l32 = float(np.float32(w.gamma)), float(np.float32(w.lam))
+        units = w.B * w.T
+
+        def one():
+            oracle.discounted_return(r, w.start, g32)
+            oracle.gae(r, v, w.start, g32, l32, vn=vn, done=w.done)
+        for b0, b1 in _bounds(w.B, threads):
+            def job(b0=b0, b1=b1):
+                oracle.discounted_return(r[b0:b1], w.start[b0:b1], g32)
+                oracle.gae(r[b0:b1], v[b0:b1], w.start[b0:b1], g32, l32, vn=vn[b0:b1], done=w.done[b0:b1])
+            jobs.append(job)
+        what = "return + advantage, fp64"
+        lanes = "tapes"
+    elif wl.kind == "linattn":
+        q, k, v = w.q.astype(np.float64), w.k.astype(np.float64), w.v.astype(np.float64)
+        g = w.g_host.astype(np.float64) if wl.backward else None
+        units = w.T * w.H * w.dv
+
+        def one():
+            oracle.linattn(q, k, v, w.start)
+            if g is not None:
+                oracle.linattn_bwd(q, k, v, w.start, g)
+        for h0, h1 in _bounds(w.H, threads):
+            sl = [np.ascontiguousarray(t[:, h0:h1]) for t in (q, k, v)]
+            gs = np.ascontiguousarray(g[:, h0:h1]) if g is not None else None
+
+            def job(sl=sl, gs=gs):
+                oracle.linattn(*sl, w.start)
+                if gs is not None:
+                    oracle.linattn_bwd(*sl, w.start, gs)
+            jobs.append(job)
+        what = ("forward readout and its gradient" if wl.backward else "forward readout") + ", fp64"
+        lanes = "heads"
+    else:
+        a, x = w.decoded("a"), w.decoded("x")
+        g = w.decoded("g") if wl.backward else None
+        units = w.B * w.T * w.d
+
+        def one():
+            h, _ = oracle.diag_fwd(a, x, w.start)
+            if g is not None:
+                oracle.diag_bwd(a, w.start, h, g)
+        if w.B >= threads:
+            for b0, b1 in _bounds(w.B, threads):
+                sl = (a if w.a_invariant else a[b0:b1], x[b0:b1], w.start[b0:b1], None if g is None else g[b0:b1])
+                jobs.append(sl)
+            lanes = "tapes"
         else:
-            T = max(1, cap // d)
-    t = tapes.make_diag(key, B=B, T=T)
-    a, x = t.decoded("a"), t.decoded("x")
-    t0 = time.perf_counter()
-    h, _ = oracle.diag_fwd(a, x, t.start)
-    if w.backward:
-        oracle.diag_bwd(a, t.start, h, t.decoded("g"))
-    dt = time.perf_counter() - t0
-    what = "forward + reverse" if w.backward else "forward"
-    return {"value": B * T * d / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
-            "sample": "%d tape(s) x %d steps x %d features of the same law, %s, fp64, %.1f s"
-                      % (B, T, d, what, dt)}
+            for j0, j1 in _bounds(w.d, threads):
+                sl = (np.ascontiguousarray(a[j0:j1] if w.a_invariant else a[:, :, j0:j1]),
+                      np.ascontiguousarray(x[:, :, j0:j1]), w.start,
+                      None if g is None else np.ascontiguousarray(g[:, :, j0:j1]))
+                jobs.append(sl)
+            lanes = "feature blocks"
+
+        def make(sl):
+            def job():
+                h, _ = oracle.diag_fwd(sl[0], sl[1], sl[2])
+                if sl[3] is not None:
+                    oracle.diag_bwd(sl[0], sl[2], h, sl[3])
+            return job
+        jobs = [make(sl) for sl in jobs]
+        what = ("forward + reverse" if wl.backward else "forward") + ", fp64"
+    t1 = _median_seconds(one)
+    res = {"unit": UNIT, "kind": "oracle", "cpu_model": model, "cpu_share": threads,
+           "one_thread": {"value": units / t1, "cores": 1, "seconds": round(t1, 4)}}
+    split = "no independent slices to split over"
+    if len(jobs) > 1:
+        tn = _median_seconds(lambda: _run_parallel(jobs, threads))
+        res["n_threads"] = {"value": units / tn, "cores": len(jobs), "seconds": round(tn, 4)}
+        split = "the %d-thread run splits it over independent %s" % (len(jobs), lanes)
+    best = max((res["one_thread"], res.get("n_threads")), key=lambda v: v["value"] if v else -1.0)
+    res["value"], res["cores"] = best["value"], best["cores"]
+    res["sample"] = ("the whole workload on the GPU steps' own input arrays (%s), median of 3 runs on 1 thread and "
+                     "on up to %d; %s; value is the faster" % (what, threads, split))
+    return res
 
 
 def main():
@@ -526,6 +630,21 @@ def main():
             print("bench.py: workspace status %s" % mb.status_string(st), file=sys.stderr)
             sys.exit(1)
 
+    # the same step through the self-initialising entry points (a fill of
+    # each call's workspace header, counters and first bank, then the
+    # kernels); the prepared workspaces are rebound by this, so their status
+    # was checked above
+    SUFFIX[0] = ""
+    for i in range(max(args.warmup, 1)):
+        step(i, warm, ())
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, timers, ())
+    torch.cuda.synchronize()
+    self_init_ms = (time.perf_counter() - t0) * 1e3 / max(args.steps, 1)
+    SUFFIX[0] = "_prepared"
+
     per_call_ms = {name: timers[name].mean_ms() for name in calls}
     if flops is not None:
         achieved = flops[dom] / (per_call_ms[dom] * 1e-3) / 1e12
@@ -554,6 +673,10 @@ def main():
     roof["algorithmic_bytes_per_launch"] = int(bytes_per[dom])
     if flops is not None:
         roof["algorithmic_flops_per_launch"] = int(flops[dom])
+        roof["step_frac"] = round(sum(flops.get(k, 0) for k in calls) / (ms_per_step * 1e-3) / 1e12
+                                  / FP32_MFMA_PEAK_TFLOPS, 4)
+    else:
+        roof["step_frac"] = round(sum(bytes_per[k] for k in calls) / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
 
     result = {
         "metric": METRIC,
@@ -573,6 +696,9 @@ def main():
                    **({"m": wl.dk, "c": wl.dv} if wl.kind == "ffm" else {}),
                    **({"gamma": wl.gamma, "lambda": wl.lam} if wl.kind == "discount" else {}),
                    "passes": list(calls.keys()),
+                   "flags_sha256": tapes.flags_sha256(w.start),
+                   "entry_points": "*_prepared (workspaces prepared once before timing)",
+                   "self_init_ms_per_step": round(self_init_ms, 4),
                    "buffer_sets": len(sets),
                    "ms_per_call": {k: round(v, 4) for k, v in per_call_ms.items()},
                    "GBps_per_call": {k: round(bytes_per[k] / (per_call_ms[k] * 1e-3) / 1e9, 1)
@@ -580,7 +706,7 @@ def main():
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(key, tapes)
+        result["cpu_baseline"] = cpu_baseline(key, tapes, w)
     print(json.dumps(result), flush=True)
 
 

@@ -38,30 +38,34 @@
  *    2 complex64) take the vectorised kernels; other shapes take a scalar
  *    kernel with identical results.
  *  - The workspace is caller-allocated device memory of at least the size the
- *    matching *_workspace_bytes query returns for the same arguments, 16-byte
- *    aligned (256 for linear attention).  Concurrent calls must use distinct
- *    workspaces.  Two kinds of call:
- *      * PREPARED (memoroid_scan_diag, _diag_bwd, _ffm, _ffm_bwd,
- *        memoroid_discounted_return, memoroid_gae,
- *        memoroid_tbb_begin_indices, memoroid_tbb_sample): the call
- *        initialises nothing in the workspace (sampling runs two kernels,
- *        the others one).  The workspace must have been prepared with
+ *    matching *_workspace_bytes query (or memoroid_workspace_bytes) returns
+ *    for the same arguments, 16-byte aligned (256 for linear attention).
+ *    Concurrent calls must use distinct workspaces.  Two kinds of call:
+ *      * SELF-INITIALISING -- every entry point without the _prepared
+ *        suffix.  The workspace contents are undefined on entry and on exit;
+ *        the call initialises what it needs on `stream` (one fill kernel of
+ *        the workspace's header, counters and first descriptor bank, then
+ *        the computation).  Any workspace of sufficient size works, whatever
+ *        it held before.
+ *      * PREPARED -- the *_prepared variants of the diagonal scans, FFM and
+ *        its gradient, return, GAE and the TBB operations, for callers that
+ *        repeat a call with the same sizes and want no fill kernel: the call
+ *        initialises nothing (sampling runs two kernels, the others one).
+ *        The workspace must have been prepared with
  *        memoroid_workspace_prepare() (on a stream ordered before the call)
  *        and then used only by calls of this library.  The first call binds
- *        it to that entry point and those sizes; every later call with the same entry
- *        point, sizes and flags finds it ready again, with no preparation in
- *        between.  The binding also covers: the dtypes; whether the
- *        vectorised kernels run (pointer alignment, d); a time-invariant a;
- *        whether grad_a / the FFM parameter gradients are asked for.  A call
- *        that differs in any of these returns MEMOROID_OK but computes
- *        nothing: memoroid_workspace_status() then reports
- *        MEMOROID_EMISMATCH, and the workspace must be prepared again before
- *        any further use.  Prepare it again as well after
- *        MEMOROID_ETIMEOUT, and after any other writes to its memory.
- *      * SELF-INITIALISING (memoroid_scan_linattn, _linattn_bwd): contents
- *        undefined on entry and on exit; the call initialises what it needs
- *        on `stream`.
- */
+ *        it to that entry point and those sizes; every later call with the
+ *        same entry point, sizes and flags finds it ready again, with no
+ *        preparation in between.  The binding also covers: the dtypes;
+ *        whether the vectorised kernels run (pointer alignment, d); a
+ *        time-invariant a; whether grad_a / the FFM parameter gradients are
+ *        asked for.  A call that differs in any of these returns MEMOROID_OK
+ *        but computes nothing and leaves its outputs as they were:
+ *        memoroid_workspace_status() then reports MEMOROID_EMISMATCH, and the
+ *        workspace must be prepared again before any further use.  Prepare
+ *        it again as well after MEMOROID_ETIMEOUT, and after any other writes
+ *        to its memory (a self-initialising call included).
+  */
 #ifndef MEMOROID_H
 #define MEMOROID_H
 
@@ -72,7 +76,7 @@
 extern "C" {
 #endif
 
-#define MEMOROID_ABI_VERSION 3
+#define MEMOROID_ABI_VERSION 4
 
 typedef enum {
     MEMOROID_OK = 0,
@@ -91,11 +95,38 @@ typedef enum {
     MEMOROID_C64 = 2    /* complex float, interleaved (re, im) */
 } memoroid_dtype;
 
+/* Entry points, for the generic workspace query. */
+typedef enum {
+    MEMOROID_OP_DIAG = 0,              /* memoroid_scan_diag[_prepared]:      (B, T, d_or_H = d) */
+    MEMOROID_OP_DIAG_BWD = 1,          /* memoroid_scan_diag_bwd[_prepared]:  (B, T, d_or_H = d) */
+    MEMOROID_OP_LINATTN = 2,           /* memoroid_scan_linattn:      (T, d_or_H = H, dk, dv, chunk) */
+    MEMOROID_OP_LINATTN_BWD = 3,       /* memoroid_scan_linattn_bwd:  (T, d_or_H = H, dk, dv, chunk) */
+    MEMOROID_OP_FFM = 4,               /* memoroid_scan_ffm[_prepared]:       (B, T, d_or_H = m, dk = c) */
+    MEMOROID_OP_FFM_BWD = 5,           /* memoroid_scan_ffm_bwd[_prepared]:   (B, T, d_or_H = m, dk = c) */
+    MEMOROID_OP_RETURN = 6,            /* memoroid_discounted_return[_prepared]: (B, T) */
+    MEMOROID_OP_GAE = 7,               /* memoroid_gae[_prepared]:            (B, T) */
+    MEMOROID_OP_TBB_BEGIN_INDICES = 8, /* memoroid_tbb_begin_indices[_prepared]: (T = n) */
+    MEMOROID_OP_TBB_SAMPLE = 9         /* memoroid_tbb_sample[_prepared]:     (B = n_draws, T = batch) */
+} memoroid_op;
+
 /* Version of this header the library was built from (MEMOROID_ABI_VERSION). */
 int memoroid_abi_version(void);
 
 /* Static, human-readable text for a memoroid_status value. */
 const char* memoroid_status_string(int status);
+
+/* ------------------------------------------------------------------------
+ * Workspace size of any entry point: enough for every dtype and flag
+ * combination the entry point accepts at these sizes (the per-entry queries
+ * below give the exact size for one combination).  Arguments an operation
+ * does not use are ignored; the comments of memoroid_op say which ones each
+ * operation reads (B is ignored by the linear-attention operations, which
+ * take one tape).  Returns 0 for an empty problem, for sizes or shapes the
+ * operation rejects (negative extents, linear attention with dk, dv or chunk
+ * other than 64), and for an unknown op.
+ * ------------------------------------------------------------------------ */
+size_t memoroid_workspace_bytes(memoroid_op op, int64_t B, int64_t T, int64_t d_or_H,
+                                int64_t dk, int64_t dv, int64_t chunk);
 
 /* ------------------------------------------------------------------------
  * Diagonal linear memoroid, forward.
@@ -121,7 +152,9 @@ const char* memoroid_status_string(int status);
  *              bf16 inputs are decoded exactly and the state is carried in
  *              fp32; bf16 outputs are rounded to nearest even.  Other pairs:
  *              EUNSUPPORTED.
- *   Workspace (prepared): memoroid_scan_diag_workspace_bytes(B, T, d, in_dtype, out_dtype).
+ *   Workspace: memoroid_scan_diag_workspace_bytes(B, T, d, in_dtype, out_dtype) bytes;
+ *   memoroid_scan_diag initialises it, memoroid_scan_diag_prepared takes a
+ *   prepared one (same arguments otherwise).
  * ------------------------------------------------------------------------ */
 size_t memoroid_scan_diag_workspace_bytes(int64_t B, int64_t T, int64_t d,
                                           int in_dtype, int out_dtype);
@@ -132,6 +165,13 @@ int memoroid_scan_diag(const void* a, int64_t a_stride_t,
                        int64_t B, int64_t T, int64_t d,
                        int in_dtype, int out_dtype,
                        void* workspace, size_t workspace_bytes, void* stream);
+
+int memoroid_scan_diag_prepared(const void* a, int64_t a_stride_t,
+                                const void* x, const uint8_t* start,
+                                void* h, int32_t* episode_idx,
+                                int64_t B, int64_t T, int64_t d,
+                                int in_dtype, int out_dtype,
+                                void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Diagonal linear memoroid, reverse scan (gradients).
@@ -153,7 +193,8 @@ int memoroid_scan_diag(const void* a, int64_t a_stride_t,
  *   grad_a     out [B][T][d] when a_stride_t == d; out [d], summed over every
  *              tape and step, when a_stride_t == 0.  NULL skips it.
  *   dtype      MEMOROID_F32 or MEMOROID_C64 (all tensors of that dtype).
- *   Workspace (prepared): memoroid_scan_diag_bwd_workspace_bytes(B, T, d, dtype, a_stride_t).
+ *   Workspace: memoroid_scan_diag_bwd_workspace_bytes(B, T, d, dtype, a_stride_t)
+ *   bytes; self-initialising, or prepared for memoroid_scan_diag_bwd_prepared.
  * ------------------------------------------------------------------------ */
 size_t memoroid_scan_diag_bwd_workspace_bytes(int64_t B, int64_t T, int64_t d,
                                               int dtype, int64_t a_stride_t);
@@ -163,6 +204,12 @@ int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t,
                            void* grad_x, void* grad_a,
                            int64_t B, int64_t T, int64_t d, int dtype,
                            void* workspace, size_t workspace_bytes, void* stream);
+
+int memoroid_scan_diag_bwd_prepared(const void* a, int64_t a_stride_t,
+                                    const uint8_t* start, const void* h, const void* grad_h,
+                                    void* grad_x, void* grad_a,
+                                    int64_t B, int64_t T, int64_t d, int dtype,
+                                    void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * FFM aggregator (App. G.4, the fast-and-forgetful-memory memoroid): a
@@ -181,7 +228,8 @@ int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t,
  *   S          out [B][T][m][c] complex64, interleaved (re, im).
  *   episode_idx  optional out int32[B][T]; NULL skips it.
  *   Vectorised when m * c is even and S is 16-byte aligned.
- *   Workspace (prepared): memoroid_scan_ffm_workspace_bytes(B, T, m, c).
+ *   Workspace: memoroid_scan_ffm_workspace_bytes(B, T, m, c) bytes;
+ *   self-initialising, or prepared for memoroid_scan_ffm_prepared.
  * ------------------------------------------------------------------------ */
 size_t memoroid_scan_ffm_workspace_bytes(int64_t B, int64_t T, int64_t m, int64_t c);
 
@@ -189,6 +237,11 @@ int memoroid_scan_ffm(const float* alpha, const float* omega, const float* x,
                       const uint8_t* start, void* S, int32_t* episode_idx,
                       int64_t B, int64_t T, int64_t m, int64_t c,
                       void* workspace, size_t workspace_bytes, void* stream);
+
+int memoroid_scan_ffm_prepared(const float* alpha, const float* omega, const float* x,
+                               const uint8_t* start, void* S, int32_t* episode_idx,
+                               int64_t B, int64_t T, int64_t m, int64_t c,
+                               void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Gradient of the FFM aggregator (App. G.4), conjugate (PyTorch) convention
@@ -207,7 +260,8 @@ int memoroid_scan_ffm(const float* alpha, const float* omega, const float* x,
  *   grad_alpha optional out [m] fp32;  grad_omega: optional out [c] fp32.
  *   c must be a power of two no larger than 16 (MEMOROID_EUNSUPPORTED
  *   otherwise): the input gradient is reduced over c inside the kernel.
- *   Workspace (prepared): memoroid_scan_ffm_bwd_workspace_bytes(B, T, m, c).
+ *   Workspace: memoroid_scan_ffm_bwd_workspace_bytes(B, T, m, c) bytes;
+ *   self-initialising, or prepared for memoroid_scan_ffm_bwd_prepared.
  * ------------------------------------------------------------------------ */
 size_t memoroid_scan_ffm_bwd_workspace_bytes(int64_t B, int64_t T, int64_t m, int64_t c);
 
@@ -216,6 +270,12 @@ int memoroid_scan_ffm_bwd(const float* alpha, const float* omega, const uint8_t*
                           float* grad_alpha, float* grad_omega,
                           int64_t B, int64_t T, int64_t m, int64_t c,
                           void* workspace, size_t workspace_bytes, void* stream);
+
+int memoroid_scan_ffm_bwd_prepared(const float* alpha, const float* omega, const uint8_t* start,
+                                   const void* S, const void* grad_S, float* grad_x,
+                                   float* grad_alpha, float* grad_omega,
+                                   int64_t B, int64_t T, int64_t m, int64_t c,
+                                   void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Linear-transformer memoroid (App. G.1), forward readout, one tape of T
@@ -283,13 +343,18 @@ int memoroid_scan_linattn_bwd(const float* q, const float* k, const float* v,
  *   G          out [B][T] fp32; must not alias r or start.
  *   Rows with T % 4 == 0 and 16-byte aligned r and G (4-byte aligned start)
  *   take the vectorised kernel, other shapes a scalar one.
- *   Workspace (prepared): memoroid_discount_workspace_bytes(B, T) bytes.
+ *   Workspace: memoroid_discount_workspace_bytes(B, T) bytes; self-initialising,
+ *   or prepared for memoroid_discounted_return_prepared.
  * ------------------------------------------------------------------------ */
 size_t memoroid_discount_workspace_bytes(int64_t B, int64_t T);
 
 int memoroid_discounted_return(const float* r, const uint8_t* start, float gamma, float* G,
                                int64_t B, int64_t T,
                                void* workspace, size_t workspace_bytes, void* stream);
+
+int memoroid_discounted_return_prepared(const float* r, const uint8_t* start, float gamma, float* G,
+                                        int64_t B, int64_t T,
+                                        void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Generalized advantage estimate over a tape (App. E, the GAE memoroid:
@@ -314,12 +379,18 @@ int memoroid_discounted_return(const float* r, const uint8_t* start, float gamma
  *              Outputs must not alias any input or each other.
  *   Vectorised when T % 4 == 0, every fp32 pointer is 16-byte aligned and
  *   the flag pointers 4-byte aligned.
- *   Workspace (prepared): memoroid_discount_workspace_bytes(B, T) bytes.
+ *   Workspace: memoroid_discount_workspace_bytes(B, T) bytes; self-initialising,
+ *   or prepared for memoroid_gae_prepared.
  * ------------------------------------------------------------------------ */
 int memoroid_gae(const float* r, const float* value, const float* value_next, const uint8_t* done,
                  const uint8_t* start, float gamma, float lambda, float* adv, float* target,
                  int64_t B, int64_t T,
                  void* workspace, size_t workspace_bytes, void* stream);
+
+int memoroid_gae_prepared(const float* r, const float* value, const float* value_next, const uint8_t* done,
+                          const uint8_t* start, float gamma, float lambda, float* adv, float* target,
+                          int64_t B, int64_t T,
+                          void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Tape-Based Batching, insertion (Alg. 1): the begin indices of a rollout,
@@ -333,13 +404,18 @@ int memoroid_gae(const float* r, const float* value, const float* value_next, co
  *   indices    out, room for n int64 values (only count are written).
  *   count      out, one int64 in device memory.
  *   n < 2^31 (MEMOROID_EUNSUPPORTED otherwise); n == 0 writes count = 0.
- *   Workspace (prepared): memoroid_tbb_begin_indices_workspace_bytes(n).
+ *   Workspace: memoroid_tbb_begin_indices_workspace_bytes(n) bytes;
+ *   self-initialising, or prepared for memoroid_tbb_begin_indices_prepared.
  * ------------------------------------------------------------------------ */
 size_t memoroid_tbb_begin_indices_workspace_bytes(int64_t n);
 
 int memoroid_tbb_begin_indices(const uint8_t* start, int64_t n, int64_t offset,
                                int64_t* indices, int64_t* count,
                                void* workspace, size_t workspace_bytes, void* stream);
+
+int memoroid_tbb_begin_indices_prepared(const uint8_t* start, int64_t n, int64_t offset,
+                                        int64_t* indices, int64_t* count,
+                                        void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Tape-Based Batching, sampling (Alg. 2): the batch is the concatenation of
@@ -362,12 +438,12 @@ int memoroid_tbb_begin_indices(const uint8_t* start, int64_t n, int64_t offset,
  *   n_draws <= 2^24, row_bytes <= 2^24, batch < 2^47 and n_D < 2^47
  *   (MEMOROID_EUNSUPPORTED otherwise).  Rows move in 16-byte units when
  *   row_bytes % 16 == 0 and D, out are 16-byte aligned.
- *   Workspace (prepared, bound to n_draws and batch):
- *   memoroid_tbb_sample_workspace_bytes(n_draws, batch); not used when
- *   n_draws or batch is 0.  It holds, per call, where each draw starts in
+ *   Workspace: memoroid_tbb_sample_workspace_bytes(n_draws, batch) bytes,
+ *   self-initialising, or prepared for memoroid_tbb_sample_prepared (bound to
+ *   n_draws and batch); not used when n_draws or batch is 0.  It holds, per call, where each draw starts in
  *   the batch and which draw holds the first row of each group of 256
- *   output rows.  A call that finds it bound to other sizes writes no
- *   output (memoroid_workspace_status reports MEMOROID_EMISMATCH).
+ *   output rows.  A prepared call that finds it bound to other sizes writes
+ *   no output (memoroid_workspace_status reports MEMOROID_EMISMATCH).
  * ------------------------------------------------------------------------ */
 size_t memoroid_tbb_sample_workspace_bytes(int64_t n_draws, int64_t batch);
 
@@ -376,13 +452,19 @@ int memoroid_tbb_sample(const void* D, int64_t n_D, int64_t row_bytes,
                         int64_t batch, void* out, uint8_t* out_start, int64_t* out_src,
                         int64_t* filled, void* workspace, size_t workspace_bytes, void* stream);
 
+int memoroid_tbb_sample_prepared(const void* D, int64_t n_D, int64_t row_bytes,
+                                 const int64_t* I, int64_t n_I, const int64_t* draws, int64_t n_draws,
+                                 int64_t batch, void* out, uint8_t* out_start, int64_t* out_src,
+                                 int64_t* filled, void* workspace, size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------------
- * Prepare a workspace for the PREPARED calls (see the conventions above):
+ * Prepare a workspace for the PREPARED calls (the *_prepared variants, see
+ * the conventions above):
  * enqueues on `stream` one kernel that fills the first workspace_bytes
  * (rounded down to a multiple of 16) with all-ones bytes: an unbound
  * workspace, with no tile counted and no descriptor published.  workspace
  * must be 16-byte aligned and at least 256 bytes (MEMOROID_EINVAL
- * otherwise).  Not needed by the SELF-INITIALISING calls.  The caller keeps
+ * otherwise).  Not needed by the self-initialising calls.  The caller keeps
  * ownership; nothing is allocated.
  * ------------------------------------------------------------------------ */
 int memoroid_workspace_prepare(void* workspace, size_t workspace_bytes, void* stream);

@@ -7,13 +7,14 @@ runs in the library's HIP kernels:
   for pointers), for callers that manage device memory themselves;
 * ``scan_diag``, ``scan_diag_bwd``, ``scan_linattn`` ... taking torch CUDA
   tensors: they check shapes, dtypes and contiguity, allocate outputs with
-  ``torch.empty`` and launch on the current torch stream.  Workspaces of the
-  prepared entry points (one kernel per call, see include/memoroid.h) come
-  from a small cache of prepared workspaces, one per (device, stream, entry
-  point, sizes, flags, operand alignment): after the first call with a key,
-  a call launches exactly one kernel.  A workspace tensor passed in
-  explicitly is prepared on every call.  ``DiagScan`` wraps the diagonal pair
-  as a ``torch.autograd.Function``.
+  ``torch.empty`` and launch on the current torch stream.  Without a
+  ``workspace`` argument they call the ``*_prepared`` entry points (one
+  kernel per call, see include/memoroid.h) on a workspace from a small cache
+  of prepared workspaces, one per (device, stream, entry point, sizes,
+  flags, operand alignment).  A workspace tensor passed in explicitly goes
+  to the self-initialising entry point (which fills what it needs on the
+  stream).  ``DiagScan`` wraps the diagonal pair as a
+  ``torch.autograd.Function``.
 
 Loading fails loudly (``MemoroidError``) if the shared library is missing:
 there is no fallback implementation.
@@ -29,6 +30,8 @@ LIB_PATH = os.path.join(HERE, "libmemoroid.so")
 
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP, ETIMEOUT, EMISMATCH = 0, -1, -2, -3, -4, -5, -6
 F32, BF16, C64 = 0, 1, 2
+(OP_DIAG, OP_DIAG_BWD, OP_LINATTN, OP_LINATTN_BWD, OP_FFM, OP_FFM_BWD, OP_RETURN, OP_GAE,
+ OP_TBB_BEGIN_INDICES, OP_TBB_SAMPLE) = range(10)
 
 _lib = None
 
@@ -94,6 +97,18 @@ def lib() -> ctypes.CDLL:
         L.memoroid_workspace_status.argtypes = [P, SZ, P]
         L.memoroid_workspace_prepare.restype = I32
         L.memoroid_workspace_prepare.argtypes = [P, SZ, P]
+        for name in ("memoroid_scan_diag", "memoroid_scan_diag_bwd", "memoroid_scan_ffm", "memoroid_scan_ffm_bwd",
+                     "memoroid_discounted_return", "memoroid_gae", "memoroid_tbb_begin_indices",
+                     "memoroid_tbb_sample"):
+            fp = getattr(L, name + "_prepared")
+            fp.restype = I32
+            fp.argtypes = getattr(L, name).argtypes
+        L.memoroid_workspace_bytes.restype = SZ
+        L.memoroid_workspace_bytes.argtypes = [I32, I64, I64, I64, I64, I64, I64]
+        L.memoroid_testing_set_fallback_polls.restype = I64
+        L.memoroid_testing_set_fallback_polls.argtypes = [I64]
+        L.memoroid_testing_tile_steps.restype = I64
+        L.memoroid_testing_tile_steps.argtypes = [I32, I64, I64, I64, I32, I64, I32]
         _lib = L
     return _lib
 
@@ -115,6 +130,18 @@ def memoroid_status_string(status: int) -> str:
     return status_string(status)
 
 
+def memoroid_workspace_bytes(op, B, T, d_or_H, dk, dv, chunk) -> int:
+    return lib().memoroid_workspace_bytes(op, B, T, d_or_H, dk, dv, chunk)
+
+
+def memoroid_testing_set_fallback_polls(polls) -> int:
+    return lib().memoroid_testing_set_fallback_polls(polls)
+
+
+def memoroid_testing_tile_steps(reverse, B, T, d, dtype, a_stride_t, vectorised) -> int:
+    return lib().memoroid_testing_tile_steps(reverse, B, T, d, dtype, a_stride_t, vectorised)
+
+
 def memoroid_scan_diag_workspace_bytes(B, T, d, in_dtype, out_dtype) -> int:
     return lib().memoroid_scan_diag_workspace_bytes(B, T, d, in_dtype, out_dtype)
 
@@ -125,6 +152,12 @@ def memoroid_scan_diag(a, a_stride_t, x, start, h, episode_idx, B, T, d, in_dtyp
                                     out_dtype, workspace, workspace_bytes, stream)
 
 
+def memoroid_scan_diag_prepared(a, a_stride_t, x, start, h, episode_idx, B, T, d, in_dtype, out_dtype,
+                                workspace, workspace_bytes, stream) -> int:
+    return lib().memoroid_scan_diag_prepared(a, a_stride_t, x, start, h, episode_idx, B, T, d, in_dtype,
+                                             out_dtype, workspace, workspace_bytes, stream)
+
+
 def memoroid_scan_diag_bwd_workspace_bytes(B, T, d, dtype, a_stride_t) -> int:
     return lib().memoroid_scan_diag_bwd_workspace_bytes(B, T, d, dtype, a_stride_t)
 
@@ -133,6 +166,12 @@ def memoroid_scan_diag_bwd(a, a_stride_t, start, h, grad_h, grad_x, grad_a, B, T
                            workspace, workspace_bytes, stream) -> int:
     return lib().memoroid_scan_diag_bwd(a, a_stride_t, start, h, grad_h, grad_x, grad_a, B, T, d,
                                         dtype, workspace, workspace_bytes, stream)
+
+
+def memoroid_scan_diag_bwd_prepared(a, a_stride_t, start, h, grad_h, grad_x, grad_a, B, T, d, dtype,
+                                    workspace, workspace_bytes, stream) -> int:
+    return lib().memoroid_scan_diag_bwd_prepared(a, a_stride_t, start, h, grad_h, grad_x, grad_a, B, T, d,
+                                                 dtype, workspace, workspace_bytes, stream)
 
 
 def memoroid_scan_linattn_workspace_bytes(T, H, dk, dv, chunk) -> int:
@@ -165,12 +204,24 @@ def memoroid_scan_ffm(alpha, omega, x, start, S, episode_idx, B, T, m, c, worksp
                                    workspace_bytes, stream)
 
 
+def memoroid_scan_ffm_prepared(alpha, omega, x, start, S, episode_idx, B, T, m, c, workspace, workspace_bytes,
+                               stream) -> int:
+    return lib().memoroid_scan_ffm_prepared(alpha, omega, x, start, S, episode_idx, B, T, m, c, workspace,
+                                            workspace_bytes, stream)
+
+
 def memoroid_tbb_begin_indices_workspace_bytes(n) -> int:
     return lib().memoroid_tbb_begin_indices_workspace_bytes(n)
 
 
 def memoroid_tbb_begin_indices(start, n, offset, indices, count, workspace, workspace_bytes, stream) -> int:
     return lib().memoroid_tbb_begin_indices(start, n, offset, indices, count, workspace, workspace_bytes, stream)
+
+
+def memoroid_tbb_begin_indices_prepared(start, n, offset, indices, count, workspace, workspace_bytes,
+                                        stream) -> int:
+    return lib().memoroid_tbb_begin_indices_prepared(start, n, offset, indices, count, workspace,
+                                                     workspace_bytes, stream)
 
 
 def memoroid_tbb_sample_workspace_bytes(n_draws, batch) -> int:
@@ -183,6 +234,12 @@ def memoroid_tbb_sample(D, n_D, row_bytes, I, n_I, draws, n_draws, batch, out, o
                                      filled, workspace, workspace_bytes, stream)
 
 
+def memoroid_tbb_sample_prepared(D, n_D, row_bytes, I, n_I, draws, n_draws, batch, out, out_start, out_src,
+                                 filled, workspace, workspace_bytes, stream) -> int:
+    return lib().memoroid_tbb_sample_prepared(D, n_D, row_bytes, I, n_I, draws, n_draws, batch, out, out_start,
+                                              out_src, filled, workspace, workspace_bytes, stream)
+
+
 def memoroid_scan_ffm_bwd_workspace_bytes(B, T, m, c) -> int:
     return lib().memoroid_scan_ffm_bwd_workspace_bytes(B, T, m, c)
 
@@ -193,6 +250,12 @@ def memoroid_scan_ffm_bwd(alpha, omega, start, S, grad_S, grad_x, grad_alpha, gr
                                        workspace, workspace_bytes, stream)
 
 
+def memoroid_scan_ffm_bwd_prepared(alpha, omega, start, S, grad_S, grad_x, grad_alpha, grad_omega, B, T, m, c,
+                                   workspace, workspace_bytes, stream) -> int:
+    return lib().memoroid_scan_ffm_bwd_prepared(alpha, omega, start, S, grad_S, grad_x, grad_alpha, grad_omega,
+                                                B, T, m, c, workspace, workspace_bytes, stream)
+
+
 def memoroid_discount_workspace_bytes(B, T) -> int:
     return lib().memoroid_discount_workspace_bytes(B, T)
 
@@ -201,10 +264,20 @@ def memoroid_discounted_return(r, start, gamma, G, B, T, workspace, workspace_by
     return lib().memoroid_discounted_return(r, start, gamma, G, B, T, workspace, workspace_bytes, stream)
 
 
+def memoroid_discounted_return_prepared(r, start, gamma, G, B, T, workspace, workspace_bytes, stream) -> int:
+    return lib().memoroid_discounted_return_prepared(r, start, gamma, G, B, T, workspace, workspace_bytes, stream)
+
+
 def memoroid_gae(r, value, value_next, done, start, gamma, lam, adv, target, B, T,
                  workspace, workspace_bytes, stream) -> int:
     return lib().memoroid_gae(r, value, value_next, done, start, gamma, lam, adv, target, B, T,
                               workspace, workspace_bytes, stream)
+
+
+def memoroid_gae_prepared(r, value, value_next, done, start, gamma, lam, adv, target, B, T,
+                          workspace, workspace_bytes, stream) -> int:
+    return lib().memoroid_gae_prepared(r, value, value_next, done, start, gamma, lam, adv, target, B, T,
+                                       workspace, workspace_bytes, stream)
 
 
 def memoroid_workspace_status(workspace, workspace_bytes, stream) -> int:
@@ -271,18 +344,18 @@ _PREPARED = None            # OrderedDict: key -> prepared workspace tensor
 _PREPARED_MAX = 32
 
 
-def _prepared(nbytes: int, device, key, operands, workspace=None):
-    """Workspace of a prepared entry point.  `key` names the entry point and
-    the sizes and flags its layout depends on; the alignment of the operands
-    (which selects the vectorised kernels) is added here.  A workspace given
-    by the caller is prepared again on every call."""
+def _prepared(nbytes: int, device, key, operands, workspace=None, entry=None):
+    """Workspace and entry point of a call.  With no workspace given: a
+    prepared workspace from the cache and the `entry`_prepared function.
+    `key` names the entry point and the sizes and flags its layout depends
+    on; the alignment of the operands (which selects the vectorised kernels)
+    is added here.  A workspace given by the caller goes to the
+    self-initialising `entry` (a smaller one raises EWORKSPACE there)."""
     global _PREPARED
     torch = _torch()
     stream = _stream_ptr(device)
-    if workspace is not None and workspace.numel() >= nbytes:
-        _raise(lib().memoroid_workspace_prepare(workspace.data_ptr(), workspace.numel(), stream),
-               "memoroid_workspace_prepare")
-        return workspace
+    if workspace is not None:
+        return workspace, getattr(lib(), entry)
     import collections
     if _PREPARED is None:
         _PREPARED = collections.OrderedDict()
@@ -295,7 +368,7 @@ def _prepared(nbytes: int, device, key, operands, workspace=None):
         while len(_PREPARED) > _PREPARED_MAX:
             _PREPARED.popitem(last=False)
     _PREPARED.move_to_end(full)
-    return ws
+    return ws, getattr(lib(), entry + "_prepared")
 
 
 def _diag_shapes(a, x, start):
@@ -335,8 +408,9 @@ def scan_diag(a, x, start, out_dtype=None, episode_idx: bool = False, workspace=
     h = torch.empty((B, T, d), dtype=out_torch, device=dev)
     idx = torch.empty((B, T), dtype=torch.int32, device=dev) if episode_idx else None
     nbytes = lib().memoroid_scan_diag_workspace_bytes(B, T, d, in_dt, out_dt)
-    ws = _prepared(nbytes, dev, ("diag", B, T, d, in_dt, out_dt, stride), (a, x, h), workspace)
-    st = lib().memoroid_scan_diag(a.data_ptr(), stride, x.data_ptr(), start.data_ptr(), h.data_ptr(),
+    ws, fn = _prepared(nbytes, dev, ("diag", B, T, d, in_dt, out_dt, stride), (a, x, h), workspace,
+                       "memoroid_scan_diag")
+    st = fn(a.data_ptr(), stride, x.data_ptr(), start.data_ptr(), h.data_ptr(),
                                   idx.data_ptr() if idx is not None else None, B, T, d, in_dt, out_dt,
                                   ws.data_ptr(), ws.numel(), _stream_ptr(dev))
     _raise(st, "memoroid_scan_diag")
@@ -363,8 +437,9 @@ def scan_diag_bwd(a, start, h, grad_h, need_grad_a: bool = True, workspace=None)
     if need_grad_a:
         ga = torch.empty((B, T, d) if stride else (d,), dtype=grad_h.dtype, device=dev)
     nbytes = lib().memoroid_scan_diag_bwd_workspace_bytes(B, T, d, dt, stride)
-    ws = _prepared(nbytes, dev, ("diag_bwd", B, T, d, dt, stride, need_grad_a), (a, h, grad_h, gx, ga), workspace)
-    st = lib().memoroid_scan_diag_bwd(a.data_ptr(), stride, start.data_ptr(),
+    ws, fn = _prepared(nbytes, dev, ("diag_bwd", B, T, d, dt, stride, need_grad_a), (a, h, grad_h, gx, ga),
+                       workspace, "memoroid_scan_diag_bwd")
+    st = fn(a.data_ptr(), stride, start.data_ptr(),
                                       h.data_ptr() if h is not None else None, grad_h.data_ptr(),
                                       gx.data_ptr(), ga.data_ptr() if ga is not None else None,
                                       B, T, d, dt, ws.data_ptr(), ws.numel(), _stream_ptr(dev))
@@ -418,8 +493,9 @@ def scan_ffm(alpha, omega, x, start, episode_idx: bool = False, workspace=None):
         raise TypeError("start must be uint8")
     S = torch.empty((B, T, m, c), dtype=torch.complex64, device=dev)
     idx = torch.empty((B, T), dtype=torch.int32, device=dev) if episode_idx else None
-    ws = _prepared(lib().memoroid_scan_ffm_workspace_bytes(B, T, m, c), dev, ("ffm", B, T, m, c), (S,), workspace)
-    st = lib().memoroid_scan_ffm(alpha.data_ptr(), omega.data_ptr(), x.data_ptr(), start.data_ptr(), S.data_ptr(),
+    ws, fn = _prepared(lib().memoroid_scan_ffm_workspace_bytes(B, T, m, c), dev, ("ffm", B, T, m, c), (S,),
+                       workspace, "memoroid_scan_ffm")
+    st = fn(alpha.data_ptr(), omega.data_ptr(), x.data_ptr(), start.data_ptr(), S.data_ptr(),
                                  idx.data_ptr() if idx is not None else None, B, T, m, c, ws.data_ptr(), ws.numel(),
                                  _stream_ptr(dev))
     _raise(st, "memoroid_scan_ffm")
@@ -440,8 +516,9 @@ def tbb_begin_indices(start, offset: int = 0, workspace=None):
     n = start.numel()
     idx = torch.empty(max(n, 1), dtype=torch.int64, device=dev)
     count = torch.empty(1, dtype=torch.int64, device=dev)
-    ws = _prepared(lib().memoroid_tbb_begin_indices_workspace_bytes(n), dev, ("tbb_begins", n), (), workspace)
-    st = lib().memoroid_tbb_begin_indices(start.data_ptr(), n, int(offset), idx.data_ptr(), count.data_ptr(),
+    ws, fn = _prepared(lib().memoroid_tbb_begin_indices_workspace_bytes(n), dev, ("tbb_begins", n), (),
+                       workspace, "memoroid_tbb_begin_indices")
+    st = fn(start.data_ptr(), n, int(offset), idx.data_ptr(), count.data_ptr(),
                                           ws.data_ptr(), ws.numel(), _stream_ptr(dev))
     _raise(st, "memoroid_tbb_begin_indices")
     return idx, count
@@ -462,9 +539,9 @@ def tbb_sample(D, I, draws, batch: int, workspace=None):
     out_src = torch.empty(batch, dtype=torch.int64, device=dev)
     filled = torch.empty(1, dtype=torch.int64, device=dev)
     nd = draws.numel()
-    ws = _prepared(lib().memoroid_tbb_sample_workspace_bytes(nd, batch), dev, ("tbb_sample", nd, batch), (),
-                   workspace)
-    st = lib().memoroid_tbb_sample(D.data_ptr(), n_D, row_bytes, I.data_ptr(), I.numel(), draws.data_ptr(), nd,
+    ws, fn = _prepared(lib().memoroid_tbb_sample_workspace_bytes(nd, batch), dev, ("tbb_sample", nd, batch), (),
+                       workspace, "memoroid_tbb_sample")
+    st = fn(D.data_ptr(), n_D, row_bytes, I.data_ptr(), I.numel(), draws.data_ptr(), nd,
                                    batch, out.data_ptr(), out_start.data_ptr(), out_src.data_ptr(),
                                    filled.data_ptr(), ws.data_ptr(), ws.numel(), _stream_ptr(dev))
     _raise(st, "memoroid_tbb_sample")
@@ -487,9 +564,9 @@ def scan_ffm_bwd(alpha, omega, start, S, grad_S, params: bool = True, workspace=
     gx = torch.empty((B, T, m), dtype=torch.float32, device=dev)
     ga = torch.empty(m, dtype=torch.float32, device=dev) if params else None
     gw = torch.empty(c, dtype=torch.float32, device=dev) if params else None
-    ws = _prepared(lib().memoroid_scan_ffm_bwd_workspace_bytes(B, T, m, c), dev, ("ffm_bwd", B, T, m, c, params),
-                   (S, grad_S), workspace)
-    st = lib().memoroid_scan_ffm_bwd(alpha.data_ptr(), omega.data_ptr(), start.data_ptr(),
+    ws, fn = _prepared(lib().memoroid_scan_ffm_bwd_workspace_bytes(B, T, m, c), dev,
+                       ("ffm_bwd", B, T, m, c, params), (S, grad_S), workspace, "memoroid_scan_ffm_bwd")
+    st = fn(alpha.data_ptr(), omega.data_ptr(), start.data_ptr(),
                                      S.data_ptr() if S is not None else None, grad_S.data_ptr(), gx.data_ptr(),
                                      ga.data_ptr() if ga is not None else None,
                                      gw.data_ptr() if gw is not None else None, B, T, m, c, ws.data_ptr(),
@@ -518,8 +595,9 @@ def discounted_return(r, start, gamma: float, workspace=None):
     if r.dtype != torch.float32 or start.dtype != torch.uint8:
         raise TypeError("r must be float32 and start uint8")
     G = torch.empty((B, T), dtype=torch.float32, device=dev)
-    ws = _prepared(lib().memoroid_discount_workspace_bytes(B, T), dev, ("return", B, T), (), workspace)
-    st = lib().memoroid_discounted_return(r.data_ptr(), start.data_ptr(), float(gamma), G.data_ptr(), B, T,
+    ws, fn = _prepared(lib().memoroid_discount_workspace_bytes(B, T), dev, ("return", B, T), (), workspace,
+                       "memoroid_discounted_return")
+    st = fn(r.data_ptr(), start.data_ptr(), float(gamma), G.data_ptr(), B, T,
                                           ws.data_ptr(), ws.numel(), _stream_ptr(dev))
     _raise(st, "memoroid_discounted_return")
     return G.reshape(shape)
@@ -542,8 +620,9 @@ def gae(r, value, start, gamma: float, lam: float, value_next=None, done=None, t
             raise TypeError("start and done must be uint8")
     adv = torch.empty((B, T), dtype=torch.float32, device=dev)
     tg = torch.empty((B, T), dtype=torch.float32, device=dev) if target else None
-    ws = _prepared(lib().memoroid_discount_workspace_bytes(B, T), dev, ("gae", B, T), (), workspace)
-    st = lib().memoroid_gae(r.data_ptr(), value.data_ptr(),
+    ws, fn = _prepared(lib().memoroid_discount_workspace_bytes(B, T), dev, ("gae", B, T), (), workspace,
+                       "memoroid_gae")
+    st = fn(r.data_ptr(), value.data_ptr(),
                             value_next.data_ptr() if value_next is not None else None,
                             done.data_ptr() if done is not None else None, start.data_ptr(),
                             float(gamma), float(lam), adv.data_ptr(), tg.data_ptr() if tg is not None else None,
@@ -575,8 +654,9 @@ def scan_linattn_bwd(q, k, v, start, out, grad_out, chunk: int = 64, workspace=N
 
 def workspace_status(workspace) -> int:
     """Synchronise and report OK, ETIMEOUT (a cross-tile wait gave up) or
-    EMISMATCH (the workspace was bound to another call) for the calls that
-    used `workspace` since it was prepared."""
+    EMISMATCH (a prepared workspace was bound to another call) for the calls
+    that used `workspace` since it was prepared (self-initialising calls:
+    the last call)."""
     return lib().memoroid_workspace_status(workspace.data_ptr(), workspace.numel(),
                                            _stream_ptr(workspace.device))
 

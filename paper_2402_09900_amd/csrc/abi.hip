@@ -2,11 +2,13 @@
 // argument validation (before any HIP call), tiling plans, workspace layout
 // and kernel launches.
 #include <limits.h>
+#include <atomic>
 #include <initializer_list>
 #include <stdlib.h>
 #include <string.h>
 
 #include "memoroid.h"
+#include "memoroid_testing.h"
 #include "kernels.hpp"
 #include "scan_common.hpp"
 
@@ -46,6 +48,7 @@ struct DiagPlan {
     size_t off_ctr = 0, off_agg = 0, off_incl = 0, off_cnt = 0, off_part = 0, off_sum1 = 0, off_sum2 = 0;
     size_t bank_bytes = 0;
     bool fused_da = false;   // one tape: da summed inside the reverse kernel
+    size_t init_bytes = 0;   // what a self-initialising call fills: header, counters, bank 0
     size_t total = 0;
 };
 
@@ -114,6 +117,7 @@ bool plan_diag(int64_t B, int64_t T, int64_t d, int state_dtype, bool vec, int r
         off = align_up(off + (size_t)p->nt * (size_t)d * 8);
     }
     p->bank_bytes = off - bank0;
+    p->init_bytes = off;
     off += p->bank_bytes;
     if (bwd && ainv && want_grad_a && !fused) {
         const size_t sb = cplx ? 8 : 4;
@@ -131,6 +135,19 @@ bool plan_diag(int64_t B, int64_t T, int64_t d, int state_dtype, bool vec, int r
 }
 
 int check_hip(hipError_t e) { return e == hipSuccess ? MEMOROID_OK : MEMOROID_EHIP; }
+
+// How a call treats its workspace (include/memoroid.h): a self-initialising
+// call first fills the part its kernels read before writing (header, tile
+// counters or epoch words, the bank the first epoch uses) with all-ones
+// bytes, which is exactly the state memoroid_workspace_prepare leaves; the
+// kernels then run as the first call on a prepared workspace.  A prepared
+// call launches the kernels alone.
+enum class WsMode { kSelfInit, kPrepared };
+
+int init_if_self(WsMode mode, void* ws, size_t init_bytes, hipStream_t s) {
+    if (mode != WsMode::kSelfInit) return MEMOROID_OK;
+    return check_hip(ws_init_launch(nullptr, 0, ws, init_bytes, s));
+}
 
 // Workspace fields of a diagonal scan's arguments: counters and bank-0
 // descriptor regions at `base` (the plan's offset 0), header at `hdr`.
@@ -205,9 +222,9 @@ size_t memoroid_scan_diag_workspace_bytes(int64_t B, int64_t T, int64_t d, int i
     return best;
 }
 
-int memoroid_scan_diag(const void* a, int64_t a_stride_t, const void* x, const uint8_t* start, void* h,
-                       int32_t* episode_idx, int64_t B, int64_t T, int64_t d, int in_dtype, int out_dtype,
-                       void* workspace, size_t workspace_bytes, void* stream) {
+static int scan_diag_run(const void* a, int64_t a_stride_t, const void* x, const uint8_t* start, void* h,
+                         int32_t* episode_idx, int64_t B, int64_t T, int64_t d, int in_dtype, int out_dtype,
+                         void* workspace, size_t workspace_bytes, void* stream, WsMode mode) {
     if (B < 0 || T < 0 || d < 0) return MEMOROID_EINVAL;
     if (!diag_dtypes_ok(in_dtype, out_dtype)) return MEMOROID_EUNSUPPORTED;
     if (B == 0 || T == 0 || d == 0) return MEMOROID_OK;
@@ -250,8 +267,24 @@ int memoroid_scan_diag(const void* a, int64_t a_stride_t, const void* x, const u
     args.cnt = (uint64_t*)(ws + p.off_cnt);
     const int ik = in_dtype == MEMOROID_F32 ? K_F32 : in_dtype == MEMOROID_BF16 ? K_BF16 : K_C64;
     const int ok = out_dtype == MEMOROID_F32 ? K_F32 : out_dtype == MEMOROID_BF16 ? K_BF16 : K_C64;
+    const int st = init_if_self(mode, ws, p.init_bytes, s);
+    if (st != MEMOROID_OK) return st;
     if (diag_fwd_launch(ik, ok, vec, ainv, args, p.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
     return MEMOROID_OK;
+}
+
+int memoroid_scan_diag(const void* a, int64_t a_stride_t, const void* x, const uint8_t* start, void* h,
+                       int32_t* episode_idx, int64_t B, int64_t T, int64_t d, int in_dtype, int out_dtype,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+    return scan_diag_run(a, a_stride_t, x, start, h, episode_idx, B, T, d, in_dtype, out_dtype, workspace,
+                         workspace_bytes, stream, WsMode::kSelfInit);
+}
+
+int memoroid_scan_diag_prepared(const void* a, int64_t a_stride_t, const void* x, const uint8_t* start, void* h,
+                                int32_t* episode_idx, int64_t B, int64_t T, int64_t d, int in_dtype,
+                                int out_dtype, void* workspace, size_t workspace_bytes, void* stream) {
+    return scan_diag_run(a, a_stride_t, x, start, h, episode_idx, B, T, d, in_dtype, out_dtype, workspace,
+                         workspace_bytes, stream, WsMode::kPrepared);
 }
 
 // ------------------------------------------------------------------- FFM
@@ -268,9 +301,9 @@ size_t memoroid_scan_ffm_workspace_bytes(int64_t B, int64_t T, int64_t m, int64_
     return best;
 }
 
-int memoroid_scan_ffm(const float* alpha, const float* omega, const float* x, const uint8_t* start, void* S,
-                      int32_t* episode_idx, int64_t B, int64_t T, int64_t m, int64_t c, void* workspace,
-                      size_t workspace_bytes, void* stream) {
+static int scan_ffm_run(const float* alpha, const float* omega, const float* x, const uint8_t* start, void* S,
+                        int32_t* episode_idx, int64_t B, int64_t T, int64_t m, int64_t c, void* workspace,
+                        size_t workspace_bytes, void* stream, WsMode mode) {
     if (B < 0 || T < 0 || m < 0 || c < 0) return MEMOROID_EINVAL;
     if (B == 0 || T == 0 || m == 0 || c == 0) return MEMOROID_OK;
     int64_t d, BT, BTd;
@@ -311,7 +344,23 @@ int memoroid_scan_ffm(const float* alpha, const float* omega, const float* x, co
     args.omega = omega;
     args.ffm_m = m;
     args.ffm_c = c;
+    const int st = init_if_self(mode, ws, p.init_bytes, s);
+    if (st != MEMOROID_OK) return st;
     return check_hip(ffm_fwd_launch(vec, args, p.ntiles, s));
+}
+
+int memoroid_scan_ffm(const float* alpha, const float* omega, const float* x, const uint8_t* start, void* S,
+                      int32_t* episode_idx, int64_t B, int64_t T, int64_t m, int64_t c, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+    return scan_ffm_run(alpha, omega, x, start, S, episode_idx, B, T, m, c, workspace, workspace_bytes, stream,
+                        WsMode::kSelfInit);
+}
+
+int memoroid_scan_ffm_prepared(const float* alpha, const float* omega, const float* x, const uint8_t* start,
+                               void* S, int32_t* episode_idx, int64_t B, int64_t T, int64_t m, int64_t c,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+    return scan_ffm_run(alpha, omega, x, start, S, episode_idx, B, T, m, c, workspace, workspace_bytes, stream,
+                        WsMode::kPrepared);
 }
 
 // ------------------------------------------------------------ FFM gradient
@@ -350,9 +399,10 @@ size_t memoroid_scan_ffm_bwd_workspace_bytes(int64_t B, int64_t T, int64_t m, in
     return best;
 }
 
-int memoroid_scan_ffm_bwd(const float* alpha, const float* omega, const uint8_t* start, const void* S,
-                          const void* grad_S, float* grad_x, float* grad_alpha, float* grad_omega, int64_t B,
-                          int64_t T, int64_t m, int64_t c, void* workspace, size_t workspace_bytes, void* stream) {
+static int scan_ffm_bwd_run(const float* alpha, const float* omega, const uint8_t* start, const void* S,
+                            const void* grad_S, float* grad_x, float* grad_alpha, float* grad_omega, int64_t B,
+                            int64_t T, int64_t m, int64_t c, void* workspace, size_t workspace_bytes, void* stream,
+                            WsMode mode) {
     if (B < 0 || T < 0 || m < 0 || c < 0) return MEMOROID_EINVAL;
     if (B == 0 || T == 0 || m == 0 || c == 0) return MEMOROID_OK;
     int64_t d, BT, BTd;
@@ -403,6 +453,8 @@ int memoroid_scan_ffm_bwd(const float* alpha, const float* omega, const uint8_t*
     args.ffm_m = m;
     args.ffm_c = c;
     args.dxr = (float*)(ws + off_dxw);
+    const int sti = init_if_self(mode, ws, p.init_bytes, s);
+    if (sti != MEMOROID_OK) return sti;
     if (ffm_bwd_launch(vec, args, p.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
     float* da = (float*)(ws + off_da);
     if (params && !p.fused_da) {
@@ -426,6 +478,21 @@ int memoroid_scan_ffm_bwd(const float* alpha, const float* omega, const uint8_t*
     return check_hip(ffm_bwd_finish_launch(fa, s));
 }
 
+int memoroid_scan_ffm_bwd(const float* alpha, const float* omega, const uint8_t* start, const void* S,
+                          const void* grad_S, float* grad_x, float* grad_alpha, float* grad_omega, int64_t B,
+                          int64_t T, int64_t m, int64_t c, void* workspace, size_t workspace_bytes, void* stream) {
+    return scan_ffm_bwd_run(alpha, omega, start, S, grad_S, grad_x, grad_alpha, grad_omega, B, T, m, c, workspace,
+                            workspace_bytes, stream, WsMode::kSelfInit);
+}
+
+int memoroid_scan_ffm_bwd_prepared(const float* alpha, const float* omega, const uint8_t* start, const void* S,
+                                   const void* grad_S, float* grad_x, float* grad_alpha, float* grad_omega,
+                                   int64_t B, int64_t T, int64_t m, int64_t c, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+    return scan_ffm_bwd_run(alpha, omega, start, S, grad_S, grad_x, grad_alpha, grad_omega, B, T, m, c, workspace,
+                            workspace_bytes, stream, WsMode::kPrepared);
+}
+
 // ------------------------------------------------------------ diag backward
 
 size_t memoroid_scan_diag_bwd_workspace_bytes(int64_t B, int64_t T, int64_t d, int dtype, int64_t a_stride_t) {
@@ -440,9 +507,9 @@ size_t memoroid_scan_diag_bwd_workspace_bytes(int64_t B, int64_t T, int64_t d, i
     return best;
 }
 
-int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t, const uint8_t* start, const void* h,
-                           const void* grad_h, void* grad_x, void* grad_a, int64_t B, int64_t T, int64_t d,
-                           int dtype, void* workspace, size_t workspace_bytes, void* stream) {
+static int scan_diag_bwd_run(const void* a, int64_t a_stride_t, const uint8_t* start, const void* h,
+                             const void* grad_h, void* grad_x, void* grad_a, int64_t B, int64_t T, int64_t d,
+                             int dtype, void* workspace, size_t workspace_bytes, void* stream, WsMode mode) {
     if (B < 0 || T < 0 || d < 0) return MEMOROID_EINVAL;
     if (dtype != MEMOROID_F32 && dtype != MEMOROID_C64) return MEMOROID_EUNSUPPORTED;
     if (B == 0 || T == 0 || d == 0) return MEMOROID_OK;
@@ -489,6 +556,8 @@ int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t, const uint8_t* sta
                 layout_sig({kSigDiagBwd, B, T, d, dtype, vec, ainv, grad_a != nullptr}));
     const int k = dtype == MEMOROID_F32 ? K_F32 : K_C64;
     const int64_t cols = d * (dtype == MEMOROID_C64 ? 2 : 1);
+    const int sti = init_if_self(mode, ws, p.init_bytes, s);
+    if (sti != MEMOROID_OK) return sti;
     if (diag_bwd_launch(k, vec, ainv, args, p.ntiles, s) != hipSuccess) return MEMOROID_EHIP;
     if (ainv && grad_a && !p.fused_da) {
         const int st = reduce_rows((const float*)(ws + p.off_part), (float*)(ws + p.off_sum1),
@@ -496,6 +565,20 @@ int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t, const uint8_t* sta
         if (st != MEMOROID_OK) return st;
     }
     return MEMOROID_OK;
+}
+
+int memoroid_scan_diag_bwd(const void* a, int64_t a_stride_t, const uint8_t* start, const void* h,
+                           const void* grad_h, void* grad_x, void* grad_a, int64_t B, int64_t T, int64_t d,
+                           int dtype, void* workspace, size_t workspace_bytes, void* stream) {
+    return scan_diag_bwd_run(a, a_stride_t, start, h, grad_h, grad_x, grad_a, B, T, d, dtype, workspace,
+                             workspace_bytes, stream, WsMode::kSelfInit);
+}
+
+int memoroid_scan_diag_bwd_prepared(const void* a, int64_t a_stride_t, const uint8_t* start, const void* h,
+                                    const void* grad_h, void* grad_x, void* grad_a, int64_t B, int64_t T,
+                                    int64_t d, int dtype, void* workspace, size_t workspace_bytes, void* stream) {
+    return scan_diag_bwd_run(a, a_stride_t, start, h, grad_h, grad_x, grad_a, B, T, d, dtype, workspace,
+                             workspace_bytes, stream, WsMode::kPrepared);
 }
 
 // ---------------------------------------------------------- linear attention
@@ -771,7 +854,7 @@ namespace {
 
 struct DiscPlan {
     int64_t nt = 0, ntiles = 0;
-    size_t off_epoch = 0, off_agg = 0, off_incl = 0, bank_bytes = 0, total = 0;
+    size_t off_epoch = 0, off_agg = 0, off_incl = 0, bank_bytes = 0, init_bytes = 0, total = 0;
 };
 
 // header, per-tile epoch words, then two banks of tile words
@@ -787,6 +870,7 @@ bool plan_disc(int64_t B, int64_t T, bool gae, DiscPlan* p) {
     p->off_incl = off;
     off = align_up(off + (size_t)p->ntiles * 8);
     p->bank_bytes = off - bank0;
+    p->init_bytes = off;
     p->total = off + p->bank_bytes;
     return true;
 }
@@ -794,21 +878,15 @@ bool plan_disc(int64_t B, int64_t T, bool gae, DiscPlan* p) {
 bool unit_interval(float v) { return v >= 0.0f && v <= 1.0f; }   // false for NaN
 
 // Polls of an awaited tile without progress before a look-back computes
-// that tile's aggregate from its inputs.  MEMOROID_FALLBACK_POLLS overrides
-// the default (tests set it to 0 to run the fallback on every wait).
-uint32_t fallback_polls() {
-    const char* e = getenv("MEMOROID_FALLBACK_POLLS");
-    if (e && *e) {
-        char* end = nullptr;
-        const unsigned long v = strtoul(e, &end, 10);
-        if (end && *end == 0 && v <= 0xFFFFFFFFul) return (uint32_t)v;
-    }
-    return 4096u;
-}
+// that tile's aggregate from its inputs (memoroid_testing_set_fallback_polls
+// lowers it in tests, to run the fallback on every wait).
+constexpr uint32_t kDefaultFallbackPolls = 4096u;
+std::atomic<uint32_t> g_fallback_polls{kDefaultFallbackPolls};
+uint32_t fallback_polls() { return g_fallback_polls.load(std::memory_order_relaxed); }
 
 int disc_run(const float* r, const float* value, const float* value_next, const uint8_t* done,
              const uint8_t* start, float a, float gamma, float* out, float* target, int64_t B, int64_t T,
-             void* workspace, size_t workspace_bytes, void* stream, bool gae) {
+             void* workspace, size_t workspace_bytes, void* stream, bool gae, WsMode mode) {
     int64_t BT;
     if (!mul_ok(B, T, &BT) || BT > INT64_MAX / 16) return MEMOROID_EINVAL;
     const float* fin[3] = {r, value, value_next};
@@ -852,6 +930,8 @@ int disc_run(const float* r, const float* value, const float* value_next, const 
     // the return and the advantage tile differently: each binds its own workspace
     args.sig = layout_sig({kSigDiscount, B, T, gae});
     args.epoch = (uint32_t*)(ws + p.off_epoch);
+    const int st = init_if_self(mode, ws, p.init_bytes, s);
+    if (st != MEMOROID_OK) return st;
     return check_hip(disc_launch(vec, gae, args, p.ntiles, s));
 }
 
@@ -864,23 +944,47 @@ size_t memoroid_discount_workspace_bytes(int64_t B, int64_t T) {
     return pr.total > pg.total ? pr.total : pg.total;
 }
 
-int memoroid_discounted_return(const float* r, const uint8_t* start, float gamma, float* G, int64_t B, int64_t T,
-                               void* workspace, size_t workspace_bytes, void* stream) {
+static int return_run(const float* r, const uint8_t* start, float gamma, float* G, int64_t B, int64_t T,
+                      void* workspace, size_t workspace_bytes, void* stream, WsMode mode) {
     if (B < 0 || T < 0 || !unit_interval(gamma)) return MEMOROID_EINVAL;
     if (B == 0 || T == 0) return MEMOROID_OK;
     if (!r || !start || !G) return MEMOROID_EINVAL;
     return disc_run(r, nullptr, nullptr, nullptr, start, gamma, gamma, G, nullptr, B, T, workspace,
-                    workspace_bytes, stream, false);
+                    workspace_bytes, stream, false, mode);
+}
+
+int memoroid_discounted_return(const float* r, const uint8_t* start, float gamma, float* G, int64_t B, int64_t T,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+    return return_run(r, start, gamma, G, B, T, workspace, workspace_bytes, stream, WsMode::kSelfInit);
+}
+
+int memoroid_discounted_return_prepared(const float* r, const uint8_t* start, float gamma, float* G, int64_t B,
+                                        int64_t T, void* workspace, size_t workspace_bytes, void* stream) {
+    return return_run(r, start, gamma, G, B, T, workspace, workspace_bytes, stream, WsMode::kPrepared);
+}
+
+static int gae_run(const float* r, const float* value, const float* value_next, const uint8_t* done,
+                   const uint8_t* start, float gamma, float lambda, float* adv, float* target, int64_t B, int64_t T,
+                   void* workspace, size_t workspace_bytes, void* stream, WsMode mode) {
+    if (B < 0 || T < 0 || !unit_interval(gamma) || !unit_interval(lambda)) return MEMOROID_EINVAL;
+    if (B == 0 || T == 0) return MEMOROID_OK;
+    if (!r || !value || !start || !adv) return MEMOROID_EINVAL;
+    return disc_run(r, value, value_next, done, start, gamma * lambda, gamma, adv, target, B, T, workspace,
+                    workspace_bytes, stream, true, mode);
 }
 
 int memoroid_gae(const float* r, const float* value, const float* value_next, const uint8_t* done,
                  const uint8_t* start, float gamma, float lambda, float* adv, float* target, int64_t B, int64_t T,
                  void* workspace, size_t workspace_bytes, void* stream) {
-    if (B < 0 || T < 0 || !unit_interval(gamma) || !unit_interval(lambda)) return MEMOROID_EINVAL;
-    if (B == 0 || T == 0) return MEMOROID_OK;
-    if (!r || !value || !start || !adv) return MEMOROID_EINVAL;
-    return disc_run(r, value, value_next, done, start, gamma * lambda, gamma, adv, target, B, T, workspace,
-                    workspace_bytes, stream, true);
+    return gae_run(r, value, value_next, done, start, gamma, lambda, adv, target, B, T, workspace, workspace_bytes,
+                   stream, WsMode::kSelfInit);
+}
+
+int memoroid_gae_prepared(const float* r, const float* value, const float* value_next, const uint8_t* done,
+                          const uint8_t* start, float gamma, float lambda, float* adv, float* target, int64_t B,
+                          int64_t T, void* workspace, size_t workspace_bytes, void* stream) {
+    return gae_run(r, value, value_next, done, start, gamma, lambda, adv, target, B, T, workspace, workspace_bytes,
+                   stream, WsMode::kPrepared);
 }
 
 // ------------------------------------------------- tape-based batching
@@ -890,7 +994,7 @@ namespace {
 // header, per-tile epoch words, then two banks of count words
 struct TbbPlan {
     int64_t ntiles = 0;
-    size_t off_epoch = 0, off_cnt = 0, bank_bytes = 0, total = 0;
+    size_t off_epoch = 0, off_cnt = 0, bank_bytes = 0, init_bytes = 0, total = 0;
 };
 
 void plan_tbb(int64_t n, TbbPlan* p) {
@@ -898,6 +1002,7 @@ void plan_tbb(int64_t n, TbbPlan* p) {
     p->off_epoch = kAlign;
     p->off_cnt = align_up(p->off_epoch + (size_t)p->ntiles * 4);
     p->bank_bytes = align_up((size_t)p->ntiles * 8);
+    p->init_bytes = p->off_cnt + p->bank_bytes;
     p->total = p->off_cnt + 2 * p->bank_bytes;
 }
 
@@ -907,7 +1012,7 @@ void plan_tbb(int64_t n, TbbPlan* p) {
 struct SamplePlan {
     int64_t ntiles = 0, groups = 0;
     size_t off_epoch = 0, off_cnt = 0, bank_bytes = 0, off_meta = 0, off_dec = 0, off_first = 0, off_row0 = 0,
-           off_shift = 0, total = 0;
+           off_shift = 0, init_bytes = 0, total = 0;
 };
 
 constexpr int64_t kSampleMaxRows = (int64_t)1 << 47;   // batch and n_D bound: row sums stay below 2^48
@@ -921,6 +1026,9 @@ void plan_sample(int64_t n_draws, int64_t batch, SamplePlan* p) {
     p->off_meta = p->off_cnt + 2 * p->bank_bytes;
     p->off_dec = align_up(p->off_meta + 16);
     p->off_first = align_up(p->off_dec + 64 * 128);    // 64 verdict words, one per 128-byte line
+    // the verdict words carry the call's epoch: a self-initialising call
+    // (always epoch 0) clears them too
+    p->init_bytes = p->off_first;
     p->off_row0 = align_up(p->off_first + (size_t)p->groups * 8);
     p->off_shift = align_up(p->off_row0 + (size_t)n_draws * 8);
     p->total = align_up(p->off_shift + (size_t)n_draws * 8);
@@ -935,8 +1043,8 @@ size_t memoroid_tbb_begin_indices_workspace_bytes(int64_t n) {
     return p.total;
 }
 
-int memoroid_tbb_begin_indices(const uint8_t* start, int64_t n, int64_t offset, int64_t* indices, int64_t* count,
-                               void* workspace, size_t workspace_bytes, void* stream) {
+static int tbb_begins_run(const uint8_t* start, int64_t n, int64_t offset, int64_t* indices, int64_t* count,
+                          void* workspace, size_t workspace_bytes, void* stream, WsMode mode) {
     if (n < 0) return MEMOROID_EINVAL;
     if (n > (int64_t)INT32_MAX) return MEMOROID_EUNSUPPORTED;
     if (!count) return MEMOROID_EINVAL;
@@ -970,7 +1078,19 @@ int memoroid_tbb_begin_indices(const uint8_t* start, int64_t n, int64_t offset, 
     a.epoch = (uint32_t*)(ws + p.off_epoch);
     a.fallback_polls = fallback_polls();
     const bool vec = aligned(start, 16) && n % 16 == 0;
+    const int st = init_if_self(mode, ws, p.init_bytes, s);
+    if (st != MEMOROID_OK) return st;
     return check_hip(tbb_begins_launch(vec, a, p.ntiles, s));
+}
+
+int memoroid_tbb_begin_indices(const uint8_t* start, int64_t n, int64_t offset, int64_t* indices, int64_t* count,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+    return tbb_begins_run(start, n, offset, indices, count, workspace, workspace_bytes, stream, WsMode::kSelfInit);
+}
+
+int memoroid_tbb_begin_indices_prepared(const uint8_t* start, int64_t n, int64_t offset, int64_t* indices,
+                                        int64_t* count, void* workspace, size_t workspace_bytes, void* stream) {
+    return tbb_begins_run(start, n, offset, indices, count, workspace, workspace_bytes, stream, WsMode::kPrepared);
 }
 
 size_t memoroid_tbb_sample_workspace_bytes(int64_t n_draws, int64_t batch) {
@@ -980,9 +1100,10 @@ size_t memoroid_tbb_sample_workspace_bytes(int64_t n_draws, int64_t batch) {
     return p.total;
 }
 
-int memoroid_tbb_sample(const void* D, int64_t n_D, int64_t row_bytes, const int64_t* I, int64_t n_I,
-                        const int64_t* draws, int64_t n_draws, int64_t batch, void* out, uint8_t* out_start,
-                        int64_t* out_src, int64_t* filled, void* workspace, size_t workspace_bytes, void* stream) {
+static int tbb_sample_run(const void* D, int64_t n_D, int64_t row_bytes, const int64_t* I, int64_t n_I,
+                          const int64_t* draws, int64_t n_draws, int64_t batch, void* out, uint8_t* out_start,
+                          int64_t* out_src, int64_t* filled, void* workspace, size_t workspace_bytes, void* stream,
+                          WsMode mode) {
     if (n_D < 0 || row_bytes <= 0 || n_I < 0 || n_draws < 0 || batch < 0) return MEMOROID_EINVAL;
     if (n_draws > ((int64_t)1 << 24) || row_bytes > ((int64_t)1 << 24)) return MEMOROID_EUNSUPPORTED;
     int64_t tmp;
@@ -1043,12 +1164,88 @@ int memoroid_tbb_sample(const void* D, int64_t n_D, int64_t row_bytes, const int
         a.lead = tiles < (double)p.ntiles ? (int64_t)tiles : p.ntiles;
         if (a.lead < 1) a.lead = 1;
     }
+    if (n_draws > 0) {
+        const int st = init_if_self(mode, workspace, p.init_bytes, s);
+        if (st != MEMOROID_OK) return st;
+    }
     return check_hip(tbb_sample_launch(unit, a, p.ntiles, s));
+}
+
+int memoroid_tbb_sample(const void* D, int64_t n_D, int64_t row_bytes, const int64_t* I, int64_t n_I,
+                        const int64_t* draws, int64_t n_draws, int64_t batch, void* out, uint8_t* out_start,
+                        int64_t* out_src, int64_t* filled, void* workspace, size_t workspace_bytes, void* stream) {
+    return tbb_sample_run(D, n_D, row_bytes, I, n_I, draws, n_draws, batch, out, out_start, out_src, filled,
+                          workspace, workspace_bytes, stream, WsMode::kSelfInit);
+}
+
+int memoroid_tbb_sample_prepared(const void* D, int64_t n_D, int64_t row_bytes, const int64_t* I, int64_t n_I,
+                                 const int64_t* draws, int64_t n_draws, int64_t batch, void* out,
+                                 uint8_t* out_start, int64_t* out_src, int64_t* filled, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+    return tbb_sample_run(D, n_D, row_bytes, I, n_I, draws, n_draws, batch, out, out_start, out_src, filled,
+                          workspace, workspace_bytes, stream, WsMode::kPrepared);
 }
 
 int memoroid_workspace_prepare(void* workspace, size_t workspace_bytes, void* stream) {
     if (!workspace || workspace_bytes < sizeof(WsHeader) || !aligned(workspace, 16)) return MEMOROID_EINVAL;
     return check_hip(ws_init_launch(nullptr, 0, workspace, workspace_bytes / 16 * 16, (hipStream_t)stream));
+}
+
+size_t memoroid_workspace_bytes(memoroid_op op, int64_t B, int64_t T, int64_t d_or_H, int64_t dk, int64_t dv,
+                                int64_t chunk) {
+    size_t best = 0;
+    auto take = [&best](size_t v) {
+        if (v > best) best = v;
+    };
+    switch (op) {
+        case MEMOROID_OP_DIAG: {
+            const int pairs[4][2] = {{MEMOROID_F32, MEMOROID_F32},
+                                     {MEMOROID_BF16, MEMOROID_BF16},
+                                     {MEMOROID_BF16, MEMOROID_F32},
+                                     {MEMOROID_C64, MEMOROID_C64}};
+            for (const auto& pr : pairs) take(memoroid_scan_diag_workspace_bytes(B, T, d_or_H, pr[0], pr[1]));
+            return best;
+        }
+        case MEMOROID_OP_DIAG_BWD:
+            for (int dt : {MEMOROID_F32, MEMOROID_C64})
+                for (int64_t stride : {(int64_t)0, d_or_H})
+                    take(memoroid_scan_diag_bwd_workspace_bytes(B, T, d_or_H, dt, stride));
+            return best;
+        case MEMOROID_OP_LINATTN:
+            return memoroid_scan_linattn_workspace_bytes(T, d_or_H, dk, dv, chunk);
+        case MEMOROID_OP_LINATTN_BWD:
+            return memoroid_scan_linattn_bwd_workspace_bytes(T, d_or_H, dk, dv, chunk);
+        case MEMOROID_OP_FFM:
+            return memoroid_scan_ffm_workspace_bytes(B, T, d_or_H, dk);
+        case MEMOROID_OP_FFM_BWD:
+            return memoroid_scan_ffm_bwd_workspace_bytes(B, T, d_or_H, dk);
+        case MEMOROID_OP_RETURN:
+        case MEMOROID_OP_GAE:
+            return memoroid_discount_workspace_bytes(B, T);
+        case MEMOROID_OP_TBB_BEGIN_INDICES:
+            return memoroid_tbb_begin_indices_workspace_bytes(T);
+        case MEMOROID_OP_TBB_SAMPLE:
+            return memoroid_tbb_sample_workspace_bytes(B, T);
+    }
+    return 0;
+}
+
+int64_t memoroid_testing_set_fallback_polls(int64_t polls) {
+    const uint32_t v = polls < 0 ? kDefaultFallbackPolls : (polls > 0xFFFFFFFFll ? 0xFFFFFFFFu : (uint32_t)polls);
+    return (int64_t)g_fallback_polls.exchange(v, std::memory_order_relaxed);
+}
+
+int64_t memoroid_testing_tile_steps(int reverse, int64_t B, int64_t T, int64_t d, int dtype, int64_t a_stride_t,
+                                    int vectorised) {
+    if (B <= 0 || T <= 0 || d <= 0 || (a_stride_t != 0 && a_stride_t != d)) return 0;
+    if (dtype != MEMOROID_F32 && dtype != MEMOROID_BF16 && dtype != MEMOROID_C64) return 0;
+    if (reverse && dtype == MEMOROID_BF16) return 0;
+    const bool ainv = a_stride_t == 0;
+    DiagPlan p;
+    if (!plan_diag(B, T, d, dtype, vectorised != 0, diag_rows(reverse != 0, ainv), reverse != 0, ainv, reverse != 0,
+                   &p))
+        return 0;
+    return p.L;
 }
 
 int memoroid_workspace_status(const void* workspace, size_t workspace_bytes, void* stream) {

@@ -42,3 +42,19 @@ def cond_err(y, ref, mag):
 def announce(msg):
     """Name the case before a GPU step (a fault ends the process)."""
     print("\n[case] " + msg, flush=True)
+
+
+class forced_fallback:
+    """Within the block, every look-back of the return, GAE and TBB kernels
+    that finds its predecessor unpublished computes that predecessor's
+    summary itself (test-only control of the library)."""
+
+    def __enter__(self):
+        from paper_2402_09900_amd import binding
+        self._lib = binding
+        self._old = binding.memoroid_testing_set_fallback_polls(0)
+        return self
+
+    def __exit__(self, *exc):
+        self._lib.memoroid_testing_set_fallback_polls(self._old)
+        return False

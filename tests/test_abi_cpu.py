@@ -2,6 +2,7 @@
 rejects bad arguments before touching the GPU.  No kernel is launched here:
 every call below fails validation or is an empty problem."""
 import ctypes
+import glob
 import os
 import re
 import subprocess
@@ -12,22 +13,30 @@ from conftest import ROOT
 from paper_2402_09900_amd import binding as mb
 
 HEADER = os.path.join(ROOT, "include", "memoroid.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 
 def declared_functions():
-    src = open(HEADER).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(memoroid_\w+)\s*\(", src)))
+    names = set()
+    for h in HEADERS:
+        src = open(h).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        names |= set(re.findall(r"\b(memoroid_\w+)\s*\(", src))
+    return sorted(names)
 
 
 def test_header_compiles_as_c_and_cxx(tmp_path):
-    for lang, comp in (("c", "gcc"), ("c++", "g++")):
-        subprocess.run([comp, "-x", lang, "-fsyntax-only", "-Wall", "-Werror", HEADER], check=True)
+    assert HEADER in HEADERS
+    for h in HEADERS:
+        for lang, comp in (("c", "gcc"), ("c++", "g++")):
+            subprocess.run([comp, "-x", lang, "-fsyntax-only", "-Wall", "-Werror", h], check=True)
 
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
     assert "memoroid_scan_diag" in names and "memoroid_scan_linattn" in names
+    assert "memoroid_workspace_bytes" in names and "memoroid_scan_diag_prepared" in names
+    assert "memoroid_testing_set_fallback_polls" in names
     lib = ctypes.CDLL(mb.LIB_PATH)
     missing = [n for n in names if not hasattr(lib, n)]
     assert not missing, missing
@@ -36,7 +45,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert mb.memoroid_abi_version() == 3
+    assert mb.memoroid_abi_version() == 4
     for s in (mb.OK, mb.EINVAL, mb.EUNSUPPORTED, mb.EWORKSPACE, mb.EHIP, mb.ETIMEOUT, mb.EMISMATCH):
         assert mb.status_string(s) and mb.status_string(s) != "unknown status"
     assert mb.status_string(12345) == "unknown status"
@@ -59,6 +68,63 @@ def test_prepared_workspaces_hold_two_banks():
     # 16x the tiles: 16 (tiles per chain) * 16 chains * 16 features * 24 bytes per bank
     per_tile_pair = (large - small) / ((1 << 20) - (1 << 16)) * 512
     assert per_tile_pair >= 2 * 16 * 16 * 24 * 0.99
+
+
+def test_generic_workspace_query():
+    """memoroid_workspace_bytes(op, ...) covers every dtype and flag
+    combination of the entry point at those sizes."""
+    q = mb.memoroid_workspace_bytes
+    B, T, d = 2, 70000, 96
+    assert q(mb.OP_DIAG, B, T, d, 0, 0, 0) == max(mb.memoroid_scan_diag_workspace_bytes(B, T, d, i, o) for i, o in
+                                                 ((mb.F32, mb.F32), (mb.BF16, mb.BF16), (mb.BF16, mb.F32),
+                                                  (mb.C64, mb.C64)))
+    assert q(mb.OP_DIAG_BWD, B, T, d, 0, 0, 0) == max(mb.memoroid_scan_diag_bwd_workspace_bytes(B, T, d, dt, s)
+                                                     for dt in (mb.F32, mb.C64) for s in (0, d))
+    assert q(mb.OP_LINATTN, 1, 32768, 4, 64, 64, 64) == mb.memoroid_scan_linattn_workspace_bytes(32768, 4, 64, 64, 64)
+    assert q(mb.OP_LINATTN_BWD, 7, 32768, 4, 64, 64, 64) == \
+        mb.memoroid_scan_linattn_bwd_workspace_bytes(32768, 4, 64, 64, 64)
+    assert q(mb.OP_LINATTN, 1, 32768, 4, 32, 64, 64) == 0
+    assert q(mb.OP_FFM, 1, 1 << 18, 32, 8, 0, 0) == mb.memoroid_scan_ffm_workspace_bytes(1, 1 << 18, 32, 8)
+    assert q(mb.OP_FFM_BWD, 1, 1 << 18, 32, 8, 0, 0) == mb.memoroid_scan_ffm_bwd_workspace_bytes(1, 1 << 18, 32, 8)
+    assert q(mb.OP_RETURN, 3, 1 << 20, 0, 0, 0, 0) == mb.memoroid_discount_workspace_bytes(3, 1 << 20)
+    assert q(mb.OP_GAE, 3, 1 << 20, 0, 0, 0, 0) == mb.memoroid_discount_workspace_bytes(3, 1 << 20)
+    assert q(mb.OP_TBB_BEGIN_INDICES, 0, 1 << 24, 0, 0, 0, 0) == mb.memoroid_tbb_begin_indices_workspace_bytes(1 << 24)
+    assert q(mb.OP_TBB_SAMPLE, 1 << 20, 1 << 20, 0, 0, 0, 0) == mb.memoroid_tbb_sample_workspace_bytes(1 << 20, 1 << 20)
+    assert q(mb.OP_DIAG, -1, T, d, 0, 0, 0) == 0 and q(mb.OP_DIAG, B, 0, d, 0, 0, 0) == 0
+    assert q(99, B, T, d, 0, 0, 0) == 0
+    for op in range(10):
+        assert q(op, 1, 4096, 64, 64, 64, 64) > 0
+
+
+def test_prepared_variants_validate_like_the_defaults():
+    """The *_prepared entry points reject the same bad arguments (before any
+    HIP call) as the self-initialising ones."""
+    for entry in (mb.memoroid_scan_diag, mb.memoroid_scan_diag_prepared):
+        def call(**kw):
+            args = dict(a=A, a_stride_t=8, x=X, start=S, h=H, episode_idx=None, B=2, T=100, d=8,
+                        in_dtype=mb.F32, out_dtype=mb.F32, workspace=W, workspace_bytes=1 << 30, stream=None)
+            args.update(kw)
+            return entry(*args.values())
+        assert call(B=-1) == mb.EINVAL and call(T=0) == mb.OK
+        assert call(in_dtype=mb.F32, out_dtype=mb.BF16) == mb.EUNSUPPORTED
+        assert call(h=X) == mb.EINVAL and call(workspace=None) == mb.EWORKSPACE
+    assert mb.memoroid_scan_diag_bwd_prepared(A, 8, S, H, X, X, None, 1, 50, 8, mb.F32, W, 1 << 30, None) == mb.EINVAL
+    assert mb.memoroid_scan_ffm_prepared(A, X, S, H + 0x100, I + 4, None, 2, 100, 4, 3, W, 1 << 30, None) == mb.EINVAL
+    assert mb.memoroid_scan_ffm_bwd_prepared(A, X, S, H, I, 0x90000, None, None, 1, 100, 4, 3, W, 1 << 30,
+                                             None) == mb.EUNSUPPORTED
+    assert mb.memoroid_discounted_return_prepared(A, S, 1.5, H, 2, 100, W, 1 << 30, None) == mb.EINVAL
+    assert mb.memoroid_gae_prepared(A, X, None, None, S, 0.99, 0.95, H, I, 2, 100, None, 0, None) == mb.EWORKSPACE
+    assert mb.memoroid_tbb_begin_indices_prepared(S, -1, 0, I, A, W, 1 << 30, None) == mb.EINVAL
+    assert mb.memoroid_tbb_sample_prepared(A, 1000, 0, X, 10, S, 100, 500, H, I, None, None, W, 1 << 30,
+                                           None) == mb.EINVAL
+
+
+def test_fallback_control_round_trips():
+    old = mb.memoroid_testing_set_fallback_polls(0)
+    assert old == 4096
+    assert mb.memoroid_testing_set_fallback_polls(17) == 0
+    assert mb.memoroid_testing_set_fallback_polls(-1) == 17
+    assert mb.memoroid_testing_set_fallback_polls(-1) == 4096
 
 
 def test_workspace_queries():

@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 
 import oracle
-from conftest import announce, cond_err
+from conftest import announce, cond_err, forced_fallback
 from paper_2402_09900_amd import tapes
 
 torch = pytest.importorskip("torch")
@@ -203,16 +203,16 @@ def test_repeated_calls_share_a_workspace():
         assert cond_err(G, ref, m) <= TOL
 
 
-def test_lookback_fallback_computes_awaited_tiles(monkeypatch):
+def test_lookback_fallback_computes_awaited_tiles():
     """With the fallback threshold at 0 polls, a look-back that finds its
     nearest tile unpublished computes that tile's aggregate from the inputs at
     once; results must not change."""
-    monkeypatch.setenv("MEMOROID_FALLBACK_POLLS", "0")
-    for T, law in ((64 * 4096 + 12, tapes._uniform_int(1000, 30000)), (40 * 4096, tapes._uniform_int(1, 1000))):
-        tp = tapes.make_discount(6, seed=93, B=2, T=T, episodes=law)
-        check_return(tp, 0.999, "fallback")
-        check_gae(tp, 0.99, 0.95, "fallback", with_vn=False)
-    tp = tapes.make_discount(6, seed=94, B=1, T=32 * 4096 + 3)        # scalar kernel
-    tp.start[:] = 0
-    check_return(tp, 1.0, "fallback scalar")
-    check_gae(tp, 0.99, 0.95, "fallback scalar")
+    with forced_fallback():
+        for T, law in ((64 * 4096 + 12, tapes._uniform_int(1000, 30000)), (40 * 4096, tapes._uniform_int(1, 1000))):
+            tp = tapes.make_discount(6, seed=93, B=2, T=T, episodes=law)
+            check_return(tp, 0.999, "fallback")
+            check_gae(tp, 0.99, 0.95, "fallback", with_vn=False)
+        tp = tapes.make_discount(6, seed=94, B=1, T=32 * 4096 + 3)        # scalar kernel
+        tp.start[:] = 0
+        check_return(tp, 1.0, "fallback scalar")
+        check_gae(tp, 0.99, 0.95, "fallback scalar")

@@ -59,7 +59,7 @@ def test_misaligned_output_takes_scalar_kernel():
     assert mb.memoroid_workspace_prepare(ws.data_ptr(), ws.numel(), torch.cuda.current_stream().cuda_stream) == mb.OK
     S = big[1:]
     al, om, x, s = dev(f.alpha), dev(f.omega), dev(f.x), dev(f.start)     # held until the kernel has run
-    st = mb.memoroid_scan_ffm(al.data_ptr(), om.data_ptr(), x.data_ptr(), s.data_ptr(), S.data_ptr(), None,
+    st = mb.memoroid_scan_ffm_prepared(al.data_ptr(), om.data_ptr(), x.data_ptr(), s.data_ptr(), S.data_ptr(), None,
                               f.B, f.T, f.m, f.c, ws.data_ptr(), ws.numel(), torch.cuda.current_stream().cuda_stream)
     assert st == mb.OK
     torch.cuda.synchronize()

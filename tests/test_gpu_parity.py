@@ -8,8 +8,9 @@ element by element:
     for bf16 inputs (fp32 state);
   * integers (episode indices): bit-exact.
 Full-size workloads run at their real shape in the launch configuration the
-benchmark times, and are compared on whole tapes / feature columns that the
-oracle computes independently (every tape and feature is its own scan).
+benchmark times, and are compared on every element: the oracle runs on one
+tape, or one block of 32 feature columns, at a time (every tape and feature
+is its own scan), so host memory stays bounded.
 """
 import numpy as np
 import pytest
@@ -189,8 +190,20 @@ def w4():
     return tapes.make_diag(4)
 
 
-def test_workload4_full_sampled_tapes(w4):
-    check_fwd(w4, tapes_sel=[0, 17, 63], label="workload4")
+def test_workload4_full_every_tape(w4):
+    """All 64 tapes x 16384 steps x 512 features, bf16 out, against the
+    oracle tape by tape."""
+    announce("fwd workload4 full B=%d T=%d d=%d (every element)" % (w4.B, w4.T, w4.d))
+    h, idx = run_fwd(w4, idx=True)
+    np.testing.assert_array_equal(idx.cpu().numpy(), oracle.episode_idx(w4.start))
+    bits = h.view(torch.int16).cpu().numpy().view(np.uint16)
+    del h
+    worst = 0.0
+    for b in range(w4.B):
+        got = tapes.bf16_bits_to_f32(bits[b:b + 1]).astype(np.float64)
+        ref, mag = oracle.diag_fwd(select(w4, "a", [b]), select(w4, "x", [b]), w4.start[b:b + 1])
+        worst = max(worst, cond_err(got, ref, mag))
+        assert worst <= TOL["bf16"], (b, worst)
 
 
 def test_workload4_reduced_both_outputs():
@@ -204,12 +217,45 @@ def w5():
     return tapes.make_diag(5)
 
 
-def test_workload5_full_fwd_sampled_columns(w5):
-    check_fwd(w5, cols=[0, 1, 77, 128, 200, 255], label="workload5")
+BLOCK = 32                      # feature columns the oracle takes at a time
 
 
-def test_workload5_full_bwd_sampled_columns(w5):
-    check_bwd(w5, cols=[0, 3, 64, 130, 254, 255], label="workload5")
+def test_workload5_full_fwd_every_element(w5):
+    """T = 2^20 steps x 256 features, forward with episode indices, against
+    the oracle one block of 32 columns at a time."""
+    announce("fwd workload5 full T=%d d=%d (every element)" % (w5.T, w5.d))
+    h, idx = run_fwd(w5, idx=True)
+    np.testing.assert_array_equal(idx.cpu().numpy(), oracle.episode_idx(w5.start))
+    h = h.cpu().numpy()
+    for c0 in range(0, w5.d, BLOCK):
+        cols = list(range(c0, min(c0 + BLOCK, w5.d)))
+        ref, mag = oracle.diag_fwd(select(w5, "a", None, cols), select(w5, "x", None, cols), w5.start)
+        err = cond_err(h[:, :, cols].astype(np.float64), ref, mag)
+        assert err <= TOL["f32"], (c0, err)
+
+
+def test_workload5_full_bwd_every_element(w5):
+    """The reverse scan of workload 5 on every element: the saved state h is
+    the oracle's forward in float32, built block by block, and dx, da are
+    compared block by block."""
+    announce("bwd workload5 full T=%d d=%d (every element)" % (w5.T, w5.d))
+    h_in = np.empty(w5.x.shape, dtype=np.float32)
+    blocks = [list(range(c0, min(c0 + BLOCK, w5.d))) for c0 in range(0, w5.d, BLOCK)]
+    for cols in blocks:
+        ref, _ = oracle.diag_fwd(select(w5, "a", None, cols), select(w5, "x", None, cols), w5.start)
+        h_in[:, :, cols] = ref.astype(np.float32)
+    ws = torch.empty(mb.memoroid_scan_diag_bwd_workspace_bytes(w5.B, w5.T, w5.d, mb.F32, w5.d),
+                     dtype=torch.uint8, device=DEV)
+    gx, ga = mb.scan_diag_bwd(to_dev(w5.a, "f32"), to_dev(w5.start, "u8"), to_dev(h_in, "f32"),
+                              to_dev(w5.g, "f32"), workspace=ws)
+    assert mb.workspace_status(ws) == mb.OK
+    gx, ga = gx.cpu().numpy(), ga.cpu().numpy()
+    for cols in blocks:
+        dx, da, m_dx, m_da = oracle.diag_bwd(select(w5, "a", None, cols), w5.start,
+                                             h_in[:, :, cols].astype(np.float64), select(w5, "g", None, cols))
+        e_dx = cond_err(gx[:, :, cols], dx, m_dx)
+        e_da = cond_err(ga[:, :, cols], da, m_da)
+        assert e_dx <= TOL["f32"] and e_da <= TOL["f32"], (cols[0], e_dx, e_da)
 
 
 def test_workload5_reduced_ragged():
@@ -233,6 +279,38 @@ def test_edge_shapes(dtype, inv, shape):
     check_fwd(w, label="edge")
     if dtype != "bf16":
         check_bwd(w, label="edge")
+
+
+def _tile_lengths(dtype, inv, d):
+    """Forward and reverse tile lengths (steps) of the plans these tapes get
+    (torch allocations are 256-byte aligned, so vectorisation follows d)."""
+    code = {"f32": mb.F32, "bf16": mb.BF16, "c64": mb.C64}[dtype]
+    vec = d % (2 if dtype == "c64" else 4) == 0
+    stride = 0 if inv else d
+    Ls = {mb.memoroid_testing_tile_steps(0, 2, 1 << 16, d, code, stride, vec)}
+    if dtype != "bf16":
+        Ls.add(mb.memoroid_testing_tile_steps(1, 2, 1 << 16, d, code, stride, vec))
+    assert all(L > 0 for L in Ls)
+    return sorted(Ls)
+
+
+BOUNDARY_CASES = [(dt, inv, d) for dt in ("f32", "bf16", "c64") for inv in (False, True) for d in (256, 7)]
+
+
+@pytest.mark.parametrize("dtype,inv,d", BOUNDARY_CASES, ids=lambda v: str(v))
+def test_tile_boundary_lengths(dtype, inv, d):
+    """T at L - 1, L, L + 1 and 2L + 1 for every tile length L of the
+    forward and reverse plans (a tape ending one step before, at and after a
+    tile edge; a last tile of a single step)."""
+    Ls = _tile_lengths(dtype, inv, d)
+    if dtype == "f32" and d == 256:
+        assert Ls == sorted({512, 512 if inv else 384}), Ls
+    Ts = sorted({t for L in Ls for t in (L - 1, L, L + 1, 2 * L + 1)})
+    for T in Ts:
+        w = tapes.make_custom_diag(dtype, 2, T, d, inv, seed=3000 + T + d, mean_episode=150.0)
+        check_fwd(w, label="tile edge L=%s" % Ls)
+        if dtype != "bf16":
+            check_bwd(w, label="tile edge L=%s" % Ls)
 
 
 @pytest.mark.parametrize("pattern", ["all_begins", "single_episode", "begin_at_end", "flag_bytes"])

@@ -5,7 +5,7 @@ import numpy as np
 import pytest
 
 import oracle
-from conftest import announce, read_golden
+from conftest import announce, forced_fallback, read_golden
 from paper_2402_09900_amd import tapes
 
 torch = pytest.importorskip("torch")
@@ -68,13 +68,13 @@ def test_begin_indices_shapes(n):
     check_begins(f, 7, "none")
 
 
-def test_begin_indices_workload8_and_fallback(monkeypatch):
+def test_begin_indices_workload8_and_fallback():
     tb = tapes.make_tbb(8)
     check_begins(tb.start, 12345, "workload8")
-    monkeypatch.setenv("MEMOROID_FALLBACK_POLLS", "0")
-    check_begins(tb.start, 0, "workload8 fallback")
-    f = tb.start[:3 * 16384 + 5].copy()
-    check_begins(f, 0, "fallback scalar")
+    with forced_fallback():
+        check_begins(tb.start, 0, "workload8 fallback")
+        f = tb.start[:3 * 16384 + 5].copy()
+        check_begins(f, 0, "fallback scalar")
 
 
 def test_begin_indices_misaligned_flags():
@@ -145,13 +145,13 @@ def test_sample_group_table_edge_cases():
     check_sample(D, bad, [0, 1, 2, 3, 4, 5, 0], 200, "bounds outside D")
 
 
-def test_sample_many_tiles_and_fallback(monkeypatch):
+def test_sample_many_tiles_and_fallback():
     """Row sums over many draw tiles, with the look-back's fallback forced
     (every awaited tile's sum computed by the waiting tile)."""
     tb = tapes.make_tbb(8, seed=34, n=300000, batch=200000, n_draws=150000, episodes=tapes._uniform_int(1, 3))
     check_sample(tb.D, tb.begins, tb.draws, tb.batch, "many tiles")
-    monkeypatch.setenv("MEMOROID_FALLBACK_POLLS", "0")
-    check_sample(tb.D, tb.begins, tb.draws, tb.batch, "many tiles fallback")
+    with forced_fallback():
+        check_sample(tb.D, tb.begins, tb.draws, tb.batch, "many tiles fallback")
 
 
 def test_sample_without_optional_outputs():
@@ -166,7 +166,7 @@ def test_sample_without_optional_outputs():
     assert mb.memoroid_workspace_prepare(ws.data_ptr(), ws.numel(), s) == mb.OK
     out = torch.empty((batch, tb.D.shape[1]), dtype=torch.float32, device=DEV)
     ost = torch.empty(batch, dtype=torch.uint8, device=DEV)
-    assert mb.memoroid_tbb_sample(D.data_ptr(), tb.D.shape[0], tb.D.shape[1] * 4, I.data_ptr(), I.numel(),
+    assert mb.memoroid_tbb_sample_prepared(D.data_ptr(), tb.D.shape[0], tb.D.shape[1] * 4, I.data_ptr(), I.numel(),
                                   dr.data_ptr(), K, batch, out.data_ptr(), ost.data_ptr(), None, None,
                                   ws.data_ptr(), ws.numel(), s) == mb.OK
     assert mb.memoroid_workspace_status(ws.data_ptr(), ws.numel(), s) == mb.OK

@@ -1,11 +1,19 @@
-"""The prepared-workspace protocol of the single-kernel entry points, through
-the C ABI: one preparation, then many calls with the same sizes and no
-initialisation in between (the descriptor words alternate between two banks
-from call to call, so four calls use each bank twice); return and GAE calls
-interleaved on their own workspaces; a call with other sizes on a bound workspace
-(stands down and reports MEMOROID_EMISMATCH); memory that was never prepared.
+"""Workspaces through the C ABI.
+
+Prepared protocol (the *_prepared entry points, one kernel per call): one
+preparation, then many calls with the same sizes and no initialisation in
+between (the descriptor words alternate between two banks from call to
+call, so four calls use each bank twice); return and GAE calls interleaved
+on their own workspaces; a call with other sizes on a bound workspace
+(stands down and reports MEMOROID_EMISMATCH); memory that was never
+prepared.
+
+Self-initialising protocol (the default entry points): workspaces holding
+arbitrary bytes, bound by a prepared call, or shared by different entry
+points and sizes one call after another.
+
 Every result is compared with the fp64 oracle (conditioned relative error,
-1e-4 for fp32 arithmetic; indices bit-exact)."""
+1e-4 for fp32 arithmetic; indices and TBB outputs bit-exact)."""
 import numpy as np
 import pytest
 
@@ -45,7 +53,7 @@ def diag_call(w, ws, idx=None):
     code = {"f32": mb.F32, "c64": mb.C64}[w.dtype]
     a, x, s = dev(w.a), dev(w.x), dev(w.start)
     h = torch.empty((w.B, w.T, w.d), dtype=x.dtype, device=DEV)
-    st = mb.memoroid_scan_diag(a.data_ptr(), 0 if w.a_invariant else w.d, x.data_ptr(), s.data_ptr(), h.data_ptr(),
+    st = mb.memoroid_scan_diag_prepared(a.data_ptr(), 0 if w.a_invariant else w.d, x.data_ptr(), s.data_ptr(), h.data_ptr(),
                                idx.data_ptr() if idx is not None else None, w.B, w.T, w.d, code, code,
                                ws.data_ptr(), ws.numel(), stream())
     assert st == mb.OK
@@ -84,7 +92,7 @@ def test_diag_reverse_repeated_calls(dtype, a_inv, B, T, d):
         a, s, hd, g = dev(w.a), dev(w.start), dev(h32), dev(w.g)
         gx = torch.empty_like(g)
         ga = torch.empty((d,) if a_inv else (B, T, d), dtype=g.dtype, device=DEV)
-        st = mb.memoroid_scan_diag_bwd(a.data_ptr(), 0 if a_inv else d, s.data_ptr(), hd.data_ptr(), g.data_ptr(),
+        st = mb.memoroid_scan_diag_bwd_prepared(a.data_ptr(), 0 if a_inv else d, s.data_ptr(), hd.data_ptr(), g.data_ptr(),
                                        gx.data_ptr(), ga.data_ptr(), B, T, d, code, ws.data_ptr(), ws.numel(),
                                        stream())
         assert st == mb.OK
@@ -104,7 +112,7 @@ def test_ffm_forward_and_gradient_repeated_calls():
         announce("workspace ffm call %d" % call)
         al, om, x, s = dev(f.alpha), dev(f.omega), dev(f.x), dev(f.start)
         S = torch.empty((B, T, m, c), dtype=torch.complex64, device=DEV)
-        assert mb.memoroid_scan_ffm(al.data_ptr(), om.data_ptr(), x.data_ptr(), s.data_ptr(), S.data_ptr(), None,
+        assert mb.memoroid_scan_ffm_prepared(al.data_ptr(), om.data_ptr(), x.data_ptr(), s.data_ptr(), S.data_ptr(), None,
                                     B, T, m, c, wsf.data_ptr(), wsf.numel(), stream()) == mb.OK
         rng = np.random.Generator(np.random.PCG64(800 + call))
         G = (rng.standard_normal((B, T, m, c), dtype=np.float32)
@@ -113,7 +121,7 @@ def test_ffm_forward_and_gradient_repeated_calls():
         gx = torch.empty((B, T, m), dtype=torch.float32, device=DEV)
         ga = torch.empty(m, dtype=torch.float32, device=DEV)
         gw = torch.empty(c, dtype=torch.float32, device=DEV)
-        assert mb.memoroid_scan_ffm_bwd(al.data_ptr(), om.data_ptr(), s.data_ptr(), S.data_ptr(), Gd.data_ptr(),
+        assert mb.memoroid_scan_ffm_bwd_prepared(al.data_ptr(), om.data_ptr(), s.data_ptr(), S.data_ptr(), Gd.data_ptr(),
                                         gx.data_ptr(), ga.data_ptr(), gw.data_ptr(), B, T, m, c, wsb.data_ptr(),
                                         wsb.numel(), stream()) == mb.OK
         torch.cuda.synchronize()
@@ -132,7 +140,7 @@ def test_ffm_forward_and_gradient_repeated_calls():
 def _return_call(tp, ws, B, T):
     r, s = dev(tp.r), dev(tp.start)
     out = torch.empty((B, T), dtype=torch.float32, device=DEV)
-    assert mb.memoroid_discounted_return(r.data_ptr(), s.data_ptr(), 0.97, out.data_ptr(), B, T, ws.data_ptr(),
+    assert mb.memoroid_discounted_return_prepared(r.data_ptr(), s.data_ptr(), 0.97, out.data_ptr(), B, T, ws.data_ptr(),
                                          ws.numel(), stream()) == mb.OK
     torch.cuda.synchronize()
     return out.cpu().numpy()
@@ -141,7 +149,7 @@ def _return_call(tp, ws, B, T):
 def _gae_call(tp, ws, B, T):
     r, v, vn, dn, s = dev(tp.r), dev(tp.v), dev(tp.vn), dev(tp.done), dev(tp.start)
     out = torch.empty((B, T), dtype=torch.float32, device=DEV)
-    assert mb.memoroid_gae(r.data_ptr(), v.data_ptr(), vn.data_ptr(), dn.data_ptr(), s.data_ptr(), 0.99, 0.95,
+    assert mb.memoroid_gae_prepared(r.data_ptr(), v.data_ptr(), vn.data_ptr(), dn.data_ptr(), s.data_ptr(), 0.99, 0.95,
                            out.data_ptr(), None, B, T, ws.data_ptr(), ws.numel(), stream()) == mb.OK
     torch.cuda.synchronize()
     return out.cpu().numpy()
@@ -186,7 +194,7 @@ def test_begin_indices_repeated_calls():
         s = dev(flags)
         idx = torch.empty(n, dtype=torch.int64, device=DEV)
         cnt = torch.empty(1, dtype=torch.int64, device=DEV)
-        assert mb.memoroid_tbb_begin_indices(s.data_ptr(), n, 5, idx.data_ptr(), cnt.data_ptr(), ws.data_ptr(),
+        assert mb.memoroid_tbb_begin_indices_prepared(s.data_ptr(), n, 5, idx.data_ptr(), cnt.data_ptr(), ws.data_ptr(),
                                              ws.numel(), stream()) == mb.OK
         torch.cuda.synchronize()
         ref = oracle.tbb_begin_indices(flags, 5)
@@ -203,7 +211,7 @@ def _sample_call(tb, draws, batch, ws):
     ost = torch.empty(batch, dtype=torch.uint8, device=DEV)
     osrc = torch.empty(batch, dtype=torch.int64, device=DEV)
     filled = torch.full((1,), -3, dtype=torch.int64, device=DEV)
-    assert mb.memoroid_tbb_sample(D.data_ptr(), tb.D.shape[0], row_bytes, I.data_ptr(), I.numel(), dr.data_ptr(),
+    assert mb.memoroid_tbb_sample_prepared(D.data_ptr(), tb.D.shape[0], row_bytes, I.data_ptr(), I.numel(), dr.data_ptr(),
                                   dr.numel(), batch, out.data_ptr(), ost.data_ptr(), osrc.data_ptr(),
                                   filled.data_ptr(), ws.data_ptr(), ws.numel(), stream()) == mb.OK
     torch.cuda.synchronize()
@@ -268,7 +276,7 @@ def test_unprepared_workspace_computes_nothing():
     announce("workspace unprepared")
     a, x, s = dev(w.a), dev(w.x), dev(w.start)
     h = torch.full((1, 3000, 16), 7.0, dtype=torch.float32, device=DEV)
-    assert mb.memoroid_scan_diag(a.data_ptr(), 0, x.data_ptr(), s.data_ptr(), h.data_ptr(), None, 1, 3000, 16,
+    assert mb.memoroid_scan_diag_prepared(a.data_ptr(), 0, x.data_ptr(), s.data_ptr(), h.data_ptr(), None, 1, 3000, 16,
                                  mb.F32, mb.F32, ws.data_ptr(), ws.numel(), stream()) == mb.OK
     assert status(ws) == mb.EMISMATCH
     assert bool((h == 7.0).all())
@@ -285,3 +293,172 @@ def test_binding_cache_reuses_prepared_workspaces():
         h = mb.scan_diag(a, x, s)
         torch.cuda.synchronize()
         assert cond_err(h.cpu().numpy(), ref, m) <= TOL, call
+
+
+# ------------------------------------------------- self-initialising calls
+
+
+def garbage(nbytes, seed):
+    """Workspace memory holding arbitrary bytes."""
+    g = torch.Generator().manual_seed(seed)
+    return torch.randint(0, 256, (max(nbytes, 256),), dtype=torch.uint8, generator=g).to(DEV)
+
+
+def _diag_default(w, ws, idx=None):
+    code = {"f32": mb.F32, "c64": mb.C64}[w.dtype]
+    a, x, s = dev(w.a), dev(w.x), dev(w.start)
+    h = torch.full((w.B, w.T, w.d), 7.0, dtype=x.dtype, device=DEV)
+    st = mb.memoroid_scan_diag(a.data_ptr(), 0 if w.a_invariant else w.d, x.data_ptr(), s.data_ptr(), h.data_ptr(),
+                               idx.data_ptr() if idx is not None else None, w.B, w.T, w.d, code, code,
+                               ws.data_ptr(), ws.numel(), stream())
+    assert st == mb.OK
+    torch.cuda.synchronize()
+    return h.cpu().numpy()
+
+
+def _diag_bwd_default(w, ws):
+    code = {"f32": mb.F32, "c64": mb.C64}[w.dtype]
+    h, _ = oracle.diag_fwd(w.a, w.x, w.start)
+    h32 = h.astype(w.x.dtype)
+    a, s, hd, g = dev(w.a), dev(w.start), dev(h32), dev(w.g)
+    gx = torch.empty_like(g)
+    ga = torch.empty((w.d,) if w.a_invariant else (w.B, w.T, w.d), dtype=g.dtype, device=DEV)
+    st = mb.memoroid_scan_diag_bwd(a.data_ptr(), 0 if w.a_invariant else w.d, s.data_ptr(), hd.data_ptr(),
+                                   g.data_ptr(), gx.data_ptr(), ga.data_ptr(), w.B, w.T, w.d, code, ws.data_ptr(),
+                                   ws.numel(), stream())
+    assert st == mb.OK
+    torch.cuda.synchronize()
+    dx, da, mdx, mda = oracle.diag_bwd(w.a, w.start, h32, w.g)
+    return cond_err(gx.cpu().numpy(), dx, mdx), cond_err(ga.cpu().numpy(), da, mda)
+
+
+@pytest.mark.parametrize("dtype,a_inv,d", [("f32", False, 40), ("c64", True, 64), ("f32", True, 7)])
+def test_self_initialising_diag_on_garbage_then_smaller_then_foreign(dtype, a_inv, d):
+    """The default entry points need no preparation: a workspace holding
+    arbitrary bytes, then the same workspace for a smaller tape, then after
+    a reverse scan used it, always gives the oracle's results."""
+    code = {"f32": mb.F32, "c64": mb.C64}[dtype]
+    big = max(mb.memoroid_workspace_bytes(mb.OP_DIAG, 2, 9000, d, 0, 0, 0),
+              mb.memoroid_workspace_bytes(mb.OP_DIAG_BWD, 2, 9000, d, 0, 0, 0))
+    assert big >= mb.memoroid_scan_diag_workspace_bytes(2, 9000, d, code, code)
+    ws = garbage(big, 7)
+    for call, (B, T) in enumerate(((2, 9000), (1, 2500), (2, 9000))):
+        w = tapes.make_custom_diag(dtype, B, T, d, a_inv, seed=1500 + call)
+        announce("self-init diag fwd %s B=%d T=%d d=%d call %d" % (dtype, B, T, d, call))
+        idx = torch.empty((B, T), dtype=torch.int32, device=DEV)
+        ref, m = oracle.diag_fwd(w.a, w.x, w.start)
+        assert cond_err(_diag_default(w, ws, idx), ref, m) <= TOL, call
+        np.testing.assert_array_equal(idx.cpu().numpy(), oracle.episode_idx(w.start))
+        announce("self-init diag bwd %s B=%d T=%d d=%d call %d" % (dtype, B, T, d, call))
+        e_dx, e_da = _diag_bwd_default(w, ws)
+        assert e_dx <= TOL and e_da <= TOL, call
+
+
+def test_self_initialising_call_on_a_bound_prepared_workspace():
+    """A workspace bound by a prepared call to other sizes is just memory to
+    a self-initialising call."""
+    d = 32
+    ws = prepared(mb.memoroid_workspace_bytes(mb.OP_DIAG, 1, 6000, d, 0, 0, 0))
+    w1 = tapes.make_custom_diag("f32", 1, 6000, d, False, seed=1601, with_grad=False)
+    w2 = tapes.make_custom_diag("f32", 1, 4000, d, False, seed=1602, with_grad=False)
+    announce("self-init after a prepared bind")
+    ref1, m1 = oracle.diag_fwd(w1.a, w1.x, w1.start)
+    assert cond_err(diag_call(w1, ws), ref1, m1) <= TOL
+    assert status(ws) == mb.OK
+    ref2, m2 = oracle.diag_fwd(w2.a, w2.x, w2.start)
+    assert cond_err(_diag_default(w2, ws), ref2, m2) <= TOL
+
+
+def test_self_initialising_ffm_return_gae_and_tbb_share_one_garbage_workspace():
+    """Every other self-initialising entry point on one workspace of
+    arbitrary bytes, one after another and again with smaller sizes."""
+    B, T, m, c = 1, 9000, 8, 4
+    n, batch, K = 200000, 60000, 40000
+    need = max(mb.memoroid_workspace_bytes(mb.OP_FFM, B, T, m, c, 0, 0),
+               mb.memoroid_workspace_bytes(mb.OP_FFM_BWD, B, T, m, c, 0, 0),
+               mb.memoroid_workspace_bytes(mb.OP_RETURN, 2, 70000, 0, 0, 0, 0),
+               mb.memoroid_workspace_bytes(mb.OP_GAE, 2, 70000, 0, 0, 0, 0),
+               mb.memoroid_workspace_bytes(mb.OP_TBB_BEGIN_INDICES, 0, n, 0, 0, 0, 0),
+               mb.memoroid_workspace_bytes(mb.OP_TBB_SAMPLE, K, batch, 0, 0, 0, 0))
+    ws = garbage(need, 11)
+    for call, shrink in enumerate((1, 2)):
+        Tf = T // shrink
+        f = tapes.make_ffm(7, seed=1700 + call, B=B, T=Tf, m=m, c=c)
+        announce("self-init ffm T=%d" % Tf)
+        al, om, x, s = dev(f.alpha), dev(f.omega), dev(f.x), dev(f.start)
+        S = torch.empty((B, Tf, m, c), dtype=torch.complex64, device=DEV)
+        assert mb.memoroid_scan_ffm(al.data_ptr(), om.data_ptr(), x.data_ptr(), s.data_ptr(), S.data_ptr(), None,
+                                    B, Tf, m, c, ws.data_ptr(), ws.numel(), stream()) == mb.OK
+        torch.cuda.synchronize()
+        ref, mag = oracle.ffm(f.alpha.astype(np.float64), f.omega.astype(np.float64), f.x.astype(np.float64),
+                              f.start)
+        Sg = S.cpu().numpy()
+        assert cond_err(Sg, ref, mag) <= TOL, call
+        rng = np.random.Generator(np.random.PCG64(1800 + call))
+        G = (rng.standard_normal((B, Tf, m, c), dtype=np.float32)
+             + 1j * rng.standard_normal((B, Tf, m, c), dtype=np.float32)).astype(np.complex64)
+        Gd = dev(G)
+        gx = torch.empty((B, Tf, m), dtype=torch.float32, device=DEV)
+        ga = torch.empty(m, dtype=torch.float32, device=DEV)
+        gw = torch.empty(c, dtype=torch.float32, device=DEV)
+        announce("self-init ffm grad T=%d" % Tf)
+        assert mb.memoroid_scan_ffm_bwd(al.data_ptr(), om.data_ptr(), s.data_ptr(), S.data_ptr(), Gd.data_ptr(),
+                                        gx.data_ptr(), ga.data_ptr(), gw.data_ptr(), B, Tf, m, c, ws.data_ptr(),
+                                        ws.numel(), stream()) == mb.OK
+        torch.cuda.synchronize()
+        rdx, rda, rdw, mdx, mda, mdw = oracle.ffm_bwd(f.alpha.astype(np.float64), f.omega.astype(np.float64),
+                                                      f.start, Sg.astype(np.complex128), G.astype(np.complex128))
+        assert cond_err(gx.cpu().numpy(), rdx, mdx) <= TOL, call
+        assert cond_err(ga.cpu().numpy(), rda, mda) <= TOL, call
+        assert cond_err(gw.cpu().numpy(), rdw, mdw) <= TOL, call
+
+        Td = 70000 // shrink
+        tp = tapes.make_discount(6, seed=1900 + call, B=2, T=Td)
+        announce("self-init return / gae T=%d" % Td)
+        r, st_, v, vn, dn = dev(tp.r), dev(tp.start), dev(tp.v), dev(tp.vn), dev(tp.done)
+        out = torch.empty((2, Td), dtype=torch.float32, device=DEV)
+        assert mb.memoroid_discounted_return(r.data_ptr(), st_.data_ptr(), 0.97, out.data_ptr(), 2, Td,
+                                             ws.data_ptr(), ws.numel(), stream()) == mb.OK
+        torch.cuda.synchronize()
+        ref, mr = oracle.discounted_return(tp.r.astype(np.float64), tp.start, float(np.float32(0.97)))
+        assert cond_err(out.cpu().numpy(), ref, mr) <= TOL, call
+        assert mb.memoroid_gae(r.data_ptr(), v.data_ptr(), vn.data_ptr(), dn.data_ptr(), st_.data_ptr(), 0.99, 0.95,
+                               out.data_ptr(), None, 2, Td, ws.data_ptr(), ws.numel(), stream()) == mb.OK
+        torch.cuda.synchronize()
+        ref, _, mr, _ = oracle.gae(tp.r.astype(np.float64), tp.v.astype(np.float64), tp.start,
+                                   float(np.float32(0.99)), float(np.float32(0.95)),
+                                   vn=tp.vn.astype(np.float64), done=tp.done)
+        assert cond_err(out.cpu().numpy(), ref, mr) <= TOL, call
+
+        nn = n // shrink
+        rng = np.random.Generator(np.random.PCG64(2000 + call))
+        flags = (rng.random(nn) < 0.01).astype(np.uint8)
+        announce("self-init begin indices n=%d" % nn)
+        sf = dev(flags)
+        idx = torch.empty(nn, dtype=torch.int64, device=DEV)
+        cnt = torch.empty(1, dtype=torch.int64, device=DEV)
+        assert mb.memoroid_tbb_begin_indices(sf.data_ptr(), nn, 5, idx.data_ptr(), cnt.data_ptr(), ws.data_ptr(),
+                                             ws.numel(), stream()) == mb.OK
+        torch.cuda.synchronize()
+        refi = oracle.tbb_begin_indices(flags, 5)
+        assert int(cnt.item()) == refi.size
+        np.testing.assert_array_equal(idx.cpu().numpy()[:refi.size], refi)
+
+        tb = tapes.make_tbb(8, seed=2100 + call, n=n, batch=batch, n_draws=K)
+        kk, bb = K // shrink, batch // shrink
+        draws = np.random.Generator(np.random.PCG64(2200 + call)).integers(0, tb.begins.size, size=kk)
+        announce("self-init sample draws=%d batch=%d" % (kk, bb))
+        D, I, dr = dev(tb.D), dev(tb.begins), dev(np.asarray(draws, np.int64))
+        o = torch.empty((bb, tb.D.shape[1]), dtype=torch.float32, device=DEV)
+        ost = torch.empty(bb, dtype=torch.uint8, device=DEV)
+        osrc = torch.empty(bb, dtype=torch.int64, device=DEV)
+        filled = torch.empty(1, dtype=torch.int64, device=DEV)
+        assert mb.memoroid_tbb_sample(D.data_ptr(), tb.D.shape[0], tb.D.shape[1] * 4, I.data_ptr(), I.numel(),
+                                      dr.data_ptr(), kk, bb, o.data_ptr(), ost.data_ptr(), osrc.data_ptr(),
+                                      filled.data_ptr(), ws.data_ptr(), ws.numel(), stream()) == mb.OK
+        torch.cuda.synchronize()
+        r_out, r_st, r_src, r_filled = oracle.tbb_sample(tb.D, tb.begins, draws, bb)
+        assert int(filled.item()) == r_filled
+        np.testing.assert_array_equal(osrc.cpu().numpy(), r_src)
+        np.testing.assert_array_equal(ost.cpu().numpy(), r_st)
+        assert np.array_equal(o.cpu().numpy().view(np.uint8), r_out.view(np.uint8))
