@@ -174,6 +174,39 @@ int memoroid_scan_diag_prepared(const void* a, int64_t a_stride_t,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * memoroid_scan_diag for callers that cannot allocate device memory or own
+ * a workspace: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  Same arguments and results as memoroid_scan_diag
+ * without the workspace: the call uses a fixed scratch array of
+ * MEMOROID_NOALLOC_SCRATCH_BYTES inside the library (device memory that each
+ * GPU the library runs on holds from the library's load until the process
+ * ends), initialises what it needs of it on `stream` (a fill kernel, no
+ * memset), and calls no hipMalloc, hipFree or other allocating routine.  The
+ * first call with a device current looks up that device's copy of the
+ * array once.
+ *
+ * Limit: a call whose tiling needs more than MEMOROID_NOALLOC_SCRATCH_BYTES
+ * of workspace returns MEMOROID_EWORKSPACE and enqueues nothing.  Every
+ * problem for which memoroid_scan_diag_workspace_bytes(...) is at most that
+ * size is accepted (2^20 steps x 256 fp32 features, for example).  The
+ * vectorised kernels (16-byte aligned tensors, d a multiple of the vector
+ * width) need a quarter of that query's size or less, so e.g. 64 tapes x
+ * 16384 steps x 512 bf16 features fits on them too.
+ *
+ * Every call on one GPU shares that GPU's array: calls that overlap in time
+ * on one GPU (on different streams, or from different threads) race and
+ * must be serialised by the caller.  The array keeps the last call's
+ * contents, which the next call re-initialises.
+ * ------------------------------------------------------------------------ */
+#define MEMOROID_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+int memoroid_scan_diag_noalloc(const void* a, int64_t a_stride_t,
+                               const void* x, const uint8_t* start,
+                               void* h, int32_t* episode_idx,
+                               int64_t B, int64_t T, int64_t d,
+                               int in_dtype, int out_dtype, void* stream);
+
+/* ------------------------------------------------------------------------
  * Diagonal linear memoroid, reverse scan (gradients).
  *
  * The paper differentiates through the scan with automatic differentiation;

@@ -103,6 +103,8 @@ def lib() -> ctypes.CDLL:
             fp = getattr(L, name + "_prepared")
             fp.restype = I32
             fp.argtypes = getattr(L, name).argtypes
+        L.memoroid_scan_diag_noalloc.restype = I32
+        L.memoroid_scan_diag_noalloc.argtypes = [P, I64, P, P, P, P, I64, I64, I64, I32, I32, P]
         L.memoroid_workspace_bytes.restype = SZ
         L.memoroid_workspace_bytes.argtypes = [I32, I64, I64, I64, I64, I64, I64]
         L.memoroid_testing_set_fallback_polls.restype = I64
@@ -156,6 +158,15 @@ def memoroid_scan_diag_prepared(a, a_stride_t, x, start, h, episode_idx, B, T, d
                                 workspace, workspace_bytes, stream) -> int:
     return lib().memoroid_scan_diag_prepared(a, a_stride_t, x, start, h, episode_idx, B, T, d, in_dtype,
                                              out_dtype, workspace, workspace_bytes, stream)
+
+
+def memoroid_scan_diag_noalloc(a, a_stride_t, x, start, h, episode_idx, B, T, d, in_dtype, out_dtype,
+                               stream) -> int:
+    return lib().memoroid_scan_diag_noalloc(a, a_stride_t, x, start, h, episode_idx, B, T, d, in_dtype,
+                                            out_dtype, stream)
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20    # MEMOROID_NOALLOC_SCRATCH_BYTES
 
 
 def memoroid_scan_diag_bwd_workspace_bytes(B, T, d, dtype, a_stride_t) -> int:

@@ -3,6 +3,7 @@
 // and kernel launches.
 #include <limits.h>
 #include <atomic>
+#include <mutex>
 #include <initializer_list>
 #include <stdlib.h>
 #include <string.h>
@@ -142,11 +143,46 @@ int check_hip(hipError_t e) { return e == hipSuccess ? MEMOROID_OK : MEMOROID_EH
 // bytes, which is exactly the state memoroid_workspace_prepare leaves; the
 // kernels then run as the first call on a prepared workspace.  A prepared
 // call launches the kernels alone.
-enum class WsMode { kSelfInit, kPrepared };
+// kNoAlloc: self-initialising, on the library's own static scratch array
+// instead of a caller's workspace (memoroid_scan_diag_noalloc).
+enum class WsMode { kSelfInit, kPrepared, kNoAlloc };
 
 int init_if_self(WsMode mode, void* ws, size_t init_bytes, hipStream_t s) {
-    if (mode != WsMode::kSelfInit) return MEMOROID_OK;
+    if (mode == WsMode::kPrepared) return MEMOROID_OK;
     return check_hip(ws_init_launch(nullptr, 0, ws, init_bytes, s));
+}
+
+}  // namespace
+
+// ---------------------------------------------------------- static scratch
+// Workspace of memoroid_scan_diag_noalloc: one fixed array in device memory,
+// held by every GPU that the library runs on until the process ends.  In
+// host code `scratch` names a host-side stand-in, never the device array:
+// host code uses only the address hipGetSymbolAddress returns for the
+// current device (each GPU holds its own copy at its own address).
+constexpr size_t kNoAllocScratchBytes = MEMOROID_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+// Device address of the current device's scratch array, looked up on the
+// first call made with that device current and kept.
+int scratch_address(void** out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return MEMOROID_EHIP;
+    if (dev < 0 || dev >= kMaxDevices) return MEMOROID_EUNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return MEMOROID_EHIP;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return MEMOROID_OK;
 }
 
 // Workspace fields of a diagonal scan's arguments: counters and bank-0
@@ -244,10 +280,20 @@ static int scan_diag_run(const void* a, int64_t a_stride_t, const void* x, const
     const int sd = in_dtype == MEMOROID_C64 ? MEMOROID_C64 : (in_dtype == MEMOROID_BF16 ? MEMOROID_BF16 : MEMOROID_F32);
     DiagPlan p;
     if (!plan_diag(B, T, d, sd, vec, diag_rows(false, ainv), false, ainv, false, &p)) return MEMOROID_EUNSUPPORTED;
-    if (!workspace) return MEMOROID_EWORKSPACE;
-    if (workspace_bytes < memoroid_scan_diag_workspace_bytes(B, T, d, in_dtype, out_dtype) ||
-        workspace_bytes < p.total)
-        return MEMOROID_EWORKSPACE;
+    if (mode == WsMode::kNoAlloc) {
+        // the plan's own size (the scratch array is never shared with
+        // another plan's call in flight, so the query's maximum over plans
+        // is not needed)
+        if (p.total > kNoAllocScratchBytes) return MEMOROID_EWORKSPACE;
+        const int st = scratch_address(&workspace);
+        if (st != MEMOROID_OK) return st;
+        workspace_bytes = kNoAllocScratchBytes;
+    } else {
+        if (!workspace) return MEMOROID_EWORKSPACE;
+        if (workspace_bytes < memoroid_scan_diag_workspace_bytes(B, T, d, in_dtype, out_dtype) ||
+            workspace_bytes < p.total)
+            return MEMOROID_EWORKSPACE;
+    }
     if (!aligned(workspace, 16)) return MEMOROID_EINVAL;
 
     hipStream_t s = (hipStream_t)stream;
@@ -285,6 +331,13 @@ int memoroid_scan_diag_prepared(const void* a, int64_t a_stride_t, const void* x
                                 int out_dtype, void* workspace, size_t workspace_bytes, void* stream) {
     return scan_diag_run(a, a_stride_t, x, start, h, episode_idx, B, T, d, in_dtype, out_dtype, workspace,
                          workspace_bytes, stream, WsMode::kPrepared);
+}
+
+int memoroid_scan_diag_noalloc(const void* a, int64_t a_stride_t, const void* x, const uint8_t* start, void* h,
+                               int32_t* episode_idx, int64_t B, int64_t T, int64_t d, int in_dtype, int out_dtype,
+                               void* stream) {
+    return scan_diag_run(a, a_stride_t, x, start, h, episode_idx, B, T, d, in_dtype, out_dtype, nullptr, 0, stream,
+                         WsMode::kNoAlloc);
 }
 
 // ------------------------------------------------------------------- FFM

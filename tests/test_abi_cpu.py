@@ -330,3 +330,23 @@ def test_torch_layer_rejects_cpu_tensors():
     a = torch.rand(4, 8)
     with pytest.raises(ValueError):
         mb.scan_diag(a, torch.rand(4, 8), torch.zeros(4, dtype=torch.uint8))
+
+
+def test_noalloc_rejects_before_any_hip_call():
+    """memoroid_scan_diag_noalloc validates like memoroid_scan_diag and
+    rejects a tiling larger than its fixed scratch array with EWORKSPACE,
+    all before touching the GPU."""
+    def na(**kw):
+        args = dict(a=A, a_stride_t=8, x=X, start=S, h=H, episode_idx=None, B=2, T=100, d=8,
+                    in_dtype=mb.F32, out_dtype=mb.F32, stream=None)
+        args.update(kw)
+        return mb.memoroid_scan_diag_noalloc(*args.values())
+    assert na(B=-1) == mb.EINVAL and na(T=0) == mb.OK and na(d=0) == mb.OK
+    assert na(in_dtype=mb.F32, out_dtype=mb.BF16) == mb.EUNSUPPORTED
+    assert na(h=X) == mb.EINVAL and na(x=None) == mb.EINVAL and na(a_stride_t=3) == mb.EINVAL
+    # 64 tapes x 65536 steps x 512 bf16 features: about 4 x 48 MiB of tiles' words
+    assert na(B=64, T=65536, d=512, a_stride_t=512, in_dtype=mb.BF16, out_dtype=mb.BF16) == mb.EWORKSPACE
+    assert na(B=1, T=1 << 24, d=256, a_stride_t=256) == mb.EWORKSPACE
+    assert mb.memoroid_scan_diag_workspace_bytes(1, 1 << 20, 256, mb.F32, mb.F32) <= mb.NOALLOC_SCRATCH_BYTES
+    m = re.search(r"#define MEMOROID_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", open(HEADER).read())
+    assert m and int(m.group(1)) << int(m.group(2)) == mb.NOALLOC_SCRATCH_BYTES
