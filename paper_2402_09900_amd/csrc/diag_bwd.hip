@@ -126,11 +126,12 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
         if (want_da) raw_bload(rh[r], rs_h, h_back ? off : off - step);
     }
     __builtin_amdgcn_sched_barrier(0);
-    uint32_t ends = 0, begins = 0;
+    uint32_t ends = 0, begins = 0, valid = 0;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         const int64_t t = row0 + r;
         const uint32_t in = t < T ? 1u : 0u;
+        valid |= in << r;
         begins |= (in & ((t == 0 ? 1u : 0u) | (fl[r] != 0u ? 1u : 0u))) << r;
         ends |= (in & ((t + 1 == T ? 1u : 0u) | (fl[r + 1] != 0u ? 1u : 0u))) << r;
     }
@@ -252,14 +253,16 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
 #pragma unroll
         for (int r = R - 1; r >= 0; --r) {
             const bool e = (ends >> r) & 1u;
-            const bool bg = (begins >> r) & 1u;
+            // no da at a begin step, nor past T: there lam is 0, but the
+            // step T reads h_{T-1}, and 0 * Inf would reach the sum
+            const bool no_da = ((begins | ~valid) >> r) & 1u;
 #pragma unroll
             for (int v = 0; v < VEC; ++v) {
                 const S gv = C::get(rg[r], v);
                 lam[v] = e ? gv : mad(coef(r, v), lam[v], gv);
-                const S dav = bg ? s_zero<S>() : lam[v] * conj(C::get(rh[r], v));
+                const S dav = no_da ? s_zero<S>() : lam[v] * conj(C::get(rh[r], v));
                 if constexpr (AINV) {
-                    dsum[v] = dsum[v] + dav;             // zero past T (h reads zeros there)
+                    dsum[v] = dsum[v] + dav;
                 } else {
                     C::put(ra[r], v, dav);
                 }

@@ -384,6 +384,33 @@ __device__ __forceinline__ void grad_mfma_kblocks(const float* sA, const float* 
     }
 }
 
+// any value of the fetched rows that is not finite
+__device__ __forceinline__ bool grad_nonfinite(const f32x4 (&v)[kGradPer]) {
+    bool bad = false;
+#pragma unroll
+    for (int u = 0; u < kGradPer; ++u) bad |= !finite4(v[u]);
+    return bad;
+}
+
+// Products of a causal factor P (masked to the episodes: exact zeros outside
+// them) with a row operand Y, summed over each row's own episode only, for
+// chunks holding a value that is not finite, where the dense product would
+// carry it to other episodes through 0 * NaN.  Both tiles are rotated.
+//   rows of P:    out[i][col] = sum over j in [lo_i, i]   of P[i][j] Y[j][col]
+//   columns of P: out[j][col] = sum over i in [j, end_j)  of P[i][j] Y[i][col]
+// (lo_i: row i's episode start in the chunk; end_j: the first begin after
+// row j, or the chunk's valid rows).
+__device__ __forceinline__ float episode_row_sum(const float* sP, const float* sY, int i, int lo, int col) {
+    float acc = 0.0f;
+    for (int j = lo; j <= i; ++j) acc += sP[i * kLD + rot_col(i, j)] * sY[j * kLD + rot_col(j, col)];
+    return acc;
+}
+__device__ __forceinline__ float episode_col_sum(const float* sP, const float* sY, int j, int end, int col) {
+    float acc = 0.0f;
+    for (int i = j; i < end; ++i) acc += sP[i * kLD + rot_col(i, j)] * sY[i * kLD + rot_col(i, col)];
+    return acc;
+}
+
 __device__ __forceinline__ void zero2(f32x4 (&acc)[2]) {
     acc[0] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     acc[1] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
@@ -399,7 +426,10 @@ __device__ __forceinline__ void zero2(f32x4 (&acc)[2]) {
 // The state products are skipped by wavefronts none of whose rows take them
 // (dK2, dV2: rows at or after the chunk's last begin; dQ2: rows before its
 // first), dP, A skip their column tiles above the diagonal, and dQ1, dK1,
-// dV1 the k-blocks where their causal factor is zero.
+// dV1 the k-blocks where their causal factor is zero.  A chunk whose phi(K),
+// phi(Q) or dnum holds a value that is not finite forms dQ1, dK1 and dV1 as
+// explicit sums over each row's own episode instead (the masked factor's
+// zeros would otherwise meet that value in the dense product).
 __global__ __launch_bounds__(kGradThreads, 2) void linattn_bwd_grad_kernel(LinBwdArgs p) {
     __shared__ __attribute__((aligned(16))) float X0[kC * kLD];   // U_out [kd][n], then phi(Q), then S_in^T [n][kd]
     __shared__ __attribute__((aligned(16))) float X1[kC * kLD];   // phi(K)
@@ -466,7 +496,9 @@ __global__ __launch_bounds__(kGradThreads, 2) void linattn_bwd_grad_kernel(LinBw
             accP[jj][r] = keep_ij(row, col, ri[r], nvalid) ? accP[jj][r] + dd[r] : 0.0f;
         }
     grad_phi(qreg, nvalid);
-    __syncthreads();                                         // X0 (U_out), X2 (V) free
+    const bool nonfinite =
+        __syncthreads_or(grad_nonfinite(kreg) || grad_nonfinite(qreg) || grad_nonfinite(dnreg)) != 0;
+    // X0 (U_out), X2 (V) free
     grad_store(X0, qreg);
     grad_acc_to_lds(X2, accP, rb, ch);
     __syncthreads();
@@ -477,10 +509,32 @@ __global__ __launch_bounds__(kGradThreads, 2) void linattn_bwd_grad_kernel(LinBw
     zero2(accQ1);
     zero2(accK1);
     grad_mfma<true, true>(X0, X1, accA, rb, ch, rb);         // sum_kd Q[i][kd] K[j][kd]
-    // dP[i][j] = 0 for j > i: row block rb of dQ1 takes j < 16 rb + 16, and
-    // of dK1 (rows j) takes i >= 16 rb
-    grad_mfma_kblocks<true, false>(X2, X1, accQ1, rb, ch, 0, rb);    // sum_j dP[i][j] K[j][kd]
-    grad_mfma_kblocks<false, false>(X2, X0, accK1, rb, ch, rb, 3);   // sum_i dP[i][j] Q[i][kd]
+    // episode bounds of this lane's rows, for the explicit sums
+    int lo_r[4], end_r[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int row = 16 * rb + 4 * (lane >> 4) + r;
+        lo_r[r] = ri[r] > 0 ? ri[r] : 0;
+        const uint64_t later = row < 63 ? mb & ~((2ull << row) - 1ull) : 0ull;   // begins after row
+        end_r[r] = later ? __builtin_ctzll(later) : nvalid;
+    }
+    if (!nonfinite) {
+        // dP[i][j] = 0 for j > i: row block rb of dQ1 takes j < 16 rb + 16,
+        // and of dK1 (rows j) takes i >= 16 rb
+        grad_mfma_kblocks<true, false>(X2, X1, accQ1, rb, ch, 0, rb);    // sum_j dP[i][j] K[j][kd]
+        grad_mfma_kblocks<false, false>(X2, X0, accK1, rb, ch, rb, 3);   // sum_i dP[i][j] Q[i][kd]
+    } else {
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = 16 * rb + 4 * (lane >> 4) + r, col = 16 * (2 * ch + jj) + (lane & 15);
+                if (row < nvalid) {
+                    accQ1[jj][r] = episode_row_sum(X2, X1, row, lo_r[r], col);
+                    accK1[jj][r] = episode_col_sum(X2, X0, row, end_r[r], col);
+                }
+            }
+    }
     // this lane's accumulator elements (row, col): A masked; phi'(q) kept for
     // dq; dk (rows j, columns kd) written, with phi'(k) from phi(K)
     float pq[2][4];
@@ -505,7 +559,17 @@ __global__ __launch_bounds__(kGradThreads, 2) void linattn_bwd_grad_kernel(LinBw
     f32x4 accV1[2], accQ2[2];
     zero2(accV1);
     zero2(accQ2);
-    grad_mfma_kblocks<false, false>(X2, X3, accV1, rb, ch, rb, 3);   // sum_{i >= j} A[i][j] dnum[i][n]
+    if (!nonfinite) {
+        grad_mfma_kblocks<false, false>(X2, X3, accV1, rb, ch, rb, 3);   // sum_{i >= j} A[i][j] dnum[i][n]
+    } else {
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = 16 * rb + 4 * (lane >> 4) + r, col = 16 * (2 * ch + jj) + (lane & 15);
+                if (row < nvalid) accV1[jj][r] = episode_col_sum(X2, X3, row, end_r[r], col);
+            }
+    }
     if (have_s && 16 * rb < firstb) grad_mfma<true, false>(X3, X0, accQ2, rb, ch);   // sum_n dnum[i][n] S_in[kd][n]
 #pragma unroll
     for (int jj = 0; jj < 2; ++jj)

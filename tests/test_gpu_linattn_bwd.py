@@ -99,3 +99,38 @@ def test_autograd_function():
     assert cond_err(q.grad.cpu().numpy(), rq, mq) <= TOL
     assert cond_err(k.grad.cpu().numpy(), rk, mk) <= TOL
     assert cond_err(v.grad.cpu().numpy(), rv, mv) <= TOL
+
+
+def test_nonfinite_values_stay_in_their_episode():
+    """NaN in k, q, v and the upstream gradient, each inside one episode of a
+    chunk that holds other episodes: every element the oracle computes as
+    finite (the other episodes, and the steps of the same episode that do
+    not depend on the planted value) is finite on the GPU and within the
+    tolerance, and every element the oracle leaves non-finite is non-finite
+    (the reset theorem's barrier, carried by selects, for the gradient)."""
+    T, H = 5 * 64 + 9, 2
+    la = tapes.make_linattn(3, seed=91, T=T, H=H)
+    f = np.zeros(T, np.uint8)
+    f[[0, 70, 90, 100, 140, 200, 230, 260, 300]] = 1       # several episodes per chunk
+    la.start = f
+    g = grad_input(la, 9)
+    la.k[95, 0, 3] = np.nan        # episode [90, 100), chunk 1, head 0
+    la.q[150, 1, 5] = np.nan       # episode [140, 200), chunks 2-3, head 1
+    la.v[210, 0, 7] = np.nan       # episode [200, 230), chunk 3, head 0
+    g[245, 1, 11] = np.nan         # episode [230, 260), chunk 3, head 1
+    announce("linattn bwd non-finite T=%d H=%d" % (T, H))
+    q, k, v, s = dev(la.q), dev(la.k), dev(la.v), dev(la.start)
+    out = mb.scan_linattn(q, k, v, s)
+    gq, gk, gv = mb.scan_linattn_bwd(q, k, v, s, out, dev(g))
+    torch.cuda.synchronize()
+    ro, mo = oracle.linattn(la.q.astype(np.float64), la.k.astype(np.float64), la.v.astype(np.float64), la.start)
+    rq, rk, rv, mq, mk, mv = oracle.linattn_bwd(la.q.astype(np.float64), la.k.astype(np.float64),
+                                                la.v.astype(np.float64), la.start, g.astype(np.float64))
+    for name, got, ref, m in (("out", out, ro, mo), ("dq", gq, rq, mq), ("dk", gk, rk, mk), ("dv", gv, rv, mv)):
+        got = got.cpu().numpy()
+        fin = np.isfinite(ref)
+        assert (~fin).any(), name                       # the planted values reach their episodes
+        assert np.isfinite(got[fin]).all(), (name, np.argwhere(fin & ~np.isfinite(got))[:5])
+        assert not np.isfinite(got[~fin]).any(), name
+        e = cond_err(got[fin], ref[fin], m[fin])
+        assert e <= TOL, (name, e)

@@ -375,6 +375,23 @@ def test_nan_stays_in_its_episode():
     assert np.isfinite(gx[0, :700, 7]).all() and np.isfinite(gx[0, 1001:, 7]).all()
 
 
+@pytest.mark.parametrize("dtype", ["f32", "c64"])
+@pytest.mark.parametrize("B", [1, 2])
+def test_time_invariant_da_ignores_the_state_after_the_tape_end(dtype, B):
+    """With a time-invariant a the reverse scan sums da over the tape; the
+    saved state of the last step, h_{T-1}, enters no term of that sum.  A NaN
+    there (x NaN at the last step) must leave da finite, also when T is not
+    a multiple of the tile length (one tape: da summed in the kernel; two:
+    through the partial rows)."""
+    T, d = 1000 + 3, 16
+    w = tapes.make_custom_diag(dtype, B, T, d, True, seed=12 + B)
+    assert T % mb.memoroid_testing_tile_steps(1, B, T, d, mb.F32 if dtype == "f32" else mb.C64, 0, 1) != 0
+    w.x[:, T - 1, :] = np.nan
+    announce("bwd invariant-a da with NaN at h_{T-1} %s B=%d" % (dtype, B))
+    e_dx, e_da = check_bwd(w, label="NaN h at tape end")
+    assert e_dx <= TOL[dtype] and e_da <= TOL[dtype]
+
+
 def test_linattn_nan_stays_in_its_episode():
     la = tapes.make_linattn(T=640, seed=11)
     la.start[:] = 0
