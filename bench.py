@@ -385,7 +385,7 @@ def setup_tbb(torch, mb, tapes, key):
 
 def kernel_source_hash():
     """sha256 over the library's HIP sources (same recipe as
-    paper_2402_09900_amd/profsum.py), to tell whether recorded counters still apply."""
+    profsum.py), to tell whether recorded counters still apply."""
     import glob
     import hashlib
     hs = hashlib.sha256()

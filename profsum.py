@@ -1,10 +1,10 @@
 #!/usr/bin/env python3
 """Summaries of rocprofv3 output for the profiles/ folder.
 
-    python -m paper_2402_09900_amd.profsum trace  <kernel_trace results.db> <title> <command>
-    python -m paper_2402_09900_amd.profsum traffic <FETCH_SIZE results.db> <WRITE_SIZE results.db> <title> <command>
-    python -m paper_2402_09900_amd.profsum json <out.json> <command> <workload>=<FETCH db>,<WRITE db> ...
-    python -m paper_2402_09900_amd.profsum mfma <SQ counter db> <kernel trace db> <title> <command> <kernel>=<wavefronts> ...
+    python profsum.py trace  <kernel_trace results.db> <title> <command>
+    python profsum.py traffic <FETCH_SIZE results.db> <WRITE_SIZE results.db> <title> <command>
+    python profsum.py json <out.json> <command> <workload>=<FETCH db>,<WRITE db> ...
+    python profsum.py mfma <SQ counter db> <kernel trace db> <title> <command> <kernel>=<wavefronts> ...
 
 `trace` prints per-kernel dispatch counts and durations.  `traffic` prints,
 per kernel, the FETCH_SIZE / WRITE_SIZE counters (KiB per dispatch) and the
@@ -41,8 +41,9 @@ def trace(db, title, cmd):
                                                             min(v), max(v), 100 * sum(v) / tot))
     notes = []
     if any(k.startswith("memoroid::ws_init_kernel") for k in agg):
-        notes.append("`ws_init_kernel`: the one-time preparation of the prepared workspaces "
-                     "(memoroid_workspace_prepare), before the timed steps.")
+        notes.append("`ws_init_kernel`: the preparation of the prepared workspaces "
+                     "(memoroid_workspace_prepare) before the timed steps, and the workspace fills of the "
+                     "self-initialising steps bench.py times after them.")
     if COPY_KERNEL in agg:
         notes.append("`%s`: input uploads and the byte-counter calibration copy, before the timed steps."
                      % COPY_KERNEL)
@@ -184,7 +185,7 @@ def call_bytes(key, fdb, wdb):
 def write_json(out, cmd, specs):
     import json
     import os
-    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    root = os.path.dirname(os.path.abspath(__file__))
     rec = {"source_sha256": source_hash(root),
            "note": "bytes per library call: FETCH_SIZE + WRITE_SIZE of every kernel the call launches, "
                    "scaled by what the counters read for a 256 MiB device copy",
