@@ -32,6 +32,8 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     constexpr int NT = 256;
     constexpr int NW = NT / 64;
     constexpr int EB = KindInfo<K>::bytes;
+    // widest lane group of this kernel's plans: one chain row of VEC-wide lanes
+    constexpr int kQpMax = kChainRowBytes / (VEC * EB) > 0 ? (int)(kChainRowBytes / (VEC * EB)) : 1;
 
     __shared__ uint32_t s_ticket;          // place in the chain; all ones: stand down
     __shared__ uint32_t s_bank;
@@ -181,7 +183,7 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     // ---- scan the wavefront's groups (later groups first), then combine the
     // wavefront totals (later wavefronts first) through LDS
     SegT inc = own, exc;
-    wave_group_scan<S, VEC, true>(inc, exc, Qp);
+    wave_group_scan<S, VEC, true, kQpMax>(inc, exc, Qp);
     if (j == 0) {
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {
@@ -289,7 +291,7 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
                     float part = 0.0f;
 #pragma unroll
                     for (int v = 0; v < VEC; ++v) part += C::get(rg[r], v).re;
-                    for (int off = 1; off < (int)(cc / VEC); off <<= 1) part += __shfl_xor(part, off, 64);
+                    for (int off = 1; off < (int)(cc / VEC); off <<= 1) part += lanes_xor(part, off);
                     if (in && (q & ((int)(cc / VEC) - 1)) == 0) dxw[t * jpc + ((q * VEC) >> csh)] = part;
                 } else {
 #pragma unroll

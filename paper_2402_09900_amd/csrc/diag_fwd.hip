@@ -39,7 +39,8 @@
 // begin step (nothing older can reach past it), else as an aggregate -- while
 // the first wavefront looks back over predecessor tiles for the carry-in;
 // (5) the tile's inclusive prefix is published, and every lane replays its
-// steps from its carry-in and streams h out.  a and x are read from HBM once
+// steps from its carry-in and streams h out.  The cross-lane moves of (3)
+// and of the begin counts are DPP / swizzle / permlane butterflies.  a and x are read from HBM once
 // and h written once; cross-tile traffic is a few bytes per feature per tile.
 #include <type_traits>
 
@@ -59,6 +60,8 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     constexpr int NW = NT / 64;
     constexpr int IB = KindInfo<IN>::bytes;
     constexpr int OB = KindInfo<OUT>::bytes;
+    // widest lane group of this kernel's plans: one chain row of VEC-wide lanes
+    constexpr int kQpMax = kChainRowBytes / (VEC * IB) > 0 ? (int)(kChainRowBytes / (VEC * IB)) : 1;
 
     __shared__ uint32_t s_ticket;          // place in the chain; all ones: stand down
     __shared__ uint32_t s_bank;
@@ -223,16 +226,13 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     const uint32_t c_own = __builtin_popcount(begins);
     uint32_t c_inc = c_own;
     if (want_idx) {
-        for (int k = 1; k < Gw; k <<= 1) {
-            const uint32_t o = (uint32_t)__shfl((int)c_inc, j >= k ? lane - k * Qp : lane, 64);
-            if (j >= k) c_inc += o;
-        }
+        c_inc = lanes_prefix_sum(c_own, Qp);
         if (j == Gw - 1 && q == 0) sWC[wave] = c_inc;
     }
 
     // ---- (3) scan the wavefront's groups; combine wavefront totals in LDS
     SegT inc = own, exc;
-    wave_group_scan<S, VEC, false>(inc, exc, Qp);
+    wave_group_scan<S, VEC, false, kQpMax>(inc, exc, Qp);
     if (j == Gw - 1) {
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {

@@ -56,24 +56,76 @@ __device__ __forceinline__ float rmap_apply(const RMap& m, float after) {
     return m.f ? m.H : __builtin_fmaf(m.A, after, m.H);
 }
 
-__device__ __forceinline__ RMap rmap_shfl_down(const RMap& m, int k) {
-    return RMap{__shfl_down(m.A, k, 64), __shfl_down(m.H, k, 64), __shfl_down((int)m.f, k, 64) != 0};
+// the value of lane (l & ~(2M - 1)) | M (the first lane of the upper half
+// of each block of 2M lanes; see sk_move)
+template <int M>
+__device__ __forceinline__ RMap rmap_upper_first(const RMap& m) {
+    return RMap{sk_move<true, M, 1>(m.A), sk_move<true, M, 1>(m.H), sk_move<true, M, 1>((uint32_t)m.f) != 0u};
 }
 
-__device__ __forceinline__ RMap rmap_bcast(const RMap& m, int src) {
-    return RMap{__shfl(m.A, src, 64), __shfl(m.H, src, 64), __shfl((int)m.f, src, 64) != 0};
-}
-
-// Inclusive suffix composition over the wavefront: lane l ends with
-// m_l . m_{l+1} . ... . m_63.
-__device__ __forceinline__ RMap wave_suffix(RMap m) {
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int k = 1; k < 64; k <<= 1) {
-        const RMap o = rmap_shfl_down(m, k);
-        if (lane + k < 64) m = rmap_then(m, o);
+template <int M>
+__device__ __forceinline__ void suffix_steps(RMap& m) {
+    if constexpr (M < 64) {
+        const int lane = threadIdx.x & 63;
+        const RMap o = rmap_upper_first<M>(m);
+        const RMap n = rmap_then(m, o);
+        // component-wise selects (a select of whole structs would keep them
+        // in private memory)
+        const bool takes = (lane & M) == 0;
+        m.A = takes ? n.A : m.A;
+        m.H = takes ? n.H : m.H;
+        m.f = takes ? n.f : m.f;
+        suffix_steps<2 * M>(m);
     }
-    return m;
+}
+
+__device__ __forceinline__ float readlane_f(float v, int l) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+
+// The value of lane l + 1 (lane 63 gets its own): DPP row_shl:1 inside each
+// row of 16 lanes, and the next row's first lane, read as a scalar, for the
+// last lane of a row.  Called with every lane active (no ds_bpermute, whose
+// reads of a disabled lane would be undefined).
+__device__ __forceinline__ uint32_t lane_next(uint32_t v) {
+    const int lane = threadIdx.x & 63;
+    uint32_t r = (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x101, 0xF, 0xF, false);   // row_shl:1
+    const uint32_t n16 = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
+    const uint32_t n32 = (uint32_t)__builtin_amdgcn_readlane((int)v, 32);
+    const uint32_t n48 = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
+    r = lane == 15 ? n16 : r;
+    r = lane == 31 ? n32 : r;
+    r = lane == 47 ? n48 : r;
+    return r;
+}
+__device__ __forceinline__ float lane_next(float v) { return __uint_as_float(lane_next(__float_as_uint(v))); }
+
+// Suffix composition over the wavefront: `exc` gets m_{l+1} . ... . m_63
+// (the lanes after lane l; identity for lane 63) and `total` m_0 . ... .
+// m_63 (the same in every lane).  A Sklansky scan towards lane 0: at step
+// M the lower half of each block of 2M lanes (earlier steps) appends the
+// upper half's total, which the upper half's first lane holds -- one partner
+// move (ds_swizzle within 32 lanes, a scalar lane read across the halves)
+// and one combine per step, no LDS memory; the exclusive suffix is the next
+// lane's (lane_next) and the total lane 0's (a scalar read).
+__device__ __forceinline__ void wave_suffix(const RMap& m0, RMap& exc, RMap& total) {
+    const int lane = threadIdx.x & 63;
+    RMap m = m0;
+    suffix_steps<1>(m);
+    const float na = lane_next(m.A), nh = lane_next(m.H);
+    const uint32_t nf = lane_next((uint32_t)m.f);
+    const bool last = lane == 63;
+    exc.A = last ? 1.0f : na;
+    exc.H = last ? 0.0f : nh;
+    exc.f = last ? false : nf != 0u;
+    total = RMap{readlane_f(m.A, 0), readlane_f(m.H, 0), __builtin_amdgcn_readlane((int)m.f, 0) != 0};
+}
+
+// m_0 . ... . m_63 in every lane
+__device__ __forceinline__ RMap wave_total(const RMap& m) {
+    RMap exc, total;
+    wave_suffix(m, exc, total);
+    return total;
 }
 
 template <int VEC>
@@ -188,7 +240,7 @@ __device__ __forceinline__ RMap tile_map_from_inputs(const DiscArgs& p, int64_t 
         }
         uint32_t eb;
         const RMap m = lane_map<VEC, GAE>(p, t0, x, vv, vn, fl, dn, next_fl, next_v, eb);
-        TM = rmap_then(rmap_bcast(wave_suffix(m), 0), TM);
+        TM = rmap_then(wave_total(m), TM);
     }
     return TM;
 }
@@ -257,20 +309,18 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
         const int64_t t0 = t_seg + 64 * VEC * u + VEC * lane;
         // begin flag (and value) of the step after the lane's last step: the
         // next lane's first step, or the next load's (or wavefront's) first
-        const uint32_t next_lane_fl = __shfl_down(fl[u], 1, 64);
-        const uint32_t fl_next_run = u + 1 < NB ? __shfl(fl[u + 1 < NB ? u + 1 : u], 0, 64) : fl_after;
+        const uint32_t next_lane_fl = lane_next(fl[u]);
+        const uint32_t fl_next_run =
+            u + 1 < NB ? (uint32_t)__builtin_amdgcn_readlane((int)fl[u + 1 < NB ? u + 1 : u], 0) : fl_after;
         const uint32_t next_fl = lane < 63 ? next_lane_fl : fl_next_run;
         float next_v = 0.0f;
         if constexpr (GAE) {
-            const float nl = __shfl_down(comp<VEC>(vv[u], 0), 1, 64);
-            const float nr = u + 1 < NB ? __shfl(comp<VEC>(vv[u + 1 < NB ? u + 1 : u], 0), 0, 64) : v_after;
+            const float nl = lane_next(comp<VEC>(vv[u], 0));
+            const float nr = u + 1 < NB ? readlane_f(comp<VEC>(vv[u + 1 < NB ? u + 1 : u], 0), 0) : v_after;
             next_v = lane < 63 ? nl : nr;
         }
         const RMap m = lane_map<VEC, GAE>(p, t0, x[u], vv[u], vn[u], fl[u], dn[u], next_fl, next_v, ebits[u]);
-        const RMap S = wave_suffix(m);
-        E[u] = rmap_shfl_down(S, 1);
-        if (lane == 63) E[u] = rmap_id();
-        Bm[u] = rmap_bcast(S, 0);
+        wave_suffix(m, E[u], Bm[u]);
     }
     RMap W = Bm[NB - 1];
 #pragma unroll
@@ -332,7 +382,7 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
                 RMap m = rmap_id();
                 if (lane < upto) m = RMap{unpack_hi(wa), unpack_lo(wa), false};
                 if (ft < fn && lane == ft) m = RMap{1.0f, unpack_lo(wi), true};
-                const RMap R = rmap_bcast(wave_suffix(m), 0);
+                const RMap R = wave_total(m);
                 acc = rmap_then(acc, R);
                 if (ft < fn) {
                     carry = acc.H;

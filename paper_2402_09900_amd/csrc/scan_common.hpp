@@ -255,6 +255,100 @@ template <int VEC> struct Codec<K_C64, VEC> {
     }
 };
 
+// ------------------------------------------------------ cross-lane moves
+// The value held by the lane whose index differs from this lane's in bit m
+// (m a power of two from 1 to 32, the same in every lane; every lane
+// active).  Where the hardware allows it the move is a modifier of a VALU
+// instruction rather than a trip through the LDS crossbar: DPP quad
+// permutations for m = 1 and 2, the 16-lane row rotation by 8 for m = 8
+// (within a row of 16 lanes, i + 8 mod 16 = i xor 8), and v_permlane32_swap
+// (gfx950) for m = 32, which exchanges the wavefront's two halves; m = 4 and
+// 16 use ds_swizzle's xor mode (lanes within 32, no LDS memory).
+__device__ __forceinline__ uint32_t lanes_xor(uint32_t v, int m) {
+    switch (m) {
+        case 1: return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
+        case 2: return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
+        case 4: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x101F);                         // xor mask 4
+        case 8: return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x128, 0xF, 0xF, false); // row_ror:8
+        case 16: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x401F);                        // xor mask 16
+        default: {
+            // new vdst: the low half copied to the high half; new vsrc: the
+            // high half copied to the low half
+            const auto pr = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+            return (threadIdx.x & 32) ? pr[0] : pr[1];
+        }
+    }
+}
+__device__ __forceinline__ float lanes_xor(float v, int m) { return __uint_as_float(lanes_xor(__float_as_uint(v), m)); }
+// the value of lane `src` (ds_bpermute)
+__device__ __forceinline__ float lanes_read(float v, int src) { return __shfl(v, src, 64); }
+__device__ __forceinline__ cf lanes_read(cf v, int src) { return cf{__shfl(v.re, src, 64), __shfl(v.im, src, 64)}; }
+__device__ __forceinline__ cf lanes_xor(cf v, int m) { return cf{lanes_xor(v.re, m), lanes_xor(v.im, m)}; }
+__device__ __forceinline__ uint64_t lanes_xor(uint64_t v, int m) {
+    return (uint64_t)lanes_xor((uint32_t)v, m) | ((uint64_t)lanes_xor((uint32_t)(v >> 32), m) << 32);
+}
+__device__ __forceinline__ int64_t lanes_xor(int64_t v, int m) { return (int64_t)lanes_xor((uint64_t)v, m); }
+
+// ds_swizzle in bitmask mode: lane l (of each group of 32) reads lane
+// (l & AND) | OR of its group; no LDS memory is touched.
+template <int AND, int OR>
+__device__ __forceinline__ uint32_t swz(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, AND | (OR << 5));
+}
+// every lane reads the same lane index in the other half of the wavefront
+__device__ __forceinline__ uint32_t half_swap(uint32_t v) {
+    const auto pr = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return (threadIdx.x & 32) ? pr[0] : pr[1];
+}
+
+// Moves of a Sklansky scan over lane groups (lane = j * QP + q, QP a power
+// of two).  At step M (a multiple of QP below 64) the lanes form blocks of
+// 2M; sk_move<false> gives every lane the value of the LAST group of the
+// lower half of its block, (l & ~(2M - 1)) | (M - QP) | q, which is what the
+// upper half needs for a forward scan; sk_move<true> gives the FIRST group
+// of the upper half, (l & ~(2M - 1)) | M | q, for a reverse scan.  The row
+// shifts by 8 are DPP modifiers, the others ds_swizzle patterns within 32
+// lanes (source (l & AND) | OR), followed by a half swap when the block is
+// the whole wavefront; M = 32 with QP = 1 is a scalar lane read.
+template <bool UP, int M, int QP>
+__device__ __forceinline__ uint32_t sk_move(uint32_t v) {
+    static_assert(QP >= 1 && QP <= M && M <= 32 && (QP & (QP - 1)) == 0 && (M & (M - 1)) == 0, "Sklansky step");
+    constexpr int Q = QP - 1;
+    if constexpr (M == 8 && QP == 8) {
+        return UP ? (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x108, 0xF, 0xF, false)   // row_shl:8
+                  : (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x118, 0xF, 0xF, false);  // row_shr:8
+    } else if constexpr (M == 32 && QP == 1) {
+        return (uint32_t)__builtin_amdgcn_readlane((int)v, UP ? 32 : 31);
+    } else if constexpr (M == 32) {
+        return half_swap(swz<Q, UP ? 0 : 32 - QP>(v));
+    } else {
+        return swz<(0x1F & ~(2 * M - 1)) | Q, UP ? M : M - QP>(v);
+    }
+}
+template <bool UP, int M, int QP>
+__device__ __forceinline__ float sk_move(float v) {
+    return __uint_as_float(sk_move<UP, M, QP>(__float_as_uint(v)));
+}
+template <bool UP, int M, int QP>
+__device__ __forceinline__ cf sk_move(cf v) {
+    return cf{sk_move<UP, M, QP>(v.re), sk_move<UP, M, QP>(v.im)};
+}
+
+// Inclusive prefix sum over the lanes of a wavefront in strides of `stride`
+// lanes (lane = j * stride + q; the groups j = 0, 1, ... are summed in
+// order, separately for each q): an xor butterfly, log2(64 / stride) moves.
+template <class V>
+__device__ __forceinline__ V lanes_prefix_sum(V v, int stride) {
+    const int lane = threadIdx.x & 63;
+    V tot = v;
+    for (int m = stride; m < 64; m <<= 1) {
+        const V o = lanes_xor(tot, m);
+        if (lane & m) v += o;
+        tot += o;
+    }
+    return v;
+}
+
 // ------------------------------------------------------- descriptor words
 // Cross-tile communication of the single-pass scan.  Every word is written
 // once per call with a relaxed agent-scope atomic store and read with relaxed
@@ -303,8 +397,6 @@ __device__ __forceinline__ uint64_t pack_state(cf v) { return pack2(v.re, v.im);
 template <class S> __device__ __forceinline__ S unpack_state(uint64_t w);
 template <> __device__ __forceinline__ float unpack_state<float>(uint64_t w) { return unpack_lo(w); }
 template <> __device__ __forceinline__ cf unpack_state<cf>(uint64_t w) { return cf{unpack_lo(w), unpack_hi(w)}; }
-__device__ __forceinline__ float shfl_xor_state(float v, int m) { return __shfl_xor(v, m, 64); }
-__device__ __forceinline__ cf shfl_xor_state(cf v, int m) { return cf{__shfl_xor(v.re, m, 64), __shfl_xor(v.im, m, 64)}; }
 
 // Per-feature tile summary of the scan state, in the two forms a successor
 // can use.  AGG: (A, H) of a tile without a begin step, i.e. h_end =
@@ -560,42 +652,89 @@ __device__ __forceinline__ S seg_apply(const Seg<S, VEC>& sg, int v, S before) {
     return sg.f ? sg.H[v] : mad(sg.A[v], before, sg.H[v]);
 }
 
-__device__ __forceinline__ float shfl_from(float x, int src) { return __shfl(x, src, 64); }
-__device__ __forceinline__ cf shfl_from(cf x, int src) { return cf{__shfl(x.re, src, 64), __shfl(x.im, src, 64)}; }
+
+template <class S, int VEC>
+__device__ __forceinline__ Seg<S, VEC> seg_select(bool c, const Seg<S, VEC>& x, const Seg<S, VEC>& y) {
+    Seg<S, VEC> r;
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) {
+        r.A[v] = c ? x.A[v] : y.A[v];
+        r.H[v] = c ? x.H[v] : y.H[v];
+    }
+    r.f = c ? x.f : y.f;
+    return r;
+}
+
+template <class S, int VEC, bool UP, int M, int QP>
+__device__ __forceinline__ Seg<S, VEC> seg_sk_move(const Seg<S, VEC>& x) {
+    Seg<S, VEC> r;
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) {
+        r.A[v] = sk_move<UP, M, QP>(x.A[v]);
+        r.H[v] = sk_move<UP, M, QP>(x.H[v]);
+    }
+    r.f = sk_move<UP, M, QP>((uint32_t)x.f) != 0u;
+    return r;
+}
+
+// the Sklansky steps M, 2 M, ... 32 of wave_group_scan (groups of QP lanes)
+template <class S, int VEC, bool REV, int M, int QP>
+__device__ __forceinline__ void sk_steps(Seg<S, VEC>& inc) {
+    if constexpr (M < 64) {
+        const int lane = threadIdx.x & 63;
+        const Seg<S, VEC> o = seg_sk_move<S, VEC, REV, M, QP>(inc);
+        const bool takes = REV ? (lane & M) == 0 : (lane & M) != 0;
+        inc = seg_select<S, VEC>(takes, seg_then<S, VEC>(o, inc), inc);
+        sk_steps<S, VEC, REV, 2 * M, QP>(inc);
+    }
+}
 
 template <class S, int VEC>
 __device__ __forceinline__ Seg<S, VEC> seg_shfl(const Seg<S, VEC>& x, int src) {
     Seg<S, VEC> r;
 #pragma unroll
     for (int v = 0; v < VEC; ++v) {
-        r.A[v] = shfl_from(x.A[v], src);
-        r.H[v] = shfl_from(x.H[v], src);
+        r.A[v] = lanes_read(x.A[v], src);
+        r.H[v] = lanes_read(x.H[v], src);
     }
     r.f = __shfl((int)x.f, src, 64) != 0;
     return r;
 }
 
 // Scan across the Gw = 64 / Qp lane groups of a wavefront (lane = j * Qp + q;
+// Qp <= QMAX;
 // group j holds consecutive steps, group j + 1 the ones after).  Forward
 // (REV = false): groups earlier in time come first; reverse: later ones.  On
 // return `inc` is the run from the wavefront's first group (in scan order)
 // through this lane's group, and `exc` the run before this lane's group.
-// Kogge-Stone over log2(Gw) cross-lane shuffles; no LDS, no barrier.
-template <class S, int VEC, bool REV>
+// Sklansky: at step M (M = Qp, 2 Qp, ... 32) the half of each block of 2M
+// lanes that comes second in scan order puts the other half's total (the
+// inclusive run of that half's last group in scan order) in front of its
+// own run -- one partner move (DPP row shift, ds_swizzle, permlane half
+// swap: sk_move) and one combine per step, no LDS memory and no barrier.
+// The exclusive run is the inclusive run of the previous group, one
+// ds_bpermute.
+template <class S, int VEC, bool REV, int QMAX = 64>
 __device__ __forceinline__ void wave_group_scan(Seg<S, VEC>& inc, Seg<S, VEC>& exc, int Qp) {
     const int lane = threadIdx.x & 63;
     const int qsh = __builtin_ctz((unsigned)Qp);   // Qp is a power of two
     const int j = lane >> qsh;
     const int Gw = 64 >> qsh;
-    for (int k = 1; k < Gw; k <<= 1) {
-        const int src = REV ? lane + k * Qp : lane - k * Qp;
-        const bool has = REV ? (j + k < Gw) : (j >= k);
-        const Seg<S, VEC> o = seg_shfl<S, VEC>(inc, has ? src : lane);
-        if (has) inc = seg_then<S, VEC>(o, inc);
+    // one uniform dispatch on the group width; every step's moves are then
+    // fixed at compile time
+    // (QMAX: the largest group width the kernel's plans use)
+    switch (Qp) {
+        case 1: sk_steps<S, VEC, REV, 1, 1>(inc); break;
+        case 2: if constexpr (QMAX >= 2) sk_steps<S, VEC, REV, 2, 2>(inc); break;
+        case 4: if constexpr (QMAX >= 4) sk_steps<S, VEC, REV, 4, 4>(inc); break;
+        case 8: if constexpr (QMAX >= 8) sk_steps<S, VEC, REV, 8, 8>(inc); break;
+        case 16: if constexpr (QMAX >= 16) sk_steps<S, VEC, REV, 16, 16>(inc); break;
+        case 32: if constexpr (QMAX >= 32) sk_steps<S, VEC, REV, 32, 32>(inc); break;
+        default: break;                                  // one group: nothing to scan
     }
     const bool has = REV ? (j + 1 < Gw) : (j >= 1);
     const Seg<S, VEC> o = seg_shfl<S, VEC>(inc, has ? (REV ? lane + Qp : lane - Qp) : lane);
-    exc = has ? o : seg_identity<S, VEC>();
+    exc = seg_select<S, VEC>(has, o, seg_identity<S, VEC>());
 }
 
 // ------------------------------------------------------- count look-back
@@ -616,13 +755,13 @@ constexpr uint64_t kCountValue = kCountOwn - 1;
 
 __device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += (uint32_t)__shfl_xor((int)v, off, 64);
+    for (int m = 1; m < 64; m <<= 1) v += lanes_xor(v, m);
     return v;
 }
 
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += (uint64_t)__shfl_xor((long long)v, off, 64);
+    for (int m = 1; m < 64; m <<= 1) v += lanes_xor(v, m);
     return v;
 }
 __device__ __forceinline__ uint32_t wave_sum(uint32_t v) { return wave_sum_u32(v); }

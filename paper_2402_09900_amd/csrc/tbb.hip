@@ -58,15 +58,8 @@ __device__ __forceinline__ uint64_t lane_begin_mask(Rsrc rs, uint32_t off) {
     return m;
 }
 
-__device__ __forceinline__ uint32_t wave_incl_sum(uint32_t v) {
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int k = 1; k < 64; k <<= 1) {
-        const uint32_t o = (uint32_t)__shfl_up((int)v, k, 64);
-        if (lane >= k) v += o;
-    }
-    return v;
-}
+// inclusive prefix sums over the 64 lanes (DPP / swizzle / permlane butterfly)
+__device__ __forceinline__ uint32_t wave_incl_sum(uint32_t v) { return lanes_prefix_sum(v, 1); }
 
 }  // namespace
 
@@ -205,15 +198,7 @@ __device__ __forceinline__ void draw_rows(const TbbSampleArgs& p, int64_t k, int
     len = b - a;
 }
 
-__device__ __forceinline__ int64_t wave_incl_sum64(int64_t v) {
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int k = 1; k < 64; k <<= 1) {
-        const int64_t o = __shfl_up(v, k, 64);
-        if (lane >= k) v += o;
-    }
-    return v;
-}
+__device__ __forceinline__ int64_t wave_incl_sum64(int64_t v) { return lanes_prefix_sum(v, 1); }
 
 __device__ __forceinline__ uint64_t min_u64(uint64_t a, uint64_t b) { return a < b ? a : b; }
 
