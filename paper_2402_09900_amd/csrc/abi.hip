@@ -22,9 +22,10 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 int elem_bytes(int dt) { return dt == MEMOROID_F32 ? 4 : dt == MEMOROID_BF16 ? 2 : 8; }
 int vec_width(int dt) { return dt == MEMOROID_F32 ? 4 : dt == MEMOROID_BF16 ? 4 : 2; }
+// smallest power of two >= v, capped at 2^62 (callers cap it far lower)
 int64_t next_pow2(int64_t v) {
     int64_t p = 1;
-    while (p < v) p <<= 1;
+    while (p < v && p < ((int64_t)1 << 62)) p <<= 1;
     return p;
 }
 bool aligned(const void* p, size_t n) { return ((uintptr_t)p % n) == 0; }
@@ -74,6 +75,8 @@ enum SigKind : int64_t { kSigDiag = 1, kSigDiagBwd, kSigFfm, kSigFfmBwd, kSigDis
 // vectorised lane width; `state_complex` picks the descriptor size.
 bool plan_diag(int64_t B, int64_t T, int64_t d, int state_dtype, bool vec, int rows, bool bwd,
                bool ainv, bool want_grad_a, DiagPlan* p) {
+    // extents no tiling can address (and whose sums below would overflow)
+    if (B <= 0 || T <= 0 || d <= 0 || d > (int64_t)INT32_MAX || T > INT64_MAX / 4) return false;
     const int VEC = vec ? vec_width(state_dtype) : 1;
     const int64_t lanes = (d + VEC - 1) / VEC;
     // a chain's row block is (at most) one 128-byte line of the feature row
@@ -92,7 +95,9 @@ bool plan_diag(int64_t B, int64_t T, int64_t d, int state_dtype, bool vec, int r
     // buffer offsets below 2^31
     // (4 bytes at least: bf16 input may be written as f32)
     const int64_t wb = elem_bytes(state_dtype) > 4 ? elem_bytes(state_dtype) : 4;
-    if ((p->L + 2) * d * wb >= (int64_t)INT32_MAX) return false;
+    int64_t tile_bytes;
+    if (!mul_ok(p->L + 2, d, &tile_bytes) || !mul_ok(tile_bytes, wb, &tile_bytes) || tile_bytes >= (int64_t)INT32_MAX)
+        return false;
     const bool cplx = state_dtype == MEMOROID_C64;
     const size_t agg_b = cplx ? 16 : 8, incl_b = cplx ? 8 : 4;
     int64_t ndesc;
@@ -912,6 +917,7 @@ struct DiscPlan {
 
 // header, per-tile epoch words, then two banks of tile words
 bool plan_disc(int64_t B, int64_t T, bool gae, DiscPlan* p) {
+    if (B <= 0 || T <= 0 || T > INT64_MAX / 4) return false;
     p->nt = (T + disc_tile(gae) - 1) / disc_tile(gae);
     if (!mul_ok(B, p->nt, &p->ntiles) || p->ntiles >= (int64_t)INT32_MAX) return false;
     size_t off = kAlign;
@@ -1244,8 +1250,13 @@ int memoroid_workspace_prepare(void* workspace, size_t workspace_bytes, void* st
     return check_hip(ws_init_launch(nullptr, 0, workspace, workspace_bytes / 16 * 16, (hipStream_t)stream));
 }
 
-size_t memoroid_workspace_bytes(memoroid_op op, int64_t B, int64_t T, int64_t d_or_H, int64_t dk, int64_t dv,
+size_t memoroid_workspace_bytes(memoroid_op op_in, int64_t B, int64_t T, int64_t d_or_H, int64_t dk, int64_t dv,
                                 int64_t chunk) {
+    // the operation as a plain int: a C caller may pass any value, which a
+    // C++ load of the enum type would not allow
+    int op;
+    static_assert(sizeof op == sizeof op_in, "memoroid_op is int-sized");
+    memcpy(&op, &op_in, sizeof op);
     size_t best = 0;
     auto take = [&best](size_t v) {
         if (v > best) best = v;
