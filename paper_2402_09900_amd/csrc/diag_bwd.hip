@@ -111,6 +111,12 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
                                 want_da ? (rows_left + h_back) * rowB : 0);
     const uint32_t step = active ? (uint32_t)rowB : 0u;
     const uint32_t off0 = active ? (uint32_t)((int64_t)lrow * rowB + f0 * EB) : kOob;
+    // the previous tile's inclusive words, ahead of everything else (the
+    // look-back below is skipped when they were all published)
+    S spec[VEC];
+    bool spec_ok = false;
+    if (wave == NW - 1 && j == 0 && active && k > 0)
+        spec_ok = peek_incl_ahead<S, VEC>(incl, (int64_t)ticket - p.nchains, Dp, Qp, q, spec);
     uint32_t fl[R + 1];
 #pragma unroll
     for (int r = 0; r <= R; ++r) fl[r] = bload_u8(rs_st, lrow + r);
@@ -228,8 +234,13 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     if (wave == NW - 1) {
         const bool need_carry = !((t_last + 1 == T) || fl_after != 0);
         S carry[VEC];
-        lookback<S, VEC>(agg, incl, (int64_t)ticket - p.nchains, p.nchains, Dp, Qp, need_carry && active, carry,
-                         sLb, &p.hdr->timeout);
+        if (need_carry && __all(j != 0 || !active || spec_ok)) {
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) carry[v] = active ? spec[v] : s_zero<S>();
+        } else {
+            lookback<S, VEC>(agg, incl, (int64_t)ticket - p.nchains, p.nchains, Dp, Qp, need_carry && active, carry,
+                             sLb, &p.hdr->timeout);
+        }
         if (j == 0) {
 #pragma unroll
             for (int v = 0; v < VEC; ++v) sCarry[q * VEC + v] = carry[v];

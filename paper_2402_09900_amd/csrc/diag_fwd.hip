@@ -132,6 +132,12 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     const Rsrc rs_a = make_rsrc(AINV ? p.a : (const char*)p.a + tape_row0 * p.d * IB, AINV ? 0 : rows_left * p.d * IB);
     const uint32_t in_step = active ? (uint32_t)(p.d * IB) : 0u;
     const uint32_t in_off = active ? (uint32_t)((int64_t)lrow * p.d * IB + f0 * IB) : kOob;
+    // the previous tile's inclusive words, ahead of everything else (the
+    // look-back below is skipped when they were all published)
+    S spec[VEC];
+    bool spec_ok = false;
+    if (wave == 0 && j == 0 && active && tile > 0)
+        spec_ok = peek_incl_ahead<S, VEC>(incl, (int64_t)ticket - p.nchains, Dp, Qp, q, spec);
     uint32_t fl[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) fl[r] = bload_u8(rs_st, lrow + r);
@@ -217,6 +223,19 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
         }
     }
     own.f = begins != 0;
+    // packed inputs (bf16) are decoded again for the replay rather than kept
+    // decoded: an empty asm on each stored word hides that the decode would
+    // repeat, so only the packed words stay live across the scan
+    if constexpr (IB < 4) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+#pragma unroll
+            for (int k = 0; k < RawVec<IN, VEC>::WORDS; ++k) {
+                asm volatile("" : "+v"(rx[r].w[k]));
+                if constexpr (!AINV) asm volatile("" : "+v"(ra[r].w[k]));
+            }
+        }
+    }
 
     // ---- episode index (optional): the tiles of each tape's first feature
     // block count begin steps; the count of the lane's earlier groups comes
@@ -297,8 +316,13 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     if (wave == 0) {
         const bool need_carry = !(tile_row0 == 0 || fl_tile0 != 0);
         S carry[VEC];
-        lookback<S, VEC>(agg, incl, (int64_t)ticket - p.nchains, p.nchains, Dp, Qp, need_carry && active, carry,
-                         sLb, &p.hdr->timeout);
+        if (need_carry && __all(j != 0 || !active || spec_ok)) {
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) carry[v] = active ? spec[v] : s_zero<S>();
+        } else {
+            lookback<S, VEC>(agg, incl, (int64_t)ticket - p.nchains, p.nchains, Dp, Qp, need_carry && active, carry,
+                             sLb, &p.hdr->timeout);
+        }
         if (j == 0) {
 #pragma unroll
             for (int v = 0; v < VEC; ++v) sCarry[q * VEC + v] = carry[v];
@@ -385,11 +409,12 @@ hipError_t diag_fwd_launch(int in_kind, int out_kind, bool vec, bool ainv,
     if (in_kind == K_F32 && out_kind == K_F32)
         return vec ? launch_fwd<K_F32, K_F32, VF, R>(args, ntiles, ainv, s)
                    : launch_fwd<K_F32, K_F32, 1, R>(args, ntiles, ainv, s);
+    constexpr int RB = kFwdRowsBf16;
     if (in_kind == K_BF16 && out_kind == K_BF16)
-        return vec ? launch_fwd<K_BF16, K_BF16, VB, R>(args, ntiles, ainv, s)
+        return vec ? launch_fwd<K_BF16, K_BF16, VB, RB>(args, ntiles, ainv, s)
                    : launch_fwd<K_BF16, K_BF16, 1, R>(args, ntiles, ainv, s);
     if (in_kind == K_BF16 && out_kind == K_F32)
-        return vec ? launch_fwd<K_BF16, K_F32, VB, R>(args, ntiles, ainv, s)
+        return vec ? launch_fwd<K_BF16, K_F32, VB, RB>(args, ntiles, ainv, s)
                    : launch_fwd<K_BF16, K_F32, 1, R>(args, ntiles, ainv, s);
     if (in_kind == K_C64 && out_kind == K_C64)
         return vec ? launch_fwd<K_C64, K_C64, VC, R>(args, ntiles, ainv, s)

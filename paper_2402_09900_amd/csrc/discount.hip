@@ -176,20 +176,30 @@ __device__ __forceinline__ void store_vec(float* p, const typename F<VEC>::T& v)
     __builtin_nontemporal_store(v, (typename F<VEC>::T*)p);
 }
 
-// Inputs x (delta for the advantage, computed here in place) and the map of
-// one lane's VEC steps t0 .. t0+VEC-1.  next_fl / next_v: begin flag and
-// V(s) of the step after the lane's last step.  eb gets bit k set when step
-// k is the last of its episode.
+// Inputs x (delta for the advantage, computed here in place) of one lane's
+// VEC steps t0 .. t0+VEC-1; returns bit k set when step k is the last of its
+// episode.  next_fl / next_v: begin flag and V(s) of the step after the
+// lane's last step.
 template <int VEC, bool GAE>
-__device__ __forceinline__ RMap lane_map(const DiscArgs& p, int64_t t0, typename F<VEC>::T& x,
-                                         const typename F<VEC>::T& vv, const typename F<VEC>::T& vn, uint32_t fl,
-                                         uint32_t dn, uint32_t next_fl, float next_v, uint32_t& eb) {
-    eb = 0;
+__device__ __forceinline__ uint32_t prep_chunk(const DiscArgs& p, int64_t t0, typename F<VEC>::T& x,
+                                               const typename F<VEC>::T& vv, const typename F<VEC>::T& vn,
+                                               uint32_t fl, uint32_t dn, uint32_t next_fl, float next_v) {
+    // steps k >= lim are the tape's last step or past it
+    const int64_t rem = p.T - 1 - t0;
+    const int lim = rem <= 0 ? 0 : (rem >= VEC ? VEC : (int)rem);
+    uint32_t eb = ((1u << VEC) - 1u) & ~((1u << lim) - 1u);
+    if constexpr (VEC == 4) {
+        // begin flags of steps t0+1 .. t0+4, one per byte; a byte's top bit
+        // set exactly when the byte is nonzero, then the four top bits
+        const uint32_t w = __builtin_amdgcn_alignbyte(next_fl, fl, 1);
+        const uint32_t hb = (((w & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | w) & 0x80808080u;
+        eb |= ((hb >> 7) | (hb >> 14) | (hb >> 21) | (hb >> 28)) & 0xFu;
+    } else {
+        eb |= (next_fl & 0xFFu) != 0u ? 1u : 0u;
+    }
 #pragma unroll
     for (int k = 0; k < VEC; ++k) {
-        const uint32_t nb = k + 1 < VEC ? ((fl >> (8 * (k + 1))) & 0xFFu) : (next_fl & 0xFFu);
-        const bool e = (t0 + k + 1 >= p.T) || nb != 0u;
-        eb |= (uint32_t)e << k;
+        const bool e = (eb >> k) & 1u;
         if constexpr (GAE) {
             float nxt;
             if (p.vn) {
@@ -203,10 +213,37 @@ __device__ __forceinline__ RMap lane_map(const DiscArgs& p, int64_t t0, typename
             set_comp<VEC>(x, k, __builtin_fmaf(g, nxt, comp<VEC>(x, k)) - comp<VEC>(vv, k));
         }
     }
+    return eb;
+}
+
+// The map of VEC steps with inputs x and episode-end bits eb.
+template <int VEC>
+__device__ __forceinline__ RMap chunk_map(float a, const typename F<VEC>::T& x, uint32_t eb) {
     RMap m = rmap_id();
 #pragma unroll
-    for (int k = VEC - 1; k >= 0; --k) m = rmap_then(RMap{p.a, comp<VEC>(x, k), ((eb >> k) & 1u) != 0u}, m);
+    for (int k = VEC - 1; k >= 0; --k) m = rmap_then(RMap{a, comp<VEC>(x, k), ((eb >> k) & 1u) != 0u}, m);
     return m;
+}
+
+// One step of the reverse recurrence as a bit select (no multiply by zero
+// at a reset, so a non-finite value never crosses an episode end): the
+// value at step s of a lane's run given the value y after it, with bit s of
+// m set when step s ends its episode.
+__device__ __forceinline__ float step_back(uint32_t m, int s, float a, float x, float y) {
+    const uint32_t mk = (uint32_t)((int32_t)(m << (31 - s)) >> 31);
+    const float ny = __builtin_fmaf(a, y, x);
+    return __uint_as_float((__float_as_uint(x) & mk) | (__float_as_uint(ny) & ~mk));
+}
+
+// Position of chunk k of lane o's run in the wavefront's LDS rows of NC
+// chunks: XOR-swizzled within the row, so that an instruction of the
+// coalesced side (64 consecutive chunks) and one of the owner side (chunk k
+// of every row) both reach distinct banks.
+template <int NC>
+__device__ __forceinline__ int owner_slot(int o, int k) {
+    constexpr int LG = NC == 4 ? 2 : NC == 8 ? 3 : NC == 16 ? 4 : 5;
+    static_assert(NC == (1 << LG), "rows of 4, 8, 16 or 32 chunks");
+    return o * NC + (k ^ ((o ^ (o >> LG)) & (NC - 1)));
 }
 
 // Aggregate map of tile `tile` of tape row `row`, computed by one wavefront
@@ -238,8 +275,8 @@ __device__ __forceinline__ RMap tile_map_from_inputs(const DiscArgs& p, int64_t 
                 if (!p.vn && t0 + VEC < p.T) next_v = p.v[row + t0 + VEC];
             }
         }
-        uint32_t eb;
-        const RMap m = lane_map<VEC, GAE>(p, t0, x, vv, vn, fl, dn, next_fl, next_v, eb);
+        const uint32_t eb = prep_chunk<VEC, GAE>(p, t0, x, vv, vn, fl, dn, next_fl, next_v);
+        const RMap m = chunk_map<VEC>(p.a, x, eb);
         TM = rmap_then(wave_total(m), TM);
     }
     return TM;
@@ -249,15 +286,18 @@ __device__ __forceinline__ RMap tile_map_from_inputs(const DiscArgs& p, int64_t 
 
 template <int VEC, bool GAE>
 __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
-    constexpr int kRows = disc_rows(GAE);     // steps per lane
+    constexpr int kRows = disc_rows(GAE);     // steps per lane: one contiguous run
     constexpr int kSeg = 64 * kRows;          // steps per wavefront
     constexpr int kTile = disc_tile(GAE);
-    constexpr int NB = kRows / VEC;           // loads per lane
+    constexpr int NC = kRows / VEC;           // chunks of VEC steps per lane (loads per lane)
     typedef typename F<VEC>::T V;
+    __shared__ V s_x[4][64 * NC];             // per wavefront: inputs in owner rows, then outputs
+    __shared__ __attribute__((aligned(16))) uint8_t s_e[4][64 * NC];   // episode-end bits per chunk
     __shared__ float s_wA[4], s_wH[4];
     __shared__ int s_wf[4];
     __shared__ float s_carry;
     __shared__ uint32_t s_bank;               // epoch parity; all ones: stand down
+    __shared__ int s_need;
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int64_t ticket = blockIdx.x;
@@ -265,7 +305,8 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
     uint64_t sig_seen = 0;
     uint32_t epoch = 0;
     if (tid == 0) sig_seen = peek_sig(p.hdr);
-    const int64_t j = ticket / p.B;           // tiles counted from the tape's end
+    // tiles counted from the tape's end (fewer than 2^31 tiles: a 32-bit division)
+    const int64_t j = (int64_t)((uint32_t)ticket / (uint32_t)p.B);
     const int64_t b = ticket - j * p.B;
     const int64_t i = p.nt - 1 - j;           // tile index from the tape's start
     const int64_t T = p.T;
@@ -273,12 +314,13 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
     const int64_t t_seg = i * kTile + (int64_t)w * kSeg;
     const int64_t t_after = t_seg + kSeg;     // first step after this wavefront's steps
 
-    // ------------------------------------------------------------- loads
-    V x[NB], vv[NB] = {}, vn[NB] = {};
-    uint32_t fl[NB], dn[NB] = {};
+    // ------------------------------------------------ loads (coalesced)
+    // load u of lane l holds chunk 64u + l of the wavefront's run
+    V x[NC], vv[NC] = {}, vn[NC] = {};
+    uint32_t fl[NC], dn[NC] = {};
 #pragma unroll
-    for (int u = 0; u < NB; ++u) {
-        const int64_t t = t_seg + 64 * VEC * u + VEC * lane;
+    for (int u = 0; u < NC; ++u) {
+        const int64_t t = t_seg + VEC * (64 * u + lane);
         const bool ok = t < T;
         fl[u] = ok ? load_flags<VEC>(p.start + row + t) : 0u;
         x[u] = ok ? load_vec<VEC>(p.r + row + t) : V{};
@@ -299,38 +341,78 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
         if (after_in && !p.vn) v_after = p.v[row + t_after];
     }
 
-    // -------------------------------------- per-step inputs and lane maps
-    // e bit k of load u: step is the last of its episode
-    uint32_t ebits[NB];
-    RMap E[NB];                               // exclusive suffix: lanes after this one, same load
-    RMap Bm[NB];                              // whole load (wave-uniform)
+    // ------------------- per-step inputs, then the transpose to owner rows
+    // Each chunk's inputs (delta for the advantage) and episode-end bits are
+    // formed where the chunk was loaded, with the step after it taken from
+    // the next lane (or the next load's first lane, or the next run); then
+    // the chunks go to LDS, where lane o's row holds chunks NC*o .. NC*o+NC-1:
+    // its own contiguous run of kRows steps.
 #pragma unroll
-    for (int u = 0; u < NB; ++u) {
-        const int64_t t0 = t_seg + 64 * VEC * u + VEC * lane;
-        // begin flag (and value) of the step after the lane's last step: the
-        // next lane's first step, or the next load's (or wavefront's) first
+    for (int u = 0; u < NC; ++u) {
+        const int c = 64 * u + lane;
+        const int64_t t0 = t_seg + VEC * c;
         const uint32_t next_lane_fl = lane_next(fl[u]);
         const uint32_t fl_next_run =
-            u + 1 < NB ? (uint32_t)__builtin_amdgcn_readlane((int)fl[u + 1 < NB ? u + 1 : u], 0) : fl_after;
+            u + 1 < NC ? (uint32_t)__builtin_amdgcn_readlane((int)fl[u + 1 < NC ? u + 1 : u], 0) : fl_after;
         const uint32_t next_fl = lane < 63 ? next_lane_fl : fl_next_run;
         float next_v = 0.0f;
         if constexpr (GAE) {
             const float nl = lane_next(comp<VEC>(vv[u], 0));
-            const float nr = u + 1 < NB ? readlane_f(comp<VEC>(vv[u + 1 < NB ? u + 1 : u], 0), 0) : v_after;
+            const float nr = u + 1 < NC ? readlane_f(comp<VEC>(vv[u + 1 < NC ? u + 1 : u], 0), 0) : v_after;
             next_v = lane < 63 ? nl : nr;
         }
-        const RMap m = lane_map<VEC, GAE>(p, t0, x[u], vv[u], vn[u], fl[u], dn[u], next_fl, next_v, ebits[u]);
-        wave_suffix(m, E[u], Bm[u]);
+        const uint32_t eb = prep_chunk<VEC, GAE>(p, t0, x[u], vv[u], vn[u], fl[u], dn[u], next_fl, next_v);
+        s_x[w][owner_slot<NC>(c / NC, c % NC)] = x[u];
+        s_e[w][c] = (uint8_t)eb;
     }
-    RMap W = Bm[NB - 1];
+    // the wavefront's own LDS rows only: its LDS operations run in program
+    // order, so a compiler-only fence is all the ordering needed
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    V xo[NC];
 #pragma unroll
-    for (int u = NB - 2; u >= 0; --u) W = rmap_then(Bm[u], W);
-    if (lane == 0) {
-        s_wA[w] = W.A;
-        s_wH[w] = W.H;
-        s_wf[w] = (int)W.f;
+    for (int k = 0; k < NC; ++k) xo[k] = s_x[w][owner_slot<NC>(lane, k)];
+    // bit s of m: step s of the lane's run ends its episode
+    uint32_t m = 0;
+    {
+        const uint32_t* ew = (const uint32_t*)&s_e[w][lane * NC];
+        uint32_t d[(NC + 3) / 4];
+#pragma unroll
+        for (int q = 0; q < (NC + 3) / 4; ++q) d[q] = ew[q];
+#pragma unroll
+        for (int q = 0; q < NC; ++q) m |= ((d[q / 4] >> (8 * (q % 4))) & ((1u << VEC) - 1u)) << (VEC * q);
     }
-    if (tid == 0) s_bank = ws_bound_to(p.hdr, p.sig, sig_seen, ticket == 0) ? (epoch & 1u) : kEmpty32;
+    const float a = p.a;
+
+    // ------------------------------------------- lane maps, wavefront scan
+    // the lane's map: its run folded right to left from a zero after it
+    float y = 0.0f;
+#pragma unroll
+    for (int q = NC - 1; q >= 0; --q)
+#pragma unroll
+        for (int k = VEC - 1; k >= 0; --k) y = step_back(m, VEC * q + k, a, comp<VEC>(xo[q], k), y);
+    float aR = a;                             // a^kRows: the map's factor when no step of the run ends an episode
+#pragma unroll
+    for (int n = 1; n < kRows; n *= 2) aR *= aR;
+    RMap E, Wtot;                             // E: the lanes after this one; Wtot: the whole wavefront
+    wave_suffix(RMap{aR, y, m != 0u}, E, Wtot);
+    if (lane == 0) {
+        s_wA[w] = Wtot.A;
+        s_wH[w] = Wtot.H;
+        s_wf[w] = (int)Wtot.f;
+    }
+    // a carry from the next tile is needed unless the tile's last step ends
+    // an episode (the last wavefront holds the next tile's first flag)
+    if (tid == 192) s_need = (j > 0 && fl_after == 0u) ? 1 : 0;
+    const int64_t slot = b * p.nt + j;
+    // Wavefront 0 holds the tile's first steps: when they include an episode
+    // end it knows the value at the tile's first step already, and publishes
+    // it before the barrier, so that a look-back waiting for this tile does
+    // not wait for the tile's other wavefronts.
+    if (tid == 0) {
+        const bool bound = ws_bound_to(p.hdr, p.sig, sig_seen, ticket == 0);
+        s_bank = bound ? (epoch & 1u) : kEmpty32;
+        if (bound && Wtot.f) publish64((uint64_t*)((char*)p.incl + ((epoch & 1u) ? p.bank : 0)) + slot, pack2(Wtot.H, 0.0f));
+    }
     __syncthreads();
     const uint32_t bank = __builtin_amdgcn_readfirstlane(s_bank);
     if (bank == kEmpty32) return;             // workspace bound to another call: every tile stands down
@@ -340,135 +422,123 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
 #pragma unroll
     for (int ww = 0; ww < 4; ++ww) Wt[ww] = RMap{s_wA[ww], s_wH[ww], s_wf[ww] != 0};
     const RMap TM = rmap_then(Wt[0], rmap_then(Wt[1], rmap_then(Wt[2], Wt[3])));
-    const int64_t slot = b * p.nt + j;
+    const bool need = __builtin_amdgcn_readfirstlane(s_need) != 0;
+    // wavefront ww depends on the carry when no later wavefront of the tile
+    // holds an episode end (a tile that needs no carry ends one itself)
+    bool dep[4];
+    dep[3] = need;
+#pragma unroll
+    for (int ww = 2; ww >= 0; --ww) dep[ww] = dep[ww + 1] && !Wt[ww + 1].f;
+
+    // ------------------------------------------------------------ outputs
+    // The value entering the wavefront's last step passes through the later
+    // wavefronts' maps from the tile's carry c; each lane takes it through
+    // the later lanes' maps, runs its steps right to left, and the results
+    // go back through the LDS rows to coalesced stores.
+    auto emit = [&](float c) {
+#pragma unroll
+        for (int ww = 3; ww > 0; --ww)
+            if (ww > w) c = rmap_apply(Wt[ww], c);
+        float yv = rmap_apply(E, c);
+        // the step masks are formed again from an opaque copy of m rather
+        // than kept from the lane map's loop (32 of them would not fit)
+        uint32_t m2 = m;
+        asm volatile("" : "+v"(m2));
+#pragma unroll
+        for (int q = NC - 1; q >= 0; --q)
+#pragma unroll
+            for (int k = VEC - 1; k >= 0; --k) {
+                yv = step_back(m2, VEC * q + k, a, comp<VEC>(xo[q], k), yv);
+                set_comp<VEC>(xo[q], k, yv);
+            }
+#pragma unroll
+        for (int k = 0; k < NC; ++k) s_x[w][owner_slot<NC>(lane, k)] = xo[k];
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+#pragma unroll
+        for (int u = 0; u < NC; ++u) {
+            const int cc = 64 * u + lane;
+            const int64_t t0 = t_seg + VEC * cc;
+            const V out = s_x[w][owner_slot<NC>(cc / NC, cc % NC)];
+            if (t0 < T) {
+                store_vec<VEC>(p.out + row + t0, out);
+                if constexpr (GAE) {
+                    if (p.target) store_vec<VEC>(p.target + row + t0, out + vv[u]);
+                }
+            }
+        }
+    };
 
     // ------------------------------------------------ publish, look back
-    // Wavefront 3 publishes the tile's aggregate (or, when the tile holds an
-    // episode end, its value at the first step, which then needs nothing from
-    // the right); wavefront 0 polls, so no wavefront both stores and polls.
-    if (w == 3 && lane == 0) {
-        if (TM.f)
-            publish64(incl + slot, pack2(TM.H, 0.0f));
-        else
+    // Wavefront 2 publishes the tile's aggregate (or, when the tile holds an
+    // episode end that wavefront 0 did not hold, its value at the first step,
+    // which then needs nothing from the right); wavefront 3, the one that
+    // needs the carry, looks back; so no wavefront both stores and polls.
+    // Wavefronts that do not depend on the carry store their outputs at once.
+    if (w == 2 && lane == 0) {
+        if (!TM.f)
             publish64(agg + slot, pack2(TM.H, TM.A));
+        else if (!Wt[0].f)
+            publish64(incl + slot, pack2(TM.H, 0.0f));
         // this tile's words of the idle bank, for the next call
         const int64_t idle = bank ? 0 : p.bank;
         ((uint64_t*)((char*)p.agg + idle))[slot] = kEmpty64;
         ((uint64_t*)((char*)p.incl + idle))[slot] = kEmpty64;
     }
-    if (w == 0) {
-        // a carry is needed unless the tile's last step ends an episode
-        const int64_t t_next_tile = (i + 1) * (int64_t)kTile;
-        const bool need = j > 0 && p.start[row + t_next_tile] == 0;
-        float carry = 0.0f;
-        if (need) {
-            RMap acc = rmap_id();
-            int64_t base = j - 1;
-            uint32_t polls = 0;
-            while (true) {
-                const int64_t pj = base - lane;
-                uint64_t wi = pack2(0.0f, 0.0f), wa = kEmpty64;
-                if (pj >= 0) {
-                    wi = peek64(incl + b * p.nt + pj);
-                    if (wi == kEmpty64) wa = peek64(agg + b * p.nt + pj);
-                }
-                const bool term = wi != kEmpty64;
-                const bool ready = term || wa != kEmpty64;
-                const uint64_t m_term = __ballot(term);
-                const uint64_t m_nr = __ballot(!ready);
-                const int ft = m_term ? __builtin_ctzll(m_term) : 64;
-                const int fn = m_nr ? __builtin_ctzll(m_nr) : 64;
-                const int upto = ft < fn ? ft : fn;   // lanes before `upto` hold aggregates
-                RMap m = rmap_id();
-                if (lane < upto) m = RMap{unpack_hi(wa), unpack_lo(wa), false};
-                if (ft < fn && lane == ft) m = RMap{1.0f, unpack_lo(wi), true};
-                const RMap R = wave_total(m);
-                acc = rmap_then(acc, R);
-                if (ft < fn) {
+    if (!dep[w]) emit(0.0f);                  // exact: the carry does not reach these steps
+    float carry = 0.0f;
+    if (w == 3 && need) {
+        RMap acc = rmap_id();
+        int64_t base = j - 1;
+        uint32_t polls = 0;
+        while (true) {
+            const int64_t pj = base - lane;
+            uint64_t wi = pack2(0.0f, 0.0f), wa = kEmpty64;
+            if (pj >= 0) {
+                wi = peek64(incl + b * p.nt + pj);
+                if (wi == kEmpty64) wa = peek64(agg + b * p.nt + pj);
+            }
+            const bool term = wi != kEmpty64;
+            const bool ready = term || wa != kEmpty64;
+            const uint64_t m_term = __ballot(term);
+            const uint64_t m_nr = __ballot(!ready);
+            const int ft = m_term ? __builtin_ctzll(m_term) : 64;
+            const int fn = m_nr ? __builtin_ctzll(m_nr) : 64;
+            const int upto = ft < fn ? ft : fn;   // lanes before `upto` hold aggregates
+            RMap mm = rmap_id();
+            if (lane < upto) mm = RMap{unpack_hi(wa), unpack_lo(wa), false};
+            if (ft < fn && lane == ft) mm = RMap{1.0f, unpack_lo(wi), true};
+            const RMap R = wave_total(mm);
+            acc = rmap_then(acc, R);
+            if (ft < fn) {
+                carry = acc.H;
+                break;
+            }
+            base -= fn;
+            if (fn > 0) {
+                polls = 0;
+            } else if (++polls > p.fallback_polls) {
+                // tile `base` has not published: fold its aggregate in
+                // from its inputs (tile index from the tape's start)
+                const RMap M = tile_map_from_inputs<VEC, GAE>(p, row, p.nt - 1 - base);
+                acc = rmap_then(acc, M);
+                if (M.f) {
                     carry = acc.H;
                     break;
                 }
-                base -= fn;
-                if (fn > 0) {
-                    polls = 0;
-                } else if (++polls > p.fallback_polls) {
-                    // tile `base` has not published: fold its aggregate in
-                    // from its inputs (tile index from the tape's start)
-                    const RMap M = tile_map_from_inputs<VEC, GAE>(p, row, p.nt - 1 - base);
-                    acc = rmap_then(acc, M);
-                    if (M.f) {
-                        carry = acc.H;
-                        break;
-                    }
-                    base -= 1;
-                    polls = 0;
-                } else {
-                    __builtin_amdgcn_s_sleep(1);
-                }
+                base -= 1;
+                polls = 0;
+            } else {
+                __builtin_amdgcn_s_sleep(1);
             }
         }
         if (!TM.f && lane == 0) publish64(incl + slot, pack2(rmap_apply(TM, carry), 0.0f));
-        if (lane == 0) s_carry = carry;
+        if (dep[2] && lane == 0) s_carry = carry;
     }
-
-    // ------------------------------------------------------------ outputs
-    // Block u of a lane starts from the carry passed through the later
-    // wavefronts' and blocks' maps; where one of those maps holds a reset the
-    // value no longer depends on the carry, and such blocks are formed and
-    // stored before the carry is known (wavefronts 1-3 do it while wavefront
-    // 0 looks back), so their stores overlap the wait.
-    auto emit = [&](int u, float c) {
-        const int64_t t0 = t_seg + 64 * VEC * u + VEC * lane;
-        float y = rmap_apply(E[u], c);
-        V out;
-#pragma unroll
-        for (int k = VEC - 1; k >= 0; --k) {
-            const float xk = comp<VEC>(x[u], k);
-            y = ((ebits[u] >> k) & 1u) ? xk : __builtin_fmaf(p.a, y, xk);
-            set_comp<VEC>(out, k, y);
-        }
-        if (t0 < T) {
-            store_vec<VEC>(p.out + row + t0, out);
-            if constexpr (GAE) {
-                if (p.target) {
-                    V tg;
-#pragma unroll
-                    for (int k = 0; k < VEC; ++k) set_comp<VEC>(tg, k, comp<VEC>(out, k) + comp<VEC>(vv[u], k));
-                    store_vec<VEC>(p.target + row + t0, tg);
-                }
-            }
-        }
-    };
-    uint32_t stored = 0;
-    {
-        float c = 0.0f;                       // exact wherever `dep` is false
-        bool dep = true;
-#pragma unroll
-        for (int ww = 3; ww > 0; --ww)
-            if (ww > w) {
-                dep = dep && !Wt[ww].f;
-                c = rmap_apply(Wt[ww], c);
-            }
-#pragma unroll
-        for (int u = NB - 1; u >= 0; --u) {
-            if (!dep || E[u].f) {
-                emit(u, c);
-                stored |= 1u << u;
-            }
-            dep = dep && !Bm[u].f;
-            c = rmap_apply(Bm[u], c);
-        }
+    if (dep[2]) {                             // workgroup-uniform: earlier wavefronts wait for the carry too
+        __syncthreads();
+        carry = s_carry;
     }
-    __syncthreads();
-    float c = s_carry;
-#pragma unroll
-    for (int ww = 3; ww > 0; --ww)
-        if (ww > w) c = rmap_apply(Wt[ww], c);
-#pragma unroll
-    for (int u = NB - 1; u >= 0; --u) {
-        if (!((stored >> u) & 1u)) emit(u, c);
-        c = rmap_apply(Bm[u], c);
-    }
+    if (dep[w]) emit(carry);
     if (tid == 0) write_epoch(p.epoch + ticket, epoch);
 }
 

@@ -27,12 +27,21 @@ struct WsHeader;
 #ifndef MEMOROID_CHAIN_ROW_BYTES
 #define MEMOROID_CHAIN_ROW_BYTES 128
 #endif
+#ifndef MEMOROID_FWD_ROWS_BF16
+#define MEMOROID_FWD_ROWS_BF16 12
+#endif
 constexpr int kFwdRows = MEMOROID_FWD_ROWS;
+// bf16 input, vectorised: 8 features per lane (one 16-byte access), so a
+// lane's steps hold half the bytes they would in f32 for the same registers
+constexpr int kFwdRowsBf16 = MEMOROID_FWD_ROWS_BF16;
 constexpr int kBwdRows = MEMOROID_BWD_ROWS;
 constexpr int kBwdRowsPerStepA = MEMOROID_BWD_ROWS_PER_STEP_A;
 // Bytes of a feature row one chain covers (one 128-byte line by default).
 constexpr int64_t kChainRowBytes = MEMOROID_CHAIN_ROW_BYTES;
 constexpr int diag_rows(bool bwd, bool ainv) { return !bwd ? kFwdRows : (ainv ? kBwdRows : kBwdRowsPerStepA); }
+// steps per lane of the forward scan of a state dtype (a memoroid_dtype:
+// bf16 is 1), vectorised or not
+constexpr int diag_fwd_rows(int state_dtype, bool vec) { return state_dtype == 1 && vec ? kFwdRowsBf16 : kFwdRows; }
 // The FFM gradient keeps more per-tile state (the input-gradient reduction)
 // and runs fastest with shorter tiles and more workgroups per CU.
 #ifndef MEMOROID_FFM_BWD_ROWS
@@ -200,7 +209,13 @@ hipError_t linattn_bwd_grad_launch(const LinBwdArgs& a, hipStream_t s);
 // ------------------------------------------- discounted return and GAE
 // Steps per lane: 32 for the return (two streams in registers), 16 for the
 // advantage (four); a tile is 4 wavefronts of 64 lanes.
-constexpr int disc_rows(bool gae) { return gae ? 16 : 32; }
+#ifndef MEMOROID_RETURN_ROWS
+#define MEMOROID_RETURN_ROWS 32
+#endif
+#ifndef MEMOROID_GAE_ROWS
+#define MEMOROID_GAE_ROWS 16
+#endif
+constexpr int disc_rows(bool gae) { return gae ? MEMOROID_GAE_ROWS : MEMOROID_RETURN_ROWS; }
 constexpr int disc_tile(bool gae) { return 4 * 64 * disc_rows(gae); }
 
 struct DiscArgs {

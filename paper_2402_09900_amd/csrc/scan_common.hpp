@@ -19,7 +19,7 @@ enum Kind { K_F32 = 0, K_BF16 = 1, K_C64 = 2 };
 
 template <Kind K> struct KindInfo;
 template <> struct KindInfo<K_F32> { static constexpr int bytes = 4; static constexpr int vec = 4; };
-template <> struct KindInfo<K_BF16> { static constexpr int bytes = 2; static constexpr int vec = 4; };
+template <> struct KindInfo<K_BF16> { static constexpr int bytes = 2; static constexpr int vec = 8; };
 template <> struct KindInfo<K_C64> { static constexpr int bytes = 8; static constexpr int vec = 2; };
 
 // ------------------------------------------------------------ complex float
@@ -607,6 +607,20 @@ __device__ __forceinline__ void lookback(const void* agg, const void* incl, int6
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
+}
+
+// The nearest predecessor's inclusive words for lane position q, read ahead
+// of the look-back (a speculative first poll): a tile usually starts well
+// after the previous tile of its chain was handed out, so these words are
+// often published already, and reading them before the tile's data loads
+// hides the round trip behind those loads.  Returns whether all were there.
+template <class S, int VEC>
+__device__ __forceinline__ bool peek_incl_ahead(const void* incl, int64_t pred, int Dp, int Qp, int q,
+                                                S (&h)[VEC]) {
+    bool ok = true;
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) ok = Desc<S>::get_incl(incl, desc_slot(pred, Dp, Qp, q, v), h[v]) && ok;
+    return ok;
 }
 
 // ------------------------------------------------------------ segments
