@@ -60,7 +60,7 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
         s_ticket = bound ? c.pos : kEmpty32;
         s_bank = c.bank;
     }
-    __syncthreads();
+    barrier_lds();
     const uint32_t claimed = __builtin_amdgcn_readfirstlane(s_ticket);
     if (claimed == kEmpty32) return;       // workspace bound to another call: every tile stands down
     const int64_t k = (int64_t)claimed;
@@ -198,7 +198,7 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
         }
         if (q == 0) sWF[wave] = inc.f;
     }
-    __syncthreads();
+    barrier_lds();
     auto wave_total = [&](int w) -> SegT {
         SegT t;
 #pragma unroll
@@ -246,7 +246,7 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
             for (int v = 0; v < VEC; ++v) sCarry[q * VEC + v] = carry[v];
         }
     }
-    __syncthreads();
+    barrier_lds();
 
     // ---- the tile's inclusive prefix goes out first; then replay backwards
     // from the carry-in and emit dx (built in the registers that held g) and

@@ -90,7 +90,7 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
         s_ticket = bound ? c.pos : kEmpty32;
         s_bank = c.bank;
     }
-    __syncthreads();
+    barrier_lds();
     const uint32_t claimed = __builtin_amdgcn_readfirstlane(s_ticket);
     if (claimed == kEmpty32) return;       // workspace bound to another call: every tile stands down
     const int64_t tile = (int64_t)claimed;
@@ -260,7 +260,7 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
         }
         if (q == 0) sWF[wave] = inc.f;
     }
-    __syncthreads();
+    barrier_lds();
     auto wave_total = [&](int w) -> SegT {
         SegT t;
 #pragma unroll
@@ -328,7 +328,7 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
             for (int v = 0; v < VEC; ++v) sCarry[q * VEC + v] = carry[v];
         }
     }
-    __syncthreads();
+    barrier_lds();
 
     // ---- (5) the tile's inclusive prefix goes out first (successors may be
     // waiting for it); then every lane replays its steps from its carry-in and

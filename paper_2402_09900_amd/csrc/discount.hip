@@ -413,7 +413,7 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
         s_bank = bound ? (epoch & 1u) : kEmpty32;
         if (bound && Wtot.f) publish64((uint64_t*)((char*)p.incl + ((epoch & 1u) ? p.bank : 0)) + slot, pack2(Wtot.H, 0.0f));
     }
-    __syncthreads();
+    barrier_lds();
     const uint32_t bank = __builtin_amdgcn_readfirstlane(s_bank);
     if (bank == kEmpty32) return;             // workspace bound to another call: every tile stands down
     uint64_t* const agg = (uint64_t*)((char*)p.agg + (bank ? p.bank : 0));
@@ -535,7 +535,7 @@ __global__ __launch_bounds__(256) void disc_kernel(DiscArgs p) {
         if (dep[2] && lane == 0) s_carry = carry;
     }
     if (dep[2]) {                             // workgroup-uniform: earlier wavefronts wait for the carry too
-        __syncthreads();
+        barrier_lds();
         carry = s_carry;
     }
     if (dep[w]) emit(carry);

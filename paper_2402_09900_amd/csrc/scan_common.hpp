@@ -609,6 +609,17 @@ __device__ __forceinline__ void lookback(const void* agg, const void* incl, int6
     }
 }
 
+// A workgroup barrier that orders LDS only.  __syncthreads also waits until
+// the wavefront's global stores are acknowledged (one completion counter
+// covers loads and stores here), which puts a store round trip on the path of
+// every barrier that follows a publication; these barriers hand on LDS values
+// only.
+__device__ __forceinline__ void barrier_lds() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // The nearest predecessor's inclusive words for lane position q, read ahead
 // of the look-back (a speculative first poll): a tile usually starts well
 // after the previous tile of its chain was handed out, so these words are
