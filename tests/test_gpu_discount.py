@@ -83,10 +83,13 @@ def test_workload6_full_gae(w6):
     check_gae(w6, w6.gamma, w6.lam, "workload6")
 
 
-# T around the 4096-step tile and the 4-step vector: ragged tails, one-tile
-# tapes, T % 4 != 0 (scalar kernel)
-SHAPES = [(1, 1), (1, 3), (1, 4), (2, 5), (3, 63), (1, 64), (2, 65), (1, 4095), (2, 4096), (3, 4097),
-          (2, 3 * 4096 + 36), (5, 3 * 4096 + 37), (4, 20000), (7, 9 * 4096 + 2)]
+# T around the tiles (8192 steps for the return, 4096 for the advantage),
+# the wavefront runs (2048 / 1024 steps), the lanes' runs (32 / 16 steps) and
+# the 4-step vector: ragged tails, one-tile tapes, T % 4 != 0 (scalar kernel)
+SHAPES = [(1, 1), (1, 3), (1, 4), (2, 5), (1, 15), (2, 16), (1, 17), (1, 31), (2, 32), (2, 33), (3, 63),
+          (1, 64), (2, 65), (1, 1023), (2, 1024), (1, 1025), (1, 2047), (2, 2048), (2, 2049), (1, 4095),
+          (2, 4096), (3, 4097), (1, 8191), (2, 8192), (3, 8193), (2, 2 * 8192 + 1), (2, 3 * 4096 + 36),
+          (5, 3 * 4096 + 37), (4, 20000), (7, 9 * 4096 + 2)]
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "B%dT%d" % s)

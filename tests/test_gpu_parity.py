@@ -285,7 +285,7 @@ def _tile_lengths(dtype, inv, d):
     """Forward and reverse tile lengths (steps) of the plans these tapes get
     (torch allocations are 256-byte aligned, so vectorisation follows d)."""
     code = {"f32": mb.F32, "bf16": mb.BF16, "c64": mb.C64}[dtype]
-    vec = d % (2 if dtype == "c64" else 4) == 0
+    vec = d % {"c64": 2, "f32": 4, "bf16": 8}[dtype] == 0
     stride = 0 if inv else d
     Ls = {mb.memoroid_testing_tile_steps(0, 2, 1 << 16, d, code, stride, vec)}
     if dtype != "bf16":
@@ -294,7 +294,10 @@ def _tile_lengths(dtype, inv, d):
     return sorted(Ls)
 
 
-BOUNDARY_CASES = [(dt, inv, d) for dt in ("f32", "bf16", "c64") for inv in (False, True) for d in (256, 7)]
+# d = 36: a multiple of 4 but not of 8, so bf16 (8 features per vector lane)
+# takes the scalar kernel while f32 stays vectorised
+BOUNDARY_CASES = [(dt, inv, d) for dt in ("f32", "bf16", "c64") for inv in (False, True) for d in (256, 7)] + \
+    [("bf16", False, 36), ("bf16", True, 36), ("f32", False, 36)]
 
 
 @pytest.mark.parametrize("dtype,inv,d", BOUNDARY_CASES, ids=lambda v: str(v))
