@@ -83,20 +83,12 @@ __device__ __forceinline__ float readlane_f(float v, int l) {
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
 }
 
-// The value of lane l + 1 (lane 63 gets its own): DPP row_shl:1 inside each
-// row of 16 lanes, and the next row's first lane, read as a scalar, for the
-// last lane of a row.  Called with every lane active (no ds_bpermute, whose
-// reads of a disabled lane would be undefined).
+// The value of lane l + 1 (lane 63 gets its own): one DPP move with the
+// whole-wavefront shift wave_shl:1 (gfx9 DPP; lane 63, which has no source,
+// keeps the `old` operand, here its own value).  Called with every lane
+// active (no ds_bpermute, whose reads of a disabled lane would be undefined).
 __device__ __forceinline__ uint32_t lane_next(uint32_t v) {
-    const int lane = threadIdx.x & 63;
-    uint32_t r = (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x101, 0xF, 0xF, false);   // row_shl:1
-    const uint32_t n16 = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
-    const uint32_t n32 = (uint32_t)__builtin_amdgcn_readlane((int)v, 32);
-    const uint32_t n48 = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
-    r = lane == 15 ? n16 : r;
-    r = lane == 31 ? n32 : r;
-    r = lane == 47 ? n48 : r;
-    return r;
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x130, 0xF, 0xF, false);   // wave_shl:1
 }
 __device__ __forceinline__ float lane_next(float v) { return __uint_as_float(lane_next(__float_as_uint(v))); }
 
@@ -230,9 +222,13 @@ __device__ __forceinline__ RMap chunk_map(float a, const typename F<VEC>::T& x, 
 // value at step s of a lane's run given the value y after it, with bit s of
 // m set when step s ends its episode.
 __device__ __forceinline__ float step_back(uint32_t m, int s, float a, float x, float y) {
-    const uint32_t mk = (uint32_t)((int32_t)(m << (31 - s)) >> 31);
+    const uint32_t mk = (uint32_t)((int32_t)(m << (31 - s)) >> 31);   // v_bfe_i32: all ones or zero
     const float ny = __builtin_fmaf(a, y, x);
-    return __uint_as_float((__float_as_uint(x) & mk) | (__float_as_uint(ny) & ~mk));
+    // one v_bfi_b32 (written out: the compiler would turn the bit select
+    // into a compare and a v_cndmask, one instruction more per step)
+    uint32_t r;
+    asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(mk), "v"(__float_as_uint(x)), "v"(__float_as_uint(ny)));
+    return __uint_as_float(r);
 }
 
 // Position of chunk k of lane o's run in the wavefront's LDS rows of NC
