@@ -247,7 +247,7 @@ hipError_t disc_launch(bool vec, bool gae, const DiscArgs& a, int64_t ntiles, hi
 constexpr int kTbbBeginBlocks = MEMOROID_TBB_BEGIN_BLOCKS;    // blocks of 16384 flags per compaction workgroup
 constexpr int kTbbBeginTile = 16384 * kTbbBeginBlocks;        // flags per workgroup of the compaction
 #ifndef MEMOROID_TBB_DRAW_TILE
-#define MEMOROID_TBB_DRAW_TILE 2048
+#define MEMOROID_TBB_DRAW_TILE 512
 #endif
 #ifndef MEMOROID_TBB_ROWS_PER_GROUP
 #define MEMOROID_TBB_ROWS_PER_GROUP 256

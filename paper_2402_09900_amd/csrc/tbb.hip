@@ -204,7 +204,7 @@ __device__ __forceinline__ uint64_t min_u64(uint64_t a, uint64_t b) { return a <
 
 }  // namespace
 
-// Row sums of the draws: tile = kTbbDrawTile consecutive draws (8 per
+// Row sums of the draws: tile = kTbbDrawTile consecutive draws (2 per
 // lane).  Each tile sums its episode lengths, publishes the sum, looks back
 // over earlier tiles for the rows before it (ordered by workgroup index, with
 // the same fallback as the compaction: an awaited tile that has not
