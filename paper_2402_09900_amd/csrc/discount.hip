@@ -10,14 +10,18 @@
 // (the TD error, computed in the kernel) for the advantage.  A step is the
 // last of its episode when the next step begins an episode or the tape ends.
 //
-// One tape per row of [B][T]; a tile is 4096 consecutive steps of one tape,
-// handled by 4 wavefronts of 1024 steps.  In a wavefront, load u puts steps
-// 64*VEC*u + VEC*lane .. + VEC-1 into lane `lane` (so every load is one
-// contiguous, coalesced run).  The recurrence is carried as maps
-// "value at the run's first step = f ? H : A * (value after the run) + H";
-// lanes compose their own VEC steps, wavefronts scan the 64 lane maps of
-// each load with shuffles, and tiles find the value entering from their
-// right with a decoupled look-back over the tiles to their right.
+// One tape per row of [B][T]; a tile is 4 wavefronts of 64 lanes, each lane
+// owning one contiguous run of disc_rows(GAE) steps (32 for the return, 16
+// for the advantage: tiles of 8192 and 4096 steps).  Loads are coalesced
+// (load u of a wavefront puts steps VEC*(64u + lane) .. + VEC-1 into lane
+// `lane`); each VEC-step chunk's episode-end bits and, for the advantage, TD
+// errors are formed there, and the chunks then move through LDS into the
+// lanes that own them.  The recurrence is carried as maps "value at the
+// run's first step = f ? H : A * (value after the run) + H": a lane folds
+// its run, the wavefront scans its 64 lane maps once, the wavefronts combine
+// through LDS, and tiles find the value entering from their right with a
+// decoupled look-back over the tiles to their right.  Outputs go back
+// through LDS to coalesced stores.
 //
 // Tiles are numbered from the tape's end by their workgroup index, with no
 // ticket counter (a single counter serialises every workgroup on one memory
