@@ -277,7 +277,7 @@ __global__ __launch_bounds__(256, 4) void linattn_output_kernel(LinOutputArgs p)
 #pragma unroll
             for (int jt = 0; jt < 4; ++jt) {
                 const float num = accO[jt][r] + (ri[r] < 0 ? accS[jt][r] : 0.0f);
-                orow[16 * jt] = num * rden[r];
+                __builtin_nontemporal_store(num * rden[r], &orow[16 * jt]);   // written once, read by no later kernel
             }
         }
     }
