@@ -673,6 +673,15 @@ def main():
     roof["algorithmic_bytes_per_launch"] = int(bytes_per[dom])
     if flops is not None:
         roof["algorithmic_flops_per_launch"] = int(flops[dom])
+        # the recurrent form's own count (no chunking, no masked work), the
+        # O(dk) normaliser terms left out: per step and head the forward adds
+        # phi(k) v^T to the state and reads phi(q)^T S (2 dk dv each); the
+        # gradient rebuilds the state, reads dq from it, accumulates the
+        # state's gradient and reads dk and dv from that (2 dk dv each)
+        dkdv = wl.dk * wl.dv * wl.T * wl.d
+        rec = {"fwd": 4 * dkdv, "bwd": 10 * dkdv}[dom]
+        roof["recurrent_flops_per_launch"] = int(rec)
+        roof["frac_recurrent"] = round(rec / (per_call_ms[dom] * 1e-3) / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4)
         roof["step_frac"] = round(sum(flops.get(k, 0) for k in calls) / (ms_per_step * 1e-3) / 1e12
                                   / FP32_MFMA_PEAK_TFLOPS, 4)
     else:
