@@ -353,7 +353,7 @@ size_t memoroid_scan_ffm_workspace_bytes(int64_t B, int64_t T, int64_t m, int64_
     size_t best = 0;
     for (int vec = 0; vec < 2; ++vec) {
         DiagPlan p;
-        if (!plan_diag(B, T, d, MEMOROID_C64, vec, diag_rows(false, true), false, true, false, &p)) return 0;
+        if (!plan_diag(B, T, d, MEMOROID_C64, vec, kFfmFwdRows, false, true, false, &p)) return 0;
         if (p.total > best) best = p.total;
     }
     return best;
@@ -375,9 +375,10 @@ static int scan_ffm_run(const float* alpha, const float* omega, const float* x, 
         (const void*)episode_idx == S || (const void*)episode_idx == (const void*)x ||
         (const void*)episode_idx == (const void*)start)
         return MEMOROID_EINVAL;
-    const bool vec = d % 2 == 0 && aligned(S, 16);
+    // two features per lane when they always share a row of x (c even)
+    const bool vec = c % 2 == 0 && aligned(S, 16);
     DiagPlan p;
-    if (!plan_diag(B, T, d, MEMOROID_C64, vec, diag_rows(false, true), false, true, false, &p))
+    if (!plan_diag(B, T, d, MEMOROID_C64, vec, kFfmFwdRows, false, true, false, &p))
         return MEMOROID_EUNSUPPORTED;
     if (!workspace) return MEMOROID_EWORKSPACE;
     if (workspace_bytes < memoroid_scan_ffm_workspace_bytes(B, T, m, c) || workspace_bytes < p.total)

@@ -117,6 +117,10 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     bool spec_ok = false;
     if (wave == NW - 1 && j == 0 && active && k > 0)
         spec_ok = peek_incl_ahead<S, VEC>(incl, (int64_t)ticket - p.nchains, Dp, Qp, q, spec);
+    // FFM: the parameters of the chain's transitions, ahead of the tile's
+    // loads, so that the table need not wait for them
+    FfmParam fpar{0.f, 0.f};
+    if constexpr (FFM) fpar = ffm_param_load(p.alpha, p.omega, p.d, p.ffm_c, (int64_t)fb * Dp, Dp);
     uint32_t fl[R + 1];
 #pragma unroll
     for (int r = 0; r <= R; ++r) fl[r] = bload_u8(rs_st, lrow + r);
@@ -148,8 +152,8 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
         // conj(a) of the chain's features, evaluated once per tile as in the
         // forward pass
         if constexpr (std::is_same<S, cf>::value) {
-            ffm_table(sFfm, p.alpha, p.omega, p.d, p.ffm_c, (int64_t)fb * Dp, Dp, true);
-            __syncthreads();
+            ffm_table_store(sFfm, fpar, Dp, true);
+            barrier_lds();
 #pragma unroll
             for (int v = 0; v < VEC; ++v) ainv[v] = sFfm[q * VEC + v];
         }

@@ -80,7 +80,20 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     // so that no chain stays on one XCD); its place in the chain comes from
     // the chain's own counter, in the order tiles start
     const uint32_t nch = (uint32_t)p.nchains;
-    const int chain = (int)((blockIdx.x % nch + blockIdx.x / nch) % nch);
+    int chain;
+    if constexpr (FFM) {
+        // FFM chains of a tape all read each step's real input row: in runs
+        // of kXcds * nchains workgroups, workgroups g = kXcds * i + x (x: the
+        // XCD it lands on) take chain i mod nchains, so a chain's kXcds
+        // tiles of the run go to different XCDs and the same tile of every
+        // chain goes to one, whose L2 then fetches the input row once; the
+        // last partial run takes one tile of each chain in turn
+        const uint32_t run = kXcds * nch;
+        const uint32_t full = gridDim.x / run * run;
+        chain = (int)(blockIdx.x < full ? (blockIdx.x / kXcds) % nch : (blockIdx.x - full) % nch);
+    } else {
+        chain = (int)((blockIdx.x % nch + blockIdx.x / nch) % nch);
+    }
     if (tid == 0) {
         // the signature load goes first: the compiler waits for the atomic's
         // result right after issuing it, and both round trips then overlap
@@ -138,6 +151,10 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     bool spec_ok = false;
     if (wave == 0 && j == 0 && active && tile > 0)
         spec_ok = peek_incl_ahead<S, VEC>(incl, (int64_t)ticket - p.nchains, Dp, Qp, q, spec);
+    // FFM: the parameters of the chain's transitions, ahead of the tile's
+    // loads, so that the table need not wait for them
+    FfmParam fpar{0.f, 0.f};
+    if constexpr (FFM) fpar = ffm_param_load(p.alpha, p.omega, p.d, p.ffm_c, (int64_t)fb * Dp, Dp);
     uint32_t fl[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) fl[r] = bload_u8(rs_st, lrow + r);
@@ -148,20 +165,19 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     if constexpr (FFM) {
         // real x[B][T][m] read once per feature's row j and broadcast over
         // the row's c columns (imaginary parts zero)
+        // (VEC > 1 only for even c, so a lane's features share one row j
+        // and one load per step serves them all)
         const int64_t m = p.ffm_m;
         const Rsrc rs_xf = make_rsrc((const char*)p.x + tape_row0 * m * 4, rows_left * m * 4);
-        uint32_t xo[VEC];
-#pragma unroll
-        for (int v = 0; v < VEC; ++v)
-            xo[v] = active && f0 + v < p.d
-                        ? (uint32_t)(((int64_t)lrow * m + (int64_t)((uint32_t)(f0 + v) / (uint32_t)p.ffm_c)) * 4)
-                        : kOob;
+        const uint32_t xo = active ? (uint32_t)(((int64_t)lrow * m + (int64_t)((uint32_t)f0 / (uint32_t)p.ffm_c)) * 4)
+                                   : kOob;
         const uint32_t xstep = active ? (uint32_t)(m * 4) : 0u;
 #pragma unroll
         for (int r = 0; r < R; ++r) {
+            const uint32_t w = __builtin_amdgcn_raw_buffer_load_b32(rs_xf, (int)(xo + r * xstep), 0, 0);
 #pragma unroll
             for (int v = 0; v < VEC; ++v) {
-                rx[r].w[2 * v] = __builtin_amdgcn_raw_buffer_load_b32(rs_xf, (int)(xo[v] + r * xstep), 0, 0);
+                rx[r].w[2 * v] = w;
                 rx[r].w[2 * v + 1] = 0u;
             }
         }
@@ -186,8 +202,8 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
         // the chain's transitions, evaluated once per tile by wavefront 0
         // while the loads are in flight
         if constexpr (std::is_same<S, cf>::value) {
-            ffm_table(sFfm, p.alpha, p.omega, p.d, p.ffm_c, (int64_t)fb * Dp, Dp, false);
-            __syncthreads();
+            ffm_table_store(sFfm, fpar, Dp, false);
+            barrier_lds();
 #pragma unroll
             for (int v = 0; v < VEC; ++v) ainv[v] = sFfm[q * VEC + v];
         }
@@ -331,10 +347,8 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     barrier_lds();
 
     // ---- (5) the tile's inclusive prefix goes out first (successors may be
-    // waiting for it); then every lane replays its steps from its carry-in and
-    // streams h out.  All outputs are computed before any store (in the
-    // registers that held x when the dtypes match), so the stores go out in
-    // one burst and never wait on one another.
+    // waiting for it); then every lane replays its steps from its carry-in
+    // and streams h out.
     S hv[VEC];
 #pragma unroll
     for (int v = 0; v < VEC; ++v) {
@@ -356,26 +370,45 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
             }
         }
     }
-    constexpr bool kInPlace = (int)IN == (int)OUT;
-    RawVec<OUT, VEC> o[kInPlace ? 1 : R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
+    const Rsrc rs_h = make_rsrc((char*)p.h + tape_row0 * p.d * OB, rows_left * p.d * OB);
+    const uint32_t out_step = active ? (uint32_t)(p.d * OB) : 0u;
+    const uint32_t out_off = active ? (uint32_t)((int64_t)lrow * p.d * OB + f0 * OB) : kOob;
+    auto replay = [&](int r) {
         const bool bg = (begins >> r) & 1u;
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {
             const S xv = CIn::get(rx[r], v);
             hv[v] = bg ? xv : mad(a_at(r, v), hv[v], xv);
         }
-        if constexpr (kInPlace) CIn::put_all(rx[r], hv);
-        else COut::put_all(o[r], hv);
-    }
-    const Rsrc rs_h = make_rsrc((char*)p.h + tape_row0 * p.d * OB, rows_left * p.d * OB);
-    const uint32_t out_step = active ? (uint32_t)(p.d * OB) : 0u;
-    const uint32_t out_off = active ? (uint32_t)((int64_t)lrow * p.d * OB + f0 * OB) : kOob;
+    };
+    if constexpr (FFM) {
+        // one real input word per step serves all of a lane's features, so
+        // holding every step's output would take several times the input's
+        // registers: each step's h is stored as soon as it is known
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-        if constexpr (kInPlace) raw_bstore_nt(rs_h, out_off + r * out_step, rx[r]);
-        else raw_bstore_nt(rs_h, out_off + r * out_step, o[r]);
+        for (int r = 0; r < R; ++r) {
+            replay(r);
+            RawVec<OUT, VEC> o1;
+            COut::put_all(o1, hv);
+            raw_bstore_nt(rs_h, out_off + r * out_step, o1);
+        }
+    } else {
+        // all outputs are computed before any store (in the registers that
+        // held x when the dtypes match), so the stores go out in one burst
+        // and never wait on one another
+        constexpr bool kInPlace = (int)IN == (int)OUT;
+        RawVec<OUT, VEC> o[kInPlace ? 1 : R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            replay(r);
+            if constexpr (kInPlace) CIn::put_all(rx[r], hv);
+            else COut::put_all(o[r], hv);
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            if constexpr (kInPlace) raw_bstore_nt(rs_h, out_off + r * out_step, rx[r]);
+            else raw_bstore_nt(rs_h, out_off + r * out_step, o[r]);
+        }
     }
 }
 
@@ -391,7 +424,7 @@ static hipError_t launch_fwd(const DiagFwdArgs& args, int64_t ntiles, bool ainv,
 }
 
 hipError_t ffm_fwd_launch(bool vec, const DiagFwdArgs& args, int64_t ntiles, hipStream_t s) {
-    constexpr int R = kFwdRows;
+    constexpr int R = kFfmFwdRows;
     constexpr int VC = KindInfo<K_C64>::vec;
     if (vec)
         hipLaunchKernelGGL((diag_fwd_kernel<K_C64, K_C64, VC, R, true, true>), dim3((unsigned)ntiles), dim3(256), 0, s,

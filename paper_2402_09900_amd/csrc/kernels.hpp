@@ -38,6 +38,9 @@ constexpr int kBwdRows = MEMOROID_BWD_ROWS;
 constexpr int kBwdRowsPerStepA = MEMOROID_BWD_ROWS_PER_STEP_A;
 // Bytes of a feature row one chain covers (one 128-byte line by default).
 constexpr int64_t kChainRowBytes = MEMOROID_CHAIN_ROW_BYTES;
+// Accelerator dies (XCDs, each with its own L2) of an MI355X; the dispatcher
+// hands consecutive workgroups to them in turn.
+constexpr uint32_t kXcds = 8;
 constexpr int diag_rows(bool bwd, bool ainv) { return !bwd ? kFwdRows : (ainv ? kBwdRows : kBwdRowsPerStepA); }
 // steps per lane of the forward scan of a state dtype (a memoroid_dtype:
 // bf16 is 1), vectorised or not
@@ -48,6 +51,13 @@ constexpr int diag_fwd_rows(int state_dtype, bool vec) { return state_dtype == 1
 #define MEMOROID_FFM_BWD_ROWS 8
 #endif
 constexpr int kFfmBwdRows = MEMOROID_FFM_BWD_ROWS;
+// The FFM forward holds only the real input per step (its outputs stream
+// out), so its register count and tile length are set on their own.
+#ifndef MEMOROID_FFM_FWD_ROWS
+#define MEMOROID_FFM_FWD_ROWS 24
+#endif
+constexpr int kFfmFwdRows = MEMOROID_FFM_FWD_ROWS;
+
 
 struct DiagFwdArgs {
     const void* a;

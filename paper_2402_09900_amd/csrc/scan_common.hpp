@@ -471,16 +471,30 @@ template <> struct Desc<cf> {
 // and rounded once to float (with |a| near 1 the error of a is amplified by up
 // to the episode length), into tab[l].  conj_a stores conj(a) (the reverse
 // scan's coefficient).  Features past d get a valid, unused value.  The caller
-// synchronises the workgroup before reading tab.
-__device__ __forceinline__ void ffm_table(cf* tab, const float* alpha, const float* omega, int64_t d, int64_t c,
-                                          int64_t f_base, int Dp, bool conj_a) {
+// synchronises the workgroup before reading tab.  Two steps, so that a
+// kernel can load the parameters first and evaluate the table while its
+// other loads are in flight.
+struct FfmParam {
+    float alpha, omega;
+};
+__device__ __forceinline__ FfmParam ffm_param_load(const float* alpha, const float* omega, int64_t d, int64_t c,
+                                                   int64_t f_base, int Dp) {
+    FfmParam r{0.f, 0.f};
     const int l = threadIdx.x;
     if (l < Dp) {
         const int64_t f = f_base + l < d ? f_base + l : 0;
         const int64_t jj = f / c, kk = f - jj * c;
-        const double mag = exp(-fabs((double)alpha[jj]));
+        r.alpha = alpha[jj];
+        r.omega = omega[kk];
+    }
+    return r;
+}
+__device__ __forceinline__ void ffm_table_store(cf* tab, FfmParam pr, int Dp, bool conj_a) {
+    const int l = threadIdx.x;
+    if (l < Dp) {
+        const double mag = exp(-fabs((double)pr.alpha));
         double sn, cs;
-        sincos((double)omega[kk], &sn, &cs);
+        sincos((double)pr.omega, &sn, &cs);
         const float im = (float)(mag * sn);
         tab[l] = cf{(float)(mag * cs), conj_a ? -im : im};
     }
