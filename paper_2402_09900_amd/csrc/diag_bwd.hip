@@ -26,6 +26,7 @@ namespace memoroid {
 template <Kind K, int VEC, int R, bool AINV, bool FFM = false>
 __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     static_assert(!FFM || (K == K_C64 && AINV), "FFM: complex state, generated a");
+    static_assert(R >= 1 && R <= 32, "a lane's steps are bits of 32-bit masks");
     using S = typename StateOf<K>::type;
     using C = Codec<K, VEC>;
     using SegT = Seg<S, VEC>;

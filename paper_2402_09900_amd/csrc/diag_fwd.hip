@@ -52,6 +52,7 @@ namespace memoroid {
 template <Kind IN, Kind OUT, int VEC, int R, bool AINV, bool FFM = false>
 __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     static_assert(!FFM || (IN == K_C64 && OUT == K_C64 && AINV), "FFM: complex state, generated a");
+    static_assert(R >= 1 && R <= 32, "a lane's steps are bits of 32-bit masks");
     using S = typename StateOf<IN>::type;
     using CIn = Codec<IN, VEC>;
     using COut = Codec<OUT, VEC>;
