@@ -81,20 +81,7 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     // so that no chain stays on one XCD); its place in the chain comes from
     // the chain's own counter, in the order tiles start
     const uint32_t nch = (uint32_t)p.nchains;
-    int chain;
-    if constexpr (FFM) {
-        // FFM chains of a tape all read each step's real input row: in runs
-        // of kXcds * nchains workgroups, workgroups g = kXcds * i + x (x: the
-        // XCD it lands on) take chain i mod nchains, so a chain's kXcds
-        // tiles of the run go to different XCDs and the same tile of every
-        // chain goes to one, whose L2 then fetches the input row once; the
-        // last partial run takes one tile of each chain in turn
-        const uint32_t run = kXcds * nch;
-        const uint32_t full = gridDim.x / run * run;
-        chain = (int)(blockIdx.x < full ? (blockIdx.x / kXcds) % nch : (blockIdx.x - full) % nch);
-    } else {
-        chain = (int)((blockIdx.x % nch + blockIdx.x / nch) % nch);
-    }
+    const int chain = (int)((blockIdx.x % nch + blockIdx.x / nch) % nch);
     if (tid == 0) {
         // the signature load goes first: the compiler waits for the atomic's
         // result right after issuing it, and both round trips then overlap

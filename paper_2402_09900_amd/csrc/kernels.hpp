@@ -38,9 +38,6 @@ constexpr int kBwdRows = MEMOROID_BWD_ROWS;
 constexpr int kBwdRowsPerStepA = MEMOROID_BWD_ROWS_PER_STEP_A;
 // Bytes of a feature row one chain covers (one 128-byte line by default).
 constexpr int64_t kChainRowBytes = MEMOROID_CHAIN_ROW_BYTES;
-// Accelerator dies (XCDs, each with its own L2) of an MI355X; the dispatcher
-// hands consecutive workgroups to them in turn.
-constexpr uint32_t kXcds = 8;
 constexpr int diag_rows(bool bwd, bool ainv) { return !bwd ? kFwdRows : (ainv ? kBwdRows : kBwdRowsPerStepA); }
 // steps per lane of the forward scan of a state dtype (a memoroid_dtype:
 // bf16 is 1), vectorised or not
