@@ -256,9 +256,11 @@ size_t memoroid_scan_diag_workspace_bytes(int64_t B, int64_t T, int64_t d, int i
     const int sd = in_dtype == MEMOROID_C64 ? MEMOROID_C64 : (in_dtype == MEMOROID_BF16 ? MEMOROID_BF16 : MEMOROID_F32);
     size_t best = 0;
     for (int vec = 0; vec < 2; ++vec) {
-        DiagPlan& p = vec ? pv : ps;
-        if (!plan_diag(B, T, d, sd, vec, diag_fwd_rows(sd, vec), false, false, false, &p)) return 0;
-        if (p.total > best) best = p.total;
+        for (int ainv = 0; ainv < 2; ++ainv) {
+            DiagPlan& p = vec ? pv : ps;
+            if (!plan_diag(B, T, d, sd, vec, diag_fwd_rows(sd, vec, ainv), false, ainv, false, &p)) return 0;
+            if (p.total > best) best = p.total;
+        }
     }
     return best;
 }
@@ -284,7 +286,8 @@ static int scan_diag_run(const void* a, int64_t a_stride_t, const void* x, const
     const bool vec = d % VW == 0 && aligned(x, 16) && aligned(h, 16) && aligned(a, 16);
     const int sd = in_dtype == MEMOROID_C64 ? MEMOROID_C64 : (in_dtype == MEMOROID_BF16 ? MEMOROID_BF16 : MEMOROID_F32);
     DiagPlan p;
-    if (!plan_diag(B, T, d, sd, vec, diag_fwd_rows(sd, vec), false, ainv, false, &p)) return MEMOROID_EUNSUPPORTED;
+    if (!plan_diag(B, T, d, sd, vec, diag_fwd_rows(sd, vec, ainv), false, ainv, false, &p))
+        return MEMOROID_EUNSUPPORTED;
     if (mode == WsMode::kNoAlloc) {
         // the plan's own size (the scratch array is never shared with
         // another plan's call in flight, so the query's maximum over plans
@@ -1307,7 +1310,7 @@ int64_t memoroid_testing_tile_steps(int reverse, int64_t B, int64_t T, int64_t d
     if (reverse && dtype == MEMOROID_BF16) return 0;
     const bool ainv = a_stride_t == 0;
     DiagPlan p;
-    const int rows = reverse ? diag_rows(true, ainv) : diag_fwd_rows(dtype, vectorised != 0);
+    const int rows = reverse ? diag_rows(true, ainv) : diag_fwd_rows(dtype, vectorised != 0, ainv);
     if (!plan_diag(B, T, d, dtype, vectorised != 0, rows, reverse != 0, ainv, reverse != 0, &p))
         return 0;
     return p.L;

@@ -402,12 +402,14 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
 
 // ------------------------------------------------------------------ launch
 
-template <Kind IN, Kind OUT, int VEC, int R>
+// R: steps per lane with a time-invariant a; RS with a per-step a (the host
+// plans the tiles with the same counts, diag_fwd_rows)
+template <Kind IN, Kind OUT, int VEC, int R, int RS = R>
 static hipError_t launch_fwd(const DiagFwdArgs& args, int64_t ntiles, bool ainv, hipStream_t s) {
     if (ainv)
         hipLaunchKernelGGL((diag_fwd_kernel<IN, OUT, VEC, R, true>), dim3((unsigned)ntiles), dim3(256), 0, s, args);
     else
-        hipLaunchKernelGGL((diag_fwd_kernel<IN, OUT, VEC, R, false>), dim3((unsigned)ntiles), dim3(256), 0, s, args);
+        hipLaunchKernelGGL((diag_fwd_kernel<IN, OUT, VEC, RS, false>), dim3((unsigned)ntiles), dim3(256), 0, s, args);
     return hipGetLastError();
 }
 
@@ -428,7 +430,7 @@ hipError_t diag_fwd_launch(int in_kind, int out_kind, bool vec, bool ainv,
     constexpr int R = kFwdRows;
     constexpr int VF = KindInfo<K_F32>::vec, VB = KindInfo<K_BF16>::vec, VC = KindInfo<K_C64>::vec;
     if (in_kind == K_F32 && out_kind == K_F32)
-        return vec ? launch_fwd<K_F32, K_F32, VF, R>(args, ntiles, ainv, s)
+        return vec ? launch_fwd<K_F32, K_F32, VF, R, kFwdRowsF32StepA>(args, ntiles, ainv, s)
                    : launch_fwd<K_F32, K_F32, 1, R>(args, ntiles, ainv, s);
     constexpr int RB = kFwdRowsBf16;
     if (in_kind == K_BF16 && out_kind == K_BF16)

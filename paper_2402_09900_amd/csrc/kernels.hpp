@@ -30,18 +30,26 @@ struct WsHeader;
 #ifndef MEMOROID_FWD_ROWS_BF16
 #define MEMOROID_FWD_ROWS_BF16 12
 #endif
+#ifndef MEMOROID_FWD_ROWS_F32_STEP_A
+#define MEMOROID_FWD_ROWS_F32_STEP_A 18
+#endif
 constexpr int kFwdRows = MEMOROID_FWD_ROWS;
 // bf16 input, vectorised: 8 features per lane (one 16-byte access), so a
 // lane's steps hold half the bytes they would in f32 for the same registers
 constexpr int kFwdRowsBf16 = MEMOROID_FWD_ROWS_BF16;
+// f32 with a per-step a, vectorised: 18 steps still fit two workgroups per CU
+// and the longer tiles spread the per-tile fixed cost further
+constexpr int kFwdRowsF32StepA = MEMOROID_FWD_ROWS_F32_STEP_A;
 constexpr int kBwdRows = MEMOROID_BWD_ROWS;
 constexpr int kBwdRowsPerStepA = MEMOROID_BWD_ROWS_PER_STEP_A;
 // Bytes of a feature row one chain covers (one 128-byte line by default).
 constexpr int64_t kChainRowBytes = MEMOROID_CHAIN_ROW_BYTES;
 constexpr int diag_rows(bool bwd, bool ainv) { return !bwd ? kFwdRows : (ainv ? kBwdRows : kBwdRowsPerStepA); }
 // steps per lane of the forward scan of a state dtype (a memoroid_dtype:
-// bf16 is 1), vectorised or not
-constexpr int diag_fwd_rows(int state_dtype, bool vec) { return state_dtype == 1 && vec ? kFwdRowsBf16 : kFwdRows; }
+// f32 is 0, bf16 1), vectorised or not, with a time-invariant a or not
+constexpr int diag_fwd_rows(int state_dtype, bool vec, bool ainv) {
+    return !vec ? kFwdRows : state_dtype == 1 ? kFwdRowsBf16 : (state_dtype == 0 && !ainv) ? kFwdRowsF32StepA : kFwdRows;
+}
 // The FFM gradient keeps more per-tile state (the input-gradient reduction)
 // and runs fastest with shorter tiles and more workgroups per CU.
 #ifndef MEMOROID_FFM_BWD_ROWS
