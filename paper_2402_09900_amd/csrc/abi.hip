@@ -484,7 +484,8 @@ static int scan_ffm_bwd_run(const float* alpha, const float* omega, const uint8_
         for (int o2 = 0; o2 < o; ++o2)
             if (outs[o2] && outs[o] == outs[o2]) return MEMOROID_EINVAL;
     }
-    const bool vec = d % 2 == 0 && aligned(grad_S, 16) && (!S || aligned(S, 16));
+    // two features per lane only when they always share a row of x (c even)
+    const bool vec = c % 2 == 0 && aligned(grad_S, 16) && (!S || aligned(S, 16));
     DiagPlan p;
     size_t off_da, off_dxw, total;
     if (!ffm_bwd_plan(B, T, m, c, vec, params, &p, &off_da, &off_dxw, &total)) return MEMOROID_EUNSUPPORTED;

@@ -175,10 +175,30 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     // ---- per-lane summary, walking its R steps backwards.  Steps past T
     // hold zeros and come before the tape's last step, which ends an episode,
     // so they never reach a real output.
+    //
+    // FFM: the fold also takes from g and h all that the replay needs, so
+    // neither is held across the look-back.  With lam_in the adjoint that
+    // enters the lane's last step, lam_t = l_t + c_t lam_in, where l_t is the
+    // lane's own recurrence from zero (own.H after step t) and c_t the
+    // product of conj(a) over steps t.. up to the lane's last, zero from its
+    // first end downwards.  Kept: sum_v Re(l_t) per step (the input gradient
+    // adds Re over the lane's features, which share one row j), and for da
+    // D1 = sum_t l_t conj(h_{t-1}), D2 = sum_t c_t conj(h_{t-1}).
+    constexpr int RF = FFM ? R : 1;
+    float lre[RF];
+    S d1[VEC], d2[VEC], cp[VEC];
+    bool alive = true, d2_live = false;      // c_t not forced to zero yet / some term of D2 counts
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) {
+        d1[v] = s_zero<S>();
+        d2[v] = s_zero<S>();
+        cp[v] = s_one<S>();
+    }
     SegT own = seg_identity<S, VEC>();
 #pragma unroll
     for (int r = R - 1; r >= 0; --r) {
         const bool e = (ends >> r) & 1u;
+        const bool no_da = ((begins | ~valid) >> r) & 1u;
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {
             const S gv = C::get(rg[r], v);
@@ -187,6 +207,23 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
             const S na = own.A[v] * cv;
             own.H[v] = e ? gv : nh;
             own.A[v] = e ? s_one<S>() : na;
+            if constexpr (FFM) {
+                const S ncp = cv * cp[v];
+                cp[v] = e ? s_zero<S>() : ncp;
+                if (want_da) {
+                    const S hc = conj(C::get(rh[r], v));
+                    d1[v] = no_da ? d1[v] : mad(own.H[v], hc, d1[v]);
+                    d2[v] = no_da ? d2[v] : mad(cp[v], hc, d2[v]);
+                }
+            }
+        }
+        if constexpr (FFM) {
+            alive = alive && !e;
+            d2_live = d2_live || (alive && !no_da);
+            float sre = 0.0f;
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) sre += re_part(own.H[v]);
+            lre[r] = sre;
         }
     }
     own.f = ends != 0;
@@ -268,54 +305,61 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
 #pragma unroll
     for (int v = 0; v < VEC; ++v) dsum[v] = s_zero<S>();
     if (active) {
-#pragma unroll
-        for (int r = R - 1; r >= 0; --r) {
-            const bool e = (ends >> r) & 1u;
-            // no da at a begin step, nor past T: there lam is 0, but the
-            // step T reads h_{T-1}, and 0 * Inf would reach the sum
-            const bool no_da = ((begins | ~valid) >> r) & 1u;
-#pragma unroll
-            for (int v = 0; v < VEC; ++v) {
-                const S gv = C::get(rg[r], v);
-                lam[v] = e ? gv : mad(coef(r, v), lam[v], gv);
-                const S dav = no_da ? s_zero<S>() : lam[v] * conj(C::get(rh[r], v));
-                if constexpr (AINV) {
-                    dsum[v] = dsum[v] + dav;
-                } else {
-                    C::put(ra[r], v, dav);
-                }
-                C::put(rg[r], v, lam[v]);
-            }
-        }
         if constexpr (FFM) {
+            // the adjoint entering the lane's last step, lam_in, completes
+            // what the fold kept: da adds lam_in D2 (a select: when no term
+            // of D2 counts, a non-finite lam_in cut off by an end stays out),
+            // and lam_t = l_t + m_t with m_t = c_t lam_in, run down from
+            // lam_in (reset to zero by a select at an end).
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) dsum[v] = d2_live ? mad(lam[v], d2[v], d1[v]) : d1[v];
             // x is real and broadcast over the c columns of its row j: its
             // gradient is the sum of Re(lam) over those columns.  c is a power
-            // of two: with c >= VEC a lane's features share one j and groups
-            // of c / VEC lanes are combined by shuffles; with c < VEC each
-            // feature is its own j.  The chain's jpc = Dp / c rows go to the
-            // chain-major workspace [chain][T][jpc], so that a tile writes
-            // whole lines (ffm_bwd_finish_kernel puts them in [B][T][m] order).
+            // of two and at least VEC (the host picks one feature per lane
+            // otherwise), so a lane's features share one j and groups of
+            // c / VEC lanes are combined by shuffles.  The chain's jpc = Dp / c
+            // rows go to the chain-major workspace [chain][T][jpc], so that a
+            // tile writes whole lines (ffm_bwd_finish_kernel puts them in
+            // [B][T][m] order).
             const int64_t cc = p.ffm_c;
-            const int csh = __builtin_ctzll((uint64_t)cc);  // c is a power of two here
+            const int csh = __builtin_ctzll((uint64_t)cc);
             const int64_t jpc = Dp >> csh;
+            const int gsz = (int)(cc / VEC);
             float* const dxw = p.dxr + (int64_t)chain * T * jpc;
 #pragma unroll
             for (int r = R - 1; r >= 0; --r) {
                 const int64_t t = row0 + r;
-                const bool in = t < T;
-                if (cc >= VEC) {
-                    float part = 0.0f;
+                const bool e = (ends >> r) & 1u;
+                float part = lre[r];
 #pragma unroll
-                    for (int v = 0; v < VEC; ++v) part += C::get(rg[r], v).re;
-                    for (int off = 1; off < (int)(cc / VEC); off <<= 1) part += lanes_xor(part, off);
-                    if (in && (q & ((int)(cc / VEC) - 1)) == 0) dxw[t * jpc + ((q * VEC) >> csh)] = part;
-                } else {
-#pragma unroll
-                    for (int v = 0; v < VEC; ++v)
-                        if (in && f0 + v < p.d) dxw[t * jpc + ((q * VEC + v) >> csh)] = C::get(rg[r], v).re;
+                for (int v = 0; v < VEC; ++v) {
+                    const S nm = coef(r, v) * lam[v];
+                    lam[v] = e ? s_zero<S>() : nm;
+                    part += re_part(lam[v]);
                 }
+                for (int off = 1; off < gsz; off <<= 1) part += lanes_xor(part, off);
+                if (t < T && (q & (gsz - 1)) == 0) dxw[t * jpc + ((q * VEC) >> csh)] = part;
             }
         } else {
+#pragma unroll
+            for (int r = R - 1; r >= 0; --r) {
+                const bool e = (ends >> r) & 1u;
+                // no da at a begin step, nor past T: there lam is 0, but the
+                // step T reads h_{T-1}, and 0 * Inf would reach the sum
+                const bool no_da = ((begins | ~valid) >> r) & 1u;
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) {
+                    const S gv = C::get(rg[r], v);
+                    lam[v] = e ? gv : mad(coef(r, v), lam[v], gv);
+                    const S dav = no_da ? s_zero<S>() : lam[v] * conj(C::get(rh[r], v));
+                    if constexpr (AINV) {
+                        dsum[v] = dsum[v] + dav;
+                    } else {
+                        C::put(ra[r], v, dav);
+                    }
+                    C::put(rg[r], v, lam[v]);
+                }
+            }
             const Rsrc rs_dx = make_rsrc((char*)p.dx + tape_row0 * rowB, rows_left * rowB);
             const Rsrc rs_da = make_rsrc(AINV ? p.dx : (char*)p.da + tape_row0 * rowB, AINV ? 0 : rows_left * rowB);
 #pragma unroll

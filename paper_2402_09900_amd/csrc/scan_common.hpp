@@ -34,6 +34,8 @@ __device__ __forceinline__ cf operator*(cf a, cf b) {
 __device__ __forceinline__ cf operator+(cf a, cf b) { return cf{a.re + b.re, a.im + b.im}; }
 __device__ __forceinline__ cf conj(cf a) { return cf{a.re, -a.im}; }
 __device__ __forceinline__ float conj(float a) { return a; }
+__device__ __forceinline__ float re_part(cf a) { return a.re; }
+__device__ __forceinline__ float re_part(float a) { return a; }
 
 // a * b + c, fused per component where the arithmetic allows
 __device__ __forceinline__ float mad(float a, float b, float c) { return __builtin_fmaf(a, b, c); }
