@@ -564,7 +564,9 @@ size_t memoroid_scan_diag_bwd_workspace_bytes(int64_t B, int64_t T, int64_t d, i
     size_t best = 0;
     for (int vec = 0; vec < 2; ++vec) {
         DiagPlan p;
-        if (!plan_diag(B, T, d, dtype, vec, diag_rows(true, a_stride_t == 0), true, a_stride_t == 0, true, &p)) return 0;
+        if (!plan_diag(B, T, d, dtype, vec, diag_bwd_rows(dtype, vec, a_stride_t == 0), true, a_stride_t == 0, true,
+                       &p))
+            return 0;
         if (p.total > best) best = p.total;
     }
     return best;
@@ -592,7 +594,8 @@ static int scan_diag_bwd_run(const void* a, int64_t a_stride_t, const uint8_t* s
     const bool vec = d % VW == 0 && aligned(a, 16) && aligned(grad_h, 16) && aligned(grad_x, 16) &&
                      (!h || aligned(h, 16)) && (!grad_a || aligned(grad_a, 16));
     DiagPlan p;
-    if (!plan_diag(B, T, d, dtype, vec, diag_rows(true, ainv), true, ainv, grad_a != nullptr, &p)) return MEMOROID_EUNSUPPORTED;
+    if (!plan_diag(B, T, d, dtype, vec, diag_bwd_rows(dtype, vec, ainv), true, ainv, grad_a != nullptr, &p))
+        return MEMOROID_EUNSUPPORTED;
     if (!workspace) return MEMOROID_EWORKSPACE;
     if (workspace_bytes < memoroid_scan_diag_bwd_workspace_bytes(B, T, d, dtype, a_stride_t) ||
         workspace_bytes < p.total)
@@ -1311,7 +1314,7 @@ int64_t memoroid_testing_tile_steps(int reverse, int64_t B, int64_t T, int64_t d
     if (reverse && dtype == MEMOROID_BF16) return 0;
     const bool ainv = a_stride_t == 0;
     DiagPlan p;
-    const int rows = reverse ? diag_rows(true, ainv) : diag_fwd_rows(dtype, vectorised != 0, ainv);
+    const int rows = reverse ? diag_bwd_rows(dtype, vectorised != 0, ainv) : diag_fwd_rows(dtype, vectorised != 0, ainv);
     if (!plan_diag(B, T, d, dtype, vectorised != 0, rows, reverse != 0, ainv, reverse != 0, &p))
         return 0;
     return p.L;

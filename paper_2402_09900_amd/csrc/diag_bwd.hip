@@ -176,14 +176,18 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
     // hold zeros and come before the tape's last step, which ends an episode,
     // so they never reach a real output.
     //
-    // FFM: the fold also takes from g and h all that the replay needs, so
-    // neither is held across the look-back.  With lam_in the adjoint that
-    // enters the lane's last step, lam_t = l_t + c_t lam_in, where l_t is the
-    // lane's own recurrence from zero (own.H after step t) and c_t the
-    // product of conj(a) over steps t.. up to the lane's last, zero from its
-    // first end downwards.  Kept: sum_v Re(l_t) per step (the input gradient
-    // adds Re over the lane's features, which share one row j), and for da
-    // D1 = sum_t l_t conj(h_{t-1}), D2 = sum_t c_t conj(h_{t-1}).
+    // With a time-invariant complex a the fold also takes from h all that da
+    // needs, so h is not held across the look-back (and for FFM neither is
+    // g); the real kernels keep the plain replay, whose registers this would
+    // raise.
+    // With lam_in the adjoint that enters the lane's last step,
+    // lam_t = l_t + c_t lam_in, where l_t is the lane's own recurrence from
+    // zero (own.H after step t) and c_t the product of conj(a) over steps t..
+    // up to the lane's last, zero from its first end downwards.  Kept:
+    // D1 = sum_t l_t conj(h_{t-1}) and D2 = sum_t c_t conj(h_{t-1}) (da's
+    // partial is D1 + lam_in D2), and for FFM sum_v Re(l_t) per step (the
+    // input gradient adds Re over the lane's features, which share one row j).
+    constexpr bool kFoldDa = AINV && std::is_same<S, cf>::value;
     constexpr int RF = FFM ? R : 1;
     float lre[RF];
     S d1[VEC], d2[VEC], cp[VEC];
@@ -207,7 +211,7 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
             const S na = own.A[v] * cv;
             own.H[v] = e ? gv : nh;
             own.A[v] = e ? s_one<S>() : na;
-            if constexpr (FFM) {
+            if constexpr (kFoldDa) {
                 const S ncp = cv * cp[v];
                 cp[v] = e ? s_zero<S>() : ncp;
                 if (want_da) {
@@ -217,9 +221,11 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
                 }
             }
         }
-        if constexpr (FFM) {
+        if constexpr (kFoldDa) {
             alive = alive && !e;
             d2_live = d2_live || (alive && !no_da);
+        }
+        if constexpr (FFM) {
             float sre = 0.0f;
 #pragma unroll
             for (int v = 0; v < VEC; ++v) sre += re_part(own.H[v]);
@@ -305,14 +311,16 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
 #pragma unroll
     for (int v = 0; v < VEC; ++v) dsum[v] = s_zero<S>();
     if (active) {
-        if constexpr (FFM) {
-            // the adjoint entering the lane's last step, lam_in, completes
-            // what the fold kept: da adds lam_in D2 (a select: when no term
-            // of D2 counts, a non-finite lam_in cut off by an end stays out),
-            // and lam_t = l_t + m_t with m_t = c_t lam_in, run down from
-            // lam_in (reset to zero by a select at an end).
+        // the adjoint entering the lane's last step, lam_in, completes what
+        // the fold kept: da adds lam_in D2 (a select: when no term of D2
+        // counts, a non-finite lam_in cut off by an end stays out)
+        if constexpr (kFoldDa) {
 #pragma unroll
             for (int v = 0; v < VEC; ++v) dsum[v] = d2_live ? mad(lam[v], d2[v], d1[v]) : d1[v];
+        }
+        if constexpr (FFM) {
+            // lam_t = l_t + m_t with m_t = c_t lam_in, run down from lam_in
+            // (reset to zero by a select at an end)
             // x is real and broadcast over the c columns of its row j: its
             // gradient is the sum of Re(lam) over those columns.  c is a power
             // of two and at least VEC (the host picks one feature per lane
@@ -351,11 +359,10 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
                 for (int v = 0; v < VEC; ++v) {
                     const S gv = C::get(rg[r], v);
                     lam[v] = e ? gv : mad(coef(r, v), lam[v], gv);
-                    const S dav = no_da ? s_zero<S>() : lam[v] * conj(C::get(rh[r], v));
-                    if constexpr (AINV) {
-                        dsum[v] = dsum[v] + dav;
-                    } else {
-                        C::put(ra[r], v, dav);
+                    if constexpr (!kFoldDa) {
+                        const S dav = no_da ? s_zero<S>() : lam[v] * conj(C::get(rh[r], v));
+                        if constexpr (AINV) dsum[v] = dsum[v] + dav;
+                        else C::put(ra[r], v, dav);
                     }
                     C::put(rg[r], v, lam[v]);
                 }
@@ -617,7 +624,7 @@ hipError_t diag_bwd_launch(int kind, bool vec, bool ainv, const DiagBwdArgs& arg
         return vec ? launch_bwd<K_F32, KindInfo<K_F32>::vec, RS>(args, ntiles, false, s) : launch_bwd<K_F32, 1, RS>(args, ntiles, false, s);
     }
     if (kind == K_C64) {
-        if (ainv) return vec ? launch_bwd<K_C64, KindInfo<K_C64>::vec, RI>(args, ntiles, true, s) : launch_bwd<K_C64, 1, RI>(args, ntiles, true, s);
+        if (ainv) return vec ? launch_bwd<K_C64, KindInfo<K_C64>::vec, kBwdRowsC64Inv>(args, ntiles, true, s) : launch_bwd<K_C64, 1, RI>(args, ntiles, true, s);
         return vec ? launch_bwd<K_C64, KindInfo<K_C64>::vec, RS>(args, ntiles, false, s) : launch_bwd<K_C64, 1, RS>(args, ntiles, false, s);
     }
     return hipErrorInvalidValue;

@@ -45,6 +45,16 @@ constexpr int kBwdRowsPerStepA = MEMOROID_BWD_ROWS_PER_STEP_A;
 // Bytes of a feature row one chain covers (one 128-byte line by default).
 constexpr int64_t kChainRowBytes = MEMOROID_CHAIN_ROW_BYTES;
 constexpr int diag_rows(bool bwd, bool ainv) { return !bwd ? kFwdRows : (ainv ? kBwdRows : kBwdRowsPerStepA); }
+// The reverse scan of complex state with a time-invariant a, vectorised,
+// runs shorter tiles: at 8 steps it keeps three workgroups per CU.
+#ifndef MEMOROID_BWD_ROWS_C64_INV
+#define MEMOROID_BWD_ROWS_C64_INV 8
+#endif
+constexpr int kBwdRowsC64Inv = MEMOROID_BWD_ROWS_C64_INV;
+// steps per lane of the reverse scan of a state dtype (f32 is 0, c64 2)
+constexpr int diag_bwd_rows(int state_dtype, bool vec, bool ainv) {
+    return state_dtype == 2 && vec && ainv ? kBwdRowsC64Inv : diag_rows(true, ainv);
+}
 // steps per lane of the forward scan of a state dtype (a memoroid_dtype:
 // f32 is 0, bf16 1), vectorised or not, with a time-invariant a or not
 constexpr int diag_fwd_rows(int state_dtype, bool vec, bool ainv) {
