@@ -117,6 +117,36 @@ def test_grad_shapes(shape):
                "shape")
 
 
+def test_grad_nonfinite_adjoint_at_a_begin():
+    """A non-finite upstream gradient at a begin step reaches that step's
+    input gradient only: the step before ends an episode, and begin steps
+    take no term of dalpha, domega (at 704 a lane's first step, at 1500
+    inside a lane)."""
+    f = tapes.make_ffm(7, seed=402, B=1, T=3000, m=4, c=4)
+    s = np.zeros((1, f.T), np.uint8)
+    s[0, [0, 704, 1500, 2200]] = 1
+    f.start = s
+    rng = np.random.Generator(np.random.PCG64(10))
+    G = (rng.standard_normal((1, f.T, 4, 4), dtype=np.float32)
+         + 1j * rng.standard_normal((1, f.T, 4, 4), dtype=np.float32)).astype(np.complex64)
+    G[0, 704, 1, 2] = np.nan
+    G[0, 1500, 3, 0] = np.nan
+    announce("ffm bwd NaN adjoint at begins")
+    al, om, x, sd = dev(f.alpha), dev(f.omega), dev(f.x), dev(s)
+    S = mb.scan_ffm(al, om, x, sd)
+    gx, ga, gw = mb.scan_ffm_bwd(al, om, sd, S, dev(G))
+    gx, ga, gw = gx.cpu().numpy(), ga.cpu().numpy(), gw.cpu().numpy()
+    rdx, rda, rdw, mdx, mda, mdw = oracle.ffm_bwd(f.alpha.astype(np.float64), f.omega.astype(np.float64), s,
+                                                  S.cpu().numpy().astype(np.complex128), G.astype(np.complex128))
+    bad = np.isnan(rdx)
+    assert bad[0, 704, 1] and bad[0, 1500, 3] and bad.sum() == 2
+    assert np.array_equal(np.isnan(gx), bad)
+    assert cond_err(gx[~bad], rdx[~bad], mdx[~bad]) <= GTOL
+    assert np.isfinite(ga).all() and np.isfinite(gw).all()
+    assert cond_err(ga, rda, mda) <= GTOL
+    assert cond_err(gw, rdw, mdw) <= GTOL
+
+
 def test_grad_without_parameter_gradients():
     f = tapes.make_ffm(7, seed=401, B=2, T=2000, m=8, c=4)
     announce("ffm bwd x only")

@@ -397,6 +397,36 @@ def test_time_invariant_da_ignores_the_state_after_the_tape_end(dtype, B):
     assert e_dx <= TOL[dtype] and e_da <= TOL[dtype]
 
 
+@pytest.mark.parametrize("dtype", ["f32", "c64"])
+def test_invariant_a_nonfinite_adjoint_at_a_begin(dtype):
+    """A non-finite upstream gradient at a begin step makes that step's
+    adjoint non-finite, but no earlier step's (the step before ends an
+    episode) and no term of the time-invariant da (begin steps take none):
+    da stays finite and equal to the oracle's.  One begin opens a lane's
+    steps (704: a multiple of the lane's 8 or 16 steps), the other falls
+    inside a lane (1500)."""
+    T, d = 3000, 16
+    w = tapes.make_custom_diag(dtype, 1, T, d, True, seed=31)
+    w.start[:] = 0
+    w.start[0, [0, 704, 1500, 2200]] = 1
+    g = w.g.copy()
+    g[0, 704, 3] = np.nan
+    g[0, 1500, 5] = np.nan
+    announce("bwd invariant-a NaN adjoint at begins %s" % dtype)
+    store = np.complex64 if dtype == "c64" else np.float32
+    h_ref, _ = oracle.diag_fwd(dec(w.a, dtype), dec(w.x, dtype), w.start)
+    h_in = h_ref.astype(store)
+    gx, ga = mb.scan_diag_bwd(to_dev(w.a, dtype), to_dev(w.start, "u8"), to_dev(h_in, dtype), to_dev(g, dtype))
+    gx, ga = from_dev(gx), from_dev(ga)
+    dx, da, m_dx, m_da = oracle.diag_bwd(dec(w.a, dtype), w.start, dec(h_in, dtype), dec(g, dtype))
+    bad = np.isnan(dx)
+    assert bad[0, 704, 3] and bad[0, 1500, 5] and bad.sum() == 2
+    assert np.array_equal(np.isnan(gx), bad)
+    assert cond_err(gx[~bad], dx[~bad], m_dx[~bad]) <= TOL[dtype]
+    assert np.isfinite(da).all() and np.isfinite(ga).all()
+    assert cond_err(ga, da, m_da) <= TOL[dtype]
+
+
 def test_linattn_nan_stays_in_its_episode():
     la = tapes.make_linattn(T=640, seed=11)
     la.start[:] = 0
