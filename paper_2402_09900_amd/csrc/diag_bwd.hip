@@ -524,10 +524,21 @@ hipError_t ffm_bwd_launch(bool vec, const DiagBwdArgs& args, int64_t ntiles, hip
 // into LDS, in parallel, so that the sums are plain multiply-adds (the same
 // operations in the same order as evaluating them inside the sums).
 constexpr int kParamRows = 1024, kParamCols = 256, kParamDa = 4096;
+// The finish kernel's LDS, shared by its two kinds of workgroup: the
+// parameter tables (and da) of the last one, the row block of the others.
+constexpr int kFinRows = 256;          // steps per copying workgroup
+constexpr int kFinLdsCols = 32;        // m up to this: rows gathered in LDS
+constexpr int kFinBatch = 16;          // gather loads in flight per thread
+constexpr int kParamLdsBytes = kParamRows * 8 + 2 * kParamCols * 8 + kParamDa * 4;
+constexpr int kBlockLdsBytes = kFinRows * kFinLdsCols * 4;
+constexpr int kFinLdsBytes = kParamLdsBytes > kBlockLdsBytes ? kParamLdsBytes : kBlockLdsBytes;
+
 __device__ void ffm_param_grad(const float* alpha, const float* omega, const float* da_g, int64_t m, int64_t c,
-                               float* dalpha, float* domega) {
-    __shared__ double s_mag[kParamRows], s_cs[kParamCols], s_sn[kParamCols];
-    __shared__ float s_da[kParamDa];       // da as well, when it fits (loaded once, coalesced)
+                               float* dalpha, float* domega, unsigned char* lds) {
+    double* const s_mag = (double*)lds;
+    double* const s_cs = s_mag + kParamRows;
+    double* const s_sn = s_cs + kParamCols;
+    float* const s_da = (float*)(s_sn + kParamCols);   // da as well, when it fits (loaded once, coalesced)
     const bool tab = m <= kParamRows && c <= kParamCols;
     const bool lds_da = 2 * m * c <= kParamDa;
     if (tab) {
@@ -577,15 +588,65 @@ __device__ void ffm_param_grad(const float* alpha, const float* omega, const flo
 // each (the chains' rows of those steps are whole lines, read once); the
 // last workgroup forms the parameter gradients from the summed da when asked.
 __global__ __launch_bounds__(256) void ffm_bwd_finish_kernel(FfmFinishArgs p) {
-    const int64_t nblk_t = (p.T + 255) / 256;
+    __shared__ __attribute__((aligned(16))) unsigned char s_lds[kFinLdsBytes];
+    const int64_t nblk_t = (p.T + kFinRows - 1) / kFinRows;
     if ((int64_t)blockIdx.x == p.B * nblk_t) {
-        if (p.dalpha || p.domega) ffm_param_grad(p.alpha, p.omega, p.da, p.m, p.c, p.dalpha, p.domega);
+        if (p.dalpha || p.domega) ffm_param_grad(p.alpha, p.omega, p.da, p.m, p.c, p.dalpha, p.domega, s_lds);
         return;
     }
     const int64_t b = blockIdx.x / nblk_t;
-    const int64_t t0 = (blockIdx.x - b * nblk_t) * 256;
-    const int rows = (int)(p.T - t0 < 256 ? p.T - t0 : 256);
+    const int64_t t0 = (blockIdx.x - b * nblk_t) * kFinRows;
+    const int rows = (int)(p.T - t0 < kFinRows ? p.T - t0 : kFinRows);
     const int64_t nfb = (p.m + p.jpc - 1) / p.jpc;
+    if (p.m <= kFinLdsCols) {
+        // the block's rows are gathered in LDS: each chain's run of
+        // rows * jpc floats is contiguous, read with consecutive threads on
+        // consecutive words, and every row of dx then goes out whole.  Row r
+        // keeps column j at r * 32 + (j ^ (r & 31)), so neither the gather
+        // (rows across the lanes) nor the row reads meet bank conflicts.
+        float* const blk = (float*)s_lds;
+        const int jpc = (int)p.jpc, m = (int)p.m;
+        const int lj = __builtin_ctz((unsigned)jpc);     // jpc = Dp / c, a power of two
+        const int run = rows << lj;
+        // thread t takes the words t, t + 256, ... of the chains' runs laid
+        // end to end; (fb, w) is advanced by subtraction, not division
+        int fb = 0, w = (int)threadIdx.x;
+        while (fb < (int)nfb && w >= run) {
+            w -= run;
+            ++fb;
+        }
+        while (fb < (int)nfb) {
+            float v[kFinBatch];
+            int at[kFinBatch];
+#pragma unroll
+            for (int u = 0; u < kFinBatch; ++u) {
+                v[u] = 0.0f;
+                at[u] = -1;
+                if (fb < (int)nfb) {
+                    const int r = w >> lj, j = (fb << lj) + (w & (jpc - 1));
+                    v[u] = p.dxw[((b * nfb + fb) * p.T + t0) * jpc + w];
+                    if (j < m) at[u] = r * kFinLdsCols + (j ^ (r & (kFinLdsCols - 1)));
+                    w += 256;
+                    while (fb < (int)nfb && w >= run) {
+                        w -= run;
+                        ++fb;
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kFinBatch; ++u)
+                if (at[u] >= 0) blk[at[u]] = v[u];
+        }
+        __syncthreads();
+        // thread (r0, j) writes column j of rows r0, r0 + per, ...
+        float* const dst = p.dx + (b * p.T + t0) * p.m;
+        const int per = 256 / m, r0 = (int)threadIdx.x / m, jc = (int)threadIdx.x - r0 * m;
+        if (r0 < per) {
+            for (int r = r0; r < rows; r += per)
+                __builtin_nontemporal_store(blk[r * kFinLdsCols + (jc ^ (r & (kFinLdsCols - 1)))], &dst[r * m + jc]);
+        }
+        return;
+    }
     // thread (r0, j) copies column j of rows r0, r0 + per, ...; for m > 256
     // one row per pass and several columns per thread
     const int64_t per = p.m <= 256 ? 256 / p.m : 1;
@@ -611,7 +672,7 @@ __global__ __launch_bounds__(256) void ffm_bwd_finish_kernel(FfmFinishArgs p) {
 }
 
 hipError_t ffm_bwd_finish_launch(const FfmFinishArgs& a, hipStream_t s) {
-    const int64_t nblk = a.B * ((a.T + 255) / 256) + 1;
+    const int64_t nblk = a.B * ((a.T + kFinRows - 1) / kFinRows) + 1;
     hipLaunchKernelGGL(ffm_bwd_finish_kernel, dim3((unsigned)nblk), dim3(256), 0, s, a);
     return hipGetLastError();
 }

@@ -109,8 +109,10 @@ def test_grad_workload7_full():
     check_grad(tapes.make_ffm(7), "workload7")
 
 
+# m up to 32: the finish kernel gathers rows in LDS; 33 and 40: the direct copy
 @pytest.mark.parametrize("shape", [(1, 1, 1, 1), (2, 513, 3, 4), (1, 1000, 32, 8), (3, 2049, 7, 2), (2, 4096, 1, 16),
-                                   (1, 777, 16, 1), (4, 3000, 5, 4)], ids=lambda s: "B%dT%dm%dc%d" % s)
+                                   (1, 777, 16, 1), (4, 3000, 5, 4), (2, 300, 33, 4), (1, 700, 40, 2)],
+                         ids=lambda s: "B%dT%dm%dc%d" % s)
 def test_grad_shapes(shape):
     B, T, m, c = shape
     check_grad(tapes.make_ffm(7, seed=400 + T + m * c, B=B, T=T, m=m, c=c, episodes=tapes._geometric(150.0)),
