@@ -56,6 +56,7 @@ fp64 and slicing happen before timing.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import os
 import sys
@@ -83,29 +84,78 @@ def parse():
     return p.parse_args()
 
 
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000
+
+
+class TimingEvent:
+    """A timing-only HIP event, created with hipEventDisableSystemFence.  A
+    default event (torch.cuda.Event) performs a system-scope release when it
+    is recorded, writing back and invalidating the caches: on this GPU that
+    left about 6 us of idle time around each record and started the next
+    kernel cold, inflating both the per-call and the per-step times.  The
+    HIP runtime is the one torch has loaded (same soname)."""
+    _hip = None
+
+    @classmethod
+    def hip(cls):
+        if cls._hip is None:
+            L = ctypes.CDLL("libamdhip64.so.7")
+            L.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            L.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            L.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+            L.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            cls._hip = L
+        return cls._hip
+
+    def __init__(self):
+        self.h = ctypes.c_void_p()
+        st = self.hip().hipEventCreateWithFlags(ctypes.byref(self.h), HIP_EVENT_DISABLE_SYSTEM_FENCE)
+        if st != 0:
+            raise RuntimeError("hipEventCreateWithFlags failed: %d" % st)
+
+    def record(self, stream):
+        st = self.hip().hipEventRecord(self.h, ctypes.c_void_p(stream))
+        if st != 0:
+            raise RuntimeError("hipEventRecord failed: %d" % st)
+
+    def elapsed_time(self, other):
+        ms = ctypes.c_float()
+        st = self.hip().hipEventElapsedTime(ctypes.byref(ms), self.h, other.h)
+        if st != 0:
+            raise RuntimeError("hipEventElapsedTime failed: %d" % st)
+        return float(ms.value)
+
+    def __del__(self):
+        if self._hip is not None and self.h:
+            self._hip.hipEventDestroy(self.h)
+
+
 class Timer:
-    """HIP events on the launch stream around one library call."""
+    """Timing-only HIP events on the launch stream around one library call."""
 
     def __init__(self, torch):
         self.torch = torch
         self.pairs = []
 
     def __call__(self, fn):
-        t = self.torch
-        e0, e1 = t.cuda.Event(enable_timing=True), t.cuda.Event(enable_timing=True)
-        e0.record(t.cuda.current_stream())
+        stream = self.torch.cuda.current_stream().cuda_stream
+        e0, e1 = TimingEvent(), TimingEvent()
+        e0.record(stream)
         fn()
-        e1.record(t.cuda.current_stream())
+        e1.record(stream)
         self.pairs.append((e0, e1))
 
+    def times_ms(self):
+        return [a.elapsed_time(b) for a, b in self.pairs]
+
     def mean_ms(self):
-        return float(np.mean([a.elapsed_time(b) for a, b in self.pairs])) if self.pairs else 0.0
+        return float(np.mean(self.times_ms())) if self.pairs else 0.0
 
     def median_ms(self):
-        return float(np.median([a.elapsed_time(b) for a, b in self.pairs])) if self.pairs else 0.0
+        return float(np.median(self.times_ms())) if self.pairs else 0.0
 
     def percentiles_ms(self, qs=(10, 50, 90)):
-        v = [a.elapsed_time(b) for a, b in self.pairs]
+        v = self.times_ms()
         return [round(float(np.percentile(v, q)), 4) for q in qs] if v else None
 
 
