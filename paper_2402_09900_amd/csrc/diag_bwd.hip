@@ -202,6 +202,8 @@ __global__ __launch_bounds__(256) void diag_bwd_kernel(DiagBwdArgs p) {
 #pragma unroll
     for (int r = R - 1; r >= 0; --r) {
         const bool e = (ends >> r) & 1u;
+        // no da at a begin step, nor past T (a select: the step T reads
+        // h_{T-1}, and 0 * Inf would reach the sum)
         const bool no_da = ((begins | ~valid) >> r) & 1u;
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {
