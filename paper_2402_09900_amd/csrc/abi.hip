@@ -73,8 +73,10 @@ enum SigKind : int64_t { kSigDiag = 1, kSigDiagBwd, kSigFfm, kSigFfmBwd, kSigDis
 
 // Tiling and workspace layout of a diagonal scan.  `vec` selects the
 // vectorised lane width; `state_complex` picks the descriptor size.
+// ctr_groups: tile counters per chain (the FFM forward keeps one per XCD
+// group of workgroups, kXcds)
 bool plan_diag(int64_t B, int64_t T, int64_t d, int state_dtype, bool vec, int rows, bool bwd,
-               bool ainv, bool want_grad_a, DiagPlan* p) {
+               bool ainv, bool want_grad_a, DiagPlan* p, int ctr_groups = 1) {
     // extents no tiling can address (and whose sums below would overflow)
     if (B <= 0 || T <= 0 || d <= 0 || d > (int64_t)INT32_MAX || T > INT64_MAX / 4) return false;
     const int VEC = vec ? vec_width(state_dtype) : 1;
@@ -91,6 +93,9 @@ bool plan_diag(int64_t B, int64_t T, int64_t d, int state_dtype, bool vec, int r
     if (!mul_ok(B, p->nfb, &p->nchains)) return false;
     if (!mul_ok(p->nt, p->nchains, &p->ntiles)) return false;
     if (p->ntiles >= (int64_t)INT32_MAX || p->nchains >= (int64_t)INT32_MAX) return false;
+    // a grid padded to whole groups of ctr_groups positions per chain
+    if (ctr_groups > 1 && ((p->nt + ctr_groups - 1) / ctr_groups) * ctr_groups > (int64_t)INT32_MAX / p->nchains)
+        return false;
     // a tile's rows (plus one step on each side) are addressed with 32-bit
     // buffer offsets below 2^31
     // (4 bytes at least: bf16 input may be written as f32)
@@ -105,7 +110,7 @@ bool plan_diag(int64_t B, int64_t T, int64_t d, int state_dtype, bool vec, int r
     if (ndesc > INT64_MAX / 32) return false;
     size_t off = kAlign;                                   // header
     p->off_ctr = off;                                      // per-chain tile counters
-    off = align_up(off + (size_t)p->nchains * kCtrStride * 4);
+    off = align_up(off + (size_t)p->nchains * (size_t)ctr_groups * kCtrStride * 4);
     // bank 0 of the self-validating words, then bank 1 with the same layout
     const size_t bank0 = off;
     p->off_agg = off;
@@ -356,7 +361,7 @@ size_t memoroid_scan_ffm_workspace_bytes(int64_t B, int64_t T, int64_t m, int64_
     size_t best = 0;
     for (int vec = 0; vec < 2; ++vec) {
         DiagPlan p;
-        if (!plan_diag(B, T, d, MEMOROID_C64, vec, kFfmFwdRows, false, true, false, &p)) return 0;
+        if (!plan_diag(B, T, d, MEMOROID_C64, vec, kFfmFwdRows, false, true, false, &p, (int)kXcds)) return 0;
         if (p.total > best) best = p.total;
     }
     return best;
@@ -381,7 +386,7 @@ static int scan_ffm_run(const float* alpha, const float* omega, const float* x, 
     // two features per lane when they always share a row of x (c even)
     const bool vec = c % 2 == 0 && aligned(S, 16);
     DiagPlan p;
-    if (!plan_diag(B, T, d, MEMOROID_C64, vec, kFfmFwdRows, false, true, false, &p))
+    if (!plan_diag(B, T, d, MEMOROID_C64, vec, kFfmFwdRows, false, true, false, &p, (int)kXcds))
         return MEMOROID_EUNSUPPORTED;
     if (!workspace) return MEMOROID_EWORKSPACE;
     if (workspace_bytes < memoroid_scan_ffm_workspace_bytes(B, T, m, c) || workspace_bytes < p.total)

@@ -81,19 +81,39 @@ __global__ __launch_bounds__(256) void diag_fwd_kernel(DiagFwdArgs p) {
     // so that no chain stays on one XCD); its place in the chain comes from
     // the chain's own counter, in the order tiles start
     const uint32_t nch = (uint32_t)p.nchains;
-    const int chain = (int)((blockIdx.x % nch + blockIdx.x / nch) % nch);
+    // FFM: the chains of a tape all read each step's real input row.  The
+    // grid runs in groups of kXcds * nchains workgroups; workgroup
+    // g = kXcds * i + x takes chain i mod nchains and counter (chain, x),
+    // whose n-th ticket is position kXcds * n + x, so every chain's tile at a
+    // position runs on the same XCD x and its L2 fetches the input rows once.
+    // A counter hands out its positions in the order its workgroups start;
+    // those of group x - 1 (and of the group before) come earlier in the
+    // grid, so the tile a workgroup waits for was claimed by one that is
+    // running or finished.  The grid is padded to whole groups: positions
+    // past the last tile stand down.
+    int chain;
+    uint32_t grp = 0, per_call = (uint32_t)p.nt;
+    if constexpr (FFM) {
+        chain = (int)((blockIdx.x / kXcds) % nch);
+        grp = blockIdx.x % kXcds;
+        per_call = (uint32_t)((p.nt + kXcds - 1) / kXcds);
+    } else {
+        chain = (int)((blockIdx.x % nch + blockIdx.x / nch) % nch);
+    }
     if (tid == 0) {
         // the signature load goes first: the compiler waits for the atomic's
         // result right after issuing it, and both round trips then overlap
         const uint64_t seen = peek_sig(p.hdr);
-        const Claim c = claim_of(take_ticket(p.ctr + (size_t)chain * kCtrStride, (uint32_t)p.nt), (uint32_t)p.nt);
-        const bool bound = ws_bound_to(p.hdr, p.sig, seen, chain == 0 && c.pos == 0);
-        s_ticket = bound ? c.pos : kEmpty32;
+        uint32_t* const ctr = p.ctr + ((size_t)chain * (FFM ? kXcds : 1u) + grp) * kCtrStride;
+        const Claim c = claim_of(take_ticket(ctr, per_call), per_call);
+        const uint32_t pos = FFM ? c.pos * kXcds + grp : c.pos;
+        const bool bound = ws_bound_to(p.hdr, p.sig, seen, chain == 0 && pos == 0);
+        s_ticket = bound && pos < (uint32_t)p.nt ? pos : kEmpty32;
         s_bank = c.bank;
     }
     barrier_lds();
     const uint32_t claimed = __builtin_amdgcn_readfirstlane(s_ticket);
-    if (claimed == kEmpty32) return;       // workspace bound to another call: every tile stands down
+    if (claimed == kEmpty32) return;       // workspace bound to another call (every tile stands down), or padding
     const int64_t tile = (int64_t)claimed;
     const uint32_t ticket = (uint32_t)(tile * p.nchains + chain);
     // descriptor banks: this call's (epoch parity) and the idle one
@@ -416,11 +436,14 @@ static hipError_t launch_fwd(const DiagFwdArgs& args, int64_t ntiles, bool ainv,
 hipError_t ffm_fwd_launch(bool vec, const DiagFwdArgs& args, int64_t ntiles, hipStream_t s) {
     constexpr int R = kFfmFwdRows;
     constexpr int VC = KindInfo<K_C64>::vec;
+    (void)ntiles;
+    // whole groups of kXcds positions per chain (see the kernel)
+    const int64_t grid = ((args.nt + kXcds - 1) / kXcds) * kXcds * args.nchains;
     if (vec)
-        hipLaunchKernelGGL((diag_fwd_kernel<K_C64, K_C64, VC, R, true, true>), dim3((unsigned)ntiles), dim3(256), 0, s,
+        hipLaunchKernelGGL((diag_fwd_kernel<K_C64, K_C64, VC, R, true, true>), dim3((unsigned)grid), dim3(256), 0, s,
                            args);
     else
-        hipLaunchKernelGGL((diag_fwd_kernel<K_C64, K_C64, 1, R, true, true>), dim3((unsigned)ntiles), dim3(256), 0, s,
+        hipLaunchKernelGGL((diag_fwd_kernel<K_C64, K_C64, 1, R, true, true>), dim3((unsigned)grid), dim3(256), 0, s,
                            args);
     return hipGetLastError();
 }

@@ -47,6 +47,9 @@ constexpr int kBwdRows = MEMOROID_BWD_ROWS;
 constexpr int kBwdRowsPerStepA = MEMOROID_BWD_ROWS_PER_STEP_A;
 // Bytes of a feature row one chain covers (one 128-byte line by default).
 constexpr int64_t kChainRowBytes = MEMOROID_CHAIN_ROW_BYTES;
+// Accelerator dies (XCDs, each with its own L2) of an MI355X: the dispatcher
+// hands workgroup g to XCD g mod kXcds.
+constexpr uint32_t kXcds = 8;
 constexpr int diag_rows(bool bwd, bool ainv) { return !bwd ? kFwdRows : (ainv ? kBwdRows : kBwdRowsPerStepA); }
 // The reverse scan of complex state with a time-invariant a, vectorised,
 // runs shorter tiles: at 8 steps it keeps three workgroups per CU.
