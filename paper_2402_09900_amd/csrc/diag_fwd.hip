@@ -28,7 +28,9 @@
 //            The counters are never reset: they wrap every two calls, so a
 //            ticket also tells the call's epoch parity, which picks the
 //            descriptor bank (the tile clears its words of the other bank
-//            for the next call).
+//            for the next call).  The FFM aggregator keeps one counter per
+//            (chain, XCD group) instead, so that every chain's tile at a
+//            position runs on one XCD (its chains share the input rows).
 //
 // Per tile: (1) every load is issued up front: the begin flags of the lane's
 // steps, then a and x, one wide access per step; (2) each lane folds its R
