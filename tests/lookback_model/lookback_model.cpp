@@ -8,7 +8,9 @@
 //
 //   diagonal forward scan (memoroid_scan_diag): per-chain wrapping ticket
 //   counters (two calls per cycle) giving the tile's place and the call's
-//   epoch parity; two banks of self-validating descriptor words (all ones =
+//   epoch parity -- or, as the FFM forward keeps them, one counter per
+//   (chain, group of G workgroups), the n-th ticket of counter (chain, x)
+//   being position G n + x, with the grid padded to whole groups; two banks of self-validating descriptor words (all ones =
 //   unpublished, NaN canonicalised); the tile publishing its aggregate, or
 //   its inclusive prefix when it holds a begin step; the idle bank's words
 //   cleared by their owner for the next call; the look-back folding
@@ -32,6 +34,7 @@
 // every expectation holds (for a mutation: when the model detects it).
 //
 //   lookback_model <dir> diag <schedules> <mutation>
+//   lookback_model <dir> diag_grouped <schedules> <mutation>
 //   lookback_model <dir> return <schedules> <mutation>
 #include <atomic>
 #include <chrono>
@@ -201,6 +204,7 @@ struct DiagProblem {
 // Workspace of one layout (F features per chain, L steps per tile).
 struct DiagWs {
     int64_t F = 0, L = 0, nt = 0, nfb = 0, nch = 0, ntiles = 0, B = 0;
+    int64_t groups = 1;               // tile counters per chain (G)
     uint64_t sig = kEmpty64;          // header: signature word
     uint32_t timeout = kEmpty32;      // header: a wait gave up
     std::vector<uint32_t> ctr;        // per-chain ticket counters
@@ -213,7 +217,7 @@ struct DiagWs {
         nfb = (d + F - 1) / F;
         nch = B * nfb;
         ntiles = nt * nch;
-        ctr.assign((size_t)nch, 0);
+        ctr.assign((size_t)(nch * groups), 0);
         for (int k = 0; k < 2; ++k) {
             agg[k].assign((size_t)(ntiles * F), 0);
             incl[k].assign((size_t)(ntiles * F), 0);
@@ -257,19 +261,24 @@ bool bound_to(uint64_t* hdr_sig, uint64_t sig, uint64_t seen, bool designated, i
 // `sig`.  Outputs h and idx are written by the tiles that run.
 void diag_call(const DiagProblem& P, DiagWs& ws, uint64_t sig, Pool& pool, int mut, std::vector<float>& h,
                std::vector<int32_t>& idx) {
-    const int64_t nt = ws.nt, nch = ws.nch, F = ws.F, L = ws.L, T = P.T, d = P.d, B = P.B;
-    pool.launch(ws.ntiles, [&](int64_t g, Rng& r) {
-        const int64_t chain = (g % nch + g / nch) % nch;
+    const int64_t nt = ws.nt, nch = ws.nch, F = ws.F, L = ws.L, T = P.T, d = P.d, B = P.B, G = ws.groups;
+    // grouped counters: the grid is padded to whole groups of G positions per
+    // chain, and workgroup g = G i + x takes chain i mod nch, counter (chain, x)
+    const int64_t grid = G > 1 ? (nt + G - 1) / G * G * nch : ws.ntiles;
+    pool.launch(grid, [&](int64_t g, Rng& r) {
+        const int64_t chain = G > 1 ? (g / G) % nch : (g % nch + g / nch) % nch;
+        const int64_t grp = G > 1 ? g % G : 0;
         const uint64_t seen = peek(&ws.sig);
-        const uint32_t per_call = (uint32_t)nt;
+        const uint32_t per_call = (uint32_t)(G > 1 ? (nt + G - 1) / G : nt);
         const uint32_t top = mut == kWrapEveryCall ? per_call - 1u : 2u * per_call - 1u;
-        const uint32_t old = atomic_inc_wrap(&ws.ctr[(size_t)chain], top);
+        const uint32_t old = atomic_inc_wrap(&ws.ctr[(size_t)(chain * G + grp)], top);
         const uint32_t t = old >= top ? 0u : old + 1u;
-        const uint32_t pos = t < per_call ? t : t - per_call;
+        const uint32_t n = t < per_call ? t : t - per_call;
+        const uint32_t pos = (uint32_t)(n * G + grp);
         uint32_t bank = t < per_call ? 0u : 1u;
         if (mut == kOneBank) bank = 0;
         if (!bound_to(&ws.sig, sig, seen, chain == 0 && pos == 0, mut)) return;   // stand down
-        if (pos >= (uint32_t)nt) return;   // only reachable with a broken wrap; the result check catches it
+        if (pos >= (uint32_t)nt) return;   // grid padding (or a broken wrap; the result check catches it)
         jitter(r);
         const int64_t tile = pos, ticket = tile * nch + chain;
         const int64_t b = chain / ws.nfb, fb = chain % ws.nfb;
@@ -423,7 +432,7 @@ bool load_diag(const std::string& dir, int k, DiagProblem& P) {
 // workspace, which must stand down and leave its outputs untouched, a call
 // with the original layout that must stand down too (poisoned), and a new
 // preparation after which the original layout computes again.
-int run_diag(const std::string& dir, int schedules, int mut) {
+int run_diag(const std::string& dir, int schedules, int mut, bool grouped) {
     DiagProblem P[3];
     for (int k = 0; k < 3; ++k)
         if (!load_diag(dir, k, P[k])) {
@@ -438,6 +447,7 @@ int run_diag(const std::string& dir, int schedules, int mut) {
         const int64_t F = 1 + r.below(3), L = 4 + r.below(13);
         const DiagProblem& P0 = P[0];
         DiagWs ws;
+        ws.groups = grouped ? 2 + (int64_t)r.below(7) : 1;
         ws.size_for(P0.B, P0.T, P0.d, F, L);
         ws.prepare();
         const uint64_t sig = 0x1234ull + (uint64_t)(F * 131 + L);
@@ -485,7 +495,8 @@ int run_diag(const std::string& dir, int schedules, int mut) {
             if (mut != kNone) break;              // detected
         }
     }
-    std::printf("diag mutation %d schedules %d failures %d worst_err %.3g\n", mut, schedules, failures, worst);
+    std::printf("diag%s mutation %d schedules %d failures %d worst_err %.3g\n", grouped ? " grouped" : "", mut,
+                schedules, failures, worst);
     if (mut == kNone) return failures == 0 ? 0 : 1;
     return failures > 0 ? 0 : 1;
 }
@@ -688,13 +699,14 @@ int run_return(const std::string& dir, int schedules, int mut) {
 
 int main(int argc, char** argv) {
     if (argc != 5) {
-        std::printf("usage: %s <dir> diag|return <schedules> <mutation>\n", argv[0]);
+        std::printf("usage: %s <dir> diag|diag_grouped|return <schedules> <mutation>\n", argv[0]);
         return 2;
     }
     const std::string dir = argv[1], what = argv[2];
     const int schedules = std::atoi(argv[3]), mut = std::atoi(argv[4]);
     if (mut < 0 || mut >= kMutations) return 2;
-    if (what == "diag") return run_diag(dir, schedules, mut);
+    if (what == "diag") return run_diag(dir, schedules, mut, false);
+    if (what == "diag_grouped") return run_diag(dir, schedules, mut, true);
     if (what == "return") return run_return(dir, schedules, mut);
     return 2;
 }

@@ -4,7 +4,8 @@ here with g++ and ThreadSanitizer).
 
 The GPU runs the protocol in the dispatcher's natural order only; the model
 runs its state machine with worker threads delayed at random points: tickets
-from wrapping per-chain counters (epoch parity), two banks of self-validating
+from wrapping per-chain counters (epoch parity) or, as in the FFM forward,
+from one counter per (chain, group of workgroups) over a padded grid, two banks of self-validating
 descriptor words cleared for the next call by their owners, the look-back,
 the episode-index counts, the workspace signature (binding, poisoning,
 standing down), and the discounted return's index-ordered tiles with per-tile
@@ -101,6 +102,18 @@ def _caught(res, name):
 
 def test_diag_protocol_under_random_schedules(model):
     _clean(_run(model, "diag", 3000, 0))
+
+
+def test_grouped_counters_under_random_schedules(model):
+    """One counter per (chain, group): a workgroup's predecessor position
+    belongs to another counter, claimed by a workgroup earlier in the grid;
+    with as few workers as the model draws, every wait still ends."""
+    _clean(_run(model, "diag_grouped", 2000, 0))
+
+
+@pytest.mark.parametrize("mutation", [2, 3], ids=["one_bank", "counter_wraps_every_call"])
+def test_grouped_counters_mutation_is_caught(model, mutation):
+    _caught(_run(model, "diag_grouped", 400, mutation), MUTATIONS_DIAG[mutation])
 
 
 def test_return_protocol_and_fallback_under_random_schedules(model):
