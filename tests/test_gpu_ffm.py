@@ -40,9 +40,12 @@ def test_workload7_full():
 
 
 # odd c -> one feature per lane (384-step tiles), even c -> two (768-step
-# tiles); c = 1; m = 1; ragged T around one and several tiles
+# tiles); c = 1; m = 1; ragged T around one and several tiles; tile counts
+# per chain below, at and past one group of 8 positions (the forward's grid
+# is padded to whole groups)
 SHAPES = [(1, 1, 1, 1), (1, 5, 1, 3), (2, 513, 3, 5), (1, 1000, 32, 8), (3, 2049, 7, 2), (2, 4096, 1, 16),
-          (1, 777, 16, 1), (4, 3000, 5, 4), (1, 767, 8, 4), (2, 769, 4, 2), (1, 1537, 6, 3), (1, 385, 2, 1)]
+          (1, 777, 16, 1), (4, 3000, 5, 4), (1, 767, 8, 4), (2, 769, 4, 2), (1, 1537, 6, 3), (1, 385, 2, 1),
+          (2, 6144, 4, 4), (1, 6913, 2, 8), (1, 12289, 3, 3)]
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "B%dT%dm%dc%d" % s)
